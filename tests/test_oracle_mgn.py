@@ -1,0 +1,362 @@
+"""Pins for the oracle's MGN forward/backward and integrators.
+
+* MLP/LayerNorm against torch's textbook implementations (fp64).
+* A dense brute force of the whole MGN call written with one-hot incidence
+  matrices in torch (no index gathers, no sparse sums), and its autograd
+  gradients against the oracle's hand-written reverse mode.
+* fp64 central finite differences.
+* Permutation equivariance, locality (m-hop receptive field, Sec. 2.1), the
+  in-degree special case of the aggregation.
+* Patch equivalence conditions (1)-(3) of Sec. 2.2.
+* Integrators: the paper's H2 formula (App. A, equation heun), Taylor
+  closed forms with a linear stand-in, and observed local-error orders
+  (Sec. 2.3, equation FE_HUEN).
+"""
+import json
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import synth
+
+torch.set_default_dtype(torch.float64)
+GOLD = os.path.join(os.path.dirname(__file__), "golden", "paper_facts.json")
+
+
+def small(shape=(5, 4), m=2, seed=0, randomize=True):
+    M = synth.mesh(shape, seed)
+    g = O.build_graph(M["cells"], M["pos"])
+    P = synth.xavier_params(m, seed, randomize_norm=randomize)
+    return M, g, P
+
+
+# ---------------------------------------------------------------- MLP / LN
+def test_mlp_ln_vs_torch():
+    rng = np.random.default_rng(0)
+    x = rng.standard_normal((7, 12))
+    p = {"W1": rng.standard_normal((16, 12)), "b1": rng.standard_normal(16),
+         "W2": rng.standard_normal((5, 16)), "b2": rng.standard_normal(5),
+         "gamma": rng.standard_normal(5), "beta": rng.standard_normal(5)}
+    y, _ = O.mlp(x, p)
+    T = {k: torch.tensor(v) for k, v in p.items()}
+    ref = torch.nn.functional.linear(
+        torch.relu(torch.nn.functional.linear(torch.tensor(x), T["W1"], T["b1"])),
+        T["W2"], T["b2"])
+    assert np.allclose(y, ref.numpy(), rtol=1e-13, atol=1e-13)
+    ln, _ = O.layer_norm(y, p["gamma"], p["beta"])
+    ref_ln = torch.nn.functional.layer_norm(ref, (5,), T["gamma"], T["beta"], 1e-5)
+    assert np.allclose(ln, ref_ln.numpy(), rtol=1e-12, atol=1e-12)
+
+
+def test_layer_norm_constant_gives_beta():
+    beta = np.linspace(-1, 1, 128)
+    gamma = np.full(128, 3.0)
+    y, _ = O.layer_norm(np.full((3, 128), 7.25), gamma, beta)
+    assert np.array_equal(y, np.broadcast_to(beta, (3, 128)))
+    z = np.random.default_rng(1).standard_normal((4, 128)) * 5
+    y, _ = O.layer_norm(z, np.ones(128), np.zeros(128))
+    var = z.var(axis=1)
+    assert np.allclose(y.mean(axis=1), 0, atol=1e-13)
+    assert np.allclose(y.var(axis=1), var / (var + 1e-5), rtol=1e-12)
+
+
+# ----------------------------------------------- dense brute force (torch)
+def dense_mgn(g, P, node_in, efeat, m, D=128):
+    """Whole MGN call with dense one-hot incidence matrices (torch fp64)."""
+    N, E = g.n_nodes, g.n_edges
+    S = torch.zeros(E, N)
+    S[torch.arange(E), torch.tensor(g.senders)] = 1.0
+    R = torch.zeros(E, N)
+    R[torch.arange(E), torch.tensor(g.receivers)] = 1.0
+    F = torch.nn.functional
+    off = [0]
+    flat = P
+
+    def take(*shape):
+        n = int(np.prod(shape))
+        v = flat[off[0]:off[0] + n].reshape(shape)
+        off[0] += n
+        return v
+
+    def block(din, dout, ln):
+        W1, b1, W2, b2 = take(D, din), take(D), take(dout, D), take(dout)
+        gb = (take(dout), take(dout)) if ln else None
+
+        def f(x):
+            y = F.linear(F.relu(F.linear(x, W1, b1)), W2, b2)
+            return F.layer_norm(y, (dout,), gb[0], gb[1], 1e-5) if ln else y
+        return f
+
+    enc_n, enc_e = block(8, D, True), block(4, D, True)
+    blocks = [(block(3 * D, D, True), block(2 * D, D, True)) for _ in range(m)]
+    dec = block(D, 4, False)
+    h = enc_n(node_in)
+    e = enc_e(efeat)
+    for fe, fn in blocks:
+        msg = fe(torch.cat([e, S @ h, R @ h], dim=1))
+        agg = R.T @ msg
+        h, e = h + fn(torch.cat([h, agg], dim=1)), e + msg
+    return dec(h)
+
+
+@pytest.mark.parametrize("shape,m", [((4, 3), 1), ((5, 4), 2), ((3, 3, 3), 2)])
+def test_dense_brute_force_forward_and_autograd(shape, m):
+    M, g, P = small(shape, m, seed=3)
+    w = synth.loss_weights(g.n_nodes, 3)
+    out, tape = O.mgn_forward(g, P, M["node_in"], g.efeat, m, keep=True)
+    gp, gin = O.mgn_backward(tape, w)
+    Pt = torch.tensor(P.astype(np.float64), requires_grad=True)
+    xt = torch.tensor(M["node_in"].astype(np.float64), requires_grad=True)
+    ref = dense_mgn(g, Pt, xt, torch.tensor(g.efeat.astype(np.float64)), m)
+    assert np.allclose(out, ref.detach().numpy(), rtol=1e-11, atol=1e-11)
+    (ref * torch.tensor(w.astype(np.float64))).sum().backward()
+    assert np.allclose(gp, Pt.grad.numpy(), rtol=1e-9, atol=1e-9)
+    assert np.allclose(gin, xt.grad.numpy(), rtol=1e-9, atol=1e-9)
+
+
+def test_finite_differences():
+    m = 2
+    M, g, P = small((4, 4), m, seed=5)
+    P = P.astype(np.float64)
+    w = synth.loss_weights(g.n_nodes, 5).astype(np.float64)
+    x = M["node_in"].astype(np.float64)
+
+    def loss(Pv, xv):
+        return float((O.mgn_forward(g, Pv, xv, g.efeat, m) * w).sum())
+
+    _, tape = O.mgn_forward(g, P, x, g.efeat, m, keep=True)
+    gp, gin = O.mgn_backward(tape, w)
+    rng = np.random.default_rng(9)
+    idx = rng.choice(P.size, 24, replace=False)
+    h = 1e-6
+    for i in idx:
+        Pp, Pm = P.copy(), P.copy()
+        Pp[i] += h
+        Pm[i] -= h
+        fd = (loss(Pp, x) - loss(Pm, x)) / (2 * h)
+        assert abs(fd - gp[i]) <= 1e-6 * max(1.0, abs(gp[i])), (i, fd, gp[i])
+    for (v, c) in [(0, 4), (5, 6), (11, 7), (15, 5)]:
+        xp, xm = x.copy(), x.copy()
+        xp[v, c] += h
+        xm[v, c] -= h
+        fd = (loss(P, xp) - loss(P, xm)) / (2 * h)
+        assert abs(fd - gin[v, c]) <= 1e-6 * max(1.0, abs(gin[v, c]))
+
+
+def test_backward_linear_in_grad_out():
+    M, g, P = small((4, 3), 1, seed=2)
+    _, tape = O.mgn_forward(g, P, M["node_in"], g.efeat, 1, keep=True)
+    w1 = synth.loss_weights(g.n_nodes, 1).astype(np.float64)
+    w2 = synth.loss_weights(g.n_nodes, 2).astype(np.float64)
+    a, _ = O.mgn_backward(tape, w1)
+    b, _ = O.mgn_backward(tape, w2)
+    c, _ = O.mgn_backward(tape, 2.0 * w1 - 3.0 * w2)
+    assert np.allclose(c, 2 * a - 3 * b, rtol=1e-10, atol=1e-10)
+
+
+# ----------------------------------------------------- structural pins
+def test_aggregate_is_in_degree():
+    """Edge MLP weights zero and LayerNorm offset one: every message is the
+    all-ones vector, so the aggregate of a node is its in-degree."""
+    m = 1
+    M, g, P = small((5, 4, 3), m, seed=1)
+    Pd = O.unpack_params(P, m)
+    P64 = P.astype(np.float64).copy()
+    off = 0
+    for name, fields in O.param_layout(m):
+        for f, shape in fields:
+            n = int(np.prod(shape))
+            if name == "block0.edge":
+                if f in ("W1", "W2", "b1", "b2"):
+                    P64[off:off + n] = 0.0
+                if f == "beta":
+                    P64[off:off + n] = 1.0
+            off += n
+    del Pd
+    _, tape = O.mgn_forward(g, P64, M["node_in"], g.efeat, m, keep=True)
+    (x_mlp, _, _), _ = tape["blocks"][0][1]
+    agg = x_mlp[:, 128:]
+    deg = np.diff(g.rowptr).astype(np.float64)
+    assert np.array_equal(agg, np.repeat(deg[:, None], 128, axis=1))
+
+
+def test_permutation_equivariance():
+    m = 2
+    shape = (5, 4, 3)
+    M, g, P = small(shape, m, seed=4)
+    out = O.mgn_forward(g, P, M["node_in"], g.efeat, m)
+    perm = synth.relabel(g.n_nodes, 4)  # new id of old node i
+    pos2 = np.empty_like(M["pos"])
+    pos2[perm] = M["pos"]
+    x2 = np.empty_like(M["node_in"])
+    x2[perm] = M["node_in"]
+    g2 = O.build_graph(perm[M["cells"]], pos2)
+    out2 = O.mgn_forward(g2, P, x2, g2.efeat, m)
+    assert np.allclose(out2[perm], out, rtol=1e-11, atol=1e-11)
+
+
+def test_locality_receptive_field():
+    """After m steps a node sees exactly its m-hop neighbourhood (Sec. 2.1)."""
+    m = 2
+    M, g, P = small((9, 3), m, seed=6)
+    x = M["node_in"].astype(np.float64)
+    out = O.mgn_forward(g, P, x, g.efeat, m)
+    src = np.zeros(g.n_nodes, bool)
+    src[0] = True
+    hop = O.hop_distance(g, src, g.n_nodes)
+    x2 = x.copy()
+    x2[0, 4:] += 0.5
+    out2 = O.mgn_forward(g, P, x2, g.efeat, m)
+    far = hop > m
+    assert far.any()
+    assert np.array_equal(out2[far], out[far])
+    near = (hop >= 0) & (hop <= m)
+    assert np.all(np.abs(out2[near] - out[near]).max(axis=1) > 0)
+
+
+# --------------------------------------------------- patch equivalence
+def _patch_inputs(M, pt):
+    return M["node_in"][pt.node_l2g]
+
+
+@pytest.mark.parametrize("shape,splits,m,k", [((9, 8), (3, 2), 2, 2),
+                                              ((5, 5, 6), (1, 1, 3), 2, 3)])
+def test_condition1_interior_outputs_bitwise(shape, splits, m, k):
+    M, g, P = small(shape, m, seed=7)
+    out = O.mgn_forward(g, P, M["node_in"], g.efeat, m)
+    part = O.partition(M["pos"], splits)
+    for p in range(int(part.max()) + 1):
+        pt = O.extract_patch(g, part, p, k)
+        if pt.n_nodes == 0:
+            continue
+        o = O.mgn_forward(pt, P, _patch_inputs(M, pt), pt.efeat, m)
+        it = pt.hop == 0
+        assert np.array_equal(o[it], out[pt.node_l2g[it]])
+
+
+def test_condition1_violated_differs():
+    m = 3
+    M, g, P = small((10, 6), m, seed=8)
+    out = O.mgn_forward(g, P, M["node_in"], g.efeat, m)
+    part = O.partition(M["pos"], (2, 1))
+    pt = O.extract_patch(g, part, 0, 1)  # k = 1 < m
+    o = O.mgn_forward(pt, P, _patch_inputs(M, pt), pt.efeat, m)
+    it = pt.hop == 0
+    assert not np.allclose(o[it], out[pt.node_l2g[it]], rtol=1e-6, atol=1e-6)
+
+
+def test_conditions_2_3_gradient_accumulation():
+    """Summing, over all patches, gradients of the loss on subdomain nodes
+    equals the whole-mesh gradient (Sec. 2.2 conditions 2 and 3)."""
+    m = 2
+    M, g, P = small((8, 7), m, seed=9)
+    w = synth.loss_weights(g.n_nodes, 9)
+    _, tape = O.mgn_forward(g, P, M["node_in"], g.efeat, m, keep=True)
+    gw, _ = O.mgn_backward(tape, w)
+    part = O.partition(M["pos"], (2, 2))
+    acc = np.zeros_like(gw)
+    for p in range(4):
+        pt = O.extract_patch(g, part, p, m)
+        _, t = O.mgn_forward(pt, P, _patch_inputs(M, pt), pt.efeat, m, keep=True)
+        wp = w[pt.node_l2g] * (pt.hop == 0)[:, None]
+        gp, _ = O.mgn_backward(t, wp)
+        acc += gp
+    assert np.allclose(acc, gw, rtol=1e-10, atol=1e-10 * np.abs(gw).max())
+
+
+# --------------------------------------------------------- integrators
+def test_heun2_matches_paper_formula():
+    """App. A, equation heun: y + 1/2 (MGN(y) + MGN(y + MGN(y)))."""
+    m = 1
+    M, g, P = small((4, 4), m, seed=10)
+    st, y = M["onehot"].astype(np.float64), M["states"].astype(np.float64)
+
+    def mgn(v):
+        return O.mgn_forward(g, P, np.concatenate([st, v], 1), g.efeat, m)
+    ref = y + 0.5 * (mgn(y) + mgn(y + mgn(y)))
+    got = O.integrate_step(g, P, "heun2", st, y, g.efeat, m)
+    assert np.allclose(got, ref, rtol=1e-14, atol=1e-14)
+    fe = O.integrate_step(g, P, "euler", st, y, g.efeat, m)
+    assert np.array_equal(fe, y + mgn(y))
+
+
+@pytest.mark.parametrize("scheme,order", [("euler", 1), ("heun2", 2),
+                                          ("midpoint", 2), ("heun3", 3),
+                                          ("rk4", 4)])
+def test_linear_standin_taylor(scheme, order):
+    """With K(y) = y A the step is the Taylor polynomial sum_j y A^j / j!
+    up to the method's order."""
+    rng = np.random.default_rng(11)
+    A = rng.standard_normal((4, 4)) * 0.3
+    y = rng.standard_normal((6, 4))
+    got = O.integrate_step(None, None, scheme, np.zeros((6, 4)), y, None, 0,
+                           model=lambda v: v @ A)
+    ref, term = y.copy(), y.copy()
+    for j in range(1, order + 1):
+        term = term @ A / j
+        ref = ref + term
+    assert np.allclose(got, ref, rtol=1e-13, atol=1e-13)
+
+
+@pytest.mark.parametrize("scheme", ["euler", "heun2", "heun3", "rk4", "midpoint"])
+def test_observed_local_error_order(scheme):
+    """y' = -y^2 (exact y(t) = y0/(1+y0 t)): halving h divides the one-step
+    error by 2^(p+1).  Paper: FE O(h^2), H2 O(h^3), H3 O(h^4)."""
+    facts = json.load(open(GOLD))
+    p_expect = {"euler": 2, "heun2": 3, "midpoint": 3, "heun3": 4, "rk4": 5}[scheme]
+    if scheme in facts["local_error_order"]:
+        assert facts["local_error_order"][scheme] == p_expect
+    y0 = np.array([[0.7, 1.1, 0.3, 1.5]])
+    errs = []
+    for h in (0.02, 0.01, 0.005):
+        got = O.integrate_step(None, None, scheme, np.zeros_like(y0), y0, None, 0,
+                               model=lambda v, h=h: -h * v * v)
+        errs.append(np.abs(got - y0 / (1 + y0 * h)).max())
+    orders = np.log2(np.array(errs[:-1]) / np.array(errs[1:]))
+    assert np.all(np.abs(orders - p_expect) < 0.25), orders
+
+
+def test_integrator_backward_fd():
+    m = 1
+    M, g, P = small((4, 3), m, seed=12)
+    st, y = M["onehot"].astype(np.float64), M["states"].astype(np.float64)
+    w = synth.loss_weights(g.n_nodes, 12).astype(np.float64)
+    for scheme in ("heun2", "rk4", "heun3"):
+        yn, tape = O.integrate_step(g, P, scheme, st, y, g.efeat, m, keep=True)
+        gp, gy = O.integrate_backward(tape, w)
+
+        def L(Pv, yv):
+            return float((O.integrate_step(g, Pv, scheme, st, yv, g.efeat, m) * w).sum())
+        h = 1e-6
+        for (v, c) in [(0, 0), (3, 2), (7, 3)]:
+            yp, ym = y.copy(), y.copy()
+            yp[v, c] += h
+            ym[v, c] -= h
+            fd = (L(P, yp) - L(P, ym)) / (2 * h)
+            assert abs(fd - gy[v, c]) <= 1e-6 * max(1, abs(fd))
+        P64 = P.astype(np.float64)
+        for i in (5, 20000, 60000, P.size - 3):
+            Pp, Pm = P64.copy(), P64.copy()
+            Pp[i] += h
+            Pm[i] -= h
+            fd = (L(Pp, y) - L(Pm, y)) / (2 * h)
+            assert abs(fd - gp[i]) <= 1e-6 * max(1, abs(fd))
+
+
+def test_param_layout_matches_generator():
+    """The oracle's unpacking order agrees with the generator's field list and
+    the documented total (1,788,036 floats at 15 steps, latent 128)."""
+    assert O.n_params(15) == 1788036
+    names = [(f"{n}.{f}", s) for n, fs in O.param_layout(15) for f, s in fs]
+    gen = [(n, s) for n, _, s in synth.param_shapes(15)]
+    assert names == gen
+
+
+def test_masked_mse_grad():
+    out = np.array([[1.0, 2, 3, 4], [0, 0, 0, 0]])
+    tgt = np.zeros((2, 4))
+    gr = O.masked_mse_grad(out, tgt, np.array([1, 0]))
+    assert np.allclose(gr[0], 2 * out[0] / 4) and np.all(gr[1] == 0)
