@@ -1,0 +1,235 @@
+/*
+ * mgn.h -- C ABI of the MI355X (gfx950) MeshGraphNets message-passing library.
+ *
+ * What the library computes (Bartoldson, Hu et al., "Scientific Computing
+ * Algorithms to Learn Enhanced Scalable Surrogates for Mesh Physics",
+ * arXiv 2304.00338):
+ *   - the mesh graph whose edges come from the simplices of the mesh
+ *     (App. B) with MGN edge features (App. C);
+ *   - equal-split subdomains and k-hop ghost-zone patches (Sec. 2.2);
+ *   - one MGN call: encoder, m message-passing steps (each updates every edge
+ *     from its incident nodes, then every node from the sum of its incident
+ *     edge messages, Sec. 2.1), decoder; and its reverse mode;
+ *   - one explicit integration step y' = y + sum_i b_i K_i with
+ *     K_i = MGN(stage i), i.e. the update rule of Sec. 2.1 and the Heun forms
+ *     of Sec. 2.3 / App. A (equation heun) generalised to a Butcher tableau.
+ *
+ * Conventions
+ *   - Every function returns an int status: MGN_OK (0) or a negative MGN_ERR_*.
+ *     On error the out-parameters are left untouched and mgn_last_error()
+ *     returns a message (thread-local, valid until the next call on the same
+ *     thread).  No C++ exception crosses this boundary.
+ *   - Host pointers are used for graph and patch construction.  Device
+ *     pointers (HIP device memory) are used by mgn_forward, mgn_backward and
+ *     mgn_integrate_step; those calls are asynchronous on the HIP stream
+ *     passed as `stream` (a hipStream_t cast to void*, NULL = default
+ *     stream), and every buffer must stay alive until that stream has
+ *     finished the work (and, for a saved call, until mgn_backward has run).
+ *   - The caller owns every buffer it passes; the library never frees caller
+ *     memory and never allocates device memory: all device scratch lives in
+ *     the caller's workspace, whose size mgn_ctx_create reports.
+ *   - Opaque handles (mgn_graph, mgn_ctx) are created and destroyed by the
+ *     library; destroying NULL is a no-op.
+ *   - Index arrays are int32 (E < 2^31 and N < 2^31 are checked); features
+ *     and parameters are float32, row-major.
+ */
+#ifndef MGN_H
+#define MGN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes ---------------------------------------------------- */
+#define MGN_OK 0
+#define MGN_ERR_ARG (-1)       /* null pointer, negative size, unknown enum */
+#define MGN_ERR_RANGE (-2)     /* an index outside [0, N) or a bad subdomain id */
+#define MGN_ERR_SHAPE (-3)     /* unsupported dimensions, or N/E too large */
+#define MGN_ERR_WORKSPACE (-4) /* caller workspace smaller than required */
+#define MGN_ERR_STATE (-5)     /* backward without a saved call, ctx/graph mismatch */
+#define MGN_ERR_DEVICE (-6)    /* a HIP runtime error (message kept) */
+#define MGN_ERR_NOMEM (-7)     /* host allocation failed */
+
+/* ---- enums ----------------------------------------------------------- */
+#define MGN_FP32 0 /* fp32 MFMA, fp32 latent streams */
+#define MGN_BF16 1 /* bf16 MFMA operands, bf16 edge-latent stream, fp32
+                      accumulation, LayerNorm statistics, sums and node state */
+
+/* Integration schemes: Butcher tableaux with MGN in place of h*f.
+ * EULER    y' = y + K1                                  (Sec. 2.1)
+ * HEUN2    a21 = 1, b = (1/2, 1/2)                       (App. A, eq. heun)
+ * MIDPOINT a21 = 1/2, b = (0, 1)
+ * HEUN3    a21 = 1/3, a32 = 2/3, b = (1/4, 0, 3/4)       (Heun's 3rd order, Sec. 2.3)
+ * RK4      a21 = a32 = 1/2, a43 = 1, b = (1, 2, 2, 1)/6 */
+#define MGN_EULER 0
+#define MGN_HEUN2 1
+#define MGN_MIDPOINT 2
+#define MGN_HEUN3 3
+#define MGN_RK4 4
+
+/* ---- model configuration --------------------------------------------- */
+typedef struct mgn_config {
+  int32_t node_in;    /* node input features; must be 8 (4 one-hot + 4 state) */
+  int32_t edge_in;    /* edge input features; must be 4 */
+  int32_t latent;     /* latent width; must be 128 */
+  int32_t out;        /* decoder outputs; must be 4 */
+  int32_t mp_steps;   /* m >= 0 message-passing steps (unshared weights) */
+  int32_t mlp_layers; /* Linear layers per MLP; must be 2 */
+  float ln_eps;       /* LayerNorm epsilon (biased variance), e.g. 1e-5 */
+  int32_t precision;  /* MGN_FP32 or MGN_BF16 */
+} mgn_config;
+
+/* Flat float32 parameter buffer, in this order (weights [out][in] row-major):
+ *   enc_node: W1[128][8]  b1[128] W2[128][128] b2[128] gamma[128] beta[128]
+ *   enc_edge: W1[128][4]  b1 W2[128][128] b2 gamma beta
+ *   for each block i < m:
+ *     edge:   W1[128][384] (input order: edge latent, sender latent,
+ *             receiver latent) b1 W2[128][128] b2 gamma beta
+ *     node:   W1[128][256] (input order: node latent, aggregate) b1
+ *             W2[128][128] b2 gamma beta
+ *   dec:      W1[128][128] b1[128] W2[4][128] b2[4]          (no LayerNorm)
+ * 17,920 + 17,408 + m * (66,048 + 49,664) + 17,028 floats
+ * (1,788,036 at m = 15). */
+int64_t mgn_param_count(const mgn_config* cfg);
+
+/* ---- host graphs (App. B edges, Sec. 2.2 patches) --------------------- */
+typedef struct mgn_graph mgn_graph;
+
+/* Every unordered pair of distinct vertices that share a cell becomes one
+ * undirected mesh edge, stored as two directed edges; duplicates are merged
+ * and repeated vertices in a cell make no self-loop.  Edges are sorted by
+ * (receiver, sender).  rev[e] is the edge in the opposite direction.  Edge
+ * features: [x_s - x_r, |x_s - x_r|] evaluated in fp64 from the float32
+ * positions and rounded once to float32 (2D: [dx, dy, |d|, 0]).
+ * cells [n_cells][verts_per_cell] (2, 3 or 4), pos [n_nodes][dim] (2 or 3).
+ * Errors: ARG (null, bad dim / verts_per_cell), RANGE (vertex id outside
+ * [0, n_nodes)), SHAPE (n_nodes or edge count >= 2^31). */
+int mgn_build_graph(const int32_t* cells, int64_t n_cells,
+                    int32_t verts_per_cell, const float* pos, int64_t n_nodes,
+                    int32_t dim, mgn_graph** out);
+
+/* Node and directed-edge counts; either pointer may be NULL. */
+int mgn_graph_info(const mgn_graph* g, int64_t* n_nodes, int64_t* n_edges);
+
+/* Copy the CSR arrays out (host buffers; any pointer may be NULL):
+ * rowptr[N+1], senders[E], receivers[E], rev[E], efeat[E][4]. */
+int mgn_graph_copy(const mgn_graph* g, int32_t* rowptr, int32_t* senders,
+                   int32_t* receivers, int32_t* rev, float* efeat);
+
+/* Receiver-aligned edge tiles for the device kernels.  Tile t is int32[4]
+ * {node_begin, node_end, edge_begin, edge_end}: the whole in-edge segments
+ * of nodes [node_begin, node_end), at most mgn_tile_edges() edges and
+ * mgn_tile_nodes() nodes.  A node with more in-edges than one tile holds is
+ * split into chunk tiles {v, -1 - slot, edge_begin, edge_end} whose sums go to
+ * partial slot `slot`, and listed in long_nodes as int32[4]
+ * {v, first_slot, n_chunks, 0}.  Tiles cover every node in order, so the
+ * sum over a segment never depends on where the segment sits in the array.
+ * Query the counts with NULL buffers first. */
+int mgn_graph_schedule(const mgn_graph* g, int32_t* tiles, int64_t* n_tiles,
+                       int32_t* long_nodes, int64_t* n_long);
+int32_t mgn_tile_edges(void);
+int32_t mgn_tile_nodes(void);
+
+void mgn_graph_destroy(mgn_graph* g);
+
+/* Subdomain ids from an equal split of the bounding box along every axis
+ * (Sec. 2.2; App. C uses 3 x 4 in 2D and 12 x 12 x 15 in 3D).  Per axis the
+ * index is floor(splits * (x - lo) / (hi - lo)), evaluated in fp64 left to
+ * right and clamped to [0, splits - 1] (0 on a degenerate axis); ids run x
+ * fastest.  pos [n][dim], splits [dim], part_out [n] (host).
+ * Errors: ARG. */
+int mgn_partition(const float* pos, int64_t n, int32_t dim,
+                  const int32_t* splits, int32_t* part_out);
+
+/* Patch p of a partition (Sec. 2.2, Fig. 1): the nodes of subdomain p plus
+ * every node within k undirected hops (the ghost zone), with the induced
+ * edges.  Local node ids follow ascending global ids, so in-segment edge
+ * order matches the whole graph.  An empty subdomain gives a valid 0-node
+ * patch.  part [N] is a host array of subdomain ids >= 0.
+ * Errors: ARG (k < 0, null), RANGE (p outside [0, max(part)], or a negative
+ * id in part). */
+int mgn_extract_patch(const mgn_graph* g, const int32_t* part, int32_t p,
+                      int32_t k, mgn_graph** patch);
+
+/* Patch maps (host buffers; any pointer may be NULL): node_l2g[Np] global id
+ * of each local node, hop[Np] ghost distance (0 = subdomain node),
+ * interior[Np] 1 for subdomain nodes, edge_l2g[Ep] global edge id,
+ * n_interior number of subdomain nodes.  Errors: STATE if g is not a patch. */
+int mgn_patch_copy_maps(const mgn_graph* patch, int32_t* node_l2g,
+                        int32_t* hop, uint8_t* interior, int64_t* edge_l2g,
+                        int64_t* n_interior);
+
+/* ---- device execution -------------------------------------------------- */
+
+/* Device view of a graph: device copies of the arrays above. */
+typedef struct mgn_dgraph {
+  int64_t n_nodes;
+  int64_t n_edges;
+  const int32_t* rowptr;     /* [N+1] */
+  const int32_t* senders;    /* [E] */
+  const int32_t* rev;        /* [E] */
+  const int32_t* tiles;      /* [n_tiles][4] from mgn_graph_schedule */
+  int64_t n_tiles;
+  const int32_t* long_nodes; /* [n_long][4], may be NULL when n_long == 0 */
+  int64_t n_long;
+} mgn_dgraph;
+
+typedef struct mgn_ctx mgn_ctx;
+
+/* A context plans the device workspace for graphs of up to max_nodes nodes
+ * and max_edges edges, integration schemes of up to max_stages stages, and
+ * (save != 0) keeping activations for mgn_backward.  *ws_bytes receives the
+ * workspace size, a pure function of these arguments.
+ * Errors: ARG, SHAPE (unsupported config, sizes >= 2^31). */
+int mgn_ctx_create(const mgn_config* cfg, int64_t max_nodes, int64_t max_edges,
+                   int32_t max_stages, int32_t save, size_t* ws_bytes,
+                   mgn_ctx** out);
+void mgn_ctx_destroy(mgn_ctx* ctx);
+
+/* One MGN call (Sec. 2.1): out[N][4] = decoder(processor^m(encoder(node_in,
+ * efeat))).  params: flat float32 buffer (device).  node_in [N][8],
+ * efeat [E][4], out [N][4] (device).  With save != 0 the activations stay in
+ * the workspace for mgn_backward (the context must have been created with
+ * save).  The workspace must stay untouched until backward.  N = 0 is a no-op.
+ * Errors: ARG, SHAPE (graph larger than the context), WORKSPACE, DEVICE. */
+int mgn_forward(mgn_ctx* ctx, const mgn_dgraph* g, const float* params,
+                const float* node_in, const float* efeat, float* out,
+                int32_t save, void* workspace, size_t ws_bytes, void* stream);
+
+/* Reverse mode of the last saved mgn_forward or mgn_integrate_step on ctx.
+ * grad_out: [N][4] gradient of the loss with respect to out (or to y_next).
+ * grad_params: flat float32 [mgn_param_count]; the gradient is ADDED to it, so
+ * gradients of several patches accumulate (Sec. 2.2, condition 3).
+ * grad_in (nullable): for a forward call, [N][8] gradient with respect to
+ * node_in; for an integration step, [N][4] gradient with respect to y.  The
+ * accumulation order is fixed, so results are bitwise reproducible.
+ * Errors: ARG, STATE (nothing saved), DEVICE. */
+int mgn_backward(mgn_ctx* ctx, const float* grad_out, float* grad_params,
+                 float* grad_in, void* stream);
+
+/* One explicit integration step with MGN as the scaled derivative
+ * (Sec. 2.1, Sec. 2.3, App. A): K_i = MGN([static, y + sum_j a_ij K_j]),
+ * y_next = y + sum_i b_i K_i.  static [N][4] (one-hot node type),
+ * y [N][4], efeat [E][4], y_next [N][4] (device).
+ * Errors: ARG (unknown scheme, or more stages than the context plans), plus
+ * those of mgn_forward. */
+int mgn_integrate_step(mgn_ctx* ctx, const mgn_dgraph* g, const float* params,
+                       int32_t scheme, const float* static_feat,
+                       const float* y, const float* efeat, float* y_next,
+                       int32_t save, void* workspace, size_t ws_bytes,
+                       void* stream);
+
+/* Number of stages of a scheme (1, 2, 2, 3, 4), or MGN_ERR_ARG. */
+int mgn_scheme_stages(int32_t scheme);
+
+/* Library version string and the last error message of this thread. */
+const char* mgn_version(void);
+const char* mgn_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* MGN_H */

@@ -48,7 +48,7 @@ __all__ = [
     "Graph", "Patch", "build_graph", "partition", "extract_patch",
     "param_layout", "unpack_params", "n_params", "mlp", "layer_norm", "hop_distance", "edge_features", "pack_grads",
     "mgn_forward", "mgn_backward", "TABLEAUS", "integrate_step",
-    "integrate_backward", "masked_mse_grad",
+    "integrate_backward", "masked_mse_grad", "relu_kinks",
 ]
 
 LN_EPS = 1e-5
@@ -324,9 +324,11 @@ def _mlp_ln(x, p, eps):
     return y, (t_mlp, t_ln)
 
 
-def _mlp_ln_bwd(tape, ybar, p, g):
+def _mlp_ln_bwd(tape, ybar, p, g, flip=None):
     """Reverse mode of _mlp_ln; adds parameter gradients into g and returns
-    the gradient with respect to the MLP input."""
+    the gradient with respect to the MLP input.  ``flip`` (rows, units)
+    selects ReLU inputs at which the other one-sided derivative is taken
+    (a different valid subgradient at a kink)."""
     (x, z1, a1), t_ln = tape
     if t_ln is not None:
         xhat, rstd = t_ln
@@ -340,7 +342,11 @@ def _mlp_ln_bwd(tape, ybar, p, g):
     g["W2"] += z2bar.T @ a1
     g["b2"] += z2bar.sum(axis=0)
     a1bar = z2bar @ p["W2"]
-    z1bar = a1bar * (z1 > 0.0)
+    mask = z1 > 0.0
+    if flip is not None:
+        mask = mask.copy()
+        mask[flip[0], flip[1]] ^= True
+    z1bar = a1bar * mask
     g["W1"] += z1bar.T @ x
     g["b1"] += z1bar.sum(axis=0)
     return z1bar @ p["W1"]
@@ -390,27 +396,56 @@ def mgn_forward(g: Graph, params, node_in, efeat, mp_steps, latent=128,
     return out, tape
 
 
-def mgn_backward(tape, grad_out):
+def relu_kinks(tape, tau):
+    """ReLU inputs of one saved MGN call with |z| < tau: where an evaluation
+    in another precision may take the other branch.  Returns a list of
+    (mlp_name, row, unit)."""
+    out = []
+    named = [("enc_node", tape["enc_n"]), ("enc_edge", tape["enc_e"]), ("dec", tape["dec"])]
+    for i, (t_e, t_n) in enumerate(tape["blocks"]):
+        named += [(f"block{i}.edge", t_e), (f"block{i}.node", t_n)]
+    for name, t in named:
+        z1 = t[0][1]
+        rows, units = np.nonzero(np.abs(z1) < tau)
+        out += [(name, int(r), int(u)) for r, u in zip(rows, units)]
+    return out
+
+
+def _flip_sets(kinks):
+    fl = {}
+    for name, r, u in kinks or ():
+        fl.setdefault(name, ([], []))
+        fl[name][0].append(r)
+        fl[name][1].append(u)
+    return {k: (np.array(v[0]), np.array(v[1])) for k, v in fl.items()}
+
+
+def mgn_backward(tape, grad_out, flips=None):
     """Reverse mode of mgn_forward.  Returns (flat parameter gradient,
-    gradient with respect to node_in)."""
+    gradient with respect to node_in).  ``flips``: optional list of
+    (mlp_name, row, unit) ReLU inputs at which the other one-sided
+    derivative is used (see relu_kinks)."""
+    fl = _flip_sets(flips)
     P, g, R = tape["P"], tape["g"], tape["R"]
     m_steps, D = tape["mp_steps"], tape["latent"]
     S = _incidence(g.senders, g.n_nodes)
     G = zero_grads(P)
     ybar = np.asarray(grad_out, dtype=np.float64)
-    hbar = _mlp_ln_bwd(tape["dec"], ybar, P["dec"], G["dec"])
+    hbar = _mlp_ln_bwd(tape["dec"], ybar, P["dec"], G["dec"], fl.get("dec"))
     ebar = np.zeros((g.n_edges, D))
     for i in reversed(range(m_steps)):
         t_e, t_n = tape["blocks"][i]
-        xnbar = _mlp_ln_bwd(t_n, hbar, P[f"block{i}.node"], G[f"block{i}.node"])
+        xnbar = _mlp_ln_bwd(t_n, hbar, P[f"block{i}.node"], G[f"block{i}.node"],
+                            fl.get(f"block{i}.node"))
         hbar = hbar + xnbar[:, :D]
         aggbar = xnbar[:, D:]
         mbar = ebar + aggbar[g.receivers]
-        xebar = _mlp_ln_bwd(t_e, mbar, P[f"block{i}.edge"], G[f"block{i}.edge"])
+        xebar = _mlp_ln_bwd(t_e, mbar, P[f"block{i}.edge"], G[f"block{i}.edge"],
+                            fl.get(f"block{i}.edge"))
         ebar = ebar + xebar[:, :D]
         hbar = hbar + S @ xebar[:, D:2 * D] + R @ xebar[:, 2 * D:]
-    _mlp_ln_bwd(tape["enc_e"], ebar, P["enc_edge"], G["enc_edge"])
-    gin = _mlp_ln_bwd(tape["enc_n"], hbar, P["enc_node"], G["enc_node"])
+    _mlp_ln_bwd(tape["enc_e"], ebar, P["enc_edge"], G["enc_edge"], fl.get("enc_edge"))
+    gin = _mlp_ln_bwd(tape["enc_n"], hbar, P["enc_node"], G["enc_node"], fl.get("enc_node"))
     return pack_grads(G, m_steps, D), gin
 
 

@@ -1,0 +1,616 @@
+// C-ABI entry points for device execution: context and workspace planning,
+// one MGN call (Sec. 2.1), its reverse mode (with the gradient accumulation
+// of Sec. 2.2, condition 3) and explicit integration steps (Sec. 2.1, 2.3,
+// App. A).  All device memory is the caller's workspace; every launch goes
+// to the caller's stream.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "internal.hpp"
+#include "launch.hpp"
+
+namespace mgn {
+
+namespace {
+
+constexpr int D = 128;
+constexpr int kPartBlocks = 512;       // persistent blocks of the backward kernels
+constexpr int64_t kPartStride = 49664; // largest per-block partial (node MLP)
+
+struct Off {
+  int64_t W1 = 0, b1 = 0, W2 = 0, b2 = 0, g = -1, bt = -1, size = 0;
+};
+
+struct PackOff {
+  int64_t W1 = -1, W1t = -1, W2 = -1, W2t = -1;
+};
+
+struct Model {
+  int m = 0;
+  Off enc_node, enc_edge, dec;
+  std::vector<Off> edge, node;
+  int64_t total = 0;
+  PackOff p_enc_node, p_enc_edge, p_dec;
+  std::vector<PackOff> p_edge, p_node;
+  int64_t pack_elems = 0;
+  std::vector<PackEnt> ents;
+};
+
+Off mlp_off(int64_t& o, int din, int dout, bool ln) {
+  Off r;
+  r.W1 = o;
+  o += (int64_t)D * din;
+  r.b1 = o;
+  o += D;
+  r.W2 = o;
+  o += (int64_t)dout * D;
+  r.b2 = o;
+  o += dout;
+  if (ln) {
+    r.g = o;
+    o += dout;
+    r.bt = o;
+    o += dout;
+  }
+  r.size = o - r.W1;
+  return r;
+}
+
+void add_pack(Model& M, int64_t src, int rows, int cols, int64_t& W, int64_t& Wt) {
+  auto al = [](int64_t x) { return (x + 63) & ~int64_t(63); };
+  M.pack_elems = al(M.pack_elems);
+  W = M.pack_elems;
+  M.pack_elems = al(M.pack_elems + (int64_t)rows * cols);
+  Wt = M.pack_elems;
+  M.pack_elems += (int64_t)rows * cols;
+  PackEnt e;
+  e.src = src;
+  e.dst = W;
+  e.dstt = Wt;
+  e.rows = rows;
+  e.cols = cols;
+  M.ents.push_back(e);
+}
+
+Model make_model(int m) {
+  Model M;
+  M.m = m;
+  int64_t o = 0;
+  M.enc_node = mlp_off(o, 8, D, true);
+  M.enc_edge = mlp_off(o, 4, D, true);
+  for (int i = 0; i < m; ++i) {
+    M.edge.push_back(mlp_off(o, 3 * D, D, true));
+    M.node.push_back(mlp_off(o, 2 * D, D, true));
+  }
+  M.dec = mlp_off(o, D, 4, false);
+  M.total = o;
+  add_pack(M, M.enc_node.W2, D, D, M.p_enc_node.W2, M.p_enc_node.W2t);
+  add_pack(M, M.enc_edge.W2, D, D, M.p_enc_edge.W2, M.p_enc_edge.W2t);
+  M.p_edge.resize(m);
+  M.p_node.resize(m);
+  for (int i = 0; i < m; ++i) {
+    add_pack(M, M.edge[i].W1, D, 3 * D, M.p_edge[i].W1, M.p_edge[i].W1t);
+    add_pack(M, M.edge[i].W2, D, D, M.p_edge[i].W2, M.p_edge[i].W2t);
+    add_pack(M, M.node[i].W1, D, 2 * D, M.p_node[i].W1, M.p_node[i].W1t);
+    add_pack(M, M.node[i].W2, D, D, M.p_node[i].W2, M.p_node[i].W2t);
+  }
+  add_pack(M, M.dec.W1, D, D, M.p_dec.W1, M.p_dec.W1t);
+  return M;
+}
+
+size_t al256(size_t x) { return (x + 255) & ~size_t(255); }
+
+struct Layout {
+  size_t pack = 0;
+  // activation sets
+  size_t act = 0, act_stride = 0;
+  size_t e_off = 0, h_off = 0, agg_off = 0, P_off = 0;  // within a set
+  size_t node_in = 0, K = 0, slots = 0;
+  // backward
+  size_t ebar = 0, zbar = 0, hb_a = 0, hb_b = 0, aggbar = 0, R = 0, part = 0, kbar = 0, ystage = 0, gin = 0;
+  size_t total = 0;
+};
+
+}  // namespace
+
+struct Ctx {
+  mgn_config cfg;
+  int64_t maxN = 0, maxE = 0;
+  int32_t max_stages = 1, save = 0;
+  int se = 4;  // bytes per element of the edge-latent stream
+  int ne_sets = 1;
+  Model M;
+  Layout L;
+  // saved state of the last call with save != 0
+  int saved = 0;  // 0 none, 1 forward, 2 integration step
+  int32_t scheme = 0, stages = 0;
+  mgn_dgraph g{};
+  const float* params = nullptr;
+  const float* efeat = nullptr;
+  const float* node_in = nullptr;
+  char* ws = nullptr;
+};
+
+namespace {
+
+struct Tableau {
+  int s;
+  float a[4][4];
+  float b[4];
+};
+
+bool tableau(int32_t scheme, Tableau& t) {
+  std::memset(&t, 0, sizeof(t));
+  switch (scheme) {
+    case MGN_EULER:
+      t.s = 1;
+      t.b[0] = 1.f;
+      return true;
+    case MGN_HEUN2:
+      t.s = 2;
+      t.a[1][0] = 1.f;
+      t.b[0] = 0.5f;
+      t.b[1] = 0.5f;
+      return true;
+    case MGN_MIDPOINT:
+      t.s = 2;
+      t.a[1][0] = 0.5f;
+      t.b[1] = 1.f;
+      return true;
+    case MGN_HEUN3:
+      t.s = 3;
+      t.a[1][0] = 1.f / 3.f;
+      t.a[2][1] = 2.f / 3.f;
+      t.b[0] = 0.25f;
+      t.b[2] = 0.75f;
+      return true;
+    case MGN_RK4:
+      t.s = 4;
+      t.a[1][0] = 0.5f;
+      t.a[2][1] = 0.5f;
+      t.a[3][2] = 1.f;
+      t.b[0] = 1.f / 6.f;
+      t.b[1] = 1.f / 3.f;
+      t.b[2] = 1.f / 3.f;
+      t.b[3] = 1.f / 6.f;
+      return true;
+  }
+  return false;
+}
+
+void plan(Ctx& c) {
+  const int64_t N = c.maxN, E = c.maxE;
+  const int m = c.cfg.mp_steps;
+  const size_t tsz = c.cfg.precision == MGN_BF16 ? 2 : 4;
+  Layout& L = c.L;
+  size_t o = 0;
+  L.pack = o;
+  o = al256(o + (size_t)c.M.pack_elems * tsz);
+  const int le = c.save ? std::max(m, 1) : 1;
+  const int lh = c.save ? m + 1 : 1;
+  const int la = c.save ? std::max(m, 1) : 1;
+  size_t so = 0;
+  L.e_off = so;
+  so = al256(so + (size_t)le * E * D * c.se);
+  L.h_off = so;
+  so = al256(so + (size_t)lh * N * D * 4);
+  L.agg_off = so;
+  so = al256(so + (size_t)la * N * D * 4);
+  L.P_off = so;
+  so = al256(so + (size_t)la * N * 2 * D * 4);
+  L.act_stride = so;
+  L.act = o;
+  o = al256(o + so * c.ne_sets);
+  L.node_in = o;
+  o = al256(o + (size_t)c.max_stages * N * 8 * 4);
+  L.K = o;
+  o = al256(o + (size_t)c.max_stages * N * 4 * 4);
+  L.slots = o;
+  o = al256(o + (size_t)max_slots(E) * D * 4);
+  if (c.save) {
+    L.ebar = o;
+    o = al256(o + (size_t)E * D * 4);
+    L.zbar = o;
+    o = al256(o + (size_t)E * D * c.se);
+    L.hb_a = o;
+    o = al256(o + (size_t)N * D * 4);
+    L.hb_b = o;
+    o = al256(o + (size_t)N * D * 4);
+    L.aggbar = o;
+    o = al256(o + (size_t)N * D * 4);
+    L.R = o;
+    o = al256(o + (size_t)N * D * 4);
+    L.part = o;
+    o = al256(o + (size_t)kPartBlocks * kPartStride * 4);
+    L.kbar = o;
+    o = al256(o + (size_t)N * 4 * 4);
+    L.ystage = o;
+    o = al256(o + (size_t)c.max_stages * N * 4 * 4);
+    L.gin = o;
+    o = al256(o + (size_t)N * 8 * 4);
+  }
+  L.total = o;
+}
+
+inline hipStream_t S(void* s) { return (hipStream_t)s; }
+
+#define HIP_TRY(expr)                                                                 \
+  do {                                                                                \
+    hipError_t _e = (expr);                                                           \
+    if (_e != hipSuccess) return fail(MGN_ERR_DEVICE, "%s: %s", #expr, hipGetErrorString(_e)); \
+  } while (0)
+
+struct Run {
+  Ctx& c;
+  const mgn_dgraph& g;
+  const float* params;
+  char* ws;
+  hipStream_t s;
+  int64_t N, E;
+  int m;
+  int prec;
+  float eps;
+
+  char* pack() const { return ws + c.L.pack; }
+  size_t tsz() const { return prec == MGN_BF16 ? 2 : 4; }
+  const void* P(int64_t off) const { return pack() + (size_t)off * tsz(); }
+  char* set(int k) const { return ws + c.L.act + (size_t)k * c.L.act_stride; }
+  void* e_l(int k, int l) const { return set(k) + c.L.e_off + (c.save ? (size_t)l * E * D * c.se : 0); }
+  float* h_l(int k, int l) const {
+    return (float*)(set(k) + c.L.h_off) + (c.save ? (size_t)l * N * D : 0);
+  }
+  float* agg_l(int k, int l) const {
+    return (float*)(set(k) + c.L.agg_off) + (c.save ? (size_t)l * N * D : 0);
+  }
+  float* P_l(int k, int l) const {
+    return (float*)(set(k) + c.L.P_off) + (c.save ? (size_t)l * N * 2 * D : 0);
+  }
+  float* slots() const { return (float*)(ws + c.L.slots); }
+
+  MlpW W(const Off& o, const PackOff& p) const {
+    MlpW w;
+    w.W1 = p.W1 >= 0 ? P(p.W1) : nullptr;
+    w.W1t = p.W1t >= 0 ? P(p.W1t) : nullptr;
+    w.W2 = p.W2 >= 0 ? P(p.W2) : nullptr;
+    w.W2t = p.W2t >= 0 ? P(p.W2t) : nullptr;
+    w.W1f = params + o.W1;
+    w.W2f = params + o.W2;
+    w.b1 = params + o.b1;
+    w.b2 = params + o.b2;
+    w.gamma = o.g >= 0 ? params + o.g : nullptr;
+    w.beta = o.bt >= 0 ? params + o.bt : nullptr;
+    return w;
+  }
+  EdgeTiles tiles() const {
+    EdgeTiles t;
+    t.tiles = g.tiles;
+    t.n_tiles = g.n_tiles;
+    t.rowptr = g.rowptr;
+    t.senders = g.senders;
+    return t;
+  }
+  Partials part() const {
+    Partials p;
+    p.buf = (float*)(ws + c.L.part);
+    p.stride = kPartStride;
+    p.max_blocks = kPartBlocks;
+    return p;
+  }
+
+  int pack_weights() {
+    const Model& M = c.M;
+    for (size_t b = 0; b < M.ents.size(); b += kPackMax) {
+      PackList L;
+      L.n = (int32_t)std::min<size_t>(kPackMax, M.ents.size() - b);
+      for (int j = 0; j < L.n; ++j) L.e[j] = M.ents[b + j];
+      HIP_TRY(launch_pack(prec, params, pack(), L, s));
+    }
+    return MGN_OK;
+  }
+
+  int forward(const float* node_in, const float* efeat, float* out, int k) {
+    const Model& M = c.M;
+    const EdgeTiles tl = tiles();
+    MlpW e0;
+    if (m > 0) e0 = W(M.edge[0], M.p_edge[0]);
+    HIP_TRY(launch_node_enc(prec, N, node_in, W(M.enc_node, M.p_enc_node), m > 0 ? &e0 : nullptr, eps, h_l(k, 0),
+                            P_l(k, 0), s));
+    if (m > 0) HIP_TRY(launch_edge_enc(prec, E, efeat, W(M.enc_edge, M.p_enc_edge), eps, e_l(k, 0), s));
+    for (int l = 0; l < m; ++l) {
+      const bool last = l == m - 1;
+      void* e_out = c.save ? (last ? nullptr : e_l(k, l + 1)) : e_l(k, 0);
+      HIP_TRY(launch_edge_fwd(prec, tl, e_l(k, l), e_out, last ? 0 : 1, P_l(k, l), W(M.edge[l], M.p_edge[l]), eps,
+                              agg_l(k, l), slots(), s));
+      HIP_TRY(launch_slot_fixup(g.long_nodes, g.n_long, slots(), agg_l(k, l), s));
+      MlpW nx;
+      if (!last) nx = W(M.edge[l + 1], M.p_edge[l + 1]);
+      HIP_TRY(launch_node_fwd(prec, N, h_l(k, l), agg_l(k, l), W(M.node[l], M.p_node[l]), last ? nullptr : &nx, eps,
+                              h_l(k, l + 1), last ? nullptr : P_l(k, l + 1), s));
+    }
+    HIP_TRY(launch_decoder(prec, N, h_l(k, m), W(M.dec, M.p_dec), out, s));
+    return MGN_OK;
+  }
+
+  int reduce(int nb, int64_t src, int rows, int cols, float* grad, int64_t dst, int64_t ld) {
+    HIP_TRY(launch_reduce(part(), nb, src, rows, cols, grad, dst, ld, s));
+    return MGN_OK;
+  }
+
+  int backward(int k, const float* node_in, const float* efeat, const float* gout, float* grad, float* gin) {
+    const Model& M = c.M;
+    const EdgeTiles tl = tiles();
+    const Partials pt = part();
+    float* hb_cur = (float*)(ws + c.L.hb_a);
+    float* hb_part = (float*)(ws + c.L.hb_b);
+    float* aggbar = (float*)(ws + c.L.aggbar);
+    float* R = (float*)(ws + c.L.R);
+    float* ebar = (float*)(ws + c.L.ebar);
+    void* zbar = ws + c.L.zbar;
+    int nb = 0, rc;
+    HIP_TRY(launch_decoder_bwd(prec, N, h_l(k, m), gout, W(M.dec, M.p_dec), hb_cur, pt, &nb, s));
+    if ((rc = reduce(nb, 0, 1, (int)M.dec.size, grad, M.dec.W1, 0)) != MGN_OK) return rc;
+    for (int l = m - 1; l >= 0; --l) {
+      const Off& oe = M.edge[l];
+      const Off& on = M.node[l];
+      HIP_TRY(launch_node_bwd(prec, N, h_l(k, l), agg_l(k, l), hb_cur, W(on, M.p_node[l]), eps, hb_part, aggbar, pt,
+                              &nb, s));
+      if ((rc = reduce(nb, 0, 1, (int)on.size, grad, on.W1, 0)) != MGN_OK) return rc;
+      HIP_TRY(launch_edge_bwd(prec, tl, e_l(k, l), ebar, l < m - 1 ? 1 : 0, ebar, P_l(k, l), aggbar,
+                              W(oe, M.p_edge[l]), eps, zbar, R, slots(), pt, &nb, s));
+      if ((rc = reduce(nb, 0, D, D, grad, oe.W1, 3 * D)) != MGN_OK) return rc;
+      if ((rc = reduce(nb, 16384, 1, (int)(oe.size - 3 * D * D), grad, oe.b1, 0)) != MGN_OK) return rc;
+      HIP_TRY(launch_slot_fixup(g.long_nodes, g.n_long, slots(), R, s));
+      HIP_TRY(launch_node_srcsum(prec, N, g.rowptr, g.rev, zbar, R, h_l(k, l), hb_part, W(oe, M.p_edge[l]), hb_cur,
+                                 pt, &nb, s));
+      if ((rc = reduce(nb, 0, D, D, grad, oe.W1 + D, 3 * D)) != MGN_OK) return rc;
+      if ((rc = reduce(nb, 16384, D, D, grad, oe.W1 + 2 * D, 3 * D)) != MGN_OK) return rc;
+    }
+    if (m > 0) {
+      HIP_TRY(launch_edge_enc_bwd(prec, E, efeat, ebar, W(M.enc_edge, M.p_enc_edge), eps, pt, &nb, s));
+      if ((rc = reduce(nb, 0, 1, (int)M.enc_edge.size, grad, M.enc_edge.W1, 0)) != MGN_OK) return rc;
+    }
+    HIP_TRY(launch_node_enc_bwd(prec, N, node_in, hb_cur, W(M.enc_node, M.p_enc_node), eps, gin, pt, &nb, s));
+    if ((rc = reduce(nb, 0, 1, (int)M.enc_node.size, grad, M.enc_node.W1, 0)) != MGN_OK) return rc;
+    return MGN_OK;
+  }
+};
+
+int check_cfg(const mgn_config* cfg) {
+  if (!cfg) return fail(MGN_ERR_ARG, "null config");
+  if (cfg->node_in != 8 || cfg->edge_in != 4 || cfg->latent != D || cfg->out != 4 || cfg->mlp_layers != 2)
+    return fail(MGN_ERR_SHAPE,
+                "unsupported config (node_in 8, edge_in 4, latent 128, out 4, mlp_layers 2 are supported)");
+  if (cfg->mp_steps < 0 || cfg->mp_steps > 4096) return fail(MGN_ERR_ARG, "mp_steps out of range");
+  if (cfg->precision != MGN_FP32 && cfg->precision != MGN_BF16) return fail(MGN_ERR_ARG, "unknown precision");
+  if (!(cfg->ln_eps > 0.f)) return fail(MGN_ERR_ARG, "ln_eps must be > 0");
+  return MGN_OK;
+}
+
+int check_call(Ctx* c, const mgn_dgraph* g, const float* params, void* ws, size_t ws_bytes, int32_t save) {
+  if (!c || !g) return fail(MGN_ERR_ARG, "null ctx or graph");
+  if (g->n_nodes < 0 || g->n_edges < 0) return fail(MGN_ERR_ARG, "negative graph size");
+  if (g->n_nodes > c->maxN || g->n_edges > c->maxE)
+    return fail(MGN_ERR_SHAPE, "graph (%lld nodes, %lld edges) larger than the context (%lld, %lld)",
+                (long long)g->n_nodes, (long long)g->n_edges, (long long)c->maxN, (long long)c->maxE);
+  if (save && !c->save) return fail(MGN_ERR_STATE, "context was created without save");
+  if (ws_bytes < c->L.total)
+    return fail(MGN_ERR_WORKSPACE, "workspace %zu bytes < required %zu", ws_bytes, c->L.total);
+  if (g->n_nodes > 0) {
+    if (!params || !ws) return fail(MGN_ERR_ARG, "null params or workspace");
+    if (!g->rowptr || !g->tiles || g->n_tiles <= 0 || (g->n_edges > 0 && (!g->senders || !g->rev)))
+      return fail(MGN_ERR_ARG, "device graph arrays missing");
+    if (g->n_long > 0 && !g->long_nodes) return fail(MGN_ERR_ARG, "long_nodes missing");
+  }
+  return MGN_OK;
+}
+
+}  // namespace
+}  // namespace mgn
+
+struct mgn_ctx {
+  mgn::Ctx c;
+};
+
+using namespace mgn;
+
+extern "C" {
+
+const char* mgn_version(void) { return "mgn-gfx950 0.1.0"; }
+
+int mgn_scheme_stages(int32_t scheme) {
+  Tableau t;
+  if (!tableau(scheme, t)) return fail(MGN_ERR_ARG, "unknown scheme %d", scheme);
+  return t.s;
+}
+
+int64_t mgn_param_count(const mgn_config* cfg) {
+  if (check_cfg(cfg) != MGN_OK) return -1;
+  return make_model(cfg->mp_steps).total;
+}
+
+int mgn_ctx_create(const mgn_config* cfg, int64_t max_nodes, int64_t max_edges, int32_t max_stages, int32_t save,
+                   size_t* ws_bytes, mgn_ctx** out) {
+  int rc = check_cfg(cfg);
+  if (rc != MGN_OK) return rc;
+  if (!ws_bytes || !out) return fail(MGN_ERR_ARG, "mgn_ctx_create: null output pointer");
+  if (max_nodes < 0 || max_edges < 0 || max_stages < 1 || max_stages > 4)
+    return fail(MGN_ERR_ARG, "mgn_ctx_create: bad sizes or max_stages (1..4)");
+  if (max_nodes >= (int64_t)INT32_MAX || max_edges >= (int64_t)INT32_MAX)
+    return fail(MGN_ERR_SHAPE, "mgn_ctx_create: sizes must be < 2^31");
+  mgn_ctx* h = new (std::nothrow) mgn_ctx();
+  if (!h) return fail(MGN_ERR_NOMEM, "mgn_ctx_create: out of host memory");
+  Ctx& c = h->c;
+  c.cfg = *cfg;
+  c.maxN = max_nodes;
+  c.maxE = max_edges;
+  c.max_stages = max_stages;
+  c.save = save ? 1 : 0;
+  c.se = cfg->precision == MGN_BF16 ? 2 : 4;
+  c.ne_sets = c.save ? max_stages : 1;
+  try {
+    c.M = make_model(cfg->mp_steps);
+  } catch (const std::bad_alloc&) {
+    delete h;
+    return fail(MGN_ERR_NOMEM, "mgn_ctx_create: out of host memory");
+  }
+  plan(c);
+  *ws_bytes = c.L.total;
+  *out = h;
+  return MGN_OK;
+}
+
+void mgn_ctx_destroy(mgn_ctx* ctx) { delete ctx; }
+
+int mgn_forward(mgn_ctx* ctx, const mgn_dgraph* g, const float* params, const float* node_in, const float* efeat,
+                float* out, int32_t save, void* ws, size_t ws_bytes, void* stream) {
+  if (!ctx) return fail(MGN_ERR_ARG, "mgn_forward: null ctx");
+  int rc = check_call(&ctx->c, g, params, ws, ws_bytes, save);
+  if (rc != MGN_OK) return rc;
+  Ctx& c = ctx->c;
+  if (g->n_nodes > 0 && (!node_in || !out || (g->n_edges > 0 && !efeat)))
+    return fail(MGN_ERR_ARG, "mgn_forward: null input or output");
+  c.saved = 0;
+  Run r{c, *g, params, (char*)ws, S(stream), g->n_nodes, g->n_edges, c.cfg.mp_steps, c.cfg.precision, c.cfg.ln_eps};
+  if (g->n_nodes > 0) {
+    if ((rc = r.pack_weights()) != MGN_OK) return rc;
+    if ((rc = r.forward(node_in, efeat, out, 0)) != MGN_OK) return rc;
+  }
+  if (save) {
+    c.saved = 1;
+    c.stages = 1;
+    c.g = *g;
+    c.params = params;
+    c.efeat = efeat;
+    c.node_in = node_in;
+    c.ws = (char*)ws;
+  }
+  return MGN_OK;
+}
+
+int mgn_integrate_step(mgn_ctx* ctx, const mgn_dgraph* g, const float* params, int32_t scheme,
+                       const float* static_feat, const float* y, const float* efeat, float* y_next, int32_t save,
+                       void* ws, size_t ws_bytes, void* stream) {
+  if (!ctx) return fail(MGN_ERR_ARG, "mgn_integrate_step: null ctx");
+  Tableau tb;
+  if (!tableau(scheme, tb)) return fail(MGN_ERR_ARG, "mgn_integrate_step: unknown scheme %d", scheme);
+  int rc = check_call(&ctx->c, g, params, ws, ws_bytes, save);
+  if (rc != MGN_OK) return rc;
+  Ctx& c = ctx->c;
+  if (tb.s > c.max_stages)
+    return fail(MGN_ERR_ARG, "mgn_integrate_step: scheme needs %d stages, context plans %d", tb.s, c.max_stages);
+  if (g->n_nodes > 0 && (!static_feat || !y || !y_next || (g->n_edges > 0 && !efeat)))
+    return fail(MGN_ERR_ARG, "mgn_integrate_step: null input or output");
+  c.saved = 0;
+  const int64_t N = g->n_nodes;
+  char* w = (char*)ws;
+  Run r{c, *g, params, w, S(stream), N, g->n_edges, c.cfg.mp_steps, c.cfg.precision, c.cfg.ln_eps};
+  if (N > 0) {
+    if ((rc = r.pack_weights()) != MGN_OK) return rc;
+    float* node_in = (float*)(w + c.L.node_in);
+    float* K = (float*)(w + c.L.K);
+    for (int i = 0; i < tb.s; ++i) {
+      LinComb lc{};
+      lc.x[0] = y;
+      lc.ld[0] = 4;
+      lc.c[0] = 1.f;
+      lc.n = 1;
+      for (int j = 0; j < i; ++j)
+        if (tb.a[i][j] != 0.f) {
+          lc.x[lc.n] = K + (size_t)j * N * 4;
+          lc.ld[lc.n] = 4;
+          lc.c[lc.n] = tb.a[i][j];
+          ++lc.n;
+        }
+      float* ni = node_in + (size_t)i * N * 8;
+      HIP_TRY(launch_stage_input(N, static_feat, lc, ni, S(stream)));
+      if ((rc = r.forward(ni, efeat, K + (size_t)i * N * 4, save ? i : 0)) != MGN_OK) return rc;
+    }
+    LinComb lc{};
+    lc.x[0] = y;
+    lc.ld[0] = 4;
+    lc.c[0] = 1.f;
+    lc.n = 1;
+    for (int i = 0; i < tb.s; ++i)
+      if (tb.b[i] != 0.f) {
+        lc.x[lc.n] = K + (size_t)i * N * 4;
+        lc.ld[lc.n] = 4;
+        lc.c[lc.n] = tb.b[i];
+        ++lc.n;
+      }
+    HIP_TRY(launch_lincomb(N, lc, y_next, 4, 0, S(stream)));
+  }
+  if (save) {
+    c.saved = 2;
+    c.scheme = scheme;
+    c.stages = tb.s;
+    c.g = *g;
+    c.params = params;
+    c.efeat = efeat;
+    c.node_in = nullptr;
+    c.ws = w;
+  }
+  return MGN_OK;
+}
+
+int mgn_backward(mgn_ctx* ctx, const float* grad_out, float* grad_params, float* grad_in, void* stream) {
+  if (!ctx) return fail(MGN_ERR_ARG, "mgn_backward: null ctx");
+  Ctx& c = ctx->c;
+  if (!c.saved) return fail(MGN_ERR_STATE, "mgn_backward: no saved forward or integration step");
+  const int64_t N = c.g.n_nodes;
+  if (N == 0) return MGN_OK;
+  if (!grad_out || !grad_params) return fail(MGN_ERR_ARG, "mgn_backward: null gradient buffer");
+  Run r{c, c.g, c.params, c.ws, S(stream), N, c.g.n_edges, c.cfg.mp_steps, c.cfg.precision, c.cfg.ln_eps};
+  int rc;
+  if (c.saved == 1) return r.backward(0, c.node_in, c.efeat, grad_out, grad_params, grad_in);
+  Tableau tb;
+  tableau(c.scheme, tb);
+  char* w = c.ws;
+  float* node_in = (float*)(w + c.L.node_in);
+  float* kbar = (float*)(w + c.L.kbar);
+  float* ys = (float*)(w + c.L.ystage);
+  float* gin = (float*)(w + c.L.gin);
+  for (int i = tb.s - 1; i >= 0; --i) {
+    LinComb lc{};
+    lc.x[0] = grad_out;
+    lc.ld[0] = 4;
+    lc.c[0] = tb.b[i];
+    lc.n = 1;
+    for (int j = i + 1; j < tb.s; ++j)
+      if (tb.a[j][i] != 0.f) {
+        lc.x[lc.n] = ys + (size_t)j * N * 4;
+        lc.ld[lc.n] = 4;
+        lc.c[lc.n] = tb.a[j][i];
+        ++lc.n;
+      }
+    HIP_TRY(launch_lincomb(N, lc, kbar, 4, 0, S(stream)));
+    if ((rc = r.backward(i, node_in + (size_t)i * N * 8, c.efeat, kbar, grad_params, gin)) != MGN_OK) return rc;
+    LinComb cp{};
+    cp.x[0] = gin;
+    cp.ld[0] = 8;
+    cp.off[0] = 4;
+    cp.c[0] = 1.f;
+    cp.n = 1;
+    HIP_TRY(launch_lincomb(N, cp, ys + (size_t)i * N * 4, 4, 0, S(stream)));
+  }
+  if (grad_in) {
+    LinComb lc{};
+    lc.x[0] = grad_out;
+    lc.ld[0] = 4;
+    lc.c[0] = 1.f;
+    lc.n = 1;
+    for (int i = 0; i < tb.s; ++i) {
+      lc.x[lc.n] = ys + (size_t)i * N * 4;
+      lc.ld[lc.n] = 4;
+      lc.c[lc.n] = 1.f;
+      ++lc.n;
+    }
+    HIP_TRY(launch_lincomb(N, lc, grad_in, 4, 0, S(stream)));
+  }
+  return MGN_OK;
+}
+
+}  // extern "C"

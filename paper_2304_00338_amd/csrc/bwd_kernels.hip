@@ -1,0 +1,689 @@
+// Reverse-mode kernels of one MGN call on gfx950: decoder, node phase, edge
+// phase, sender-side sums and encoders.  Activations inside each MLP are
+// recomputed from the saved block inputs (edge latents, node latents,
+// aggregates and node products).  Weight gradients are accumulated per
+// persistent block in registers and written as per-block partials, which
+// k_reduce sums in block order: no atomics anywhere, so gradients are
+// bitwise reproducible.
+//
+// Sender-side sums use the reverse-edge index: the out-edges of node v are
+// the reverses of its in-edges, so sum_{e: s(e)=v} x_e is a gather over the
+// in-segment of v through rev[], in a fixed order.
+#include "dev_common.hpp"
+#include "launch.hpp"
+
+namespace mgn {
+namespace dev {
+
+// Column partial: sum over q groups, lane q == 0 holds the result.
+__device__ __forceinline__ void put_col(float* dst, float v, int q) {
+  v = sum_q(v);
+  if (q == 0) *dst = v;
+}
+
+// Write an [o: 16w + q*4 + r][cb*16 + i] accumulator block set.
+template <int NCB>
+__device__ __forceinline__ void put_w(float* base, int ld, const f32x4 (&acc)[NCB], int w8, int i, int q) {
+#pragma unroll
+  for (int cb = 0; cb < NCB; ++cb)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) base[(size_t)(w8 * 16 + q * 4 + r) * ld + cb * 16 + i] = acc[cb][r];
+}
+
+// ------------------------------------------------------------ decoder
+template <int PREC>
+__global__ void __launch_bounds__(NT) k_decoder_bwd(int64_t N, const float* __restrict__ h,
+                                                    const float* __restrict__ gout, MlpW w,
+                                                    float* __restrict__ hbar, Partials part) {
+  typedef Tr<PREC> P;
+  typedef typename P::T T;
+  constexpr int LDT = D + P::PAD;
+  __shared__ __align__(16) T sX[TM * LDT];
+  __shared__ __align__(16) T sG[TM * LDT];
+  __shared__ float sO[TM][4];
+  const int tid = threadIdx.x, w8 = tid >> 6, lane = tid & 63, i = lane & 15, q = lane >> 4;
+  const int n = w8 * 16 + i;
+  const float b1 = w.b1[n];
+  float w2c[4];
+#pragma unroll
+  for (int o = 0; o < 4; ++o) w2c[o] = w.W2f[o * D + n];
+  f32x4 dW1[8];
+#pragma unroll
+  for (int cb = 0; cb < 8; ++cb) dW1[cb] = zero4();
+  float db1 = 0.f, dW2[4] = {0.f, 0.f, 0.f, 0.f}, db2 = 0.f;
+  const int64_t ntiles = (N + TM - 1) / TM;
+  for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
+    const int64_t r0 = t * TM;
+    const int nr = (int)min((int64_t)TM, N - r0);
+    stage_rows(sX, LDT, h + (size_t)r0 * D, nr, tid);
+    if (tid < TM * 4) {
+      const int row = tid >> 2, o = tid & 3;
+      sO[row][o] = row < nr ? gout[(r0 + row) * 4 + o] : 0.f;
+    }
+    __syncthreads();
+    if (tid < 4)
+      for (int row = 0; row < nr; ++row) db2 += sO[row][tid];
+    f32x4 acc[NRB];
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb) acc[rb] = f32x4{b1, b1, b1, b1};
+    gemm_tile<PREC, D>(acc, sX, LDT, (const T*)w.W1, D, w8 * 16, 0, i, q);
+    f32x4 g[NRB];
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = rb * 16 + q * 4 + r;
+        const float a1 = fmaxf(acc[rb][r], 0.f);
+        float ab = 0.f;
+#pragma unroll
+        for (int o = 0; o < 4; ++o) {
+          const float go = sO[row][o];
+          dW2[o] += go * a1;
+          ab += go * w2c[o];
+        }
+        const float zb = acc[rb][r] > 0.f ? ab : 0.f;
+        db1 += zb;
+        g[rb][r] = zb;
+        sG[row * LDT + n] = P::cvt(zb);
+      }
+    gtx<PREC, 8>(dW1, g, sX, LDT, 0, i, q);
+    __syncthreads();
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb) acc[rb] = zero4();
+    gemm_tile<PREC, D>(acc, sG, LDT, (const T*)w.W1t, D, w8 * 16, 0, i, q);
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = rb * 16 + q * 4 + r;
+        if (row < nr) hbar[(size_t)(r0 + row) * D + n] = acc[rb][r];
+      }
+    __syncthreads();
+  }
+  float* base = part.buf + (size_t)blockIdx.x * part.stride;
+  put_w<8>(base, D, dW1, w8, i, q);
+  put_col(base + 16384 + n, db1, q);
+#pragma unroll
+  for (int o = 0; o < 4; ++o) put_col(base + 16512 + o * D + n, dW2[o], q);
+  if (tid < 4) base[17024 + tid] = db2;
+}
+
+// --------------------------------------------------------- node phase
+// Given hbar_in = dL/dh_out for h_out = h + LN(MLP([h, agg])):
+// hbar_part = hbar_in + dL/dh through the MLP, aggbar = dL/dagg.
+template <int PREC>
+__global__ void __launch_bounds__(NT) k_node_bwd(int64_t N, const float* __restrict__ h, const float* __restrict__ agg,
+                                                 const float* __restrict__ hbar_in, MlpW w, float eps,
+                                                 float* __restrict__ hbar_part, float* __restrict__ aggbar,
+                                                 Partials part) {
+  typedef Tr<PREC> P;
+  typedef typename P::T T;
+  constexpr int LDT = D + P::PAD;
+  constexpr int LDX = 2 * D + P::PAD;
+  __shared__ __align__(16) T sX[TM * LDX];
+  __shared__ __align__(16) T sA[TM * LDT];
+  __shared__ __align__(16) T sG[TM * LDT];
+  __shared__ float red[TM][NW], red2[TM][NW];
+  __shared__ float red2x[TM][NW][2];
+  const int tid = threadIdx.x, w8 = tid >> 6, lane = tid & 63, i = lane & 15, q = lane >> 4;
+  const int n = w8 * 16 + i;
+  const float b1 = w.b1[n], b2 = w.b2[n], gam = w.gamma[n];
+  f32x4 dW1[16], dW2[8];
+#pragma unroll
+  for (int cb = 0; cb < 16; ++cb) dW1[cb] = zero4();
+#pragma unroll
+  for (int cb = 0; cb < 8; ++cb) dW2[cb] = zero4();
+  float db1 = 0.f, db2 = 0.f, dg = 0.f, dbt = 0.f;
+  const int64_t ntiles = (N + TM - 1) / TM;
+  for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
+    const int64_t r0 = t * TM;
+    const int nr = (int)min((int64_t)TM, N - r0);
+    stage_rows(sX, LDX, h + (size_t)r0 * D, nr, tid);
+    stage_rows(sX + D, LDX, agg + (size_t)r0 * D, nr, tid);
+    __syncthreads();
+    f32x4 acc[NRB];
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb) acc[rb] = f32x4{b1, b1, b1, b1};
+    gemm_tile<PREC, 2 * D>(acc, sX, LDX, (const T*)w.W1, 2 * D, w8 * 16, 0, i, q);
+    uint32_t mask = 0;
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        if (acc[rb][r] > 0.f) mask |= 1u << (rb * 4 + r);
+        sA[(rb * 16 + q * 4 + r) * LDT + n] = P::cvt(fmaxf(acc[rb][r], 0.f));
+      }
+    __syncthreads();
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb) acc[rb] = f32x4{b2, b2, b2, b2};
+    gemm_tile<PREC, D>(acc, sA, LDT, (const T*)w.W2, D, w8 * 16, 0, i, q);
+    f32x4 mean[NRB], rstd[NRB], xh[NRB], yb[NRB];
+    ln_stats(acc, red, red2, eps, w8, i, q, mean, rstd);
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = rb * 16 + q * 4 + r;
+        xh[rb][r] = (acc[rb][r] - mean[rb][r]) * rstd[rb][r];
+        yb[rb][r] = row < nr ? hbar_in[(size_t)(r0 + row) * D + n] : 0.f;
+        dg += yb[rb][r] * xh[rb][r];
+        dbt += yb[rb][r];
+      }
+    f32x4 g[NRB];
+    ln_bwd(g, yb, xh, rstd, gam, red2x, w8, i, q);
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        db2 += g[rb][r];
+        sG[(rb * 16 + q * 4 + r) * LDT + n] = P::cvt(g[rb][r]);
+      }
+    gtx<PREC, 8>(dW2, g, sA, LDT, 0, i, q);
+    __syncthreads();
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb) acc[rb] = zero4();
+    gemm_tile<PREC, D>(acc, sG, LDT, (const T*)w.W2t, D, w8 * 16, 0, i, q);
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        g[rb][r] = (mask >> (rb * 4 + r)) & 1u ? acc[rb][r] : 0.f;
+        db1 += g[rb][r];
+      }
+    gtx<PREC, 16>(dW1, g, sX, LDX, 0, i, q);
+    __syncthreads();
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) sG[(rb * 16 + q * 4 + r) * LDT + n] = P::cvt(g[rb][r]);
+    __syncthreads();
+    f32x4 xa[NRB];
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb) acc[rb] = xa[rb] = zero4();
+    gemm_tile<PREC, D>(acc, sG, LDT, (const T*)w.W1t, D, w8 * 16, 0, i, q);
+    gemm_tile<PREC, D>(xa, sG, LDT, (const T*)w.W1t, D, D + w8 * 16, 0, i, q);
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = rb * 16 + q * 4 + r;
+        if (row < nr) {
+          hbar_part[(size_t)(r0 + row) * D + n] = yb[rb][r] + acc[rb][r];
+          aggbar[(size_t)(r0 + row) * D + n] = xa[rb][r];
+        }
+      }
+    __syncthreads();
+  }
+  float* base = part.buf + (size_t)blockIdx.x * part.stride;
+  put_w<16>(base, 2 * D, dW1, w8, i, q);
+  put_col(base + 32768 + n, db1, q);
+  put_w<8>(base + 32896, D, dW2, w8, i, q);
+  put_col(base + 49280 + n, db2, q);
+  put_col(base + 49408 + n, dg, q);
+  put_col(base + 49536 + n, dbt, q);
+}
+
+// --------------------------------------------------------- edge phase
+// Given ebar_in = dL/de_out (absent for the last block) and aggbar:
+// mbar = ebar_in + aggbar[receiver]; back through LN and the MLP to
+// zbar = dL/dz1 (written out for the sender sums, and summed per receiver
+// into R), ebar_out = ebar_in + W1e^T zbar.
+template <int PREC>
+__global__ void __launch_bounds__(NT) k_edge_bwd(EdgeTiles tl, const typename Tr<PREC>::T* __restrict__ e,
+                                                 const float* __restrict__ ebar_in, int have_ebar,
+                                                 float* __restrict__ ebar_out, const float* __restrict__ Pn,
+                                                 const float* __restrict__ aggbar, MlpW w, float eps,
+                                                 typename Tr<PREC>::T* __restrict__ zbar, float* __restrict__ R,
+                                                 float* __restrict__ slots, Partials part) {
+  typedef Tr<PREC> P;
+  typedef typename P::T T;
+  constexpr int LDT = D + P::PAD;
+  __shared__ __align__(16) T sE[TM * LDT];
+  __shared__ __align__(16) T sA1[TM * LDT];
+  __shared__ __align__(16) T sG[TM * LDT];
+  __shared__ float red[TM][NW], red2[TM][NW];
+  __shared__ float red2x[TM][NW][2];
+  __shared__ int sSend[TM], sRecv[TM];
+  const int tid = threadIdx.x, w8 = tid >> 6, lane = tid & 63, i = lane & 15, q = lane >> 4;
+  const int n = w8 * 16 + i;
+  const float b1 = w.b1[n], b2 = w.b2[n], gam = w.gamma[n];
+  f32x4 dW1[8], dW2[8];
+#pragma unroll
+  for (int cb = 0; cb < 8; ++cb) dW1[cb] = dW2[cb] = zero4();
+  float db1 = 0.f, db2 = 0.f, dg = 0.f, dbt = 0.f;
+
+  for (int64_t t = blockIdx.x; t < tl.n_tiles; t += gridDim.x) {
+    const int4 td = reinterpret_cast<const int4*>(tl.tiles)[t];
+    const int nb = td.x, eb = td.z, ne_ = td.w - td.z;
+    const bool full = td.y >= 0;
+    const int nv = full ? td.y - nb : 1;
+    stage_rows(sE, LDT, e + (size_t)eb * D, ne_, tid);
+    if (tid < ne_) sSend[tid] = tl.senders[eb + tid];
+    if (full) {
+      for (int j = tid; j < nv; j += NT) {
+        const int a = tl.rowptr[nb + j] - eb, b = tl.rowptr[nb + j + 1] - eb;
+        for (int u = a; u < b; ++u) sRecv[u] = nb + j;
+      }
+    } else if (tid < ne_) {
+      sRecv[tid] = nb;
+    }
+    __syncthreads();
+
+    f32x4 acc[NRB];
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = rb * 16 + q * 4 + r;
+        float z = 0.f;
+        if (row < ne_) {
+          z = b1 + Pn[(size_t)sSend[row] * (2 * D) + n];
+          z += Pn[(size_t)sRecv[row] * (2 * D) + D + n];
+        }
+        acc[rb][r] = z;
+      }
+    gemm_tile<PREC, D>(acc, sE, LDT, (const T*)w.W1, 3 * D, w8 * 16, 0, i, q);
+    uint32_t mask = 0;
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        if (acc[rb][r] > 0.f) mask |= 1u << (rb * 4 + r);
+        sA1[(rb * 16 + q * 4 + r) * LDT + n] = P::cvt(fmaxf(acc[rb][r], 0.f));
+      }
+    __syncthreads();
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb) acc[rb] = f32x4{b2, b2, b2, b2};
+    gemm_tile<PREC, D>(acc, sA1, LDT, (const T*)w.W2, D, w8 * 16, 0, i, q);
+    f32x4 mean[NRB], rstd[NRB], xh[NRB], mb[NRB], eb_in[NRB];
+    ln_stats(acc, red, red2, eps, w8, i, q, mean, rstd);
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = rb * 16 + q * 4 + r;
+        xh[rb][r] = (acc[rb][r] - mean[rb][r]) * rstd[rb][r];
+        float eo = 0.f, m = 0.f;
+        if (row < ne_) {
+          if (have_ebar) eo = ebar_in[(size_t)(eb + row) * D + n];
+          m = eo + aggbar[(size_t)sRecv[row] * D + n];
+        }
+        eb_in[rb][r] = eo;
+        mb[rb][r] = m;
+        dg += m * xh[rb][r];
+        dbt += m;
+      }
+    f32x4 g[NRB];
+    ln_bwd(g, mb, xh, rstd, gam, red2x, w8, i, q);
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        db2 += g[rb][r];
+        sG[(rb * 16 + q * 4 + r) * LDT + n] = P::cvt(g[rb][r]);
+      }
+    gtx<PREC, 8>(dW2, g, sA1, LDT, 0, i, q);
+    __syncthreads();
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb) acc[rb] = zero4();
+    gemm_tile<PREC, D>(acc, sG, LDT, (const T*)w.W2t, D, w8 * 16, 0, i, q);
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        g[rb][r] = (mask >> (rb * 4 + r)) & 1u ? acc[rb][r] : 0.f;
+        db1 += g[rb][r];
+      }
+    gtx<PREC, 8>(dW1, g, sE, LDT, 0, i, q);
+    __syncthreads();
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) sG[(rb * 16 + q * 4 + r) * LDT + n] = P::cvt(g[rb][r]);
+    __syncthreads();
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb) acc[rb] = eb_in[rb];
+    gemm_tile<PREC, D>(acc, sG, LDT, (const T*)w.W1t, D, w8 * 16, 0, i, q);
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = rb * 16 + q * 4 + r;
+        if (row < ne_) ebar_out[(size_t)(eb + row) * D + n] = acc[rb][r];
+      }
+    for (int idx = tid; idx < ne_ * (D / 8); idx += NT) {
+      const int row = idx >> 4, c = (idx & 15) * 8;
+      T* dst = zbar + (size_t)(eb + row) * D + c;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) dst[j] = sG[row * LDT + c + j];
+    }
+    {
+      const int c = tid & (D - 1), vg = tid >> 7;
+      if (full) {
+        for (int j = vg; j < nv; j += NT / D) {
+          const int a = tl.rowptr[nb + j] - eb, b = tl.rowptr[nb + j + 1] - eb;
+          float s = 0.f;
+          for (int u = a; u < b; ++u) s += tof(sG[u * LDT + c]);
+          R[(size_t)(nb + j) * D + c] = s;
+        }
+      } else if (vg == 0) {
+        float s = 0.f;
+        for (int u = 0; u < ne_; ++u) s += tof(sG[u * LDT + c]);
+        slots[(size_t)(-1 - td.y) * D + c] = s;
+      }
+    }
+    __syncthreads();
+  }
+  float* base = part.buf + (size_t)blockIdx.x * part.stride;
+  put_w<8>(base, D, dW1, w8, i, q);
+  put_col(base + 16384 + n, db1, q);
+  put_w<8>(base + 16512, D, dW2, w8, i, q);
+  put_col(base + 32896 + n, db2, q);
+  put_col(base + 33024 + n, dg, q);
+  put_col(base + 33152 + n, dbt, q);
+}
+
+// ------------------------------------------------- sender-side sums
+// S[v] = sum over in-edges e of v of zbar[rev[e]] (= sum over out-edges of v),
+// then hbar_out = hbar_part + W1s^T S + W1r^T R and the weight gradients of
+// the sender / receiver parts of the edge MLP's first layer.
+template <int PREC>
+__global__ void __launch_bounds__(NT) k_node_srcsum(int64_t N, const int32_t* __restrict__ rowptr,
+                                                    const int32_t* __restrict__ rev,
+                                                    const typename Tr<PREC>::T* __restrict__ zbar,
+                                                    const float* __restrict__ R, const float* __restrict__ h,
+                                                    const float* __restrict__ hbar_part, MlpW w,
+                                                    float* __restrict__ hbar_out, Partials part) {
+  typedef Tr<PREC> P;
+  typedef typename P::T T;
+  constexpr int LDT = D + P::PAD;
+  constexpr int LDX = 2 * D + P::PAD;
+  __shared__ __align__(16) T sSR[TM * LDX];
+  __shared__ __align__(16) T sH[TM * LDT];
+  const int tid = threadIdx.x, w8 = tid >> 6, lane = tid & 63, i = lane & 15, q = lane >> 4;
+  const int n = w8 * 16 + i;
+  f32x4 dWs[8], dWr[8];
+#pragma unroll
+  for (int cb = 0; cb < 8; ++cb) dWs[cb] = dWr[cb] = zero4();
+  const int64_t ntiles = (N + TM - 1) / TM;
+  for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
+    const int64_t r0 = t * TM;
+    const int nr = (int)min((int64_t)TM, N - r0);
+    {
+      const int c = tid & (D - 1), vg = tid >> 7;
+      for (int j = vg; j < TM; j += NT / D) {
+        float s = 0.f;
+        if (j < nr) {
+          const int v = (int)(r0 + j);
+          for (int e = rowptr[v]; e < rowptr[v + 1]; ++e) s += tof(zbar[(size_t)rev[e] * D + c]);
+        }
+        sSR[j * LDX + c] = P::cvt(s);
+      }
+    }
+    stage_rows(sSR + D, LDX, R + (size_t)r0 * D, nr, tid);
+    stage_rows(sH, LDT, h + (size_t)r0 * D, nr, tid);
+    __syncthreads();
+    f32x4 acc[NRB];
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = rb * 16 + q * 4 + r;
+        acc[rb][r] = row < nr ? hbar_part[(size_t)(r0 + row) * D + n] : 0.f;
+      }
+    gemm_tile<PREC, D>(acc, sSR, LDX, (const T*)w.W1t, D, D + w8 * 16, 0, i, q);
+    gemm_tile<PREC, D>(acc, sSR + D, LDX, (const T*)w.W1t, D, 2 * D + w8 * 16, 0, i, q);
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = rb * 16 + q * 4 + r;
+        if (row < nr) hbar_out[(size_t)(r0 + row) * D + n] = acc[rb][r];
+      }
+    f32x4 g[NRB];
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) g[rb][r] = tof(sSR[(rb * 16 + q * 4 + r) * LDX + n]);
+    gtx<PREC, 8>(dWs, g, sH, LDT, 0, i, q);
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) g[rb][r] = tof(sSR[(rb * 16 + q * 4 + r) * LDX + D + n]);
+    gtx<PREC, 8>(dWr, g, sH, LDT, 0, i, q);
+    __syncthreads();
+  }
+  float* base = part.buf + (size_t)blockIdx.x * part.stride;
+  put_w<8>(base, D, dWs, w8, i, q);
+  put_w<8>(base + 16384, D, dWr, w8, i, q);
+}
+
+// ------------------------------------------------------- encoders
+template <int PREC, int KIN>
+__global__ void __launch_bounds__(NT) k_enc_bwd(int64_t M, const float* __restrict__ x_in,
+                                                const float* __restrict__ ybar, MlpW w, float eps,
+                                                float* __restrict__ gin, Partials part) {
+  typedef Tr<PREC> P;
+  typedef typename P::T T;
+  constexpr int LDT = D + P::PAD;
+  constexpr int LDM = D + 4;
+  __shared__ float sX[TM][KIN];
+  __shared__ __align__(16) T sA[TM * LDT];
+  __shared__ __align__(16) T sG[TM * LDT];
+  __shared__ float sZ[KIN == 8 ? TM * LDM : 1];
+  __shared__ float red[TM][NW], red2[TM][NW];
+  __shared__ float red2x[TM][NW][2];
+  const int tid = threadIdx.x, w8 = tid >> 6, lane = tid & 63, i = lane & 15, q = lane >> 4;
+  const int n = w8 * 16 + i;
+  const float b1 = w.b1[n], b2 = w.b2[n], gam = w.gamma[n];
+  float w1[KIN];
+#pragma unroll
+  for (int k = 0; k < KIN; ++k) w1[k] = w.W1f[n * KIN + k];
+  f32x4 dW2[8];
+#pragma unroll
+  for (int cb = 0; cb < 8; ++cb) dW2[cb] = zero4();
+  float dW1[KIN];
+#pragma unroll
+  for (int k = 0; k < KIN; ++k) dW1[k] = 0.f;
+  float db1 = 0.f, db2 = 0.f, dg = 0.f, dbt = 0.f;
+  const int64_t ntiles = (M + TM - 1) / TM;
+  for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
+    const int64_t r0 = t * TM;
+    const int nr = (int)min((int64_t)TM, M - r0);
+    for (int idx = tid; idx < TM * KIN; idx += NT) {
+      const int row = idx / KIN, k = idx % KIN;
+      sX[row][k] = row < nr ? x_in[(r0 + row) * KIN + k] : 0.f;
+    }
+    __syncthreads();
+    uint32_t mask = 0;
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = rb * 16 + q * 4 + r;
+        float z = b1;
+#pragma unroll
+        for (int k = 0; k < KIN; ++k) z += w1[k] * sX[row][k];
+        if (z > 0.f) mask |= 1u << (rb * 4 + r);
+        sA[row * LDT + n] = P::cvt(fmaxf(z, 0.f));
+      }
+    __syncthreads();
+    f32x4 acc[NRB];
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb) acc[rb] = f32x4{b2, b2, b2, b2};
+    gemm_tile<PREC, D>(acc, sA, LDT, (const T*)w.W2, D, w8 * 16, 0, i, q);
+    f32x4 mean[NRB], rstd[NRB], xh[NRB], yb[NRB];
+    ln_stats(acc, red, red2, eps, w8, i, q, mean, rstd);
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = rb * 16 + q * 4 + r;
+        xh[rb][r] = (acc[rb][r] - mean[rb][r]) * rstd[rb][r];
+        yb[rb][r] = row < nr ? ybar[(size_t)(r0 + row) * D + n] : 0.f;
+        dg += yb[rb][r] * xh[rb][r];
+        dbt += yb[rb][r];
+      }
+    f32x4 g[NRB];
+    ln_bwd(g, yb, xh, rstd, gam, red2x, w8, i, q);
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        db2 += g[rb][r];
+        sG[(rb * 16 + q * 4 + r) * LDT + n] = P::cvt(g[rb][r]);
+      }
+    gtx<PREC, 8>(dW2, g, sA, LDT, 0, i, q);
+    __syncthreads();
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb) acc[rb] = zero4();
+    gemm_tile<PREC, D>(acc, sG, LDT, (const T*)w.W2t, D, w8 * 16, 0, i, q);
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = rb * 16 + q * 4 + r;
+        const float zb = (mask >> (rb * 4 + r)) & 1u ? acc[rb][r] : 0.f;
+        db1 += zb;
+#pragma unroll
+        for (int k = 0; k < KIN; ++k) dW1[k] += zb * sX[row][k];
+        if (KIN == 8) sZ[row * LDM + n] = zb;
+      }
+    if (KIN == 8 && gin) {
+      __syncthreads();
+      const int row = tid >> 3, k = tid & 7;
+      if (row < nr) {
+        float s = 0.f;
+        for (int c = 0; c < D; ++c) s += sZ[row * LDM + c] * w.W1f[c * KIN + k];
+        gin[(r0 + row) * KIN + k] = s;
+      }
+    }
+    __syncthreads();
+  }
+  float* base = part.buf + (size_t)blockIdx.x * part.stride;
+#pragma unroll
+  for (int k = 0; k < KIN; ++k) put_col(base + n * KIN + k, dW1[k], q);
+  const int o1 = D * KIN;
+  put_col(base + o1 + n, db1, q);
+  put_w<8>(base + o1 + D, D, dW2, w8, i, q);
+  put_col(base + o1 + D + D * D + n, db2, q);
+  put_col(base + o1 + 2 * D + D * D + n, dg, q);
+  put_col(base + o1 + 3 * D + D * D + n, dbt, q);
+}
+
+// ----------------------------------------------------------- reduce
+__global__ void __launch_bounds__(256) k_reduce(Partials part, int nblocks, int64_t src, int32_t rows, int32_t cols,
+                                                float* __restrict__ grad, int64_t dst, int64_t dst_ld) {
+  const int64_t total = (int64_t)rows * cols;
+  for (int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x; idx < total; idx += (int64_t)gridDim.x * 256) {
+    float s = 0.f;
+    for (int b = 0; b < nblocks; ++b) s += part.buf[(size_t)b * part.stride + src + idx];
+    const int64_t r = idx / cols, c = idx % cols;
+    grad[dst + r * dst_ld + c] += s;
+  }
+}
+
+}  // namespace dev
+
+// ============================================================ launchers
+using namespace dev;
+
+static constexpr int kBwdBlocks = 512;
+
+static int bwd_grid(int64_t n_tiles, const Partials& p) {
+  return grid_for(n_tiles, std::min(kBwdBlocks, p.max_blocks));
+}
+
+hipError_t launch_decoder_bwd(int prec, int64_t N, const float* h, const float* gout, const MlpW& w, float* hbar,
+                              const Partials& part, int* nblocks, hipStream_t s) {
+  const int g = bwd_grid((N + TM - 1) / TM, part);
+  *nblocks = g;
+  if (!g) return hipSuccess;
+  if (prec == MGN_BF16)
+    hipLaunchKernelGGL(k_decoder_bwd<MGN_BF16>, dim3(g), dim3(NT), 0, s, N, h, gout, w, hbar, part);
+  else
+    hipLaunchKernelGGL(k_decoder_bwd<MGN_FP32>, dim3(g), dim3(NT), 0, s, N, h, gout, w, hbar, part);
+  return hipGetLastError();
+}
+
+hipError_t launch_node_bwd(int prec, int64_t N, const float* h, const float* agg, const float* hbar_in,
+                           const MlpW& w, float eps, float* hbar_part, float* aggbar, const Partials& part,
+                           int* nblocks, hipStream_t s) {
+  const int g = bwd_grid((N + TM - 1) / TM, part);
+  *nblocks = g;
+  if (!g) return hipSuccess;
+  if (prec == MGN_BF16)
+    hipLaunchKernelGGL(k_node_bwd<MGN_BF16>, dim3(g), dim3(NT), 0, s, N, h, agg, hbar_in, w, eps, hbar_part, aggbar,
+                       part);
+  else
+    hipLaunchKernelGGL(k_node_bwd<MGN_FP32>, dim3(g), dim3(NT), 0, s, N, h, agg, hbar_in, w, eps, hbar_part, aggbar,
+                       part);
+  return hipGetLastError();
+}
+
+hipError_t launch_edge_bwd(int prec, const EdgeTiles& t, const void* e, const float* ebar_in, int have_ebar,
+                           float* ebar_out, const float* Pn, const float* aggbar, const MlpW& w, float eps,
+                           void* zbar, float* R, float* slots, const Partials& part, int* nblocks, hipStream_t s) {
+  const int g = bwd_grid(t.n_tiles, part);
+  *nblocks = g;
+  if (!g) return hipSuccess;
+  if (prec == MGN_BF16)
+    hipLaunchKernelGGL(k_edge_bwd<MGN_BF16>, dim3(g), dim3(NT), 0, s, t, (const bf16*)e, ebar_in, have_ebar,
+                       ebar_out, Pn, aggbar, w, eps, (bf16*)zbar, R, slots, part);
+  else
+    hipLaunchKernelGGL(k_edge_bwd<MGN_FP32>, dim3(g), dim3(NT), 0, s, t, (const float*)e, ebar_in, have_ebar,
+                       ebar_out, Pn, aggbar, w, eps, (float*)zbar, R, slots, part);
+  return hipGetLastError();
+}
+
+hipError_t launch_node_srcsum(int prec, int64_t N, const int32_t* rowptr, const int32_t* rev, const void* zbar,
+                              const float* R, const float* h, const float* hbar_part, const MlpW& w,
+                              float* hbar_out, const Partials& part, int* nblocks, hipStream_t s) {
+  const int g = bwd_grid((N + TM - 1) / TM, part);
+  *nblocks = g;
+  if (!g) return hipSuccess;
+  if (prec == MGN_BF16)
+    hipLaunchKernelGGL(k_node_srcsum<MGN_BF16>, dim3(g), dim3(NT), 0, s, N, rowptr, rev, (const bf16*)zbar, R, h,
+                       hbar_part, w, hbar_out, part);
+  else
+    hipLaunchKernelGGL(k_node_srcsum<MGN_FP32>, dim3(g), dim3(NT), 0, s, N, rowptr, rev, (const float*)zbar, R, h,
+                       hbar_part, w, hbar_out, part);
+  return hipGetLastError();
+}
+
+hipError_t launch_edge_enc_bwd(int prec, int64_t E, const float* efeat, const float* ebar, const MlpW& w,
+                               float eps, const Partials& part, int* nblocks, hipStream_t s) {
+  const int g = bwd_grid((E + TM - 1) / TM, part);
+  *nblocks = g;
+  if (!g) return hipSuccess;
+  if (prec == MGN_BF16)
+    hipLaunchKernelGGL((k_enc_bwd<MGN_BF16, 4>), dim3(g), dim3(NT), 0, s, E, efeat, ebar, w, eps, (float*)nullptr,
+                       part);
+  else
+    hipLaunchKernelGGL((k_enc_bwd<MGN_FP32, 4>), dim3(g), dim3(NT), 0, s, E, efeat, ebar, w, eps, (float*)nullptr,
+                       part);
+  return hipGetLastError();
+}
+
+hipError_t launch_node_enc_bwd(int prec, int64_t N, const float* node_in, const float* hbar, const MlpW& w,
+                               float eps, float* gin, const Partials& part, int* nblocks, hipStream_t s) {
+  const int g = bwd_grid((N + TM - 1) / TM, part);
+  *nblocks = g;
+  if (!g) return hipSuccess;
+  if (prec == MGN_BF16)
+    hipLaunchKernelGGL((k_enc_bwd<MGN_BF16, 8>), dim3(g), dim3(NT), 0, s, N, node_in, hbar, w, eps, gin, part);
+  else
+    hipLaunchKernelGGL((k_enc_bwd<MGN_FP32, 8>), dim3(g), dim3(NT), 0, s, N, node_in, hbar, w, eps, gin, part);
+  return hipGetLastError();
+}
+
+hipError_t launch_reduce(const Partials& part, int nblocks, int64_t src, int32_t rows, int32_t cols, float* grad,
+                         int64_t dst, int64_t dst_ld, hipStream_t s) {
+  if (nblocks <= 0 || rows <= 0 || cols <= 0) return hipSuccess;
+  const int64_t total = (int64_t)rows * cols;
+  const int g = (int)std::min<int64_t>((total + 255) / 256, 2048);
+  hipLaunchKernelGGL(k_reduce, dim3(g), dim3(256), 0, s, part, nblocks, src, rows, cols, grad, dst, dst_ld);
+  return hipGetLastError();
+}
+
+}  // namespace mgn

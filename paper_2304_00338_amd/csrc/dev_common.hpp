@@ -1,0 +1,280 @@
+// Device helpers shared by the gfx950 kernels: MFMA operand traits, tile
+// staging, row LayerNorm statistics and deterministic in-wave reductions.
+//
+// Every kernel works on tiles of TM = 64 rows (edges or nodes) with 512
+// threads = 8 wave64s.  Wave w owns output columns [16w, 16w+16) of every
+// 128-wide layer.  MFMA 16x16xK operand layout (lane l, i = l & 15,
+// q = l >> 4):
+//   A fragment: A[i][k0 + q*KQ + j]   (KQ = 1 for fp32, 8 for bf16)
+//   B fragment: B[k0 + q*KQ + j][i]
+//   C/D:        c[r] = C[q*4 + r][i]
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/mgn.h"
+
+namespace mgn {
+namespace dev {
+
+constexpr int D = 128;     // latent width
+constexpr int NT = 512;    // threads per block
+constexpr int NW = 8;      // waves per block
+constexpr int TM = 64;     // rows per tile
+constexpr int NRB = TM / 16;
+
+typedef __bf16 bf16;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+template <int PREC>
+struct Tr;
+
+template <>
+struct Tr<MGN_FP32> {
+  typedef float T;
+  typedef float Frag;
+  static constexpr int KS = 4;   // K per MFMA
+  static constexpr int PAD = 4;  // LDS row padding (elements)
+  static __device__ __forceinline__ f32x4 mma(Frag a, Frag b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+  }
+  // A[row0 + i][k0 + q] from a row-major LDS tile
+  static __device__ __forceinline__ Frag lda(const T* t, int ld, int row0, int k0, int i, int q) {
+    return t[(row0 + i) * ld + k0 + q];
+  }
+  // B[k][n] = W[n0 + n][k] from a row-major [n][k] matrix
+  static __device__ __forceinline__ Frag ldb(const T* W, int ldw, int n0, int k0, int i, int q) {
+    return W[(size_t)(n0 + i) * ldw + k0 + q];
+  }
+  static __device__ __forceinline__ T cvt(float x) { return x; }
+};
+
+template <>
+struct Tr<MGN_BF16> {
+  typedef bf16 T;
+  typedef bf16x8 Frag;
+  static constexpr int KS = 32;
+  static constexpr int PAD = 8;
+  static __device__ __forceinline__ f32x4 mma(Frag a, Frag b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+  }
+  static __device__ __forceinline__ Frag lda(const T* t, int ld, int row0, int k0, int i, int q) {
+    return *reinterpret_cast<const bf16x8*>(t + (row0 + i) * ld + k0 + q * 8);
+  }
+  static __device__ __forceinline__ Frag ldb(const T* W, int ldw, int n0, int k0, int i, int q) {
+    return *reinterpret_cast<const bf16x8*>(W + (size_t)(n0 + i) * ldw + k0 + q * 8);
+  }
+  static __device__ __forceinline__ T cvt(float x) { return (bf16)x; }
+};
+
+__device__ __forceinline__ float tof(float x) { return x; }
+__device__ __forceinline__ float tof(bf16 x) { return (float)x; }
+
+__device__ __forceinline__ f32x4 zero4() {
+  f32x4 z = {0.f, 0.f, 0.f, 0.f};
+  return z;
+}
+
+// acc[rb] += A[rb*16 .. +16][0..K) * B, B[k][n] = W[n0 + n][kofs + k].
+template <int PREC, int K>
+__device__ __forceinline__ void gemm_tile(f32x4 (&acc)[NRB], const typename Tr<PREC>::T* A, int lda,
+                                          const typename Tr<PREC>::T* W, int ldw, int n0, int kofs,
+                                          int i, int q) {
+  typedef Tr<PREC> P;
+#pragma unroll 4
+  for (int k0 = 0; k0 < K; k0 += P::KS) {
+    const typename P::Frag b = P::ldb(W, ldw, n0, kofs + k0, i, q);
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb) acc[rb] = P::mma(P::lda(A, lda, rb * 16, k0, i, q), b, acc[rb]);
+  }
+}
+
+// acc[cb] += sum over the tile's rows of G[row][o] * X[row][xcol0 + cb*16 + n]
+// where G arrives in C layout (g[rb][r] = G[rb*16 + q*4 + r][o = 16w + i]).
+// The MFMA's K dimension runs over tile rows; the row order inside K is a
+// fixed permutation applied to both operands.
+template <int PREC, int NCB>
+__device__ __forceinline__ void gtx(f32x4 (&acc)[NCB], const f32x4 (&g)[NRB],
+                                    const typename Tr<PREC>::T* X, int ldx, int xcol0, int i, int q);
+
+template <>
+__device__ __forceinline__ void gtx<MGN_FP32, 8>(f32x4 (&acc)[8], const f32x4 (&g)[NRB], const float* X,
+                                                 int ldx, int xcol0, int i, int q) {
+#pragma unroll
+  for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float a = g[rb][r];
+      const float* xr = X + (rb * 16 + q * 4 + r) * ldx + xcol0 + i;
+#pragma unroll
+      for (int cb = 0; cb < 8; ++cb) acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, xr[cb * 16], acc[cb], 0, 0, 0);
+    }
+}
+
+template <>
+__device__ __forceinline__ void gtx<MGN_FP32, 16>(f32x4 (&acc)[16], const f32x4 (&g)[NRB], const float* X,
+                                                  int ldx, int xcol0, int i, int q) {
+#pragma unroll
+  for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float a = g[rb][r];
+      const float* xr = X + (rb * 16 + q * 4 + r) * ldx + xcol0 + i;
+#pragma unroll
+      for (int cb = 0; cb < 16; ++cb)
+        acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, xr[cb * 16], acc[cb], 0, 0, 0);
+    }
+}
+
+template <int NCB>
+__device__ __forceinline__ void gtx_bf16(f32x4 (&acc)[NCB], const f32x4 (&g)[NRB], const bf16* X, int ldx,
+                                         int xcol0, int i, int q) {
+#pragma unroll
+  for (int t = 0; t < NRB / 2; ++t) {
+    bf16x8 a;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      a[j] = (bf16)g[2 * t][j];
+      a[4 + j] = (bf16)g[2 * t + 1][j];
+    }
+    const bf16* x0 = X + ((2 * t) * 16 + q * 4) * ldx + xcol0 + i;
+    const bf16* x1 = X + ((2 * t + 1) * 16 + q * 4) * ldx + xcol0 + i;
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) {
+      bf16x8 b;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        b[j] = x0[j * ldx + cb * 16];
+        b[4 + j] = x1[j * ldx + cb * 16];
+      }
+      acc[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc[cb], 0, 0, 0);
+    }
+  }
+}
+
+template <>
+__device__ __forceinline__ void gtx<MGN_BF16, 8>(f32x4 (&acc)[8], const f32x4 (&g)[NRB], const bf16* X,
+                                                 int ldx, int xcol0, int i, int q) {
+  gtx_bf16<8>(acc, g, X, ldx, xcol0, i, q);
+}
+template <>
+__device__ __forceinline__ void gtx<MGN_BF16, 16>(f32x4 (&acc)[16], const f32x4 (&g)[NRB], const bf16* X,
+                                                  int ldx, int xcol0, int i, int q) {
+  gtx_bf16<16>(acc, g, X, ldx, xcol0, i, q);
+}
+
+// Sum over the 16 lanes that share q (one row of a 16-column block), in a
+// fixed butterfly order.
+__device__ __forceinline__ float sum16(float s) {
+  s += __shfl_xor(s, 8, 16);
+  s += __shfl_xor(s, 4, 16);
+  s += __shfl_xor(s, 2, 16);
+  s += __shfl_xor(s, 1, 16);
+  return s;
+}
+
+// Sum over the four q groups (lanes i, i+16, i+32, i+48).
+__device__ __forceinline__ float sum_q(float s) {
+  s += __shfl_xor(s, 16, 64);
+  s += __shfl_xor(s, 32, 64);
+  return s;
+}
+
+// Per-row mean and 1/sqrt(var + eps) over the 128 columns held by the 8
+// waves (biased variance, two passes).  red/red2: LDS [TM][NW] scratch.
+// Contains two block barriers; every thread of the block must call it.
+__device__ __forceinline__ void ln_stats(const f32x4 (&v)[NRB], float (*red)[NW], float (*red2)[NW], float eps,
+                                         int w, int i, int q, f32x4 (&mean)[NRB], f32x4 (&rstd)[NRB]) {
+#pragma unroll
+  for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float s = sum16(v[rb][r]);
+      if (i == 0) red[rb * 16 + q * 4 + r][w] = s;
+    }
+  __syncthreads();
+#pragma unroll
+  for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float* p = red[rb * 16 + q * 4 + r];
+      float t = 0.f;
+#pragma unroll
+      for (int u = 0; u < NW; ++u) t += p[u];
+      mean[rb][r] = t * (1.0f / D);
+      const float d = v[rb][r] - mean[rb][r];
+      const float s = sum16(d * d);
+      if (i == 0) red2[rb * 16 + q * 4 + r][w] = s;
+    }
+  __syncthreads();
+#pragma unroll
+  for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float* p = red2[rb * 16 + q * 4 + r];
+      float t = 0.f;
+#pragma unroll
+      for (int u = 0; u < NW; ++u) t += p[u];
+      rstd[rb][r] = 1.0f / sqrtf(t * (1.0f / D) + eps);
+    }
+}
+
+// LayerNorm backward for one tile: given dy (C layout), xhat, rstd and this
+// lane's gain, returns dz = rstd * (dxh - mean(dxh) - xhat * mean(dxh*xhat))
+// with dxh = dy * gamma.  red2x: LDS [TM][NW][2].  One block barrier.
+__device__ __forceinline__ void ln_bwd(f32x4 (&dz)[NRB], const f32x4 (&dy)[NRB], const f32x4 (&xhat)[NRB],
+                                       const f32x4 (&rstd)[NRB], float gam, float (*red2x)[NW][2], int w,
+                                       int i, int q) {
+#pragma unroll
+  for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float dxh = dy[rb][r] * gam;
+      const float s1 = sum16(dxh);
+      const float s2 = sum16(dxh * xhat[rb][r]);
+      if (i == 0) {
+        red2x[rb * 16 + q * 4 + r][w][0] = s1;
+        red2x[rb * 16 + q * 4 + r][w][1] = s2;
+      }
+    }
+  __syncthreads();
+#pragma unroll
+  for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float(*p)[2] = red2x[rb * 16 + q * 4 + r];
+      float t1 = 0.f, t2 = 0.f;
+#pragma unroll
+      for (int u = 0; u < NW; ++u) {
+        t1 += p[u][0];
+        t2 += p[u][1];
+      }
+      const float m1 = t1 * (1.0f / D), m2 = t2 * (1.0f / D);
+      const float dxh = dy[rb][r] * gam;
+      dz[rb][r] = rstd[rb][r] * (dxh - m1 - xhat[rb][r] * m2);
+    }
+}
+
+// Copy rows [0, nrows) of a row-major global [.][128] array (element type S)
+// into an LDS tile of T with row stride ld, zero-filling rows nrows..TM-1.
+// Each thread moves 8 consecutive elements per step.
+template <typename T, typename S>
+__device__ __forceinline__ void stage_rows(T* lds, int ld, const S* src, int nrows, int tid) {
+  for (int idx = tid; idx < TM * (D / 8); idx += NT) {
+    const int row = idx >> 4, c = (idx & 15) * 8;
+    T* dst = lds + row * ld + c;
+    if (row < nrows) {
+      const S* s = src + (size_t)row * D + c;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) dst[j] = (T)tof(s[j]);
+    } else {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) dst[j] = (T)0.f;
+    }
+  }
+}
+
+}  // namespace dev
+}  // namespace mgn

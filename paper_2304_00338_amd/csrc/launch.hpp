@@ -1,0 +1,104 @@
+// Host-side launchers of the gfx950 kernels (internal to libmgn).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mgn {
+
+// Weights of one two-layer MLP as the kernels see them.  W1/W2 point into
+// the packed operand copy (precision of the MFMA operands), row-major
+// [out][in]; W1t/W2t are the transposed copies [in][out].  Biases and
+// LayerNorm parameters are the caller's float32 values.
+struct MlpW {
+  const void* W1;
+  const void* W1t;
+  const void* W2;
+  const void* W2t;
+  const float* W1f;  // float32 first-layer weights (encoders: K = 4 / 8 on VALU)
+  const float* W2f;  // float32 second-layer weights (decoder: 4 outputs on VALU)
+  const float* b1;
+  const float* b2;
+  const float* gamma;
+  const float* beta;
+};
+
+struct PackEnt {
+  int64_t src;   // float offset of the [rows][cols] matrix in params
+  int64_t dst;   // element offset of the copy in the pack
+  int64_t dstt;  // element offset of the transposed copy
+  int32_t rows, cols;
+};
+constexpr int kPackMax = 64;
+struct PackList {
+  PackEnt e[kPackMax];
+  int32_t n;
+};
+
+struct EdgeTiles {
+  const int32_t* tiles;  // [n_tiles][4]
+  int64_t n_tiles;
+  const int32_t* rowptr;
+  const int32_t* senders;
+};
+
+// Per-block partial buffers for deterministic weight-gradient reductions.
+struct Partials {
+  float* buf;
+  int64_t stride;  // floats per block
+  int32_t max_blocks;
+};
+
+// Persistent grid size: number of blocks the kernels are launched with for
+// a given number of tiles (also the number of partial rows to reduce).
+int grid_for(int64_t n_tiles, int max_blocks);
+
+hipError_t launch_pack(int prec, const float* params, void* pack, const PackList& L, hipStream_t s);
+
+hipError_t launch_node_enc(int prec, int64_t N, const float* node_in, const MlpW& w, const MlpW* next_edge,
+                           float eps, float* h_out, float* P_out, hipStream_t s);
+hipError_t launch_edge_enc(int prec, int64_t E, const float* efeat, const MlpW& w, float eps, void* e_out,
+                           hipStream_t s);
+hipError_t launch_edge_fwd(int prec, const EdgeTiles& t, const void* e_in, void* e_out, int write_e,
+                           const float* P, const MlpW& w, float eps, float* agg, float* slots, hipStream_t s);
+hipError_t launch_slot_fixup(const int32_t* long_nodes, int64_t n_long, const float* slots, float* dst,
+                             hipStream_t s);
+hipError_t launch_node_fwd(int prec, int64_t N, const float* h_in, const float* agg, const MlpW& w,
+                           const MlpW* next_edge, float eps, float* h_out, float* P_out, hipStream_t s);
+hipError_t launch_decoder(int prec, int64_t N, const float* h, const MlpW& w, float* out, hipStream_t s);
+
+hipError_t launch_decoder_bwd(int prec, int64_t N, const float* h, const float* gout, const MlpW& w,
+                              float* hbar, const Partials& part, int* nblocks, hipStream_t s);
+hipError_t launch_node_bwd(int prec, int64_t N, const float* h, const float* agg, const float* hbar_in,
+                           const MlpW& w, float eps, float* hbar_part, float* aggbar, const Partials& part,
+                           int* nblocks, hipStream_t s);
+hipError_t launch_edge_bwd(int prec, const EdgeTiles& t, const void* e, const float* ebar_in, int have_ebar,
+                           float* ebar_out, const float* P, const float* aggbar, const MlpW& w, float eps,
+                           void* zbar, float* R, float* slots, const Partials& part, int* nblocks,
+                           hipStream_t s);
+hipError_t launch_node_srcsum(int prec, int64_t N, const int32_t* rowptr, const int32_t* rev, const void* zbar,
+                              const float* R, const float* h, const float* hbar_part, const MlpW& w,
+                              float* hbar_out, const Partials& part, int* nblocks, hipStream_t s);
+hipError_t launch_edge_enc_bwd(int prec, int64_t E, const float* efeat, const float* ebar, const MlpW& w,
+                               float eps, const Partials& part, int* nblocks, hipStream_t s);
+hipError_t launch_node_enc_bwd(int prec, int64_t N, const float* node_in, const float* hbar, const MlpW& w,
+                               float eps, float* gin, const Partials& part, int* nblocks, hipStream_t s);
+
+// grad[dst + r*dst_ld + c] += sum_b part[b*stride + src + r*cols + c]
+hipError_t launch_reduce(const Partials& part, int nblocks, int64_t src, int32_t rows, int32_t cols,
+                         float* grad, int64_t dst, int64_t dst_ld, hipStream_t s);
+
+// out[v][c] = c0 * x0[v][c] + sum_j cj * xj[v][ldx_j*v + off_j + c], c < 4
+struct LinComb {
+  const float* x[6];
+  int32_t ld[6];
+  int32_t off[6];
+  float c[6];
+  int32_t n;
+};
+hipError_t launch_lincomb(int64_t N, const LinComb& lc, float* out, int32_t out_ld, int32_t out_off,
+                          hipStream_t s);
+// node_in[v] = [static[v][0..4), y-combination[v][0..4)]
+hipError_t launch_stage_input(int64_t N, const float* st, const LinComb& lc, float* node_in, hipStream_t s);
+
+}  // namespace mgn

@@ -1,0 +1,49 @@
+// Small node-state kernels of the explicit integrators (Sec. 2.1 update
+// rule, Sec. 2.3 / App. A Heun forms): stage inputs y + sum_j a_ij K_j and
+// the final combination y + sum_i b_i K_i, summed in ascending term order.
+#include "dev_common.hpp"
+#include "launch.hpp"
+
+namespace mgn {
+namespace dev {
+
+__global__ void __launch_bounds__(256) k_lincomb(int64_t N, LinComb lc, float* __restrict__ out, int32_t out_ld,
+                                                 int32_t out_off) {
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= N * 4) return;
+  const int64_t v = idx >> 2;
+  const int c = (int)(idx & 3);
+  float s = lc.c[0] * lc.x[0][v * lc.ld[0] + lc.off[0] + c];
+  for (int j = 1; j < lc.n; ++j) s += lc.c[j] * lc.x[j][v * lc.ld[j] + lc.off[j] + c];
+  out[v * out_ld + out_off + c] = s;
+}
+
+__global__ void __launch_bounds__(256) k_copy_static(int64_t N, const float* __restrict__ st, float* __restrict__ node_in) {
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= N * 4) return;
+  const int64_t v = idx >> 2;
+  const int c = (int)(idx & 3);
+  node_in[v * 8 + c] = st[v * 4 + c];
+}
+
+}  // namespace dev
+
+using namespace dev;
+
+hipError_t launch_lincomb(int64_t N, const LinComb& lc, float* out, int32_t out_ld, int32_t out_off, hipStream_t s) {
+  if (N <= 0) return hipSuccess;
+  const unsigned g = (unsigned)((N * 4 + 255) / 256);
+  hipLaunchKernelGGL(k_lincomb, dim3(g), dim3(256), 0, s, N, lc, out, out_ld, out_off);
+  return hipGetLastError();
+}
+
+hipError_t launch_stage_input(int64_t N, const float* st, const LinComb& lc, float* node_in, hipStream_t s) {
+  if (N <= 0) return hipSuccess;
+  const unsigned g = (unsigned)((N * 4 + 255) / 256);
+  hipLaunchKernelGGL(k_copy_static, dim3(g), dim3(256), 0, s, N, st, node_in);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return launch_lincomb(N, lc, node_in, 8, 4, s);
+}
+
+}  // namespace mgn

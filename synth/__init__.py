@@ -189,6 +189,25 @@ def xavier_params(mp_steps: int, seed: int, latent: int = LATENT,
     return np.concatenate(chunks).astype(np.float32)
 
 
+def smooth_params(mp_steps: int, seed: int, latent: int = LATENT,
+                  bias: float = 6.0, w1_scale: float = 0.05) -> np.ndarray:
+    """Like xavier_params(randomize_norm=True) but every first-layer weight is
+    scaled by ``w1_scale`` and every first-layer bias is ``bias``.  With the
+    defaults every ReLU input stays several units above its kink on the
+    synthetic meshes used here, so the network is smooth at this point and
+    its gradient is unique."""
+    flat = xavier_params(mp_steps, seed, latent, randomize_norm=True)
+    off = 0
+    for name, _, shape in param_shapes(mp_steps, latent):
+        n = int(np.prod(shape))
+        if name.endswith(".b1"):
+            flat[off:off + n] = bias
+        if name.endswith(".W1"):
+            flat[off:off + n] *= w1_scale
+        off += n
+    return flat.astype(np.float32)
+
+
 def loss_weights(n_nodes: int, seed: int, n_out: int = OUT) -> np.ndarray:
     """Fixed random weights w for the linear test loss sum(w * out). [N, 4]."""
     return _rng(seed + 3).standard_normal((n_nodes, n_out)).astype(np.float32)

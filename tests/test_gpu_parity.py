@@ -1,0 +1,224 @@
+"""GPU parity: the HIP path through the C ABI against the fp64 oracle on the
+same seeded inputs, element by element, at sizes that span several tiles
+with ragged tails; plus determinism, patch equivalence on the GPU, long
+in-segments, isolated nodes, empty graphs and device-side error paths."""
+import numpy as np
+import pytest
+
+import oracle as O
+from gpu_util import BF16_GRAD_TOL, BF16_TOL, FP32_TOL, Problem, kink_resolved, rel_l2, segments
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+from paper_2304_00338_amd import mgn  # noqa: E402
+
+
+def run_fwd_bwd(pb, prec, grad_in=True):
+    N, E = pb.g.n_nodes, pb.g.n_edges
+    ctx = mgn.Context(pb.m, N, E, prec, save=True)
+    out = mgn.mgn_forward(ctx, pb.dg, pb.d_params, pb.d_node_in, pb.dg.efeat, save=True)
+    gp = torch.zeros_like(pb.d_params)
+    gi = torch.zeros((N, 8), dtype=torch.float32, device="cuda") if grad_in else None
+    mgn.mgn_backward(ctx, pb.d_w, gp, gi)
+    torch.cuda.synchronize()
+    return out.cpu().numpy(), gp.cpu().numpy(), (gi.cpu().numpy() if grad_in else None)
+
+
+def oracle_fwd_bwd(pb, prec="bf16", gpu=None):
+    """Oracle output and gradients; for fp32 the gradient is the valid
+    subgradient nearest the GPU result (see kink_resolved)."""
+    out, tape = O.mgn_forward(pb.go, pb.params, pb.node_in, pb.go.efeat, pb.m, keep=True)
+    if prec == "fp32" and gpu is not None:
+        gp, gi, _ = kink_resolved(tape, pb.w, gpu[1], gpu[2])
+    else:
+        gp, gi = O.mgn_backward(tape, pb.w)
+    return out, gp, gi
+
+
+CASES = [((32, 32), 2), ((9, 8, 7), 3), ((5, 4, 3), 1), ((13, 11), 0), ((12, 12, 12), 6)]
+
+
+def check(out, gp, gi, ref, m, tol, gtol):
+    ro, rgp, rgi = ref
+    assert rel_l2(out, ro) < tol, rel_l2(out, ro)
+    for name, a, b in segments(m):
+        assert rel_l2(gp[a:b], rgp[a:b]) < gtol, (name, rel_l2(gp[a:b], rgp[a:b]))
+    assert rel_l2(gi, rgi) < gtol, rel_l2(gi, rgi)
+
+
+@pytest.mark.parametrize("shape,m", CASES)
+@pytest.mark.parametrize("prec", ["fp32", "bf16"])
+def test_forward_backward_parity(shape, m, prec):
+    pb = Problem(shape, m, seed=11).device()
+    res = run_fwd_bwd(pb, prec)
+    ref = oracle_fwd_bwd(pb, prec, res)
+    if prec == "fp32":
+        check(*res, ref, m, FP32_TOL, FP32_TOL)
+    else:
+        check(*res, ref, m, BF16_TOL, BF16_GRAD_TOL)
+
+
+@pytest.mark.parametrize("shape,m", [((32, 32), 2), ((12, 12, 12), 6)])
+@pytest.mark.parametrize("prec", ["fp32", "bf16"])
+def test_smooth_point_gradients(shape, m, prec):
+    """Every ReLU input far from its kink: the gradient is unique, so both
+    precisions are held to their output tolerance."""
+    pb = Problem(shape, m, seed=12, smooth=True).device()
+    res = run_fwd_bwd(pb, prec)
+    ro, tape = O.mgn_forward(pb.go, pb.params, pb.node_in, pb.go.efeat, m, keep=True)
+    assert O.relu_kinks(tape, 0.5) == []
+    rgp, rgi = O.mgn_backward(tape, pb.w)
+    tol = FP32_TOL if prec == "fp32" else BF16_TOL
+    check(*res, (ro, rgp, rgi), m, tol, tol)
+
+
+@pytest.mark.parametrize("prec", ["fp32", "bf16"])
+def test_bitwise_determinism(prec):
+    pb = Problem((10, 9, 8), 2, seed=5).device()
+    a = run_fwd_bwd(pb, prec)
+    b = run_fwd_bwd(pb, prec)
+    for x, y in zip(a, b):
+        assert np.array_equal(x.view(np.uint32), y.view(np.uint32))
+
+
+@pytest.mark.parametrize("prec", ["fp32", "bf16"])
+def test_patch_equivalence_on_gpu(prec):
+    """Condition 1 of Sec. 2.2 on the GPU: with k >= m the subdomain nodes of
+    every patch get bitwise the whole-mesh outputs."""
+    m, k = 2, 2
+    pb = Problem((8, 7, 12), m, seed=6).device()
+    ctx = mgn.Context(m, pb.g.n_nodes, pb.g.n_edges, prec)
+    whole = mgn.mgn_forward(ctx, pb.dg, pb.d_params, pb.d_node_in, pb.dg.efeat).cpu().numpy()
+    part = O.partition(pb.pos, (1, 2, 3)).astype(np.int32)
+    for p in range(6):
+        pt = mgn.extract_patch(pb.g, part, p, k)
+        mp = pt.patch_maps()
+        dpt = mgn.DeviceGraph(pt)
+        x = torch.from_numpy(pb.node_in[mp["node_l2g"]]).cuda()
+        o = mgn.mgn_forward(ctx, dpt, pb.d_params, x, dpt.efeat).cpu().numpy()
+        it = mp["interior"] == 1
+        assert np.array_equal(o[it].view(np.uint32), whole[mp["node_l2g"][it]].view(np.uint32))
+
+
+def fan_problem(k=300, m=2, seed=3):
+    ang = np.linspace(0, 2 * np.pi, k, endpoint=False)
+    rim = np.stack([np.cos(ang), np.sin(ang)], 1)
+    pos = np.concatenate([[[0.0, 0.0]], rim, 2 * rim]).astype(np.float32)
+    cells = [[0, 1 + j, 1 + (j + 1) % k] for j in range(k)]
+    cells += [[1 + j, 1 + k + j, 1 + (j + 1) % k] for j in range(k)]
+    cells = np.array(cells)
+    rng = np.random.default_rng(seed)
+    node_in = np.concatenate([np.eye(4)[rng.integers(0, 4, pos.shape[0])],
+                              rng.standard_normal((pos.shape[0], 4))], 1).astype(np.float32)
+    return Problem(None, m, seed=seed, cells=cells, pos=pos, node_in=node_in)
+
+
+@pytest.mark.parametrize("prec", ["fp32", "bf16"])
+def test_long_segment_hub(prec):
+    """Centre node with 300 in-edges: its sums span several chunk tiles."""
+    pb = fan_problem().device()
+    assert pb.dg.n_long == 1
+    out, gp, gi = run_fwd_bwd(pb, prec)
+    ro, rgp, rgi = oracle_fwd_bwd(pb, prec, (out, gp, gi))
+    tol = FP32_TOL if prec == "fp32" else BF16_TOL
+    gtol = FP32_TOL if prec == "fp32" else BF16_GRAD_TOL
+    assert rel_l2(out, ro) < tol
+    assert rel_l2(out[:1], ro[:1]) < tol
+    assert rel_l2(gp, rgp) < gtol
+    assert rel_l2(gi, rgi) < gtol
+
+
+def test_isolated_nodes_and_duplicates():
+    rng = np.random.default_rng(4)
+    n = 150
+    cells = rng.integers(0, n - 20, size=(200, 3))
+    cells = np.concatenate([cells, cells[:30]])
+    pos = rng.standard_normal((n, 3)).astype(np.float32)
+    node_in = np.concatenate([np.eye(4)[rng.integers(0, 4, n)], rng.standard_normal((n, 4))], 1)
+    pb = Problem(None, 2, seed=4, cells=cells, pos=pos, node_in=node_in).device()
+    out, gp, gi = run_fwd_bwd(pb, "fp32")
+    ro, rgp, rgi = oracle_fwd_bwd(pb, "fp32", (out, gp, gi))
+    assert rel_l2(out, ro) < FP32_TOL
+    assert rel_l2(gp, rgp) < FP32_TOL
+    assert rel_l2(gi, rgi) < FP32_TOL
+
+
+def test_empty_graph_is_noop():
+    pb = Problem((6, 6), 1, seed=0)
+    part = np.zeros(pb.g.n_nodes, np.int32)
+    part[:3] = 2
+    pt = mgn.extract_patch(pb.g, part, 1, 1)
+    dpt = mgn.DeviceGraph(pt)
+    ctx = mgn.Context(1, 10, 10, "fp32", save=True)
+    params = torch.from_numpy(pb.params).cuda()
+    x = torch.zeros((0, 8), dtype=torch.float32, device="cuda")
+    out = mgn.mgn_forward(ctx, dpt, params, x, dpt.efeat, save=True)
+    assert out.shape == (0, 4)
+    gp = torch.zeros_like(params)
+    mgn.mgn_backward(ctx, torch.zeros((0, 4), device="cuda"), gp)
+    assert float(gp.abs().sum()) == 0.0
+
+
+def test_device_error_paths():
+    pb = Problem((6, 5, 4), 1, seed=2).device()
+    small = mgn.Context(1, 10, 10, "fp32")
+    with pytest.raises(mgn.MgnError) as e:
+        mgn.mgn_forward(small, pb.dg, pb.d_params, pb.d_node_in, pb.dg.efeat)
+    assert e.value.code == mgn.ERR_SHAPE
+    ctx = mgn.Context(1, pb.g.n_nodes, pb.g.n_edges, "fp32")
+    ctx.ws_bytes -= 256
+    with pytest.raises(mgn.MgnError) as e:
+        mgn.mgn_forward(ctx, pb.dg, pb.d_params, pb.d_node_in, pb.dg.efeat)
+    assert e.value.code == mgn.ERR_WORKSPACE
+    ctx2 = mgn.Context(1, pb.g.n_nodes, pb.g.n_edges, "fp32")
+    with pytest.raises(mgn.MgnError) as e:
+        mgn.mgn_forward(ctx2, pb.dg, pb.d_params, pb.d_node_in, pb.dg.efeat, save=True)
+    assert e.value.code == mgn.ERR_STATE
+
+
+def run_integrate(pb, prec, scheme):
+    N, E = pb.g.n_nodes, pb.g.n_edges
+    ctx = mgn.Context(pb.m, N, E, prec, max_stages=4, save=True)
+    yn = mgn.mgn_integrate_step(ctx, pb.dg, pb.d_params, scheme, pb.d_onehot, pb.d_states,
+                                pb.dg.efeat, save=True)
+    gp = torch.zeros_like(pb.d_params)
+    gy = torch.zeros((N, 4), dtype=torch.float32, device="cuda")
+    mgn.mgn_backward(ctx, pb.d_w, gp, gy)
+    torch.cuda.synchronize()
+    return yn.cpu().numpy(), gp.cpu().numpy(), gy.cpu().numpy()
+
+
+@pytest.mark.parametrize("scheme", ["euler", "heun2", "midpoint", "heun3", "rk4"])
+@pytest.mark.parametrize("prec", ["fp32", "bf16"])
+def test_integrators(scheme, prec):
+    """Outputs at an ordinary point; gradients through all stages at a
+    smooth point (unique gradient)."""
+    tol = FP32_TOL if prec == "fp32" else BF16_TOL
+    pb = Problem((7, 6, 5), 2, seed=8).device()
+    yn, _, _ = run_integrate(pb, prec, scheme)
+    ryn = O.integrate_step(pb.go, pb.params, scheme, pb.onehot, pb.states, pb.go.efeat, pb.m)
+    # y_next = y + increment: compare the increment, which is what MGN computes
+    assert rel_l2(yn - pb.states, ryn - pb.states) < tol
+    ps = Problem((7, 6, 5), 2, seed=8, smooth=True).device()
+    yn, gp, gy = run_integrate(ps, prec, scheme)
+    ryn, tape = O.integrate_step(ps.go, ps.params, scheme, ps.onehot, ps.states, ps.go.efeat, ps.m,
+                                 keep=True)
+    rgp, rgy = O.integrate_backward(tape, ps.w)
+    assert rel_l2(yn - ps.states, ryn - ps.states) < tol
+    assert rel_l2(gp, rgp) < tol
+    assert rel_l2(gy, rgy) < tol
+
+
+def test_gradient_accumulates():
+    """grad_params is accumulated into, so patch gradients can be summed
+    (Sec. 2.2, condition 3)."""
+    pb = Problem((6, 6, 5), 1, seed=9).device()
+    ctx = mgn.Context(1, pb.g.n_nodes, pb.g.n_edges, "fp32", save=True)
+    mgn.mgn_forward(ctx, pb.dg, pb.d_params, pb.d_node_in, pb.dg.efeat, save=True)
+    g1 = torch.zeros_like(pb.d_params)
+    mgn.mgn_backward(ctx, pb.d_w, g1)
+    g2 = g1.clone()
+    mgn.mgn_backward(ctx, pb.d_w, g2)
+    torch.cuda.synchronize()
+    assert torch.equal(g2, g1 + g1)

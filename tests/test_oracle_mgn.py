@@ -360,3 +360,83 @@ def test_masked_mse_grad():
     tgt = np.zeros((2, 4))
     gr = O.masked_mse_grad(out, tgt, np.array([1, 0]))
     assert np.allclose(gr[0], 2 * out[0] / 4) and np.all(gr[1] == 0)
+
+
+def test_subgradient_flip_matches_autograd():
+    """oracle.mgn_backward(flips=...) takes the other one-sided derivative at
+    the listed ReLU inputs: compare with autograd on the dense brute force
+    where those units' derivative is changed without changing values."""
+    m = 1
+    M, g, P = small((4, 3), m, seed=13)
+    w = synth.loss_weights(g.n_nodes, 13).astype(np.float64)
+    _, tape = O.mgn_forward(g, P, M["node_in"], g.efeat, m, keep=True)
+    z1 = tape["blocks"][0][0][0][1]
+    # one inactive and one active unit of the edge MLP, one of the decoder
+    r0, u0 = np.argwhere(z1 < 0)[3]
+    r1, u1 = np.argwhere(z1 > 0)[5]
+    zd = tape["dec"][0][1]
+    r2, u2 = np.argwhere(zd > 0)[2]
+    flips = [("block0.edge", int(r0), int(u0)), ("block0.edge", int(r1), int(u1)),
+             ("dec", int(r2), int(u2))]
+    gp, gin = O.mgn_backward(tape, w, flips=flips)
+    assert O.relu_kinks(tape, 0.0) == []
+    assert len(O.relu_kinks(tape, np.inf)) > 0
+
+    F = torch.nn.functional
+    orig_relu = F.relu
+    calls = {"n": 0}
+
+    def relu_with_flips(z):
+        # call order in dense_mgn: enc_n, enc_e, block0.edge, block0.node, dec
+        k = calls["n"]
+        calls["n"] += 1
+        y = orig_relu(z)
+        sel = torch.zeros_like(z)
+        if k == 2:
+            sel[r0, u0] = 1.0
+            sel[r1, u1] = -1.0
+        if k == 4:
+            sel[r2, u2] = -1.0
+        return y + sel * (z - z.detach())
+
+    Pt = torch.tensor(P.astype(np.float64), requires_grad=True)
+    xt = torch.tensor(M["node_in"].astype(np.float64), requires_grad=True)
+    F.relu = relu_with_flips
+    try:
+        ref = dense_mgn(g, Pt, xt, torch.tensor(g.efeat.astype(np.float64)), m)
+    finally:
+        F.relu = orig_relu
+    (ref * torch.tensor(w)).sum().backward()
+    assert np.allclose(gp, Pt.grad.numpy(), rtol=1e-9, atol=1e-9)
+    assert np.allclose(gin, xt.grad.numpy(), rtol=1e-9, atol=1e-9)
+    g0, _ = O.mgn_backward(tape, w)
+    assert not np.allclose(g0, gp)
+
+
+def test_bf16_gradient_conditioning():
+    """Why bf16 gradients get a looser bound than bf16 outputs: even in fp64,
+    a 2^-9 relative perturbation of the weights (one bf16 rounding) moves
+    the gradient by several percent because ReLU inputs near their kink
+    switch branch, while the outputs move by well under 1%."""
+    m = 2
+    M, g, P = small((32, 32), m, seed=11)
+    w = synth.loss_weights(g.n_nodes, 11)
+    P = P.astype(np.float64)
+    o0, t0 = O.mgn_forward(g, P, M["node_in"], g.efeat, m, keep=True)
+    g0, _ = O.mgn_backward(t0, w)
+    P1 = P * (1 + np.random.default_rng(0).uniform(-2.0 ** -9, 2.0 ** -9, P.shape))
+    o1, t1 = O.mgn_forward(g, P1, M["node_in"], g.efeat, m, keep=True)
+    g1, _ = O.mgn_backward(t1, w)
+    rel = lambda a, b: np.linalg.norm(a - b) / np.linalg.norm(b)
+    assert rel(o1, o0) < 1e-2
+    assert rel(g1, g0) > 3e-2
+    # with every ReLU far from its kink the same perturbation moves the
+    # gradient by about as much as the outputs
+    S = synth.smooth_params(m, 11).astype(np.float64)
+    s0, ts0 = O.mgn_forward(g, S, M["node_in"], g.efeat, m, keep=True)
+    assert O.relu_kinks(ts0, 1e-2) == []
+    gs0, _ = O.mgn_backward(ts0, w)
+    S1 = S * (1 + np.random.default_rng(0).uniform(-2.0 ** -9, 2.0 ** -9, S.shape))
+    s1, ts1 = O.mgn_forward(g, S1, M["node_in"], g.efeat, m, keep=True)
+    gs1, _ = O.mgn_backward(ts1, w)
+    assert rel(gs1, gs0) < 2e-2
