@@ -225,6 +225,19 @@ int mgn_integrate_step(mgn_ctx* ctx, const mgn_dgraph* g, const float* params,
 /* Number of stages of a scheme (1, 2, 2, 3, 4), or MGN_ERR_ARG. */
 int mgn_scheme_stages(int32_t scheme);
 
+/* Per-kernel timing for benchmarks.  While enabled, every kernel launch of
+ * the context is bracketed by two HIP events recorded on the caller's stream.
+ * mgn_profile_collect waits for the last recorded event, then fills, for up
+ * to max_kernels kernel kinds, the kind's name (NUL-terminated, 32 bytes per
+ * entry in `names`), its summed duration in milliseconds and its launch
+ * count; *n_kernels receives the number of kinds.  Collecting resets the
+ * counters.  Events are created on first use and released by
+ * mgn_ctx_destroy.  Errors: ARG, DEVICE. */
+int mgn_profile_enable(mgn_ctx* ctx, int32_t enable);
+int mgn_profile_collect(mgn_ctx* ctx, int32_t max_kernels, char* names,
+                        double* total_ms, int64_t* launches,
+                        int32_t* n_kernels);
+
 /* Library version string and the last error message of this thread. */
 const char* mgn_version(void);
 const char* mgn_last_error(void);

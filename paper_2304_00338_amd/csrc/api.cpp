@@ -117,6 +117,21 @@ struct Layout {
 
 }  // namespace
 
+enum Kern {
+  K_PACK, K_NODE_ENC, K_EDGE_ENC, K_EDGE_FWD, K_FIXUP, K_NODE_FWD, K_DECODER, K_DECODER_BWD, K_NODE_BWD,
+  K_EDGE_BWD, K_SRCSUM, K_EDGE_ENC_BWD, K_NODE_ENC_BWD, K_REDUCE, K_LINCOMB, K_COUNT
+};
+const char* const kKernName[K_COUNT] = {
+    "pack", "node_enc", "edge_enc", "edge_fwd", "slot_fixup", "node_fwd", "decoder", "decoder_bwd", "node_bwd",
+    "edge_bwd", "node_srcsum", "edge_enc_bwd", "node_enc_bwd", "reduce", "lincomb"};
+
+struct Prof {
+  bool on = false;
+  std::vector<hipEvent_t> pool;
+  size_t used = 0;
+  std::vector<int> kind;  // per event pair
+};
+
 struct Ctx {
   mgn_config cfg;
   int64_t maxN = 0, maxE = 0;
@@ -133,6 +148,10 @@ struct Ctx {
   const float* efeat = nullptr;
   const float* node_in = nullptr;
   char* ws = nullptr;
+  Prof prof;
+  ~Ctx() {
+    for (hipEvent_t e : prof.pool) (void)hipEventDestroy(e);
+  }
 };
 
 namespace {
@@ -238,6 +257,13 @@ void plan(Ctx& c) {
 
 inline hipStream_t S(void* s) { return (hipStream_t)s; }
 
+#define LAUNCH(kind, expr)         \
+  do {                             \
+    HIP_TRY(mark_begin(kind));     \
+    HIP_TRY(expr);                 \
+    HIP_TRY(mark_end());           \
+  } while (0)
+
 #define HIP_TRY(expr)                                                                 \
   do {                                                                                \
     hipError_t _e = (expr);                                                           \
@@ -254,6 +280,25 @@ struct Run {
   int m;
   int prec;
   float eps;
+
+  // Bracket a launch with profiling events when enabled.
+  hipError_t mark_begin(int kind) {
+    Prof& p = c.prof;
+    if (!p.on) return hipSuccess;
+    while (p.pool.size() < p.used + 2) {
+      hipEvent_t e;
+      hipError_t r = hipEventCreate(&e);
+      if (r != hipSuccess) return r;
+      p.pool.push_back(e);
+    }
+    p.kind.push_back(kind);
+    return hipEventRecord(p.pool[p.used++], s);
+  }
+  hipError_t mark_end() {
+    Prof& p = c.prof;
+    if (!p.on) return hipSuccess;
+    return hipEventRecord(p.pool[p.used++], s);
+  }
 
   char* pack() const { return ws + c.L.pack; }
   size_t tsz() const { return prec == MGN_BF16 ? 2 : 4; }
@@ -307,7 +352,7 @@ struct Run {
       PackList L;
       L.n = (int32_t)std::min<size_t>(kPackMax, M.ents.size() - b);
       for (int j = 0; j < L.n; ++j) L.e[j] = M.ents[b + j];
-      HIP_TRY(launch_pack(prec, params, pack(), L, s));
+      LAUNCH(K_PACK, launch_pack(prec, params, pack(), L, s));
     }
     return MGN_OK;
   }
@@ -317,26 +362,26 @@ struct Run {
     const EdgeTiles tl = tiles();
     MlpW e0;
     if (m > 0) e0 = W(M.edge[0], M.p_edge[0]);
-    HIP_TRY(launch_node_enc(prec, N, node_in, W(M.enc_node, M.p_enc_node), m > 0 ? &e0 : nullptr, eps, h_l(k, 0),
+    LAUNCH(K_NODE_ENC, launch_node_enc(prec, N, node_in, W(M.enc_node, M.p_enc_node), m > 0 ? &e0 : nullptr, eps, h_l(k, 0),
                             P_l(k, 0), s));
-    if (m > 0) HIP_TRY(launch_edge_enc(prec, E, efeat, W(M.enc_edge, M.p_enc_edge), eps, e_l(k, 0), s));
+    if (m > 0) LAUNCH(K_EDGE_ENC, launch_edge_enc(prec, E, efeat, W(M.enc_edge, M.p_enc_edge), eps, e_l(k, 0), s));
     for (int l = 0; l < m; ++l) {
       const bool last = l == m - 1;
       void* e_out = c.save ? (last ? nullptr : e_l(k, l + 1)) : e_l(k, 0);
-      HIP_TRY(launch_edge_fwd(prec, tl, e_l(k, l), e_out, last ? 0 : 1, P_l(k, l), W(M.edge[l], M.p_edge[l]), eps,
+      LAUNCH(K_EDGE_FWD, launch_edge_fwd(prec, tl, e_l(k, l), e_out, last ? 0 : 1, P_l(k, l), W(M.edge[l], M.p_edge[l]), eps,
                               agg_l(k, l), slots(), s));
-      HIP_TRY(launch_slot_fixup(g.long_nodes, g.n_long, slots(), agg_l(k, l), s));
+      if (g.n_long > 0) LAUNCH(K_FIXUP, launch_slot_fixup(g.long_nodes, g.n_long, slots(), agg_l(k, l), s));
       MlpW nx;
       if (!last) nx = W(M.edge[l + 1], M.p_edge[l + 1]);
-      HIP_TRY(launch_node_fwd(prec, N, h_l(k, l), agg_l(k, l), W(M.node[l], M.p_node[l]), last ? nullptr : &nx, eps,
+      LAUNCH(K_NODE_FWD, launch_node_fwd(prec, N, h_l(k, l), agg_l(k, l), W(M.node[l], M.p_node[l]), last ? nullptr : &nx, eps,
                               h_l(k, l + 1), last ? nullptr : P_l(k, l + 1), s));
     }
-    HIP_TRY(launch_decoder(prec, N, h_l(k, m), W(M.dec, M.p_dec), out, s));
+    LAUNCH(K_DECODER, launch_decoder(prec, N, h_l(k, m), W(M.dec, M.p_dec), out, s));
     return MGN_OK;
   }
 
   int reduce(int nb, int64_t src, int rows, int cols, float* grad, int64_t dst, int64_t ld) {
-    HIP_TRY(launch_reduce(part(), nb, src, rows, cols, grad, dst, ld, s));
+    LAUNCH(K_REDUCE, launch_reduce(part(), nb, src, rows, cols, grad, dst, ld, s));
     return MGN_OK;
   }
 
@@ -351,29 +396,29 @@ struct Run {
     float* ebar = (float*)(ws + c.L.ebar);
     void* zbar = ws + c.L.zbar;
     int nb = 0, rc;
-    HIP_TRY(launch_decoder_bwd(prec, N, h_l(k, m), gout, W(M.dec, M.p_dec), hb_cur, pt, &nb, s));
+    LAUNCH(K_DECODER_BWD, launch_decoder_bwd(prec, N, h_l(k, m), gout, W(M.dec, M.p_dec), hb_cur, pt, &nb, s));
     if ((rc = reduce(nb, 0, 1, (int)M.dec.size, grad, M.dec.W1, 0)) != MGN_OK) return rc;
     for (int l = m - 1; l >= 0; --l) {
       const Off& oe = M.edge[l];
       const Off& on = M.node[l];
-      HIP_TRY(launch_node_bwd(prec, N, h_l(k, l), agg_l(k, l), hb_cur, W(on, M.p_node[l]), eps, hb_part, aggbar, pt,
+      LAUNCH(K_NODE_BWD, launch_node_bwd(prec, N, h_l(k, l), agg_l(k, l), hb_cur, W(on, M.p_node[l]), eps, hb_part, aggbar, pt,
                               &nb, s));
       if ((rc = reduce(nb, 0, 1, (int)on.size, grad, on.W1, 0)) != MGN_OK) return rc;
-      HIP_TRY(launch_edge_bwd(prec, tl, e_l(k, l), ebar, l < m - 1 ? 1 : 0, ebar, P_l(k, l), aggbar,
+      LAUNCH(K_EDGE_BWD, launch_edge_bwd(prec, tl, e_l(k, l), ebar, l < m - 1 ? 1 : 0, ebar, P_l(k, l), aggbar,
                               W(oe, M.p_edge[l]), eps, zbar, R, slots(), pt, &nb, s));
       if ((rc = reduce(nb, 0, D, D, grad, oe.W1, 3 * D)) != MGN_OK) return rc;
       if ((rc = reduce(nb, 16384, 1, (int)(oe.size - 3 * D * D), grad, oe.b1, 0)) != MGN_OK) return rc;
-      HIP_TRY(launch_slot_fixup(g.long_nodes, g.n_long, slots(), R, s));
-      HIP_TRY(launch_node_srcsum(prec, N, g.rowptr, g.rev, zbar, R, h_l(k, l), hb_part, W(oe, M.p_edge[l]), hb_cur,
+      if (g.n_long > 0) LAUNCH(K_FIXUP, launch_slot_fixup(g.long_nodes, g.n_long, slots(), R, s));
+      LAUNCH(K_SRCSUM, launch_node_srcsum(prec, N, g.rowptr, g.rev, zbar, R, h_l(k, l), hb_part, W(oe, M.p_edge[l]), hb_cur,
                                  pt, &nb, s));
       if ((rc = reduce(nb, 0, D, D, grad, oe.W1 + D, 3 * D)) != MGN_OK) return rc;
       if ((rc = reduce(nb, 16384, D, D, grad, oe.W1 + 2 * D, 3 * D)) != MGN_OK) return rc;
     }
     if (m > 0) {
-      HIP_TRY(launch_edge_enc_bwd(prec, E, efeat, ebar, W(M.enc_edge, M.p_enc_edge), eps, pt, &nb, s));
+      LAUNCH(K_EDGE_ENC_BWD, launch_edge_enc_bwd(prec, E, efeat, ebar, W(M.enc_edge, M.p_enc_edge), eps, pt, &nb, s));
       if ((rc = reduce(nb, 0, 1, (int)M.enc_edge.size, grad, M.enc_edge.W1, 0)) != MGN_OK) return rc;
     }
-    HIP_TRY(launch_node_enc_bwd(prec, N, node_in, hb_cur, W(M.enc_node, M.p_enc_node), eps, gin, pt, &nb, s));
+    LAUNCH(K_NODE_ENC_BWD, launch_node_enc_bwd(prec, N, node_in, hb_cur, W(M.enc_node, M.p_enc_node), eps, gin, pt, &nb, s));
     if ((rc = reduce(nb, 0, 1, (int)M.enc_node.size, grad, M.enc_node.W1, 0)) != MGN_OK) return rc;
     return MGN_OK;
   }
@@ -464,6 +509,43 @@ int mgn_ctx_create(const mgn_config* cfg, int64_t max_nodes, int64_t max_edges, 
 }
 
 void mgn_ctx_destroy(mgn_ctx* ctx) { delete ctx; }
+
+int mgn_profile_enable(mgn_ctx* ctx, int32_t enable) {
+  if (!ctx) return fail(MGN_ERR_ARG, "mgn_profile_enable: null ctx");
+  ctx->c.prof.on = enable != 0;
+  return MGN_OK;
+}
+
+int mgn_profile_collect(mgn_ctx* ctx, int32_t max_kernels, char* names, double* total_ms, int64_t* launches,
+                        int32_t* n_kernels) {
+  if (!ctx || !n_kernels || max_kernels < 0 || (max_kernels > 0 && (!names || !total_ms || !launches)))
+    return fail(MGN_ERR_ARG, "mgn_profile_collect: bad arguments");
+  Prof& p = ctx->c.prof;
+  double ms[K_COUNT] = {0};
+  int64_t cnt[K_COUNT] = {0};
+  if (p.used > 0) HIP_TRY(hipEventSynchronize(p.pool[p.used - 1]));
+  for (size_t k = 0; k < p.kind.size(); ++k) {
+    float t = 0.f;
+    HIP_TRY(hipEventElapsedTime(&t, p.pool[2 * k], p.pool[2 * k + 1]));
+    ms[p.kind[k]] += t;
+    cnt[p.kind[k]] += 1;
+  }
+  p.used = 0;
+  p.kind.clear();
+  int32_t n = 0;
+  for (int k = 0; k < K_COUNT; ++k) {
+    if (!cnt[k]) continue;
+    if (n < max_kernels) {
+      std::strncpy(names + 32 * n, kKernName[k], 31);
+      names[32 * n + 31] = 0;
+      total_ms[n] = ms[k];
+      launches[n] = cnt[k];
+    }
+    ++n;
+  }
+  *n_kernels = n;
+  return MGN_OK;
+}
 
 int mgn_forward(mgn_ctx* ctx, const mgn_dgraph* g, const float* params, const float* node_in, const float* efeat,
                 float* out, int32_t save, void* ws, size_t ws_bytes, void* stream) {

@@ -48,7 +48,8 @@ EXPORTS = [
     "mgn_graph_schedule", "mgn_tile_edges", "mgn_tile_nodes", "mgn_graph_destroy",
     "mgn_partition", "mgn_extract_patch", "mgn_patch_copy_maps", "mgn_ctx_create",
     "mgn_ctx_destroy", "mgn_forward", "mgn_backward", "mgn_integrate_step",
-    "mgn_scheme_stages", "mgn_version", "mgn_last_error",
+    "mgn_scheme_stages", "mgn_version", "mgn_last_error", "mgn_profile_enable",
+    "mgn_profile_collect",
 ]
 
 
@@ -81,6 +82,8 @@ def lib():
         "mgn_scheme_stages": (C.c_int, [i32]),
         "mgn_version": (C.c_char_p, []),
         "mgn_last_error": (C.c_char_p, []),
+        "mgn_profile_enable": (C.c_int, [vp, i32]),
+        "mgn_profile_collect": (C.c_int, [vp, i32, vp, vp, vp, P(i32)]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -313,6 +316,25 @@ def mgn_integrate_step(ctx: Context, g: DeviceGraph, params, scheme, static, y, 
                                     _dptr(y_next, torch.float32, (N, 4), "y_next"), 1 if save else 0,
                                     _dptr(ctx.ws, name="workspace"), ctx.ws_bytes, _stream(stream)))
     return y_next
+
+
+def mgn_profile_enable(ctx: Context, enable=True):
+    _check(lib().mgn_profile_enable(ctx._h, 1 if enable else 0))
+
+
+def mgn_profile_collect(ctx: Context, max_kernels=32):
+    """{kernel kind: (total_ms, launches)} since the last collect."""
+    names = C.create_string_buffer(32 * max_kernels)
+    ms = np.zeros(max_kernels, np.float64)
+    cnt = np.zeros(max_kernels, np.int64)
+    n = C.c_int32()
+    _check(lib().mgn_profile_collect(ctx._h, max_kernels, names, ms.ctypes.data, cnt.ctypes.data,
+                                     C.byref(n)))
+    out = {}
+    for k in range(min(n.value, max_kernels)):
+        nm = names.raw[32 * k:32 * k + 32].split(b"\0")[0].decode()
+        out[nm] = (float(ms[k]), int(cnt[k]))
+    return out
 
 
 def scheme_stages(scheme):
