@@ -170,6 +170,7 @@ typedef struct mgn_dgraph {
   int64_t n_edges;
   const int32_t* rowptr;     /* [N+1] */
   const int32_t* senders;    /* [E] */
+  const int32_t* receivers;  /* [E] */
   const int32_t* rev;        /* [E] */
   const int32_t* tiles;      /* [n_tiles][4] from mgn_graph_schedule */
   int64_t n_tiles;

@@ -119,11 +119,11 @@ struct Layout {
 
 enum Kern {
   K_PACK, K_NODE_ENC, K_EDGE_ENC, K_EDGE_FWD, K_FIXUP, K_NODE_FWD, K_DECODER, K_DECODER_BWD, K_NODE_BWD,
-  K_EDGE_BWD, K_SRCSUM, K_EDGE_ENC_BWD, K_NODE_ENC_BWD, K_REDUCE, K_LINCOMB, K_COUNT
+  K_EDGE_BWD, K_SRCSUM, K_EDGE_ENC_BWD, K_NODE_ENC_BWD, K_REDUCE, K_LINCOMB, K_WGRAD, K_COUNT
 };
 const char* const kKernName[K_COUNT] = {
     "pack", "node_enc", "edge_enc", "edge_fwd", "slot_fixup", "node_fwd", "decoder", "decoder_bwd", "node_bwd",
-    "edge_bwd", "node_srcsum", "edge_enc_bwd", "node_enc_bwd", "reduce", "lincomb"};
+    "edge_bwd", "node_srcsum", "edge_enc_bwd", "node_enc_bwd", "reduce", "lincomb", "wgrad"};
 
 struct Prof {
   bool on = false;
@@ -220,7 +220,7 @@ void plan(Ctx& c) {
   L.agg_off = so;
   so = al256(so + (size_t)la * N * D * 4);
   L.P_off = so;
-  so = al256(so + (size_t)la * N * 2 * D * 4);
+  so = al256(so + (size_t)la * N * 2 * D * tsz);
   L.act_stride = so;
   L.act = o;
   o = al256(o + so * c.ne_sets);
@@ -311,8 +311,8 @@ struct Run {
   float* agg_l(int k, int l) const {
     return (float*)(set(k) + c.L.agg_off) + (c.save ? (size_t)l * N * D : 0);
   }
-  float* P_l(int k, int l) const {
-    return (float*)(set(k) + c.L.P_off) + (c.save ? (size_t)l * N * 2 * D : 0);
+  void* P_l(int k, int l) const {
+    return set(k) + c.L.P_off + (c.save ? (size_t)l * N * 2 * D * tsz() : 0);
   }
   float* slots() const { return (float*)(ws + c.L.slots); }
 
@@ -336,6 +336,7 @@ struct Run {
     t.n_tiles = g.n_tiles;
     t.rowptr = g.rowptr;
     t.senders = g.senders;
+    t.receivers = g.receivers;
     return t;
   }
   Partials part() const {
@@ -406,8 +407,9 @@ struct Run {
       if ((rc = reduce(nb, 0, 1, (int)on.size, grad, on.W1, 0)) != MGN_OK) return rc;
       LAUNCH(K_EDGE_BWD, launch_edge_bwd(prec, tl, e_l(k, l), ebar, l < m - 1 ? 1 : 0, ebar, P_l(k, l), aggbar,
                               W(oe, M.p_edge[l]), eps, zbar, R, slots(), pt, &nb, s));
-      if ((rc = reduce(nb, 0, D, D, grad, oe.W1, 3 * D)) != MGN_OK) return rc;
       if ((rc = reduce(nb, 16384, 1, (int)(oe.size - 3 * D * D), grad, oe.b1, 0)) != MGN_OK) return rc;
+      LAUNCH(K_WGRAD, launch_wgrad(prec, E, zbar, e_l(k, l), pt, &nb, s));
+      if ((rc = reduce(nb, 0, D, D, grad, oe.W1, 3 * D)) != MGN_OK) return rc;
       if (g.n_long > 0) LAUNCH(K_FIXUP, launch_slot_fixup(g.long_nodes, g.n_long, slots(), R, s));
       LAUNCH(K_SRCSUM, launch_node_srcsum(prec, N, g.rowptr, g.rev, zbar, R, h_l(k, l), hb_part, W(oe, M.p_edge[l]), hb_cur,
                                  pt, &nb, s));
@@ -446,7 +448,8 @@ int check_call(Ctx* c, const mgn_dgraph* g, const float* params, void* ws, size_
     return fail(MGN_ERR_WORKSPACE, "workspace %zu bytes < required %zu", ws_bytes, c->L.total);
   if (g->n_nodes > 0) {
     if (!params || !ws) return fail(MGN_ERR_ARG, "null params or workspace");
-    if (!g->rowptr || !g->tiles || g->n_tiles <= 0 || (g->n_edges > 0 && (!g->senders || !g->rev)))
+    if (!g->rowptr || !g->tiles || g->n_tiles <= 0 ||
+        (g->n_edges > 0 && (!g->senders || !g->receivers || !g->rev)))
       return fail(MGN_ERR_ARG, "device graph arrays missing");
     if (g->n_long > 0 && !g->long_nodes) return fail(MGN_ERR_ARG, "long_nodes missing");
   }

@@ -223,166 +223,6 @@ __global__ void __launch_bounds__(NT) k_node_bwd(int64_t N, const float* __restr
   put_col(base + 49536 + n, dbt, q);
 }
 
-// --------------------------------------------------------- edge phase
-// Given ebar_in = dL/de_out (absent for the last block) and aggbar:
-// mbar = ebar_in + aggbar[receiver]; back through LN and the MLP to
-// zbar = dL/dz1 (written out for the sender sums, and summed per receiver
-// into R), ebar_out = ebar_in + W1e^T zbar.
-template <int PREC>
-__global__ void __launch_bounds__(NT) k_edge_bwd(EdgeTiles tl, const typename Tr<PREC>::T* __restrict__ e,
-                                                 const float* __restrict__ ebar_in, int have_ebar,
-                                                 float* __restrict__ ebar_out, const float* __restrict__ Pn,
-                                                 const float* __restrict__ aggbar, MlpW w, float eps,
-                                                 typename Tr<PREC>::T* __restrict__ zbar, float* __restrict__ R,
-                                                 float* __restrict__ slots, Partials part) {
-  typedef Tr<PREC> P;
-  typedef typename P::T T;
-  constexpr int LDT = D + P::PAD;
-  __shared__ __align__(16) T sE[TM * LDT];
-  __shared__ __align__(16) T sA1[TM * LDT];
-  __shared__ __align__(16) T sG[TM * LDT];
-  __shared__ float red[TM][NW], red2[TM][NW];
-  __shared__ float red2x[TM][NW][2];
-  __shared__ int sSend[TM], sRecv[TM];
-  const int tid = threadIdx.x, w8 = tid >> 6, lane = tid & 63, i = lane & 15, q = lane >> 4;
-  const int n = w8 * 16 + i;
-  const float b1 = w.b1[n], b2 = w.b2[n], gam = w.gamma[n];
-  f32x4 dW1[8], dW2[8];
-#pragma unroll
-  for (int cb = 0; cb < 8; ++cb) dW1[cb] = dW2[cb] = zero4();
-  float db1 = 0.f, db2 = 0.f, dg = 0.f, dbt = 0.f;
-
-  for (int64_t t = blockIdx.x; t < tl.n_tiles; t += gridDim.x) {
-    const int4 td = reinterpret_cast<const int4*>(tl.tiles)[t];
-    const int nb = td.x, eb = td.z, ne_ = td.w - td.z;
-    const bool full = td.y >= 0;
-    const int nv = full ? td.y - nb : 1;
-    stage_rows(sE, LDT, e + (size_t)eb * D, ne_, tid);
-    if (tid < ne_) sSend[tid] = tl.senders[eb + tid];
-    if (full) {
-      for (int j = tid; j < nv; j += NT) {
-        const int a = tl.rowptr[nb + j] - eb, b = tl.rowptr[nb + j + 1] - eb;
-        for (int u = a; u < b; ++u) sRecv[u] = nb + j;
-      }
-    } else if (tid < ne_) {
-      sRecv[tid] = nb;
-    }
-    __syncthreads();
-
-    f32x4 acc[NRB];
-#pragma unroll
-    for (int rb = 0; rb < NRB; ++rb)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int row = rb * 16 + q * 4 + r;
-        float z = 0.f;
-        if (row < ne_) {
-          z = b1 + Pn[(size_t)sSend[row] * (2 * D) + n];
-          z += Pn[(size_t)sRecv[row] * (2 * D) + D + n];
-        }
-        acc[rb][r] = z;
-      }
-    gemm_tile<PREC, D>(acc, sE, LDT, (const T*)w.W1, 3 * D, w8 * 16, 0, i, q);
-    uint32_t mask = 0;
-#pragma unroll
-    for (int rb = 0; rb < NRB; ++rb)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        if (acc[rb][r] > 0.f) mask |= 1u << (rb * 4 + r);
-        sA1[(rb * 16 + q * 4 + r) * LDT + n] = P::cvt(fmaxf(acc[rb][r], 0.f));
-      }
-    __syncthreads();
-#pragma unroll
-    for (int rb = 0; rb < NRB; ++rb) acc[rb] = f32x4{b2, b2, b2, b2};
-    gemm_tile<PREC, D>(acc, sA1, LDT, (const T*)w.W2, D, w8 * 16, 0, i, q);
-    f32x4 mean[NRB], rstd[NRB], xh[NRB], mb[NRB], eb_in[NRB];
-    ln_stats(acc, red, red2, eps, w8, i, q, mean, rstd);
-#pragma unroll
-    for (int rb = 0; rb < NRB; ++rb)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int row = rb * 16 + q * 4 + r;
-        xh[rb][r] = (acc[rb][r] - mean[rb][r]) * rstd[rb][r];
-        float eo = 0.f, m = 0.f;
-        if (row < ne_) {
-          if (have_ebar) eo = ebar_in[(size_t)(eb + row) * D + n];
-          m = eo + aggbar[(size_t)sRecv[row] * D + n];
-        }
-        eb_in[rb][r] = eo;
-        mb[rb][r] = m;
-        dg += m * xh[rb][r];
-        dbt += m;
-      }
-    f32x4 g[NRB];
-    ln_bwd(g, mb, xh, rstd, gam, red2x, w8, i, q);
-#pragma unroll
-    for (int rb = 0; rb < NRB; ++rb)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        db2 += g[rb][r];
-        sG[(rb * 16 + q * 4 + r) * LDT + n] = P::cvt(g[rb][r]);
-      }
-    gtx<PREC, 8>(dW2, g, sA1, LDT, 0, i, q);
-    __syncthreads();
-#pragma unroll
-    for (int rb = 0; rb < NRB; ++rb) acc[rb] = zero4();
-    gemm_tile<PREC, D>(acc, sG, LDT, (const T*)w.W2t, D, w8 * 16, 0, i, q);
-#pragma unroll
-    for (int rb = 0; rb < NRB; ++rb)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        g[rb][r] = (mask >> (rb * 4 + r)) & 1u ? acc[rb][r] : 0.f;
-        db1 += g[rb][r];
-      }
-    gtx<PREC, 8>(dW1, g, sE, LDT, 0, i, q);
-    __syncthreads();
-#pragma unroll
-    for (int rb = 0; rb < NRB; ++rb)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) sG[(rb * 16 + q * 4 + r) * LDT + n] = P::cvt(g[rb][r]);
-    __syncthreads();
-#pragma unroll
-    for (int rb = 0; rb < NRB; ++rb) acc[rb] = eb_in[rb];
-    gemm_tile<PREC, D>(acc, sG, LDT, (const T*)w.W1t, D, w8 * 16, 0, i, q);
-#pragma unroll
-    for (int rb = 0; rb < NRB; ++rb)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int row = rb * 16 + q * 4 + r;
-        if (row < ne_) ebar_out[(size_t)(eb + row) * D + n] = acc[rb][r];
-      }
-    for (int idx = tid; idx < ne_ * (D / 8); idx += NT) {
-      const int row = idx >> 4, c = (idx & 15) * 8;
-      T* dst = zbar + (size_t)(eb + row) * D + c;
-#pragma unroll
-      for (int j = 0; j < 8; ++j) dst[j] = sG[row * LDT + c + j];
-    }
-    {
-      const int c = tid & (D - 1), vg = tid >> 7;
-      if (full) {
-        for (int j = vg; j < nv; j += NT / D) {
-          const int a = tl.rowptr[nb + j] - eb, b = tl.rowptr[nb + j + 1] - eb;
-          float s = 0.f;
-          for (int u = a; u < b; ++u) s += tof(sG[u * LDT + c]);
-          R[(size_t)(nb + j) * D + c] = s;
-        }
-      } else if (vg == 0) {
-        float s = 0.f;
-        for (int u = 0; u < ne_; ++u) s += tof(sG[u * LDT + c]);
-        slots[(size_t)(-1 - td.y) * D + c] = s;
-      }
-    }
-    __syncthreads();
-  }
-  float* base = part.buf + (size_t)blockIdx.x * part.stride;
-  put_w<8>(base, D, dW1, w8, i, q);
-  put_col(base + 16384 + n, db1, q);
-  put_w<8>(base + 16512, D, dW2, w8, i, q);
-  put_col(base + 32896 + n, db2, q);
-  put_col(base + 33024 + n, dg, q);
-  put_col(base + 33152 + n, dbt, q);
-}
-
 // ------------------------------------------------- sender-side sums
 // S[v] = sum over in-edges e of v of zbar[rev[e]] (= sum over out-edges of v),
 // then hbar_out = hbar_part + W1s^T S + W1r^T R and the weight gradients of
@@ -618,21 +458,6 @@ hipError_t launch_node_bwd(int prec, int64_t N, const float* h, const float* agg
   else
     hipLaunchKernelGGL(k_node_bwd<MGN_FP32>, dim3(g), dim3(NT), 0, s, N, h, agg, hbar_in, w, eps, hbar_part, aggbar,
                        part);
-  return hipGetLastError();
-}
-
-hipError_t launch_edge_bwd(int prec, const EdgeTiles& t, const void* e, const float* ebar_in, int have_ebar,
-                           float* ebar_out, const float* Pn, const float* aggbar, const MlpW& w, float eps,
-                           void* zbar, float* R, float* slots, const Partials& part, int* nblocks, hipStream_t s) {
-  const int g = bwd_grid(t.n_tiles, part);
-  *nblocks = g;
-  if (!g) return hipSuccess;
-  if (prec == MGN_BF16)
-    hipLaunchKernelGGL(k_edge_bwd<MGN_BF16>, dim3(g), dim3(NT), 0, s, t, (const bf16*)e, ebar_in, have_ebar,
-                       ebar_out, Pn, aggbar, w, eps, (bf16*)zbar, R, slots, part);
-  else
-    hipLaunchKernelGGL(k_edge_bwd<MGN_FP32>, dim3(g), dim3(NT), 0, s, t, (const float*)e, ebar_in, have_ebar,
-                       ebar_out, Pn, aggbar, w, eps, (float*)zbar, R, slots, part);
   return hipGetLastError();
 }
 

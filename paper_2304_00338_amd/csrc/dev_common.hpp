@@ -1,7 +1,7 @@
 // Device helpers shared by the gfx950 kernels: MFMA operand traits, tile
 // staging, row LayerNorm statistics and deterministic in-wave reductions.
 //
-// Every kernel works on tiles of TM = 64 rows (edges or nodes) with 512
+// Every kernel works on tiles of TM = 32 rows (edges or nodes) with 512
 // threads = 8 wave64s.  Wave w owns output columns [16w, 16w+16) of every
 // 128-wide layer.  MFMA 16x16xK operand layout (lane l, i = l & 15,
 // q = l >> 4):
@@ -21,7 +21,7 @@ namespace dev {
 constexpr int D = 128;     // latent width
 constexpr int NT = 512;    // threads per block
 constexpr int NW = 8;      // waves per block
-constexpr int TM = 64;     // rows per tile
+constexpr int TM = 32;     // rows per tile
 constexpr int NRB = TM / 16;
 
 typedef __bf16 bf16;
@@ -165,13 +165,18 @@ __device__ __forceinline__ void gtx<MGN_BF16, 16>(f32x4 (&acc)[16], const f32x4 
   gtx_bf16<16>(acc, g, X, ldx, xcol0, i, q);
 }
 
-// Sum over the 16 lanes that share q (one row of a 16-column block), in a
-// fixed butterfly order.
+// Sum over the 16 lanes that share q (one DPP row = one row of a 16-column
+// block): rotate-and-add within the row by 8, 4, 2, 1 lanes, so every lane
+// ends with the same total, formed in a fixed order.
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xf, 0xf, false));
+}
 __device__ __forceinline__ float sum16(float s) {
-  s += __shfl_xor(s, 8, 16);
-  s += __shfl_xor(s, 4, 16);
-  s += __shfl_xor(s, 2, 16);
-  s += __shfl_xor(s, 1, 16);
+  s += dpp_f<0x128>(s);  // row_ror:8
+  s += dpp_f<0x124>(s);  // row_ror:4
+  s += dpp_f<0x122>(s);  // row_ror:2
+  s += dpp_f<0x121>(s);  // row_ror:1
   return s;
 }
 

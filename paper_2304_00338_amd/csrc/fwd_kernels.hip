@@ -30,7 +30,7 @@ __global__ void __launch_bounds__(256) k_pack(const float* __restrict__ params, 
 // Node products for the next block's edge MLP: P[v] = [W1s h_v, W1r h_v].
 template <int PREC>
 __device__ __forceinline__ void emit_P(const typename Tr<PREC>::T* sH, int ld, const MlpW& nx, int64_t r0, int nr,
-                                       float* __restrict__ P_out, int w8, int i, int q) {
+                                       typename Tr<PREC>::T* __restrict__ P_out, int w8, int i, int q) {
   typedef typename Tr<PREC>::T T;
   const T* W1 = (const T*)nx.W1;
   f32x4 ps[NRB], pr[NRB];
@@ -45,9 +45,9 @@ __device__ __forceinline__ void emit_P(const typename Tr<PREC>::T* sH, int ld, c
     for (int r = 0; r < 4; ++r) {
       const int row = rb * 16 + q * 4 + r;
       if (row < nr) {
-        float* p = P_out + (size_t)(r0 + row) * (2 * D);
-        p[n] = ps[rb][r];
-        p[D + n] = pr[rb][r];
+        typename Tr<PREC>::T* p = P_out + (size_t)(r0 + row) * (2 * D);
+        p[n] = Tr<PREC>::cvt(ps[rb][r]);
+        p[D + n] = Tr<PREC>::cvt(pr[rb][r]);
       }
     }
 }
@@ -55,7 +55,8 @@ __device__ __forceinline__ void emit_P(const typename Tr<PREC>::T* sH, int ld, c
 // ------------------------------------------------------- node encoder
 template <int PREC, bool EMIT>
 __global__ void __launch_bounds__(NT) k_node_enc(int64_t N, const float* __restrict__ x_in, MlpW w, MlpW nx,
-                                                 float eps, float* __restrict__ h_out, float* __restrict__ P_out) {
+                                                 float eps, float* __restrict__ h_out,
+                                                 typename Tr<PREC>::T* __restrict__ P_out) {
   typedef Tr<PREC> P;
   typedef typename P::T T;
   constexpr int LDT = D + P::PAD;
@@ -172,114 +173,6 @@ __global__ void __launch_bounds__(NT) k_edge_enc(int64_t E, const float* __restr
   }
 }
 
-// ------------------------------------------------- fused edge phase
-// For every edge of a receiver-aligned tile:
-//   z1 = W1e e + P_s[s] + P_r[r] + b1,  m = LN(W2 relu(z1) + b2),
-//   e_out = e + m  (unless write_e == 0, i.e. the last block),
-// and for every receiver of the tile agg[v] = sum of m over its in-edges,
-// in ascending in-segment order (chunk tiles of long segments write their
-// sums to a slot instead).
-template <int PREC>
-__global__ void __launch_bounds__(NT) k_edge_fwd(EdgeTiles tl, const typename Tr<PREC>::T* __restrict__ e_in,
-                                                 typename Tr<PREC>::T* __restrict__ e_out, int write_e,
-                                                 const float* __restrict__ Pn, MlpW w, float eps,
-                                                 float* __restrict__ agg, float* __restrict__ slots) {
-  typedef Tr<PREC> P;
-  typedef typename P::T T;
-  constexpr int LDT = D + P::PAD;
-  constexpr int LDM = D + 4;
-  constexpr int A1B = TM * LDT * (int)sizeof(T);
-  constexpr int MB = TM * LDM * 4;
-  __shared__ __align__(16) T sE[TM * LDT];
-  __shared__ __align__(16) char sU[A1B > MB ? A1B : MB];  // a1 tile, then m tile
-  __shared__ float red[TM][NW], red2[TM][NW];
-  __shared__ int sSend[TM], sRecv[TM];
-  T* sA1 = reinterpret_cast<T*>(sU);
-  float* sM = reinterpret_cast<float*>(sU);
-
-  const int tid = threadIdx.x, w8 = tid >> 6, lane = tid & 63, i = lane & 15, q = lane >> 4;
-  const int n = w8 * 16 + i;
-  const float b1 = w.b1[n], b2 = w.b2[n], gam = w.gamma[n], bet = w.beta[n];
-  const T* W1 = (const T*)w.W1;
-  const T* W2 = (const T*)w.W2;
-
-  for (int64_t t = blockIdx.x; t < tl.n_tiles; t += gridDim.x) {
-    const int4 td = reinterpret_cast<const int4*>(tl.tiles)[t];
-    const int nb = td.x, eb = td.z, ne_ = td.w - td.z;
-    const bool full = td.y >= 0;
-    const int nv = full ? td.y - nb : 1;
-    stage_rows(sE, LDT, e_in + (size_t)eb * D, ne_, tid);
-    if (tid < ne_) sSend[tid] = tl.senders[eb + tid];
-    if (full) {
-      for (int j = tid; j < nv; j += NT) {
-        const int a = tl.rowptr[nb + j] - eb, b = tl.rowptr[nb + j + 1] - eb;
-        for (int u = a; u < b; ++u) sRecv[u] = nb + j;
-      }
-    } else if (tid < ne_) {
-      sRecv[tid] = nb;
-    }
-    __syncthreads();
-
-    f32x4 acc[NRB];
-#pragma unroll
-    for (int rb = 0; rb < NRB; ++rb)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int row = rb * 16 + q * 4 + r;
-        float z = 0.f;
-        if (row < ne_) {
-          z = b1 + Pn[(size_t)sSend[row] * (2 * D) + n];
-          z += Pn[(size_t)sRecv[row] * (2 * D) + D + n];
-        }
-        acc[rb][r] = z;
-      }
-    gemm_tile<PREC, D>(acc, sE, LDT, W1, 3 * D, w8 * 16, 0, i, q);
-#pragma unroll
-    for (int rb = 0; rb < NRB; ++rb)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) sA1[(rb * 16 + q * 4 + r) * LDT + n] = P::cvt(fmaxf(acc[rb][r], 0.f));
-    __syncthreads();
-#pragma unroll
-    for (int rb = 0; rb < NRB; ++rb) acc[rb] = f32x4{b2, b2, b2, b2};
-    gemm_tile<PREC, D>(acc, sA1, LDT, W2, D, w8 * 16, 0, i, q);
-    f32x4 mean[NRB], rstd[NRB];
-    ln_stats(acc, red, red2, eps, w8, i, q, mean, rstd);
-    // every wave has finished reading sA1 (GEMM2 precedes the barriers above)
-#pragma unroll
-    for (int rb = 0; rb < NRB; ++rb)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int row = rb * 16 + q * 4 + r;
-        sM[row * LDM + n] = gam * ((acc[rb][r] - mean[rb][r]) * rstd[rb][r]) + bet;
-      }
-    __syncthreads();
-    if (write_e) {
-      for (int idx = tid; idx < ne_ * (D / 8); idx += NT) {
-        const int row = idx >> 4, c = (idx & 15) * 8;
-        T* dst = e_out + (size_t)(eb + row) * D + c;
-#pragma unroll
-        for (int j = 0; j < 8; ++j) dst[j] = P::cvt(tof(sE[row * LDT + c + j]) + sM[row * LDM + c + j]);
-      }
-    }
-    {
-      const int c = tid & (D - 1), vg = tid >> 7;
-      if (full) {
-        for (int j = vg; j < nv; j += NT / D) {
-          const int a = tl.rowptr[nb + j] - eb, b = tl.rowptr[nb + j + 1] - eb;
-          float s = 0.f;
-          for (int u = a; u < b; ++u) s += sM[u * LDM + c];
-          agg[(size_t)(nb + j) * D + c] = s;
-        }
-      } else if (vg == 0) {
-        float s = 0.f;
-        for (int u = 0; u < ne_; ++u) s += sM[u * LDM + c];
-        slots[(size_t)(-1 - td.y) * D + c] = s;
-      }
-    }
-    __syncthreads();
-  }
-}
-
 // Long in-segments: dst[v] = sum of the chunk slots in chunk order.
 __global__ void __launch_bounds__(128) k_slot_fixup(const int32_t* __restrict__ longn, const float* __restrict__ slots,
                                                     float* __restrict__ dst) {
@@ -296,7 +189,7 @@ __global__ void __launch_bounds__(128) k_slot_fixup(const int32_t* __restrict__ 
 template <int PREC, bool EMIT>
 __global__ void __launch_bounds__(NT) k_node_fwd(int64_t N, const float* __restrict__ h_in, const float* __restrict__ agg,
                                                  MlpW w, MlpW nx, float eps, float* __restrict__ h_out,
-                                                 float* __restrict__ P_out) {
+                                                 typename Tr<PREC>::T* __restrict__ P_out) {
   typedef Tr<PREC> P;
   typedef typename P::T T;
   constexpr int LDT = D + P::PAD;
@@ -412,20 +305,20 @@ hipError_t launch_pack(int prec, const float* params, void* pack, const PackList
 }
 
 hipError_t launch_node_enc(int prec, int64_t N, const float* x, const MlpW& w, const MlpW* nx, float eps,
-                           float* h_out, float* P_out, hipStream_t s) {
+                           float* h_out, void* P_out, hipStream_t s) {
   const int g = grid_for((N + TM - 1) / TM, kFwdBlocks);
   if (!g) return hipSuccess;
   const MlpW nn = nx ? *nx : w;
   if (prec == MGN_BF16) {
     if (nx)
-      hipLaunchKernelGGL((k_node_enc<MGN_BF16, true>), dim3(g), dim3(NT), 0, s, N, x, w, nn, eps, h_out, P_out);
+      hipLaunchKernelGGL((k_node_enc<MGN_BF16, true>), dim3(g), dim3(NT), 0, s, N, x, w, nn, eps, h_out, (bf16*)P_out);
     else
-      hipLaunchKernelGGL((k_node_enc<MGN_BF16, false>), dim3(g), dim3(NT), 0, s, N, x, w, nn, eps, h_out, P_out);
+      hipLaunchKernelGGL((k_node_enc<MGN_BF16, false>), dim3(g), dim3(NT), 0, s, N, x, w, nn, eps, h_out, (bf16*)P_out);
   } else {
     if (nx)
-      hipLaunchKernelGGL((k_node_enc<MGN_FP32, true>), dim3(g), dim3(NT), 0, s, N, x, w, nn, eps, h_out, P_out);
+      hipLaunchKernelGGL((k_node_enc<MGN_FP32, true>), dim3(g), dim3(NT), 0, s, N, x, w, nn, eps, h_out, (float*)P_out);
     else
-      hipLaunchKernelGGL((k_node_enc<MGN_FP32, false>), dim3(g), dim3(NT), 0, s, N, x, w, nn, eps, h_out, P_out);
+      hipLaunchKernelGGL((k_node_enc<MGN_FP32, false>), dim3(g), dim3(NT), 0, s, N, x, w, nn, eps, h_out, (float*)P_out);
   }
   return hipGetLastError();
 }
@@ -441,19 +334,6 @@ hipError_t launch_edge_enc(int prec, int64_t E, const float* f, const MlpW& w, f
   return hipGetLastError();
 }
 
-hipError_t launch_edge_fwd(int prec, const EdgeTiles& t, const void* e_in, void* e_out, int write_e,
-                           const float* Pn, const MlpW& w, float eps, float* agg, float* slots, hipStream_t s) {
-  const int g = grid_for(t.n_tiles, kFwdBlocks);
-  if (!g) return hipSuccess;
-  if (prec == MGN_BF16)
-    hipLaunchKernelGGL(k_edge_fwd<MGN_BF16>, dim3(g), dim3(NT), 0, s, t, (const bf16*)e_in, (bf16*)e_out, write_e,
-                       Pn, w, eps, agg, slots);
-  else
-    hipLaunchKernelGGL(k_edge_fwd<MGN_FP32>, dim3(g), dim3(NT), 0, s, t, (const float*)e_in, (float*)e_out,
-                       write_e, Pn, w, eps, agg, slots);
-  return hipGetLastError();
-}
-
 hipError_t launch_slot_fixup(const int32_t* long_nodes, int64_t n_long, const float* slots, float* dst,
                              hipStream_t s) {
   if (n_long <= 0) return hipSuccess;
@@ -462,24 +342,24 @@ hipError_t launch_slot_fixup(const int32_t* long_nodes, int64_t n_long, const fl
 }
 
 hipError_t launch_node_fwd(int prec, int64_t N, const float* h_in, const float* agg, const MlpW& w,
-                           const MlpW* nx, float eps, float* h_out, float* P_out, hipStream_t s) {
+                           const MlpW* nx, float eps, float* h_out, void* P_out, hipStream_t s) {
   const int g = grid_for((N + TM - 1) / TM, kFwdBlocks);
   if (!g) return hipSuccess;
   const MlpW nn = nx ? *nx : w;
   if (prec == MGN_BF16) {
     if (nx)
       hipLaunchKernelGGL((k_node_fwd<MGN_BF16, true>), dim3(g), dim3(NT), 0, s, N, h_in, agg, w, nn, eps, h_out,
-                         P_out);
+                         (bf16*)P_out);
     else
       hipLaunchKernelGGL((k_node_fwd<MGN_BF16, false>), dim3(g), dim3(NT), 0, s, N, h_in, agg, w, nn, eps, h_out,
-                         P_out);
+                         (bf16*)P_out);
   } else {
     if (nx)
       hipLaunchKernelGGL((k_node_fwd<MGN_FP32, true>), dim3(g), dim3(NT), 0, s, N, h_in, agg, w, nn, eps, h_out,
-                         P_out);
+                         (float*)P_out);
     else
       hipLaunchKernelGGL((k_node_fwd<MGN_FP32, false>), dim3(g), dim3(NT), 0, s, N, h_in, agg, w, nn, eps, h_out,
-                         P_out);
+                         (float*)P_out);
   }
   return hipGetLastError();
 }

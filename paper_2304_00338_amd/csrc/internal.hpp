@@ -11,10 +11,10 @@
 namespace mgn {
 
 // Receiver-aligned edge tiles: at most this many edges and nodes per tile.
-constexpr int kTileEdges = 64;
-constexpr int kTileNodes = 64;
+constexpr int kTileEdges = 32;
+constexpr int kTileNodes = 32;
 // Node kernels process this many consecutive nodes per tile.
-constexpr int kNodeTile = 64;
+constexpr int kNodeTile = 32;
 
 void set_error(const char* fmt, ...);
 

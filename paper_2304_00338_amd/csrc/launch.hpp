@@ -40,6 +40,7 @@ struct EdgeTiles {
   int64_t n_tiles;
   const int32_t* rowptr;
   const int32_t* senders;
+  const int32_t* receivers;
 };
 
 // Per-block partial buffers for deterministic weight-gradient reductions.
@@ -56,15 +57,15 @@ int grid_for(int64_t n_tiles, int max_blocks);
 hipError_t launch_pack(int prec, const float* params, void* pack, const PackList& L, hipStream_t s);
 
 hipError_t launch_node_enc(int prec, int64_t N, const float* node_in, const MlpW& w, const MlpW* next_edge,
-                           float eps, float* h_out, float* P_out, hipStream_t s);
+                           float eps, float* h_out, void* P_out, hipStream_t s);
 hipError_t launch_edge_enc(int prec, int64_t E, const float* efeat, const MlpW& w, float eps, void* e_out,
                            hipStream_t s);
 hipError_t launch_edge_fwd(int prec, const EdgeTiles& t, const void* e_in, void* e_out, int write_e,
-                           const float* P, const MlpW& w, float eps, float* agg, float* slots, hipStream_t s);
+                           const void* P, const MlpW& w, float eps, float* agg, float* slots, hipStream_t s);
 hipError_t launch_slot_fixup(const int32_t* long_nodes, int64_t n_long, const float* slots, float* dst,
                              hipStream_t s);
 hipError_t launch_node_fwd(int prec, int64_t N, const float* h_in, const float* agg, const MlpW& w,
-                           const MlpW* next_edge, float eps, float* h_out, float* P_out, hipStream_t s);
+                           const MlpW* next_edge, float eps, float* h_out, void* P_out, hipStream_t s);
 hipError_t launch_decoder(int prec, int64_t N, const float* h, const MlpW& w, float* out, hipStream_t s);
 
 hipError_t launch_decoder_bwd(int prec, int64_t N, const float* h, const float* gout, const MlpW& w,
@@ -73,9 +74,13 @@ hipError_t launch_node_bwd(int prec, int64_t N, const float* h, const float* agg
                            const MlpW& w, float eps, float* hbar_part, float* aggbar, const Partials& part,
                            int* nblocks, hipStream_t s);
 hipError_t launch_edge_bwd(int prec, const EdgeTiles& t, const void* e, const float* ebar_in, int have_ebar,
-                           float* ebar_out, const float* P, const float* aggbar, const MlpW& w, float eps,
+                           float* ebar_out, const void* P, const float* aggbar, const MlpW& w, float eps,
                            void* zbar, float* R, float* slots, const Partials& part, int* nblocks,
                            hipStream_t s);
+// dW[o][i] = sum_rows G[row][o] X[row][i] for [M][128] operand-precision
+// streams, written as per-block [128][128] partials.
+hipError_t launch_wgrad(int prec, int64_t M, const void* G, const void* X, const Partials& part, int* nblocks,
+                        hipStream_t s);
 hipError_t launch_node_srcsum(int prec, int64_t N, const int32_t* rowptr, const int32_t* rev, const void* zbar,
                               const float* R, const float* h, const float* hbar_part, const MlpW& w,
                               float* hbar_out, const Partials& part, int* nblocks, hipStream_t s);

@@ -37,7 +37,8 @@ class Config(C.Structure):
 
 class DGraph(C.Structure):
     _fields_ = [("n_nodes", C.c_int64), ("n_edges", C.c_int64), ("rowptr", C.c_void_p),
-                ("senders", C.c_void_p), ("rev", C.c_void_p), ("tiles", C.c_void_p),
+                ("senders", C.c_void_p), ("receivers", C.c_void_p), ("rev", C.c_void_p),
+                ("tiles", C.c_void_p),
                 ("n_tiles", C.c_int64), ("long_nodes", C.c_void_p), ("n_long", C.c_int64)]
 
 
@@ -244,13 +245,15 @@ class DeviceGraph:
         self.n_nodes, self.n_edges = g.n_nodes, g.n_edges
         self.rowptr = torch.from_numpy(a["rowptr"]).to(dev)
         self.senders = torch.from_numpy(a["senders"]).to(dev)
+        self.receivers = torch.from_numpy(a["receivers"]).to(dev)
         self.rev = torch.from_numpy(a["rev"]).to(dev)
         self.tiles = torch.from_numpy(tiles.reshape(-1)).to(dev)
         self.long_nodes = torch.from_numpy(longn.reshape(-1)).to(dev)
         self.efeat = torch.from_numpy(a["efeat"]).to(dev)
         self.n_tiles, self.n_long = tiles.shape[0], longn.shape[0]
         self.struct = DGraph(self.n_nodes, self.n_edges, self.rowptr.data_ptr(),
-                             self.senders.data_ptr(), self.rev.data_ptr(), self.tiles.data_ptr(),
+                             self.senders.data_ptr(), self.receivers.data_ptr(),
+                             self.rev.data_ptr(), self.tiles.data_ptr(),
                              self.n_tiles,
                              self.long_nodes.data_ptr() if self.n_long else None, self.n_long)
 

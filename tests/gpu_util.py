@@ -9,11 +9,13 @@ import synth
 FP32_TOL = 1e-4   # relative L2, fp32 outputs and gradients
 BF16_TOL = 2e-2   # relative L2, bf16-MLP outputs; also bf16 gradients at a
                   # smooth point (every ReLU input far from its kink)
-# Relative L2 of bf16 gradients at an ordinary point.  The fp64 oracle's own
-# gradient moves by 5-9% under a single 2^-9 (one bf16 rounding) relative
-# perturbation of the weights and by 7.5-11% under 2^-8, because ReLU inputs
-# near zero switch branch; the bf16 path rounds weights and every activation
-# operand once per GEMM, so its gradient error is of the 2^-8 size.
+# Relative L2 of bf16 gradients at an ordinary point: the gradient there is
+# not a smooth function of the weights (ReLU inputs near zero switch branch),
+# so no fixed tolerance fits every case.  The bf16 path rounds the weights
+# and every activation operand once per GEMM (relative 2^-9 each); the bound
+# per MLP segment is twice the largest change of the oracle's own gradient
+# under random relative 2^-8 sign perturbations of all weights (see
+# bf16_grad_tols), never below BF16_GRAD_TOL.
 BF16_GRAD_TOL = 0.15
 KINK_TAU = 3e-6   # |ReLU input| below which fp32 and fp64 may take different branches
 
@@ -60,6 +62,23 @@ def kink_resolved(tape, w, gp, gi, tau=KINK_TAU, max_kinks=48):
         return g0, gi0, []
     gS, giS = O.mgn_backward(tape, w, flips=S)
     return gS, giS, S
+
+
+def bf16_grad_tols(pb, trials=2, scale=2.0):
+    """Per-segment tolerances {name: tol, 'gin': tol} for bf16 gradients at
+    an ordinary point (see BF16_GRAD_TOL).  Oracle-only computation."""
+    _, tape = O.mgn_forward(pb.go, pb.params, pb.node_in, pb.go.efeat, pb.m, keep=True)
+    g0, gi0 = O.mgn_backward(tape, pb.w)
+    worst = {}
+    for t in range(trials):
+        xi = np.random.default_rng(1000 + t).choice([-1.0, 1.0], size=pb.params.shape)
+        _, t1 = O.mgn_forward(pb.go, pb.params * (1 + 2.0 ** -8 * xi), pb.node_in, pb.go.efeat, pb.m,
+                              keep=True)
+        g1, gi1 = O.mgn_backward(t1, pb.w)
+        for name, a, b in segments(pb.m):
+            worst[name] = max(worst.get(name, 0.0), rel_l2(g1[a:b], g0[a:b]))
+        worst["gin"] = max(worst.get("gin", 0.0), rel_l2(gi1, gi0))
+    return {k: max(BF16_GRAD_TOL, scale * v) for k, v in worst.items()}
 
 
 class Problem:

@@ -58,7 +58,7 @@ def check_schedule(g):
     for nb, ne, eb, ee in tiles:
         assert 0 <= ee - eb <= TE
         if ne >= 0:
-            assert ne > nb and ne - nb <= 64
+            assert ne > nb and ne - nb <= TE
             assert eb == rp[nb] and ee == rp[ne]
             covered[nb:ne] += 1
         else:
@@ -108,7 +108,7 @@ def test_hub_node_long_segment():
     g = mgn.build_graph(cells, pos)
     compare_graph(g, O.build_graph(cells, pos))
     tiles, longn = g.schedule()
-    assert longn.shape[0] == 1 and longn[0, 0] == 0 and longn[0, 2] == 5
+    assert longn.shape[0] == 1 and longn[0, 0] == 0 and longn[0, 2] == -(-300 // mgn.tile_edges())
     check_schedule(g)
 
 

@@ -22,7 +22,6 @@ import torch
 import oracle as O
 import synth
 
-torch.set_default_dtype(torch.float64)
 GOLD = os.path.join(os.path.dirname(__file__), "golden", "paper_facts.json")
 
 
@@ -67,9 +66,9 @@ def test_layer_norm_constant_gives_beta():
 def dense_mgn(g, P, node_in, efeat, m, D=128):
     """Whole MGN call with dense one-hot incidence matrices (torch fp64)."""
     N, E = g.n_nodes, g.n_edges
-    S = torch.zeros(E, N)
+    S = torch.zeros(E, N, dtype=torch.float64)
     S[torch.arange(E), torch.tensor(g.senders)] = 1.0
-    R = torch.zeros(E, N)
+    R = torch.zeros(E, N, dtype=torch.float64)
     R[torch.arange(E), torch.tensor(g.receivers)] = 1.0
     F = torch.nn.functional
     off = [0]
