@@ -123,8 +123,7 @@ __global__ void __launch_bounds__(NT) k_node_bwd(int64_t N, const float* __restr
   __shared__ __align__(16) T sX[TM * LDX];
   __shared__ __align__(16) T sA[TM * LDT];
   __shared__ __align__(16) T sG[TM * LDT];
-  __shared__ float red[TM][NW], red2[TM][NW];
-  __shared__ float red2x[TM][NW][2];
+  __shared__ LnScratch ln;
   const int tid = threadIdx.x, w8 = tid >> 6, lane = tid & 63, i = lane & 15, q = lane >> 4;
   const int n = w8 * 16 + i;
   const float b1 = w.b1[n], b2 = w.b2[n], gam = w.gamma[n];
@@ -158,7 +157,7 @@ __global__ void __launch_bounds__(NT) k_node_bwd(int64_t N, const float* __restr
     for (int rb = 0; rb < NRB; ++rb) acc[rb] = f32x4{b2, b2, b2, b2};
     gemm_tile<PREC, D>(acc, sA, LDT, (const T*)w.W2, D, w8 * 16, 0, i, q);
     f32x4 mean[NRB], rstd[NRB], xh[NRB], yb[NRB];
-    ln_stats(acc, red, red2, eps, w8, i, q, mean, rstd);
+    ln_stats(acc, ln, eps, w8, i, q, mean, rstd);
 #pragma unroll
     for (int rb = 0; rb < NRB; ++rb)
 #pragma unroll
@@ -170,7 +169,7 @@ __global__ void __launch_bounds__(NT) k_node_bwd(int64_t N, const float* __restr
         dbt += yb[rb][r];
       }
     f32x4 g[NRB];
-    ln_bwd(g, yb, xh, rstd, gam, red2x, w8, i, q);
+    ln_bwd(g, yb, xh, rstd, gam, ln, w8, i, q);
 #pragma unroll
     for (int rb = 0; rb < NRB; ++rb)
 #pragma unroll
@@ -311,8 +310,7 @@ __global__ void __launch_bounds__(NT) k_enc_bwd(int64_t M, const float* __restri
   __shared__ __align__(16) T sA[TM * LDT];
   __shared__ __align__(16) T sG[TM * LDT];
   __shared__ float sZ[KIN == 8 ? TM * LDM : 1];
-  __shared__ float red[TM][NW], red2[TM][NW];
-  __shared__ float red2x[TM][NW][2];
+  __shared__ LnScratch ln;
   const int tid = threadIdx.x, w8 = tid >> 6, lane = tid & 63, i = lane & 15, q = lane >> 4;
   const int n = w8 * 16 + i;
   const float b1 = w.b1[n], b2 = w.b2[n], gam = w.gamma[n];
@@ -353,7 +351,7 @@ __global__ void __launch_bounds__(NT) k_enc_bwd(int64_t M, const float* __restri
     for (int rb = 0; rb < NRB; ++rb) acc[rb] = f32x4{b2, b2, b2, b2};
     gemm_tile<PREC, D>(acc, sA, LDT, (const T*)w.W2, D, w8 * 16, 0, i, q);
     f32x4 mean[NRB], rstd[NRB], xh[NRB], yb[NRB];
-    ln_stats(acc, red, red2, eps, w8, i, q, mean, rstd);
+    ln_stats(acc, ln, eps, w8, i, q, mean, rstd);
 #pragma unroll
     for (int rb = 0; rb < NRB; ++rb)
 #pragma unroll
@@ -365,7 +363,7 @@ __global__ void __launch_bounds__(NT) k_enc_bwd(int64_t M, const float* __restri
         dbt += yb[rb][r];
       }
     f32x4 g[NRB];
-    ln_bwd(g, yb, xh, rstd, gam, red2x, w8, i, q);
+    ln_bwd(g, yb, xh, rstd, gam, ln, w8, i, q);
 #pragma unroll
     for (int rb = 0; rb < NRB; ++rb)
 #pragma unroll

@@ -170,7 +170,7 @@ __device__ __forceinline__ void gtx<MGN_BF16, 16>(f32x4 (&acc)[16], const f32x4 
 // ends with the same total, formed in a fixed order.
 template <int CTRL>
 __device__ __forceinline__ float dpp_f(float v) {
-  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xf, 0xf, false));
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xf, 0xf, false));
 }
 __device__ __forceinline__ float sum16(float s) {
   s += dpp_f<0x128>(s);  // row_ror:8
@@ -178,6 +178,27 @@ __device__ __forceinline__ float sum16(float s) {
   s += dpp_f<0x122>(s);  // row_ror:2
   s += dpp_f<0x121>(s);  // row_ror:1
   return s;
+}
+// sum16 of all 4*NRB values of a C-layout tile, one rotation step at a time
+// so that independent DPP operations fill each other's wait states.  Same
+// order of additions per value as sum16.
+__device__ __forceinline__ void sum16x(f32x4 (&v)[NRB]) {
+#pragma unroll
+  for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) v[rb][r] += dpp_f<0x128>(v[rb][r]);
+#pragma unroll
+  for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) v[rb][r] += dpp_f<0x124>(v[rb][r]);
+#pragma unroll
+  for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) v[rb][r] += dpp_f<0x122>(v[rb][r]);
+#pragma unroll
+  for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) v[rb][r] += dpp_f<0x121>(v[rb][r]);
 }
 
 // Sum over the four q groups (lanes i, i+16, i+32, i+48).
@@ -187,79 +208,126 @@ __device__ __forceinline__ float sum_q(float s) {
   return s;
 }
 
+// LDS scratch of the row LayerNorm helpers.  red/red2/red2x hold one partial
+// per (row, wave); fin holds, per wave, the 32 row totals that wave formed
+// itself (so reading them back needs no block barrier).
+struct LnScratch {
+  float red[TM][NW];
+  float red2[TM][NW];
+  float red2x[TM][NW][2];
+  float fin[NW][2 * TM];
+};
+
+// Orders this wave's LDS writes before its later LDS reads of other lanes'
+// data (LDS requests of one wave are served in issue order).
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// Sum of the 8 per-wave partials of one row in wave order.
+__device__ __forceinline__ float row_total(const float* p) {
+  const f32x4 a = *reinterpret_cast<const f32x4*>(p), b = *reinterpret_cast<const f32x4*>(p + 4);
+  return ((((((a[0] + a[1]) + a[2]) + a[3]) + b[0]) + b[1]) + b[2]) + b[3];
+}
+
 // Per-row mean and 1/sqrt(var + eps) over the 128 columns held by the 8
-// waves (biased variance, two passes).  red/red2: LDS [TM][NW] scratch.
+// waves (biased variance, two passes).  Each wave reduces its 16 columns
+// with DPP, the 8 wave partials of a row are summed once per wave by lane
+// row (lanes 0..31) and handed back through the wave's own LDS slot.
 // Contains two block barriers; every thread of the block must call it.
-__device__ __forceinline__ void ln_stats(const f32x4 (&v)[NRB], float (*red)[NW], float (*red2)[NW], float eps,
-                                         int w, int i, int q, f32x4 (&mean)[NRB], f32x4 (&rstd)[NRB]) {
+__device__ __forceinline__ void ln_stats(const f32x4 (&v)[NRB], LnScratch& S, float eps, int w, int i, int q,
+                                         f32x4 (&mean)[NRB], f32x4 (&rstd)[NRB]) {
+  const int lane = threadIdx.x & 63;
+  float* fin = S.fin[w];
+  {
+    f32x4 s[NRB];
 #pragma unroll
-  for (int rb = 0; rb < NRB; ++rb)
+    for (int rb = 0; rb < NRB; ++rb) s[rb] = v[rb];
+    sum16x(s);
+    if (i == 0)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const float s = sum16(v[rb][r]);
-      if (i == 0) red[rb * 16 + q * 4 + r][w] = s;
-    }
+      for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) S.red[rb * 16 + q * 4 + r][w] = s[rb][r];
+  }
   __syncthreads();
+  if (lane < TM) fin[lane] = row_total(S.red[lane]) * (1.0f / D);
+  wave_lds_sync();
+  {
+    f32x4 s[NRB];
 #pragma unroll
-  for (int rb = 0; rb < NRB; ++rb)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const float* p = red[rb * 16 + q * 4 + r];
-      float t = 0.f;
-#pragma unroll
-      for (int u = 0; u < NW; ++u) t += p[u];
-      mean[rb][r] = t * (1.0f / D);
-      const float d = v[rb][r] - mean[rb][r];
-      const float s = sum16(d * d);
-      if (i == 0) red2[rb * 16 + q * 4 + r][w] = s;
+    for (int rb = 0; rb < NRB; ++rb) {
+      mean[rb] = *reinterpret_cast<const f32x4*>(fin + rb * 16 + q * 4);
+      const f32x4 d = v[rb] - mean[rb];
+      s[rb] = d * d;
     }
+    sum16x(s);
+    if (i == 0)
+#pragma unroll
+      for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) S.red2[rb * 16 + q * 4 + r][w] = s[rb][r];
+  }
   __syncthreads();
+  if (lane < TM) fin[TM + lane] = __builtin_amdgcn_rsqf(row_total(S.red2[lane]) * (1.0f / D) + eps);
+  wave_lds_sync();
 #pragma unroll
-  for (int rb = 0; rb < NRB; ++rb)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const float* p = red2[rb * 16 + q * 4 + r];
-      float t = 0.f;
-#pragma unroll
-      for (int u = 0; u < NW; ++u) t += p[u];
-      rstd[rb][r] = 1.0f / sqrtf(t * (1.0f / D) + eps);
-    }
+  for (int rb = 0; rb < NRB; ++rb) rstd[rb] = *reinterpret_cast<const f32x4*>(fin + TM + rb * 16 + q * 4);
 }
 
 // LayerNorm backward for one tile: given dy (C layout), xhat, rstd and this
 // lane's gain, returns dz = rstd * (dxh - mean(dxh) - xhat * mean(dxh*xhat))
-// with dxh = dy * gamma.  red2x: LDS [TM][NW][2].  One block barrier.
+// with dxh = dy * gamma.  One block barrier.
 __device__ __forceinline__ void ln_bwd(f32x4 (&dz)[NRB], const f32x4 (&dy)[NRB], const f32x4 (&xhat)[NRB],
-                                       const f32x4 (&rstd)[NRB], float gam, float (*red2x)[NW][2], int w,
-                                       int i, int q) {
+                                       const f32x4 (&rstd)[NRB], float gam, LnScratch& S, int w, int i, int q) {
+  const int lane = threadIdx.x & 63;
+  float* fin = S.fin[w];
+  {
+    f32x4 s1[NRB], s2[NRB];
 #pragma unroll
-  for (int rb = 0; rb < NRB; ++rb)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const float dxh = dy[rb][r] * gam;
-      const float s1 = sum16(dxh);
-      const float s2 = sum16(dxh * xhat[rb][r]);
-      if (i == 0) {
-        red2x[rb * 16 + q * 4 + r][w][0] = s1;
-        red2x[rb * 16 + q * 4 + r][w][1] = s2;
-      }
+    for (int rb = 0; rb < NRB; ++rb) {
+      s1[rb] = dy[rb] * gam;
+      s2[rb] = s1[rb] * xhat[rb];
     }
+    sum16x(s1);
+    sum16x(s2);
+    if (i == 0)
+#pragma unroll
+      for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          S.red2x[rb * 16 + q * 4 + r][w][0] = s1[rb][r];
+          S.red2x[rb * 16 + q * 4 + r][w][1] = s2[rb][r];
+        }
+  }
   __syncthreads();
+  if (lane < TM) {
+    const f32x4* p = reinterpret_cast<const f32x4*>(S.red2x[lane]);
+    float t1 = 0.f, t2 = 0.f;
 #pragma unroll
-  for (int rb = 0; rb < NRB; ++rb)
+    for (int u = 0; u < NW / 2; ++u) {
+      const f32x4 x = p[u];
+      t1 += x[0];
+      t2 += x[1];
+      t1 += x[2];
+      t2 += x[3];
+    }
+    fin[lane] = t1 * (1.0f / D);
+    fin[TM + lane] = t2 * (1.0f / D);
+  }
+  wave_lds_sync();
+#pragma unroll
+  for (int rb = 0; rb < NRB; ++rb) {
+    const f32x4 m1 = *reinterpret_cast<const f32x4*>(fin + rb * 16 + q * 4);
+    const f32x4 m2 = *reinterpret_cast<const f32x4*>(fin + TM + rb * 16 + q * 4);
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const float(*p)[2] = red2x[rb * 16 + q * 4 + r];
-      float t1 = 0.f, t2 = 0.f;
-#pragma unroll
-      for (int u = 0; u < NW; ++u) {
-        t1 += p[u][0];
-        t2 += p[u][1];
-      }
-      const float m1 = t1 * (1.0f / D), m2 = t2 * (1.0f / D);
       const float dxh = dy[rb][r] * gam;
-      dz[rb][r] = rstd[rb][r] * (dxh - m1 - xhat[rb][r] * m2);
+      dz[rb][r] = rstd[rb][r] * (dxh - m1[r] - xhat[rb][r] * m2[r]);
     }
+  }
 }
 
 // Copy rows [0, nrows) of a row-major global [.][128] array (element type S)

@@ -221,7 +221,7 @@ __global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
   __shared__ __align__(16) T sE[TM * LDT];
   __shared__ __align__(16) float sP[TM * LDM];
   __shared__ __align__(16) char sU[A1B > MB ? A1B : MB];  // a1 tile, then m tile
-  __shared__ float red[TM][NW], red2[TM][NW];
+  __shared__ LnScratch ln;
   __shared__ int2 sSR[2][TM];
   T* sA1 = reinterpret_cast<T*>(sU);
   float* sM = reinterpret_cast<float*>(sU);
@@ -305,7 +305,7 @@ __global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
     for (int rb = 0; rb < NRB; ++rb) acc[rb] = f32x4{b2, b2, b2, b2};
     gemm_w<PREC>(acc, sA1, LDT, w2, i, q);
     f32x4 mean[NRB], rstd[NRB];
-    ln_stats(acc, red, red2, eps, w8, i, q, mean, rstd);
+    ln_stats(acc, ln, eps, w8, i, q, mean, rstd);
 #pragma unroll
     for (int rb = 0; rb < NRB; ++rb)
 #pragma unroll
@@ -370,8 +370,7 @@ k_edge_bwd(EdgeTiles tl, const typename Tr<PREC>::T* __restrict__ e, const float
   __shared__ __align__(16) bf16 sA1T[TX ? D * LDTT : 8];
   __shared__ __align__(16) T sW2t[TX ? D * LDT : 8];
   __shared__ __align__(16) T sW1t[TX ? D * LDT : 8];
-  __shared__ float red[TM][NW], red2[TM][NW];
-  __shared__ float red2x[TM][NW][2];
+  __shared__ LnScratch ln;
   __shared__ int2 sSR[2][TM];
 
   const int tid = threadIdx.x, w8 = tid >> 6, lane = tid & 63, i = lane & 15, q = lane >> 4;
@@ -498,7 +497,7 @@ k_edge_bwd(EdgeTiles tl, const typename Tr<PREC>::T* __restrict__ e, const float
     f32x4 rstd[NRB];
     {
       f32x4 mean[NRB];
-      ln_stats(acc, red, red2, eps, w8, i, q, mean, rstd);
+      ln_stats(acc, ln, eps, w8, i, q, mean, rstd);
 #pragma unroll
       for (int rb = 0; rb < NRB; ++rb) acc[rb] = (acc[rb] - mean[rb]) * rstd[rb];  // xhat
     }
@@ -511,7 +510,7 @@ k_edge_bwd(EdgeTiles tl, const typename Tr<PREC>::T* __restrict__ e, const float
         dbt += mb[rb][r];
       }
     f32x4 g[NRB];
-    ln_bwd(g, mb, acc, rstd, gam, red2x, w8, i, q);
+    ln_bwd(g, mb, acc, rstd, gam, ln, w8, i, q);
 #pragma unroll
     for (int rb = 0; rb < NRB; ++rb)
 #pragma unroll
@@ -664,6 +663,7 @@ static constexpr int kWgradBlocks = 512;
 
 hipError_t launch_edge_fwd(int prec, const EdgeTiles& t, const void* e_in, void* e_out, int write_e, const void* Pn,
                            const MlpW& w, float eps, float* agg, float* slots, hipStream_t s) {
+  if (prec == MGN_BF16) return launch_edge_fwd_rows(t, e_in, e_out, write_e, Pn, w, eps, agg, slots, s);
   const int g = grid_for(t.n_tiles, kEdgeFwdBlocks);
   if (!g) return hipSuccess;
   if (prec == MGN_BF16)

@@ -21,9 +21,10 @@ __global__ void __launch_bounds__(256) k_pack(const float* __restrict__ params, 
   const int64_t n = (int64_t)pe.rows * pe.cols;
   for (int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x; idx < n; idx += (int64_t)gridDim.x * 256) {
     const int64_t r = idx / pe.cols, c = idx % pe.cols;
-    const T v = (T)params[pe.src + idx];
+    const int64_t sr = pe.perm ? perm_row((int)r) : r;
+    const T v = (T)params[pe.src + sr * pe.ld + c];
     pack[pe.dst + idx] = v;
-    pack[pe.dstt + c * pe.rows + r] = v;
+    if (pe.dstt >= 0) pack[pe.dstt + c * pe.rows + r] = v;
   }
 }
 
@@ -62,7 +63,7 @@ __global__ void __launch_bounds__(NT) k_node_enc(int64_t N, const float* __restr
   constexpr int LDT = D + P::PAD;
   __shared__ float sX[TM][8];
   __shared__ __align__(16) T sA[TM * LDT];
-  __shared__ float red[TM][NW], red2[TM][NW];
+  __shared__ LnScratch ln;
   const int tid = threadIdx.x, w8 = tid >> 6, lane = tid & 63, i = lane & 15, q = lane >> 4;
   const int n = w8 * 16 + i;
   const float b1 = w.b1[n], b2 = w.b2[n], gam = w.gamma[n], bet = w.beta[n];
@@ -94,7 +95,7 @@ __global__ void __launch_bounds__(NT) k_node_enc(int64_t N, const float* __restr
     for (int rb = 0; rb < NRB; ++rb) acc[rb] = f32x4{b2, b2, b2, b2};
     gemm_tile<PREC, D>(acc, sA, LDT, (const T*)w.W2, D, w8 * 16, 0, i, q);
     f32x4 mean[NRB], rstd[NRB];
-    ln_stats(acc, red, red2, eps, w8, i, q, mean, rstd);
+    ln_stats(acc, ln, eps, w8, i, q, mean, rstd);
 #pragma unroll
     for (int rb = 0; rb < NRB; ++rb)
 #pragma unroll
@@ -122,7 +123,7 @@ __global__ void __launch_bounds__(NT) k_edge_enc(int64_t E, const float* __restr
   constexpr int LDT = D + P::PAD;
   __shared__ float sX[TM][4];
   __shared__ __align__(16) T sA[TM * LDT];
-  __shared__ float red[TM][NW], red2[TM][NW];
+  __shared__ LnScratch ln;
   const int tid = threadIdx.x, w8 = tid >> 6, lane = tid & 63, i = lane & 15, q = lane >> 4;
   const int n = w8 * 16 + i;
   const float b1 = w.b1[n], b2 = w.b2[n], gam = w.gamma[n], bet = w.beta[n];
@@ -154,7 +155,7 @@ __global__ void __launch_bounds__(NT) k_edge_enc(int64_t E, const float* __restr
     for (int rb = 0; rb < NRB; ++rb) acc[rb] = f32x4{b2, b2, b2, b2};
     gemm_tile<PREC, D>(acc, sA, LDT, (const T*)w.W2, D, w8 * 16, 0, i, q);
     f32x4 mean[NRB], rstd[NRB];
-    ln_stats(acc, red, red2, eps, w8, i, q, mean, rstd);
+    ln_stats(acc, ln, eps, w8, i, q, mean, rstd);
 #pragma unroll
     for (int rb = 0; rb < NRB; ++rb)
 #pragma unroll
@@ -196,7 +197,7 @@ __global__ void __launch_bounds__(NT) k_node_fwd(int64_t N, const float* __restr
   constexpr int LDX = 2 * D + P::PAD;
   __shared__ __align__(16) T sX[TM * LDX];  // [h, agg]; later the new h
   __shared__ __align__(16) T sA[TM * LDT];
-  __shared__ float red[TM][NW], red2[TM][NW];
+  __shared__ LnScratch ln;
   const int tid = threadIdx.x, w8 = tid >> 6, lane = tid & 63, i = lane & 15, q = lane >> 4;
   const int n = w8 * 16 + i;
   const float b1 = w.b1[n], b2 = w.b2[n], gam = w.gamma[n], bet = w.beta[n];
@@ -220,7 +221,7 @@ __global__ void __launch_bounds__(NT) k_node_fwd(int64_t N, const float* __restr
     for (int rb = 0; rb < NRB; ++rb) acc[rb] = f32x4{b2, b2, b2, b2};
     gemm_tile<PREC, D>(acc, sA, LDT, (const T*)w.W2, D, w8 * 16, 0, i, q);
     f32x4 mean[NRB], rstd[NRB];
-    ln_stats(acc, red, red2, eps, w8, i, q, mean, rstd);
+    ln_stats(acc, ln, eps, w8, i, q, mean, rstd);
 #pragma unroll
     for (int rb = 0; rb < NRB; ++rb)
 #pragma unroll

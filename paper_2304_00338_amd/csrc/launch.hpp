@@ -11,6 +11,8 @@ namespace mgn {
 // [out][in]; W1t/W2t are the transposed copies [in][out].  Biases and
 // LayerNorm parameters are the caller's float32 values.
 struct MlpW {
+  const void* W1p;  // row-permuted copy of the edge-latent part of W1 (edge MLPs)
+  const void* W2p;  // row-permuted copy of W2 (edge MLPs)
   const void* W1;
   const void* W1t;
   const void* W2;
@@ -26,9 +28,21 @@ struct MlpW {
 struct PackEnt {
   int64_t src;   // float offset of the [rows][cols] matrix in params
   int64_t dst;   // element offset of the copy in the pack
-  int64_t dstt;  // element offset of the transposed copy
+  int64_t dstt;  // element offset of the transposed copy (-1: none)
   int32_t rows, cols;
+  int32_t ld;    // source row stride (floats)
+  int32_t perm;  // 1: copy row perm_row(p) of the source into row p
 };
+
+// Output-row order of the weights used by the row-per-wave edge kernels:
+// packed row p = ob*16 + m holds row 32*(m/4) + 4*ob + m%4 of W, so that an
+// MFMA C fragment of output block ob gives lane group q the features
+// 32q + 4ob + r (r < 4), i.e. every lane ends with a contiguous run of 32
+// output features, which is exactly its B operand of the next product.
+__host__ __device__ inline int perm_row(int p) {
+  const int ob = p >> 4, m = p & 15;
+  return 32 * (m >> 2) + 4 * ob + (m & 3);
+}
 constexpr int kPackMax = 64;
 struct PackList {
   PackEnt e[kPackMax];
@@ -62,6 +76,9 @@ hipError_t launch_edge_enc(int prec, int64_t E, const float* efeat, const MlpW& 
                            hipStream_t s);
 hipError_t launch_edge_fwd(int prec, const EdgeTiles& t, const void* e_in, void* e_out, int write_e,
                            const void* P, const MlpW& w, float eps, float* agg, float* slots, hipStream_t s);
+// bf16 edge forward with one wave per tile (uses MlpW::W1p / W2p).
+hipError_t launch_edge_fwd_rows(const EdgeTiles& t, const void* e_in, void* e_out, int write_e, const void* P,
+                                const MlpW& w, float eps, float* agg, float* slots, hipStream_t s);
 hipError_t launch_slot_fixup(const int32_t* long_nodes, int64_t n_long, const float* slots, float* dst,
                              hipStream_t s);
 hipError_t launch_node_fwd(int prec, int64_t N, const float* h_in, const float* agg, const MlpW& w,
