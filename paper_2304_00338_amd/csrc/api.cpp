@@ -129,10 +129,10 @@ struct Layout {
   size_t pack = 0;
   // activation sets
   size_t act = 0, act_stride = 0;
-  size_t e_off = 0, h_off = 0, agg_off = 0, P_off = 0;  // within a set
+  size_t e_off = 0, h_off = 0, agg_off = 0, P_off = 0, a1_off = 0;  // within a set
   size_t node_in = 0, K = 0, slots = 0;
   // backward
-  size_t ebar = 0, zbar = 0, hb_a = 0, hb_b = 0, aggbar = 0, R = 0, part = 0, kbar = 0, ystage = 0, gin = 0;
+  size_t ebar = 0, zbar = 0, dz = 0, hb_a = 0, hb_b = 0, aggbar = 0, R = 0, part = 0, kbar = 0, ystage = 0, gin = 0;
   size_t total = 0;
 };
 
@@ -242,6 +242,11 @@ void plan(Ctx& c) {
   so = al256(so + (size_t)la * N * D * 4);
   L.P_off = so;
   so = al256(so + (size_t)la * N * 2 * D * tsz);
+  // bf16 with save: first-layer activations of every edge MLP, read by the
+  // backward instead of recomputing the first layer
+  const bool keep_a1 = c.save && c.cfg.precision == MGN_BF16;
+  L.a1_off = so;
+  so = al256(so + (keep_a1 ? (size_t)la * E * D * 2 : 0));
   L.act_stride = so;
   L.act = o;
   o = al256(o + so * c.ne_sets);
@@ -256,6 +261,8 @@ void plan(Ctx& c) {
     o = al256(o + (size_t)E * D * 4);
     L.zbar = o;
     o = al256(o + (size_t)E * D * c.se);
+    L.dz = o;
+    o = al256(o + (keep_a1 ? (size_t)E * D * 2 : 0));
     L.hb_a = o;
     o = al256(o + (size_t)N * D * 4);
     L.hb_b = o;
@@ -332,6 +339,10 @@ struct Run {
   float* agg_l(int k, int l) const {
     return (float*)(set(k) + c.L.agg_off) + (c.save ? (size_t)l * N * D : 0);
   }
+  void* a1_l(int k, int l) const {
+    if (!(c.save && prec == MGN_BF16)) return nullptr;
+    return set(k) + c.L.a1_off + (size_t)l * E * D * 2;
+  }
   void* P_l(int k, int l) const {
     return set(k) + c.L.P_off + (c.save ? (size_t)l * N * 2 * D * tsz() : 0);
   }
@@ -393,7 +404,7 @@ struct Run {
       const bool last = l == m - 1;
       void* e_out = c.save ? (last ? nullptr : e_l(k, l + 1)) : e_l(k, 0);
       LAUNCH(K_EDGE_FWD, launch_edge_fwd(prec, tl, e_l(k, l), e_out, last ? 0 : 1, P_l(k, l), W(M.edge[l], M.p_edge[l]), eps,
-                              agg_l(k, l), slots(), s));
+                              agg_l(k, l), slots(), a1_l(k, l), s));
       if (g.n_long > 0) LAUNCH(K_FIXUP, launch_slot_fixup(g.long_nodes, g.n_long, slots(), agg_l(k, l), s));
       MlpW nx;
       if (!last) nx = W(M.edge[l + 1], M.p_edge[l + 1]);
@@ -428,11 +439,22 @@ struct Run {
       LAUNCH(K_NODE_BWD, launch_node_bwd(prec, N, h_l(k, l), agg_l(k, l), hb_cur, W(on, M.p_node[l]), eps, hb_part, aggbar, pt,
                               &nb, s));
       if ((rc = reduce(nb, 0, 1, (int)on.size, grad, on.W1, 0)) != MGN_OK) return rc;
-      LAUNCH(K_EDGE_BWD, launch_edge_bwd(prec, tl, e_l(k, l), ebar, l < m - 1 ? 1 : 0, ebar, P_l(k, l), aggbar,
-                              W(oe, M.p_edge[l]), eps, zbar, R, slots(), pt, &nb, s));
-      if ((rc = reduce(nb, 16384, 1, (int)(oe.size - 3 * D * D), grad, oe.b1, 0)) != MGN_OK) return rc;
-      LAUNCH(K_WGRAD, launch_wgrad(prec, E, zbar, e_l(k, l), pt, &nb, s));
-      if ((rc = reduce(nb, 0, D, D, grad, oe.W1, 3 * D)) != MGN_OK) return rc;
+      if (prec == MGN_BF16) {
+        void* dz = ws + c.L.dz;
+        LAUNCH(K_EDGE_BWD, launch_edge_bwd_rows(tl, a1_l(k, l), ebar, l < m - 1 ? 1 : 0, ebar, aggbar, W(oe, M.p_edge[l]),
+                                    eps, zbar, dz, R, slots(), pt, &nb, s));
+        if ((rc = reduce(nb, 16384, 1, D, grad, oe.b1, 0)) != MGN_OK) return rc;
+        if ((rc = reduce(nb, 33024, 1, 2 * D, grad, oe.g, 0)) != MGN_OK) return rc;
+        LAUNCH(K_WGRAD, launch_wgrad2(E, zbar, e_l(k, l), dz, a1_l(k, l), pt, &nb, s));
+        if ((rc = reduce(nb, 16512, 1, D * D + D, grad, oe.W2, 0)) != MGN_OK) return rc;
+        if ((rc = reduce(nb, 0, D, D, grad, oe.W1, 3 * D)) != MGN_OK) return rc;
+      } else {
+        LAUNCH(K_EDGE_BWD, launch_edge_bwd(prec, tl, e_l(k, l), ebar, l < m - 1 ? 1 : 0, ebar, P_l(k, l), aggbar,
+                                W(oe, M.p_edge[l]), eps, zbar, R, slots(), pt, &nb, s));
+        if ((rc = reduce(nb, 16384, 1, (int)(oe.size - 3 * D * D), grad, oe.b1, 0)) != MGN_OK) return rc;
+        LAUNCH(K_WGRAD, launch_wgrad(prec, E, zbar, e_l(k, l), pt, &nb, s));
+        if ((rc = reduce(nb, 0, D, D, grad, oe.W1, 3 * D)) != MGN_OK) return rc;
+      }
       if (g.n_long > 0) LAUNCH(K_FIXUP, launch_slot_fixup(g.long_nodes, g.n_long, slots(), R, s));
       LAUNCH(K_SRCSUM, launch_node_srcsum(prec, N, g.rowptr, g.rev, zbar, R, h_l(k, l), hb_part, W(oe, M.p_edge[l]), hb_cur,
                                  pt, &nb, s));

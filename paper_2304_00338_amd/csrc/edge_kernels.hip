@@ -662,8 +662,8 @@ static constexpr int kEdgeBwdBlocks = 256;
 static constexpr int kWgradBlocks = 512;
 
 hipError_t launch_edge_fwd(int prec, const EdgeTiles& t, const void* e_in, void* e_out, int write_e, const void* Pn,
-                           const MlpW& w, float eps, float* agg, float* slots, hipStream_t s) {
-  if (prec == MGN_BF16) return launch_edge_fwd_rows(t, e_in, e_out, write_e, Pn, w, eps, agg, slots, s);
+                           const MlpW& w, float eps, float* agg, float* slots, void* a1_out, hipStream_t s) {
+  if (prec == MGN_BF16) return launch_edge_fwd_rows(t, e_in, e_out, write_e, Pn, w, eps, agg, slots, a1_out, s);
   const int g = grid_for(t.n_tiles, kEdgeFwdBlocks);
   if (!g) return hipSuccess;
   if (prec == MGN_BF16)

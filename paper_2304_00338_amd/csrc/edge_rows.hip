@@ -77,10 +77,46 @@ __device__ __forceinline__ float sum_rowlanes(float s) {
   return s;
 }
 
+// In-segment node sums over one staged 16-row half [lo_row, lo_row + 16) of
+// a tile (rows past the tile's end are never inside a segment).  Node j's
+// rows are [seg(j), seg(j+1)) with seg held by lane j of segv; j is the
+// first node whose sum is still open and carry its partial sum (features
+// 2*lane, 2*lane+1), added in ascending row order.  close(j, sum) is called
+// for every node whose segment ends inside this half.
+template <class F>
+__device__ __forceinline__ void seg_pass(const float* stage, int lane, int segv, int nv, int lo_row, int& j,
+                                         float2& carry, F&& close) {
+  const int hi_row = lo_row + 16;
+  while (j < nv) {
+    const int a = __builtin_amdgcn_readlane(segv, j), b = __builtin_amdgcn_readlane(segv, j + 1);
+    const int u0 = max(a, lo_row), u1 = min(b, hi_row);
+    for (int u = u0; u < u1; ++u) {
+      const float2 v = *reinterpret_cast<const float2*>(stage + (u - lo_row) * RW_LDM + 2 * lane);
+      carry.x += v.x;
+      carry.y += v.y;
+    }
+    if (b > hi_row) break;
+    close(j, carry);
+    carry = float2{0.f, 0.f};
+    ++j;
+  }
+}
+
+// Sum over the first nr staged rows of features 2*lane, 2*lane+1.
+__device__ __forceinline__ float2 col_pass(const float* stage, int lane, int nr) {
+  float2 c = {0.f, 0.f};
+  for (int u = 0; u < nr; ++u) {
+    const float2 v = *reinterpret_cast<const float2*>(stage + u * RW_LDM + 2 * lane);
+    c.x += v.x;
+    c.y += v.y;
+  }
+  return c;
+}
+
 __global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
 k_edge_fwd_rows(EdgeTiles tl, const bf16* __restrict__ e_in, bf16* __restrict__ e_out, int write_e,
                 const bf16* __restrict__ Pn, MlpW w, float eps, float* __restrict__ agg,
-                float* __restrict__ slots) {
+                float* __restrict__ slots, bf16* __restrict__ a1_out) {
   __shared__ __align__(16) RowsLds S;
   const int tid = threadIdx.x, lane = tid & 63, i = lane & 15, q = lane >> 4;
   const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -222,6 +258,11 @@ k_edge_fwd_rows(EdgeTiles tl, const bf16* __restrict__ e_in, bf16* __restrict__ 
           a1[s][r] = (bf16)relu(acc[2 * s][r]);
           a1[s][4 + r] = (bf16)relu(acc[2 * s + 1][r]);
         }
+      if (a1_out != nullptr && rb * 16 + i < n) {
+        bf16* ap = a1_out + ((size_t)d0.z + rb * 16 + i) * D + 32 * q;
+#pragma unroll
+        for (int s = 0; s < 4; ++s) *reinterpret_cast<uint4*>(ap + 8 * s) = __builtin_bit_cast(uint4, a1[s]);
+      }
       // ---- z2 = b2 + W2 a1
 #pragma unroll
       for (int ob = 0; ob < 8; ++ob) acc[ob] = *reinterpret_cast<const f32x4*>(S.b2 + 32 * q + 4 * ob);
@@ -278,22 +319,10 @@ k_edge_fwd_rows(EdgeTiles tl, const bf16* __restrict__ e_in, bf16* __restrict__ 
         }
       }
       wave_lds_sync();
-      // ---- in-segment sums over this half's rows; lane owns features 2l, 2l+1
-      const int lo_row = rb * 16, hi_row = rb * 16 + 16;
-      while (j < nv) {
-        const int a = __builtin_amdgcn_readlane(segv, j), b = __builtin_amdgcn_readlane(segv, j + 1);
-        const int u0 = max(a, lo_row), u1 = min(b, hi_row);
-        for (int u = u0; u < u1; ++u) {
-          const float2 v = *reinterpret_cast<const float2*>(stage + (u - lo_row) * RW_LDM + 2 * lane);
-          carry.x += v.x;
-          carry.y += v.y;
-        }
-        if (b > hi_row) break;
-        float* dst = d0.y >= 0 ? agg + (size_t)(d0.x + j) * D : slots + (size_t)(-1 - d0.y) * D;
-        *reinterpret_cast<float2*>(dst + 2 * lane) = carry;
-        carry = float2{0.f, 0.f};
-        ++j;
-      }
+      seg_pass(stage, lane, segv, nv, rb * 16, j, carry, [&](int jj, float2 v) {
+        float* dst = d0.y >= 0 ? agg + (size_t)(d0.x + jj) * D : slots + (size_t)(-1 - d0.y) * D;
+        *reinterpret_cast<float2*>(dst + 2 * lane) = v;
+      });
       wave_lds_sync();
     }
     if (!issued && t + stride < tend) issue(d1, s1, r1, nxt);
@@ -309,20 +338,412 @@ k_edge_fwd_rows(EdgeTiles tl, const bf16* __restrict__ e_in, bf16* __restrict__ 
   }
 }
 
+
+// ===================================================================== reverse
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+
+// Transposing LDS read (gfx950 ds_read_b64_tr_b16): within each group of 16
+// lanes, result lane l, element j' is element l & 3 of the 8 bytes addressed
+// by lane 4j' + (l >> 2).
+__device__ __forceinline__ bf16x4 lds_tr(const bf16* p) {
+  typedef __attribute__((address_space(3))) bf16x4 lds_v4;
+  typedef __attribute__((address_space(3))) bf16 lds_b;
+  return __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_v4*)((lds_b*)p));
+}
+__device__ __forceinline__ bf16x8 cat8(bf16x4 lo, bf16x4 hi) {
+  return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+
+// A operand of the transposed product C = W^T x from the row-permuted LDS
+// copy WP of W (rows = output features o of W): A[m][k] = W[o][k'] with
+// output slot m of block ob being input feature k' = perm_row(16ob + m) and
+// k running over o = 32q + 8s + j.  Row o of W sits at packed row
+// 16(2s + t) + 4q + j' for o = 32q + 8s + 4t + j'.
+__device__ __forceinline__ bf16x8 wt_frag(const bf16* WP, int ob, int s, int lam, int q) {
+  const int jp = lam >> 2, c = lam & 3;
+  const bf16* p0 = WP + ((2 * s) * 16 + 4 * q + jp) * RW_LDW + 32 * c + 4 * ob;
+  return cat8(lds_tr(p0), lds_tr(p0 + 16 * RW_LDW));
+}
+
+// Given ebar_in = dL/de_out (absent for the last block), aggbar, and the
+// saved first-layer activations a1 of the edge MLP: mbar = ebar_in +
+// aggbar[receiver]; back through the LayerNorm and the MLP to zbar = dL/dz1
+// (written out, with dz2 = dL/dz2 for the weight-gradient kernel), the
+// per-receiver sums R of zbar, ebar_out = ebar_in + W1e^T zbar, and
+// per-block partials of db1, dgamma, dbeta.
+__global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
+k_edge_bwd_rows(EdgeTiles tl, const bf16* __restrict__ a1_in, const float* __restrict__ ebar_in, int have_ebar,
+                float* __restrict__ ebar_out, const float* __restrict__ aggbar, MlpW w, float eps,
+                bf16* __restrict__ zbar, bf16* __restrict__ dz_out, float* __restrict__ R,
+                float* __restrict__ slots, Partials part) {
+  __shared__ __align__(16) RowsLds S;
+  const int tid = threadIdx.x, lane = tid & 63, i = lane & 15, q = lane >> 4;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+  {
+    const bf16* W1p = (const bf16*)w.W1p;
+    const bf16* W2p = (const bf16*)w.W2p;
+    for (int idx = tid; idx < D * D / 8; idx += NT) {
+      const int row = idx >> 4, c = (idx & 15) * 8;
+      *reinterpret_cast<uint4*>(S.W1 + row * RW_LDW + c) = *reinterpret_cast<const uint4*>(W1p + row * D + c);
+      *reinterpret_cast<uint4*>(S.W2 + row * RW_LDW + c) = *reinterpret_cast<const uint4*>(W2p + row * D + c);
+    }
+    if (tid < D) {
+      S.b2[tid] = w.b2[tid];
+      S.g[tid] = w.gamma[tid];
+    }
+  }
+  __syncthreads();
+
+  const int64_t NTL = tl.n_tiles;
+  const int G = gridDim.x;
+  int64_t t, stride, tend;
+  if ((G & 7) == 0) {
+    const int x = blockIdx.x & 7, per = G >> 3;
+    const int64_t chunk = (NTL + 7) >> 3;
+    const int64_t lo = x * chunk;
+    tend = min(NTL, lo + chunk);
+    t = lo + (int64_t)(blockIdx.x >> 3) * NW + wv;
+    stride = (int64_t)per * NW;
+  } else {
+    t = (int64_t)blockIdx.x * NW + wv;
+    stride = (int64_t)G * NW;
+    tend = NTL;
+  }
+
+  const int4* tiles = reinterpret_cast<const int4*>(tl.tiles);
+  auto desc = [&](int64_t tt) -> int4 {
+    const bool ok = tt < tend;
+    const int4 v = tiles[ok ? tt : tend - 1];
+    int4 r;
+    r.x = ok ? v.x : 0;
+    r.y = ok ? v.y : 0;
+    r.z = ok ? v.z : 0;
+    r.w = ok ? v.w : 0;
+    return r;
+  };
+  auto issue_a1 = [&](int4 d, uint4 (&A)[2][4]) {
+    const int n = tile_rows(d);
+    if (n <= 0) return;
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb) {
+      const int rc = min(rb * 16 + i, n - 1);
+      const bf16* ap = a1_in + ((size_t)d.z + rc) * D + 32 * q;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) A[rb][k] = *reinterpret_cast<const uint4*>(ap + 8 * k);
+    }
+  };
+
+  float2 db1 = {0.f, 0.f}, dga = {0.f, 0.f}, dbe = {0.f, 0.f};
+  float* stage = S.stage[wv];
+  if (t < tend) {
+    int4 d0 = desc(t), d1 = desc(t + stride);
+    uint4 cur[2][4];
+    issue_a1(d0, cur);
+    for (; t < tend; t += stride) {
+      const int n = tile_rows(d0);
+      const int4 d2 = desc(t + 2 * stride);
+      const int nv = d0.y >= 0 ? d0.y - d0.x : 1;
+      int segv = 0;
+      if (d0.y >= 0) {
+        if (lane <= nv) segv = tl.rowptr[d0.x + lane] - d0.z;
+      } else {
+        segv = lane == 0 ? 0 : n;
+      }
+      int recv[2];
+#pragma unroll
+      for (int rb = 0; rb < 2; ++rb) recv[rb] = rb * 16 + i < n ? tl.receivers[d0.z + rb * 16 + i] : 0;
+      uint4 nxt[2][4];
+      if (t + stride < tend) issue_a1(d1, nxt);
+
+      float2 carry = {0.f, 0.f};
+      int j = 0;
+#pragma unroll
+      for (int rb = 0; rb < 2; ++rb) {
+        const int row = rb * 16 + i;
+        const int rc = max(0, min(row, n - 1));
+        const int nh = max(0, min(16, n - rb * 16));  // valid rows of this half
+        // ---- incoming gradients of this half (C layout: features 32q + 4ob + r)
+        f32x4 eb[8], g[8];
+        {
+          const float* ep = ebar_in + ((size_t)d0.z + rc) * D + 32 * q;
+          const float* ap = aggbar + (size_t)recv[rb] * D + 32 * q;
+#pragma unroll
+          for (int ob = 0; ob < 8; ++ob) {
+            eb[ob] = (have_ebar && n > 0) ? *reinterpret_cast<const f32x4*>(ep + 4 * ob) : f32x4{0.f, 0.f, 0.f, 0.f};
+            g[ob] = n > 0 ? *reinterpret_cast<const f32x4*>(ap + 4 * ob) : f32x4{0.f, 0.f, 0.f, 0.f};
+          }
+        }
+        // ---- z2 = b2 + W2 a1 and its LayerNorm statistics
+        f32x4 acc[8];
+#pragma unroll
+        for (int ob = 0; ob < 8; ++ob) acc[ob] = *reinterpret_cast<const f32x4*>(S.b2 + 32 * q + 4 * ob);
+#pragma unroll
+        for (int s = 0; s < 4; ++s)
+#pragma unroll
+          for (int ob = 0; ob < 8; ++ob) {
+            const bf16x8 a = *reinterpret_cast<const bf16x8*>(S.W2 + (ob * 16 + i) * RW_LDW + 32 * q + 8 * s);
+            acc[ob] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, as_frag(cur[rb][s]), acc[ob], 0, 0, 0);
+          }
+        float sm = 0.f;
+#pragma unroll
+        for (int ob = 0; ob < 8; ++ob)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) sm += acc[ob][r];
+        const float mean = sum_rowlanes(sm) * (1.0f / D);
+        float sq = 0.f;
+#pragma unroll
+        for (int ob = 0; ob < 8; ++ob) {
+          acc[ob] -= mean;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) sq += acc[ob][r] * acc[ob][r];
+        }
+        const float rstd = __builtin_amdgcn_rsqf(sum_rowlanes(sq) * (1.0f / D) + eps);
+#pragma unroll
+        for (int ob = 0; ob < 8; ++ob) {
+          acc[ob] *= rstd;     // xhat
+          g[ob] += eb[ob];     // mbar = ebar_in + aggbar[receiver]
+        }
+        // ---- dgamma += sum_rows mbar * xhat, dbeta += sum_rows mbar
+        float* srow = stage + i * RW_LDM + 32 * q;
+#pragma unroll
+        for (int ob = 0; ob < 8; ++ob) *reinterpret_cast<f32x4*>(srow + 4 * ob) = g[ob] * acc[ob];
+        wave_lds_sync();
+        {
+          const float2 c = col_pass(stage, lane, nh);
+          dga.x += c.x;
+          dga.y += c.y;
+        }
+        wave_lds_sync();
+#pragma unroll
+        for (int ob = 0; ob < 8; ++ob) *reinterpret_cast<f32x4*>(srow + 4 * ob) = g[ob];
+        wave_lds_sync();
+        {
+          const float2 c = col_pass(stage, lane, nh);
+          dbe.x += c.x;
+          dbe.y += c.y;
+        }
+        // ---- LayerNorm backward: dz2 = rstd (dxh - mean(dxh) - xhat mean(dxh xhat)), dxh = mbar gamma
+        float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+        for (int ob = 0; ob < 8; ++ob) {
+          g[ob] *= *reinterpret_cast<const f32x4*>(S.g + 32 * q + 4 * ob);  // dxh
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            s1 += g[ob][r];
+            s2 += g[ob][r] * acc[ob][r];
+          }
+        }
+        const float m1 = sum_rowlanes(s1) * (1.0f / D), m2 = sum_rowlanes(s2) * (1.0f / D);
+        bf16x8 dzf[4];
+#pragma unroll
+        for (int s = 0; s < 4; ++s)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            dzf[s][r] = (bf16)(rstd * (g[2 * s][r] - m1 - acc[2 * s][r] * m2));
+            dzf[s][4 + r] = (bf16)(rstd * (g[2 * s + 1][r] - m1 - acc[2 * s + 1][r] * m2));
+          }
+        if (row < n) {
+          bf16* dp = dz_out + ((size_t)d0.z + row) * D + 32 * q;
+#pragma unroll
+          for (int s = 0; s < 4; ++s) *reinterpret_cast<uint4*>(dp + 8 * s) = __builtin_bit_cast(uint4, dzf[s]);
+        }
+        // ---- da1 = W2^T dz2, zbar = da1 where a1 > 0
+#pragma unroll
+        for (int ob = 0; ob < 8; ++ob) acc[ob] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s = 0; s < 4; ++s)
+#pragma unroll
+          for (int ob = 0; ob < 8; ++ob)
+            acc[ob] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wt_frag(S.W2, ob, s, i, q), dzf[s], acc[ob], 0, 0, 0);
+        bf16x8 zf[4];
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+          const bf16x8 a = as_frag(cur[rb][s]);
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            zf[s][r] = (float)a[r] > 0.f ? (bf16)acc[2 * s][r] : (bf16)0.f;
+            zf[s][4 + r] = (float)a[4 + r] > 0.f ? (bf16)acc[2 * s + 1][r] : (bf16)0.f;
+          }
+        }
+        if (row < n) {
+          bf16* zp = zbar + ((size_t)d0.z + row) * D + 32 * q;
+#pragma unroll
+          for (int s = 0; s < 4; ++s) *reinterpret_cast<uint4*>(zp + 8 * s) = __builtin_bit_cast(uint4, zf[s]);
+        }
+        // ---- per-receiver sums of zbar (as stored) and db1
+        wave_lds_sync();
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+          f32x4 lo, hi;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            lo[r] = (float)zf[s][r];
+            hi[r] = (float)zf[s][4 + r];
+          }
+          *reinterpret_cast<f32x4*>(srow + 8 * s) = lo;
+          *reinterpret_cast<f32x4*>(srow + 8 * s + 4) = hi;
+        }
+        wave_lds_sync();
+        seg_pass(stage, lane, segv, nv, rb * 16, j, carry, [&](int jj, float2 v) {
+          float* dst = d0.y >= 0 ? R + (size_t)(d0.x + jj) * D : slots + (size_t)(-1 - d0.y) * D;
+          *reinterpret_cast<float2*>(dst + 2 * lane) = v;
+          db1.x += v.x;
+          db1.y += v.y;
+        });
+        // ---- ebar_out = ebar_in + W1e^T zbar
+#pragma unroll
+        for (int s = 0; s < 4; ++s)
+#pragma unroll
+          for (int ob = 0; ob < 8; ++ob)
+            eb[ob] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wt_frag(S.W1, ob, s, i, q), zf[s], eb[ob], 0, 0, 0);
+        if (row < n) {
+          float* op = ebar_out + ((size_t)d0.z + row) * D + 32 * q;
+#pragma unroll
+          for (int ob = 0; ob < 8; ++ob) *reinterpret_cast<f32x4*>(op + 4 * ob) = eb[ob];
+        }
+        wave_lds_sync();
+      }
+#pragma unroll
+      for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+        for (int k = 0; k < 4; ++k) cur[rb][k] = nxt[rb][k];
+      d0 = d1;
+      d1 = d2;
+    }
+  }
+  // ---- block partials: the 8 waves' column sums in wave order
+  __syncthreads();
+  float* red = &S.stage[0][0];  // [3][NW][D]
+  *reinterpret_cast<float2*>(red + (0 * NW + wv) * D + 2 * lane) = db1;
+  *reinterpret_cast<float2*>(red + (1 * NW + wv) * D + 2 * lane) = dga;
+  *reinterpret_cast<float2*>(red + (2 * NW + wv) * D + 2 * lane) = dbe;
+  __syncthreads();
+  if (tid < 3 * D) {
+    const int k = tid >> 7, f = tid & (D - 1);
+    float v = 0.f;
+#pragma unroll
+    for (int u = 0; u < NW; ++u) v += red[(k * NW + u) * D + f];
+    float* base = part.buf + (size_t)blockIdx.x * part.stride;
+    const int off = k == 0 ? 16384 : (k == 1 ? 33024 : 33152);
+    base[off + f] = v;
+  }
+}
+
+// Weight gradients of the edge MLP from the saved streams, one pass:
+// dW1e = sum_rows zbar^T e, dW2 = sum_rows dz2^T a1, db2 = sum_rows dz2.
+// Each 32-row chunk of the four bf16 streams is staged row-major in LDS
+// (rows 144 elements apart, so the transposing reads below are free of bank
+// conflicts) while the next chunk is in flight in registers; wave w owns
+// output rows [16w, 16w + 16) of both matrices and reads its MFMA operands
+// with K = the chunk's rows through ds_read_b64_tr_b16.
+constexpr int WG_LD = D + 16;
+
+__global__ void __launch_bounds__(NT) k_wgrad2(int64_t M, const bf16* __restrict__ zb, const bf16* __restrict__ e,
+                                               const bf16* __restrict__ dz, const bf16* __restrict__ a1,
+                                               Partials part) {
+  __shared__ __align__(16) bf16 Sg[2][4][TM * WG_LD];
+  const int tid = threadIdx.x, w8 = tid >> 6, lane = tid & 63, i = lane & 15, q = lane >> 4;
+  const int jp = i >> 2, c4 = i & 3;
+  f32x4 acc1[8], acc2[8], accb = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int cb = 0; cb < 8; ++cb) acc1[cb] = acc2[cb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  bf16x8 ones;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) ones[j] = (bf16)1.f;
+  const int64_t nch = (M + TM - 1) / TM, G = gridDim.x;
+  const int srow = tid >> 4, scol = (tid & 15) * 8;
+  const bf16* src[4] = {zb, e, dz, a1};
+  uint4 L[4];
+  auto issue = [&](int64_t ch) {
+    const int64_t r = ch * TM + srow;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      if (r < M)
+        L[k] = *reinterpret_cast<const uint4*>(src[k] + r * D + scol);
+      else
+        L[k] = uint4{0u, 0u, 0u, 0u};
+    }
+  };
+  // operand of 16 columns col0.. with K = the chunk's rows q*8 + j
+  auto frag = [&](const bf16* X, int col0) -> bf16x8 {
+    const bf16* p = X + (q * 8 + jp) * WG_LD + col0 + 4 * c4;
+    return cat8(lds_tr(p), lds_tr(p + 4 * WG_LD));
+  };
+  int64_t c = blockIdx.x;
+  int buf = 0;
+  if (c < nch) issue(c);
+  for (; c < nch; c += G) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) *reinterpret_cast<uint4*>(&Sg[buf][k][srow * WG_LD + scol]) = L[k];
+    __syncthreads();
+    if (c + G < nch) issue(c + G);
+    const bf16x8 az = frag(Sg[buf][0], 16 * w8);
+    const bf16x8 ad = frag(Sg[buf][2], 16 * w8);
+#pragma unroll
+    for (int cb = 0; cb < 8; ++cb) {
+      acc1[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(az, frag(Sg[buf][1], 16 * cb), acc1[cb], 0, 0, 0);
+      acc2[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ad, frag(Sg[buf][3], 16 * cb), acc2[cb], 0, 0, 0);
+    }
+    accb = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ad, ones, accb, 0, 0, 0);
+    buf ^= 1;
+  }
+  float* base = part.buf + (size_t)blockIdx.x * part.stride;
+#pragma unroll
+  for (int cb = 0; cb < 8; ++cb)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int o = w8 * 16 + q * 4 + r;
+      base[(size_t)o * D + cb * 16 + i] = acc1[cb][r];
+      base[16512 + (size_t)o * D + cb * 16 + i] = acc2[cb][r];
+    }
+  if (i == 0)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) base[32896 + w8 * 16 + q * 4 + r] = accb[r];
+}
+
 }  // namespace dev
 
 using namespace dev;
 
 static constexpr int kRowsBlocks = 256;
 
-hipError_t launch_edge_fwd_rows(const EdgeTiles& t, const void* e_in, void* e_out, int write_e, const void* Pn,
-                                const MlpW& w, float eps, float* agg, float* slots, hipStream_t s) {
-  if (t.n_tiles <= 0) return hipSuccess;
-  const int64_t need = (t.n_tiles + NW - 1) / NW;
-  int g = (int)std::min<int64_t>(need, kRowsBlocks);
+static int rows_grid(int64_t n_tiles, int max_blocks) {
+  const int64_t need = (n_tiles + NW - 1) / NW;
+  int g = (int)std::min<int64_t>(need, max_blocks);
   if (g >= 8) g &= ~7;
-  hipLaunchKernelGGL(k_edge_fwd_rows, dim3(g), dim3(NT), 0, s, t, (const bf16*)e_in, (bf16*)e_out, write_e,
-                     (const bf16*)Pn, w, eps, agg, slots);
+  return g;
+}
+
+hipError_t launch_edge_fwd_rows(const EdgeTiles& t, const void* e_in, void* e_out, int write_e, const void* Pn,
+                                const MlpW& w, float eps, float* agg, float* slots, void* a1_out, hipStream_t s) {
+  if (t.n_tiles <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_edge_fwd_rows, dim3(rows_grid(t.n_tiles, kRowsBlocks)), dim3(NT), 0, s, t, (const bf16*)e_in,
+                     (bf16*)e_out, write_e, (const bf16*)Pn, w, eps, agg, slots, (bf16*)a1_out);
+  return hipGetLastError();
+}
+
+hipError_t launch_edge_bwd_rows(const EdgeTiles& t, const void* a1, const float* ebar_in, int have_ebar,
+                                float* ebar_out, const float* aggbar, const MlpW& w, float eps, void* zbar, void* dz,
+                                float* R, float* slots, const Partials& part, int* nblocks, hipStream_t s) {
+  *nblocks = 0;
+  if (t.n_tiles <= 0) return hipSuccess;
+  const int g = rows_grid(t.n_tiles, std::min(kRowsBlocks, part.max_blocks));
+  *nblocks = g;
+  hipLaunchKernelGGL(k_edge_bwd_rows, dim3(g), dim3(NT), 0, s, t, (const bf16*)a1, ebar_in, have_ebar, ebar_out,
+                     aggbar, w, eps, (bf16*)zbar, (bf16*)dz, R, slots, part);
+  return hipGetLastError();
+}
+
+static constexpr int kWgrad2Blocks = 512;
+
+hipError_t launch_wgrad2(int64_t M, const void* zbar, const void* e, const void* dz, const void* a1,
+                         const Partials& part, int* nblocks, hipStream_t s) {
+  *nblocks = 0;
+  if (M <= 0) return hipSuccess;
+  const int g = (int)std::min<int64_t>((M + TM - 1) / TM, std::min(kWgrad2Blocks, part.max_blocks));
+  *nblocks = g;
+  hipLaunchKernelGGL(k_wgrad2, dim3(g), dim3(NT), 0, s, M, (const bf16*)zbar, (const bf16*)e, (const bf16*)dz,
+                     (const bf16*)a1, part);
   return hipGetLastError();
 }
 
