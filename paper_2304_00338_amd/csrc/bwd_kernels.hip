@@ -222,6 +222,41 @@ __global__ void __launch_bounds__(NT) k_node_bwd(int64_t N, const float* __restr
   put_col(base + 49536 + n, dbt, q);
 }
 
+// 8 consecutive elements of a row as one (bf16) or two (fp32) 16-byte loads.
+template <typename T>
+struct RowChunk;
+template <>
+struct RowChunk<bf16> {
+  struct V {
+    uint4 a;
+  };
+  static __device__ __forceinline__ V load(const bf16* p) { return V{*reinterpret_cast<const uint4*>(p)}; }
+  static __device__ __forceinline__ void add(float (&s)[8], const V& v) {
+    const bf16x8 b = __builtin_bit_cast(bf16x8, v.a);
+#pragma unroll
+    for (int u = 0; u < 8; ++u) s[u] += (float)b[u];
+  }
+};
+template <>
+struct RowChunk<float> {
+  struct V {
+    float4 a, b;
+  };
+  static __device__ __forceinline__ V load(const float* p) {
+    return V{*reinterpret_cast<const float4*>(p), *reinterpret_cast<const float4*>(p + 4)};
+  }
+  static __device__ __forceinline__ void add(float (&s)[8], const V& v) {
+    s[0] += v.a.x;
+    s[1] += v.a.y;
+    s[2] += v.a.z;
+    s[3] += v.a.w;
+    s[4] += v.b.x;
+    s[5] += v.b.y;
+    s[6] += v.b.z;
+    s[7] += v.b.w;
+  }
+};
+
 // ------------------------------------------------- sender-side sums
 // S[v] = sum over in-edges e of v of zbar[rev[e]] (= sum over out-edges of v),
 // then hbar_out = hbar_part + W1s^T S + W1r^T R and the weight gradients of
@@ -249,15 +284,34 @@ __global__ void __launch_bounds__(NT) k_node_srcsum(int64_t N, const int32_t* __
     const int64_t r0 = t * TM;
     const int nr = (int)min((int64_t)TM, N - r0);
     {
-      const int c = tid & (D - 1), vg = tid >> 7;
-      for (int j = vg; j < TM; j += NT / D) {
-        float s = 0.f;
-        if (j < nr) {
-          const int v = (int)(r0 + j);
-          for (int e = rowptr[v]; e < rowptr[v + 1]; ++e) s += tof(zbar[(size_t)rev[e] * D + c]);
+      // 16 lanes per node, 8 features per lane; the node's reversed in-edges
+      // are gathered 8 at a time (independent loads) and added in edge order
+      const int j = tid >> 4, c8 = (tid & 15) * 8;
+      float acc8[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) acc8[u] = 0.f;
+      if (j < nr) {
+        const int v = (int)(r0 + j);
+        const int e1 = rowptr[v + 1];
+        for (int e = rowptr[v]; e < e1; e += 8) {
+          int rv[8];
+#pragma unroll
+          for (int k = 0; k < 8; ++k) rv[k] = e + k < e1 ? rev[e + k] : -1;
+          typename RowChunk<T>::V x[8];
+#pragma unroll
+          for (int k = 0; k < 8; ++k)
+            if (rv[k] >= 0) x[k] = RowChunk<T>::load(zbar + (size_t)rv[k] * D + c8);
+#pragma unroll
+          for (int k = 0; k < 8; ++k)
+            if (rv[k] >= 0) RowChunk<T>::add(acc8, x[k]);
         }
-        sSR[j * LDX + c] = P::cvt(s);
       }
+      T o[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) o[u] = P::cvt(acc8[u]);
+#pragma unroll
+      for (int u = 0; u < (int)(8 * sizeof(T)) / 16; ++u)
+        reinterpret_cast<uint4*>(sSR + j * LDX + c8)[u] = reinterpret_cast<const uint4*>(o)[u];
     }
     stage_rows(sSR + D, LDX, R + (size_t)r0 * D, nr, tid);
     stage_rows(sH, LDT, h + (size_t)r0 * D, nr, tid);

@@ -338,14 +338,17 @@ __device__ __forceinline__ void stage_rows(T* lds, int ld, const S* src, int nro
   for (int idx = tid; idx < TM * (D / 8); idx += NT) {
     const int row = idx >> 4, c = (idx & 15) * 8;
     T* dst = lds + row * ld + c;
+    float v[8];
     if (row < nrows) {
       const S* s = src + (size_t)row * D + c;
 #pragma unroll
-      for (int j = 0; j < 8; ++j) dst[j] = (T)tof(s[j]);
+      for (int j = 0; j < 8; ++j) v[j] = tof(s[j]);
     } else {
 #pragma unroll
-      for (int j = 0; j < 8; ++j) dst[j] = (T)0.f;
+      for (int j = 0; j < 8; ++j) v[j] = 0.f;
     }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) dst[j] = (T)v[j];
   }
 }
 
