@@ -464,14 +464,38 @@ __global__ void __launch_bounds__(NT) k_enc_bwd(int64_t M, const float* __restri
 }
 
 // ----------------------------------------------------------- reduce
+// grad[...] += sum over the nblocks partial rows.  A block takes 16
+// consecutive entries; its 16 lane groups each sum every 16th partial row
+// (group g: rows g, g+16, ...) in row order, 8 loads in flight, and the 16
+// group sums are added in group order: a fixed order for any launch.
+constexpr int kRedCols = 16, kRedGroups = 16;
 __global__ void __launch_bounds__(256) k_reduce(Partials part, int nblocks, int64_t src, int32_t rows, int32_t cols,
                                                 float* __restrict__ grad, int64_t dst, int64_t dst_ld) {
+  __shared__ float red[kRedGroups][kRedCols];
   const int64_t total = (int64_t)rows * cols;
-  for (int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x; idx < total; idx += (int64_t)gridDim.x * 256) {
-    float s = 0.f;
-    for (int b = 0; b < nblocks; ++b) s += part.buf[(size_t)b * part.stride + src + idx];
-    const int64_t r = idx / cols, c = idx % cols;
-    grad[dst + r * dst_ld + c] += s;
+  const int c = threadIdx.x % kRedCols, gr = threadIdx.x / kRedCols;
+  const int64_t idx = (int64_t)blockIdx.x * kRedCols + c;
+  float s = 0.f;
+  if (idx < total) {
+    const float* p = part.buf + src + idx;
+    int b = gr;
+    for (; b + 7 * kRedGroups < nblocks; b += 8 * kRedGroups) {
+      float v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = p[(size_t)(b + u * kRedGroups) * part.stride];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) s += v[u];
+    }
+    for (; b < nblocks; b += kRedGroups) s += p[(size_t)b * part.stride];
+  }
+  red[gr][c] = s;
+  __syncthreads();
+  if (gr == 0 && idx < total) {
+    float t = 0.f;
+#pragma unroll
+    for (int g = 0; g < kRedGroups; ++g) t += red[g][c];
+    const int64_t r = idx / cols, cc = idx % cols;
+    grad[dst + r * dst_ld + cc] += t;
   }
 }
 
@@ -558,8 +582,8 @@ hipError_t launch_reduce(const Partials& part, int nblocks, int64_t src, int32_t
                          int64_t dst, int64_t dst_ld, hipStream_t s) {
   if (nblocks <= 0 || rows <= 0 || cols <= 0) return hipSuccess;
   const int64_t total = (int64_t)rows * cols;
-  const int g = (int)std::min<int64_t>((total + 255) / 256, 2048);
-  hipLaunchKernelGGL(k_reduce, dim3(g), dim3(256), 0, s, part, nblocks, src, rows, cols, grad, dst, dst_ld);
+  const int64_t g = (total + kRedCols - 1) / kRedCols;
+  hipLaunchKernelGGL(k_reduce, dim3((unsigned)g), dim3(256), 0, s, part, nblocks, src, rows, cols, grad, dst, dst_ld);
   return hipGetLastError();
 }
 

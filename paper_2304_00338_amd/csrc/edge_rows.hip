@@ -421,27 +421,196 @@ k_edge_bwd_rows(EdgeTiles tl, const bf16* __restrict__ a1_in, const float* __res
     r.w = ok ? v.w : 0;
     return r;
   };
-  auto issue_a1 = [&](int4 d, uint4 (&A)[2][4]) {
+  // The streamed inputs of one 16-row half of a tile for this lane's row:
+  // a1 and the incoming edge gradient, in the C layout (features 32q + 4ob
+  // + r).  The next half's streams are in flight while a half is computed;
+  // the receiver's aggregate gradient (shared by the ~14 consecutive rows of
+  // a receiver, so mostly a cache hit) is loaded when the half starts.
+  struct HalfLoads {
+    uint4 a[4];
+    f32x4 eb[8];
+  };
+  auto load_recv = [&](int4 d, int (&rv)[2]) {
+    const int n = tile_rows(d);
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb) rv[rb] = n > 0 ? tl.receivers[d.z + min(rb * 16 + i, n - 1)] : 0;
+  };
+  auto load_half = [&](int4 d, int rb, HalfLoads& H) {
     const int n = tile_rows(d);
     if (n <= 0) return;
+    const size_t row = (size_t)d.z + min(rb * 16 + i, n - 1);
+    const bf16* ap = a1_in + row * D + 32 * q;
 #pragma unroll
-    for (int rb = 0; rb < 2; ++rb) {
-      const int rc = min(rb * 16 + i, n - 1);
-      const bf16* ap = a1_in + ((size_t)d.z + rc) * D + 32 * q;
+    for (int k = 0; k < 4; ++k) H.a[k] = *reinterpret_cast<const uint4*>(ap + 8 * k);
+    if (have_ebar) {
+      const float* ep = ebar_in + row * D + 32 * q;
 #pragma unroll
-      for (int k = 0; k < 4; ++k) A[rb][k] = *reinterpret_cast<const uint4*>(ap + 8 * k);
+      for (int ob = 0; ob < 8; ++ob) H.eb[ob] = *reinterpret_cast<const f32x4*>(ep + 4 * ob);
+    } else {
+#pragma unroll
+      for (int ob = 0; ob < 8; ++ob) H.eb[ob] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
   };
 
   float2 db1 = {0.f, 0.f}, dga = {0.f, 0.f}, dbe = {0.f, 0.f};
   float* stage = S.stage[wv];
+  float* srow = stage + i * RW_LDM + 32 * q;
+
+  // One half (rows rb*16 .. +16) of tile d0 with its streams in H.
+  auto half = [&](HalfLoads& H, int4 d0, int rb, int recv, int segv, int nv, int& j, float2& carry) {
+    const int n = tile_rows(d0);
+    const int row = rb * 16 + i;
+    const int nh = max(0, min(16, n - rb * 16));  // valid rows of this half
+    f32x4 ag[8];
+    {
+      const float* gp = aggbar + (size_t)recv * D + 32 * q;
+#pragma unroll
+      for (int ob = 0; ob < 8; ++ob)
+        ag[ob] = n > 0 ? *reinterpret_cast<const f32x4*>(gp + 4 * ob) : f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+    // ---- z2 = b2 + W2 a1 and its LayerNorm statistics
+    f32x4 acc[8];
+#pragma unroll
+    for (int ob = 0; ob < 8; ++ob) acc[ob] = *reinterpret_cast<const f32x4*>(S.b2 + 32 * q + 4 * ob);
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+#pragma unroll
+      for (int ob = 0; ob < 8; ++ob) {
+        const bf16x8 a = *reinterpret_cast<const bf16x8*>(S.W2 + (ob * 16 + i) * RW_LDW + 32 * q + 8 * s);
+        acc[ob] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, as_frag(H.a[s]), acc[ob], 0, 0, 0);
+      }
+    }
+    float sm = 0.f;
+#pragma unroll
+    for (int ob = 0; ob < 8; ++ob)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) sm += acc[ob][r];
+    const float mean = sum_rowlanes(sm) * (1.0f / D);
+    float sq = 0.f;
+#pragma unroll
+    for (int ob = 0; ob < 8; ++ob) {
+      acc[ob] -= mean;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) sq += acc[ob][r] * acc[ob][r];
+    }
+    const float rstd = __builtin_amdgcn_rsqf(sum_rowlanes(sq) * (1.0f / D) + eps);
+#pragma unroll
+    for (int ob = 0; ob < 8; ++ob) {
+      acc[ob] *= rstd;          // xhat
+      ag[ob] += H.eb[ob];     // mbar = ebar_in + aggbar[receiver]
+    }
+    // ---- dgamma += sum_rows mbar * xhat, dbeta += sum_rows mbar
+#pragma unroll
+    for (int ob = 0; ob < 8; ++ob) *reinterpret_cast<f32x4*>(srow + 4 * ob) = ag[ob] * acc[ob];
+    wave_lds_sync();
+    {
+      const float2 c = col_pass(stage, lane, nh);
+      dga.x += c.x;
+      dga.y += c.y;
+    }
+    wave_lds_sync();
+#pragma unroll
+    for (int ob = 0; ob < 8; ++ob) *reinterpret_cast<f32x4*>(srow + 4 * ob) = ag[ob];
+    wave_lds_sync();
+    {
+      const float2 c = col_pass(stage, lane, nh);
+      dbe.x += c.x;
+      dbe.y += c.y;
+    }
+    // ---- LayerNorm backward: dz2 = rstd (dxh - mean(dxh) - xhat mean(dxh xhat)), dxh = mbar gamma
+    float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+    for (int ob = 0; ob < 8; ++ob) {
+      ag[ob] *= *reinterpret_cast<const f32x4*>(S.g + 32 * q + 4 * ob);  // dxh
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        s1 += ag[ob][r];
+        s2 += ag[ob][r] * acc[ob][r];
+      }
+    }
+    const float m1 = sum_rowlanes(s1) * (1.0f / D), m2 = sum_rowlanes(s2) * (1.0f / D);
+    bf16x8 dzf[4];
+#pragma unroll
+    for (int s = 0; s < 4; ++s)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        dzf[s][r] = (bf16)(rstd * (ag[2 * s][r] - m1 - acc[2 * s][r] * m2));
+        dzf[s][4 + r] = (bf16)(rstd * (ag[2 * s + 1][r] - m1 - acc[2 * s + 1][r] * m2));
+      }
+    if (row < n) {
+      bf16* dp = dz_out + ((size_t)d0.z + row) * D + 32 * q;
+#pragma unroll
+      for (int s = 0; s < 4; ++s) *reinterpret_cast<uint4*>(dp + 8 * s) = __builtin_bit_cast(uint4, dzf[s]);
+    }
+    // ---- da1 = W2^T dz2, zbar = da1 where a1 > 0
+#pragma unroll
+    for (int ob = 0; ob < 8; ++ob) acc[ob] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+#pragma unroll
+      for (int ob = 0; ob < 8; ++ob)
+        acc[ob] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wt_frag(S.W2, ob, s, i, q), dzf[s], acc[ob], 0, 0, 0);
+    }
+    bf16x8 zf[4];
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      const bf16x8 a = as_frag(H.a[s]);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        zf[s][r] = (float)a[r] > 0.f ? (bf16)acc[2 * s][r] : (bf16)0.f;
+        zf[s][4 + r] = (float)a[4 + r] > 0.f ? (bf16)acc[2 * s + 1][r] : (bf16)0.f;
+      }
+    }
+    if (row < n) {
+      bf16* zp = zbar + ((size_t)d0.z + row) * D + 32 * q;
+#pragma unroll
+      for (int s = 0; s < 4; ++s) *reinterpret_cast<uint4*>(zp + 8 * s) = __builtin_bit_cast(uint4, zf[s]);
+    }
+    // ---- per-receiver sums of zbar (as stored) and db1
+    wave_lds_sync();
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      f32x4 lo, hi;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        lo[r] = (float)zf[s][r];
+        hi[r] = (float)zf[s][4 + r];
+      }
+      *reinterpret_cast<f32x4*>(srow + 8 * s) = lo;
+      *reinterpret_cast<f32x4*>(srow + 8 * s + 4) = hi;
+    }
+    wave_lds_sync();
+    seg_pass(stage, lane, segv, nv, rb * 16, j, carry, [&](int jj, float2 v) {
+      float* dst = d0.y >= 0 ? R + (size_t)(d0.x + jj) * D : slots + (size_t)(-1 - d0.y) * D;
+      *reinterpret_cast<float2*>(dst + 2 * lane) = v;
+      db1.x += v.x;
+      db1.y += v.y;
+    });
+    // ---- ebar_out = ebar_in + W1e^T zbar
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+#pragma unroll
+      for (int ob = 0; ob < 8; ++ob)
+        H.eb[ob] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wt_frag(S.W1, ob, s, i, q), zf[s], H.eb[ob], 0, 0, 0);
+    }
+    if (row < n) {
+      float* op = ebar_out + ((size_t)d0.z + row) * D + 32 * q;
+#pragma unroll
+      for (int ob = 0; ob < 8; ++ob) *reinterpret_cast<f32x4*>(op + 4 * ob) = H.eb[ob];
+    }
+    wave_lds_sync();
+  };
+
   if (t < tend) {
     int4 d0 = desc(t), d1 = desc(t + stride);
-    uint4 cur[2][4];
-    issue_a1(d0, cur);
+    int rc0[2], rn[2];
+    load_recv(d0, rc0);
+    HalfLoads A, B;
+    load_half(d0, 0, A);
     for (; t < tend; t += stride) {
       const int n = tile_rows(d0);
       const int4 d2 = desc(t + 2 * stride);
+      load_recv(d1, rn);
       const int nv = d0.y >= 0 ? d0.y - d0.x : 1;
       int segv = 0;
       if (d0.y >= 0) {
@@ -449,166 +618,16 @@ k_edge_bwd_rows(EdgeTiles tl, const bf16* __restrict__ a1_in, const float* __res
       } else {
         segv = lane == 0 ? 0 : n;
       }
-      int recv[2];
-#pragma unroll
-      for (int rb = 0; rb < 2; ++rb) recv[rb] = rb * 16 + i < n ? tl.receivers[d0.z + rb * 16 + i] : 0;
-      uint4 nxt[2][4];
-      if (t + stride < tend) issue_a1(d1, nxt);
-
       float2 carry = {0.f, 0.f};
       int j = 0;
-#pragma unroll
-      for (int rb = 0; rb < 2; ++rb) {
-        const int row = rb * 16 + i;
-        const int rc = max(0, min(row, n - 1));
-        const int nh = max(0, min(16, n - rb * 16));  // valid rows of this half
-        // ---- incoming gradients of this half (C layout: features 32q + 4ob + r)
-        f32x4 eb[8], g[8];
-        {
-          const float* ep = ebar_in + ((size_t)d0.z + rc) * D + 32 * q;
-          const float* ap = aggbar + (size_t)recv[rb] * D + 32 * q;
-#pragma unroll
-          for (int ob = 0; ob < 8; ++ob) {
-            eb[ob] = (have_ebar && n > 0) ? *reinterpret_cast<const f32x4*>(ep + 4 * ob) : f32x4{0.f, 0.f, 0.f, 0.f};
-            g[ob] = n > 0 ? *reinterpret_cast<const f32x4*>(ap + 4 * ob) : f32x4{0.f, 0.f, 0.f, 0.f};
-          }
-        }
-        // ---- z2 = b2 + W2 a1 and its LayerNorm statistics
-        f32x4 acc[8];
-#pragma unroll
-        for (int ob = 0; ob < 8; ++ob) acc[ob] = *reinterpret_cast<const f32x4*>(S.b2 + 32 * q + 4 * ob);
-#pragma unroll
-        for (int s = 0; s < 4; ++s)
-#pragma unroll
-          for (int ob = 0; ob < 8; ++ob) {
-            const bf16x8 a = *reinterpret_cast<const bf16x8*>(S.W2 + (ob * 16 + i) * RW_LDW + 32 * q + 8 * s);
-            acc[ob] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, as_frag(cur[rb][s]), acc[ob], 0, 0, 0);
-          }
-        float sm = 0.f;
-#pragma unroll
-        for (int ob = 0; ob < 8; ++ob)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) sm += acc[ob][r];
-        const float mean = sum_rowlanes(sm) * (1.0f / D);
-        float sq = 0.f;
-#pragma unroll
-        for (int ob = 0; ob < 8; ++ob) {
-          acc[ob] -= mean;
-#pragma unroll
-          for (int r = 0; r < 4; ++r) sq += acc[ob][r] * acc[ob][r];
-        }
-        const float rstd = __builtin_amdgcn_rsqf(sum_rowlanes(sq) * (1.0f / D) + eps);
-#pragma unroll
-        for (int ob = 0; ob < 8; ++ob) {
-          acc[ob] *= rstd;     // xhat
-          g[ob] += eb[ob];     // mbar = ebar_in + aggbar[receiver]
-        }
-        // ---- dgamma += sum_rows mbar * xhat, dbeta += sum_rows mbar
-        float* srow = stage + i * RW_LDM + 32 * q;
-#pragma unroll
-        for (int ob = 0; ob < 8; ++ob) *reinterpret_cast<f32x4*>(srow + 4 * ob) = g[ob] * acc[ob];
-        wave_lds_sync();
-        {
-          const float2 c = col_pass(stage, lane, nh);
-          dga.x += c.x;
-          dga.y += c.y;
-        }
-        wave_lds_sync();
-#pragma unroll
-        for (int ob = 0; ob < 8; ++ob) *reinterpret_cast<f32x4*>(srow + 4 * ob) = g[ob];
-        wave_lds_sync();
-        {
-          const float2 c = col_pass(stage, lane, nh);
-          dbe.x += c.x;
-          dbe.y += c.y;
-        }
-        // ---- LayerNorm backward: dz2 = rstd (dxh - mean(dxh) - xhat mean(dxh xhat)), dxh = mbar gamma
-        float s1 = 0.f, s2 = 0.f;
-#pragma unroll
-        for (int ob = 0; ob < 8; ++ob) {
-          g[ob] *= *reinterpret_cast<const f32x4*>(S.g + 32 * q + 4 * ob);  // dxh
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            s1 += g[ob][r];
-            s2 += g[ob][r] * acc[ob][r];
-          }
-        }
-        const float m1 = sum_rowlanes(s1) * (1.0f / D), m2 = sum_rowlanes(s2) * (1.0f / D);
-        bf16x8 dzf[4];
-#pragma unroll
-        for (int s = 0; s < 4; ++s)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            dzf[s][r] = (bf16)(rstd * (g[2 * s][r] - m1 - acc[2 * s][r] * m2));
-            dzf[s][4 + r] = (bf16)(rstd * (g[2 * s + 1][r] - m1 - acc[2 * s + 1][r] * m2));
-          }
-        if (row < n) {
-          bf16* dp = dz_out + ((size_t)d0.z + row) * D + 32 * q;
-#pragma unroll
-          for (int s = 0; s < 4; ++s) *reinterpret_cast<uint4*>(dp + 8 * s) = __builtin_bit_cast(uint4, dzf[s]);
-        }
-        // ---- da1 = W2^T dz2, zbar = da1 where a1 > 0
-#pragma unroll
-        for (int ob = 0; ob < 8; ++ob) acc[ob] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int s = 0; s < 4; ++s)
-#pragma unroll
-          for (int ob = 0; ob < 8; ++ob)
-            acc[ob] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wt_frag(S.W2, ob, s, i, q), dzf[s], acc[ob], 0, 0, 0);
-        bf16x8 zf[4];
-#pragma unroll
-        for (int s = 0; s < 4; ++s) {
-          const bf16x8 a = as_frag(cur[rb][s]);
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            zf[s][r] = (float)a[r] > 0.f ? (bf16)acc[2 * s][r] : (bf16)0.f;
-            zf[s][4 + r] = (float)a[4 + r] > 0.f ? (bf16)acc[2 * s + 1][r] : (bf16)0.f;
-          }
-        }
-        if (row < n) {
-          bf16* zp = zbar + ((size_t)d0.z + row) * D + 32 * q;
-#pragma unroll
-          for (int s = 0; s < 4; ++s) *reinterpret_cast<uint4*>(zp + 8 * s) = __builtin_bit_cast(uint4, zf[s]);
-        }
-        // ---- per-receiver sums of zbar (as stored) and db1
-        wave_lds_sync();
-#pragma unroll
-        for (int s = 0; s < 4; ++s) {
-          f32x4 lo, hi;
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            lo[r] = (float)zf[s][r];
-            hi[r] = (float)zf[s][4 + r];
-          }
-          *reinterpret_cast<f32x4*>(srow + 8 * s) = lo;
-          *reinterpret_cast<f32x4*>(srow + 8 * s + 4) = hi;
-        }
-        wave_lds_sync();
-        seg_pass(stage, lane, segv, nv, rb * 16, j, carry, [&](int jj, float2 v) {
-          float* dst = d0.y >= 0 ? R + (size_t)(d0.x + jj) * D : slots + (size_t)(-1 - d0.y) * D;
-          *reinterpret_cast<float2*>(dst + 2 * lane) = v;
-          db1.x += v.x;
-          db1.y += v.y;
-        });
-        // ---- ebar_out = ebar_in + W1e^T zbar
-#pragma unroll
-        for (int s = 0; s < 4; ++s)
-#pragma unroll
-          for (int ob = 0; ob < 8; ++ob)
-            eb[ob] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wt_frag(S.W1, ob, s, i, q), zf[s], eb[ob], 0, 0, 0);
-        if (row < n) {
-          float* op = ebar_out + ((size_t)d0.z + row) * D + 32 * q;
-#pragma unroll
-          for (int ob = 0; ob < 8; ++ob) *reinterpret_cast<f32x4*>(op + 4 * ob) = eb[ob];
-        }
-        wave_lds_sync();
-      }
-#pragma unroll
-      for (int rb = 0; rb < 2; ++rb)
-#pragma unroll
-        for (int k = 0; k < 4; ++k) cur[rb][k] = nxt[rb][k];
+      load_half(d0, 1, B);
+      half(A, d0, 0, rc0[0], segv, nv, j, carry);
+      if (t + stride < tend) load_half(d1, 0, A);
+      half(B, d0, 1, rc0[1], segv, nv, j, carry);
       d0 = d1;
       d1 = d2;
+      rc0[0] = rn[0];
+      rc0[1] = rn[1];
     }
   }
   // ---- block partials: the 8 waves' column sums in wave order
