@@ -371,6 +371,7 @@ struct Run {
     t.rowptr = g.rowptr;
     t.senders = g.senders;
     t.receivers = g.receivers;
+    t.n_edges = g.n_edges;
     return t;
   }
   Partials part() const {
@@ -403,8 +404,11 @@ struct Run {
     for (int l = 0; l < m; ++l) {
       const bool last = l == m - 1;
       void* e_out = c.save ? (last ? nullptr : e_l(k, l + 1)) : e_l(k, 0);
-      LAUNCH(K_EDGE_FWD, launch_edge_fwd(prec, tl, e_l(k, l), e_out, last ? 0 : 1, P_l(k, l), W(M.edge[l], M.p_edge[l]), eps,
-                              agg_l(k, l), slots(), a1_l(k, l), s));
+      if (E > 0)
+        LAUNCH(K_EDGE_FWD, launch_edge_fwd(prec, tl, e_l(k, l), e_out, last ? 0 : 1, P_l(k, l), W(M.edge[l], M.p_edge[l]),
+                                eps, agg_l(k, l), slots(), a1_l(k, l), s));
+      else
+        LAUNCH(K_EDGE_FWD, launch_fill(agg_l(k, l), N * D, 0.f, s));  // no edges: every aggregate is zero
       if (g.n_long > 0) LAUNCH(K_FIXUP, launch_slot_fixup(g.long_nodes, g.n_long, slots(), agg_l(k, l), s));
       MlpW nx;
       if (!last) nx = W(M.edge[l + 1], M.p_edge[l + 1]);
@@ -439,7 +443,10 @@ struct Run {
       LAUNCH(K_NODE_BWD, launch_node_bwd(prec, N, h_l(k, l), agg_l(k, l), hb_cur, W(on, M.p_node[l]), eps, hb_part, aggbar, pt,
                               &nb, s));
       if ((rc = reduce(nb, 0, 1, (int)on.size, grad, on.W1, 0)) != MGN_OK) return rc;
-      if (prec == MGN_BF16) {
+      if (E == 0) {
+        // no edges: the edge MLP gets no gradient and every R is zero
+        LAUNCH(K_EDGE_BWD, launch_fill(R, N * D, 0.f, s));
+      } else if (prec == MGN_BF16) {
         void* dz = ws + c.L.dz;
         LAUNCH(K_EDGE_BWD, launch_edge_bwd_rows(tl, a1_l(k, l), ebar, l < m - 1 ? 1 : 0, ebar, aggbar, W(oe, M.p_edge[l]),
                                     eps, zbar, dz, R, slots(), pt, &nb, s));

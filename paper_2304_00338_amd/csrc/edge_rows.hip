@@ -6,14 +6,16 @@
 // Work split.  Each of the 8 waves of a block runs its own persistent loop
 // over tiles; the only block barrier is the one after the weights are
 // staged in LDS.  Lane l (i = l & 15, q = l >> 4) holds rows i and 16 + i of
-// the wave's tile and the 32 contiguous features [32q, 32q + 32) of each
-// row.  The GEMMs run transposed (C[feature][row] = W x^T): the A operand is
-// a 16-row block of the row-permuted weights (perm_row) read from LDS, the B
-// operand is the lane's own 8-feature runs of x, and the C fragment of
-// output block ob gives the lane features 32q + 4ob + r.  So GEMM outputs
-// are already the next GEMM's B operand, and every LayerNorm statistic is a
-// sum over the lane's 32 values plus two cross-lane steps (the four lanes
-// that share a row).
+// the wave's tile and 32 features of each: the runs [32s + 8q, 32s + 8q + 8)
+// for s < 4, so the four lanes of a row read or write 64 contiguous bytes
+// (bf16) per instruction.  The GEMMs run transposed (C[feature][row] =
+// W x^T): the A operand is a 16-row block of the row-permuted weights
+// (perm_row) read from LDS, the B operand at K step s is the lane's run s of
+// x, and the C fragment of output block ob gives the lane the features
+// fo(ob, q) + r, r < 4, which are again its runs.  So GEMM outputs are
+// already the next GEMM's B operand, and every LayerNorm statistic is a sum
+// over the lane's 32 values plus two cross-lane steps (the four lanes that
+// share a row).
 //
 // Adds of bf16 inputs into fp32 accumulators (the node products P_s + P_r
 // and the residual e + m) are MFMAs with a 0/1 selection operand: one
@@ -28,12 +30,21 @@
 namespace mgn {
 namespace dev {
 
-constexpr int RW_LDW = D + 8;  // LDS row stride of the staged weights (bf16)
 constexpr int RW_LDM = D + 4;  // LDS row stride of a wave's message half-tile (fp32)
 
+// First feature of the 4-feature run of output block ob held by lane group q.
+__device__ __forceinline__ int fo(int ob, int q) { return 32 * (ob >> 1) + 8 * q + 4 * (ob & 1); }
+
+// The staged [128][128] bf16 weights keep rows unpadded and XOR-swizzle the
+// 16-byte chunks of row R, so that both the row reads of A fragments (8
+// lanes: 8 consecutive rows, one chunk) and the transposing reads (16 lanes:
+// 4 consecutive rows x 4 chunks) hit distinct banks.
+__device__ __forceinline__ int wswz(int R) { return 4 * (R & 3) + ((R >> 2) & 3); }
+__device__ __forceinline__ const bf16* wchunk(const bf16* W, int R, int C) { return W + R * D + ((C ^ wswz(R)) << 3); }
+
 struct __attribute__((aligned(16))) RowsLds {
-  __attribute__((aligned(16))) bf16 W1[D * RW_LDW];
-  __attribute__((aligned(16))) bf16 W2[D * RW_LDW];
+  __attribute__((aligned(16))) bf16 W1[D * D];
+  __attribute__((aligned(16))) bf16 W2[D * D];
   __attribute__((aligned(16))) float b1[D];
   __attribute__((aligned(16))) float b2[D];
   __attribute__((aligned(16))) float g[D];
@@ -43,8 +54,9 @@ struct __attribute__((aligned(16))) RowsLds {
 
 typedef __attribute__((ext_vector_type(4))) unsigned int u32x4;
 
-// The 0/1 operand that adds a B fragment (features 32q + 8s + j) into the C
-// fragment of output block ob = 2s + h: A[m][k] = 1 iff k = (m/4)*8 + 4h + m%4.
+// The 0/1 operand that adds a B fragment (run s: features 32s + 8q + j) into
+// the C fragment of output block ob = 2s + h: A[m][k] = 1 iff k = (m/4)*8 +
+// 4h + m%4.
 __device__ __forceinline__ bf16x8 select_frag(int h, int i, int q) {
   bf16x8 a;
 #pragma unroll
@@ -54,8 +66,9 @@ __device__ __forceinline__ bf16x8 select_frag(int h, int i, int q) {
 
 __device__ __forceinline__ bf16x8 as_frag(const uint4& u) { return __builtin_bit_cast(bf16x8, u); }
 
-// The streams of one tile row pair a lane needs: its 32-feature run of the
-// edge latent and of the two gathered node products, for rows i and 16 + i.
+// The streams of one tile row pair a lane needs: its four 8-feature runs of
+// the edge latent and of the two gathered node products, for rows i and
+// 16 + i.
 struct RowLoads {
   uint4 e[2][4], ps[2][4], pr[2][4];
 };
@@ -78,17 +91,19 @@ __device__ __forceinline__ float sum_rowlanes(float s) {
 }
 
 // In-segment node sums over one staged 16-row half [lo_row, lo_row + 16) of
-// a tile (rows past the tile's end are never inside a segment).  Node j's
-// rows are [seg(j), seg(j+1)) with seg held by lane j of segv; j is the
-// first node whose sum is still open and carry its partial sum (features
-// 2*lane, 2*lane+1), added in ascending row order.  close(j, sum) is called
-// for every node whose segment ends inside this half.
+// a tile (rows past the tile's end are never inside a segment).  For a tile
+// of whole segments node j's rows are [rp(j) - base, rp(j+1) - base) with
+// rp(j) held by lane j of segraw; a chunk tile (chunk) is the single segment
+// [0, n).  j is the first node whose sum is still open and carry its partial
+// sum (features 2*lane, 2*lane+1), added in ascending row order; close(j,
+// sum) is called for every node whose segment ends inside this half.
 template <class F>
-__device__ __forceinline__ void seg_pass(const float* stage, int lane, int segv, int nv, int lo_row, int& j,
-                                         float2& carry, F&& close) {
+__device__ __forceinline__ void seg_pass(const float* stage, int lane, int segraw, int base, bool chunk, int n,
+                                         int nv, int lo_row, int& j, float2& carry, F&& close) {
   const int hi_row = lo_row + 16;
   while (j < nv) {
-    const int a = __builtin_amdgcn_readlane(segv, j), b = __builtin_amdgcn_readlane(segv, j + 1);
+    const int a = chunk ? 0 : __builtin_amdgcn_readlane(segraw, j) - base;
+    const int b = chunk ? n : __builtin_amdgcn_readlane(segraw, j + 1) - base;
     const int u0 = max(a, lo_row), u1 = min(b, hi_row);
     for (int u = u0; u < u1; ++u) {
       const float2 v = *reinterpret_cast<const float2*>(stage + (u - lo_row) * RW_LDM + 2 * lane);
@@ -125,8 +140,9 @@ k_edge_fwd_rows(EdgeTiles tl, const bf16* __restrict__ e_in, bf16* __restrict__ 
     const bf16* W2p = (const bf16*)w.W2p;
     for (int idx = tid; idx < D * D / 8; idx += NT) {
       const int row = idx >> 4, c = (idx & 15) * 8;
-      *reinterpret_cast<uint4*>(S.W1 + row * RW_LDW + c) = *reinterpret_cast<const uint4*>(W1p + row * D + c);
-      *reinterpret_cast<uint4*>(S.W2 + row * RW_LDW + c) = *reinterpret_cast<const uint4*>(W2p + row * D + c);
+      const int cs = ((idx & 15) ^ wswz(row)) << 3;
+      *reinterpret_cast<uint4*>(S.W1 + row * D + cs) = *reinterpret_cast<const uint4*>(W1p + row * D + c);
+      *reinterpret_cast<uint4*>(S.W2 + row * D + cs) = *reinterpret_cast<const uint4*>(W2p + row * D + c);
     }
     if (tid < D) {
       S.b1[tid] = w.b1[tid];
@@ -169,33 +185,31 @@ k_edge_fwd_rows(EdgeTiles tl, const bf16* __restrict__ e_in, bf16* __restrict__ 
     r.w = ok ? v.w : 0;
     return r;
   };
-  // sender / receiver of rows i and 16 + i of a tile (0 past its end)
+  // Every global load below is unconditional, from an index clamped into
+  // its array (so the compiler's in-order wait counts stay exact and a wait
+  // never covers a later prefetch): rows past a tile's end, and the tiles
+  // of edge-less nodes, read a valid row whose values are never stored or
+  // summed (rows never mix inside the products or the LayerNorm).
+  const int lastE = (int)max(tl.n_edges - 1, (int64_t)0);
+  auto erow = [&](int4 d, int rb) { return min(max(d.z + min(rb * 16 + i, tile_rows(d) - 1), 0), lastE); };
   auto load_sr = [&](int4 d, int (&s)[2], int (&r)[2]) {
-    const int n = tile_rows(d);
 #pragma unroll
     for (int rb = 0; rb < 2; ++rb) {
-      const int row = rb * 16 + i;
-      s[rb] = row < n ? tl.senders[d.z + row] : 0;
-      r[rb] = row < n ? tl.receivers[d.z + row] : 0;
+      s[rb] = tl.senders[erow(d, rb)];
+      r[rb] = tl.receivers[erow(d, rb)];
     }
   };
-  // Rows past the tile's end load a copy of its last edge row and node 0's
-  // products: rows never mix inside the products or the LayerNorm, and such
-  // rows are neither stored nor summed.
   auto issue = [&](int4 d, const int (&s)[2], const int (&r)[2], RowLoads& L) {
-    const int n = tile_rows(d);
-    if (n <= 0) return;  // a tile of edge-less nodes: nothing to load
 #pragma unroll
     for (int rb = 0; rb < 2; ++rb) {
-      const int rc = max(0, min(rb * 16 + i, n - 1));
-      const bf16* ep = e_in + ((size_t)d.z + rc) * D + 32 * q;
-      const bf16* sp = Pn + (size_t)s[rb] * (2 * D) + 32 * q;
-      const bf16* rp = Pn + (size_t)r[rb] * (2 * D) + D + 32 * q;
+      const bf16* ep = e_in + (size_t)erow(d, rb) * D + 8 * q;
+      const bf16* sp = Pn + (size_t)s[rb] * (2 * D) + 8 * q;
+      const bf16* rp = Pn + (size_t)r[rb] * (2 * D) + D + 8 * q;
 #pragma unroll
       for (int k = 0; k < 4; ++k) {
-        L.e[rb][k] = *reinterpret_cast<const uint4*>(ep + 8 * k);
-        L.ps[rb][k] = *reinterpret_cast<const uint4*>(sp + 8 * k);
-        L.pr[rb][k] = *reinterpret_cast<const uint4*>(rp + 8 * k);
+        L.e[rb][k] = *reinterpret_cast<const uint4*>(ep + 32 * k);
+        L.ps[rb][k] = *reinterpret_cast<const uint4*>(sp + 32 * k);
+        L.pr[rb][k] = *reinterpret_cast<const uint4*>(rp + 32 * k);
       }
     }
   };
@@ -210,20 +224,15 @@ k_edge_fwd_rows(EdgeTiles tl, const bf16* __restrict__ e_in, bf16* __restrict__ 
 
   for (; t < tend; t += stride) {
     const int n = tile_rows(d0);
+    // in-segment starts of the tile's nodes (lane j: rowptr of node j)
+    const bool chunk = d0.y < 0;
+    const int nv = chunk ? 1 : d0.y - d0.x;
+    const int segraw = tl.rowptr[min(d0.x + lane, max(d0.x, d0.y))];
     const int4 d3 = desc(t + 3 * stride);
     int s2[2], r2[2];
     load_sr(d2, s2, r2);
-    // in-segment starts of the tile's nodes (lane j holds the start of node j)
-    const int nv = d0.y >= 0 ? d0.y - d0.x : 1;
-    int segv = 0;
-    if (d0.y >= 0) {
-      if (lane <= nv) segv = tl.rowptr[d0.x + lane] - d0.z;
-    } else {
-      segv = lane == 0 ? 0 : n;
-    }
 
     RowLoads nxt;
-    bool issued = false;
     float2 carry = {0.f, 0.f};
     int j = 0;  // next node whose sum is open
 #pragma unroll
@@ -232,21 +241,17 @@ k_edge_fwd_rows(EdgeTiles tl, const bf16* __restrict__ e_in, bf16* __restrict__ 
       f32x4 acc[8];
 #pragma unroll
       for (int ob = 0; ob < 8; ++ob) {
-        acc[ob] = *reinterpret_cast<const f32x4*>(S.b1 + 32 * q + 4 * ob);
+        acc[ob] = *reinterpret_cast<const f32x4*>(S.b1 + fo(ob, q));
         const bf16x8 sel = (ob & 1) ? sel1 : sel0;
         acc[ob] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sel, as_frag(cur.ps[rb][ob >> 1]), acc[ob], 0, 0, 0);
         acc[ob] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sel, as_frag(cur.pr[rb][ob >> 1]), acc[ob], 0, 0, 0);
       }
-      if (rb == 1 && t + stride < tend) {
-        // the node products of this tile are consumed: put the next tile in flight
-        issue(d1, s1, r1, nxt);
-        issued = true;
-      }
+      if (rb == 1) issue(d1, s1, r1, nxt);  // node products consumed: next tile in flight
 #pragma unroll
       for (int s = 0; s < 4; ++s)
 #pragma unroll
         for (int ob = 0; ob < 8; ++ob) {
-          const bf16x8 a = *reinterpret_cast<const bf16x8*>(S.W1 + (ob * 16 + i) * RW_LDW + 32 * q + 8 * s);
+          const bf16x8 a = *reinterpret_cast<const bf16x8*>(wchunk(S.W1, ob * 16 + i, 4 * s + q));
           acc[ob] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, as_frag(cur.e[rb][s]), acc[ob], 0, 0, 0);
         }
       // ---- a1 = relu(z1) as the B operand of the second layer
@@ -259,18 +264,18 @@ k_edge_fwd_rows(EdgeTiles tl, const bf16* __restrict__ e_in, bf16* __restrict__ 
           a1[s][4 + r] = (bf16)relu(acc[2 * s + 1][r]);
         }
       if (a1_out != nullptr && rb * 16 + i < n) {
-        bf16* ap = a1_out + ((size_t)d0.z + rb * 16 + i) * D + 32 * q;
+        bf16* ap = a1_out + ((size_t)d0.z + rb * 16 + i) * D + 8 * q;
 #pragma unroll
-        for (int s = 0; s < 4; ++s) *reinterpret_cast<uint4*>(ap + 8 * s) = __builtin_bit_cast(uint4, a1[s]);
+        for (int s = 0; s < 4; ++s) *reinterpret_cast<uint4*>(ap + 32 * s) = __builtin_bit_cast(uint4, a1[s]);
       }
       // ---- z2 = b2 + W2 a1
 #pragma unroll
-      for (int ob = 0; ob < 8; ++ob) acc[ob] = *reinterpret_cast<const f32x4*>(S.b2 + 32 * q + 4 * ob);
+      for (int ob = 0; ob < 8; ++ob) acc[ob] = *reinterpret_cast<const f32x4*>(S.b2 + fo(ob, q));
 #pragma unroll
       for (int s = 0; s < 4; ++s)
 #pragma unroll
         for (int ob = 0; ob < 8; ++ob) {
-          const bf16x8 a = *reinterpret_cast<const bf16x8*>(S.W2 + (ob * 16 + i) * RW_LDW + 32 * q + 8 * s);
+          const bf16x8 a = *reinterpret_cast<const bf16x8*>(wchunk(S.W2, ob * 16 + i, 4 * s + q));
           acc[ob] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, a1[s], acc[ob], 0, 0, 0);
         }
       // ---- LayerNorm over the row's 128 features (4 lanes x 32)
@@ -288,13 +293,13 @@ k_edge_fwd_rows(EdgeTiles tl, const bf16* __restrict__ e_in, bf16* __restrict__ 
         for (int r = 0; r < 4; ++r) sq += acc[ob][r] * acc[ob][r];
       }
       const float rstd = __builtin_amdgcn_rsqf(sum_rowlanes(sq) * (1.0f / D) + eps);
-      float* srow = stage + i * RW_LDM + 32 * q;
+      float* srow = stage + i * RW_LDM;
 #pragma unroll
       for (int ob = 0; ob < 8; ++ob) {
-        const f32x4 ga = *reinterpret_cast<const f32x4*>(S.g + 32 * q + 4 * ob);
-        const f32x4 be = *reinterpret_cast<const f32x4*>(S.bt + 32 * q + 4 * ob);
+        const f32x4 ga = *reinterpret_cast<const f32x4*>(S.g + fo(ob, q));
+        const f32x4 be = *reinterpret_cast<const f32x4*>(S.bt + fo(ob, q));
         acc[ob] = ga * (acc[ob] * rstd) + be;  // message m
-        *reinterpret_cast<f32x4*>(srow + 4 * ob) = acc[ob];
+        *reinterpret_cast<f32x4*>(srow + fo(ob, q)) = acc[ob];
       }
       // ---- e_out = e + m
       const int row = rb * 16 + i;
@@ -313,19 +318,18 @@ k_edge_fwd_rows(EdgeTiles tl, const bf16* __restrict__ e_in, bf16* __restrict__ 
           o[s] = __builtin_bit_cast(uint4, v);
         }
         if (row < n) {
-          bf16* op = e_out + ((size_t)d0.z + row) * D + 32 * q;
+          bf16* op = e_out + ((size_t)d0.z + row) * D + 8 * q;
 #pragma unroll
-          for (int s = 0; s < 4; ++s) *reinterpret_cast<uint4*>(op + 8 * s) = o[s];
+          for (int s = 0; s < 4; ++s) *reinterpret_cast<uint4*>(op + 32 * s) = o[s];
         }
       }
       wave_lds_sync();
-      seg_pass(stage, lane, segv, nv, rb * 16, j, carry, [&](int jj, float2 v) {
-        float* dst = d0.y >= 0 ? agg + (size_t)(d0.x + jj) * D : slots + (size_t)(-1 - d0.y) * D;
+      seg_pass(stage, lane, segraw, d0.z, chunk, n, nv, rb * 16, j, carry, [&](int jj, float2 v) {
+        float* dst = !chunk ? agg + (size_t)(d0.x + jj) * D : slots + (size_t)(-1 - d0.y) * D;
         *reinterpret_cast<float2*>(dst + 2 * lane) = v;
       });
       wave_lds_sync();
     }
-    if (!issued && t + stride < tend) issue(d1, s1, r1, nxt);
     cur = nxt;
     d0 = d1;
     d1 = d2;
@@ -357,12 +361,15 @@ __device__ __forceinline__ bf16x8 cat8(bf16x4 lo, bf16x4 hi) {
 // A operand of the transposed product C = W^T x from the row-permuted LDS
 // copy WP of W (rows = output features o of W): A[m][k] = W[o][k'] with
 // output slot m of block ob being input feature k' = perm_row(16ob + m) and
-// k running over o = 32q + 8s + j.  Row o of W sits at packed row
-// 16(2s + t) + 4q + j' for o = 32q + 8s + 4t + j'.
+// k = 8q + 4t + j' running over o = 32s + 8q + 4t + j' (lane q's run s).
+// Row o of W sits at packed row 16(2s + t) + 4q + j'; lane 4j' + c supplies
+// the 4 columns perm_row(16ob + 4c + 0..3) of it (one 8-byte piece).
 __device__ __forceinline__ bf16x8 wt_frag(const bf16* WP, int ob, int s, int lam, int q) {
   const int jp = lam >> 2, c = lam & 3;
-  const bf16* p0 = WP + ((2 * s) * 16 + 4 * q + jp) * RW_LDW + 32 * c + 4 * ob;
-  return cat8(lds_tr(p0), lds_tr(p0 + 16 * RW_LDW));
+  const int R = (2 * s) * 16 + 4 * q + jp, C = 4 * (ob >> 1) + c, h = 4 * (ob & 1);
+  const bf16* p0 = wchunk(WP, R, C) + h;
+  const bf16* p1 = wchunk(WP, R + 16, C) + h;
+  return cat8(lds_tr(p0), lds_tr(p1));
 }
 
 // Given ebar_in = dL/de_out (absent for the last block), aggbar, and the
@@ -384,8 +391,9 @@ k_edge_bwd_rows(EdgeTiles tl, const bf16* __restrict__ a1_in, const float* __res
     const bf16* W2p = (const bf16*)w.W2p;
     for (int idx = tid; idx < D * D / 8; idx += NT) {
       const int row = idx >> 4, c = (idx & 15) * 8;
-      *reinterpret_cast<uint4*>(S.W1 + row * RW_LDW + c) = *reinterpret_cast<const uint4*>(W1p + row * D + c);
-      *reinterpret_cast<uint4*>(S.W2 + row * RW_LDW + c) = *reinterpret_cast<const uint4*>(W2p + row * D + c);
+      const int cs = ((idx & 15) ^ wswz(row)) << 3;
+      *reinterpret_cast<uint4*>(S.W1 + row * D + cs) = *reinterpret_cast<const uint4*>(W1p + row * D + c);
+      *reinterpret_cast<uint4*>(S.W2 + row * D + cs) = *reinterpret_cast<const uint4*>(W2p + row * D + c);
     }
     if (tid < D) {
       S.b2[tid] = w.b2[tid];
@@ -430,53 +438,52 @@ k_edge_bwd_rows(EdgeTiles tl, const bf16* __restrict__ a1_in, const float* __res
     uint4 a[4];
     f32x4 eb[8];
   };
+  // All global loads are unconditional from clamped indices (see the
+  // forward kernel); without an incoming edge gradient the loaded values are
+  // replaced by zeros.
+  const int lastE = (int)max(tl.n_edges - 1, (int64_t)0);
+  auto erow = [&](int4 d, int rb) { return min(max(d.z + min(rb * 16 + i, tile_rows(d) - 1), 0), lastE); };
   auto load_recv = [&](int4 d, int (&rv)[2]) {
-    const int n = tile_rows(d);
 #pragma unroll
-    for (int rb = 0; rb < 2; ++rb) rv[rb] = n > 0 ? tl.receivers[d.z + min(rb * 16 + i, n - 1)] : 0;
+    for (int rb = 0; rb < 2; ++rb) rv[rb] = tl.receivers[erow(d, rb)];
   };
   auto load_half = [&](int4 d, int rb, HalfLoads& H) {
-    const int n = tile_rows(d);
-    if (n <= 0) return;
-    const size_t row = (size_t)d.z + min(rb * 16 + i, n - 1);
-    const bf16* ap = a1_in + row * D + 32 * q;
+    const size_t row = (size_t)erow(d, rb);
+    const bf16* ap = a1_in + row * D + 8 * q;
 #pragma unroll
-    for (int k = 0; k < 4; ++k) H.a[k] = *reinterpret_cast<const uint4*>(ap + 8 * k);
-    if (have_ebar) {
-      const float* ep = ebar_in + row * D + 32 * q;
+    for (int k = 0; k < 4; ++k) H.a[k] = *reinterpret_cast<const uint4*>(ap + 32 * k);
+    const float* ep = ebar_in + row * D;
 #pragma unroll
-      for (int ob = 0; ob < 8; ++ob) H.eb[ob] = *reinterpret_cast<const f32x4*>(ep + 4 * ob);
-    } else {
-#pragma unroll
-      for (int ob = 0; ob < 8; ++ob) H.eb[ob] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int ob = 0; ob < 8; ++ob) {
+      const f32x4 v = *reinterpret_cast<const f32x4*>(ep + fo(ob, q));
+      H.eb[ob] = have_ebar ? v : f32x4{0.f, 0.f, 0.f, 0.f};
     }
+  };
+  auto load_ag = [&](int recv, f32x4 (&ag)[8]) {
+    const float* gp = aggbar + (size_t)recv * D;
+#pragma unroll
+    for (int ob = 0; ob < 8; ++ob) ag[ob] = *reinterpret_cast<const f32x4*>(gp + fo(ob, q));
   };
 
   float2 db1 = {0.f, 0.f}, dga = {0.f, 0.f}, dbe = {0.f, 0.f};
   float* stage = S.stage[wv];
-  float* srow = stage + i * RW_LDM + 32 * q;
+  float* srow = stage + i * RW_LDM;
 
   // One half (rows rb*16 .. +16) of tile d0 with its streams in H.
-  auto half = [&](HalfLoads& H, int4 d0, int rb, int recv, int segv, int nv, int& j, float2& carry) {
+  auto half = [&](HalfLoads& H, f32x4 (&ag)[8], int4 d0, int rb, int segraw, bool chunk, int nv, int& j,
+                  float2& carry) {
     const int n = tile_rows(d0);
     const int row = rb * 16 + i;
     const int nh = max(0, min(16, n - rb * 16));  // valid rows of this half
-    f32x4 ag[8];
-    {
-      const float* gp = aggbar + (size_t)recv * D + 32 * q;
-#pragma unroll
-      for (int ob = 0; ob < 8; ++ob)
-        ag[ob] = n > 0 ? *reinterpret_cast<const f32x4*>(gp + 4 * ob) : f32x4{0.f, 0.f, 0.f, 0.f};
-    }
     // ---- z2 = b2 + W2 a1 and its LayerNorm statistics
     f32x4 acc[8];
 #pragma unroll
-    for (int ob = 0; ob < 8; ++ob) acc[ob] = *reinterpret_cast<const f32x4*>(S.b2 + 32 * q + 4 * ob);
+    for (int ob = 0; ob < 8; ++ob) acc[ob] = *reinterpret_cast<const f32x4*>(S.b2 + fo(ob, q));
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
 #pragma unroll
       for (int ob = 0; ob < 8; ++ob) {
-        const bf16x8 a = *reinterpret_cast<const bf16x8*>(S.W2 + (ob * 16 + i) * RW_LDW + 32 * q + 8 * s);
+        const bf16x8 a = *reinterpret_cast<const bf16x8*>(wchunk(S.W2, ob * 16 + i, 4 * s + q));
         acc[ob] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, as_frag(H.a[s]), acc[ob], 0, 0, 0);
       }
     }
@@ -501,7 +508,7 @@ k_edge_bwd_rows(EdgeTiles tl, const bf16* __restrict__ a1_in, const float* __res
     }
     // ---- dgamma += sum_rows mbar * xhat, dbeta += sum_rows mbar
 #pragma unroll
-    for (int ob = 0; ob < 8; ++ob) *reinterpret_cast<f32x4*>(srow + 4 * ob) = ag[ob] * acc[ob];
+    for (int ob = 0; ob < 8; ++ob) *reinterpret_cast<f32x4*>(srow + fo(ob, q)) = ag[ob] * acc[ob];
     wave_lds_sync();
     {
       const float2 c = col_pass(stage, lane, nh);
@@ -510,7 +517,7 @@ k_edge_bwd_rows(EdgeTiles tl, const bf16* __restrict__ a1_in, const float* __res
     }
     wave_lds_sync();
 #pragma unroll
-    for (int ob = 0; ob < 8; ++ob) *reinterpret_cast<f32x4*>(srow + 4 * ob) = ag[ob];
+    for (int ob = 0; ob < 8; ++ob) *reinterpret_cast<f32x4*>(srow + fo(ob, q)) = ag[ob];
     wave_lds_sync();
     {
       const float2 c = col_pass(stage, lane, nh);
@@ -521,7 +528,7 @@ k_edge_bwd_rows(EdgeTiles tl, const bf16* __restrict__ a1_in, const float* __res
     float s1 = 0.f, s2 = 0.f;
 #pragma unroll
     for (int ob = 0; ob < 8; ++ob) {
-      ag[ob] *= *reinterpret_cast<const f32x4*>(S.g + 32 * q + 4 * ob);  // dxh
+      ag[ob] *= *reinterpret_cast<const f32x4*>(S.g + fo(ob, q));  // dxh
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         s1 += ag[ob][r];
@@ -538,9 +545,9 @@ k_edge_bwd_rows(EdgeTiles tl, const bf16* __restrict__ a1_in, const float* __res
         dzf[s][4 + r] = (bf16)(rstd * (ag[2 * s + 1][r] - m1 - acc[2 * s + 1][r] * m2));
       }
     if (row < n) {
-      bf16* dp = dz_out + ((size_t)d0.z + row) * D + 32 * q;
+      bf16* dp = dz_out + ((size_t)d0.z + row) * D + 8 * q;
 #pragma unroll
-      for (int s = 0; s < 4; ++s) *reinterpret_cast<uint4*>(dp + 8 * s) = __builtin_bit_cast(uint4, dzf[s]);
+      for (int s = 0; s < 4; ++s) *reinterpret_cast<uint4*>(dp + 32 * s) = __builtin_bit_cast(uint4, dzf[s]);
     }
     // ---- da1 = W2^T dz2, zbar = da1 where a1 > 0
 #pragma unroll
@@ -562,9 +569,9 @@ k_edge_bwd_rows(EdgeTiles tl, const bf16* __restrict__ a1_in, const float* __res
       }
     }
     if (row < n) {
-      bf16* zp = zbar + ((size_t)d0.z + row) * D + 32 * q;
+      bf16* zp = zbar + ((size_t)d0.z + row) * D + 8 * q;
 #pragma unroll
-      for (int s = 0; s < 4; ++s) *reinterpret_cast<uint4*>(zp + 8 * s) = __builtin_bit_cast(uint4, zf[s]);
+      for (int s = 0; s < 4; ++s) *reinterpret_cast<uint4*>(zp + 32 * s) = __builtin_bit_cast(uint4, zf[s]);
     }
     // ---- per-receiver sums of zbar (as stored) and db1
     wave_lds_sync();
@@ -576,12 +583,12 @@ k_edge_bwd_rows(EdgeTiles tl, const bf16* __restrict__ a1_in, const float* __res
         lo[r] = (float)zf[s][r];
         hi[r] = (float)zf[s][4 + r];
       }
-      *reinterpret_cast<f32x4*>(srow + 8 * s) = lo;
-      *reinterpret_cast<f32x4*>(srow + 8 * s + 4) = hi;
+      *reinterpret_cast<f32x4*>(srow + 32 * s + 8 * q) = lo;
+      *reinterpret_cast<f32x4*>(srow + 32 * s + 8 * q + 4) = hi;
     }
     wave_lds_sync();
-    seg_pass(stage, lane, segv, nv, rb * 16, j, carry, [&](int jj, float2 v) {
-      float* dst = d0.y >= 0 ? R + (size_t)(d0.x + jj) * D : slots + (size_t)(-1 - d0.y) * D;
+    seg_pass(stage, lane, segraw, d0.z, chunk, n, nv, rb * 16, j, carry, [&](int jj, float2 v) {
+      float* dst = !chunk ? R + (size_t)(d0.x + jj) * D : slots + (size_t)(-1 - d0.y) * D;
       *reinterpret_cast<float2*>(dst + 2 * lane) = v;
       db1.x += v.x;
       db1.y += v.y;
@@ -594,9 +601,9 @@ k_edge_bwd_rows(EdgeTiles tl, const bf16* __restrict__ a1_in, const float* __res
         H.eb[ob] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wt_frag(S.W1, ob, s, i, q), zf[s], H.eb[ob], 0, 0, 0);
     }
     if (row < n) {
-      float* op = ebar_out + ((size_t)d0.z + row) * D + 32 * q;
+      float* op = ebar_out + ((size_t)d0.z + row) * D;
 #pragma unroll
-      for (int ob = 0; ob < 8; ++ob) *reinterpret_cast<f32x4*>(op + 4 * ob) = H.eb[ob];
+      for (int ob = 0; ob < 8; ++ob) *reinterpret_cast<f32x4*>(op + fo(ob, q)) = H.eb[ob];
     }
     wave_lds_sync();
   };
@@ -608,22 +615,21 @@ k_edge_bwd_rows(EdgeTiles tl, const bf16* __restrict__ a1_in, const float* __res
     HalfLoads A, B;
     load_half(d0, 0, A);
     for (; t < tend; t += stride) {
-      const int n = tile_rows(d0);
+      // issue order = use order, so each wait covers only older requests
+      const bool chunk = d0.y < 0;
+      const int nv = chunk ? 1 : d0.y - d0.x;
+      const int segraw = tl.rowptr[min(d0.x + lane, max(d0.x, d0.y))];
       const int4 d2 = desc(t + 2 * stride);
       load_recv(d1, rn);
-      const int nv = d0.y >= 0 ? d0.y - d0.x : 1;
-      int segv = 0;
-      if (d0.y >= 0) {
-        if (lane <= nv) segv = tl.rowptr[d0.x + lane] - d0.z;
-      } else {
-        segv = lane == 0 ? 0 : n;
-      }
+      f32x4 ag[8];
+      load_ag(rc0[0], ag);
+      load_half(d0, 1, B);
       float2 carry = {0.f, 0.f};
       int j = 0;
-      load_half(d0, 1, B);
-      half(A, d0, 0, rc0[0], segv, nv, j, carry);
-      if (t + stride < tend) load_half(d1, 0, A);
-      half(B, d0, 1, rc0[1], segv, nv, j, carry);
+      half(A, ag, d0, 0, segraw, chunk, nv, j, carry);
+      load_ag(rc0[1], ag);
+      load_half(d1, 0, A);
+      half(B, ag, d0, 1, segraw, chunk, nv, j, carry);
       d0 = d1;
       d1 = d2;
       rc0[0] = rn[0];
@@ -736,6 +742,7 @@ static int rows_grid(int64_t n_tiles, int max_blocks) {
 hipError_t launch_edge_fwd_rows(const EdgeTiles& t, const void* e_in, void* e_out, int write_e, const void* Pn,
                                 const MlpW& w, float eps, float* agg, float* slots, void* a1_out, hipStream_t s) {
   if (t.n_tiles <= 0) return hipSuccess;
+  if (t.n_edges <= 0) return hipErrorInvalidValue;
   hipLaunchKernelGGL(k_edge_fwd_rows, dim3(rows_grid(t.n_tiles, kRowsBlocks)), dim3(NT), 0, s, t, (const bf16*)e_in,
                      (bf16*)e_out, write_e, (const bf16*)Pn, w, eps, agg, slots, (bf16*)a1_out);
   return hipGetLastError();
@@ -746,6 +753,7 @@ hipError_t launch_edge_bwd_rows(const EdgeTiles& t, const void* a1, const float*
                                 float* R, float* slots, const Partials& part, int* nblocks, hipStream_t s) {
   *nblocks = 0;
   if (t.n_tiles <= 0) return hipSuccess;
+  if (t.n_edges <= 0) return hipErrorInvalidValue;
   const int g = rows_grid(t.n_tiles, std::min(kRowsBlocks, part.max_blocks));
   *nblocks = g;
   hipLaunchKernelGGL(k_edge_bwd_rows, dim3(g), dim3(NT), 0, s, t, (const bf16*)a1, ebar_in, have_ebar, ebar_out,

@@ -35,13 +35,14 @@ struct PackEnt {
 };
 
 // Output-row order of the weights used by the row-per-wave edge kernels:
-// packed row p = ob*16 + m holds row 32*(m/4) + 4*ob + m%4 of W, so that an
-// MFMA C fragment of output block ob gives lane group q the features
-// 32q + 4ob + r (r < 4), i.e. every lane ends with a contiguous run of 32
-// output features, which is exactly its B operand of the next product.
+// packed row p = ob*16 + m holds row 32*(ob/2) + 8*(m/4) + 4*(ob%2) + m%4 of
+// W, so that the MFMA C fragment of output block ob gives lane group q the
+// features 32*(ob/2) + 8q + 4*(ob%2) + r (r < 4): over the 8 blocks, the
+// runs [32s + 8q, 32s + 8q + 8) that are exactly the lane's B operand of
+// the next product.
 __host__ __device__ inline int perm_row(int p) {
   const int ob = p >> 4, m = p & 15;
-  return 32 * (m >> 2) + 4 * ob + (m & 3);
+  return 32 * (ob >> 1) + 8 * (m >> 2) + 4 * (ob & 1) + (m & 3);
 }
 constexpr int kPackMax = 64;
 struct PackList {
@@ -55,6 +56,7 @@ struct EdgeTiles {
   const int32_t* rowptr;
   const int32_t* senders;
   const int32_t* receivers;
+  int64_t n_edges;
 };
 
 // Per-block partial buffers for deterministic weight-gradient reductions.
@@ -130,6 +132,8 @@ struct LinComb {
 };
 hipError_t launch_lincomb(int64_t N, const LinComb& lc, float* out, int32_t out_ld, int32_t out_off,
                           hipStream_t s);
+// p[0..n) = v
+hipError_t launch_fill(float* p, int64_t n, float v, hipStream_t s);
 // node_in[v] = [static[v][0..4), y-combination[v][0..4)]
 hipError_t launch_stage_input(int64_t N, const float* st, const LinComb& lc, float* node_in, hipStream_t s);
 

@@ -26,9 +26,20 @@ __global__ void __launch_bounds__(256) k_copy_static(int64_t N, const float* __r
   node_in[v * 8 + c] = st[v * 4 + c];
 }
 
+__global__ void __launch_bounds__(256) k_fill(int64_t n, float v, float* __restrict__ p) {
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx < n) p[idx] = v;
+}
+
 }  // namespace dev
 
 using namespace dev;
+
+hipError_t launch_fill(float* p, int64_t n, float v, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_fill, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, n, v, p);
+  return hipGetLastError();
+}
 
 hipError_t launch_lincomb(int64_t N, const LinComb& lc, float* out, int32_t out_ld, int32_t out_off, hipStream_t s) {
   if (N <= 0) return hipSuccess;
