@@ -34,23 +34,122 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def kernel_bytes(kind, N, E, n_tiles, se, have_ebar=True, write_e=True):
-    """Algorithmic HBM bytes of one launch: every input read once and every
-    output written once (P holds two fp32 node products, the latents of the
-    edge stream have se bytes per element)."""
+def kernel_bytes(kind, N, E, n_tiles, prec, have_ebar=True, write_e=True, keep_a1=True):
+    """Algorithmic HBM bytes of one launch of the kernels this build runs:
+    every input read once and every output written once (node products P
+    are [N][2D] in the operand precision; bf16 edge latents, a1, zbar and
+    dz2 streams are 2 bytes per element, gradients fp32)."""
+    se = 2 if prec == "bf16" else 4
+    row, frow = D * se, D * 4
+    tiles = n_tiles * 16 + 4 * (N + 1)
     if kind == "edge_fwd":
-        return (E * (D * se * (2 if write_e else 1) + 4)
-                + N * (2 * D * 4 + D * 4 + 4) + n_tiles * 16)
+        return (E * (row + 8 + (row if write_e else 0) + (row if keep_a1 and prec == "bf16" else 0))
+                + N * (2 * row + frow) + tiles)
     if kind == "edge_bwd":
-        return (E * (D * se + (D * 4 if have_ebar else 0) + D * 4 + D * se + 4)
-                + N * (2 * D * 4 + D * 4 + D * 4 + 4) + n_tiles * 16)
+        if prec == "bf16":  # from the saved a1: reads a1, ebar_in, aggbar; writes ebar_out, zbar, dz2, R
+            return (E * (row + (frow if have_ebar else 0) + 4 + frow + 2 * row)
+                    + N * (frow + frow) + tiles)
+        return (E * (row + (frow if have_ebar else 0) + frow + row + 8)
+                + N * (2 * row + frow + frow) + tiles)
+    if kind == "wgrad":
+        return E * row * (4 if prec == "bf16" else 2)
     if kind == "node_srcsum":
-        return E * (D * se + 4) + N * (4 + 4 * D * 4)
+        return E * (row + 4) + N * (4 + 4 * frow)
     if kind == "node_fwd":
-        return N * (D * 4 * 3 + 2 * D * 4)
+        return N * (3 * frow + 2 * row)
     if kind == "node_bwd":
-        return N * (D * 4 * 5)
+        return N * (5 * frow)
     return None
+
+
+def source_digest():
+    """Digest of the kernel sources: counter-derived traffic is reported only
+    for the sources it was measured on."""
+    import hashlib
+    h = hashlib.sha256()
+    d = os.path.join(ROOT, "paper_2304_00338_amd", "csrc")
+    for f in sorted(os.listdir(d)):
+        if f.endswith((".hip", ".hpp", ".cpp")):
+            h.update(f.encode())
+            h.update(open(os.path.join(d, f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def traffic_file(kernel):
+    return os.path.join(ROOT, "profiles", f"{kernel}_c3_patch_traffic.json")
+
+
+def measured_traffic(kernel):
+    """HBM bytes per launch of `kernel` from the committed counter summary,
+    or None when it is absent or the kernel sources changed since."""
+    try:
+        t = json.load(open(traffic_file(kernel)))
+    except (OSError, ValueError):
+        return None
+    if t.get("source_digest") != source_digest():
+        return None
+    return t.get("bytes_per_launch")
+
+
+def summarize_profile(d, kernel):
+    """Summary of a profiling directory made by the commands listed in the
+    output (kernel trace, FETCH_SIZE and WRITE_SIZE passes over one bench
+    step, and the same two counters over a 1 GiB device copy): markdown on
+    stdout, and the traffic of `kernel` written next to the summaries."""
+    import glob
+    import re
+    import sqlite3
+
+    def db(sub):
+        f = glob.glob(os.path.join(d, sub, "*_results.db"))
+        return sqlite3.connect(f[0]) if f else None
+
+    def short(n):
+        m = re.search(r"(k_[a-z0-9_]+?)(?:I|<|\()(.*)", n) or re.search(r"(k_[a-z0-9_]+)", n)
+        if not m:
+            return "copy" if "copy" in n.lower() else n[:40]
+        t = re.match(r"<([^>]*)>", n[m.end(1):])
+        if not t:
+            return m.group(1)
+        args = [a.strip() for a in t.group(1).split(",")]
+        args[0] = {"1": "bf16", "0": "fp32"}.get(args[0], args[0])
+        return m.group(1) + "<" + ", ".join(args) + ">"
+
+    def pmc(con, counter):
+        agg = {}
+        for n, v in con.execute("select kernel_name, value from counters_collection where counter_name=?",
+                                (counter,)):
+            agg.setdefault(short(n), []).append(v)
+        return {k: sum(v) / len(v) for k, v in agg.items()}
+
+    tr = db("prof_trace")
+    rows = list(tr.execute("select name, total_calls, total_duration, average, percentage from top_kernels"))
+    fetch, write = pmc(db("prof_fetch"), "FETCH_SIZE"), pmc(db("prof_write"), "WRITE_SIZE")
+    cf, cw = pmc(db("prof_copyf"), "FETCH_SIZE"), pmc(db("prof_copyw"), "WRITE_SIZE")
+    copy_bytes = float(1 << 30)
+    kf = max((k for k in cf if k == "copy" or "copy" in k), key=lambda k: cf[k])
+    kw = max((k for k in cw if k == "copy" or "copy" in k), key=lambda k: cw[k])
+    sf, sw = copy_bytes / (cf[kf] * 1024), copy_bytes / (cw[kw] * 1024)
+    print("| kernel | calls | total ms | avg ms | % | FETCH_SIZE KiB | WRITE_SIZE KiB | HBM GB (scaled) |")
+    print("|---|---|---|---|---|---|---|---|")
+    for n, c, tot, avg, pct in rows:
+        k = short(n)
+        f, w = fetch.get(k), write.get(k)
+        hbm = f"{(f * sf + w * sw) * 1024 / 1e9:.2f}" if f is not None and w is not None else ""
+        print(f"| {k} | {c} | {tot / 1e3:.3f} | {avg / 1e3:.4f} | {pct:.1f} | "
+              f"{'' if f is None else f'{f:,.0f}'} | {'' if w is None else f'{w:,.0f}'} | {hbm} |")
+    print(f"\nCopy calibration (1 GiB read and written): FETCH_SIZE {cf[kf]:,.1f} KiB -> scale {sf:.3f}; "
+          f"WRITE_SIZE {cw[kw]:,.1f} KiB -> scale {sw:.3f}")
+    k = next((short(n) for n, *_ in rows if short(n).startswith("k_" + kernel)), None)
+    if k is not None and k in fetch and k in write:
+        out = {"kernel": kernel, "profiled_as": k, "source_digest": source_digest(),
+               "fetch_kib_per_launch": fetch[k], "write_kib_per_launch": write[k],
+               "fetch_scale": sf, "write_scale": sw,
+               "bytes_per_launch": (fetch[k] * sf + write[k] * sw) * 1024}
+        with open(traffic_file(kernel), "w") as fh:
+            json.dump(out, fh, indent=1)
+        print(f"\n{k}: {out['bytes_per_launch'] / 1e9:.2f} GB of HBM traffic per launch "
+              f"(written to {os.path.relpath(traffic_file(kernel), ROOT)})")
 
 
 def setup(args):
@@ -135,7 +234,14 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibrate", action="store_true",
                     help="only run a plain device copy of known size (for counter scaling)")
+    ap.add_argument("--summarize-profile", metavar="DIR",
+                    help="summarize a rocprofv3 output directory (no GPU needed)")
+    ap.add_argument("--profile-kernel", default="edge_bwd",
+                    help="kernel whose counter traffic --summarize-profile records")
     args = ap.parse_args()
+    if args.summarize_profile:
+        summarize_profile(args.summarize_profile, args.profile_kernel)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path "
               "(the patch-parallel design is described in DESIGN.md); run with --gpus 1",
@@ -189,20 +295,21 @@ def main():
     dom = max(prof, key=lambda k: prof[k][0])
     tot, cnt = prof[dom]
     avg_ms = tot / cnt
-    se = 2 if args.precision == "bf16" else 4
     n_tiles = S["dg"].n_tiles
     if dom == "edge_bwd":
-        per = [kernel_bytes(dom, N, E, n_tiles, se, have_ebar=(l < m - 1)) for l in range(m)]
+        per = [kernel_bytes(dom, N, E, n_tiles, args.precision, have_ebar=(l < m - 1)) for l in range(m)]
     elif dom == "edge_fwd":
-        per = [kernel_bytes(dom, N, E, n_tiles, se, write_e=(l < m - 1)) for l in range(m)]
+        per = [kernel_bytes(dom, N, E, n_tiles, args.precision, write_e=(l < m - 1)) for l in range(m)]
     else:
-        per = [kernel_bytes(dom, N, E, n_tiles, se)]
+        per = [kernel_bytes(dom, N, E, n_tiles, args.precision)]
     bytes_per_launch = float(np.mean(per)) if per[0] is not None else None
     roof = None
     if bytes_per_launch is not None:
         ach = bytes_per_launch / (avg_ms * 1e-3) / 1e9
+        traffic = measured_traffic(dom) if args.precision == "bf16" else None
         roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None, "kernel": dom,
+                "frac": round(ach / HBM_PEAK_GBS, 4),
+                "traffic": None if traffic is None else int(traffic), "kernel": dom,
                 "avg_launch_ms": round(avg_ms, 4), "launches_per_step": cnt // args.steps,
                 "algorithmic_bytes_per_launch": int(bytes_per_launch)}
 

@@ -308,6 +308,7 @@ struct Run {
   int m;
   int prec;
   float eps;
+  bool keep_a1 = false;  // this call saves (or the backward reads) the edge MLPs' a1
 
   // Bracket a launch with profiling events when enabled.
   hipError_t mark_begin(int kind) {
@@ -340,7 +341,7 @@ struct Run {
     return (float*)(set(k) + c.L.agg_off) + (c.save ? (size_t)l * N * D : 0);
   }
   void* a1_l(int k, int l) const {
-    if (!(c.save && prec == MGN_BF16)) return nullptr;
+    if (!(keep_a1 && c.save && prec == MGN_BF16)) return nullptr;
     return set(k) + c.L.a1_off + (size_t)l * E * D * 2;
   }
   void* P_l(int k, int l) const {
@@ -612,6 +613,7 @@ int mgn_forward(mgn_ctx* ctx, const mgn_dgraph* g, const float* params, const fl
     return fail(MGN_ERR_ARG, "mgn_forward: null input or output");
   c.saved = 0;
   Run r{c, *g, params, (char*)ws, S(stream), g->n_nodes, g->n_edges, c.cfg.mp_steps, c.cfg.precision, c.cfg.ln_eps};
+  r.keep_a1 = save != 0;
   if (g->n_nodes > 0) {
     if ((rc = r.pack_weights()) != MGN_OK) return rc;
     if ((rc = r.forward(node_in, efeat, out, 0)) != MGN_OK) return rc;
@@ -645,6 +647,7 @@ int mgn_integrate_step(mgn_ctx* ctx, const mgn_dgraph* g, const float* params, i
   const int64_t N = g->n_nodes;
   char* w = (char*)ws;
   Run r{c, *g, params, w, S(stream), N, g->n_edges, c.cfg.mp_steps, c.cfg.precision, c.cfg.ln_eps};
+  r.keep_a1 = save != 0;
   if (N > 0) {
     if ((rc = r.pack_weights()) != MGN_OK) return rc;
     float* node_in = (float*)(w + c.L.node_in);
@@ -701,6 +704,7 @@ int mgn_backward(mgn_ctx* ctx, const float* grad_out, float* grad_params, float*
   if (N == 0) return MGN_OK;
   if (!grad_out || !grad_params) return fail(MGN_ERR_ARG, "mgn_backward: null gradient buffer");
   Run r{c, c.g, c.params, c.ws, S(stream), N, c.g.n_edges, c.cfg.mp_steps, c.cfg.precision, c.cfg.ln_eps};
+  r.keep_a1 = true;
   int rc;
   if (c.saved == 1) return r.backward(0, c.node_in, c.efeat, grad_out, grad_params, grad_in);
   Tableau tb;
