@@ -614,8 +614,12 @@ int mgn_forward(mgn_ctx* ctx, const mgn_dgraph* g, const float* params, const fl
   c.saved = 0;
   Run r{c, *g, params, (char*)ws, S(stream), g->n_nodes, g->n_edges, c.cfg.mp_steps, c.cfg.precision, c.cfg.ln_eps};
   r.keep_a1 = save != 0;
+  // a saving call keeps its own copy of node_in for mgn_backward
+  float* kept = (float*)((char*)ws + c.L.node_in);
   if (g->n_nodes > 0) {
     if ((rc = r.pack_weights()) != MGN_OK) return rc;
+    if (save) HIP_TRY(hipMemcpyAsync(kept, node_in, (size_t)g->n_nodes * 8 * sizeof(float), hipMemcpyDeviceToDevice,
+                                     S(stream)));
     if ((rc = r.forward(node_in, efeat, out, 0)) != MGN_OK) return rc;
   }
   if (save) {
@@ -624,7 +628,7 @@ int mgn_forward(mgn_ctx* ctx, const mgn_dgraph* g, const float* params, const fl
     c.g = *g;
     c.params = params;
     c.efeat = efeat;
-    c.node_in = node_in;
+    c.node_in = kept;
     c.ws = (char*)ws;
   }
   return MGN_OK;

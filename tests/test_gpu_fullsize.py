@@ -1,0 +1,199 @@
+"""GPU checks at the full sizes of the benchmark configurations.
+
+* C3: slab 8 of 16 of the jittered 146^3 Kuhn mesh with a 15-hop ghost zone
+  (852,640 nodes, 11,674,318 edges), 15 MP steps: the patch's subdomain
+  outputs equal the whole-mesh outputs bitwise (Sec. 2.2, condition 1), and
+  sampled subdomain outputs match the fp64 oracle evaluated on the 15-hop
+  ball of each sampled node (which fixes that node's output exactly).
+* C4: the whole 3,112,136-node mesh, a 10-step explicit-Euler rollout
+  without saved activations: the first step at sampled nodes against the
+  oracle, run-to-run bitwise reproducibility, finite states.
+* C2: 32^3 mesh, fp32, 15 MP steps: sampled outputs against the oracle, and
+  the gradient of the whole-mesh loss equal to the sum of the gradients of
+  the z-slab patches with the loss on their subdomains (condition 3).
+* C5: RK4 / midpoint / Euler on the C2 mesh, fp32 and bf16: the integrator
+  call equals the explicit composition of its stage MGN calls, forward and
+  backward (stage chaining of Sec. 2.3 at full size; the stage arithmetic
+  itself is checked against the oracle on small meshes in
+  test_gpu_parity.py)."""
+import numpy as np
+import pytest
+
+import oracle as O
+import synth
+from fullsize_util import node_id, oracle_node_output
+from gpu_util import BF16_TOL, FP32_TOL, rel_l2
+
+torch = pytest.importorskip("torch")
+# the 146^3 host mesh and the oracle balls take a minute or two of host time
+pytestmark = [pytest.mark.gpu, pytest.mark.timeout(600)]
+
+from paper_2304_00338_amd import mgn  # noqa: E402
+
+BIG = (146, 146, 146)
+M_STEPS = 15
+C3_SAMPLES = [(0, 0, 77), (145, 0, 80)]
+C4_SAMPLES = [(0, 0, 0), (145, 145, 145)]
+
+
+def d(a):
+    return torch.from_numpy(np.ascontiguousarray(a, np.float32)).cuda()
+
+
+@pytest.fixture(scope="module")
+def big():
+    M = synth.mesh(BIG, 0)
+    g = mgn.build_graph(M["cells"], M["pos"])
+    P = synth.xavier_params(M_STEPS, 0)
+    print(f"146^3 mesh: {g.n_nodes} nodes, {g.n_edges} edges", flush=True)
+    return M, g, P
+
+
+@pytest.fixture(scope="module")
+def big_oracle(big):
+    """fp64 oracle outputs of one MGN call at the sampled nodes."""
+    M, _, P = big
+    return {c: oracle_node_output(M, BIG, c, P, M_STEPS) for c in C3_SAMPLES + C4_SAMPLES}
+
+
+@pytest.mark.parametrize("prec", ["bf16", "fp32"])
+def test_c3_patch_equals_full_mesh(big, big_oracle, prec):
+    M, g, P = big
+    part = synth.slab_part(BIG, 16)
+    pt = mgn.extract_patch(g, part, 8, 15)
+    mp = pt.patch_maps()
+    assert pt.n_nodes == 852640 and pt.n_edges == 11674318 and mp["n_interior"] == 213160
+    ctx = mgn.Context(M_STEPS, g.n_nodes, g.n_edges, prec)
+    params = d(P)
+    dg = mgn.DeviceGraph(g)
+    whole = mgn.mgn_forward(ctx, dg, params, d(M["node_in"]), dg.efeat).cpu().numpy()
+    del dg
+    dpt = mgn.DeviceGraph(pt)
+    out = mgn.mgn_forward(ctx, dpt, params, d(M["node_in"][mp["node_l2g"]]), dpt.efeat).cpu().numpy()
+    it = mp["interior"] == 1
+    assert np.array_equal(out[it].view(np.uint32), whole[mp["node_l2g"][it]].view(np.uint32))
+    loc = [int(np.searchsorted(mp["node_l2g"], node_id(BIG, c))) for c in C3_SAMPLES]
+    assert all(mp["interior"][v] == 1 for v in loc)
+    ref = np.stack([big_oracle[c] for c in C3_SAMPLES])
+    tol = FP32_TOL if prec == "fp32" else BF16_TOL
+    err = rel_l2(out[loc], ref)
+    print(f"C3 {prec}: sampled rel L2 {err:.2e}", flush=True)
+    assert err < tol
+
+
+def test_c4_rollout(big, big_oracle):
+    M, g, P = big
+    ctx = mgn.Context(M_STEPS, g.n_nodes, g.n_edges, "bf16", max_stages=1)
+    dg = mgn.DeviceGraph(g)
+    params, st, y0 = d(P), d(M["onehot"]), d(M["states"])
+
+    def rollout():
+        y, first = y0, None
+        for t in range(10):
+            y = mgn.mgn_integrate_step(ctx, dg, params, "euler", st, y, dg.efeat)
+            if t == 0:
+                first = y.cpu().numpy()
+        return first, y.cpu().numpy()
+
+    first, last = rollout()
+    _, last2 = rollout()
+    assert np.isfinite(last).all()
+    assert np.array_equal(last.view(np.uint32), last2.view(np.uint32))
+    ids = [node_id(BIG, c) for c in C4_SAMPLES]
+    ref = M["states"][ids].astype(np.float64) + np.stack([big_oracle[c] for c in C4_SAMPLES])
+    err = rel_l2(first[ids] - M["states"][ids], ref - M["states"][ids])
+    print(f"C4 step 1: sampled rel L2 of the increment {err:.2e}", flush=True)
+    assert err < BF16_TOL
+
+
+@pytest.fixture(scope="module")
+def c2():
+    shape = (32, 32, 32)
+    M = synth.mesh(shape, 0)
+    g = mgn.build_graph(M["cells"], M["pos"])
+    assert g.n_nodes == 32768 and g.n_edges == 434558
+    return shape, M, g, synth.xavier_params(M_STEPS, 0)
+
+
+def test_c2_fp32_outputs_and_patch_gradients(c2):
+    shape, M, g, P = c2
+    params = d(P)
+    dg = mgn.DeviceGraph(g)
+    N, E = g.n_nodes, g.n_edges
+    ctx = mgn.Context(M_STEPS, N, E, "fp32", save=True)
+    out = mgn.mgn_forward(ctx, dg, params, d(M["node_in"]), dg.efeat, save=True).cpu().numpy()
+    samples = [(0, 0, 0), (31, 31, 31)]
+    ref = np.stack([oracle_node_output(M, shape, c, P, M_STEPS) for c in samples])
+    err = rel_l2(out[[node_id(shape, c) for c in samples]], ref)
+    print(f"C2 fp32: sampled rel L2 {err:.2e}", flush=True)
+    assert err < FP32_TOL
+    # condition 3: whole-mesh gradient = sum of the patch gradients with the
+    # loss on each patch's subdomain (ghost zone k = m)
+    w = synth.loss_weights(N, 0)
+    g_whole = torch.zeros_like(params)
+    mgn.mgn_backward(ctx, d(w), g_whole)
+    part = synth.slab_part(shape, 2)
+    g_sum = torch.zeros_like(params)
+    for p in range(2):
+        pt = mgn.extract_patch(g, part, p, M_STEPS)
+        mp = pt.patch_maps()
+        dpt = mgn.DeviceGraph(pt)
+        x = d(M["node_in"][mp["node_l2g"]])
+        mgn.mgn_forward(ctx, dpt, params, x, dpt.efeat, save=True)
+        wp = w[mp["node_l2g"]] * mp["interior"][:, None]
+        mgn.mgn_backward(ctx, d(wp), g_sum)
+    e = rel_l2(g_sum.cpu().numpy(), g_whole.cpu().numpy())
+    print(f"C2 fp32: patch-sum gradient rel L2 {e:.2e}", flush=True)
+    assert e < FP32_TOL
+
+
+TAB = {"euler": ([[0.0]], [1.0]),
+       "midpoint": ([[0.0, 0.0], [0.5, 0.0]], [0.0, 1.0]),
+       "rk4": ([[0, 0, 0, 0], [0.5, 0, 0, 0], [0, 0.5, 0, 0], [0, 0, 1.0, 0]], [1 / 6, 1 / 3, 1 / 3, 1 / 6])}
+
+
+@pytest.mark.parametrize("scheme", ["rk4", "midpoint", "euler"])
+@pytest.mark.parametrize("prec", ["fp32", "bf16"])
+def test_c5_stage_composition(c2, scheme, prec):
+    shape, M, g, P = c2
+    N, E = g.n_nodes, g.n_edges
+    A, b = TAB[scheme]
+    s = len(b)
+    params, dg = d(P), mgn.DeviceGraph(g)
+    st, y = d(M["onehot"]), d(M["states"])
+    gout = d(synth.loss_weights(N, 5))
+    ctx = mgn.Context(M_STEPS, N, E, prec, max_stages=4, save=True)
+    y_next = mgn.mgn_integrate_step(ctx, dg, params, scheme, st, y, dg.efeat, save=True)
+    gp = torch.zeros_like(params)
+    gy = torch.zeros((N, 4), dtype=torch.float32, device="cuda")
+    mgn.mgn_backward(ctx, gout, gp, gy)
+    # explicit composition: one saving context per stage
+    ctxs = [mgn.Context(M_STEPS, N, E, prec, save=True) for _ in range(s)]
+    K = []
+    for i in range(s):
+        yi = y.clone()
+        for j in range(i):
+            if A[i][j] != 0.0:
+                yi = yi + A[i][j] * K[j]
+        K.append(mgn.mgn_forward(ctxs[i], dg, params, torch.cat([st, yi], 1).contiguous(), dg.efeat, save=True))
+    ym = y.clone()
+    for i in range(s):
+        if b[i] != 0.0:
+            ym = ym + b[i] * K[i]
+    tol = 1e-5 if prec == "fp32" else BF16_TOL
+    assert rel_l2(y_next.cpu().numpy(), ym.cpu().numpy()) < tol
+    gp_m = torch.zeros_like(params)
+    ybar = [None] * s
+    for i in range(s - 1, -1, -1):
+        kbar = b[i] * gout
+        for j in range(i + 1, s):
+            if A[j][i] != 0.0:
+                kbar = kbar + A[j][i] * ybar[j]
+        gin = torch.zeros((N, 8), dtype=torch.float32, device="cuda")
+        mgn.mgn_backward(ctxs[i], kbar.contiguous(), gp_m, gin)
+        ybar[i] = gin[:, 4:].contiguous()
+    gy_m = gout + sum(ybar)
+    e1 = rel_l2(gp.cpu().numpy(), gp_m.cpu().numpy())
+    e2 = rel_l2(gy.cpu().numpy(), gy_m.cpu().numpy())
+    print(f"C5 {scheme} {prec}: params {e1:.2e}, y {e2:.2e}", flush=True)
+    assert e1 < tol and e2 < tol

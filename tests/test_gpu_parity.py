@@ -226,3 +226,45 @@ def test_gradient_accumulates():
     mgn.mgn_backward(ctx, pb.d_w, g2)
     torch.cuda.synchronize()
     assert torch.equal(g2, g1 + g1)
+
+
+def test_saving_forward_owns_its_input():
+    """A saving forward keeps its own copy of node_in: the caller's buffer
+    may be freed and reused before mgn_backward."""
+    pb = Problem((7, 6, 5), 2, seed=9).device()
+    N, E = pb.g.n_nodes, pb.g.n_edges
+    ref = run_fwd_bwd(pb, "fp32")
+    ctx = mgn.Context(pb.m, N, E, "fp32", save=True)
+    tmp = pb.d_node_in.clone()
+    mgn.mgn_forward(ctx, pb.dg, pb.d_params, tmp, pb.dg.efeat, save=True)
+    tmp.fill_(123.0)
+    del tmp
+    junk = torch.full((N, 8), -7.0, dtype=torch.float32, device="cuda")  # likely reuses the block
+    gp = torch.zeros_like(pb.d_params)
+    gi = torch.zeros((N, 8), dtype=torch.float32, device="cuda")
+    mgn.mgn_backward(ctx, pb.d_w, gp, gi)
+    torch.cuda.synchronize()
+    del junk
+    assert np.array_equal(gp.cpu().numpy().view(np.uint32), ref[1].view(np.uint32))
+    assert np.array_equal(gi.cpu().numpy().view(np.uint32), ref[2].view(np.uint32))
+
+
+@pytest.mark.parametrize("prec", ["fp32", "bf16"])
+def test_edgeless_graph(prec):
+    """Nodes without any edge: every aggregate is zero and the edge MLPs get
+    no gradient; the rest of the call runs as usual."""
+    rng = np.random.default_rng(8)
+    n = 45
+    pos = rng.standard_normal((n, 3)).astype(np.float32)
+    node_in = np.concatenate([np.eye(4)[rng.integers(0, 4, n)], rng.standard_normal((n, 4))], 1)
+    pb = Problem(None, 2, seed=8, cells=np.zeros((0, 3), np.int64), pos=pos, node_in=node_in)
+    assert pb.g.n_edges == 0
+    pb.device()
+    out, gp, gi = run_fwd_bwd(pb, prec)
+    ro, rgp, rgi = oracle_fwd_bwd(pb, prec, (out, gp, gi))
+    tol = FP32_TOL if prec == "fp32" else BF16_TOL
+    assert rel_l2(out, ro) < tol
+    for name, a, b in segments(pb.m):
+        if ".edge" in name or name == "enc_edge":
+            assert np.all(gp[a:b] == 0.0), name
+    check(out, gp, gi, (ro, rgp, rgi), pb.m, tol, FP32_TOL if prec == "fp32" else bf16_grad_tols(pb))

@@ -439,3 +439,21 @@ def test_bf16_gradient_conditioning():
     s1, ts1 = O.mgn_forward(g, S1, M["node_in"], g.efeat, m, keep=True)
     gs1, _ = O.mgn_backward(ts1, w)
     assert rel(gs1, gs0) < 2e-2
+
+
+def test_ball_output_equals_whole_mesh():
+    """The full-size GPU tests read oracle outputs at single nodes from the
+    m-hop ball inside a grid box (tests/fullsize_util.py): on a small mesh
+    that equals the whole-mesh oracle output at a corner, a face and an
+    interior point, up to fp64 rounding (the BLAS products of the MLPs may
+    block rows differently for different matrix sizes)."""
+    from fullsize_util import oracle_node_output, node_id
+    shape, m = (11, 10, 12), 3
+    M = synth.mesh(shape, 4)
+    g = O.build_graph(M["cells"], M["pos"])
+    P = synth.xavier_params(m, 4, randomize_norm=True)
+    whole = O.mgn_forward(g, P, M["node_in"], g.efeat, m)
+    for c in [(0, 0, 0), (5, 0, 7), (5, 4, 6), (10, 9, 11)]:
+        got = oracle_node_output(M, shape, c, P, m)
+        w = whole[node_id(shape, c)]
+        assert np.max(np.abs(got - w) / np.abs(w)) < 1e-12, c
