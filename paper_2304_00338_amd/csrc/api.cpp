@@ -27,6 +27,7 @@ struct Off {
 
 struct PackOff {
   int64_t W1 = -1, W1t = -1, W2 = -1, W2t = -1, W1p = -1, W2p = -1;
+  int64_t W1sp = -1, W1rp = -1;  // edge MLPs: row-permuted sender / receiver column blocks of W1
 };
 
 struct Model {
@@ -78,18 +79,19 @@ void add_pack(Model& M, int64_t src, int rows, int cols, int64_t& W, int64_t& Wt
   M.ents.push_back(e);
 }
 
-// Row-permuted copy (perm_row) of the first D columns of a [D][ld] matrix.
-void add_perm(Model& M, int64_t src, int ld, int64_t& W) {
+// Row-permuted copy (perm_row) of `cols` columns of a [D][ld] matrix starting
+// at float offset src.
+void add_perm(Model& M, int64_t src, int ld, int64_t& W, int cols = D) {
   auto al = [](int64_t x) { return (x + 63) & ~int64_t(63); };
   M.pack_elems = al(M.pack_elems);
   W = M.pack_elems;
-  M.pack_elems += (int64_t)D * D;
+  M.pack_elems += (int64_t)D * cols;
   PackEnt e;
   e.src = src;
   e.dst = W;
   e.dstt = -1;
   e.rows = D;
-  e.cols = D;
+  e.cols = cols;
   e.ld = ld;
   e.perm = 1;
   M.ents.push_back(e);
@@ -116,6 +118,10 @@ Model make_model(int m) {
     add_pack(M, M.edge[i].W2, D, D, M.p_edge[i].W2, M.p_edge[i].W2t);
     add_perm(M, M.edge[i].W1, 3 * D, M.p_edge[i].W1p);
     add_perm(M, M.edge[i].W2, D, M.p_edge[i].W2p);
+    add_perm(M, M.edge[i].W1 + D, 3 * D, M.p_edge[i].W1sp);
+    add_perm(M, M.edge[i].W1 + 2 * D, 3 * D, M.p_edge[i].W1rp);
+    add_perm(M, M.node[i].W1, 2 * D, M.p_node[i].W1p, 2 * D);
+    add_perm(M, M.node[i].W2, D, M.p_node[i].W2p);
     add_pack(M, M.node[i].W1, D, 2 * D, M.p_node[i].W1, M.p_node[i].W1t);
     add_pack(M, M.node[i].W2, D, D, M.p_node[i].W2, M.p_node[i].W2t);
   }
@@ -353,6 +359,8 @@ struct Run {
     MlpW w;
     w.W1p = p.W1p >= 0 ? P(p.W1p) : nullptr;
     w.W2p = p.W2p >= 0 ? P(p.W2p) : nullptr;
+    w.W1sp = p.W1sp >= 0 ? P(p.W1sp) : nullptr;
+    w.W1rp = p.W1rp >= 0 ? P(p.W1rp) : nullptr;
     w.W1 = p.W1 >= 0 ? P(p.W1) : nullptr;
     w.W1t = p.W1t >= 0 ? P(p.W1t) : nullptr;
     w.W2 = p.W2 >= 0 ? P(p.W2) : nullptr;

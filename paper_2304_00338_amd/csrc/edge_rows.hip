@@ -66,13 +66,6 @@ __device__ __forceinline__ bf16x8 select_frag(int h, int i, int q) {
 
 __device__ __forceinline__ bf16x8 as_frag(const uint4& u) { return __builtin_bit_cast(bf16x8, u); }
 
-// The streams of one tile row pair a lane needs: its four 8-feature runs of
-// the edge latent and of the two gathered node products, for rows i and
-// 16 + i.
-struct RowLoads {
-  uint4 e[2][4], ps[2][4], pr[2][4];
-};
-
 __device__ __forceinline__ int tile_rows(int4 d) { return d.w - d.z; }
 
 // max(x, 0) as one integer max on the bit pattern (negative floats have the
@@ -199,149 +192,149 @@ k_edge_fwd_rows(EdgeTiles tl, const bf16* __restrict__ e_in, bf16* __restrict__ 
       r[rb] = tl.receivers[erow(d, rb)];
     }
   };
-  auto issue = [&](int4 d, const int (&s)[2], const int (&r)[2], RowLoads& L) {
+  // The streams of one 16-row half of a tile for this lane's row: its four
+  // 8-feature runs of the edge latent and of the two gathered node products.
+  // The next half's streams are in flight while a half is computed.
+  struct HalfF {
+    uint4 e[4], ps[4], pr[4];
+  };
+  auto issue_half = [&](int4 d, int rb, int snd, int rcv, HalfF& H) {
+    const bf16* ep = e_in + (size_t)erow(d, rb) * D + 8 * q;
+    const bf16* sp = Pn + (size_t)snd * (2 * D) + 8 * q;
+    const bf16* rp = Pn + (size_t)rcv * (2 * D) + D + 8 * q;
 #pragma unroll
-    for (int rb = 0; rb < 2; ++rb) {
-      const bf16* ep = e_in + (size_t)erow(d, rb) * D + 8 * q;
-      const bf16* sp = Pn + (size_t)s[rb] * (2 * D) + 8 * q;
-      const bf16* rp = Pn + (size_t)r[rb] * (2 * D) + D + 8 * q;
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        L.e[rb][k] = *reinterpret_cast<const uint4*>(ep + 32 * k);
-        L.ps[rb][k] = *reinterpret_cast<const uint4*>(sp + 32 * k);
-        L.pr[rb][k] = *reinterpret_cast<const uint4*>(rp + 32 * k);
-      }
+    for (int k = 0; k < 4; ++k) {
+      H.e[k] = *reinterpret_cast<const uint4*>(ep + 32 * k);
+      H.ps[k] = *reinterpret_cast<const uint4*>(sp + 32 * k);
+      H.pr[k] = *reinterpret_cast<const uint4*>(rp + 32 * k);
     }
   };
-
-  int4 d0 = desc(t), d1 = desc(t + stride), d2 = desc(t + 2 * stride);
-  int s0[2], r0[2], s1[2], r1[2];
-  load_sr(d0, s0, r0);
-  load_sr(d1, s1, r1);
-  RowLoads cur;
-  issue(d0, s0, r0, cur);
   float* stage = S.stage[wv];
 
-  for (; t < tend; t += stride) {
+  // One half (rows rb*16 .. +16) of tile d0 with its streams in H.
+  auto half = [&](HalfF& H, int4 d0, int rb, int segraw, bool chunk, int nv, int& j, float2& carry) {
     const int n = tile_rows(d0);
-    // in-segment starts of the tile's nodes (lane j: rowptr of node j)
-    const bool chunk = d0.y < 0;
-    const int nv = chunk ? 1 : d0.y - d0.x;
-    const int segraw = tl.rowptr[min(d0.x + lane, max(d0.x, d0.y))];
-    const int4 d3 = desc(t + 3 * stride);
-    int s2[2], r2[2];
-    load_sr(d2, s2, r2);
-
-    RowLoads nxt;
-    float2 carry = {0.f, 0.f};
-    int j = 0;  // next node whose sum is open
+    // ---- z1 = b1 + P_s + P_r + W1e e
+    f32x4 acc[8];
 #pragma unroll
-    for (int rb = 0; rb < 2; ++rb) {
-      // ---- z1 = b1 + P_s + P_r + W1e e
-      f32x4 acc[8];
+    for (int ob = 0; ob < 8; ++ob) {
+      acc[ob] = *reinterpret_cast<const f32x4*>(S.b1 + fo(ob, q));
+      const bf16x8 sel = (ob & 1) ? sel1 : sel0;
+      acc[ob] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sel, as_frag(H.ps[ob >> 1]), acc[ob], 0, 0, 0);
+      acc[ob] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sel, as_frag(H.pr[ob >> 1]), acc[ob], 0, 0, 0);
+    }
+#pragma unroll
+    for (int s = 0; s < 4; ++s)
 #pragma unroll
       for (int ob = 0; ob < 8; ++ob) {
-        acc[ob] = *reinterpret_cast<const f32x4*>(S.b1 + fo(ob, q));
-        const bf16x8 sel = (ob & 1) ? sel1 : sel0;
-        acc[ob] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sel, as_frag(cur.ps[rb][ob >> 1]), acc[ob], 0, 0, 0);
-        acc[ob] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sel, as_frag(cur.pr[rb][ob >> 1]), acc[ob], 0, 0, 0);
+        const bf16x8 a = *reinterpret_cast<const bf16x8*>(wchunk(S.W1, ob * 16 + i, 4 * s + q));
+        acc[ob] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, as_frag(H.e[s]), acc[ob], 0, 0, 0);
       }
-      if (rb == 1) issue(d1, s1, r1, nxt);  // node products consumed: next tile in flight
+    // ---- a1 = relu(z1) as the B operand of the second layer
+    bf16x8 a1[4];
 #pragma unroll
-      for (int s = 0; s < 4; ++s)
+    for (int s = 0; s < 4; ++s)
 #pragma unroll
-        for (int ob = 0; ob < 8; ++ob) {
-          const bf16x8 a = *reinterpret_cast<const bf16x8*>(wchunk(S.W1, ob * 16 + i, 4 * s + q));
-          acc[ob] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, as_frag(cur.e[rb][s]), acc[ob], 0, 0, 0);
-        }
-      // ---- a1 = relu(z1) as the B operand of the second layer
-      bf16x8 a1[4];
+      for (int r = 0; r < 4; ++r) {
+        a1[s][r] = (bf16)relu(acc[2 * s][r]);
+        a1[s][4 + r] = (bf16)relu(acc[2 * s + 1][r]);
+      }
+    const int row = rb * 16 + i;
+    if (a1_out != nullptr && row < n) {
+      bf16* ap = a1_out + ((size_t)d0.z + row) * D + 8 * q;
 #pragma unroll
-      for (int s = 0; s < 4; ++s)
+      for (int s = 0; s < 4; ++s) *reinterpret_cast<uint4*>(ap + 32 * s) = __builtin_bit_cast(uint4, a1[s]);
+    }
+    // ---- z2 = b2 + W2 a1
+#pragma unroll
+    for (int ob = 0; ob < 8; ++ob) acc[ob] = *reinterpret_cast<const f32x4*>(S.b2 + fo(ob, q));
+#pragma unroll
+    for (int s = 0; s < 4; ++s)
+#pragma unroll
+      for (int ob = 0; ob < 8; ++ob) {
+        const bf16x8 a = *reinterpret_cast<const bf16x8*>(wchunk(S.W2, ob * 16 + i, 4 * s + q));
+        acc[ob] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, a1[s], acc[ob], 0, 0, 0);
+      }
+    // ---- LayerNorm over the row's 128 features (4 lanes x 32)
+    float sm = 0.f;
+#pragma unroll
+    for (int ob = 0; ob < 8; ++ob)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) sm += acc[ob][r];
+    const float mean = sum_rowlanes(sm) * (1.0f / D);
+    float sq = 0.f;
+#pragma unroll
+    for (int ob = 0; ob < 8; ++ob) {
+      acc[ob] -= mean;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) sq += acc[ob][r] * acc[ob][r];
+    }
+    const float rstd = __builtin_amdgcn_rsqf(sum_rowlanes(sq) * (1.0f / D) + eps);
+    float* srow = stage + i * RW_LDM;
+#pragma unroll
+    for (int ob = 0; ob < 8; ++ob) {
+      const f32x4 ga = *reinterpret_cast<const f32x4*>(S.g + fo(ob, q));
+      const f32x4 be = *reinterpret_cast<const f32x4*>(S.bt + fo(ob, q));
+      acc[ob] = ga * (acc[ob] * rstd) + be;  // message m
+      *reinterpret_cast<f32x4*>(srow + fo(ob, q)) = acc[ob];
+    }
+    // ---- e_out = e + m
+    if (write_e) {
+      uint4 o[4];
+#pragma unroll
+      for (int s = 0; s < 4; ++s) {
+        f32x4 lo = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sel0, as_frag(H.e[s]), acc[2 * s], 0, 0, 0);
+        f32x4 hi = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sel1, as_frag(H.e[s]), acc[2 * s + 1], 0, 0, 0);
+        bf16x8 v;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          a1[s][r] = (bf16)relu(acc[2 * s][r]);
-          a1[s][4 + r] = (bf16)relu(acc[2 * s + 1][r]);
+          v[r] = (bf16)lo[r];
+          v[4 + r] = (bf16)hi[r];
         }
-      if (a1_out != nullptr && rb * 16 + i < n) {
-        bf16* ap = a1_out + ((size_t)d0.z + rb * 16 + i) * D + 8 * q;
-#pragma unroll
-        for (int s = 0; s < 4; ++s) *reinterpret_cast<uint4*>(ap + 32 * s) = __builtin_bit_cast(uint4, a1[s]);
+        o[s] = __builtin_bit_cast(uint4, v);
       }
-      // ---- z2 = b2 + W2 a1
+      if (row < n) {
+        bf16* op = e_out + ((size_t)d0.z + row) * D + 8 * q;
 #pragma unroll
-      for (int ob = 0; ob < 8; ++ob) acc[ob] = *reinterpret_cast<const f32x4*>(S.b2 + fo(ob, q));
-#pragma unroll
-      for (int s = 0; s < 4; ++s)
-#pragma unroll
-        for (int ob = 0; ob < 8; ++ob) {
-          const bf16x8 a = *reinterpret_cast<const bf16x8*>(wchunk(S.W2, ob * 16 + i, 4 * s + q));
-          acc[ob] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, a1[s], acc[ob], 0, 0, 0);
-        }
-      // ---- LayerNorm over the row's 128 features (4 lanes x 32)
-      float sm = 0.f;
-#pragma unroll
-      for (int ob = 0; ob < 8; ++ob)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) sm += acc[ob][r];
-      const float mean = sum_rowlanes(sm) * (1.0f / D);
-      float sq = 0.f;
-#pragma unroll
-      for (int ob = 0; ob < 8; ++ob) {
-        acc[ob] -= mean;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) sq += acc[ob][r] * acc[ob][r];
+        for (int s = 0; s < 4; ++s) *reinterpret_cast<uint4*>(op + 32 * s) = o[s];
       }
-      const float rstd = __builtin_amdgcn_rsqf(sum_rowlanes(sq) * (1.0f / D) + eps);
-      float* srow = stage + i * RW_LDM;
-#pragma unroll
-      for (int ob = 0; ob < 8; ++ob) {
-        const f32x4 ga = *reinterpret_cast<const f32x4*>(S.g + fo(ob, q));
-        const f32x4 be = *reinterpret_cast<const f32x4*>(S.bt + fo(ob, q));
-        acc[ob] = ga * (acc[ob] * rstd) + be;  // message m
-        *reinterpret_cast<f32x4*>(srow + fo(ob, q)) = acc[ob];
-      }
-      // ---- e_out = e + m
-      const int row = rb * 16 + i;
-      if (write_e) {
-        uint4 o[4];
-#pragma unroll
-        for (int s = 0; s < 4; ++s) {
-          f32x4 lo = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sel0, as_frag(cur.e[rb][s]), acc[2 * s], 0, 0, 0);
-          f32x4 hi = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sel1, as_frag(cur.e[rb][s]), acc[2 * s + 1], 0, 0, 0);
-          bf16x8 v;
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            v[r] = (bf16)lo[r];
-            v[4 + r] = (bf16)hi[r];
-          }
-          o[s] = __builtin_bit_cast(uint4, v);
-        }
-        if (row < n) {
-          bf16* op = e_out + ((size_t)d0.z + row) * D + 8 * q;
-#pragma unroll
-          for (int s = 0; s < 4; ++s) *reinterpret_cast<uint4*>(op + 32 * s) = o[s];
-        }
-      }
-      wave_lds_sync();
-      seg_pass(stage, lane, segraw, d0.z, chunk, n, nv, rb * 16, j, carry, [&](int jj, float2 v) {
-        float* dst = !chunk ? agg + (size_t)(d0.x + jj) * D : slots + (size_t)(-1 - d0.y) * D;
-        *reinterpret_cast<float2*>(dst + 2 * lane) = v;
-      });
-      wave_lds_sync();
     }
-    cur = nxt;
+    wave_lds_sync();
+    seg_pass(stage, lane, segraw, d0.z, chunk, n, nv, rb * 16, j, carry, [&](int jj, float2 v) {
+      float* dst = !chunk ? agg + (size_t)(d0.x + jj) * D : slots + (size_t)(-1 - d0.y) * D;
+      *reinterpret_cast<float2*>(dst + 2 * lane) = v;
+    });
+    wave_lds_sync();
+  };
+
+  // issue order = use order, so each wait covers only older requests
+  int4 d0 = desc(t), d1 = desc(t + stride);
+  int sc[2], rc[2], sn[2], rn[2];
+  load_sr(d0, sc, rc);
+  HalfF A, B;
+  issue_half(d0, 0, sc[0], rc[0], A);
+  for (; t < tend; t += stride) {
+    const bool chunk = d0.y < 0;
+    const int nv = chunk ? 1 : d0.y - d0.x;
+    // in-segment starts of the tile's nodes (lane j: rowptr of node j)
+    const int segraw = tl.rowptr[min(d0.x + lane, max(d0.x, d0.y))];
+    const int4 d2 = desc(t + 2 * stride);
+    load_sr(d1, sn, rn);
+    issue_half(d0, 1, sc[1], rc[1], B);
+    float2 carry = {0.f, 0.f};
+    int j = 0;  // next node whose sum is open
+    half(A, d0, 0, segraw, chunk, nv, j, carry);
+    issue_half(d1, 0, sn[0], rn[0], A);
+    half(B, d0, 1, segraw, chunk, nv, j, carry);
     d0 = d1;
     d1 = d2;
-    d2 = d3;
 #pragma unroll
     for (int rb = 0; rb < 2; ++rb) {
-      s1[rb] = s2[rb];
-      r1[rb] = r2[rb];
+      sc[rb] = sn[rb];
+      rc[rb] = rn[rb];
     }
   }
 }
-
 
 // ===================================================================== reverse
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));

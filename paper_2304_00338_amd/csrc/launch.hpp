@@ -11,8 +11,10 @@ namespace mgn {
 // [out][in]; W1t/W2t are the transposed copies [in][out].  Biases and
 // LayerNorm parameters are the caller's float32 values.
 struct MlpW {
-  const void* W1p;  // row-permuted copy of the edge-latent part of W1 (edge MLPs)
-  const void* W2p;  // row-permuted copy of W2 (edge MLPs)
+  const void* W1p;   // row-permuted copy of W1 (edge MLPs: its edge-latent column block)
+  const void* W2p;   // row-permuted copy of W2
+  const void* W1sp;  // edge MLPs: row-permuted sender column block of W1
+  const void* W1rp;  // edge MLPs: row-permuted receiver column block of W1
   const void* W1;
   const void* W1t;
   const void* W2;
