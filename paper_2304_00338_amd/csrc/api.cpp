@@ -20,6 +20,9 @@ namespace {
 constexpr int D = 128;
 constexpr int kPartBlocks = 512;       // persistent blocks of the backward kernels
 constexpr int64_t kPartStride = 49664; // largest per-block partial (node MLP)
+// node-MLP partial layout = its parameter order: W1 [128][256], b1, W2, b2
+// (49408 floats), then gamma, beta
+constexpr int kNodeGammaPart = 49408;
 
 struct Off {
   int64_t W1 = 0, b1 = 0, W2 = 0, b2 = 0, g = -1, bt = -1, size = 0;
@@ -138,7 +141,7 @@ struct Layout {
   size_t e_off = 0, h_off = 0, agg_off = 0, P_off = 0, a1_off = 0;  // within a set
   size_t node_in = 0, K = 0, slots = 0;
   // backward
-  size_t ebar = 0, zbar = 0, dz = 0, hb_a = 0, hb_b = 0, aggbar = 0, R = 0, part = 0, kbar = 0, ystage = 0, gin = 0;
+  size_t ebar = 0, zbar = 0, dz = 0, nstr = 0, hb_a = 0, hb_b = 0, aggbar = 0, R = 0, part = 0, kbar = 0, ystage = 0, gin = 0;
   size_t total = 0;
 };
 
@@ -146,11 +149,11 @@ struct Layout {
 
 enum Kern {
   K_PACK, K_NODE_ENC, K_EDGE_ENC, K_EDGE_FWD, K_FIXUP, K_NODE_FWD, K_DECODER, K_DECODER_BWD, K_NODE_BWD,
-  K_EDGE_BWD, K_SRCSUM, K_EDGE_ENC_BWD, K_NODE_ENC_BWD, K_REDUCE, K_LINCOMB, K_WGRAD, K_COUNT
+  K_EDGE_BWD, K_SRCSUM, K_EDGE_ENC_BWD, K_NODE_ENC_BWD, K_REDUCE, K_LINCOMB, K_WGRAD, K_EMIT, K_WGRAD_NODE, K_COUNT
 };
 const char* const kKernName[K_COUNT] = {
     "pack", "node_enc", "edge_enc", "edge_fwd", "slot_fixup", "node_fwd", "decoder", "decoder_bwd", "node_bwd",
-    "edge_bwd", "node_srcsum", "edge_enc_bwd", "node_enc_bwd", "reduce", "lincomb", "wgrad"};
+    "edge_bwd", "node_srcsum", "edge_enc_bwd", "node_enc_bwd", "reduce", "lincomb", "wgrad", "emit_p", "wgrad_node"};
 
 struct Prof {
   bool on = false;
@@ -269,6 +272,9 @@ void plan(Ctx& c) {
     o = al256(o + (size_t)E * D * c.se);
     L.dz = o;
     o = al256(o + (keep_a1 ? (size_t)E * D * 2 : 0));
+    // bf16 node backward: the a1, dz2, dz1 streams of one node MLP
+    L.nstr = o;
+    o = al256(o + (keep_a1 ? (size_t)3 * N * D * 2 : 0));
     L.hb_a = o;
     o = al256(o + (size_t)N * D * 4);
     L.hb_b = o;
@@ -421,8 +427,13 @@ struct Run {
       if (g.n_long > 0) LAUNCH(K_FIXUP, launch_slot_fixup(g.long_nodes, g.n_long, slots(), agg_l(k, l), s));
       MlpW nx;
       if (!last) nx = W(M.edge[l + 1], M.p_edge[l + 1]);
-      LAUNCH(K_NODE_FWD, launch_node_fwd(prec, N, h_l(k, l), agg_l(k, l), W(M.node[l], M.p_node[l]), last ? nullptr : &nx, eps,
-                              h_l(k, l + 1), last ? nullptr : P_l(k, l + 1), s));
+      if (prec == MGN_BF16) {
+        LAUNCH(K_NODE_FWD, launch_node_fwd_rows(N, h_l(k, l), agg_l(k, l), W(M.node[l], M.p_node[l]), eps, h_l(k, l + 1), s));
+        if (!last) LAUNCH(K_EMIT, launch_emit_rows(N, h_l(k, l + 1), nx, P_l(k, l + 1), s));
+      } else {
+        LAUNCH(K_NODE_FWD, launch_node_fwd(prec, N, h_l(k, l), agg_l(k, l), W(M.node[l], M.p_node[l]), last ? nullptr : &nx,
+                                eps, h_l(k, l + 1), last ? nullptr : P_l(k, l + 1), s));
+      }
     }
     LAUNCH(K_DECODER, launch_decoder(prec, N, h_l(k, m), W(M.dec, M.p_dec), out, s));
     return MGN_OK;
@@ -449,9 +460,19 @@ struct Run {
     for (int l = m - 1; l >= 0; --l) {
       const Off& oe = M.edge[l];
       const Off& on = M.node[l];
-      LAUNCH(K_NODE_BWD, launch_node_bwd(prec, N, h_l(k, l), agg_l(k, l), hb_cur, W(on, M.p_node[l]), eps, hb_part, aggbar, pt,
-                              &nb, s));
-      if ((rc = reduce(nb, 0, 1, (int)on.size, grad, on.W1, 0)) != MGN_OK) return rc;
+      if (prec == MGN_BF16) {
+        char* ns = ws + c.L.nstr;
+        void *na1 = ns, *ndz2 = ns + (size_t)N * D * 2, *ndz1 = ns + (size_t)2 * N * D * 2;
+        LAUNCH(K_NODE_BWD, launch_node_bwd_rows(N, h_l(k, l), agg_l(k, l), hb_cur, W(on, M.p_node[l]), eps, hb_part, aggbar,
+                                     na1, ndz2, ndz1, pt, &nb, s));
+        if ((rc = reduce(nb, kNodeGammaPart, 1, 2 * D, grad, on.g, 0)) != MGN_OK) return rc;
+        LAUNCH(K_WGRAD_NODE, launch_wgrad_node(N, h_l(k, l), agg_l(k, l), ndz1, ndz2, na1, pt, &nb, s));
+        if ((rc = reduce(nb, 0, 1, kNodeGammaPart, grad, on.W1, 0)) != MGN_OK) return rc;
+      } else {
+        LAUNCH(K_NODE_BWD, launch_node_bwd(prec, N, h_l(k, l), agg_l(k, l), hb_cur, W(on, M.p_node[l]), eps, hb_part, aggbar,
+                                pt, &nb, s));
+        if ((rc = reduce(nb, 0, 1, (int)on.size, grad, on.W1, 0)) != MGN_OK) return rc;
+      }
       if (E == 0) {
         // no edges: the edge MLP gets no gradient and every R is zero
         LAUNCH(K_EDGE_BWD, launch_fill(R, N * D, 0.f, s));

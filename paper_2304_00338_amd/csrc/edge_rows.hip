@@ -5,17 +5,8 @@
 //
 // Work split.  Each of the 8 waves of a block runs its own persistent loop
 // over tiles; the only block barrier is the one after the weights are
-// staged in LDS.  Lane l (i = l & 15, q = l >> 4) holds rows i and 16 + i of
-// the wave's tile and 32 features of each: the runs [32s + 8q, 32s + 8q + 8)
-// for s < 4, so the four lanes of a row read or write 64 contiguous bytes
-// (bf16) per instruction.  The GEMMs run transposed (C[feature][row] =
-// W x^T): the A operand is a 16-row block of the row-permuted weights
-// (perm_row) read from LDS, the B operand at K step s is the lane's run s of
-// x, and the C fragment of output block ob gives the lane the features
-// fo(ob, q) + r, r < 4, which are again its runs.  So GEMM outputs are
-// already the next GEMM's B operand, and every LayerNorm statistic is a sum
-// over the lane's 32 values plus two cross-lane steps (the four lanes that
-// share a row).
+// staged in LDS.  A tile is two 16-row blocks in the lane layout of
+// rows_common.hpp.
 //
 // Adds of bf16 inputs into fp32 accumulators (the node products P_s + P_r
 // and the residual e + m) are MFMAs with a 0/1 selection operand: one
@@ -24,23 +15,13 @@
 // Node sums: the wave stages each 16-row half of the messages in its own
 // LDS area and sums every in-segment in ascending row order from 0.0, so a
 // node's aggregate does not depend on where its segment sits in a tile.
-#include "dev_common.hpp"
+#include "rows_common.hpp"
 #include "launch.hpp"
 
 namespace mgn {
 namespace dev {
 
 constexpr int RW_LDM = D + 4;  // LDS row stride of a wave's message half-tile (fp32)
-
-// First feature of the 4-feature run of output block ob held by lane group q.
-__device__ __forceinline__ int fo(int ob, int q) { return 32 * (ob >> 1) + 8 * q + 4 * (ob & 1); }
-
-// The staged [128][128] bf16 weights keep rows unpadded and XOR-swizzle the
-// 16-byte chunks of row R, so that both the row reads of A fragments (8
-// lanes: 8 consecutive rows, one chunk) and the transposing reads (16 lanes:
-// 4 consecutive rows x 4 chunks) hit distinct banks.
-__device__ __forceinline__ int wswz(int R) { return 4 * (R & 3) + ((R >> 2) & 3); }
-__device__ __forceinline__ const bf16* wchunk(const bf16* W, int R, int C) { return W + R * D + ((C ^ wswz(R)) << 3); }
 
 struct __attribute__((aligned(16))) RowsLds {
   __attribute__((aligned(16))) bf16 W1[D * D];
@@ -52,36 +33,7 @@ struct __attribute__((aligned(16))) RowsLds {
   __attribute__((aligned(16))) float stage[NW][16 * RW_LDM];
 };
 
-typedef __attribute__((ext_vector_type(4))) unsigned int u32x4;
-
-// The 0/1 operand that adds a B fragment (run s: features 32s + 8q + j) into
-// the C fragment of output block ob = 2s + h: A[m][k] = 1 iff k = (m/4)*8 +
-// 4h + m%4.
-__device__ __forceinline__ bf16x8 select_frag(int h, int i, int q) {
-  bf16x8 a;
-#pragma unroll
-  for (int j = 0; j < 8; ++j) a[j] = (bf16)(((i >> 2) == q && j == 4 * h + (i & 3)) ? 1.f : 0.f);
-  return a;
-}
-
-__device__ __forceinline__ bf16x8 as_frag(const uint4& u) { return __builtin_bit_cast(bf16x8, u); }
-
 __device__ __forceinline__ int tile_rows(int4 d) { return d.w - d.z; }
-
-// max(x, 0) as one integer max on the bit pattern (negative floats have the
-// sign bit set, so they compare below +0.0 as signed integers).
-__device__ __forceinline__ float relu(float x) { return __int_as_float(max(__float_as_int(x), 0)); }
-
-template <int CTRL>
-__device__ __forceinline__ float xlane(float v) {
-  return __shfl_xor(v, CTRL, 64);
-}
-// Sum over the four lanes that hold the same row (q = 0..3).
-__device__ __forceinline__ float sum_rowlanes(float s) {
-  s += xlane<16>(s);
-  s += xlane<32>(s);
-  return s;
-}
 
 // In-segment node sums over one staged 16-row half [lo_row, lo_row + 16) of
 // a tile (rows past the tile's end are never inside a segment).  For a tile
@@ -129,14 +81,8 @@ k_edge_fwd_rows(EdgeTiles tl, const bf16* __restrict__ e_in, bf16* __restrict__ 
   const int tid = threadIdx.x, lane = tid & 63, i = lane & 15, q = lane >> 4;
   const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
   {
-    const bf16* W1p = (const bf16*)w.W1p;
-    const bf16* W2p = (const bf16*)w.W2p;
-    for (int idx = tid; idx < D * D / 8; idx += NT) {
-      const int row = idx >> 4, c = (idx & 15) * 8;
-      const int cs = ((idx & 15) ^ wswz(row)) << 3;
-      *reinterpret_cast<uint4*>(S.W1 + row * D + cs) = *reinterpret_cast<const uint4*>(W1p + row * D + c);
-      *reinterpret_cast<uint4*>(S.W2 + row * D + cs) = *reinterpret_cast<const uint4*>(W2p + row * D + c);
-    }
+    stage_weights<D>(S.W1, (const bf16*)w.W1p, tid);
+    stage_weights<D>(S.W2, (const bf16*)w.W2p, tid);
     if (tid < D) {
       S.b1[tid] = w.b1[tid];
       S.b2[tid] = w.b2[tid];
@@ -146,24 +92,11 @@ k_edge_fwd_rows(EdgeTiles tl, const bf16* __restrict__ e_in, bf16* __restrict__ 
   }
   __syncthreads();
 
-  // Tile order: blocks are dealt to the 8 XCDs round-robin, so the waves of
-  // the blocks of one XCD walk one contiguous eighth of the tiles (their
-  // node products then mostly share that XCD's L2).
-  const int64_t NTL = tl.n_tiles;
-  const int G = gridDim.x;
-  int64_t t, stride, tend;
-  if ((G & 7) == 0) {
-    const int x = blockIdx.x & 7, per = G >> 3;
-    const int64_t chunk = (NTL + 7) >> 3;
-    const int64_t lo = x * chunk;
-    tend = min(NTL, lo + chunk);
-    t = lo + (int64_t)(blockIdx.x >> 3) * NW + wv;
-    stride = (int64_t)per * NW;
-  } else {
-    t = (int64_t)blockIdx.x * NW + wv;
-    stride = (int64_t)G * NW;
-    tend = NTL;
-  }
+  // XCD-contiguous tile ranges: the node products gathered by one XCD's
+  // waves then mostly share that XCD's L2.
+  const UnitRange ur = unit_range(tl.n_tiles, wv);
+  int64_t t = ur.t;
+  const int64_t stride = ur.stride, tend = ur.end;
   if (t >= tend) return;
 
   const bf16x8 sel0 = select_frag(0, i, q), sel1 = select_frag(1, i, q);
@@ -337,34 +270,6 @@ k_edge_fwd_rows(EdgeTiles tl, const bf16* __restrict__ e_in, bf16* __restrict__ 
 }
 
 // ===================================================================== reverse
-typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-
-// Transposing LDS read (gfx950 ds_read_b64_tr_b16): within each group of 16
-// lanes, result lane l, element j' is element l & 3 of the 8 bytes addressed
-// by lane 4j' + (l >> 2).
-__device__ __forceinline__ bf16x4 lds_tr(const bf16* p) {
-  typedef __attribute__((address_space(3))) bf16x4 lds_v4;
-  typedef __attribute__((address_space(3))) bf16 lds_b;
-  return __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_v4*)((lds_b*)p));
-}
-__device__ __forceinline__ bf16x8 cat8(bf16x4 lo, bf16x4 hi) {
-  return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-}
-
-// A operand of the transposed product C = W^T x from the row-permuted LDS
-// copy WP of W (rows = output features o of W): A[m][k] = W[o][k'] with
-// output slot m of block ob being input feature k' = perm_row(16ob + m) and
-// k = 8q + 4t + j' running over o = 32s + 8q + 4t + j' (lane q's run s).
-// Row o of W sits at packed row 16(2s + t) + 4q + j'; lane 4j' + c supplies
-// the 4 columns perm_row(16ob + 4c + 0..3) of it (one 8-byte piece).
-__device__ __forceinline__ bf16x8 wt_frag(const bf16* WP, int ob, int s, int lam, int q) {
-  const int jp = lam >> 2, c = lam & 3;
-  const int R = (2 * s) * 16 + 4 * q + jp, C = 4 * (ob >> 1) + c, h = 4 * (ob & 1);
-  const bf16* p0 = wchunk(WP, R, C) + h;
-  const bf16* p1 = wchunk(WP, R + 16, C) + h;
-  return cat8(lds_tr(p0), lds_tr(p1));
-}
-
 // Given ebar_in = dL/de_out (absent for the last block), aggbar, and the
 // saved first-layer activations a1 of the edge MLP: mbar = ebar_in +
 // aggbar[receiver]; back through the LayerNorm and the MLP to zbar = dL/dz1
@@ -380,14 +285,8 @@ k_edge_bwd_rows(EdgeTiles tl, const bf16* __restrict__ a1_in, const float* __res
   const int tid = threadIdx.x, lane = tid & 63, i = lane & 15, q = lane >> 4;
   const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
   {
-    const bf16* W1p = (const bf16*)w.W1p;
-    const bf16* W2p = (const bf16*)w.W2p;
-    for (int idx = tid; idx < D * D / 8; idx += NT) {
-      const int row = idx >> 4, c = (idx & 15) * 8;
-      const int cs = ((idx & 15) ^ wswz(row)) << 3;
-      *reinterpret_cast<uint4*>(S.W1 + row * D + cs) = *reinterpret_cast<const uint4*>(W1p + row * D + c);
-      *reinterpret_cast<uint4*>(S.W2 + row * D + cs) = *reinterpret_cast<const uint4*>(W2p + row * D + c);
-    }
+    stage_weights<D>(S.W1, (const bf16*)w.W1p, tid);
+    stage_weights<D>(S.W2, (const bf16*)w.W2p, tid);
     if (tid < D) {
       S.b2[tid] = w.b2[tid];
       S.g[tid] = w.gamma[tid];
@@ -395,21 +294,9 @@ k_edge_bwd_rows(EdgeTiles tl, const bf16* __restrict__ a1_in, const float* __res
   }
   __syncthreads();
 
-  const int64_t NTL = tl.n_tiles;
-  const int G = gridDim.x;
-  int64_t t, stride, tend;
-  if ((G & 7) == 0) {
-    const int x = blockIdx.x & 7, per = G >> 3;
-    const int64_t chunk = (NTL + 7) >> 3;
-    const int64_t lo = x * chunk;
-    tend = min(NTL, lo + chunk);
-    t = lo + (int64_t)(blockIdx.x >> 3) * NW + wv;
-    stride = (int64_t)per * NW;
-  } else {
-    t = (int64_t)blockIdx.x * NW + wv;
-    stride = (int64_t)G * NW;
-    tend = NTL;
-  }
+  const UnitRange ur = unit_range(tl.n_tiles, wv);
+  int64_t t = ur.t;
+  const int64_t stride = ur.stride, tend = ur.end;
 
   const int4* tiles = reinterpret_cast<const int4*>(tl.tiles);
   auto desc = [&](int64_t tt) -> int4 {

@@ -93,6 +93,20 @@ hipError_t launch_edge_bwd_rows(const EdgeTiles& t, const void* a1, const float*
 // bf16 dW1e = sum zbar^T e, dW2 = sum dz2^T a1, db2 = sum dz2 as per-block partials.
 hipError_t launch_wgrad2(int64_t M, const void* zbar, const void* e, const void* dz, const void* a1,
                          const Partials& part, int* nblocks, hipStream_t s);
+// bf16 node phase with one wave per 16-node block (uses MlpW::W1p / W2p of
+// the node MLP): h_out = h_in + LN(MLP([h_in, agg])), h_out may alias h_in.
+hipError_t launch_node_fwd_rows(int64_t N, const float* h_in, const float* agg, const MlpW& w, float eps,
+                                float* h_out, hipStream_t s);
+// bf16 node products P = [W1s h; W1r h] of the next edge layer (W1sp / W1rp).
+hipError_t launch_emit_rows(int64_t N, const float* h, const MlpW& next_edge, void* P, hipStream_t s);
+// bf16 node backward: hbar_part, aggbar, the bf16 streams a1, dz2, dz1 and
+// per-block partials of dgamma, dbeta (node-MLP partial layout).
+hipError_t launch_node_bwd_rows(int64_t N, const float* h, const float* agg, const float* hbar_in, const MlpW& w,
+                                float eps, float* hbar_part, float* aggbar, void* a1, void* dz2, void* dz1,
+                                const Partials& part, int* nblocks, hipStream_t s);
+// bf16 node-MLP weight gradients dW1, db1, dW2, db2 from those streams.
+hipError_t launch_wgrad_node(int64_t N, const float* h, const float* agg, const void* dz1, const void* dz2,
+                             const void* a1, const Partials& part, int* nblocks, hipStream_t s);
 hipError_t launch_slot_fixup(const int32_t* long_nodes, int64_t n_long, const float* slots, float* dst,
                              hipStream_t s);
 hipError_t launch_node_fwd(int prec, int64_t N, const float* h_in, const float* agg, const MlpW& w,
