@@ -36,30 +36,60 @@ def log(*a):
 
 def kernel_bytes(kind, N, E, n_tiles, prec, have_ebar=True, write_e=True, keep_a1=True):
     """Algorithmic HBM bytes of one launch of the kernels this build runs:
-    every input read once and every output written once (node products P
-    are [N][2D] in the operand precision; bf16 edge latents, a1, zbar and
-    dz2 streams are 2 bytes per element, gradients fp32)."""
+    every input read once and every output written once.  In bf16 the edge
+    latents, their gradient stream, node products P ([N][2D]) and the a1 /
+    zbar / dz streams are 2 bytes per element; node latents, aggregates and
+    node gradients are fp32 throughout."""
     se = 2 if prec == "bf16" else 4
     row, frow = D * se, D * 4
+    erow = row if prec == "bf16" else frow  # edge-gradient stream
     tiles = n_tiles * 16 + 4 * (N + 1)
+    bf = prec == "bf16"
     if kind == "edge_fwd":
-        return (E * (row + 8 + (row if write_e else 0) + (row if keep_a1 and prec == "bf16" else 0))
+        return (E * (row + 8 + (row if write_e else 0) + (row if keep_a1 and bf else 0))
                 + N * (2 * row + frow) + tiles)
     if kind == "edge_bwd":
-        if prec == "bf16":  # from the saved a1: reads a1, ebar_in, aggbar; writes ebar_out, zbar, dz2, R
-            return (E * (row + (frow if have_ebar else 0) + 4 + frow + 2 * row)
+        if bf:  # from the saved a1: reads a1, ebar_in, aggbar; writes ebar_out, zbar, dz2, R
+            return (E * (row + (erow if have_ebar else 0) + 4 + erow + 2 * row)
                     + N * (frow + frow) + tiles)
         return (E * (row + (frow if have_ebar else 0) + frow + row + 8)
                 + N * (2 * row + frow + frow) + tiles)
     if kind == "wgrad":
-        return E * row * (4 if prec == "bf16" else 2)
+        return E * row * (4 if bf else 2)
     if kind == "node_srcsum":
         return E * (row + 4) + N * (4 + 4 * frow)
     if kind == "node_fwd":
-        return N * (3 * frow + 2 * row)
+        return N * 3 * frow if bf else N * (3 * frow + 2 * row)
+    if kind == "emit_p":
+        return N * (frow + 2 * row)
     if kind == "node_bwd":
-        return N * (5 * frow)
+        return N * (5 * frow + (3 * row if bf else 0))
+    if kind == "wgrad_node":
+        return N * (2 * frow + 3 * row)
+    if kind == "edge_enc":
+        return E * (16 + row)
+    if kind == "edge_enc_bwd":
+        return E * (16 + erow)
+    if kind == "node_enc":
+        return N * (32 + frow + 2 * row)
+    if kind == "decoder":
+        return N * (frow + 16)
     return None
+
+
+def step_bytes(kind, N, E, n_tiles, prec, m):
+    """Algorithmic bytes of every launch of `kind` in one fwd+bwd step (one
+    saving MGN call and its backward), or None."""
+    if kind == "edge_fwd":
+        return sum(kernel_bytes(kind, N, E, n_tiles, prec, write_e=(l < m - 1)) for l in range(m))
+    if kind == "edge_bwd":
+        return sum(kernel_bytes(kind, N, E, n_tiles, prec, have_ebar=(l < m - 1)) for l in range(m))
+    if kind == "emit_p":
+        return (m - 1) * kernel_bytes(kind, N, E, n_tiles, prec)
+    if kind in ("wgrad", "node_srcsum", "node_fwd", "node_bwd", "wgrad_node"):
+        return m * kernel_bytes(kind, N, E, n_tiles, prec)
+    b = kernel_bytes(kind, N, E, n_tiles, prec)
+    return b
 
 
 def source_digest():
@@ -331,6 +361,9 @@ def main():
         "mgn_calls_per_s_fwd": round(1e3 / fwd_ms, 3),
         "mgn_calls_per_s_fwdbwd": round(1e3 / ms, 3),
         "kernel_ms_per_step": {k: round(v, 3) for k, v in sorted(kern_ms.items(), key=lambda x: -x[1])},
+        "kernel_hbm_gbs": {k: round(sb / (kern_ms[k] * 1e-3) / 1e9, 1)
+                           for k in sorted(kern_ms, key=lambda x: -kern_ms[x])
+                           if (sb := step_bytes(k, N, E, n_tiles, args.precision, m)) is not None},
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(args)

@@ -114,6 +114,7 @@ Model make_model(int m) {
   M.total = o;
   add_pack(M, M.enc_node.W2, D, D, M.p_enc_node.W2, M.p_enc_node.W2t);
   add_pack(M, M.enc_edge.W2, D, D, M.p_enc_edge.W2, M.p_enc_edge.W2t);
+  add_perm(M, M.enc_edge.W2, D, M.p_enc_edge.W2p);
   M.p_edge.resize(m);
   M.p_node.resize(m);
   for (int i = 0; i < m; ++i) {
@@ -266,8 +267,8 @@ void plan(Ctx& c) {
   L.slots = o;
   o = al256(o + (size_t)max_slots(E) * D * 4);
   if (c.save) {
-    L.ebar = o;
-    o = al256(o + (size_t)E * D * 4);
+    L.ebar = o;  // edge-gradient stream, in the edge-latent element type
+    o = al256(o + (size_t)E * D * c.se);
     L.zbar = o;
     o = al256(o + (size_t)E * D * c.se);
     L.dz = o;
@@ -415,7 +416,12 @@ struct Run {
     if (m > 0) e0 = W(M.edge[0], M.p_edge[0]);
     LAUNCH(K_NODE_ENC, launch_node_enc(prec, N, node_in, W(M.enc_node, M.p_enc_node), m > 0 ? &e0 : nullptr, eps, h_l(k, 0),
                             P_l(k, 0), s));
-    if (m > 0) LAUNCH(K_EDGE_ENC, launch_edge_enc(prec, E, efeat, W(M.enc_edge, M.p_enc_edge), eps, e_l(k, 0), s));
+    if (m > 0) {
+      if (prec == MGN_BF16)
+        LAUNCH(K_EDGE_ENC, launch_edge_enc_rows(E, efeat, W(M.enc_edge, M.p_enc_edge), eps, e_l(k, 0), s));
+      else
+        LAUNCH(K_EDGE_ENC, launch_edge_enc(prec, E, efeat, W(M.enc_edge, M.p_enc_edge), eps, e_l(k, 0), s));
+    }
     for (int l = 0; l < m; ++l) {
       const bool last = l == m - 1;
       void* e_out = c.save ? (last ? nullptr : e_l(k, l + 1)) : e_l(k, 0);
@@ -452,7 +458,7 @@ struct Run {
     float* hb_part = (float*)(ws + c.L.hb_b);
     float* aggbar = (float*)(ws + c.L.aggbar);
     float* R = (float*)(ws + c.L.R);
-    float* ebar = (float*)(ws + c.L.ebar);
+    void* ebar = ws + c.L.ebar;  // bf16: the edge-latent element type
     void* zbar = ws + c.L.zbar;
     int nb = 0, rc;
     LAUNCH(K_DECODER_BWD, launch_decoder_bwd(prec, N, h_l(k, m), gout, W(M.dec, M.p_dec), hb_cur, pt, &nb, s));
@@ -486,7 +492,7 @@ struct Run {
         if ((rc = reduce(nb, 16512, 1, D * D + D, grad, oe.W2, 0)) != MGN_OK) return rc;
         if ((rc = reduce(nb, 0, D, D, grad, oe.W1, 3 * D)) != MGN_OK) return rc;
       } else {
-        LAUNCH(K_EDGE_BWD, launch_edge_bwd(prec, tl, e_l(k, l), ebar, l < m - 1 ? 1 : 0, ebar, P_l(k, l), aggbar,
+        LAUNCH(K_EDGE_BWD, launch_edge_bwd(prec, tl, e_l(k, l), (float*)ebar, l < m - 1 ? 1 : 0, (float*)ebar, P_l(k, l), aggbar,
                                 W(oe, M.p_edge[l]), eps, zbar, R, slots(), pt, &nb, s));
         if ((rc = reduce(nb, 16384, 1, (int)(oe.size - 3 * D * D), grad, oe.b1, 0)) != MGN_OK) return rc;
         LAUNCH(K_WGRAD, launch_wgrad(prec, E, zbar, e_l(k, l), pt, &nb, s));
@@ -499,7 +505,10 @@ struct Run {
       if ((rc = reduce(nb, 16384, D, D, grad, oe.W1 + 2 * D, 3 * D)) != MGN_OK) return rc;
     }
     if (m > 0) {
-      LAUNCH(K_EDGE_ENC_BWD, launch_edge_enc_bwd(prec, E, efeat, ebar, W(M.enc_edge, M.p_enc_edge), eps, pt, &nb, s));
+      if (prec == MGN_BF16)
+        LAUNCH(K_EDGE_ENC_BWD, launch_edge_enc_bwd_rows(E, efeat, ebar, W(M.enc_edge, M.p_enc_edge), eps, pt, &nb, s));
+      else
+        LAUNCH(K_EDGE_ENC_BWD, launch_edge_enc_bwd(prec, E, efeat, (float*)ebar, W(M.enc_edge, M.p_enc_edge), eps, pt, &nb, s));
       if ((rc = reduce(nb, 0, 1, (int)M.enc_edge.size, grad, M.enc_edge.W1, 0)) != MGN_OK) return rc;
     }
     LAUNCH(K_NODE_ENC_BWD, launch_node_enc_bwd(prec, N, node_in, hb_cur, W(M.enc_node, M.p_enc_node), eps, gin, pt, &nb, s));

@@ -275,10 +275,12 @@ k_edge_fwd_rows(EdgeTiles tl, const bf16* __restrict__ e_in, bf16* __restrict__ 
 // aggbar[receiver]; back through the LayerNorm and the MLP to zbar = dL/dz1
 // (written out, with dz2 = dL/dz2 for the weight-gradient kernel), the
 // per-receiver sums R of zbar, ebar_out = ebar_in + W1e^T zbar, and
-// per-block partials of db1, dgamma, dbeta.
+// per-block partials of db1, dgamma, dbeta.  The edge-gradient stream is
+// bf16 like the edge latents it belongs to: ebar_out is formed in fp32 and
+// rounded once.
 __global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
-k_edge_bwd_rows(EdgeTiles tl, const bf16* __restrict__ a1_in, const float* __restrict__ ebar_in, int have_ebar,
-                float* __restrict__ ebar_out, const float* __restrict__ aggbar, MlpW w, float eps,
+k_edge_bwd_rows(EdgeTiles tl, const bf16* __restrict__ a1_in, const bf16* ebar_in, int have_ebar,
+                bf16* ebar_out, const float* __restrict__ aggbar, MlpW w, float eps,
                 bf16* __restrict__ zbar, bf16* __restrict__ dz_out, float* __restrict__ R,
                 float* __restrict__ slots, Partials part) {
   __shared__ __align__(16) RowsLds S;
@@ -310,13 +312,11 @@ k_edge_bwd_rows(EdgeTiles tl, const bf16* __restrict__ a1_in, const float* __res
     return r;
   };
   // The streamed inputs of one 16-row half of a tile for this lane's row:
-  // a1 and the incoming edge gradient, in the C layout (features 32q + 4ob
-  // + r).  The next half's streams are in flight while a half is computed;
+  // the four runs of a1 and of the incoming edge gradient.  The next half's streams are in flight while a half is computed;
   // the receiver's aggregate gradient (shared by the ~14 consecutive rows of
   // a receiver, so mostly a cache hit) is loaded when the half starts.
   struct HalfLoads {
-    uint4 a[4];
-    f32x4 eb[8];
+    uint4 a[4], eb[4];
   };
   // All global loads are unconditional from clamped indices (see the
   // forward kernel); without an incoming edge gradient the loaded values are
@@ -332,11 +332,14 @@ k_edge_bwd_rows(EdgeTiles tl, const bf16* __restrict__ a1_in, const float* __res
     const bf16* ap = a1_in + row * D + 8 * q;
 #pragma unroll
     for (int k = 0; k < 4; ++k) H.a[k] = *reinterpret_cast<const uint4*>(ap + 32 * k);
-    const float* ep = ebar_in + row * D;
+    const bf16* ep = ebar_in + row * D + 8 * q;
 #pragma unroll
-    for (int ob = 0; ob < 8; ++ob) {
-      const f32x4 v = *reinterpret_cast<const f32x4*>(ep + fo(ob, q));
-      H.eb[ob] = have_ebar ? v : f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int k = 0; k < 4; ++k) {
+      const uint4 v = *reinterpret_cast<const uint4*>(ep + 32 * k);
+      H.eb[k].x = have_ebar ? v.x : 0u;
+      H.eb[k].y = have_ebar ? v.y : 0u;
+      H.eb[k].z = have_ebar ? v.z : 0u;
+      H.eb[k].w = have_ebar ? v.w : 0u;
     }
   };
   auto load_ag = [&](int recv, f32x4 (&ag)[8]) {
@@ -384,7 +387,7 @@ k_edge_bwd_rows(EdgeTiles tl, const bf16* __restrict__ a1_in, const float* __res
 #pragma unroll
     for (int ob = 0; ob < 8; ++ob) {
       acc[ob] *= rstd;          // xhat
-      ag[ob] += H.eb[ob];     // mbar = ebar_in + aggbar[receiver]
+      ag[ob] += run_block(H.eb, ob);  // mbar = ebar_in + aggbar[receiver]
     }
     // ---- dgamma += sum_rows mbar * xhat, dbeta += sum_rows mbar
 #pragma unroll
@@ -475,15 +478,18 @@ k_edge_bwd_rows(EdgeTiles tl, const bf16* __restrict__ a1_in, const float* __res
     });
     // ---- ebar_out = ebar_in + W1e^T zbar
 #pragma unroll
+    for (int ob = 0; ob < 8; ++ob) acc[ob] = run_block(H.eb, ob);
+#pragma unroll
     for (int s = 0; s < 4; ++s) {
 #pragma unroll
       for (int ob = 0; ob < 8; ++ob)
-        H.eb[ob] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wt_frag(S.W1, ob, s, i, q), zf[s], H.eb[ob], 0, 0, 0);
+        acc[ob] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wt_frag(S.W1, ob, s, i, q), zf[s], acc[ob], 0, 0, 0);
     }
     if (row < n) {
-      float* op = ebar_out + ((size_t)d0.z + row) * D;
+      bf16* op = ebar_out + ((size_t)d0.z + row) * D + 8 * q;
 #pragma unroll
-      for (int ob = 0; ob < 8; ++ob) *reinterpret_cast<f32x4*>(op + fo(ob, q)) = H.eb[ob];
+      for (int s = 0; s < 4; ++s)
+        *reinterpret_cast<uint4*>(op + 32 * s) = __builtin_bit_cast(uint4, pack_run(acc[2 * s], acc[2 * s + 1]));
     }
     wave_lds_sync();
   };
@@ -628,15 +634,15 @@ hipError_t launch_edge_fwd_rows(const EdgeTiles& t, const void* e_in, void* e_ou
   return hipGetLastError();
 }
 
-hipError_t launch_edge_bwd_rows(const EdgeTiles& t, const void* a1, const float* ebar_in, int have_ebar,
-                                float* ebar_out, const float* aggbar, const MlpW& w, float eps, void* zbar, void* dz,
+hipError_t launch_edge_bwd_rows(const EdgeTiles& t, const void* a1, const void* ebar_in, int have_ebar,
+                                void* ebar_out, const float* aggbar, const MlpW& w, float eps, void* zbar, void* dz,
                                 float* R, float* slots, const Partials& part, int* nblocks, hipStream_t s) {
   *nblocks = 0;
   if (t.n_tiles <= 0) return hipSuccess;
   if (t.n_edges <= 0) return hipErrorInvalidValue;
   const int g = rows_grid(t.n_tiles, std::min(kRowsBlocks, part.max_blocks));
   *nblocks = g;
-  hipLaunchKernelGGL(k_edge_bwd_rows, dim3(g), dim3(NT), 0, s, t, (const bf16*)a1, ebar_in, have_ebar, ebar_out,
+  hipLaunchKernelGGL(k_edge_bwd_rows, dim3(g), dim3(NT), 0, s, t, (const bf16*)a1, (const bf16*)ebar_in, have_ebar, (bf16*)ebar_out,
                      aggbar, w, eps, (bf16*)zbar, (bf16*)dz, R, slots, part);
   return hipGetLastError();
 }

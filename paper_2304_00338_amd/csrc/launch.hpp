@@ -85,10 +85,11 @@ hipError_t launch_edge_fwd(int prec, const EdgeTiles& t, const void* e_in, void*
 // (nullable) receives the first-layer activations of every edge.
 hipError_t launch_edge_fwd_rows(const EdgeTiles& t, const void* e_in, void* e_out, int write_e, const void* P,
                                 const MlpW& w, float eps, float* agg, float* slots, void* a1_out, hipStream_t s);
-// bf16 edge backward from the saved a1 (one wave per tile); writes zbar, dz2,
-// R / slots, ebar_out and per-block partials of db1, dgamma, dbeta.
-hipError_t launch_edge_bwd_rows(const EdgeTiles& t, const void* a1, const float* ebar_in, int have_ebar,
-                                float* ebar_out, const float* aggbar, const MlpW& w, float eps, void* zbar, void* dz,
+// bf16 edge backward from the saved a1 (one wave per tile; bf16 edge-gradient
+// stream ebar, in place allowed); writes zbar, dz2, R / slots, ebar_out and
+// per-block partials of db1, dgamma, dbeta.
+hipError_t launch_edge_bwd_rows(const EdgeTiles& t, const void* a1, const void* ebar_in, int have_ebar,
+                                void* ebar_out, const float* aggbar, const MlpW& w, float eps, void* zbar, void* dz,
                                 float* R, float* slots, const Partials& part, int* nblocks, hipStream_t s);
 // bf16 dW1e = sum zbar^T e, dW2 = sum dz2^T a1, db2 = sum dz2 as per-block partials.
 hipError_t launch_wgrad2(int64_t M, const void* zbar, const void* e, const void* dz, const void* a1,
@@ -107,6 +108,12 @@ hipError_t launch_node_bwd_rows(int64_t N, const float* h, const float* agg, con
 // bf16 node-MLP weight gradients dW1, db1, dW2, db2 from those streams.
 hipError_t launch_wgrad_node(int64_t N, const float* h, const float* agg, const void* dz1, const void* dz2,
                              const void* a1, const Partials& part, int* nblocks, hipStream_t s);
+// bf16 edge encoder in the row layout (uses MlpW::W2p and the fp32 W1f).
+hipError_t launch_edge_enc_rows(int64_t E, const float* efeat, const MlpW& w, float eps, void* e_out, hipStream_t s);
+// bf16 edge-encoder backward from the bf16 edge-gradient stream: per-block
+// partials of every encoder parameter (encoder parameter order).
+hipError_t launch_edge_enc_bwd_rows(int64_t E, const float* efeat, const void* ebar, const MlpW& w, float eps,
+                                    const Partials& part, int* nblocks, hipStream_t s);
 hipError_t launch_slot_fixup(const int32_t* long_nodes, int64_t n_long, const float* slots, float* dst,
                              hipStream_t s);
 hipError_t launch_node_fwd(int prec, int64_t N, const float* h_in, const float* agg, const MlpW& w,

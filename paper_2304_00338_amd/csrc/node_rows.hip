@@ -99,59 +99,6 @@ __device__ __forceinline__ void node_gemm2(const NodeLds& S, const AOff<D>& A2, 
     for (int ob = 0; ob < 8; ++ob) acc[ob] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A2.a(S.W2, ob, s), a1[s], acc[ob], 0, 0, 0);
 }
 
-// Overwrites z with xhat = (z - mean) * rstd over the row's 128 features
-// (biased variance, two passes) and returns rstd.
-__device__ __forceinline__ float ln_normalize(f32x4 (&z)[8], float eps) {
-  float sm = 0.f;
-#pragma unroll
-  for (int ob = 0; ob < 8; ++ob)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) sm += z[ob][r];
-  const float mean = sum_rowlanes(sm) * (1.0f / D);
-  float sq = 0.f;
-#pragma unroll
-  for (int ob = 0; ob < 8; ++ob) {
-    z[ob] -= mean;
-#pragma unroll
-    for (int r = 0; r < 4; ++r) sq += z[ob][r] * z[ob][r];
-  }
-  const float rstd = __builtin_amdgcn_rsqf(sum_rowlanes(sq) * (1.0f / D) + eps);
-#pragma unroll
-  for (int ob = 0; ob < 8; ++ob) z[ob] *= rstd;
-  return rstd;
-}
-
-// Column sums over the 16 rows of a unit (the 16 lanes of one DPP row) of
-// the 32 C-layout values v[ob][r], as a butterfly that halves the values
-// held at every step (partners i ^ 15, i ^ 7, i ^ 3, i ^ 1): lane i ends
-// with the sums of value indices 2i and 2i + 1 (= 4ob + r), i.e. features
-// fo(i / 2, q) + 2 (i % 2) + {0, 1}.  Every lane adds in a fixed order.
-template <int CTRL>
-__device__ __forceinline__ float dpp_mov(float v) {
-  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xf, 0xf, false));
-}
-template <int N, int CTRL>
-__device__ __forceinline__ void bfly_step(float* v, bool hi) {
-#pragma unroll
-  for (int k = 0; k < N; ++k) {
-    const float send = hi ? v[k] : v[k + N];
-    const float keep = hi ? v[k + N] : v[k];
-    v[k] = keep + dpp_mov<CTRL>(send);
-  }
-}
-__device__ __forceinline__ float2 colsum16(const f32x4 (&c)[8], int i) {
-  float v[32];
-#pragma unroll
-  for (int ob = 0; ob < 8; ++ob)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) v[4 * ob + r] = c[ob][r];
-  bfly_step<16, 0x140>(v, (i >> 3) & 1);  // row_mirror: lane 15 - i
-  bfly_step<8, 0x141>(v, (i >> 2) & 1);   // row_half_mirror: lane i ^ 7
-  bfly_step<4, 0x1B>(v, (i >> 1) & 1);    // quad_perm [3,2,1,0]: lane i ^ 3
-  bfly_step<2, 0xB1>(v, i & 1);           // quad_perm [1,0,3,2]: lane i ^ 1
-  return float2{v[0], v[1]};
-}
-
 // ===================================================================== forward
 // h_out = h_in + LN(MLP([h_in, agg])); h_out may alias h_in (each row is
 // read before it is written, by the same lane).

@@ -72,6 +72,14 @@ __device__ __forceinline__ bf16x8 pack_run(const f32x4& lo, const f32x4& hi) {
   return v;
 }
 
+// C-layout fragment of output block ob (fp32) from the lane's four bf16
+// runs: run ob / 2, elements 4 (ob % 2) .. + 4.
+__device__ __forceinline__ f32x4 run_block(const uint4 (&runs)[4], int ob) {
+  const bf16x8 v = __builtin_bit_cast(bf16x8, runs[ob >> 1]);
+  const int h = 4 * (ob & 1);
+  return f32x4{(float)v[h], (float)v[h + 1], (float)v[h + 2], (float)v[h + 3]};
+}
+
 // max(x, 0) as one integer max on the bit pattern (negative floats have the
 // sign bit set, so they compare below +0.0 as signed integers).
 __device__ __forceinline__ float relu(float x) { return __int_as_float(max(__float_as_int(x), 0)); }
@@ -144,6 +152,59 @@ struct AOff {
     return cat8(lds_tr(p), lds_tr(p + 16 * LD));
   }
 };
+
+// Overwrites z with xhat = (z - mean) * rstd over the row's 128 features
+// (biased variance, two passes) and returns rstd.
+__device__ __forceinline__ float ln_normalize(f32x4 (&z)[8], float eps) {
+  float sm = 0.f;
+#pragma unroll
+  for (int ob = 0; ob < 8; ++ob)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) sm += z[ob][r];
+  const float mean = sum_rowlanes(sm) * (1.0f / D);
+  float sq = 0.f;
+#pragma unroll
+  for (int ob = 0; ob < 8; ++ob) {
+    z[ob] -= mean;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) sq += z[ob][r] * z[ob][r];
+  }
+  const float rstd = __builtin_amdgcn_rsqf(sum_rowlanes(sq) * (1.0f / D) + eps);
+#pragma unroll
+  for (int ob = 0; ob < 8; ++ob) z[ob] *= rstd;
+  return rstd;
+}
+
+// Column sums over the 16 rows of a unit (the 16 lanes of one DPP row) of
+// the 32 C-layout values v[ob][r], as a butterfly that halves the values
+// held at every step (partners i ^ 15, i ^ 7, i ^ 3, i ^ 1): lane i ends
+// with the sums of value indices 2i and 2i + 1 (= 4ob + r), i.e. features
+// fo(i / 2, q) + 2 (i % 2) + {0, 1}.  Every lane adds in a fixed order.
+template <int CTRL>
+__device__ __forceinline__ float dpp_mov(float v) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xf, 0xf, false));
+}
+template <int N, int CTRL>
+__device__ __forceinline__ void bfly_step(float* v, bool hi) {
+#pragma unroll
+  for (int k = 0; k < N; ++k) {
+    const float send = hi ? v[k] : v[k + N];
+    const float keep = hi ? v[k + N] : v[k];
+    v[k] = keep + dpp_mov<CTRL>(send);
+  }
+}
+__device__ __forceinline__ float2 colsum16(const f32x4 (&c)[8], int i) {
+  float v[32];
+#pragma unroll
+  for (int ob = 0; ob < 8; ++ob)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) v[4 * ob + r] = c[ob][r];
+  bfly_step<16, 0x140>(v, (i >> 3) & 1);  // row_mirror: lane 15 - i
+  bfly_step<8, 0x141>(v, (i >> 2) & 1);   // row_half_mirror: lane i ^ 7
+  bfly_step<4, 0x1B>(v, (i >> 1) & 1);    // quad_perm [3,2,1,0]: lane i ^ 3
+  bfly_step<2, 0xB1>(v, i & 1);           // quad_perm [1,0,3,2]: lane i ^ 1
+  return float2{v[0], v[1]};
+}
 
 // A zero the compiler cannot see through.  Kernels whose unit loop writes
 // no LDS index their staged weights with a fresh one per unit; otherwise
