@@ -34,6 +34,17 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+# Executed bf16 MFMA work per edge of the bf16 edge kernels (16x16x32 MFMAs
+# at 16,384 flop each over a 16-row block, counted as issued, select
+# operands included): the edge forward runs the K = 128 products of W1e e
+# and W2 a1, 16 + 8 selection MFMAs for P_s + P_r and e + m per 16 rows; the
+# backward the three 128 x 128 products W2 a1 (recomputed z2), W2^T dz2 and
+# W1e^T zbar.
+MFMA_FLOP_PER_EDGE = {"edge_fwd": 2 * 128 * 128 * 2 + 24 * 16384 // 16,
+                      "edge_bwd": 3 * 2 * 128 * 128}
+MFMA_PEAK_BF16_TFLOPS = 2500.0
+
+
 def kernel_bytes(kind, N, E, n_tiles, prec, have_ebar=True, write_e=True, keep_a1=True):
     """Algorithmic HBM bytes of one launch of the kernels this build runs:
     every input read once and every output written once.  In bf16 the edge
@@ -170,6 +181,17 @@ def summarize_profile(d, kernel):
               f"{'' if f is None else f'{f:,.0f}'} | {'' if w is None else f'{w:,.0f}'} | {hbm} |")
     print(f"\nCopy calibration (1 GiB read and written): FETCH_SIZE {cf[kf]:,.1f} KiB -> scale {sf:.3f}; "
           f"WRITE_SIZE {cw[kw]:,.1f} KiB -> scale {sw:.3f}")
+    if os.path.isdir(os.path.join(d, "prof_mfma")):
+        mops, busy = pmc(db("prof_mfma"), "SQ_INSTS_VALU_MFMA_MOPS_BF16"), pmc(db("prof_mfma"), "SQ_VALU_MFMA_BUSY_CYCLES")
+        avg_ms = {short(n): avg / 1e3 for n, c, tot, avg, pct in rows}
+        print("\n| kernel | bf16 MFMA TFLOP per launch (counter) | TFLOP/s at the traced avg | % of 2.5 PFLOP/s |")
+        print("|---|---|---|---|")
+        for n, *_ in rows:
+            k = short(n)
+            if mops.get(k):
+                tf = mops[k] * 512 / 1e12
+                rate = tf / (avg_ms[k] * 1e-3)
+                print(f"| {k} | {tf:.3f} | {rate:.0f} | {100 * rate / MFMA_PEAK_BF16_TFLOPS:.1f} |")
     k = next((short(n) for n, *_ in rows if short(n).startswith("k_" + kernel)), None)
     if k is not None and k in fetch and k in write:
         out = {"kernel": kernel, "profiled_as": k, "source_digest": source_digest(),
@@ -198,7 +220,6 @@ def setup(args):
     mp = pt.patch_maps()
     log(f"patch {args.slab}: {pt.n_nodes} nodes ({mp['n_interior']} interior), {pt.n_edges} edges "
         f"({time.time()-t0:.1f}s)")
-    del g
     dg = mgn.DeviceGraph(pt)
     l2g = mp["node_l2g"]
     dev = lambda a: torch.from_numpy(np.ascontiguousarray(a, np.float32)).cuda()
@@ -211,7 +232,32 @@ def setup(args):
     ctx = mgn.Context(args.mp_steps, pt.n_nodes, pt.n_edges, args.precision, max_stages=1, save=True)
     log(f"workspace {ctx.ws_bytes / 2**30:.1f} GiB ({time.time()-t0:.1f}s)")
     return {"pt": pt, "mp": mp, "dg": dg, "st": st, "y": y, "params": params, "gout": gout,
-            "ctx": ctx, "gp": torch.zeros_like(params), "ynext": torch.empty_like(y)}
+            "ctx": ctx, "gp": torch.zeros_like(params), "ynext": torch.empty_like(y), "mesh": M, "g": g}
+
+
+def c4_rollout(S, args, steps=10):
+    """Whole-mesh inference rollout (the full 146^3 mesh, bf16, no saved
+    activations): `steps` explicit-Euler MGN calls after one warm-up call."""
+    import torch
+    from paper_2304_00338_amd import mgn
+    M, g = S["mesh"], S["g"]
+    dg = mgn.DeviceGraph(g)
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a, np.float32)).cuda()
+    st, y = dev(M["onehot"]), dev(M["states"])
+    ctx = mgn.Context(args.mp_steps, g.n_nodes, g.n_edges, args.precision, max_stages=1)
+    y = mgn.mgn_integrate_step(ctx, dg, S["params"], "euler", st, y, dg.efeat)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        y = mgn.mgn_integrate_step(ctx, dg, S["params"], "euler", st, y, dg.efeat)
+    torch.cuda.synchronize()
+    dt = (time.perf_counter() - t0) / steps
+    ok = bool(torch.isfinite(y).all().item())
+    del ctx, dg
+    return {"workload": f"whole {args.grid}^3 mesh, {steps} explicit-Euler MGN calls, {args.mp_steps} MP steps, "
+                        f"no saved activations", "n_nodes": g.n_nodes, "n_edges": g.n_edges,
+            "ms_per_call": round(dt * 1e3, 3), "mgn_calls_per_s": round(1.0 / dt, 3),
+            "fwd_edges_per_s": round(g.n_edges * args.mp_steps / dt, 1), "finite": ok}
 
 
 def step(S, mgn, fwd_only=False):
@@ -262,6 +308,7 @@ def main():
     ap.add_argument("--mp-steps", type=int, default=15)
     ap.add_argument("--cpu-grid", type=int, default=13)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-c4", action="store_true", help="skip the whole-mesh rollout measurement")
     ap.add_argument("--copy-calibrate", action="store_true",
                     help="only run a plain device copy of known size (for counter scaling)")
     ap.add_argument("--summarize-profile", metavar="DIR",
@@ -365,6 +412,14 @@ def main():
                            for k in sorted(kern_ms, key=lambda x: -kern_ms[x])
                            if (sb := step_bytes(k, N, E, n_tiles, args.precision, m)) is not None},
     }
+    if dom in MFMA_FLOP_PER_EDGE and args.precision == "bf16":
+        fl = MFMA_FLOP_PER_EDGE[dom] * E
+        out["mfma"] = {"kernel": dom, "executed_flop_per_launch": fl,
+                       "achieved_tflops": round(fl / (avg_ms * 1e-3) / 1e12, 1),
+                       "peak_tflops": MFMA_PEAK_BF16_TFLOPS,
+                       "frac": round(fl / (avg_ms * 1e-3) / 1e12 / MFMA_PEAK_BF16_TFLOPS, 4)}
+    if not args.no_c4:
+        out["c4_rollout"] = c4_rollout(S, args)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(args)
     print(json.dumps(out), flush=True)
