@@ -18,7 +18,9 @@ Mesh Physics", ICLR 2023 workshop; arXiv 2304.00338):
   (condition 1), the loss covers subdomain nodes only (condition 2) and
   gradients are summed over all patches before an update (condition 3).
 * Sec. 2.3 and App. A -- Heun's second-order update (equation FE_HUEN and the
-  MGN-scaled form in equation heun) and Heun's third-order method.
+  MGN-scaled form in equation heun) and Heun's third-order method; the
+  outlook (App. D) names Ralston's methods and predict-evaluate-correct at
+  inference.
 * App. B -- mesh edges come from the simplices of the mesh; App. C -- the
   MGN edge features (relative displacement and its length), latent width 128.
 
@@ -48,7 +50,7 @@ __all__ = [
     "Graph", "Patch", "build_graph", "partition", "extract_patch",
     "param_layout", "unpack_params", "n_params", "mlp", "layer_norm", "hop_distance", "edge_features", "pack_grads",
     "mgn_forward", "mgn_backward", "TABLEAUS", "integrate_step",
-    "integrate_backward", "masked_mse_grad", "relu_kinks",
+    "integrate_backward", "masked_mse_grad", "relu_kinks", "pec_step", "pec_rollout",
 ]
 
 LN_EPS = 1e-5
@@ -462,6 +464,11 @@ TABLEAUS = {
     "rk4": ([[0.0, 0.0, 0.0, 0.0], [0.5, 0.0, 0.0, 0.0], [0.0, 0.5, 0.0, 0.0],
              [0.0, 0.0, 1.0, 0.0]],
             [1.0 / 6.0, 1.0 / 3.0, 1.0 / 3.0, 1.0 / 6.0]),
+    # Ralston's minimum-error-bound methods (named in the paper's outlook,
+    # Sec. 5 / App. D): second order c2 = 2/3, third order c = (0, 1/2, 3/4)
+    "ralston2": ([[0.0, 0.0], [2.0 / 3.0, 0.0]], [0.25, 0.75]),
+    "ralston3": ([[0.0, 0.0, 0.0], [0.5, 0.0, 0.0], [0.0, 0.75, 0.0]],
+                 [2.0 / 9.0, 1.0 / 3.0, 4.0 / 9.0]),
 }
 
 
@@ -520,6 +527,48 @@ def integrate_backward(tape, grad_y_next, n_static=4):
     for i in range(s):
         ybar = ybar + ybar_stage[i]
     return gp_total, ybar
+
+
+# --------------------------------------------------------------------------
+# Predict-evaluate-correct at inference (the paper's outlook: a higher-order
+# update for the cost of one MGN evaluation per step).  Reading: two-step
+# Adams-Bashforth predictor, trapezoidal (Adams-Moulton) corrector, no
+# re-evaluation at the corrected state, MGN in place of h*f:
+#   y_p   = y_n + 3/2 K_n - 1/2 K_{n-1}
+#   K_p   = MGN([static, y_p])
+#   y_n+1 = y_n + 1/2 (K_p + K_n),   then (K_n+1, K_n) = (K_p, K_n).
+# The history starts as K_0 = K_-1 = MGN(y_0), so the first step is
+# Heun's second-order step.
+# --------------------------------------------------------------------------
+def pec_step(g, params, static, y, K, K_prev, efeat, mp_steps, latent=128, model=None):
+    """One PEC step from y_n with history (K_n, K_n-1); returns
+    (y_n+1, K_p), the new history being (K_p, K_n)."""
+    y = np.asarray(y, dtype=np.float64)
+    yp = y + 1.5 * K - 0.5 * K_prev
+    if model is not None:
+        Kp = model(yp)
+    else:
+        Kp = mgn_forward(g, params, np.concatenate([np.asarray(static, np.float64), yp], axis=1), efeat,
+                         mp_steps, latent)
+    return y + 0.5 * (Kp + K), Kp
+
+
+def pec_rollout(g, params, static, y0, efeat, mp_steps, n_steps, latent=128, model=None):
+    """n_steps PEC steps from y0 (history bootstrapped with MGN(y0));
+    returns the list of states y_1 .. y_n."""
+    y = np.asarray(y0, dtype=np.float64)
+    if model is not None:
+        K = model(y)
+    else:
+        K = mgn_forward(g, params, np.concatenate([np.asarray(static, np.float64), y], axis=1), efeat,
+                        mp_steps, latent)
+    K_prev = K
+    out = []
+    for _ in range(n_steps):
+        y, Kp = pec_step(g, params, static, y, K, K_prev, efeat, mp_steps, latent, model)
+        K_prev, K = K, Kp
+        out.append(y)
+    return out
 
 
 def masked_mse_grad(out, target, interior):

@@ -284,7 +284,7 @@ def test_heun2_matches_paper_formula():
 
 @pytest.mark.parametrize("scheme,order", [("euler", 1), ("heun2", 2),
                                           ("midpoint", 2), ("heun3", 3),
-                                          ("rk4", 4)])
+                                          ("rk4", 4), ("ralston2", 2), ("ralston3", 3)])
 def test_linear_standin_taylor(scheme, order):
     """With K(y) = y A the step is the Taylor polynomial sum_j y A^j / j!
     up to the method's order."""
@@ -300,12 +300,12 @@ def test_linear_standin_taylor(scheme, order):
     assert np.allclose(got, ref, rtol=1e-13, atol=1e-13)
 
 
-@pytest.mark.parametrize("scheme", ["euler", "heun2", "heun3", "rk4", "midpoint"])
+@pytest.mark.parametrize("scheme", ["euler", "heun2", "heun3", "rk4", "midpoint", "ralston2", "ralston3"])
 def test_observed_local_error_order(scheme):
     """y' = -y^2 (exact y(t) = y0/(1+y0 t)): halving h divides the one-step
     error by 2^(p+1).  Paper: FE O(h^2), H2 O(h^3), H3 O(h^4)."""
     facts = json.load(open(GOLD))
-    p_expect = {"euler": 2, "heun2": 3, "midpoint": 3, "heun3": 4, "rk4": 5}[scheme]
+    p_expect = {"euler": 2, "heun2": 3, "midpoint": 3, "heun3": 4, "rk4": 5, "ralston2": 3, "ralston3": 4}[scheme]
     if scheme in facts["local_error_order"]:
         assert facts["local_error_order"][scheme] == p_expect
     y0 = np.array([[0.7, 1.1, 0.3, 1.5]])
@@ -316,6 +316,87 @@ def test_observed_local_error_order(scheme):
         errs.append(np.abs(got - y0 / (1 + y0 * h)).max())
     orders = np.log2(np.array(errs[:-1]) / np.array(errs[1:]))
     assert np.all(np.abs(orders - p_expect) < 0.25), orders
+
+
+def test_linear_standin_taylor_is_not_exceeded():
+    """A wrong Ralston coefficient shows up one order higher: the methods
+    match the Taylor polynomial to their order but not beyond (the next
+    term differs), so the order pins above are tight."""
+    rng = np.random.default_rng(12)
+    A = rng.standard_normal((4, 4)) * 0.3
+    y = rng.standard_normal((6, 4))
+    for scheme, order in (("ralston2", 2), ("ralston3", 3)):
+        got = O.integrate_step(None, None, scheme, np.zeros((6, 4)), y, None, 0, model=lambda v: v @ A)
+        ref, term = y.copy(), y.copy()
+        for j in range(1, order + 2):
+            term = term @ A / j
+            ref = ref + term
+        assert not np.allclose(got, ref, rtol=1e-10, atol=1e-10)
+
+
+def test_pec_first_step_is_heun2_and_one_evaluation_per_step():
+    """PEC bootstraps with K_-1 = K_0, so its first step is Heun's step; each
+    later step calls the model once."""
+    calls = []
+
+    def model(v):
+        calls.append(1)
+        return -0.1 * v * v
+    y0 = np.array([[0.7, 1.1, 0.3, 1.5]])
+    ys = O.pec_rollout(None, None, np.zeros_like(y0), y0, None, 0, 4, model=model)
+    h2 = O.integrate_step(None, None, "heun2", np.zeros_like(y0), y0, None, 0, model=lambda v: -0.1 * v * v)
+    assert np.allclose(ys[0], h2, rtol=1e-15, atol=1e-15)
+    assert len(calls) == 1 + 4
+
+
+def test_pec_first_step_closed_form():
+    """With K(y) = y A the bootstrap step is y0 (I + A + A^2/2), the
+    second-order Taylor polynomial, and the new history value is the
+    predicted derivative y0 (A + A^2)."""
+    rng = np.random.default_rng(13)
+    A = rng.standard_normal((4, 4)) * 0.2
+    y0 = rng.standard_normal((3, 4))
+    y1, Kp = O.pec_step(None, None, np.zeros_like(y0), y0, y0 @ A, y0 @ A, None, 0, model=lambda v: v @ A)
+    I = np.eye(4)
+    assert np.allclose(y1, y0 @ (I + A + A @ A / 2), rtol=1e-14, atol=1e-14)
+    assert np.allclose(Kp, y0 @ (A + A @ A), rtol=1e-14, atol=1e-14)
+
+
+def test_pec_error_approaches_trapezoidal_rule():
+    """The corrector is the trapezoidal rule; with the two-step
+    Adams-Bashforth predictor the predictor's (and the unevaluated
+    corrected state's) contribution to the global error is one order higher,
+    so PEC's error approaches that of the implicit trapezoidal rule (solved
+    here to convergence by fixed-point iteration) as h -> 0.  A first-order
+    predictor would leave an O(h^2) difference."""
+    y0 = np.array([[0.7, 1.1, 0.3, 1.5]])
+    exact = y0 / (1 + y0)
+    ratios = []
+    for n in (40, 80, 160):
+        h = 1.0 / n
+        ys = O.pec_rollout(None, None, np.zeros_like(y0), y0, None, 0, n, model=lambda v, h=h: -h * v * v)
+        y = y0.copy()
+        for _ in range(n):
+            z = y.copy()
+            for _ in range(200):
+                z = y + 0.5 * h * (-y * y - z * z)
+            y = z
+        ratios.append(np.abs(ys[-1] - exact).max() / np.abs(y - exact).max())
+    assert abs(ratios[-1] - 1.0) < 0.03, ratios
+    assert abs(ratios[-1] - 1.0) < abs(ratios[0] - 1.0), ratios
+
+
+def test_pec_observed_global_order():
+    """AB2 predictor + trapezoidal corrector is a second-order method: on
+    y' = -y^2 over t in [0, 1] the global error falls by 2^2 per halving of h."""
+    y0 = np.array([[0.7, 1.1, 0.3, 1.5]])
+    errs = []
+    for n in (20, 40, 80):
+        h = 1.0 / n
+        ys = O.pec_rollout(None, None, np.zeros_like(y0), y0, None, 0, n, model=lambda v, h=h: -h * v * v)
+        errs.append(np.abs(ys[-1] - y0 / (1 + y0)).max())
+    orders = np.log2(np.array(errs[:-1]) / np.array(errs[1:]))
+    assert np.all(np.abs(orders - 2.0) < 0.2), orders
 
 
 def test_integrator_backward_fd():
