@@ -104,13 +104,14 @@ def step_bytes(kind, N, E, n_tiles, prec, m):
 
 
 def source_digest():
-    """Digest of the kernel sources: counter-derived traffic is reported only
-    for the sources it was measured on."""
+    """Digest of the device sources (kernels, their headers and launchers):
+    counter-derived traffic is reported only for the kernels it was measured
+    on; host-only code does not enter."""
     import hashlib
     h = hashlib.sha256()
     d = os.path.join(ROOT, "paper_2304_00338_amd", "csrc")
     for f in sorted(os.listdir(d)):
-        if f.endswith((".hip", ".hpp", ".cpp")):
+        if f.endswith((".hip", ".hpp")):
             h.update(f.encode())
             h.update(open(os.path.join(d, f), "rb").read())
     return h.hexdigest()[:16]

@@ -63,12 +63,16 @@ extern "C" {
  * HEUN2    a21 = 1, b = (1/2, 1/2)                       (App. A, eq. heun)
  * MIDPOINT a21 = 1/2, b = (0, 1)
  * HEUN3    a21 = 1/3, a32 = 2/3, b = (1/4, 0, 3/4)       (Heun's 3rd order, Sec. 2.3)
- * RK4      a21 = a32 = 1/2, a43 = 1, b = (1, 2, 2, 1)/6 */
+ * RK4      a21 = a32 = 1/2, a43 = 1, b = (1, 2, 2, 1)/6
+ * RALSTON2 a21 = 2/3, b = (1/4, 3/4)                     (Ralston's methods,
+ * RALSTON3 a21 = 1/2, a32 = 3/4, b = (2/9, 1/3, 4/9)      outlook, App. D) */
 #define MGN_EULER 0
 #define MGN_HEUN2 1
 #define MGN_MIDPOINT 2
 #define MGN_HEUN3 3
 #define MGN_RK4 4
+#define MGN_RALSTON2 5
+#define MGN_RALSTON3 6
 
 /* ---- model configuration --------------------------------------------- */
 typedef struct mgn_config {
@@ -225,8 +229,24 @@ int mgn_integrate_step(mgn_ctx* ctx, const mgn_dgraph* g, const float* params,
                        int32_t save, void* workspace, size_t ws_bytes,
                        void* stream);
 
-/* Number of stages of a scheme (1, 2, 2, 3, 4), or MGN_ERR_ARG. */
+/* Number of stages of a scheme (1, 2, 2, 3, 4, 2, 3), or MGN_ERR_ARG. */
 int mgn_scheme_stages(int32_t scheme);
+
+/* One predict-evaluate-correct step at inference (the paper's outlook,
+ * App. D: a higher-order update for one MGN evaluation per step): two-step
+ * Adams-Bashforth predictor, trapezoidal corrector, MGN in place of h*f,
+ *   y_p = y + 3/2 K_n - 1/2 K_n-1,  K_p = MGN([static, y_p]),
+ *   y_next = y + 1/2 (K_p + K_n),   history <- (K_p, K_n).
+ * khist [2][N][4] (device, in/out): khist[0] = K_n, khist[1] = K_n-1.  With
+ * first != 0 the history is initialised first as K_0 = K_-1 = MGN([static,
+ * y]) (one extra MGN call), which makes this step Heun's second-order step.
+ * static, y, efeat, y_next as in mgn_integrate_step; y_next must not alias y
+ * or khist.  No activations are saved (inference only).
+ * Errors: those of mgn_integrate_step. */
+int mgn_pec_step(mgn_ctx* ctx, const mgn_dgraph* g, const float* params,
+                 const float* static_feat, const float* y, float* khist,
+                 const float* efeat, float* y_next, int32_t first,
+                 void* workspace, size_t ws_bytes, void* stream);
 
 /* Per-kernel timing for benchmarks.  While enabled, every kernel launch of
  * the context is bracketed by two HIP events recorded on the caller's stream.

@@ -218,6 +218,20 @@ bool tableau(int32_t scheme, Tableau& t) {
       t.b[0] = 0.25f;
       t.b[2] = 0.75f;
       return true;
+    case MGN_RALSTON2:
+      t.s = 2;
+      t.a[1][0] = 2.f / 3.f;
+      t.b[0] = 0.25f;
+      t.b[1] = 0.75f;
+      return true;
+    case MGN_RALSTON3:
+      t.s = 3;
+      t.a[1][0] = 0.5f;
+      t.a[2][1] = 0.75f;
+      t.b[0] = 2.f / 9.f;
+      t.b[1] = 1.f / 3.f;
+      t.b[2] = 4.f / 9.f;
+      return true;
     case MGN_RK4:
       t.s = 4;
       t.a[1][0] = 0.5f;
@@ -735,6 +749,53 @@ int mgn_integrate_step(mgn_ctx* ctx, const mgn_dgraph* g, const float* params, i
     c.node_in = nullptr;
     c.ws = w;
   }
+  return MGN_OK;
+}
+
+int mgn_pec_step(mgn_ctx* ctx, const mgn_dgraph* g, const float* params, const float* static_feat, const float* y,
+                 float* khist, const float* efeat, float* y_next, int32_t first, void* ws, size_t ws_bytes,
+                 void* stream) {
+  if (!ctx) return fail(MGN_ERR_ARG, "mgn_pec_step: null ctx");
+  int rc = check_call(&ctx->c, g, params, ws, ws_bytes, 0);
+  if (rc != MGN_OK) return rc;
+  Ctx& c = ctx->c;
+  const int64_t N = g->n_nodes;
+  if (N > 0 && (!static_feat || !y || !khist || !y_next || (g->n_edges > 0 && !efeat)))
+    return fail(MGN_ERR_ARG, "mgn_pec_step: null input or output");
+  if (N > 0 && (y_next == y || y_next == khist || y_next == khist + (size_t)N * 4))
+    return fail(MGN_ERR_ARG, "mgn_pec_step: y_next must not alias y or khist");
+  c.saved = 0;
+  if (N == 0) return MGN_OK;
+  char* w = (char*)ws;
+  Run r{c, *g, params, w, S(stream), N, g->n_edges, c.cfg.mp_steps, c.cfg.precision, c.cfg.ln_eps};
+  if ((rc = r.pack_weights()) != MGN_OK) return rc;
+  float* node_in = (float*)(w + c.L.node_in);
+  float* Kp = (float*)(w + c.L.K);
+  float* K0 = khist;
+  float* K1 = khist + (size_t)N * 4;
+  auto comb = [&](std::initializer_list<std::pair<const float*, float>> terms) {
+    LinComb lc{};
+    for (const auto& t : terms) {
+      lc.x[lc.n] = t.first;
+      lc.ld[lc.n] = 4;
+      lc.c[lc.n] = t.second;
+      ++lc.n;
+    }
+    return lc;
+  };
+  if (first) {
+    // K_0 = K_-1 = MGN([static, y])
+    HIP_TRY(launch_stage_input(N, static_feat, comb({{y, 1.f}}), node_in, S(stream)));
+    if ((rc = r.forward(node_in, efeat, K0, 0)) != MGN_OK) return rc;
+    HIP_TRY(launch_lincomb(N, comb({{K0, 1.f}}), K1, 4, 0, S(stream)));
+  }
+  // predict, evaluate, correct
+  HIP_TRY(launch_stage_input(N, static_feat, comb({{y, 1.f}, {K0, 1.5f}, {K1, -0.5f}}), node_in, S(stream)));
+  if ((rc = r.forward(node_in, efeat, Kp, 0)) != MGN_OK) return rc;
+  HIP_TRY(launch_lincomb(N, comb({{y, 1.f}, {Kp, 0.5f}, {K0, 0.5f}}), y_next, 4, 0, S(stream)));
+  // history <- (K_p, K_n)
+  HIP_TRY(launch_lincomb(N, comb({{K0, 1.f}}), K1, 4, 0, S(stream)));
+  HIP_TRY(launch_lincomb(N, comb({{Kp, 1.f}}), K0, 4, 0, S(stream)));
   return MGN_OK;
 }
 

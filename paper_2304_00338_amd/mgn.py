@@ -18,8 +18,9 @@ LIB_PATH = os.path.join(HERE, "libmgn.so")
 
 OK, ERR_ARG, ERR_RANGE, ERR_SHAPE, ERR_WORKSPACE, ERR_STATE, ERR_DEVICE, ERR_NOMEM = 0, -1, -2, -3, -4, -5, -6, -7
 FP32, BF16 = 0, 1
-EULER, HEUN2, MIDPOINT, HEUN3, RK4 = 0, 1, 2, 3, 4
-SCHEMES = {"euler": EULER, "heun2": HEUN2, "midpoint": MIDPOINT, "heun3": HEUN3, "rk4": RK4}
+EULER, HEUN2, MIDPOINT, HEUN3, RK4, RALSTON2, RALSTON3 = 0, 1, 2, 3, 4, 5, 6
+SCHEMES = {"euler": EULER, "heun2": HEUN2, "midpoint": MIDPOINT, "heun3": HEUN3, "rk4": RK4,
+           "ralston2": RALSTON2, "ralston3": RALSTON3}
 PRECISIONS = {"fp32": FP32, "bf16": BF16}
 
 
@@ -49,7 +50,7 @@ EXPORTS = [
     "mgn_graph_schedule", "mgn_tile_edges", "mgn_tile_nodes", "mgn_graph_destroy",
     "mgn_partition", "mgn_extract_patch", "mgn_patch_copy_maps", "mgn_ctx_create",
     "mgn_ctx_destroy", "mgn_forward", "mgn_backward", "mgn_integrate_step",
-    "mgn_scheme_stages", "mgn_version", "mgn_last_error", "mgn_profile_enable",
+    "mgn_pec_step", "mgn_scheme_stages", "mgn_version", "mgn_last_error", "mgn_profile_enable",
     "mgn_profile_collect",
 ]
 
@@ -80,6 +81,7 @@ def lib():
         "mgn_forward": (C.c_int, [vp, P(DGraph), vp, vp, vp, vp, i32, vp, C.c_size_t, vp]),
         "mgn_backward": (C.c_int, [vp, vp, vp, vp, vp]),
         "mgn_integrate_step": (C.c_int, [vp, P(DGraph), vp, i32, vp, vp, vp, vp, i32, vp, C.c_size_t, vp]),
+        "mgn_pec_step": (C.c_int, [vp, P(DGraph), vp, vp, vp, vp, vp, vp, i32, vp, C.c_size_t, vp]),
         "mgn_scheme_stages": (C.c_int, [i32]),
         "mgn_version": (C.c_char_p, []),
         "mgn_last_error": (C.c_char_p, []),
@@ -318,6 +320,24 @@ def mgn_integrate_step(ctx: Context, g: DeviceGraph, params, scheme, static, y, 
                                     _dptr(efeat, torch.float32, (E, 4), "efeat"),
                                     _dptr(y_next, torch.float32, (N, 4), "y_next"), 1 if save else 0,
                                     _dptr(ctx.ws, name="workspace"), ctx.ws_bytes, _stream(stream)))
+    return y_next
+
+
+def mgn_pec_step(ctx: Context, g: DeviceGraph, params, static, y, khist, efeat, first=False,
+                 y_next=None, stream=None):
+    """One predict-evaluate-correct inference step; khist [2][N][4] is the
+    derivative history, updated in place (see include/mgn.h)."""
+    torch = _torch()
+    N, E = g.n_nodes, g.n_edges
+    if y_next is None:
+        y_next = torch.empty((N, 4), dtype=torch.float32, device=y.device)
+    _check(lib().mgn_pec_step(ctx._h, C.byref(g.struct), _dptr(params, torch.float32, name="params"),
+                              _dptr(static, torch.float32, (N, 4), "static"),
+                              _dptr(y, torch.float32, (N, 4), "y"),
+                              _dptr(khist, torch.float32, (2, N, 4), "khist"),
+                              _dptr(efeat, torch.float32, (E, 4), "efeat"),
+                              _dptr(y_next, torch.float32, (N, 4), "y_next"), 1 if first else 0,
+                              _dptr(ctx.ws, name="workspace"), ctx.ws_bytes, _stream(stream)))
     return y_next
 
 

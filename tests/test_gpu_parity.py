@@ -193,7 +193,7 @@ def run_integrate(pb, prec, scheme):
     return yn.cpu().numpy(), gp.cpu().numpy(), gy.cpu().numpy()
 
 
-@pytest.mark.parametrize("scheme", ["euler", "heun2", "midpoint", "heun3", "rk4"])
+@pytest.mark.parametrize("scheme", ["euler", "heun2", "midpoint", "heun3", "rk4", "ralston2", "ralston3"])
 @pytest.mark.parametrize("prec", ["fp32", "bf16"])
 def test_integrators(scheme, prec):
     """Outputs at an ordinary point; gradients through all stages at a
@@ -212,6 +212,39 @@ def test_integrators(scheme, prec):
     assert rel_l2(yn - ps.states, ryn - ps.states) < tol
     assert rel_l2(gp, rgp) < tol
     assert rel_l2(gy, rgy) < tol
+
+
+@pytest.mark.parametrize("prec", ["fp32", "bf16"])
+def test_pec_rollout(prec):
+    """Predict-evaluate-correct inference: four steps against the oracle's
+    PEC rollout (change of the state since y0), the first step against Heun's step,
+    and the history buffer holding the last two evaluations."""
+    tol = FP32_TOL if prec == "fp32" else BF16_TOL
+    pb = Problem((7, 6, 5), 2, seed=13).device()
+    N = pb.g.n_nodes
+    ctx = mgn.Context(pb.m, N, pb.g.n_edges, prec)
+    st = torch.from_numpy(pb.onehot.astype(np.float32)).cuda()
+    y = torch.from_numpy(pb.states.astype(np.float32)).cuda()
+    kh = torch.full((2, N, 4), float("nan"), dtype=torch.float32, device="cuda")
+    ys = []
+    for t in range(4):
+        y = mgn.mgn_pec_step(ctx, pb.dg, pb.d_params, st, y, kh, pb.dg.efeat, first=(t == 0))
+        ys.append(y.cpu().numpy())
+    ref = O.pec_rollout(pb.go, pb.params, pb.onehot, pb.states, pb.go.efeat, pb.m, 4)
+    y0 = pb.states.astype(np.float64)
+    for t in range(4):  # the change of the state since y0
+        assert rel_l2(ys[t] - y0, ref[t] - y0) < tol, t
+    h2 = O.integrate_step(pb.go, pb.params, "heun2", pb.onehot, pb.states, pb.go.efeat, pb.m)
+    assert rel_l2(ys[0] - pb.states, h2 - pb.states) < tol
+    # after four steps the history holds the evaluations of steps 4 and 3
+    y = pb.states.astype(np.float64)
+    K = O.mgn_forward(pb.go, pb.params, np.concatenate([pb.onehot, y], 1), pb.go.efeat, pb.m)
+    Kprev = K
+    for t in range(4):
+        y, Kp = O.pec_step(pb.go, pb.params, pb.onehot, y, K, Kprev, pb.go.efeat, pb.m)
+        Kprev, K = K, Kp
+    khn = kh.cpu().numpy()
+    assert rel_l2(khn[0], K) < tol and rel_l2(khn[1], Kprev) < tol
 
 
 def test_gradient_accumulates():
