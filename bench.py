@@ -103,17 +103,20 @@ def step_bytes(kind, N, E, n_tiles, prec, m):
     return b
 
 
-def source_digest():
-    """Digest of the device sources (kernels, their headers and launchers):
-    counter-derived traffic is reported only for the kernels it was measured
-    on; host-only code does not enter."""
+# Device sources of each profiled kernel: its own file and the device
+# headers it includes (launch.hpp only declares host launchers).
+KERNEL_SOURCES = {"edge_bwd": ("edge_rows.hip", "rows_common.hpp", "dev_common.hpp")}
+
+
+def source_digest(kernel="edge_bwd"):
+    """Digest of a kernel's device sources: counter-derived traffic is
+    reported only for the kernel sources it was measured on."""
     import hashlib
     h = hashlib.sha256()
     d = os.path.join(ROOT, "paper_2304_00338_amd", "csrc")
-    for f in sorted(os.listdir(d)):
-        if f.endswith((".hip", ".hpp")):
-            h.update(f.encode())
-            h.update(open(os.path.join(d, f), "rb").read())
+    for f in KERNEL_SOURCES[kernel]:
+        h.update(f.encode())
+        h.update(open(os.path.join(d, f), "rb").read())
     return h.hexdigest()[:16]
 
 
@@ -128,7 +131,7 @@ def measured_traffic(kernel):
         t = json.load(open(traffic_file(kernel)))
     except (OSError, ValueError):
         return None
-    if t.get("source_digest") != source_digest():
+    if t.get("source_digest") != source_digest(kernel):
         return None
     return t.get("bytes_per_launch")
 
@@ -195,7 +198,7 @@ def summarize_profile(d, kernel):
                 print(f"| {k} | {tf:.3f} | {rate:.0f} | {100 * rate / MFMA_PEAK_BF16_TFLOPS:.1f} |")
     k = next((short(n) for n, *_ in rows if short(n).startswith("k_" + kernel)), None)
     if k is not None and k in fetch and k in write:
-        out = {"kernel": kernel, "profiled_as": k, "source_digest": source_digest(),
+        out = {"kernel": kernel, "profiled_as": k, "source_digest": source_digest(kernel),
                "fetch_kib_per_launch": fetch[k], "write_kib_per_launch": write[k],
                "fetch_scale": sf, "write_scale": sw,
                "bytes_per_launch": (fetch[k] * sf + write[k] * sw) * 1024}
@@ -254,11 +257,33 @@ def c4_rollout(S, args, steps=10):
     torch.cuda.synchronize()
     dt = (time.perf_counter() - t0) / steps
     ok = bool(torch.isfinite(y).all().item())
+    y_whole = y
     del ctx, dg
-    return {"workload": f"whole {args.grid}^3 mesh, {steps} explicit-Euler MGN calls, {args.mp_steps} MP steps, "
-                        f"no saved activations", "n_nodes": g.n_nodes, "n_edges": g.n_edges,
-            "ms_per_call": round(dt * 1e3, 3), "mgn_calls_per_s": round(1.0 / dt, 3),
-            "fwd_edges_per_s": round(g.n_edges * args.mp_steps / dt, 1), "finite": ok}
+    res = {"workload": f"whole {args.grid}^3 mesh, {steps} explicit-Euler MGN calls, {args.mp_steps} MP steps, "
+                       f"no saved activations", "n_nodes": g.n_nodes, "n_edges": g.n_edges,
+           "ms_per_call": round(dt * 1e3, 3), "mgn_calls_per_s": round(1.0 / dt, 3),
+           "fwd_edges_per_s": round(g.n_edges * args.mp_steps / dt, 1), "finite": ok}
+    # the same rollout computed patch by patch (ghost rows refreshed from
+    # their owners every step)
+    import synth
+    part = synth.slab_part((args.grid,) * 3, args.slabs)
+    patches = [mgn.DevicePatch(mgn.extract_patch(g, part, p, args.ghost)) for p in range(args.slabs)]
+    ctx = mgn.Context(args.mp_steps, max(p.n_nodes for p in patches), max(p.n_edges for p in patches),
+                      args.precision, max_stages=1)
+    y = mgn.mgn_patch_step(ctx, patches, S["params"], "euler", st, dev(M["states"]))
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        y = mgn.mgn_patch_step(ctx, patches, S["params"], "euler", st, y)
+    torch.cuda.synchronize()
+    dtp = (time.perf_counter() - t0) / steps
+    pe = sum(p.n_edges for p in patches)
+    res["patch_decomposed"] = {
+        "workload": f"{args.slabs} z-slab patches, {args.ghost}-hop ghost zones, ghost refresh every step",
+        "patch_edges": pe, "redundancy": round(pe / g.n_edges, 3), "ms_per_step": round(dtp * 1e3, 3),
+        "equals_whole_mesh": bool(torch.equal(y, y_whole))}
+    del ctx, patches
+    return res
 
 
 def step(S, mgn, fwd_only=False):
@@ -267,6 +292,34 @@ def step(S, mgn, fwd_only=False):
                            S["ynext"], save=not fwd_only)
     if not fwd_only:
         mgn.mgn_backward(S["ctx"], S["gout"], S["gp"])
+
+
+def integrator_steps(S, args, reps=3):
+    """Forward-only time of one integration step of each scheme on the
+    patch (no saved activations), and of one predict-evaluate-correct step."""
+    import torch
+    from paper_2304_00338_amd import mgn
+    pt = S["pt"]
+    ctx = mgn.Context(args.mp_steps, pt.n_nodes, pt.n_edges, args.precision, max_stages=4)
+    out = {}
+    for sc in ("euler", "heun2", "midpoint", "ralston2", "heun3", "ralston3", "rk4"):
+        mgn.mgn_integrate_step(ctx, S["dg"], S["params"], sc, S["st"], S["y"], S["dg"].efeat, S["ynext"])
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(reps):
+            mgn.mgn_integrate_step(ctx, S["dg"], S["params"], sc, S["st"], S["y"], S["dg"].efeat, S["ynext"])
+        torch.cuda.synchronize()
+        out[sc] = round((time.perf_counter() - t0) * 1e3 / reps, 3)
+    kh = torch.zeros((2, pt.n_nodes, 4), dtype=torch.float32, device="cuda")
+    y = mgn.mgn_pec_step(ctx, S["dg"], S["params"], S["st"], S["y"], kh, S["dg"].efeat, first=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        y = mgn.mgn_pec_step(ctx, S["dg"], S["params"], S["st"], y, kh, S["dg"].efeat)
+    torch.cuda.synchronize()
+    out["pec"] = round((time.perf_counter() - t0) * 1e3 / reps, 3)
+    del ctx
+    return out
 
 
 def cpu_baseline(args):
@@ -420,6 +473,7 @@ def main():
                        "peak_tflops": MFMA_PEAK_BF16_TFLOPS,
                        "frac": round(fl / (avg_ms * 1e-3) / 1e12 / MFMA_PEAK_BF16_TFLOPS, 4)}
     if not args.no_c4:
+        out["integrator_fwd_ms_per_step"] = integrator_steps(S, args)
         out["c4_rollout"] = c4_rollout(S, args)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(args)

@@ -182,6 +182,18 @@ typedef struct mgn_dgraph {
   int64_t n_long;
 } mgn_dgraph;
 
+/* One patch of a decomposed mesh (Sec. 2.2) as mgn_patch_step sees it; all
+ * arrays on the device.  g is the patch's local graph (mgn_extract_patch,
+ * mgn_graph_schedule), efeat its [E_p][4] edge features, node_l2g the global
+ * id of every local node and interior 1 for the subdomain nodes
+ * (mgn_patch_copy_maps). */
+typedef struct mgn_dpatch {
+  mgn_dgraph g;
+  const float* efeat;
+  const int32_t* node_l2g;  /* [N_p] */
+  const uint8_t* interior;  /* [N_p] */
+} mgn_dpatch;
+
 typedef struct mgn_ctx mgn_ctx;
 
 /* A context plans the device workspace for graphs of up to max_nodes nodes
@@ -231,6 +243,27 @@ int mgn_integrate_step(mgn_ctx* ctx, const mgn_dgraph* g, const float* params,
 
 /* Number of stages of a scheme (1, 2, 2, 3, 4, 2, 3), or MGN_ERR_ARG. */
 int mgn_scheme_stages(int32_t scheme);
+
+/* One integration step of the whole mesh computed patch by patch (Sec. 2.2:
+ * patch-decomposed inference on one GPU).  For each patch in order: every
+ * patch node takes the current global static and y rows of its global node
+ * (so ghost nodes are refreshed from their owners), the patch takes one step
+ * of the scheme as in mgn_integrate_step, and the next state of its interior
+ * nodes is written to y_next.  static, y, y_next: [n_global][4] (device);
+ * y_next must not alias y.  Rows of y_next whose node is interior to no
+ * patch are left as they were.  With ghost depth k >= s m for an s-stage
+ * scheme and m MP steps, and every node interior to exactly one patch, the
+ * result equals mgn_integrate_step on the whole mesh bitwise (patch nodes in
+ * ascending global order, Sec. 2.2 condition 1).  The context must hold the
+ * largest patch; node ids outside [0, n_global) give unspecified rows (they
+ * are clamped, never read or written out of bounds).
+ * Errors: ARG (null pointers, bad scheme or sizes, aliasing), SHAPE (a patch
+ * larger than the context), WORKSPACE, DEVICE. */
+int mgn_patch_step(mgn_ctx* ctx, int32_t n_patches, const mgn_dpatch* patches,
+                   const float* params, int32_t scheme,
+                   const float* static_feat, const float* y, float* y_next,
+                   int64_t n_global, void* workspace, size_t ws_bytes,
+                   void* stream);
 
 /* One predict-evaluate-correct step at inference (the paper's outlook,
  * App. D: a higher-order update for one MGN evaluation per step): two-step

@@ -142,6 +142,7 @@ struct Layout {
   size_t e_off = 0, h_off = 0, agg_off = 0, P_off = 0, a1_off = 0;  // within a set
   size_t node_in = 0, K = 0, slots = 0;
   // backward
+  size_t pio = 0;
   size_t ebar = 0, zbar = 0, dz = 0, nstr = 0, hb_a = 0, hb_b = 0, aggbar = 0, R = 0, part = 0, kbar = 0, ystage = 0, gin = 0;
   size_t total = 0;
 };
@@ -278,6 +279,8 @@ void plan(Ctx& c) {
   o = al256(o + (size_t)c.max_stages * N * 8 * 4);
   L.K = o;
   o = al256(o + (size_t)c.max_stages * N * 4 * 4);
+  L.pio = o;  // mgn_patch_step: a patch's static, y and y_next rows
+  o = al256(o + (size_t)3 * N * 4 * 4);
   L.slots = o;
   o = al256(o + (size_t)max_slots(E) * D * 4);
   if (c.save) {
@@ -561,6 +564,53 @@ int check_call(Ctx* c, const mgn_dgraph* g, const float* params, void* ws, size_
   return MGN_OK;
 }
 
+// One integration step on graph g (the body of mgn_integrate_step, also run
+// per patch by mgn_patch_step): K_i = MGN([static, y + sum_j a_ij K_j]),
+// y_next = y + sum_i b_i K_i.
+int integrate_core(Ctx& c, const mgn_dgraph& g, const float* params, const Tableau& tb, const float* static_feat,
+                   const float* y, const float* efeat, float* y_next, int save, char* w, hipStream_t s,
+                   bool pack) {
+  const int64_t N = g.n_nodes;
+  if (N == 0) return MGN_OK;
+  int rc;
+  Run r{c, g, params, w, s, N, g.n_edges, c.cfg.mp_steps, c.cfg.precision, c.cfg.ln_eps};
+  r.keep_a1 = save != 0;
+  if (pack && (rc = r.pack_weights()) != MGN_OK) return rc;
+  float* node_in = (float*)(w + c.L.node_in);
+  float* K = (float*)(w + c.L.K);
+  for (int i = 0; i < tb.s; ++i) {
+    LinComb lc{};
+    lc.x[0] = y;
+    lc.ld[0] = 4;
+    lc.c[0] = 1.f;
+    lc.n = 1;
+    for (int j = 0; j < i; ++j)
+      if (tb.a[i][j] != 0.f) {
+        lc.x[lc.n] = K + (size_t)j * N * 4;
+        lc.ld[lc.n] = 4;
+        lc.c[lc.n] = tb.a[i][j];
+        ++lc.n;
+      }
+    float* ni = node_in + (size_t)i * N * 8;
+    HIP_TRY(launch_stage_input(N, static_feat, lc, ni, s));
+    if ((rc = r.forward(ni, efeat, K + (size_t)i * N * 4, save ? i : 0)) != MGN_OK) return rc;
+  }
+  LinComb lc{};
+  lc.x[0] = y;
+  lc.ld[0] = 4;
+  lc.c[0] = 1.f;
+  lc.n = 1;
+  for (int i = 0; i < tb.s; ++i)
+    if (tb.b[i] != 0.f) {
+      lc.x[lc.n] = K + (size_t)i * N * 4;
+      lc.ld[lc.n] = 4;
+      lc.c[lc.n] = tb.b[i];
+      ++lc.n;
+    }
+  HIP_TRY(launch_lincomb(N, lc, y_next, 4, 0, s));
+  return MGN_OK;
+}
+
 }  // namespace
 }  // namespace mgn
 
@@ -700,45 +750,9 @@ int mgn_integrate_step(mgn_ctx* ctx, const mgn_dgraph* g, const float* params, i
   if (g->n_nodes > 0 && (!static_feat || !y || !y_next || (g->n_edges > 0 && !efeat)))
     return fail(MGN_ERR_ARG, "mgn_integrate_step: null input or output");
   c.saved = 0;
-  const int64_t N = g->n_nodes;
   char* w = (char*)ws;
-  Run r{c, *g, params, w, S(stream), N, g->n_edges, c.cfg.mp_steps, c.cfg.precision, c.cfg.ln_eps};
-  r.keep_a1 = save != 0;
-  if (N > 0) {
-    if ((rc = r.pack_weights()) != MGN_OK) return rc;
-    float* node_in = (float*)(w + c.L.node_in);
-    float* K = (float*)(w + c.L.K);
-    for (int i = 0; i < tb.s; ++i) {
-      LinComb lc{};
-      lc.x[0] = y;
-      lc.ld[0] = 4;
-      lc.c[0] = 1.f;
-      lc.n = 1;
-      for (int j = 0; j < i; ++j)
-        if (tb.a[i][j] != 0.f) {
-          lc.x[lc.n] = K + (size_t)j * N * 4;
-          lc.ld[lc.n] = 4;
-          lc.c[lc.n] = tb.a[i][j];
-          ++lc.n;
-        }
-      float* ni = node_in + (size_t)i * N * 8;
-      HIP_TRY(launch_stage_input(N, static_feat, lc, ni, S(stream)));
-      if ((rc = r.forward(ni, efeat, K + (size_t)i * N * 4, save ? i : 0)) != MGN_OK) return rc;
-    }
-    LinComb lc{};
-    lc.x[0] = y;
-    lc.ld[0] = 4;
-    lc.c[0] = 1.f;
-    lc.n = 1;
-    for (int i = 0; i < tb.s; ++i)
-      if (tb.b[i] != 0.f) {
-        lc.x[lc.n] = K + (size_t)i * N * 4;
-        lc.ld[lc.n] = 4;
-        lc.c[lc.n] = tb.b[i];
-        ++lc.n;
-      }
-    HIP_TRY(launch_lincomb(N, lc, y_next, 4, 0, S(stream)));
-  }
+  if ((rc = integrate_core(c, *g, params, tb, static_feat, y, efeat, y_next, save, w, S(stream), true)) != MGN_OK)
+    return rc;
   if (save) {
     c.saved = 2;
     c.scheme = scheme;
@@ -748,6 +762,54 @@ int mgn_integrate_step(mgn_ctx* ctx, const mgn_dgraph* g, const float* params, i
     c.efeat = efeat;
     c.node_in = nullptr;
     c.ws = w;
+  }
+  return MGN_OK;
+}
+
+int mgn_patch_step(mgn_ctx* ctx, int32_t n_patches, const mgn_dpatch* patches, const float* params,
+                   int32_t scheme, const float* static_feat, const float* y, float* y_next, int64_t n_global,
+                   void* ws, size_t ws_bytes, void* stream) {
+  if (!ctx) return fail(MGN_ERR_ARG, "mgn_patch_step: null ctx");
+  Tableau tb;
+  if (!tableau(scheme, tb)) return fail(MGN_ERR_ARG, "mgn_patch_step: unknown scheme %d", scheme);
+  if (n_patches < 0 || (n_patches > 0 && !patches) || n_global < 0)
+    return fail(MGN_ERR_ARG, "mgn_patch_step: bad patch list or global size");
+  Ctx& c = ctx->c;
+  if (tb.s > c.max_stages)
+    return fail(MGN_ERR_ARG, "mgn_patch_step: scheme needs %d stages, context plans %d", tb.s, c.max_stages);
+  if (n_global > 0 && (!static_feat || !y || !y_next))
+    return fail(MGN_ERR_ARG, "mgn_patch_step: null global state");
+  if (n_global > 0 && y_next == y) return fail(MGN_ERR_ARG, "mgn_patch_step: y_next must not alias y");
+  int rc;
+  bool any = false;
+  for (int32_t p = 0; p < n_patches; ++p) {
+    const mgn_dpatch& P = patches[p];
+    if ((rc = check_call(&c, &P.g, params, ws, ws_bytes, 0)) != MGN_OK) return rc;
+    if (P.g.n_nodes > 0) {
+      if (!P.node_l2g || !P.interior || (P.g.n_edges > 0 && !P.efeat))
+        return fail(MGN_ERR_ARG, "mgn_patch_step: patch %d: null maps or edge features", p);
+      if (n_global == 0) return fail(MGN_ERR_ARG, "mgn_patch_step: patch %d has nodes but n_global is 0", p);
+      any = true;
+    }
+  }
+  c.saved = 0;
+  if (!any) return MGN_OK;
+  char* w = (char*)ws;
+  hipStream_t s = S(stream);
+  bool packed = false;
+  for (int32_t p = 0; p < n_patches; ++p) {
+    const mgn_dpatch& P = patches[p];
+    const int64_t Np = P.g.n_nodes;
+    if (Np == 0) continue;
+    float* st_p = (float*)(w + c.L.pio);
+    float* y_p = st_p + (size_t)c.maxN * 4;
+    float* yn_p = y_p + (size_t)c.maxN * 4;
+    // ghost refresh: every patch node takes the current state of its global node
+    HIP_TRY(launch_gather_rows4(Np, static_feat, P.node_l2g, n_global, st_p, s));
+    HIP_TRY(launch_gather_rows4(Np, y, P.node_l2g, n_global, y_p, s));
+    if ((rc = integrate_core(c, P.g, params, tb, st_p, y_p, P.efeat, yn_p, 0, w, s, !packed)) != MGN_OK) return rc;
+    packed = true;
+    HIP_TRY(launch_scatter_rows4(Np, yn_p, P.node_l2g, P.interior, n_global, y_next, s));
   }
   return MGN_OK;
 }

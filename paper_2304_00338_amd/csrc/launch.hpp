@@ -157,6 +157,12 @@ hipError_t launch_lincomb(int64_t N, const LinComb& lc, float* out, int32_t out_
                           hipStream_t s);
 // p[0..n) = v
 hipError_t launch_fill(float* p, int64_t n, float v, hipStream_t s);
+// dst[r][0..4) = src[idx[r]][0..4) for r < n (idx clamped into [0, n_src))
+hipError_t launch_gather_rows4(int64_t n, const float* src, const int32_t* idx, int64_t n_src, float* dst,
+                               hipStream_t s);
+// dst[idx[r]][0..4) = src[r][0..4) for r < n with mask[r] != 0 (idx clamped)
+hipError_t launch_scatter_rows4(int64_t n, const float* src, const int32_t* idx, const uint8_t* mask, int64_t n_dst,
+                                float* dst, hipStream_t s);
 // node_in[v] = [static[v][0..4), y-combination[v][0..4)]
 hipError_t launch_stage_input(int64_t N, const float* st, const LinComb& lc, float* node_in, hipStream_t s);
 

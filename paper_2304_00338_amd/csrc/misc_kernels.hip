@@ -31,9 +31,51 @@ __global__ void __launch_bounds__(256) k_fill(int64_t n, float v, float* __restr
   if (idx < n) p[idx] = v;
 }
 
+// Row moves between a patch's local node order and the global one (4
+// floats per row, one thread per float).  Ids outside [0, n) are clamped:
+// a caller error gives wrong rows, never an out-of-bounds access.
+__global__ void __launch_bounds__(256) k_gather_rows4(int64_t n, const float* __restrict__ src,
+                                                      const int32_t* __restrict__ idx, int64_t n_src,
+                                                      float* __restrict__ dst) {
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (t >= n * 4) return;
+  const int64_t r = t >> 2;
+  const int64_t v = min(max((int64_t)idx[r], (int64_t)0), n_src - 1);
+  dst[t] = src[v * 4 + (t & 3)];
+}
+
+__global__ void __launch_bounds__(256) k_scatter_rows4(int64_t n, const float* __restrict__ src,
+                                                       const int32_t* __restrict__ idx,
+                                                       const uint8_t* __restrict__ mask, int64_t n_dst,
+                                                       float* __restrict__ dst) {
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (t >= n * 4) return;
+  const int64_t r = t >> 2;
+  if (mask[r] == 0) return;
+  const int64_t v = min(max((int64_t)idx[r], (int64_t)0), n_dst - 1);
+  dst[v * 4 + (t & 3)] = src[t];
+}
+
 }  // namespace dev
 
 using namespace dev;
+
+hipError_t launch_gather_rows4(int64_t n, const float* src, const int32_t* idx, int64_t n_src, float* dst,
+                               hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  if (n_src <= 0) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_gather_rows4, dim3((unsigned)((n * 4 + 255) / 256)), dim3(256), 0, s, n, src, idx, n_src, dst);
+  return hipGetLastError();
+}
+
+hipError_t launch_scatter_rows4(int64_t n, const float* src, const int32_t* idx, const uint8_t* mask, int64_t n_dst,
+                                float* dst, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  if (n_dst <= 0) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_scatter_rows4, dim3((unsigned)((n * 4 + 255) / 256)), dim3(256), 0, s, n, src, idx, mask,
+                     n_dst, dst);
+  return hipGetLastError();
+}
 
 hipError_t launch_fill(float* p, int64_t n, float v, hipStream_t s) {
   if (n <= 0) return hipSuccess;

@@ -43,6 +43,10 @@ class DGraph(C.Structure):
                 ("n_tiles", C.c_int64), ("long_nodes", C.c_void_p), ("n_long", C.c_int64)]
 
 
+class DPatch(C.Structure):
+    _fields_ = [("g", DGraph), ("efeat", C.c_void_p), ("node_l2g", C.c_void_p), ("interior", C.c_void_p)]
+
+
 _lib = None
 
 EXPORTS = [
@@ -50,7 +54,7 @@ EXPORTS = [
     "mgn_graph_schedule", "mgn_tile_edges", "mgn_tile_nodes", "mgn_graph_destroy",
     "mgn_partition", "mgn_extract_patch", "mgn_patch_copy_maps", "mgn_ctx_create",
     "mgn_ctx_destroy", "mgn_forward", "mgn_backward", "mgn_integrate_step",
-    "mgn_pec_step", "mgn_scheme_stages", "mgn_version", "mgn_last_error", "mgn_profile_enable",
+    "mgn_pec_step", "mgn_patch_step", "mgn_scheme_stages", "mgn_version", "mgn_last_error", "mgn_profile_enable",
     "mgn_profile_collect",
 ]
 
@@ -82,6 +86,7 @@ def lib():
         "mgn_backward": (C.c_int, [vp, vp, vp, vp, vp]),
         "mgn_integrate_step": (C.c_int, [vp, P(DGraph), vp, i32, vp, vp, vp, vp, i32, vp, C.c_size_t, vp]),
         "mgn_pec_step": (C.c_int, [vp, P(DGraph), vp, vp, vp, vp, vp, vp, i32, vp, C.c_size_t, vp]),
+        "mgn_patch_step": (C.c_int, [vp, i32, P(DPatch), vp, i32, vp, vp, vp, i64, vp, C.c_size_t, vp]),
         "mgn_scheme_stages": (C.c_int, [i32]),
         "mgn_version": (C.c_char_p, []),
         "mgn_last_error": (C.c_char_p, []),
@@ -260,6 +265,21 @@ class DeviceGraph:
                              self.long_nodes.data_ptr() if self.n_long else None, self.n_long)
 
 
+class DevicePatch:
+    """A patch on the device: its local graph (DeviceGraph) and the maps
+    node_l2g / interior of mgn_patch_copy_maps."""
+
+    def __init__(self, patch: Graph, device="cuda"):
+        torch = _torch()
+        mp = patch.patch_maps()
+        self.dg = DeviceGraph(patch, device)
+        self.node_l2g = torch.from_numpy(mp["node_l2g"]).to(device)
+        self.interior = torch.from_numpy(mp["interior"]).to(device)
+        self.n_nodes, self.n_edges, self.n_interior = patch.n_nodes, patch.n_edges, mp["n_interior"]
+        self.struct = DPatch(self.dg.struct, self.dg.efeat.data_ptr(), self.node_l2g.data_ptr(),
+                             self.interior.data_ptr())
+
+
 class Context:
     """mgn_ctx plus a workspace tensor of the size the library asks for."""
 
@@ -320,6 +340,22 @@ def mgn_integrate_step(ctx: Context, g: DeviceGraph, params, scheme, static, y, 
                                     _dptr(efeat, torch.float32, (E, 4), "efeat"),
                                     _dptr(y_next, torch.float32, (N, 4), "y_next"), 1 if save else 0,
                                     _dptr(ctx.ws, name="workspace"), ctx.ws_bytes, _stream(stream)))
+    return y_next
+
+
+def mgn_patch_step(ctx: Context, patches, params, scheme, static, y, y_next=None, stream=None):
+    """One integration step of the whole mesh computed patch by patch with
+    ghost refresh (see include/mgn.h); patches: list of DevicePatch."""
+    torch = _torch()
+    n = y.shape[0]
+    sc = SCHEMES[scheme] if isinstance(scheme, str) else int(scheme)
+    if y_next is None:
+        y_next = torch.empty((n, 4), dtype=torch.float32, device=y.device)
+    arr = (DPatch * max(1, len(patches)))(*[p.struct for p in patches])
+    _check(lib().mgn_patch_step(ctx._h, len(patches), arr, _dptr(params, torch.float32, name="params"), sc,
+                                _dptr(static, torch.float32, (n, 4), "static"), _dptr(y, torch.float32, (n, 4), "y"),
+                                _dptr(y_next, torch.float32, (n, 4), "y_next"), n,
+                                _dptr(ctx.ws, name="workspace"), ctx.ws_bytes, _stream(stream)))
     return y_next
 
 

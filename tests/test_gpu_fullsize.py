@@ -11,6 +11,9 @@
 * C2: 32^3 mesh, fp32, 15 MP steps: sampled outputs against the oracle, and
   the gradient of the whole-mesh loss equal to the sum of the gradients of
   the z-slab patches with the loss on their subdomains (condition 3).
+* C4 patch-decomposed: the same rollout computed slab patch by slab patch
+  (16 z-slabs, 15-hop ghost zones, ghost rows refreshed from their owners
+  every step) equals the whole-mesh rollout bitwise.
 * C5: RK4 / midpoint / Euler on the C2 mesh, fp32 and bf16: the integrator
   call equals the explicit composition of its stage MGN calls, forward and
   backward (stage chaining of Sec. 2.3 at full size; the stage arithmetic
@@ -104,6 +107,24 @@ def test_c4_rollout(big, big_oracle):
     err = rel_l2(first[ids] - M["states"][ids], ref - M["states"][ids])
     print(f"C4 step 1: sampled rel L2 of the increment {err:.2e}", flush=True)
     assert err < BF16_TOL
+
+
+def test_c4_patch_rollout_equals_whole_mesh(big):
+    M, g, P = big
+    part = synth.slab_part(BIG, 16)
+    patches = [mgn.DevicePatch(mgn.extract_patch(g, part, p, M_STEPS)) for p in range(16)]
+    assert sum(p.n_interior for p in patches) == g.n_nodes
+    ctx_p = mgn.Context(M_STEPS, max(p.n_nodes for p in patches), max(p.n_edges for p in patches), "bf16")
+    ctx_w = mgn.Context(M_STEPS, g.n_nodes, g.n_edges, "bf16")
+    dg = mgn.DeviceGraph(g)
+    params, st, y0 = d(P), d(M["onehot"]), d(M["states"])
+    yw, yp = y0, y0
+    for t in range(2):
+        yw = mgn.mgn_integrate_step(ctx_w, dg, params, "euler", st, yw, dg.efeat)
+        yp = mgn.mgn_patch_step(ctx_p, patches, params, "euler", st, yp)
+        assert torch.equal(yw, yp), t
+    print(f"C4 patch rollout: {sum(p.n_edges for p in patches)} patch edges for {g.n_edges} mesh edges",
+          flush=True)
 
 
 @pytest.fixture(scope="module")

@@ -247,6 +247,54 @@ def test_pec_rollout(prec):
     assert rel_l2(khn[0], K) < tol and rel_l2(khn[1], Kprev) < tol
 
 
+def _patch_setup(shape, m, k, n_slabs, seed, prec, stages):
+    import synth
+    M = synth.mesh(shape, seed)
+    g = mgn.build_graph(M["cells"], M["pos"])
+    part = synth.slab_part(shape, n_slabs)
+    patches = [mgn.DevicePatch(mgn.extract_patch(g, part, p, k)) for p in range(n_slabs)]
+    assert sum(p.n_interior for p in patches) == g.n_nodes
+    ctx_p = mgn.Context(m, max(p.n_nodes for p in patches), max(p.n_edges for p in patches), prec,
+                        max_stages=stages)
+    ctx_w = mgn.Context(m, g.n_nodes, g.n_edges, prec, max_stages=stages)
+    d = lambda a: torch.from_numpy(np.ascontiguousarray(a, np.float32)).cuda()
+    return M, g, patches, ctx_p, ctx_w, d(M["onehot"]), d(M["states"]), d(synth.xavier_params(m, seed))
+
+
+@pytest.mark.parametrize("prec", ["fp32", "bf16"])
+@pytest.mark.parametrize("scheme,k", [("euler", 2), ("heun2", 4)])
+def test_patch_rollout_equals_whole_mesh(prec, scheme, k):
+    """Patch-decomposed inference with ghost refresh (Sec. 2.2): with ghost
+    depth k >= s m every step equals the whole-mesh step bitwise; the first
+    step also matches the oracle."""
+    m = 2
+    M, g, patches, ctx_p, ctx_w, st, y0, params = _patch_setup((9, 8, 10), m, k, 3, 14, prec, 2)
+    dg = mgn.DeviceGraph(g)
+    yw, yp = y0, y0
+    for t in range(3):
+        yw = mgn.mgn_integrate_step(ctx_w, dg, params, scheme, st, yw, dg.efeat)
+        yp = mgn.mgn_patch_step(ctx_p, patches, params, scheme, st, yp)
+        assert torch.equal(yw, yp), t
+        if t == 0:
+            go = O.build_graph(M["cells"], M["pos"])
+            ref = O.integrate_step(go, params.cpu().numpy(), scheme, M["onehot"], M["states"], go.efeat, m)
+            tol = FP32_TOL if prec == "fp32" else BF16_TOL
+            assert rel_l2(yp.cpu().numpy() - M["states"], ref - M["states"]) < tol
+
+
+def test_patch_rollout_thin_ghost_zone_differs():
+    """Negative control: Heun's two stages need k >= 2m; with k = m the
+    patch step differs from the whole-mesh step near the slab planes."""
+    m = 2
+    M, g, patches, ctx_p, ctx_w, st, y0, params = _patch_setup((9, 8, 10), m, m, 3, 14, "fp32", 2)
+    dg = mgn.DeviceGraph(g)
+    yw = mgn.mgn_integrate_step(ctx_w, dg, params, "heun2", st, y0, dg.efeat)
+    yp = mgn.mgn_patch_step(ctx_p, patches, params, "heun2", st, y0)
+    assert not torch.equal(yw, yp)
+    ye = mgn.mgn_patch_step(ctx_p, patches, params, "euler", st, y0)
+    assert torch.equal(ye, mgn.mgn_integrate_step(ctx_w, dg, params, "euler", st, y0, dg.efeat))
+
+
 def test_gradient_accumulates():
     """grad_params is accumulated into, so patch gradients can be summed
     (Sec. 2.2, condition 3)."""
