@@ -51,6 +51,7 @@ __all__ = [
     "param_layout", "unpack_params", "n_params", "mlp", "layer_norm", "hop_distance", "edge_features", "pack_grads",
     "mgn_forward", "mgn_backward", "TABLEAUS", "integrate_step",
     "integrate_backward", "masked_mse_grad", "relu_kinks", "pec_step", "pec_rollout",
+    "NOISE_STD_3D", "lr_schedule", "adam_update", "masked_mse", "train_step",
 ]
 
 LN_EPS = 1e-5
@@ -569,6 +570,67 @@ def pec_rollout(g, params, static, y0, efeat, mp_steps, n_steps, latent=128, mod
         K_prev, K = K, Kp
         out.append(y)
     return out
+
+
+# --------------------------------------------------------------------------
+# Patch training step (Sec. 2.2 conditions 2 and 3; App. C: input noise,
+# Adam, learning rate decaying exponentially from 1e-3 to 1e-7 over 4e6
+# steps).  Readings: the noisy input is y + std * n with n standard normal
+# and std = (0.02, 0.02, 0.03, 0.05) for (x, y momentum, vertical momentum,
+# volume fraction), the target state is not perturbed; the loss is the mean
+# squared error of the stepped state over the subdomain nodes of the sampled
+# patches (normalised by 4 x their count); Adam with beta = (0.9, 0.999),
+# eps = 1e-8; the k-th update (k = 1, 2, ...) uses lr(k - 1) with
+# lr(t) = lr_start (lr_end / lr_start)^(t / decay_steps).
+# --------------------------------------------------------------------------
+NOISE_STD_3D = (0.02, 0.02, 0.03, 0.05)
+
+
+def lr_schedule(t, lr_start=1e-3, lr_end=1e-7, decay_steps=4_000_000):
+    return lr_start * (lr_end / lr_start) ** (float(t) / float(decay_steps))
+
+
+def adam_update(p, g, m, v, k, lr, beta1=0.9, beta2=0.999, eps=1e-8):
+    """The k-th Adam update (k >= 1) of p with gradient g; returns (p, m, v)."""
+    m = beta1 * m + (1.0 - beta1) * g
+    v = beta2 * v + (1.0 - beta2) * g * g
+    mh = m / (1.0 - beta1 ** k)
+    vh = v / (1.0 - beta2 ** k)
+    return p - lr * mh / (np.sqrt(vh) + eps), m, v
+
+
+def masked_mse(out, target, interior, n_norm=None):
+    """mean((out - target)^2) over the subdomain nodes; n_norm nodes in the
+    normaliser (default: the interior count)."""
+    out = np.asarray(out, dtype=np.float64)
+    mask = np.asarray(interior, dtype=np.float64)[:, None]
+    n = float(mask.sum()) if n_norm is None else float(n_norm)
+    return float((((out - np.asarray(target, np.float64)) ** 2) * mask).sum() / max(1.0, n * out.shape[1]))
+
+
+def train_step(patches, params, scheme, static, y, y_target, noise, mp_steps, adam_m, adam_v, k,
+               noise_std=NOISE_STD_3D, n_loss_nodes=None, latent=128):
+    """One patch-training step: noisy input, one integration step per patch,
+    masked MSE over the patches' subdomain nodes, gradients summed over the
+    patches (condition 3), one Adam update.  patches: list of Patch.
+    Returns (params, adam_m, adam_v, loss, grad)."""
+    y_noisy = np.asarray(y, np.float64) + np.asarray(noise, np.float64) * np.asarray(noise_std, np.float64)
+    if n_loss_nodes is None:
+        n_loss_nodes = sum(int(pt.n_interior) for pt in patches)
+    grad = np.zeros(np.asarray(params).size, dtype=np.float64)
+    loss = 0.0
+    for pt in patches:
+        l2g = pt.node_l2g
+        yn, tape = integrate_step(pt, params, scheme, np.asarray(static)[l2g], y_noisy[l2g], pt.efeat, mp_steps,
+                                  latent, keep=True)
+        it = pt.interior
+        tgt = np.asarray(y_target, np.float64)[l2g]
+        loss += masked_mse(yn, tgt, it, n_loss_nodes)
+        gout = masked_mse_grad(yn, tgt, it) * (float(it.sum()) / float(n_loss_nodes))
+        gp, _ = integrate_backward(tape, gout)
+        grad += gp
+    p2, m2, v2 = adam_update(np.asarray(params, np.float64), grad, adam_m, adam_v, k, lr_schedule(k - 1))
+    return p2, m2, v2, loss, grad
 
 
 def masked_mse_grad(out, target, interior):

@@ -213,6 +213,19 @@ def loss_weights(n_nodes: int, seed: int, n_out: int = OUT) -> np.ndarray:
     return _rng(seed + 3).standard_normal((n_nodes, n_out)).astype(np.float32)
 
 
+def standard_noise(n_nodes: int, seed: int, n_out: int = OUT) -> np.ndarray:
+    """Standard-normal draws [N, 4] for input noise (scaled per channel by the
+    consumer).  Sub-stream seed + 5."""
+    return _rng(seed + 5).standard_normal((n_nodes, n_out)).astype(np.float32)
+
+
+def next_states(states: np.ndarray, seed: int, scale: float = 0.1) -> np.ndarray:
+    """Synthetic next-step states: states plus N(0, scale^2) changes.
+    Sub-stream seed + 6."""
+    d = _rng(seed + 6).standard_normal(states.shape) * scale
+    return (np.asarray(states, np.float64) + d).astype(np.float32)
+
+
 def relabel(n_nodes: int, seed: int) -> np.ndarray:
     """Seeded random node permutation (new id of old node i is perm[i])."""
     return _rng(seed + 7).permutation(n_nodes).astype(np.int64)

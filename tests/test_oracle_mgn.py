@@ -442,6 +442,103 @@ def test_masked_mse_grad():
     assert np.allclose(gr[0], 2 * out[0] / 4) and np.all(gr[1] == 0)
 
 
+# --------------------------------------------------------- training step
+def test_lr_schedule_and_noise_match_paper():
+    """App. C: exponential decay 1e-3 -> 1e-7 over 4e6 steps (so 1e-5, the
+    geometric mean, half way) and the per-channel input noise."""
+    f = json.load(open(GOLD))
+    lr = lambda t: O.lr_schedule(t, f["lr_start"], f["lr_end"], f["lr_decay_steps"])
+    assert abs(lr(0) - 1e-3) < 1e-18 and abs(lr(4_000_000) / 1e-7 - 1) < 1e-12
+    assert abs(lr(2_000_000) / 1e-5 - 1) < 1e-12
+    assert abs(O.lr_schedule(4_000_000) / f["lr_end"] - 1) < 1e-12
+    assert list(O.NOISE_STD_3D) == f["noise_std_3d"]
+
+
+def test_adam_matches_torch():
+    """Three updates of the oracle's Adam against torch.optim.Adam (fp64),
+    with the scheduled learning rate set before every update."""
+    rng = np.random.default_rng(21)
+    p0 = rng.standard_normal(50)
+    grads = [rng.standard_normal(50) * s for s in (1.0, 0.1, 3.0)]
+    tp = torch.tensor(p0.copy(), dtype=torch.float64, requires_grad=True)
+    opt = torch.optim.Adam([tp], lr=1e-3, betas=(0.9, 0.999), eps=1e-8)
+    p, m, v = p0.copy(), np.zeros(50), np.zeros(50)
+    for k, g in enumerate(grads, start=1):
+        lr = O.lr_schedule(k - 1, 1e-3, 1e-7, 10)  # a fast schedule, so the rate changes
+        for grp in opt.param_groups:
+            grp["lr"] = lr
+        tp.grad = torch.tensor(g, dtype=torch.float64)
+        opt.step()
+        p, m, v = O.adam_update(p, g, m, v, k, lr)
+    st = opt.state[tp]
+    assert np.allclose(p, tp.detach().numpy(), rtol=1e-13, atol=1e-15)
+    assert np.allclose(m, st["exp_avg"].numpy(), rtol=1e-13) and np.allclose(v, st["exp_avg_sq"].numpy(), rtol=1e-13)
+
+
+def test_masked_mse_matches_torch_and_fd():
+    rng = np.random.default_rng(22)
+    out, tgt = rng.standard_normal((9, 4)), rng.standard_normal((9, 4))
+    it = (rng.random(9) < 0.6).astype(np.uint8)
+    ref = torch.nn.functional.mse_loss(torch.tensor(out[it == 1]), torch.tensor(tgt[it == 1])).item()
+    assert abs(O.masked_mse(out, tgt, it) - ref) < 1e-14
+    g = O.masked_mse_grad(out, tgt, it)
+    h = 1e-6
+    for (r, c) in [(0, 0), (4, 2), (8, 3), (int(np.argmin(it)), 1)]:
+        op, om = out.copy(), out.copy()
+        op[r, c] += h
+        om[r, c] -= h
+        fd = (O.masked_mse(op, tgt, it) - O.masked_mse(om, tgt, it)) / (2 * h)
+        assert abs(fd - g[r, c]) < 1e-8
+
+
+def _train_problem(shape, m, seed, k, splits):
+    M, g, P = small(shape, m, seed=seed)
+    st = M["onehot"].astype(np.float64)
+    y = M["states"].astype(np.float64)
+    tgt = synth.next_states(M["states"], seed).astype(np.float64)
+    nz = synth.standard_noise(g.n_nodes, seed).astype(np.float64)
+    part = O.partition(M["pos"], splits)
+    pts = [O.extract_patch(g, part, p, k) for p in range(int(np.prod(splits)))]
+    return M, g, P, st, y, tgt, nz, pts
+
+
+def test_train_step_patches_equal_whole_mesh():
+    """Conditions 2 and 3 through the integrator and the noisy input: the
+    step over all patches (k = s m) has the whole-mesh loss, gradient and
+    update; the whole mesh is the single patch of a one-part partition."""
+    m = 1
+    M, g, P, st, y, tgt, nz, pts = _train_problem((6, 5), m, 23, 2, (2, 2))
+    whole = O.extract_patch(g, np.zeros(g.n_nodes, np.int32), 0, 0)
+    z = np.zeros(P.size)
+    a = O.train_step(pts, P, "heun2", st, y, tgt, nz, m, z, z, 1)
+    b = O.train_step([whole], P, "heun2", st, y, tgt, nz, m, z, z, 1)
+    assert abs(a[3] - b[3]) < 1e-12 * abs(b[3])
+    assert np.allclose(a[4], b[4], rtol=1e-10, atol=1e-12 * np.abs(b[4]).max())
+    assert np.allclose(a[0], b[0], rtol=1e-12, atol=1e-12)
+
+
+def test_train_step_gradient_fd():
+    """The summed gradient is the derivative of the loss (fp64 central
+    differences), and the update is Adam's first step with lr(0) = 1e-3."""
+    m = 1
+    M, g, P, st, y, tgt, nz, pts = _train_problem((5, 4), m, 24, 2, (2, 1))
+    z = np.zeros(P.size)
+    p1, m1, v1, loss, grad = O.train_step(pts, P, "euler", st, y, tgt, nz, m, z, z, 1)
+
+    def L(Pv):
+        return O.train_step(pts, Pv, "euler", st, y, tgt, nz, m, z, z, 1)[3]
+    P64, h = P.astype(np.float64), 1e-6
+    for i in (7, 3000, 20000, P.size - 2):
+        Pp, Pm = P64.copy(), P64.copy()
+        Pp[i] += h
+        Pm[i] -= h
+        fd = (L(Pp) - L(Pm)) / (2 * h)
+        assert abs(fd - grad[i]) <= 1e-6 * max(1e-3, abs(fd))
+    # first update: lr g / (|g| + eps), within 1e-4 of lr sign(g) where |g| > 1e-4
+    nzg = np.abs(grad) > 1e-4
+    assert np.allclose((P64 - p1)[nzg], 1e-3 * np.sign(grad[nzg]), rtol=1e-3)
+
+
 def test_subgradient_flip_matches_autograd():
     """oracle.mgn_backward(flips=...) takes the other one-sided derivative at
     the listed ReLU inputs: compare with autograd on the dense brute force
