@@ -294,6 +294,33 @@ def step(S, mgn, fwd_only=False):
         mgn.mgn_backward(S["ctx"], S["gout"], S["gp"])
 
 
+def train_steps(S, args, reps=3):
+    """The patch-training step on the benchmark patch: noisy input (the
+    paper's 3D noise levels), one Euler step with saved activations, masked
+    MSE on the subdomain nodes, backward, Adam (paper schedule)."""
+    import torch
+    import synth
+    from paper_2304_00338_amd import mgn
+    M = S["mesh"]
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a, np.float32)).cuda()
+    patch = mgn.DevicePatch(S["pt"])
+    st, y = dev(M["onehot"]), dev(M["states"])
+    tgt, nz = dev(synth.next_states(M["states"], 0)), dev(synth.standard_noise(M["states"].shape[0], 0))
+    params = S["params"].clone()
+    grad, m, v = torch.zeros_like(params), torch.zeros_like(params), torch.zeros_like(params)
+    adam = mgn.Adam()
+    loss = mgn.mgn_train_step(S["ctx"], [patch], params, "euler", st, y, tgt, nz, grad, m, v, adam, 1)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(2, 2 + reps):
+        loss = mgn.mgn_train_step(S["ctx"], [patch], params, "euler", st, y, tgt, nz, grad, m, v, adam, k)
+    torch.cuda.synchronize()
+    dt = (time.perf_counter() - t0) / reps
+    return {"workload": "one patch per step (the benchmark patch), Euler, input noise, masked MSE, Adam",
+            "ms_per_step": round(dt * 1e3, 3), "steps_per_s": round(1.0 / dt, 3),
+            "loss_finite": bool(np.isfinite(loss.item()))}
+
+
 def integrator_steps(S, args, reps=3):
     """Forward-only time of one integration step of each scheme on the
     patch (no saved activations), and of one predict-evaluate-correct step."""
@@ -472,6 +499,7 @@ def main():
                        "achieved_tflops": round(fl / (avg_ms * 1e-3) / 1e12, 1),
                        "peak_tflops": MFMA_PEAK_BF16_TFLOPS,
                        "frac": round(fl / (avg_ms * 1e-3) / 1e12 / MFMA_PEAK_BF16_TFLOPS, 4)}
+    out["train_step"] = train_steps(S, args)
     if not args.no_c4:
         out["integrator_fwd_ms_per_step"] = integrator_steps(S, args)
         out["c4_rollout"] = c4_rollout(S, args)

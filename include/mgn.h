@@ -265,6 +265,55 @@ int mgn_patch_step(mgn_ctx* ctx, int32_t n_patches, const mgn_dpatch* patches,
                    int64_t n_global, void* workspace, size_t ws_bytes,
                    void* stream);
 
+/* Adam with the exponentially decaying learning rate of the paper's
+ * training (App. C: 1e-3 to 1e-7 over 4,000,000 steps).  The k-th update
+ * (k = 1, 2, ...) uses lr = lr_start (lr_end / lr_start)^((k - 1) /
+ * decay_steps) and the bias corrections 1 - beta^k. */
+typedef struct mgn_adam {
+  double lr_start;     /* 1e-3 */
+  double lr_end;       /* 1e-7 */
+  int64_t decay_steps; /* 4000000 */
+  double beta1;        /* 0.9 */
+  double beta2;        /* 0.999 */
+  double eps;          /* 1e-8 */
+} mgn_adam;
+
+/* Learning rate of the k-th update, or -1 for bad settings (k < 1,
+ * non-positive rates or decay_steps). */
+double mgn_adam_lr(const mgn_adam* adam, int64_t k);
+
+/* The k-th Adam update of n float32 parameters in place (device):
+ * m = b1 m + (1 - b1) g, v = b2 v + (1 - b2) g^2,
+ * p -= lr (m / (1 - b1^k)) / (sqrt(v / (1 - b2^k)) + eps), in float32 with
+ * b, 1 - b, lr and the bias corrections formed in double and rounded once.
+ * Errors: ARG (bad settings, null buffers), DEVICE. */
+int mgn_adam_step(const mgn_adam* adam, int64_t k, float* params,
+                  const float* grad, float* m, float* v, int64_t n,
+                  void* stream);
+
+/* One patch-training step (Sec. 2.2 conditions 2 and 3; App. C): for each
+ * patch in order, the noisy input y + std * noise of its nodes (ghost rows
+ * from their owners), one step of the scheme with saved activations, the
+ * squared error of the stepped state against y_target on its subdomain
+ * nodes, and the backward pass into grad; then grad holds the gradient of
+ * loss = sum over the patches' subdomain nodes and the 4 channels of
+ * (y_step - y_target)^2 / (4 n_loss_nodes), and one Adam update (k-th) is
+ * applied to params with the moments adam_m, adam_v.
+ * static, y, y_target, noise (standard normal draws, nullable: no noise):
+ * [n_global][4]; noise_std: host [4] (nullable: the paper's 3D values 0.02,
+ * 0.02, 0.03, 0.05); grad, adam_m, adam_v: [mgn_param_count] (grad is
+ * overwritten); loss: one device float (overwritten).  The context must have
+ * been created with save and hold the largest patch.  n_loss_nodes is
+ * normally the number of subdomain nodes of the given patches.
+ * Errors: ARG, STATE (context without save), SHAPE, WORKSPACE, DEVICE. */
+int mgn_train_step(mgn_ctx* ctx, int32_t n_patches, const mgn_dpatch* patches,
+                   float* params, int32_t scheme, const float* static_feat,
+                   const float* y, const float* y_target, const float* noise,
+                   const float* noise_std, int64_t n_loss_nodes, float* grad,
+                   float* adam_m, float* adam_v, const mgn_adam* adam, int64_t k,
+                   float* loss, int64_t n_global, void* workspace,
+                   size_t ws_bytes, void* stream);
+
 /* One predict-evaluate-correct step at inference (the paper's outlook,
  * App. D: a higher-order update for one MGN evaluation per step): two-step
  * Adams-Bashforth predictor, trapezoidal corrector, MGN in place of h*f,

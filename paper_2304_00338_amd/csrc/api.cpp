@@ -6,6 +6,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cmath>
 #include <cstring>
 #include <new>
 #include <vector>
@@ -142,7 +143,7 @@ struct Layout {
   size_t e_off = 0, h_off = 0, agg_off = 0, P_off = 0, a1_off = 0;  // within a set
   size_t node_in = 0, K = 0, slots = 0;
   // backward
-  size_t pio = 0;
+  size_t pio = 0, lossp = 0;
   size_t ebar = 0, zbar = 0, dz = 0, nstr = 0, hb_a = 0, hb_b = 0, aggbar = 0, R = 0, part = 0, kbar = 0, ystage = 0, gin = 0;
   size_t total = 0;
 };
@@ -279,8 +280,10 @@ void plan(Ctx& c) {
   o = al256(o + (size_t)c.max_stages * N * 8 * 4);
   L.K = o;
   o = al256(o + (size_t)c.max_stages * N * 4 * 4);
-  L.pio = o;  // mgn_patch_step: a patch's static, y and y_next rows
-  o = al256(o + (size_t)3 * N * 4 * 4);
+  L.pio = o;  // patch steps: a patch's static, y, y_next and loss-gradient rows
+  o = al256(o + (size_t)4 * N * 4 * 4);
+  L.lossp = o;  // training step: partial sums of the loss
+  o = al256(o + (size_t)loss_blocks() * 4);
   L.slots = o;
   o = al256(o + (size_t)max_slots(E) * D * 4);
   if (c.save) {
@@ -611,6 +614,62 @@ int integrate_core(Ctx& c, const mgn_dgraph& g, const float* params, const Table
   return MGN_OK;
 }
 
+// Reverse mode of the saved forward or integration step (the body of
+// mgn_backward, also run per patch by mgn_train_step).
+int backward_core(Ctx& c, const float* grad_out, float* grad_params, float* grad_in, hipStream_t s) {
+  const int64_t N = c.g.n_nodes;
+  Run r{c, c.g, c.params, c.ws, s, N, c.g.n_edges, c.cfg.mp_steps, c.cfg.precision, c.cfg.ln_eps};
+  r.keep_a1 = true;
+  int rc;
+  if (c.saved == 1) return r.backward(0, c.node_in, c.efeat, grad_out, grad_params, grad_in);
+  Tableau tb;
+  tableau(c.scheme, tb);
+  char* w = c.ws;
+  float* node_in = (float*)(w + c.L.node_in);
+  float* kbar = (float*)(w + c.L.kbar);
+  float* ys = (float*)(w + c.L.ystage);
+  float* gin = (float*)(w + c.L.gin);
+  for (int i = tb.s - 1; i >= 0; --i) {
+    LinComb lc{};
+    lc.x[0] = grad_out;
+    lc.ld[0] = 4;
+    lc.c[0] = tb.b[i];
+    lc.n = 1;
+    for (int j = i + 1; j < tb.s; ++j)
+      if (tb.a[j][i] != 0.f) {
+        lc.x[lc.n] = ys + (size_t)j * N * 4;
+        lc.ld[lc.n] = 4;
+        lc.c[lc.n] = tb.a[j][i];
+        ++lc.n;
+      }
+    HIP_TRY(launch_lincomb(N, lc, kbar, 4, 0, s));
+    if ((rc = r.backward(i, node_in + (size_t)i * N * 8, c.efeat, kbar, grad_params, gin)) != MGN_OK) return rc;
+    LinComb cp{};
+    cp.x[0] = gin;
+    cp.ld[0] = 8;
+    cp.off[0] = 4;
+    cp.c[0] = 1.f;
+    cp.n = 1;
+    HIP_TRY(launch_lincomb(N, cp, ys + (size_t)i * N * 4, 4, 0, s));
+  }
+  if (grad_in) {
+    LinComb lc{};
+    lc.x[0] = grad_out;
+    lc.ld[0] = 4;
+    lc.c[0] = 1.f;
+    lc.n = 1;
+    for (int i = 0; i < tb.s; ++i) {
+      lc.x[lc.n] = ys + (size_t)i * N * 4;
+      lc.ld[lc.n] = 4;
+      lc.c[lc.n] = 1.f;
+      ++lc.n;
+    }
+    HIP_TRY(launch_lincomb(N, lc, grad_in, 4, 0, s));
+  }
+  return MGN_OK;
+}
+
+
 }  // namespace
 }  // namespace mgn
 
@@ -814,6 +873,90 @@ int mgn_patch_step(mgn_ctx* ctx, int32_t n_patches, const mgn_dpatch* patches, c
   return MGN_OK;
 }
 
+double mgn_adam_lr(const mgn_adam* a, int64_t k) {
+  if (!a || k < 1 || a->decay_steps <= 0 || !(a->lr_start > 0) || !(a->lr_end > 0)) return -1.0;
+  return a->lr_start * std::pow(a->lr_end / a->lr_start, (double)(k - 1) / (double)a->decay_steps);
+}
+
+static int adam_checked(const mgn_adam* a, int64_t k, float* params, const float* grad, float* m, float* v, int64_t n,
+                        hipStream_t s, const char* who) {
+  const double lr = mgn_adam_lr(a, k);
+  if (lr < 0) return fail(MGN_ERR_ARG, "%s: bad Adam settings or update index %lld", who, (long long)k);
+  if (!(a->beta1 >= 0.0 && a->beta1 < 1.0 && a->beta2 >= 0.0 && a->beta2 < 1.0 && a->eps > 0.0))
+    return fail(MGN_ERR_ARG, "%s: Adam betas must lie in [0, 1) and eps be > 0", who);
+  if (n < 0 || (n > 0 && (!params || !grad || !m || !v))) return fail(MGN_ERR_ARG, "%s: null Adam buffer", who);
+  const double bc1 = 1.0 - std::pow(a->beta1, (double)k), bc2 = 1.0 - std::pow(a->beta2, (double)k);
+  HIP_TRY(launch_adam(n, params, grad, m, v, (float)lr, (float)a->beta1, (float)(1.0 - a->beta1), (float)a->beta2,
+                      (float)(1.0 - a->beta2), (float)a->eps, (float)bc1, (float)bc2, s));
+  return MGN_OK;
+}
+
+int mgn_adam_step(const mgn_adam* a, int64_t k, float* params, const float* grad, float* m, float* v, int64_t n,
+                  void* stream) {
+  return adam_checked(a, k, params, grad, m, v, n, S(stream), "mgn_adam_step");
+}
+
+int mgn_train_step(mgn_ctx* ctx, int32_t n_patches, const mgn_dpatch* patches, float* params, int32_t scheme,
+                   const float* static_feat, const float* y, const float* y_target, const float* noise,
+                   const float* noise_std, int64_t n_loss_nodes, float* grad, float* adam_m, float* adam_v,
+                   const mgn_adam* adam, int64_t k, float* loss, int64_t n_global, void* ws, size_t ws_bytes,
+                   void* stream) {
+  if (!ctx) return fail(MGN_ERR_ARG, "mgn_train_step: null ctx");
+  Ctx& c = ctx->c;
+  Tableau tb;
+  if (!tableau(scheme, tb)) return fail(MGN_ERR_ARG, "mgn_train_step: unknown scheme %d", scheme);
+  if (tb.s > c.max_stages)
+    return fail(MGN_ERR_ARG, "mgn_train_step: scheme needs %d stages, context plans %d", tb.s, c.max_stages);
+  if (!c.save) return fail(MGN_ERR_STATE, "mgn_train_step: context was created without save");
+  if (n_patches < 0 || (n_patches > 0 && !patches) || n_global < 0 || n_loss_nodes <= 0)
+    return fail(MGN_ERR_ARG, "mgn_train_step: bad patch list, global size or loss node count");
+  if (!params || !grad || !adam_m || !adam_v || !adam || !loss)
+    return fail(MGN_ERR_ARG, "mgn_train_step: null parameter, gradient, Adam or loss buffer");
+  if (n_global > 0 && (!static_feat || !y || !y_target)) return fail(MGN_ERR_ARG, "mgn_train_step: null global state");
+  int rc;
+  for (int32_t p = 0; p < n_patches; ++p) {
+    const mgn_dpatch& P = patches[p];
+    if ((rc = check_call(&c, &P.g, params, ws, ws_bytes, 1)) != MGN_OK) return rc;
+    if (P.g.n_nodes > 0 && (!P.node_l2g || !P.interior || (P.g.n_edges > 0 && !P.efeat) || n_global == 0))
+      return fail(MGN_ERR_ARG, "mgn_train_step: patch %d: null maps or edge features", p);
+  }
+  static const float kPaperStd[4] = {0.02f, 0.02f, 0.03f, 0.05f};
+  const float* sd = noise_std ? noise_std : kPaperStd;
+  const int64_t P_n = c.M.total;
+  char* w = (char*)ws;
+  hipStream_t s = S(stream);
+  HIP_TRY(launch_fill(grad, P_n, 0.f, s));
+  HIP_TRY(launch_fill(loss, 1, 0.f, s));
+  const float inv = (float)(1.0 / (4.0 * (double)n_loss_nodes));
+  bool packed = false;
+  for (int32_t p = 0; p < n_patches; ++p) {
+    const mgn_dpatch& P = patches[p];
+    const int64_t Np = P.g.n_nodes;
+    if (Np == 0) continue;
+    float* st_p = (float*)(w + c.L.pio);
+    float* y_p = st_p + (size_t)c.maxN * 4;
+    float* yn_p = y_p + (size_t)c.maxN * 4;
+    float* go_p = yn_p + (size_t)c.maxN * 4;
+    HIP_TRY(launch_gather_rows4(Np, static_feat, P.node_l2g, n_global, st_p, s));
+    HIP_TRY(launch_gather_noisy(Np, y, noise, sd, P.node_l2g, n_global, y_p, s));
+    if ((rc = integrate_core(c, P.g, params, tb, st_p, y_p, P.efeat, yn_p, 1, w, s, !packed)) != MGN_OK) return rc;
+    packed = true;
+    c.saved = 2;
+    c.scheme = scheme;
+    c.stages = tb.s;
+    c.g = P.g;
+    c.params = params;
+    c.efeat = P.efeat;
+    c.node_in = nullptr;
+    c.ws = w;
+    HIP_TRY(launch_mse(Np, yn_p, y_target, P.node_l2g, P.interior, n_global, inv, go_p, (float*)(w + c.L.lossp), loss,
+                       s));
+    if ((rc = backward_core(c, go_p, grad, nullptr, s)) != MGN_OK) return rc;
+  }
+  c.saved = 0;
+  return adam_checked(adam, k, params, grad, adam_m, adam_v, P_n, s, "mgn_train_step");
+}
+
 int mgn_pec_step(mgn_ctx* ctx, const mgn_dgraph* g, const float* params, const float* static_feat, const float* y,
                  float* khist, const float* efeat, float* y_next, int32_t first, void* ws, size_t ws_bytes,
                  void* stream) {
@@ -868,55 +1011,7 @@ int mgn_backward(mgn_ctx* ctx, const float* grad_out, float* grad_params, float*
   const int64_t N = c.g.n_nodes;
   if (N == 0) return MGN_OK;
   if (!grad_out || !grad_params) return fail(MGN_ERR_ARG, "mgn_backward: null gradient buffer");
-  Run r{c, c.g, c.params, c.ws, S(stream), N, c.g.n_edges, c.cfg.mp_steps, c.cfg.precision, c.cfg.ln_eps};
-  r.keep_a1 = true;
-  int rc;
-  if (c.saved == 1) return r.backward(0, c.node_in, c.efeat, grad_out, grad_params, grad_in);
-  Tableau tb;
-  tableau(c.scheme, tb);
-  char* w = c.ws;
-  float* node_in = (float*)(w + c.L.node_in);
-  float* kbar = (float*)(w + c.L.kbar);
-  float* ys = (float*)(w + c.L.ystage);
-  float* gin = (float*)(w + c.L.gin);
-  for (int i = tb.s - 1; i >= 0; --i) {
-    LinComb lc{};
-    lc.x[0] = grad_out;
-    lc.ld[0] = 4;
-    lc.c[0] = tb.b[i];
-    lc.n = 1;
-    for (int j = i + 1; j < tb.s; ++j)
-      if (tb.a[j][i] != 0.f) {
-        lc.x[lc.n] = ys + (size_t)j * N * 4;
-        lc.ld[lc.n] = 4;
-        lc.c[lc.n] = tb.a[j][i];
-        ++lc.n;
-      }
-    HIP_TRY(launch_lincomb(N, lc, kbar, 4, 0, S(stream)));
-    if ((rc = r.backward(i, node_in + (size_t)i * N * 8, c.efeat, kbar, grad_params, gin)) != MGN_OK) return rc;
-    LinComb cp{};
-    cp.x[0] = gin;
-    cp.ld[0] = 8;
-    cp.off[0] = 4;
-    cp.c[0] = 1.f;
-    cp.n = 1;
-    HIP_TRY(launch_lincomb(N, cp, ys + (size_t)i * N * 4, 4, 0, S(stream)));
-  }
-  if (grad_in) {
-    LinComb lc{};
-    lc.x[0] = grad_out;
-    lc.ld[0] = 4;
-    lc.c[0] = 1.f;
-    lc.n = 1;
-    for (int i = 0; i < tb.s; ++i) {
-      lc.x[lc.n] = ys + (size_t)i * N * 4;
-      lc.ld[lc.n] = 4;
-      lc.c[lc.n] = 1.f;
-      ++lc.n;
-    }
-    HIP_TRY(launch_lincomb(N, lc, grad_in, 4, 0, S(stream)));
-  }
-  return MGN_OK;
+  return backward_core(c, grad_out, grad_params, grad_in, S(stream));
 }
 
 }  // extern "C"

@@ -157,6 +157,17 @@ hipError_t launch_lincomb(int64_t N, const LinComb& lc, float* out, int32_t out_
                           hipStream_t s);
 // p[0..n) = v
 hipError_t launch_fill(float* p, int64_t n, float v, hipStream_t s);
+// Training step: partial rows of the loss sum; noisy gather dst[r] =
+// y[idx[r]] + sd * noise[idx[r]] (noise nullable); masked squared error of
+// pred against target[idx[r]] over mask rows: gradient 2 d inv, loss +=
+// inv sum d^2 (fixed order); fused Adam update.
+int loss_blocks();
+hipError_t launch_gather_noisy(int64_t n, const float* y, const float* noise, const float* sd, const int32_t* idx,
+                               int64_t n_src, float* dst, hipStream_t s);
+hipError_t launch_mse(int64_t n, const float* pred, const float* target, const int32_t* idx, const uint8_t* mask,
+                      int64_t n_src, float inv, float* gout, float* part, float* loss, hipStream_t s);
+hipError_t launch_adam(int64_t n, float* p, const float* g, float* m, float* v, float lr, float b1, float omb1, float b2,
+                       float omb2, float eps, float bc1, float bc2, hipStream_t s);
 // dst[r][0..4) = src[idx[r]][0..4) for r < n (idx clamped into [0, n_src))
 hipError_t launch_gather_rows4(int64_t n, const float* src, const int32_t* idx, int64_t n_src, float* dst,
                                hipStream_t s);

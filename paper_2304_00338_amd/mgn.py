@@ -47,6 +47,15 @@ class DPatch(C.Structure):
     _fields_ = [("g", DGraph), ("efeat", C.c_void_p), ("node_l2g", C.c_void_p), ("interior", C.c_void_p)]
 
 
+class Adam(C.Structure):
+    """mgn_adam: the paper's schedule (App. C) by default."""
+    _fields_ = [("lr_start", C.c_double), ("lr_end", C.c_double), ("decay_steps", C.c_int64),
+                ("beta1", C.c_double), ("beta2", C.c_double), ("eps", C.c_double)]
+
+    def __init__(self, lr_start=1e-3, lr_end=1e-7, decay_steps=4_000_000, beta1=0.9, beta2=0.999, eps=1e-8):
+        super().__init__(lr_start, lr_end, decay_steps, beta1, beta2, eps)
+
+
 _lib = None
 
 EXPORTS = [
@@ -54,7 +63,7 @@ EXPORTS = [
     "mgn_graph_schedule", "mgn_tile_edges", "mgn_tile_nodes", "mgn_graph_destroy",
     "mgn_partition", "mgn_extract_patch", "mgn_patch_copy_maps", "mgn_ctx_create",
     "mgn_ctx_destroy", "mgn_forward", "mgn_backward", "mgn_integrate_step",
-    "mgn_pec_step", "mgn_patch_step", "mgn_scheme_stages", "mgn_version", "mgn_last_error", "mgn_profile_enable",
+    "mgn_pec_step", "mgn_patch_step", "mgn_adam_lr", "mgn_adam_step", "mgn_train_step", "mgn_scheme_stages", "mgn_version", "mgn_last_error", "mgn_profile_enable",
     "mgn_profile_collect",
 ]
 
@@ -87,6 +96,10 @@ def lib():
         "mgn_integrate_step": (C.c_int, [vp, P(DGraph), vp, i32, vp, vp, vp, vp, i32, vp, C.c_size_t, vp]),
         "mgn_pec_step": (C.c_int, [vp, P(DGraph), vp, vp, vp, vp, vp, vp, i32, vp, C.c_size_t, vp]),
         "mgn_patch_step": (C.c_int, [vp, i32, P(DPatch), vp, i32, vp, vp, vp, i64, vp, C.c_size_t, vp]),
+        "mgn_adam_lr": (C.c_double, [P(Adam), i64]),
+        "mgn_adam_step": (C.c_int, [P(Adam), i64, vp, vp, vp, vp, i64, vp]),
+        "mgn_train_step": (C.c_int, [vp, i32, P(DPatch), vp, i32, vp, vp, vp, vp, vp, i64, vp, vp, vp, P(Adam), i64,
+                                     vp, i64, vp, C.c_size_t, vp]),
         "mgn_scheme_stages": (C.c_int, [i32]),
         "mgn_version": (C.c_char_p, []),
         "mgn_last_error": (C.c_char_p, []),
@@ -357,6 +370,45 @@ def mgn_patch_step(ctx: Context, patches, params, scheme, static, y, y_next=None
                                 _dptr(y_next, torch.float32, (n, 4), "y_next"), n,
                                 _dptr(ctx.ws, name="workspace"), ctx.ws_bytes, _stream(stream)))
     return y_next
+
+
+def mgn_adam_lr(adam, k):
+    return lib().mgn_adam_lr(C.byref(adam), int(k))
+
+
+def mgn_adam_step(adam, k, params, grad, m, v, stream=None):
+    """The k-th Adam update of params in place (see include/mgn.h)."""
+    torch = _torch()
+    n = params.numel()
+    _check(lib().mgn_adam_step(C.byref(adam), int(k), _dptr(params, torch.float32, name="params"),
+                               _dptr(grad, torch.float32, (n,), "grad"), _dptr(m, torch.float32, (n,), "m"),
+                               _dptr(v, torch.float32, (n,), "v"), n, _stream(stream)))
+
+
+def mgn_train_step(ctx: Context, patches, params, scheme, static, y, y_target, noise, grad, m, v, adam, k,
+                   n_loss_nodes=None, noise_std=None, loss=None, stream=None):
+    """One patch-training step (see include/mgn.h); returns the device loss
+    (a 1-element tensor)."""
+    torch = _torch()
+    n = y.shape[0]
+    sc = SCHEMES[scheme] if isinstance(scheme, str) else int(scheme)
+    if loss is None:
+        loss = torch.zeros(1, dtype=torch.float32, device=y.device)
+    if n_loss_nodes is None:
+        n_loss_nodes = sum(int(p.n_interior) for p in patches)
+    sd = None if noise_std is None else (C.c_float * 4)(*[float(x) for x in noise_std])
+    arr = (DPatch * max(1, len(patches)))(*[p.struct for p in patches])
+    npar = params.numel()
+    _check(lib().mgn_train_step(ctx._h, len(patches), arr, _dptr(params, torch.float32, name="params"), sc,
+                                _dptr(static, torch.float32, (n, 4), "static"), _dptr(y, torch.float32, (n, 4), "y"),
+                                _dptr(y_target, torch.float32, (n, 4), "y_target"),
+                                _dptr(noise, torch.float32, (n, 4), "noise") if noise is not None else None,
+                                C.cast(sd, C.c_void_p) if sd is not None else None, int(n_loss_nodes),
+                                _dptr(grad, torch.float32, (npar,), "grad"), _dptr(m, torch.float32, (npar,), "m"),
+                                _dptr(v, torch.float32, (npar,), "v"), C.byref(adam), int(k),
+                                _dptr(loss, torch.float32, (1,), "loss"), n,
+                                _dptr(ctx.ws, name="workspace"), ctx.ws_bytes, _stream(stream)))
+    return loss
 
 
 def mgn_pec_step(ctx: Context, g: DeviceGraph, params, static, y, khist, efeat, first=False,

@@ -295,6 +295,68 @@ def test_patch_rollout_thin_ghost_zone_differs():
     assert torch.equal(ye, mgn.mgn_integrate_step(ctx_w, dg, params, "euler", st, y0, dg.efeat))
 
 
+def test_adam_step_matches_oracle():
+    """The fused Adam kernel against the oracle's update (k = 3, the paper's
+    schedule), on the same parameters, gradient and moments."""
+    rng = np.random.default_rng(31)
+    n = 20000
+    p0 = rng.standard_normal(n).astype(np.float32)
+    g = rng.standard_normal(n).astype(np.float32)
+    m0 = (rng.standard_normal(n) * 0.1).astype(np.float32)
+    v0 = (rng.random(n) * 0.01).astype(np.float32)
+    d = lambda a: torch.from_numpy(a.copy()).cuda()
+    p, m, v = d(p0), d(m0), d(v0)
+    adam = mgn.Adam()
+    mgn.mgn_adam_step(adam, 3, p, d(g), m, v)
+    assert abs(mgn.mgn_adam_lr(adam, 3) / O.lr_schedule(2) - 1) < 1e-12
+    rp, rm, rv = O.adam_update(p0.astype(np.float64), g.astype(np.float64), m0.astype(np.float64),
+                               v0.astype(np.float64), 3, O.lr_schedule(2))
+    _assert_update(p.cpu().numpy(), rp, p0)
+    assert rel_l2(m.cpu().numpy(), rm) < 1e-6 and rel_l2(v.cpu().numpy(), rv) < 1e-6
+
+
+def _assert_update(p_gpu, p_ref, p0):
+    """fp32 parameters after an update against the fp64 reference: within
+    the fp32 rounding of the stored value (one ulp) plus 1e-5 of the update."""
+    p_gpu, p_ref = np.asarray(p_gpu, np.float64), np.asarray(p_ref, np.float64)
+    bound = np.spacing(np.abs(p_ref).astype(np.float32)).astype(np.float64) + 1e-5 * np.abs(p_ref - p0).max()
+    assert np.all(np.abs(p_gpu - p_ref) <= bound), np.abs(p_gpu - p_ref).max()
+
+
+@pytest.mark.parametrize("prec", ["fp32", "bf16"])
+def test_train_step_matches_oracle(prec):
+    """One patch-training step (noisy input, Heun step per patch, masked MSE,
+    gradients summed over the patches, Adam) against the oracle at a smooth
+    point: loss and gradient to the output tolerance, and the update equal
+    to the oracle's Adam applied to the GPU gradient."""
+    import synth
+    m, shape = 1, (8, 7, 6)
+    M = synth.mesh(shape, 32)
+    g = mgn.build_graph(M["cells"], M["pos"])
+    go = O.build_graph(M["cells"], M["pos"])
+    part = synth.slab_part(shape, 2)
+    patches = [mgn.DevicePatch(mgn.extract_patch(g, part, p, 2 * m)) for p in range(2)]
+    opatches = [O.extract_patch(go, part, p, 2 * m) for p in range(2)]
+    P = synth.smooth_params(m, 32)
+    tgt = synth.next_states(M["states"], 32)
+    nz = synth.standard_noise(g.n_nodes, 32)
+    d = lambda a: torch.from_numpy(np.ascontiguousarray(a, np.float32)).cuda()
+    ctx = mgn.Context(m, max(p.n_nodes for p in patches), max(p.n_edges for p in patches), prec, max_stages=2,
+                      save=True)
+    params = d(P)
+    grad, mm, vv = torch.zeros_like(params), torch.zeros_like(params), torch.zeros_like(params)
+    loss = mgn.mgn_train_step(ctx, patches, params, "heun2", d(M["onehot"]), d(M["states"]), d(tgt), d(nz), grad,
+                              mm, vv, mgn.Adam(), 1)
+    z = np.zeros(P.size)
+    _, _, _, rloss, rgrad = O.train_step(opatches, P, "heun2", M["onehot"], M["states"], tgt, nz, m, z, z, 1)
+    tol = FP32_TOL if prec == "fp32" else BF16_TOL
+    assert abs(loss.item() - rloss) < tol * abs(rloss)
+    gg = grad.cpu().numpy()
+    assert rel_l2(gg, rgrad) < tol
+    rp, _, _ = O.adam_update(P.astype(np.float64), gg.astype(np.float64), z, z, 1, 1e-3)
+    _assert_update(params.cpu().numpy(), rp, P)
+
+
 def test_gradient_accumulates():
     """grad_params is accumulated into, so patch gradients can be summed
     (Sec. 2.2, condition 3)."""
