@@ -210,9 +210,10 @@ void mgn_ctx_destroy(mgn_ctx* ctx);
  * efeat))).  params: flat float32 buffer (device).  node_in [N][8],
  * efeat [E][4], out [N][4] (device).  With save != 0 the activations stay in
  * the workspace for mgn_backward (the context must have been created with
- * save).  The workspace must stay untouched until backward, and params, the
- * graph arrays and efeat must stay alive and unchanged until then (node_in
- * is copied into the workspace).  N = 0 is a no-op.
+ * save).  The workspace must stay untouched until backward, and the graph
+ * arrays and efeat must stay alive and unchanged until then (params and
+ * node_in are copied into the workspace by a saving call).  N = 0 is a
+ * no-op.
  * Errors: ARG, SHAPE (graph larger than the context), WORKSPACE, DEVICE. */
 int mgn_forward(mgn_ctx* ctx, const mgn_dgraph* g, const float* params,
                 const float* node_in, const float* efeat, float* out,

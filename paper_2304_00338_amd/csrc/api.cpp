@@ -143,7 +143,7 @@ struct Layout {
   size_t e_off = 0, h_off = 0, agg_off = 0, P_off = 0, a1_off = 0;  // within a set
   size_t node_in = 0, K = 0, slots = 0;
   // backward
-  size_t pio = 0, lossp = 0;
+  size_t pio = 0, lossp = 0, pcopy = 0;
   size_t ebar = 0, zbar = 0, dz = 0, nstr = 0, hb_a = 0, hb_b = 0, aggbar = 0, R = 0, part = 0, kbar = 0, ystage = 0, gin = 0;
   size_t total = 0;
 };
@@ -287,6 +287,8 @@ void plan(Ctx& c) {
   L.slots = o;
   o = al256(o + (size_t)max_slots(E) * D * 4);
   if (c.save) {
+    L.pcopy = o;  // a saving call's own copy of the parameters
+    o = al256(o + (size_t)c.M.total * 4);
     L.ebar = o;  // edge-gradient stream, in the edge-latent element type
     o = al256(o + (size_t)E * D * c.se);
     L.zbar = o;
@@ -773,10 +775,16 @@ int mgn_forward(mgn_ctx* ctx, const mgn_dgraph* g, const float* params, const fl
   if (g->n_nodes > 0 && (!node_in || !out || (g->n_edges > 0 && !efeat)))
     return fail(MGN_ERR_ARG, "mgn_forward: null input or output");
   c.saved = 0;
+  // a saving call keeps its own copies of the parameters and node_in for
+  // mgn_backward, and computes the forward from them
+  float* kept = (float*)((char*)ws + c.L.node_in);
+  if (save && g->n_nodes > 0) {
+    float* pc = (float*)((char*)ws + c.L.pcopy);
+    HIP_TRY(hipMemcpyAsync(pc, params, (size_t)c.M.total * sizeof(float), hipMemcpyDeviceToDevice, S(stream)));
+    params = pc;
+  }
   Run r{c, *g, params, (char*)ws, S(stream), g->n_nodes, g->n_edges, c.cfg.mp_steps, c.cfg.precision, c.cfg.ln_eps};
   r.keep_a1 = save != 0;
-  // a saving call keeps its own copy of node_in for mgn_backward
-  float* kept = (float*)((char*)ws + c.L.node_in);
   if (g->n_nodes > 0) {
     if ((rc = r.pack_weights()) != MGN_OK) return rc;
     if (save) HIP_TRY(hipMemcpyAsync(kept, node_in, (size_t)g->n_nodes * 8 * sizeof(float), hipMemcpyDeviceToDevice,
@@ -810,6 +818,11 @@ int mgn_integrate_step(mgn_ctx* ctx, const mgn_dgraph* g, const float* params, i
     return fail(MGN_ERR_ARG, "mgn_integrate_step: null input or output");
   c.saved = 0;
   char* w = (char*)ws;
+  if (save && g->n_nodes > 0) {  // a saving call computes from, and keeps, its own copy of the parameters
+    float* pc = (float*)(w + c.L.pcopy);
+    HIP_TRY(hipMemcpyAsync(pc, params, (size_t)c.M.total * sizeof(float), hipMemcpyDeviceToDevice, S(stream)));
+    params = pc;
+  }
   if ((rc = integrate_core(c, *g, params, tb, static_feat, y, efeat, y_next, save, w, S(stream), true)) != MGN_OK)
     return rc;
   if (save) {

@@ -393,6 +393,36 @@ def test_saving_forward_owns_its_input():
 
 
 @pytest.mark.parametrize("prec", ["fp32", "bf16"])
+@pytest.mark.parametrize("call", ["forward", "integrate"])
+def test_saving_call_owns_its_params(prec, call):
+    """A saving call keeps its own copy of the parameters: the caller's
+    buffer may be overwritten or freed and reused before mgn_backward."""
+    pb = Problem((7, 6, 5), 2, seed=9).device()
+    N, E = pb.g.n_nodes, pb.g.n_edges
+    st = torch.from_numpy(pb.onehot.astype(np.float32)).cuda()
+    y = torch.from_numpy(pb.states.astype(np.float32)).cuda()
+
+    def run(params):
+        ctx = mgn.Context(pb.m, N, E, prec, save=True)
+        if call == "forward":
+            mgn.mgn_forward(ctx, pb.dg, params, pb.d_node_in, pb.dg.efeat, save=True)
+        else:
+            mgn.mgn_integrate_step(ctx, pb.dg, params, "euler", st, y, pb.dg.efeat, save=True)
+        return ctx
+    ctx = run(pb.d_params)
+    ref = torch.zeros_like(pb.d_params)
+    mgn.mgn_backward(ctx, pb.d_w, ref)
+    tmp = pb.d_params.clone()
+    ctx = run(tmp)
+    tmp.fill_(0.5)
+    del tmp
+    gp = torch.zeros_like(pb.d_params)  # likely reuses the freed block
+    mgn.mgn_backward(ctx, pb.d_w, gp)
+    torch.cuda.synchronize()
+    assert torch.equal(gp, ref)
+
+
+@pytest.mark.parametrize("prec", ["fp32", "bf16"])
 def test_edgeless_graph(prec):
     """Nodes without any edge: every aggregate is zero and the edge MLPs get
     no gradient; the rest of the call runs as usual."""
