@@ -18,12 +18,15 @@ namespace mgn {
 
 namespace {
 
-constexpr int D = 128;
-constexpr int kPartBlocks = 512;       // persistent blocks of the backward kernels
-constexpr int64_t kPartStride = 49664; // largest per-block partial (node MLP)
-// node-MLP partial layout = its parameter order: W1 [128][256], b1, W2, b2
-// (49408 floats), then gamma, beta
+constexpr int kPartBlocks = 512;  // persistent blocks of the backward kernels
+// Largest per-block partial at kernel width LD: the node MLP's parameters,
+// W1 [LD][2 LD], b1, W2 [LD][LD], b2, gamma, beta.
+inline int64_t part_stride(int LD) { return 3LL * LD * LD + 4LL * LD; }
+// bf16 node-MLP partial layout (width 128) = its parameter order: W1
+// [128][256], b1, W2, b2 (49408 floats), then gamma, beta
 constexpr int kNodeGammaPart = 49408;
+// the row-layout (bf16) kernels' fixed latent width
+constexpr int kRowsD = 128;
 
 struct Off {
   int64_t W1 = 0, b1 = 0, W2 = 0, b2 = 0, g = -1, bt = -1, size = 0;
@@ -35,7 +38,7 @@ struct PackOff {
 };
 
 struct Model {
-  int m = 0;
+  int m = 0, lat = 0;  // MP steps, latent width
   Off enc_node, enc_edge, dec;
   std::vector<Off> edge, node;
   int64_t total = 0;
@@ -45,14 +48,16 @@ struct Model {
   std::vector<PackEnt> ents;
 };
 
-Off mlp_off(int64_t& o, int din, int dout, bool ln) {
+// Two-layer MLP din -> hid -> dout, parameters in the order W1 [hid][din],
+// b1, W2 [dout][hid], b2, then gamma, beta when it ends in a LayerNorm.
+Off mlp_off(int64_t& o, int din, int hid, int dout, bool ln) {
   Off r;
   r.W1 = o;
-  o += (int64_t)D * din;
+  o += (int64_t)hid * din;
   r.b1 = o;
-  o += D;
+  o += hid;
   r.W2 = o;
-  o += (int64_t)dout * D;
+  o += (int64_t)dout * hid;
   r.b2 = o;
   o += dout;
   if (ln) {
@@ -83,50 +88,57 @@ void add_pack(Model& M, int64_t src, int rows, int cols, int64_t& W, int64_t& Wt
   M.ents.push_back(e);
 }
 
-// Row-permuted copy (perm_row) of `cols` columns of a [D][ld] matrix starting
-// at float offset src.
-void add_perm(Model& M, int64_t src, int ld, int64_t& W, int cols = D) {
+// Row-permuted copy (perm_row) of `cols` columns of a [128][ld] matrix
+// starting at float offset src (row-layout kernels, width 128 only).
+void add_perm(Model& M, int64_t src, int ld, int64_t& W, int cols = kRowsD) {
   auto al = [](int64_t x) { return (x + 63) & ~int64_t(63); };
   M.pack_elems = al(M.pack_elems);
   W = M.pack_elems;
-  M.pack_elems += (int64_t)D * cols;
+  M.pack_elems += (int64_t)kRowsD * cols;
   PackEnt e;
   e.src = src;
   e.dst = W;
   e.dstt = -1;
-  e.rows = D;
+  e.rows = kRowsD;
   e.cols = cols;
   e.ld = ld;
   e.perm = 1;
   M.ents.push_back(e);
 }
 
-Model make_model(int m) {
+// Parameter layout and packed operand copies of an MGN with m MP steps and
+// latent width lat (both MLP layers of every block are lat wide).
+Model make_model(int m, int lat) {
+  const int D = lat;
   Model M;
   M.m = m;
+  M.lat = lat;
   int64_t o = 0;
-  M.enc_node = mlp_off(o, 8, D, true);
-  M.enc_edge = mlp_off(o, 4, D, true);
+  M.enc_node = mlp_off(o, 8, D, D, true);
+  M.enc_edge = mlp_off(o, 4, D, D, true);
   for (int i = 0; i < m; ++i) {
-    M.edge.push_back(mlp_off(o, 3 * D, D, true));
-    M.node.push_back(mlp_off(o, 2 * D, D, true));
+    M.edge.push_back(mlp_off(o, 3 * D, D, D, true));
+    M.node.push_back(mlp_off(o, 2 * D, D, D, true));
   }
-  M.dec = mlp_off(o, D, 4, false);
+  M.dec = mlp_off(o, D, D, 4, false);
   M.total = o;
+  const bool rows = lat == kRowsD;  // row-permuted copies for the row-layout kernels
   add_pack(M, M.enc_node.W2, D, D, M.p_enc_node.W2, M.p_enc_node.W2t);
   add_pack(M, M.enc_edge.W2, D, D, M.p_enc_edge.W2, M.p_enc_edge.W2t);
-  add_perm(M, M.enc_edge.W2, D, M.p_enc_edge.W2p);
+  if (rows) add_perm(M, M.enc_edge.W2, D, M.p_enc_edge.W2p);
   M.p_edge.resize(m);
   M.p_node.resize(m);
   for (int i = 0; i < m; ++i) {
     add_pack(M, M.edge[i].W1, D, 3 * D, M.p_edge[i].W1, M.p_edge[i].W1t);
     add_pack(M, M.edge[i].W2, D, D, M.p_edge[i].W2, M.p_edge[i].W2t);
-    add_perm(M, M.edge[i].W1, 3 * D, M.p_edge[i].W1p);
-    add_perm(M, M.edge[i].W2, D, M.p_edge[i].W2p);
-    add_perm(M, M.edge[i].W1 + D, 3 * D, M.p_edge[i].W1sp);
-    add_perm(M, M.edge[i].W1 + 2 * D, 3 * D, M.p_edge[i].W1rp);
-    add_perm(M, M.node[i].W1, 2 * D, M.p_node[i].W1p, 2 * D);
-    add_perm(M, M.node[i].W2, D, M.p_node[i].W2p);
+    if (rows) {
+      add_perm(M, M.edge[i].W1, 3 * D, M.p_edge[i].W1p);
+      add_perm(M, M.edge[i].W2, D, M.p_edge[i].W2p);
+      add_perm(M, M.edge[i].W1 + D, 3 * D, M.p_edge[i].W1sp);
+      add_perm(M, M.edge[i].W1 + 2 * D, 3 * D, M.p_edge[i].W1rp);
+      add_perm(M, M.node[i].W1, 2 * D, M.p_node[i].W1p, 2 * D);
+      add_perm(M, M.node[i].W2, D, M.p_node[i].W2p);
+    }
     add_pack(M, M.node[i].W1, D, 2 * D, M.p_node[i].W1, M.p_node[i].W1t);
     add_pack(M, M.node[i].W2, D, D, M.p_node[i].W2, M.p_node[i].W2t);
   }
@@ -134,10 +146,39 @@ Model make_model(int m) {
   return M;
 }
 
+// Blocks that move the parameters of the real model R (latent dr) to the
+// zero-padded kernel model K (width LD): per MLP, W1 by input-column block
+// (node / edge input blocks of width 8 / 4 unpadded, latent blocks dr -> LD),
+// then b1, W2, b2 and the LayerNorm gain and offset.  a = R, b = K.
+std::vector<CopyBlock> pad_blocks(const Model& R, const Model& K) {
+  std::vector<CopyBlock> v;
+  const int dr = R.lat, LD = K.lat;
+  auto mlp = [&](const Off& r, const Off& k, int nin, int win_r, int win_k, int dout_r, int dout_k, bool ln) {
+    const int din_r = nin * win_r, din_k = nin * win_k;
+    for (int j = 0; j < nin; ++j) v.push_back({r.W1 + (int64_t)j * win_r, k.W1 + (int64_t)j * win_k, dr, win_r, din_r, din_k});
+    v.push_back({r.b1, k.b1, 1, dr, dr, LD});
+    v.push_back({r.W2, k.W2, dout_r, dr, dr, LD});
+    v.push_back({r.b2, k.b2, 1, dout_r, dout_r, dout_k});
+    if (ln) {
+      v.push_back({r.g, k.g, 1, dout_r, dout_r, dout_k});
+      v.push_back({r.bt, k.bt, 1, dout_r, dout_r, dout_k});
+    }
+  };
+  mlp(R.enc_node, K.enc_node, 1, 8, 8, dr, LD, true);
+  mlp(R.enc_edge, K.enc_edge, 1, 4, 4, dr, LD, true);
+  for (int i = 0; i < R.m; ++i) {
+    mlp(R.edge[i], K.edge[i], 3, dr, LD, dr, LD, true);
+    mlp(R.node[i], K.node[i], 2, dr, LD, dr, LD, true);
+  }
+  mlp(R.dec, K.dec, 1, dr, LD, 4, 4, false);
+  return v;
+}
+
 size_t al256(size_t x) { return (x + 255) & ~size_t(255); }
 
 struct Layout {
   size_t pack = 0;
+  size_t ppad = 0, gpad = 0;  // latent 150: padded parameter and gradient copies
   // activation sets
   size_t act = 0, act_stride = 0;
   size_t e_off = 0, h_off = 0, agg_off = 0, P_off = 0, a1_off = 0;  // within a set
@@ -171,7 +212,11 @@ struct Ctx {
   int32_t max_stages = 1, save = 0;
   int se = 4;  // bytes per element of the edge-latent stream
   int ne_sets = 1;
-  Model M;
+  // latent widths: DR the model's (128 or 150), LD the kernels' (128 or 160)
+  int DR = 128, LD = 128;
+  Model M;   // kernel-width model (parameters as the kernels see them)
+  Model Mr;  // the caller's parameter layout (same as M when DR == LD)
+  std::vector<CopyBlock> pad;  // Mr -> M moves when DR != LD
   Layout L;
   // saved state of the last call with save != 0
   int saved = 0;  // 0 none, 1 forward, 2 integration step
@@ -251,11 +296,16 @@ bool tableau(int32_t scheme, Tableau& t) {
 void plan(Ctx& c) {
   const int64_t N = c.maxN, E = c.maxE;
   const int m = c.cfg.mp_steps;
+  const int D = c.LD;
   const size_t tsz = c.cfg.precision == MGN_BF16 ? 2 : 4;
   Layout& L = c.L;
   size_t o = 0;
   L.pack = o;
   o = al256(o + (size_t)c.M.pack_elems * tsz);
+  if (c.LD != c.DR) {
+    L.ppad = o;  // the zero-padded copy of the parameters every call computes from
+    o = al256(o + (size_t)c.M.total * 4);
+  }
   const int le = c.save ? std::max(m, 1) : 1;
   const int lh = c.save ? m + 1 : 1;
   const int la = c.save ? std::max(m, 1) : 1;
@@ -287,8 +337,12 @@ void plan(Ctx& c) {
   L.slots = o;
   o = al256(o + (size_t)max_slots(E) * D * 4);
   if (c.save) {
-    L.pcopy = o;  // a saving call's own copy of the parameters
-    o = al256(o + (size_t)c.M.total * 4);
+    L.pcopy = o;  // a saving call's own copy of the parameters (the padded copy serves at latent 150)
+    o = al256(o + (c.LD == c.DR ? (size_t)c.M.total * 4 : 0));
+    if (c.LD != c.DR) {
+      L.gpad = o;  // gradients in the padded layout, moved to the caller's layout at the end
+      o = al256(o + (size_t)c.M.total * 4);
+    }
     L.ebar = o;  // edge-gradient stream, in the edge-latent element type
     o = al256(o + (size_t)E * D * c.se);
     L.zbar = o;
@@ -307,7 +361,7 @@ void plan(Ctx& c) {
     L.R = o;
     o = al256(o + (size_t)N * D * 4);
     L.part = o;
-    o = al256(o + (size_t)kPartBlocks * kPartStride * 4);
+    o = al256(o + (size_t)kPartBlocks * part_stride(D) * 4);
     L.kbar = o;
     o = al256(o + (size_t)N * 4 * 4);
     L.ystage = o;
@@ -344,6 +398,7 @@ struct Run {
   int prec;
   float eps;
   bool keep_a1 = false;  // this call saves (or the backward reads) the edge MLPs' a1
+  int D = c.LD;          // kernel latent width
 
   // Bracket a launch with profiling events when enabled.
   hipError_t mark_begin(int kind) {
@@ -415,7 +470,7 @@ struct Run {
   Partials part() const {
     Partials p;
     p.buf = (float*)(ws + c.L.part);
-    p.stride = kPartStride;
+    p.stride = part_stride(D);
     p.max_blocks = kPartBlocks;
     return p;
   }
@@ -436,34 +491,34 @@ struct Run {
     const EdgeTiles tl = tiles();
     MlpW e0;
     if (m > 0) e0 = W(M.edge[0], M.p_edge[0]);
-    LAUNCH(K_NODE_ENC, launch_node_enc(prec, N, node_in, W(M.enc_node, M.p_enc_node), m > 0 ? &e0 : nullptr, eps, h_l(k, 0),
+    LAUNCH(K_NODE_ENC, launch_node_enc(prec, D, N, node_in, W(M.enc_node, M.p_enc_node), m > 0 ? &e0 : nullptr, eps, h_l(k, 0),
                             P_l(k, 0), s));
     if (m > 0) {
       if (prec == MGN_BF16)
         LAUNCH(K_EDGE_ENC, launch_edge_enc_rows(E, efeat, W(M.enc_edge, M.p_enc_edge), eps, e_l(k, 0), s));
       else
-        LAUNCH(K_EDGE_ENC, launch_edge_enc(prec, E, efeat, W(M.enc_edge, M.p_enc_edge), eps, e_l(k, 0), s));
+        LAUNCH(K_EDGE_ENC, launch_edge_enc(prec, D, E, efeat, W(M.enc_edge, M.p_enc_edge), eps, e_l(k, 0), s));
     }
     for (int l = 0; l < m; ++l) {
       const bool last = l == m - 1;
       void* e_out = c.save ? (last ? nullptr : e_l(k, l + 1)) : e_l(k, 0);
       if (E > 0)
-        LAUNCH(K_EDGE_FWD, launch_edge_fwd(prec, tl, e_l(k, l), e_out, last ? 0 : 1, P_l(k, l), W(M.edge[l], M.p_edge[l]),
+        LAUNCH(K_EDGE_FWD, launch_edge_fwd(prec, D, tl, e_l(k, l), e_out, last ? 0 : 1, P_l(k, l), W(M.edge[l], M.p_edge[l]),
                                 eps, agg_l(k, l), slots(), a1_l(k, l), s));
       else
         LAUNCH(K_EDGE_FWD, launch_fill(agg_l(k, l), N * D, 0.f, s));  // no edges: every aggregate is zero
-      if (g.n_long > 0) LAUNCH(K_FIXUP, launch_slot_fixup(g.long_nodes, g.n_long, slots(), agg_l(k, l), s));
+      if (g.n_long > 0) LAUNCH(K_FIXUP, launch_slot_fixup(D, g.long_nodes, g.n_long, slots(), agg_l(k, l), s));
       MlpW nx;
       if (!last) nx = W(M.edge[l + 1], M.p_edge[l + 1]);
       if (prec == MGN_BF16) {
         LAUNCH(K_NODE_FWD, launch_node_fwd_rows(N, h_l(k, l), agg_l(k, l), W(M.node[l], M.p_node[l]), eps, h_l(k, l + 1), s));
         if (!last) LAUNCH(K_EMIT, launch_emit_rows(N, h_l(k, l + 1), nx, P_l(k, l + 1), s));
       } else {
-        LAUNCH(K_NODE_FWD, launch_node_fwd(prec, N, h_l(k, l), agg_l(k, l), W(M.node[l], M.p_node[l]), last ? nullptr : &nx,
+        LAUNCH(K_NODE_FWD, launch_node_fwd(prec, D, N, h_l(k, l), agg_l(k, l), W(M.node[l], M.p_node[l]), last ? nullptr : &nx,
                                 eps, h_l(k, l + 1), last ? nullptr : P_l(k, l + 1), s));
       }
     }
-    LAUNCH(K_DECODER, launch_decoder(prec, N, h_l(k, m), W(M.dec, M.p_dec), out, s));
+    LAUNCH(K_DECODER, launch_decoder(prec, D, N, h_l(k, m), W(M.dec, M.p_dec), out, s));
     return MGN_OK;
   }
 
@@ -483,7 +538,7 @@ struct Run {
     void* ebar = ws + c.L.ebar;  // bf16: the edge-latent element type
     void* zbar = ws + c.L.zbar;
     int nb = 0, rc;
-    LAUNCH(K_DECODER_BWD, launch_decoder_bwd(prec, N, h_l(k, m), gout, W(M.dec, M.p_dec), hb_cur, pt, &nb, s));
+    LAUNCH(K_DECODER_BWD, launch_decoder_bwd(prec, D, N, h_l(k, m), gout, W(M.dec, M.p_dec), hb_cur, pt, &nb, s));
     if ((rc = reduce(nb, 0, 1, (int)M.dec.size, grad, M.dec.W1, 0)) != MGN_OK) return rc;
     for (int l = m - 1; l >= 0; --l) {
       const Off& oe = M.edge[l];
@@ -497,7 +552,7 @@ struct Run {
         LAUNCH(K_WGRAD_NODE, launch_wgrad_node(N, h_l(k, l), agg_l(k, l), ndz1, ndz2, na1, pt, &nb, s));
         if ((rc = reduce(nb, 0, 1, kNodeGammaPart, grad, on.W1, 0)) != MGN_OK) return rc;
       } else {
-        LAUNCH(K_NODE_BWD, launch_node_bwd(prec, N, h_l(k, l), agg_l(k, l), hb_cur, W(on, M.p_node[l]), eps, hb_part, aggbar,
+        LAUNCH(K_NODE_BWD, launch_node_bwd(prec, D, N, h_l(k, l), agg_l(k, l), hb_cur, W(on, M.p_node[l]), eps, hb_part, aggbar,
                                 pt, &nb, s));
         if ((rc = reduce(nb, 0, 1, (int)on.size, grad, on.W1, 0)) != MGN_OK) return rc;
       }
@@ -514,26 +569,26 @@ struct Run {
         if ((rc = reduce(nb, 16512, 1, D * D + D, grad, oe.W2, 0)) != MGN_OK) return rc;
         if ((rc = reduce(nb, 0, D, D, grad, oe.W1, 3 * D)) != MGN_OK) return rc;
       } else {
-        LAUNCH(K_EDGE_BWD, launch_edge_bwd(prec, tl, e_l(k, l), (float*)ebar, l < m - 1 ? 1 : 0, (float*)ebar, P_l(k, l), aggbar,
+        LAUNCH(K_EDGE_BWD, launch_edge_bwd(prec, D, tl, e_l(k, l), (float*)ebar, l < m - 1 ? 1 : 0, (float*)ebar, P_l(k, l), aggbar,
                                 W(oe, M.p_edge[l]), eps, zbar, R, slots(), pt, &nb, s));
-        if ((rc = reduce(nb, 16384, 1, (int)(oe.size - 3 * D * D), grad, oe.b1, 0)) != MGN_OK) return rc;
-        LAUNCH(K_WGRAD, launch_wgrad(prec, E, zbar, e_l(k, l), pt, &nb, s));
+        if ((rc = reduce(nb, (int64_t)D * D, 1, (int)(oe.size - 3 * D * D), grad, oe.b1, 0)) != MGN_OK) return rc;
+        LAUNCH(K_WGRAD, launch_wgrad(prec, D, E, zbar, e_l(k, l), pt, &nb, s));
         if ((rc = reduce(nb, 0, D, D, grad, oe.W1, 3 * D)) != MGN_OK) return rc;
       }
-      if (g.n_long > 0) LAUNCH(K_FIXUP, launch_slot_fixup(g.long_nodes, g.n_long, slots(), R, s));
-      LAUNCH(K_SRCSUM, launch_node_srcsum(prec, N, g.rowptr, g.rev, zbar, R, h_l(k, l), hb_part, W(oe, M.p_edge[l]), hb_cur,
+      if (g.n_long > 0) LAUNCH(K_FIXUP, launch_slot_fixup(D, g.long_nodes, g.n_long, slots(), R, s));
+      LAUNCH(K_SRCSUM, launch_node_srcsum(prec, D, N, g.rowptr, g.rev, zbar, R, h_l(k, l), hb_part, W(oe, M.p_edge[l]), hb_cur,
                                  pt, &nb, s));
       if ((rc = reduce(nb, 0, D, D, grad, oe.W1 + D, 3 * D)) != MGN_OK) return rc;
-      if ((rc = reduce(nb, 16384, D, D, grad, oe.W1 + 2 * D, 3 * D)) != MGN_OK) return rc;
+      if ((rc = reduce(nb, (int64_t)D * D, D, D, grad, oe.W1 + 2 * D, 3 * D)) != MGN_OK) return rc;
     }
     if (m > 0) {
       if (prec == MGN_BF16)
         LAUNCH(K_EDGE_ENC_BWD, launch_edge_enc_bwd_rows(E, efeat, ebar, W(M.enc_edge, M.p_enc_edge), eps, pt, &nb, s));
       else
-        LAUNCH(K_EDGE_ENC_BWD, launch_edge_enc_bwd(prec, E, efeat, (float*)ebar, W(M.enc_edge, M.p_enc_edge), eps, pt, &nb, s));
+        LAUNCH(K_EDGE_ENC_BWD, launch_edge_enc_bwd(prec, D, E, efeat, (float*)ebar, W(M.enc_edge, M.p_enc_edge), eps, pt, &nb, s));
       if ((rc = reduce(nb, 0, 1, (int)M.enc_edge.size, grad, M.enc_edge.W1, 0)) != MGN_OK) return rc;
     }
-    LAUNCH(K_NODE_ENC_BWD, launch_node_enc_bwd(prec, N, node_in, hb_cur, W(M.enc_node, M.p_enc_node), eps, gin, pt, &nb, s));
+    LAUNCH(K_NODE_ENC_BWD, launch_node_enc_bwd(prec, D, N, node_in, hb_cur, W(M.enc_node, M.p_enc_node), eps, gin, pt, &nb, s));
     if ((rc = reduce(nb, 0, 1, (int)M.enc_node.size, grad, M.enc_node.W1, 0)) != MGN_OK) return rc;
     return MGN_OK;
   }
@@ -541,9 +596,12 @@ struct Run {
 
 int check_cfg(const mgn_config* cfg) {
   if (!cfg) return fail(MGN_ERR_ARG, "null config");
-  if (cfg->node_in != 8 || cfg->edge_in != 4 || cfg->latent != D || cfg->out != 4 || cfg->mlp_layers != 2)
+  if (cfg->node_in != 8 || cfg->edge_in != 4 || (cfg->latent != 128 && cfg->latent != 150) || cfg->out != 4 ||
+      cfg->mlp_layers != 2)
     return fail(MGN_ERR_SHAPE,
-                "unsupported config (node_in 8, edge_in 4, latent 128, out 4, mlp_layers 2 are supported)");
+                "unsupported config (node_in 8, edge_in 4, latent 128 or 150, out 4, mlp_layers 2 are supported)");
+  if (cfg->latent == 150 && cfg->precision != MGN_FP32)
+    return fail(MGN_ERR_SHAPE, "latent 150 runs in fp32 only");
   if (cfg->mp_steps < 0 || cfg->mp_steps > 4096) return fail(MGN_ERR_ARG, "mp_steps out of range");
   if (cfg->precision != MGN_FP32 && cfg->precision != MGN_BF16) return fail(MGN_ERR_ARG, "unknown precision");
   if (!(cfg->ln_eps > 0.f)) return fail(MGN_ERR_ARG, "ln_eps must be > 0");
@@ -565,6 +623,28 @@ int check_call(Ctx* c, const mgn_dgraph* g, const float* params, void* ws, size_
         (g->n_edges > 0 && (!g->senders || !g->receivers || !g->rev)))
       return fail(MGN_ERR_ARG, "device graph arrays missing");
     if (g->n_long > 0 && !g->long_nodes) return fail(MGN_ERR_ARG, "long_nodes missing");
+  }
+  return MGN_OK;
+}
+
+// The parameters a call computes from: at latent 150 the zero-padded
+// kernel-width copy (written here, in the workspace); otherwise the caller's
+// buffer, or for a saving call the workspace copy that the backward reads.
+int stage_params(Ctx& c, const float*& params, char* ws, int save, hipStream_t s) {
+  if (c.LD != c.DR) {
+    float* pp = (float*)(ws + c.L.ppad);
+    HIP_TRY(launch_fill(pp, c.M.total, 0.f, s));
+    for (size_t b = 0; b < c.pad.size(); b += kCopyMax) {
+      CopyList L{};
+      L.n = (int32_t)std::min<size_t>(kCopyMax, c.pad.size() - b);
+      for (int j = 0; j < L.n; ++j) L.b[j] = c.pad[b + j];
+      HIP_TRY(launch_copy_blocks(L, params, pp, 0, s));
+    }
+    params = pp;
+  } else if (save) {
+    float* pc = (float*)(ws + c.L.pcopy);
+    HIP_TRY(hipMemcpyAsync(pc, params, (size_t)c.M.total * sizeof(float), hipMemcpyDeviceToDevice, s));
+    params = pc;
   }
   return MGN_OK;
 }
@@ -618,7 +698,29 @@ int integrate_core(Ctx& c, const mgn_dgraph& g, const float* params, const Table
 
 // Reverse mode of the saved forward or integration step (the body of
 // mgn_backward, also run per patch by mgn_train_step).
+int backward_steps(Ctx& c, const float* grad_out, float* grad_params, float* grad_in, hipStream_t s);
+
+// At latent 150 the kernels accumulate into a zero-initialised padded
+// gradient, which is then added to the caller's buffer in its own layout.
 int backward_core(Ctx& c, const float* grad_out, float* grad_params, float* grad_in, hipStream_t s) {
+  if (c.LD == c.DR) return backward_steps(c, grad_out, grad_params, grad_in, s);
+  float* gp = (float*)(c.ws + c.L.gpad);
+  HIP_TRY(launch_fill(gp, c.M.total, 0.f, s));
+  int rc = backward_steps(c, grad_out, gp, grad_in, s);
+  if (rc != MGN_OK) return rc;
+  for (size_t b = 0; b < c.pad.size(); b += kCopyMax) {
+    CopyList L{};
+    L.n = (int32_t)std::min<size_t>(kCopyMax, c.pad.size() - b);
+    for (int j = 0; j < L.n; ++j) {
+      const CopyBlock& f = c.pad[b + j];
+      L.b[j] = CopyBlock{f.b_off, f.a_off, f.rows, f.cols, f.b_ld, f.a_ld};
+    }
+    HIP_TRY(launch_copy_blocks(L, gp, grad_params, 1, s));
+  }
+  return MGN_OK;
+}
+
+int backward_steps(Ctx& c, const float* grad_out, float* grad_params, float* grad_in, hipStream_t s) {
   const int64_t N = c.g.n_nodes;
   Run r{c, c.g, c.params, c.ws, s, N, c.g.n_edges, c.cfg.mp_steps, c.cfg.precision, c.cfg.ln_eps};
   r.keep_a1 = true;
@@ -693,7 +795,7 @@ int mgn_scheme_stages(int32_t scheme) {
 
 int64_t mgn_param_count(const mgn_config* cfg) {
   if (check_cfg(cfg) != MGN_OK) return -1;
-  return make_model(cfg->mp_steps).total;
+  return make_model(cfg->mp_steps, cfg->latent).total;
 }
 
 int mgn_ctx_create(const mgn_config* cfg, int64_t max_nodes, int64_t max_edges, int32_t max_stages, int32_t save,
@@ -715,8 +817,12 @@ int mgn_ctx_create(const mgn_config* cfg, int64_t max_nodes, int64_t max_edges, 
   c.save = save ? 1 : 0;
   c.se = cfg->precision == MGN_BF16 ? 2 : 4;
   c.ne_sets = c.save ? max_stages : 1;
+  c.DR = cfg->latent;
+  c.LD = cfg->latent == 150 ? 160 : cfg->latent;
   try {
-    c.M = make_model(cfg->mp_steps);
+    c.M = make_model(cfg->mp_steps, c.LD);
+    c.Mr = c.LD == c.DR ? c.M : make_model(cfg->mp_steps, c.DR);
+    if (c.LD != c.DR) c.pad = pad_blocks(c.Mr, c.M);
   } catch (const std::bad_alloc&) {
     delete h;
     return fail(MGN_ERR_NOMEM, "mgn_ctx_create: out of host memory");
@@ -778,11 +884,7 @@ int mgn_forward(mgn_ctx* ctx, const mgn_dgraph* g, const float* params, const fl
   // a saving call keeps its own copies of the parameters and node_in for
   // mgn_backward, and computes the forward from them
   float* kept = (float*)((char*)ws + c.L.node_in);
-  if (save && g->n_nodes > 0) {
-    float* pc = (float*)((char*)ws + c.L.pcopy);
-    HIP_TRY(hipMemcpyAsync(pc, params, (size_t)c.M.total * sizeof(float), hipMemcpyDeviceToDevice, S(stream)));
-    params = pc;
-  }
+  if (g->n_nodes > 0 && (rc = stage_params(c, params, (char*)ws, save, S(stream))) != MGN_OK) return rc;
   Run r{c, *g, params, (char*)ws, S(stream), g->n_nodes, g->n_edges, c.cfg.mp_steps, c.cfg.precision, c.cfg.ln_eps};
   r.keep_a1 = save != 0;
   if (g->n_nodes > 0) {
@@ -818,11 +920,8 @@ int mgn_integrate_step(mgn_ctx* ctx, const mgn_dgraph* g, const float* params, i
     return fail(MGN_ERR_ARG, "mgn_integrate_step: null input or output");
   c.saved = 0;
   char* w = (char*)ws;
-  if (save && g->n_nodes > 0) {  // a saving call computes from, and keeps, its own copy of the parameters
-    float* pc = (float*)(w + c.L.pcopy);
-    HIP_TRY(hipMemcpyAsync(pc, params, (size_t)c.M.total * sizeof(float), hipMemcpyDeviceToDevice, S(stream)));
-    params = pc;
-  }
+  // a saving call computes from, and keeps, its own copy of the parameters
+  if (g->n_nodes > 0 && (rc = stage_params(c, params, w, save, S(stream))) != MGN_OK) return rc;
   if ((rc = integrate_core(c, *g, params, tb, static_feat, y, efeat, y_next, save, w, S(stream), true)) != MGN_OK)
     return rc;
   if (save) {
@@ -868,6 +967,7 @@ int mgn_patch_step(mgn_ctx* ctx, int32_t n_patches, const mgn_dpatch* patches, c
   if (!any) return MGN_OK;
   char* w = (char*)ws;
   hipStream_t s = S(stream);
+  if ((rc = stage_params(c, params, w, 0, s)) != MGN_OK) return rc;
   bool packed = false;
   for (int32_t p = 0; p < n_patches; ++p) {
     const mgn_dpatch& P = patches[p];
@@ -935,11 +1035,15 @@ int mgn_train_step(mgn_ctx* ctx, int32_t n_patches, const mgn_dpatch* patches, f
   }
   static const float kPaperStd[4] = {0.02f, 0.02f, 0.03f, 0.05f};
   const float* sd = noise_std ? noise_std : kPaperStd;
-  const int64_t P_n = c.M.total;
+  const int64_t P_n = c.Mr.total;
   char* w = (char*)ws;
   hipStream_t s = S(stream);
   HIP_TRY(launch_fill(grad, P_n, 0.f, s));
   HIP_TRY(launch_fill(loss, 1, 0.f, s));
+  // the step's forward and backward compute from run_params (the caller's
+  // buffer, or its padded copy at latent 150); Adam then updates params
+  const float* run_params = params;
+  if ((rc = stage_params(c, run_params, w, 0, s)) != MGN_OK) return rc;
   const float inv = (float)(1.0 / (4.0 * (double)n_loss_nodes));
   bool packed = false;
   for (int32_t p = 0; p < n_patches; ++p) {
@@ -952,13 +1056,13 @@ int mgn_train_step(mgn_ctx* ctx, int32_t n_patches, const mgn_dpatch* patches, f
     float* go_p = yn_p + (size_t)c.maxN * 4;
     HIP_TRY(launch_gather_rows4(Np, static_feat, P.node_l2g, n_global, st_p, s));
     HIP_TRY(launch_gather_noisy(Np, y, noise, sd, P.node_l2g, n_global, y_p, s));
-    if ((rc = integrate_core(c, P.g, params, tb, st_p, y_p, P.efeat, yn_p, 1, w, s, !packed)) != MGN_OK) return rc;
+    if ((rc = integrate_core(c, P.g, run_params, tb, st_p, y_p, P.efeat, yn_p, 1, w, s, !packed)) != MGN_OK) return rc;
     packed = true;
     c.saved = 2;
     c.scheme = scheme;
     c.stages = tb.s;
     c.g = P.g;
-    c.params = params;
+    c.params = run_params;
     c.efeat = P.efeat;
     c.node_in = nullptr;
     c.ws = w;
@@ -985,6 +1089,7 @@ int mgn_pec_step(mgn_ctx* ctx, const mgn_dgraph* g, const float* params, const f
   c.saved = 0;
   if (N == 0) return MGN_OK;
   char* w = (char*)ws;
+  if ((rc = stage_params(c, params, w, 0, S(stream))) != MGN_OK) return rc;
   Run r{c, *g, params, w, S(stream), N, g->n_edges, c.cfg.mp_steps, c.cfg.precision, c.cfg.ln_eps};
   if ((rc = r.pack_weights()) != MGN_OK) return rc;
   float* node_in = (float*)(w + c.L.node_in);

@@ -31,12 +31,15 @@ __device__ __forceinline__ void put_w(float* base, int ld, const f32x4 (&acc)[NC
 }
 
 // ------------------------------------------------------------ decoder
-template <int PREC>
-__global__ void __launch_bounds__(NT) k_decoder_bwd(int64_t N, const float* __restrict__ h,
+template <int PREC, int LD>
+__global__ void __launch_bounds__(LD * 4) k_decoder_bwd(int64_t N, const float* __restrict__ h,
                                                     const float* __restrict__ gout, MlpW w,
                                                     float* __restrict__ hbar, Partials part) {
   typedef Tr<PREC> P;
   typedef typename P::T T;
+  constexpr int D = LD;
+  [[maybe_unused]] constexpr int NW = Width<LD>::NW, NT = Width<LD>::NT;
+  constexpr int NCB = D / 16;
   constexpr int LDT = D + P::PAD;
   __shared__ __align__(16) T sX[TM * LDT];
   __shared__ __align__(16) T sG[TM * LDT];
@@ -47,15 +50,15 @@ __global__ void __launch_bounds__(NT) k_decoder_bwd(int64_t N, const float* __re
   float w2c[4];
 #pragma unroll
   for (int o = 0; o < 4; ++o) w2c[o] = w.W2f[o * D + n];
-  f32x4 dW1[8];
+  f32x4 dW1[NCB];
 #pragma unroll
-  for (int cb = 0; cb < 8; ++cb) dW1[cb] = zero4();
+  for (int cb = 0; cb < NCB; ++cb) dW1[cb] = zero4();
   float db1 = 0.f, dW2[4] = {0.f, 0.f, 0.f, 0.f}, db2 = 0.f;
   const int64_t ntiles = (N + TM - 1) / TM;
   for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
     const int64_t r0 = t * TM;
     const int nr = (int)min((int64_t)TM, N - r0);
-    stage_rows(sX, LDT, h + (size_t)r0 * D, nr, tid);
+    stage_rows<D>(sX, LDT, h + (size_t)r0 * D, nr, tid);
     if (tid < TM * 4) {
       const int row = tid >> 2, o = tid & 3;
       sO[row][o] = row < nr ? gout[(r0 + row) * 4 + o] : 0.f;
@@ -86,7 +89,7 @@ __global__ void __launch_bounds__(NT) k_decoder_bwd(int64_t N, const float* __re
         g[rb][r] = zb;
         sG[row * LDT + n] = P::cvt(zb);
       }
-    gtx<PREC, 8>(dW1, g, sX, LDT, 0, i, q);
+    gtx<PREC, NCB>(dW1, g, sX, LDT, 0, i, q);
     __syncthreads();
 #pragma unroll
     for (int rb = 0; rb < NRB; ++rb) acc[rb] = zero4();
@@ -101,44 +104,48 @@ __global__ void __launch_bounds__(NT) k_decoder_bwd(int64_t N, const float* __re
     __syncthreads();
   }
   float* base = part.buf + (size_t)blockIdx.x * part.stride;
-  put_w<8>(base, D, dW1, w8, i, q);
-  put_col(base + 16384 + n, db1, q);
+  // decoder parameter order: W1 [D][D], b1, W2 [4][D], b2
+  put_w<NCB>(base, D, dW1, w8, i, q);
+  put_col(base + D * D + n, db1, q);
 #pragma unroll
-  for (int o = 0; o < 4; ++o) put_col(base + 16512 + o * D + n, dW2[o], q);
-  if (tid < 4) base[17024 + tid] = db2;
+  for (int o = 0; o < 4; ++o) put_col(base + D * D + D + o * D + n, dW2[o], q);
+  if (tid < 4) base[D * D + 5 * D + tid] = db2;
 }
 
 // --------------------------------------------------------- node phase
 // Given hbar_in = dL/dh_out for h_out = h + LN(MLP([h, agg])):
 // hbar_part = hbar_in + dL/dh through the MLP, aggbar = dL/dagg.
-template <int PREC>
-__global__ void __launch_bounds__(NT) k_node_bwd(int64_t N, const float* __restrict__ h, const float* __restrict__ agg,
+template <int PREC, int LD>
+__global__ void __launch_bounds__(LD * 4) k_node_bwd(int64_t N, const float* __restrict__ h, const float* __restrict__ agg,
                                                  const float* __restrict__ hbar_in, MlpW w, float eps,
                                                  float* __restrict__ hbar_part, float* __restrict__ aggbar,
                                                  Partials part) {
   typedef Tr<PREC> P;
   typedef typename P::T T;
+  constexpr int D = LD;
+  [[maybe_unused]] constexpr int NW = Width<LD>::NW, NT = Width<LD>::NT;
+  constexpr int NCB = D / 16;
   constexpr int LDT = D + P::PAD;
   constexpr int LDX = 2 * D + P::PAD;
   __shared__ __align__(16) T sX[TM * LDX];
   __shared__ __align__(16) T sA[TM * LDT];
   __shared__ __align__(16) T sG[TM * LDT];
-  __shared__ LnScratch ln;
+  __shared__ LnScratch<NW> ln;
   const int tid = threadIdx.x, w8 = tid >> 6, lane = tid & 63, i = lane & 15, q = lane >> 4;
   const int n = w8 * 16 + i;
   const float b1 = w.b1[n], b2 = w.b2[n], gam = w.gamma[n];
-  f32x4 dW1[16], dW2[8];
+  f32x4 dW1[2 * NCB], dW2[NCB];
 #pragma unroll
-  for (int cb = 0; cb < 16; ++cb) dW1[cb] = zero4();
+  for (int cb = 0; cb < 2 * NCB; ++cb) dW1[cb] = zero4();
 #pragma unroll
-  for (int cb = 0; cb < 8; ++cb) dW2[cb] = zero4();
+  for (int cb = 0; cb < NCB; ++cb) dW2[cb] = zero4();
   float db1 = 0.f, db2 = 0.f, dg = 0.f, dbt = 0.f;
   const int64_t ntiles = (N + TM - 1) / TM;
   for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
     const int64_t r0 = t * TM;
     const int nr = (int)min((int64_t)TM, N - r0);
-    stage_rows(sX, LDX, h + (size_t)r0 * D, nr, tid);
-    stage_rows(sX + D, LDX, agg + (size_t)r0 * D, nr, tid);
+    stage_rows<D>(sX, LDX, h + (size_t)r0 * D, nr, tid);
+    stage_rows<D>(sX + D, LDX, agg + (size_t)r0 * D, nr, tid);
     __syncthreads();
     f32x4 acc[NRB];
 #pragma unroll
@@ -177,7 +184,7 @@ __global__ void __launch_bounds__(NT) k_node_bwd(int64_t N, const float* __restr
         db2 += g[rb][r];
         sG[(rb * 16 + q * 4 + r) * LDT + n] = P::cvt(g[rb][r]);
       }
-    gtx<PREC, 8>(dW2, g, sA, LDT, 0, i, q);
+    gtx<PREC, NCB>(dW2, g, sA, LDT, 0, i, q);
     __syncthreads();
 #pragma unroll
     for (int rb = 0; rb < NRB; ++rb) acc[rb] = zero4();
@@ -189,7 +196,7 @@ __global__ void __launch_bounds__(NT) k_node_bwd(int64_t N, const float* __restr
         g[rb][r] = (mask >> (rb * 4 + r)) & 1u ? acc[rb][r] : 0.f;
         db1 += g[rb][r];
       }
-    gtx<PREC, 16>(dW1, g, sX, LDX, 0, i, q);
+    gtx<PREC, 2 * NCB>(dW1, g, sX, LDX, 0, i, q);
     __syncthreads();
 #pragma unroll
     for (int rb = 0; rb < NRB; ++rb)
@@ -214,12 +221,13 @@ __global__ void __launch_bounds__(NT) k_node_bwd(int64_t N, const float* __restr
     __syncthreads();
   }
   float* base = part.buf + (size_t)blockIdx.x * part.stride;
-  put_w<16>(base, 2 * D, dW1, w8, i, q);
-  put_col(base + 32768 + n, db1, q);
-  put_w<8>(base + 32896, D, dW2, w8, i, q);
-  put_col(base + 49280 + n, db2, q);
-  put_col(base + 49408 + n, dg, q);
-  put_col(base + 49536 + n, dbt, q);
+  // node-MLP parameter order: W1 [D][2D], b1, W2 [D][D], b2, gamma, beta
+  put_w<2 * NCB>(base, 2 * D, dW1, w8, i, q);
+  put_col(base + 2 * D * D + n, db1, q);
+  put_w<NCB>(base + 2 * D * D + D, D, dW2, w8, i, q);
+  put_col(base + 3 * D * D + D + n, db2, q);
+  put_col(base + 3 * D * D + 2 * D + n, dg, q);
+  put_col(base + 3 * D * D + 3 * D + n, dbt, q);
 }
 
 // 8 consecutive elements of a row as one (bf16) or two (fp32) 16-byte loads.
@@ -261,8 +269,8 @@ struct RowChunk<float> {
 // S[v] = sum over in-edges e of v of zbar[rev[e]] (= sum over out-edges of v),
 // then hbar_out = hbar_part + W1s^T S + W1r^T R and the weight gradients of
 // the sender / receiver parts of the edge MLP's first layer.
-template <int PREC>
-__global__ void __launch_bounds__(NT) k_node_srcsum(int64_t N, const int32_t* __restrict__ rowptr,
+template <int PREC, int LD>
+__global__ void __launch_bounds__(LD * 4) k_node_srcsum(int64_t N, const int32_t* __restrict__ rowptr,
                                                     const int32_t* __restrict__ rev,
                                                     const typename Tr<PREC>::T* __restrict__ zbar,
                                                     const float* __restrict__ R, const float* __restrict__ h,
@@ -270,23 +278,26 @@ __global__ void __launch_bounds__(NT) k_node_srcsum(int64_t N, const int32_t* __
                                                     float* __restrict__ hbar_out, Partials part) {
   typedef Tr<PREC> P;
   typedef typename P::T T;
+  constexpr int D = LD;
+  [[maybe_unused]] constexpr int NW = Width<LD>::NW, NT = Width<LD>::NT;
+  constexpr int NCB = D / 16;
   constexpr int LDT = D + P::PAD;
   constexpr int LDX = 2 * D + P::PAD;
   __shared__ __align__(16) T sSR[TM * LDX];
   __shared__ __align__(16) T sH[TM * LDT];
   const int tid = threadIdx.x, w8 = tid >> 6, lane = tid & 63, i = lane & 15, q = lane >> 4;
   const int n = w8 * 16 + i;
-  f32x4 dWs[8], dWr[8];
+  f32x4 dWs[NCB], dWr[NCB];
 #pragma unroll
-  for (int cb = 0; cb < 8; ++cb) dWs[cb] = dWr[cb] = zero4();
+  for (int cb = 0; cb < NCB; ++cb) dWs[cb] = dWr[cb] = zero4();
   const int64_t ntiles = (N + TM - 1) / TM;
   for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
     const int64_t r0 = t * TM;
     const int nr = (int)min((int64_t)TM, N - r0);
     {
-      // 16 lanes per node, 8 features per lane; the node's reversed in-edges
+      // D/8 lanes per node, 8 features per lane; the node's reversed in-edges
       // are gathered 8 at a time (independent loads) and added in edge order
-      const int j = tid >> 4, c8 = (tid & 15) * 8;
+      const int j = tid / (D / 8), c8 = (tid % (D / 8)) * 8;
       float acc8[8];
 #pragma unroll
       for (int u = 0; u < 8; ++u) acc8[u] = 0.f;
@@ -313,8 +324,8 @@ __global__ void __launch_bounds__(NT) k_node_srcsum(int64_t N, const int32_t* __
       for (int u = 0; u < (int)(8 * sizeof(T)) / 16; ++u)
         reinterpret_cast<uint4*>(sSR + j * LDX + c8)[u] = reinterpret_cast<const uint4*>(o)[u];
     }
-    stage_rows(sSR + D, LDX, R + (size_t)r0 * D, nr, tid);
-    stage_rows(sH, LDT, h + (size_t)r0 * D, nr, tid);
+    stage_rows<D>(sSR + D, LDX, R + (size_t)r0 * D, nr, tid);
+    stage_rows<D>(sH, LDT, h + (size_t)r0 * D, nr, tid);
     __syncthreads();
     f32x4 acc[NRB];
 #pragma unroll
@@ -338,42 +349,45 @@ __global__ void __launch_bounds__(NT) k_node_srcsum(int64_t N, const int32_t* __
     for (int rb = 0; rb < NRB; ++rb)
 #pragma unroll
       for (int r = 0; r < 4; ++r) g[rb][r] = tof(sSR[(rb * 16 + q * 4 + r) * LDX + n]);
-    gtx<PREC, 8>(dWs, g, sH, LDT, 0, i, q);
+    gtx<PREC, NCB>(dWs, g, sH, LDT, 0, i, q);
 #pragma unroll
     for (int rb = 0; rb < NRB; ++rb)
 #pragma unroll
       for (int r = 0; r < 4; ++r) g[rb][r] = tof(sSR[(rb * 16 + q * 4 + r) * LDX + D + n]);
-    gtx<PREC, 8>(dWr, g, sH, LDT, 0, i, q);
+    gtx<PREC, NCB>(dWr, g, sH, LDT, 0, i, q);
     __syncthreads();
   }
   float* base = part.buf + (size_t)blockIdx.x * part.stride;
-  put_w<8>(base, D, dWs, w8, i, q);
-  put_w<8>(base + 16384, D, dWr, w8, i, q);
+  put_w<NCB>(base, D, dWs, w8, i, q);
+  put_w<NCB>(base + D * D, D, dWr, w8, i, q);
 }
 
 // ------------------------------------------------------- encoders
-template <int PREC, int KIN>
-__global__ void __launch_bounds__(NT) k_enc_bwd(int64_t M, const float* __restrict__ x_in,
+template <int PREC, int LD, int KIN>
+__global__ void __launch_bounds__(LD * 4) k_enc_bwd(int64_t M, const float* __restrict__ x_in,
                                                 const float* __restrict__ ybar, MlpW w, float eps,
                                                 float* __restrict__ gin, Partials part) {
   typedef Tr<PREC> P;
   typedef typename P::T T;
+  constexpr int D = LD;
+  [[maybe_unused]] constexpr int NW = Width<LD>::NW, NT = Width<LD>::NT;
+  constexpr int NCB = D / 16;
   constexpr int LDT = D + P::PAD;
   constexpr int LDM = D + 4;
   __shared__ float sX[TM][KIN];
   __shared__ __align__(16) T sA[TM * LDT];
   __shared__ __align__(16) T sG[TM * LDT];
   __shared__ float sZ[KIN == 8 ? TM * LDM : 1];
-  __shared__ LnScratch ln;
+  __shared__ LnScratch<NW> ln;
   const int tid = threadIdx.x, w8 = tid >> 6, lane = tid & 63, i = lane & 15, q = lane >> 4;
   const int n = w8 * 16 + i;
   const float b1 = w.b1[n], b2 = w.b2[n], gam = w.gamma[n];
   float w1[KIN];
 #pragma unroll
   for (int k = 0; k < KIN; ++k) w1[k] = w.W1f[n * KIN + k];
-  f32x4 dW2[8];
+  f32x4 dW2[NCB];
 #pragma unroll
-  for (int cb = 0; cb < 8; ++cb) dW2[cb] = zero4();
+  for (int cb = 0; cb < NCB; ++cb) dW2[cb] = zero4();
   float dW1[KIN];
 #pragma unroll
   for (int k = 0; k < KIN; ++k) dW1[k] = 0.f;
@@ -425,7 +439,7 @@ __global__ void __launch_bounds__(NT) k_enc_bwd(int64_t M, const float* __restri
         db2 += g[rb][r];
         sG[(rb * 16 + q * 4 + r) * LDT + n] = P::cvt(g[rb][r]);
       }
-    gtx<PREC, 8>(dW2, g, sA, LDT, 0, i, q);
+    gtx<PREC, NCB>(dW2, g, sA, LDT, 0, i, q);
     __syncthreads();
 #pragma unroll
     for (int rb = 0; rb < NRB; ++rb) acc[rb] = zero4();
@@ -457,7 +471,7 @@ __global__ void __launch_bounds__(NT) k_enc_bwd(int64_t M, const float* __restri
   for (int k = 0; k < KIN; ++k) put_col(base + n * KIN + k, dW1[k], q);
   const int o1 = D * KIN;
   put_col(base + o1 + n, db1, q);
-  put_w<8>(base + o1 + D, D, dW2, w8, i, q);
+  put_w<NCB>(base + o1 + D, D, dW2, w8, i, q);
   put_col(base + o1 + D + D * D + n, db2, q);
   put_col(base + o1 + 2 * D + D * D + n, dg, q);
   put_col(base + o1 + 3 * D + D * D + n, dbt, q);
@@ -510,71 +524,90 @@ static int bwd_grid(int64_t n_tiles, const Partials& p) {
   return grid_for(n_tiles, std::min(kBwdBlocks, p.max_blocks));
 }
 
-hipError_t launch_decoder_bwd(int prec, int64_t N, const float* h, const float* gout, const MlpW& w, float* hbar,
-                              const Partials& part, int* nblocks, hipStream_t s) {
+hipError_t launch_decoder_bwd(int prec, int lat, int64_t N, const float* h, const float* gout, const MlpW& w,
+                              float* hbar, const Partials& part, int* nblocks, hipStream_t s) {
   const int g = bwd_grid((N + TM - 1) / TM, part);
   *nblocks = g;
   if (!g) return hipSuccess;
-  if (prec == MGN_BF16)
-    hipLaunchKernelGGL(k_decoder_bwd<MGN_BF16>, dim3(g), dim3(NT), 0, s, N, h, gout, w, hbar, part);
-  else
-    hipLaunchKernelGGL(k_decoder_bwd<MGN_FP32>, dim3(g), dim3(NT), 0, s, N, h, gout, w, hbar, part);
+  if (prec == MGN_BF16) {
+    hipLaunchKernelGGL((k_decoder_bwd<MGN_BF16, 128>), dim3(g), dim3(NT), 0, s, N, h, gout, w, hbar, part);
+  } else {
+#define F(LD) hipLaunchKernelGGL((k_decoder_bwd<MGN_FP32, LD>), dim3(g), dim3(LD * 4), 0, s, N, h, gout, w, hbar, part)
+    MGN_BY_WIDTH(lat, F);
+#undef F
+  }
   return hipGetLastError();
 }
 
-hipError_t launch_node_bwd(int prec, int64_t N, const float* h, const float* agg, const float* hbar_in,
+hipError_t launch_node_bwd(int prec, int lat, int64_t N, const float* h, const float* agg, const float* hbar_in,
                            const MlpW& w, float eps, float* hbar_part, float* aggbar, const Partials& part,
                            int* nblocks, hipStream_t s) {
   const int g = bwd_grid((N + TM - 1) / TM, part);
   *nblocks = g;
   if (!g) return hipSuccess;
-  if (prec == MGN_BF16)
-    hipLaunchKernelGGL(k_node_bwd<MGN_BF16>, dim3(g), dim3(NT), 0, s, N, h, agg, hbar_in, w, eps, hbar_part, aggbar,
-                       part);
-  else
-    hipLaunchKernelGGL(k_node_bwd<MGN_FP32>, dim3(g), dim3(NT), 0, s, N, h, agg, hbar_in, w, eps, hbar_part, aggbar,
-                       part);
+  if (prec == MGN_BF16) {
+    hipLaunchKernelGGL((k_node_bwd<MGN_BF16, 128>), dim3(g), dim3(NT), 0, s, N, h, agg, hbar_in, w, eps, hbar_part,
+                       aggbar, part);
+  } else {
+#define F(LD)                                                                                                         \
+  hipLaunchKernelGGL((k_node_bwd<MGN_FP32, LD>), dim3(g), dim3(LD * 4), 0, s, N, h, agg, hbar_in, w, eps, hbar_part, \
+                     aggbar, part)
+    MGN_BY_WIDTH(lat, F);
+#undef F
+  }
   return hipGetLastError();
 }
 
-hipError_t launch_node_srcsum(int prec, int64_t N, const int32_t* rowptr, const int32_t* rev, const void* zbar,
-                              const float* R, const float* h, const float* hbar_part, const MlpW& w,
+hipError_t launch_node_srcsum(int prec, int lat, int64_t N, const int32_t* rowptr, const int32_t* rev,
+                              const void* zbar, const float* R, const float* h, const float* hbar_part, const MlpW& w,
                               float* hbar_out, const Partials& part, int* nblocks, hipStream_t s) {
   const int g = bwd_grid((N + TM - 1) / TM, part);
   *nblocks = g;
   if (!g) return hipSuccess;
-  if (prec == MGN_BF16)
-    hipLaunchKernelGGL(k_node_srcsum<MGN_BF16>, dim3(g), dim3(NT), 0, s, N, rowptr, rev, (const bf16*)zbar, R, h,
-                       hbar_part, w, hbar_out, part);
-  else
-    hipLaunchKernelGGL(k_node_srcsum<MGN_FP32>, dim3(g), dim3(NT), 0, s, N, rowptr, rev, (const float*)zbar, R, h,
-                       hbar_part, w, hbar_out, part);
+  if (prec == MGN_BF16) {
+    hipLaunchKernelGGL((k_node_srcsum<MGN_BF16, 128>), dim3(g), dim3(NT), 0, s, N, rowptr, rev, (const bf16*)zbar, R,
+                       h, hbar_part, w, hbar_out, part);
+  } else {
+#define F(LD)                                                                                                       \
+  hipLaunchKernelGGL((k_node_srcsum<MGN_FP32, LD>), dim3(g), dim3(LD * 4), 0, s, N, rowptr, rev, (const float*)zbar, \
+                     R, h, hbar_part, w, hbar_out, part)
+    MGN_BY_WIDTH(lat, F);
+#undef F
+  }
   return hipGetLastError();
 }
 
-hipError_t launch_edge_enc_bwd(int prec, int64_t E, const float* efeat, const float* ebar, const MlpW& w,
+hipError_t launch_edge_enc_bwd(int prec, int lat, int64_t E, const float* efeat, const float* ebar, const MlpW& w,
                                float eps, const Partials& part, int* nblocks, hipStream_t s) {
   const int g = bwd_grid((E + TM - 1) / TM, part);
   *nblocks = g;
   if (!g) return hipSuccess;
-  if (prec == MGN_BF16)
-    hipLaunchKernelGGL((k_enc_bwd<MGN_BF16, 4>), dim3(g), dim3(NT), 0, s, E, efeat, ebar, w, eps, (float*)nullptr,
-                       part);
-  else
-    hipLaunchKernelGGL((k_enc_bwd<MGN_FP32, 4>), dim3(g), dim3(NT), 0, s, E, efeat, ebar, w, eps, (float*)nullptr,
-                       part);
+  if (prec == MGN_BF16) {
+    hipLaunchKernelGGL((k_enc_bwd<MGN_BF16, 128, 4>), dim3(g), dim3(NT), 0, s, E, efeat, ebar, w, eps,
+                       (float*)nullptr, part);
+  } else {
+#define F(LD)                                                                                                      \
+  hipLaunchKernelGGL((k_enc_bwd<MGN_FP32, LD, 4>), dim3(g), dim3(LD * 4), 0, s, E, efeat, ebar, w, eps,            \
+                     (float*)nullptr, part)
+    MGN_BY_WIDTH(lat, F);
+#undef F
+  }
   return hipGetLastError();
 }
 
-hipError_t launch_node_enc_bwd(int prec, int64_t N, const float* node_in, const float* hbar, const MlpW& w,
+hipError_t launch_node_enc_bwd(int prec, int lat, int64_t N, const float* node_in, const float* hbar, const MlpW& w,
                                float eps, float* gin, const Partials& part, int* nblocks, hipStream_t s) {
   const int g = bwd_grid((N + TM - 1) / TM, part);
   *nblocks = g;
   if (!g) return hipSuccess;
-  if (prec == MGN_BF16)
-    hipLaunchKernelGGL((k_enc_bwd<MGN_BF16, 8>), dim3(g), dim3(NT), 0, s, N, node_in, hbar, w, eps, gin, part);
-  else
-    hipLaunchKernelGGL((k_enc_bwd<MGN_FP32, 8>), dim3(g), dim3(NT), 0, s, N, node_in, hbar, w, eps, gin, part);
+  if (prec == MGN_BF16) {
+    hipLaunchKernelGGL((k_enc_bwd<MGN_BF16, 128, 8>), dim3(g), dim3(NT), 0, s, N, node_in, hbar, w, eps, gin, part);
+  } else {
+#define F(LD) \
+  hipLaunchKernelGGL((k_enc_bwd<MGN_FP32, LD, 8>), dim3(g), dim3(LD * 4), 0, s, N, node_in, hbar, w, eps, gin, part)
+    MGN_BY_WIDTH(lat, F);
+#undef F
+  }
   return hipGetLastError();
 }
 

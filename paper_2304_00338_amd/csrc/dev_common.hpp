@@ -1,9 +1,10 @@
 // Device helpers shared by the gfx950 kernels: MFMA operand traits, tile
 // staging, row LayerNorm statistics and deterministic in-wave reductions.
 //
-// Every kernel works on tiles of TM = 32 rows (edges or nodes) with 512
-// threads = 8 wave64s.  Wave w owns output columns [16w, 16w+16) of every
-// 128-wide layer.  MFMA 16x16xK operand layout (lane l, i = l & 15,
+// Every kernel works on tiles of TM = 32 rows (edges or nodes) with one
+// wave64 per 16 latent columns: 8 waves (512 threads) for the latent width
+// 128, 10 waves (640 threads) for the latent width 150 padded to 160.  Wave
+// w owns output columns [16w, 16w+16) of every latent-wide layer.  MFMA 16x16xK operand layout (lane l, i = l & 15,
 // q = l >> 4):
 //   A fragment: A[i][k0 + q*KQ + j]   (KQ = 1 for fp32, 8 for bf16)
 //   B fragment: B[k0 + q*KQ + j][i]
@@ -23,6 +24,28 @@ constexpr int NT = 512;    // threads per block
 constexpr int NW = 8;      // waves per block
 constexpr int TM = 32;     // rows per tile
 constexpr int NRB = TM / 16;
+
+// Real latent width of a kernel width LD: the 3D model's latent 150 runs
+// padded to 160 columns.  Padded weight rows and columns, biases, gains and
+// offsets are zero, so padded feature columns stay exactly zero; only the
+// LayerNorm statistics need the real width (and a mask on the padding).
+template <int LD>
+struct Width {
+  static constexpr int DR = LD == 160 ? 150 : LD;
+  static constexpr int NW = LD / 16;
+  static constexpr int NT = NW * 64;
+  static_assert(LD == 128 || LD == 160, "supported kernel widths: 128, 160");
+};
+
+// Host-side dispatch on the kernel width lat (128, or 160 for the latent
+// 150): F(LD) expands to the launch of the width-LD instantiation.
+#define MGN_BY_WIDTH(lat, F) \
+  do {                       \
+    if ((lat) == 160)        \
+      F(160);                \
+    else                     \
+      F(128);                \
+  } while (0)
 
 typedef __bf16 bf16;
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -95,13 +118,9 @@ __device__ __forceinline__ void gemm_tile(f32x4 (&acc)[NRB], const typename Tr<P
 // where G arrives in C layout (g[rb][r] = G[rb*16 + q*4 + r][o = 16w + i]).
 // The MFMA's K dimension runs over tile rows; the row order inside K is a
 // fixed permutation applied to both operands.
-template <int PREC, int NCB>
-__device__ __forceinline__ void gtx(f32x4 (&acc)[NCB], const f32x4 (&g)[NRB],
-                                    const typename Tr<PREC>::T* X, int ldx, int xcol0, int i, int q);
-
-template <>
-__device__ __forceinline__ void gtx<MGN_FP32, 8>(f32x4 (&acc)[8], const f32x4 (&g)[NRB], const float* X,
-                                                 int ldx, int xcol0, int i, int q) {
+template <int NCB>
+__device__ __forceinline__ void gtx_f32(f32x4 (&acc)[NCB], const f32x4 (&g)[NRB], const float* X, int ldx, int xcol0,
+                                        int i, int q) {
 #pragma unroll
   for (int rb = 0; rb < NRB; ++rb)
 #pragma unroll
@@ -109,21 +128,7 @@ __device__ __forceinline__ void gtx<MGN_FP32, 8>(f32x4 (&acc)[8], const f32x4 (&
       const float a = g[rb][r];
       const float* xr = X + (rb * 16 + q * 4 + r) * ldx + xcol0 + i;
 #pragma unroll
-      for (int cb = 0; cb < 8; ++cb) acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, xr[cb * 16], acc[cb], 0, 0, 0);
-    }
-}
-
-template <>
-__device__ __forceinline__ void gtx<MGN_FP32, 16>(f32x4 (&acc)[16], const f32x4 (&g)[NRB], const float* X,
-                                                  int ldx, int xcol0, int i, int q) {
-#pragma unroll
-  for (int rb = 0; rb < NRB; ++rb)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const float a = g[rb][r];
-      const float* xr = X + (rb * 16 + q * 4 + r) * ldx + xcol0 + i;
-#pragma unroll
-      for (int cb = 0; cb < 16; ++cb)
+      for (int cb = 0; cb < NCB; ++cb)
         acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, xr[cb * 16], acc[cb], 0, 0, 0);
     }
 }
@@ -154,15 +159,13 @@ __device__ __forceinline__ void gtx_bf16(f32x4 (&acc)[NCB], const f32x4 (&g)[NRB
   }
 }
 
-template <>
-__device__ __forceinline__ void gtx<MGN_BF16, 8>(f32x4 (&acc)[8], const f32x4 (&g)[NRB], const bf16* X,
-                                                 int ldx, int xcol0, int i, int q) {
-  gtx_bf16<8>(acc, g, X, ldx, xcol0, i, q);
-}
-template <>
-__device__ __forceinline__ void gtx<MGN_BF16, 16>(f32x4 (&acc)[16], const f32x4 (&g)[NRB], const bf16* X,
-                                                  int ldx, int xcol0, int i, int q) {
-  gtx_bf16<16>(acc, g, X, ldx, xcol0, i, q);
+template <int PREC, int NCB>
+__device__ __forceinline__ void gtx(f32x4 (&acc)[NCB], const f32x4 (&g)[NRB], const typename Tr<PREC>::T* X, int ldx,
+                                    int xcol0, int i, int q) {
+  if constexpr (PREC == MGN_BF16)
+    gtx_bf16<NCB>(acc, g, X, ldx, xcol0, i, q);
+  else
+    gtx_f32<NCB>(acc, g, X, ldx, xcol0, i, q);
 }
 
 // Sum over the 16 lanes that share q (one DPP row = one row of a 16-column
@@ -208,14 +211,15 @@ __device__ __forceinline__ float sum_q(float s) {
   return s;
 }
 
-// LDS scratch of the row LayerNorm helpers.  red/red2/red2x hold one partial
-// per (row, wave); fin holds, per wave, the 32 row totals that wave formed
-// itself (so reading them back needs no block barrier).
-struct LnScratch {
-  float red[TM][NW];
-  float red2[TM][NW];
-  float red2x[TM][NW][2];
-  float fin[NW][2 * TM];
+// LDS scratch of the row LayerNorm helpers for NWV waves.  red/red2/red2x
+// hold one partial per (row, wave); fin holds, per wave, the 32 row totals
+// that wave formed itself (so reading them back needs no block barrier).
+template <int NWV>
+struct alignas(16) LnScratch {
+  float red[TM][NWV];
+  float red2[TM][NWV];
+  float red2x[TM][NWV][2];
+  float fin[NWV][2 * TM];
 };
 
 // Orders this wave's LDS writes before its later LDS reads of other lanes'
@@ -226,19 +230,30 @@ __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// Sum of the 8 per-wave partials of one row in wave order.
+// Sum of the NWV per-wave partials of one row in wave order.
+template <int NWV>
 __device__ __forceinline__ float row_total(const float* p) {
-  const f32x4 a = *reinterpret_cast<const f32x4*>(p), b = *reinterpret_cast<const f32x4*>(p + 4);
-  return ((((((a[0] + a[1]) + a[2]) + a[3]) + b[0]) + b[1]) + b[2]) + b[3];
+  if constexpr (NWV == 8) {
+    const f32x4 a = *reinterpret_cast<const f32x4*>(p), b = *reinterpret_cast<const f32x4*>(p + 4);
+    return ((((((a[0] + a[1]) + a[2]) + a[3]) + b[0]) + b[1]) + b[2]) + b[3];
+  } else {
+    float t = p[0];
+#pragma unroll
+    for (int u = 1; u < NWV; ++u) t += p[u];
+    return t;
+  }
 }
 
-// Per-row mean and 1/sqrt(var + eps) over the 128 columns held by the 8
-// waves (biased variance, two passes).  Each wave reduces its 16 columns
-// with DPP, the 8 wave partials of a row are summed once per wave by lane
-// row (lanes 0..31) and handed back through the wave's own LDS slot.
-// Contains two block barriers; every thread of the block must call it.
-__device__ __forceinline__ void ln_stats(const f32x4 (&v)[NRB], LnScratch& S, float eps, int w, int i, int q,
+// Per-row mean and 1/sqrt(var + eps) over the real latent columns held by
+// the NWV waves (biased variance, two passes; padded columns are left out).
+// Each wave reduces its 16 columns with DPP, the wave partials of a row are
+// summed once per wave by lane row (lanes 0..31) and handed back through the
+// wave's own LDS slot.  Contains two block barriers; every thread of the
+// block must call it.
+template <int NWV>
+__device__ __forceinline__ void ln_stats(const f32x4 (&v)[NRB], LnScratch<NWV>& S, float eps, int w, int i, int q,
                                          f32x4 (&mean)[NRB], f32x4 (&rstd)[NRB]) {
+  constexpr int LD = NWV * 16, DR = Width<LD>::DR;
   const int lane = threadIdx.x & 63;
   float* fin = S.fin[w];
   {
@@ -253,15 +268,16 @@ __device__ __forceinline__ void ln_stats(const f32x4 (&v)[NRB], LnScratch& S, fl
         for (int r = 0; r < 4; ++r) S.red[rb * 16 + q * 4 + r][w] = s[rb][r];
   }
   __syncthreads();
-  if (lane < TM) fin[lane] = row_total(S.red[lane]) * (1.0f / D);
+  if (lane < TM) fin[lane] = row_total<NWV>(S.red[lane]) * (1.0f / DR);
   wave_lds_sync();
   {
+    const bool live = DR == LD || w * 16 + i < DR;
     f32x4 s[NRB];
 #pragma unroll
     for (int rb = 0; rb < NRB; ++rb) {
       mean[rb] = *reinterpret_cast<const f32x4*>(fin + rb * 16 + q * 4);
       const f32x4 d = v[rb] - mean[rb];
-      s[rb] = d * d;
+      s[rb] = live ? d * d : zero4();
     }
     sum16x(s);
     if (i == 0)
@@ -271,7 +287,7 @@ __device__ __forceinline__ void ln_stats(const f32x4 (&v)[NRB], LnScratch& S, fl
         for (int r = 0; r < 4; ++r) S.red2[rb * 16 + q * 4 + r][w] = s[rb][r];
   }
   __syncthreads();
-  if (lane < TM) fin[TM + lane] = __builtin_amdgcn_rsqf(row_total(S.red2[lane]) * (1.0f / D) + eps);
+  if (lane < TM) fin[TM + lane] = __builtin_amdgcn_rsqf(row_total<NWV>(S.red2[lane]) * (1.0f / DR) + eps);
   wave_lds_sync();
 #pragma unroll
   for (int rb = 0; rb < NRB; ++rb) rstd[rb] = *reinterpret_cast<const f32x4*>(fin + TM + rb * 16 + q * 4);
@@ -279,9 +295,12 @@ __device__ __forceinline__ void ln_stats(const f32x4 (&v)[NRB], LnScratch& S, fl
 
 // LayerNorm backward for one tile: given dy (C layout), xhat, rstd and this
 // lane's gain, returns dz = rstd * (dxh - mean(dxh) - xhat * mean(dxh*xhat))
-// with dxh = dy * gamma.  One block barrier.
+// with dxh = dy * gamma, the means over the real columns (a padded column's
+// gain is zero) and dz = 0 on padded columns.  One block barrier.
+template <int NWV>
 __device__ __forceinline__ void ln_bwd(f32x4 (&dz)[NRB], const f32x4 (&dy)[NRB], const f32x4 (&xhat)[NRB],
-                                       const f32x4 (&rstd)[NRB], float gam, LnScratch& S, int w, int i, int q) {
+                                       const f32x4 (&rstd)[NRB], float gam, LnScratch<NWV>& S, int w, int i, int q) {
+  constexpr int LD = NWV * 16, DR = Width<LD>::DR;
   const int lane = threadIdx.x & 63;
   float* fin = S.fin[w];
   {
@@ -307,17 +326,18 @@ __device__ __forceinline__ void ln_bwd(f32x4 (&dz)[NRB], const f32x4 (&dy)[NRB],
     const f32x4* p = reinterpret_cast<const f32x4*>(S.red2x[lane]);
     float t1 = 0.f, t2 = 0.f;
 #pragma unroll
-    for (int u = 0; u < NW / 2; ++u) {
+    for (int u = 0; u < NWV / 2; ++u) {
       const f32x4 x = p[u];
       t1 += x[0];
       t2 += x[1];
       t1 += x[2];
       t2 += x[3];
     }
-    fin[lane] = t1 * (1.0f / D);
-    fin[TM + lane] = t2 * (1.0f / D);
+    fin[lane] = t1 * (1.0f / DR);
+    fin[TM + lane] = t2 * (1.0f / DR);
   }
   wave_lds_sync();
+  const bool live = DR == LD || w * 16 + i < DR;
 #pragma unroll
   for (int rb = 0; rb < NRB; ++rb) {
     const f32x4 m1 = *reinterpret_cast<const f32x4*>(fin + rb * 16 + q * 4);
@@ -325,22 +345,23 @@ __device__ __forceinline__ void ln_bwd(f32x4 (&dz)[NRB], const f32x4 (&dy)[NRB],
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const float dxh = dy[rb][r] * gam;
-      dz[rb][r] = rstd[rb][r] * (dxh - m1[r] - xhat[rb][r] * m2[r]);
+      dz[rb][r] = live ? rstd[rb][r] * (dxh - m1[r] - xhat[rb][r] * m2[r]) : 0.f;
     }
   }
 }
 
-// Copy rows [0, nrows) of a row-major global [.][128] array (element type S)
+// Copy rows [0, nrows) of a row-major global [.][LD] array (element type S)
 // into an LDS tile of T with row stride ld, zero-filling rows nrows..TM-1.
 // Each thread moves 8 consecutive elements per step.
-template <typename T, typename S>
+template <int LD, typename T, typename S>
 __device__ __forceinline__ void stage_rows(T* lds, int ld, const S* src, int nrows, int tid) {
-  for (int idx = tid; idx < TM * (D / 8); idx += NT) {
-    const int row = idx >> 4, c = (idx & 15) * 8;
+  constexpr int CPR = LD / 8, NTH = Width<LD>::NT;
+  for (int idx = tid; idx < TM * CPR; idx += NTH) {
+    const int row = idx / CPR, c = (idx % CPR) * 8;
     T* dst = lds + row * ld + c;
     float v[8];
     if (row < nrows) {
-      const S* s = src + (size_t)row * D + c;
+      const S* s = src + (size_t)row * LD + c;
 #pragma unroll
       for (int j = 0; j < 8; ++j) v[j] = tof(s[j]);
     } else {

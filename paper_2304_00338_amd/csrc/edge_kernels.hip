@@ -20,15 +20,15 @@
 namespace mgn {
 namespace dev {
 
-// B fragments of one 16-column weight slice with K = 128:
+// B fragments of one 16-column weight slice with K = LD (the kernel width):
 // B[k][n] = W[n0 + n][kofs + k].
-template <int PREC, bool WREG>
+template <int PREC, bool WREG, int LD>
 struct WSlice;
 
-template <int PREC>
-struct WSlice<PREC, true> {
+template <int PREC, int LD>
+struct WSlice<PREC, true, LD> {
   typedef Tr<PREC> P;
-  static constexpr int NK = D / P::KS;
+  static constexpr int NK = LD / P::KS;
   typename P::Frag f[NK];
   __device__ __forceinline__ void init(const typename P::T* W, int ldw, int n0, int kofs, int i, int q) {
 #pragma unroll
@@ -37,10 +37,10 @@ struct WSlice<PREC, true> {
   __device__ __forceinline__ typename P::Frag get(int kk) const { return f[kk]; }
 };
 
-template <int PREC>
-struct WSlice<PREC, false> {
+template <int PREC, int LD>
+struct WSlice<PREC, false, LD> {
   typedef Tr<PREC> P;
-  static constexpr int NK = D / P::KS;
+  static constexpr int NK = LD / P::KS;
   const typename P::T* W;
   int ldw, n0, kofs, i, q;
   __device__ __forceinline__ void init(const typename P::T* W_, int ldw_, int n0_, int kofs_, int i_, int q_) {
@@ -54,13 +54,13 @@ struct WSlice<PREC, false> {
   __device__ __forceinline__ typename P::Frag get(int kk) const { return P::ldb(W, ldw, n0, kofs + kk * P::KS, i, q); }
 };
 
-// B fragments read from an LDS copy of a [128][128] matrix with padded rows
+// B fragments read from an LDS copy of a [LD][LD] matrix with padded rows
 // (row stride LDW elements), B[k][n] = W[n0 + n][k].
-template <int PREC>
+template <int PREC, int LD>
 struct WSliceL {
   typedef Tr<PREC> P;
-  static constexpr int NK = D / P::KS;
-  static constexpr int LDW = D + P::PAD;
+  static constexpr int NK = LD / P::KS;
+  static constexpr int LDW = LD + P::PAD;
   const typename P::T* W;
   int n0, i, q;
   __device__ __forceinline__ void init(const typename P::T* W_, int n0_, int i_, int q_) {
@@ -72,12 +72,13 @@ struct WSliceL {
   __device__ __forceinline__ typename P::Frag get(int kk) const { return P::ldb(W, LDW, n0, kk * P::KS, i, q); }
 };
 
-// Copy the first 128 rows of a row-major [.][128] global matrix into LDS with
-// padded rows (stride 128 + PAD elements).
-template <int PREC>
+// Copy the first LD rows of a row-major [.][LD] global matrix into LDS with
+// padded rows (stride LD + PAD elements).
+template <int PREC, int LD>
 __device__ __forceinline__ void stage_weights(typename Tr<PREC>::T* lds, const typename Tr<PREC>::T* __restrict__ W,
                                               int tid) {
   typedef typename Tr<PREC>::T T;
+  constexpr int D = LD, NT = Width<LD>::NT;
   constexpr int EPC = 16 / sizeof(T), LDW = D + Tr<PREC>::PAD;
   for (int idx = tid; idx < D * D / EPC; idx += NT) {
     const int row = (idx * EPC) / D, col = (idx * EPC) % D;
@@ -126,15 +127,17 @@ __device__ __forceinline__ void gtx_t(f32x4 (&acc)[NCB], const f32x4 (&g)[NRB], 
   }
 }
 
-// Row-chunk geometry: 16-byte chunks of rows of element type T.
-template <typename T>
+// Row-chunk geometry: 16-byte chunks of LD-wide rows of element type T,
+// split over the LD * 4 threads of a block.
+template <typename T, int LD>
 struct Rows {
+  static constexpr int NTH = Width<LD>::NT;
   static constexpr int EPC = 16 / sizeof(T);          // elements per chunk
-  static constexpr int CPR = D / EPC;                 // chunks per 128-wide row
-  static constexpr int CPT = TM * CPR / NT;           // chunks per thread per tile
-  static_assert(CPT >= 1 && TM * CPR == CPT * NT, "tile must split evenly");
-  __device__ __forceinline__ static int row(int tid, int k) { return (tid + k * NT) / CPR; }
-  __device__ __forceinline__ static int col(int tid, int k) { return ((tid + k * NT) % CPR) * EPC; }
+  static constexpr int CPR = LD / EPC;                // chunks per row
+  static constexpr int CPT = TM * CPR / NTH;          // chunks per thread per tile
+  static_assert(CPT >= 1 && TM * CPR == CPT * NTH, "tile must split evenly");
+  __device__ __forceinline__ static int row(int tid, int k) { return (tid + k * NTH) / CPR; }
+  __device__ __forceinline__ static int col(int tid, int k) { return ((tid + k * NTH) % CPR) * EPC; }
 };
 
 __device__ __forceinline__ void unpack(const uint4& u, float (&f)[4]) {
@@ -165,10 +168,11 @@ __device__ __forceinline__ int first_row(const int2* sr, int n, int v) {
 
 // Sum of in-tile rows per receiver (ascending in-segment order), or of all
 // rows into a slot for a chunk of a long segment.
-template <typename S>
+template <int LD, typename S>
 __device__ __forceinline__ void segment_sums(const S* rows, int ld, const int2* sr, int4 td, float* __restrict__ out,
                                              float* __restrict__ slots, int tid) {
-  const int c = tid & (D - 1), vg = tid >> 7;
+  constexpr int D = LD, NT = Width<LD>::NT;
+  const int c = tid % D, vg = tid / D;
   const int nb = td.x, ne_ = td.w - td.z;
   if (td.y >= 0) {
     const int nv = td.y - nb;
@@ -200,20 +204,24 @@ __device__ __forceinline__ int2 sr_of(const EdgeTiles& tl, int4 d, int row) {
 }
 
 // ===================================================================== forward
-template <int PREC>
+template <int PREC, int LD>
 struct FwdLoads {
-  typedef Rows<typename Tr<PREC>::T> RT;
+  typedef Rows<typename Tr<PREC>::T, LD> RT;
   uint4 e[RT::CPT], ps[RT::CPT], pr[RT::CPT];
 };
 
-template <int PREC, bool WREG>
-__global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2))) k_edge_fwd(EdgeTiles tl, const typename Tr<PREC>::T* __restrict__ e_in,
+template <int PREC, bool WREG, int LD>
+__global__ void __launch_bounds__(LD * 4) __attribute__((amdgpu_waves_per_eu(LD == 128 ? 2 : 3, LD == 128 ? 2 : 3)))
+k_edge_fwd(EdgeTiles tl, const typename Tr<PREC>::T* __restrict__ e_in,
                                                  typename Tr<PREC>::T* __restrict__ e_out, int write_e,
                                                  const typename Tr<PREC>::T* __restrict__ Pn, MlpW w, float eps,
                                                  float* __restrict__ agg, float* __restrict__ slots) {
   typedef Tr<PREC> P;
   typedef typename P::T T;
-  typedef Rows<T> RT;
+  typedef Rows<T, LD> RT;
+  constexpr int D = LD;
+  [[maybe_unused]] constexpr int NW = Width<LD>::NW, NT = Width<LD>::NT;
+  constexpr int NCB = D / 16;
   constexpr int LDT = D + P::PAD;
   constexpr int LDM = D + 4;
   constexpr int A1B = TM * LDT * (int)sizeof(T);
@@ -221,7 +229,7 @@ __global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
   __shared__ __align__(16) T sE[TM * LDT];
   __shared__ __align__(16) float sP[TM * LDM];
   __shared__ __align__(16) char sU[A1B > MB ? A1B : MB];  // a1 tile, then m tile
-  __shared__ LnScratch ln;
+  __shared__ LnScratch<NW> ln;
   __shared__ int2 sSR[2][TM];
   T* sA1 = reinterpret_cast<T*>(sU);
   float* sM = reinterpret_cast<float*>(sU);
@@ -229,7 +237,7 @@ __global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
   const int tid = threadIdx.x, w8 = tid >> 6, lane = tid & 63, i = lane & 15, q = lane >> 4;
   const int n = w8 * 16 + i;
   const float b1 = w.b1[n], b2 = w.b2[n], gam = w.gamma[n], bet = w.beta[n];
-  WSlice<PREC, WREG> w1, w2;
+  WSlice<PREC, WREG, LD> w1, w2;
   w1.init((const T*)w.W1, 3 * D, w8 * 16, 0, i, q);
   w2.init((const T*)w.W2, D, w8 * 16, 0, i, q);
 
@@ -245,7 +253,7 @@ __global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
   if (tid < TM) srn = sr_of(tl, d1, tid);
   __syncthreads();
 
-  FwdLoads<PREC> L;
+  FwdLoads<PREC, LD> L;
   auto issue = [&](int4 d, const int2* sr) {
     const int ne_ = d.w - d.z;
     const uint4 z = {0u, 0u, 0u, 0u};
@@ -324,7 +332,7 @@ __global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
         *reinterpret_cast<uint4*>(e_out + (size_t)(eb + row) * D + col) = o;
       }
     }
-    segment_sums(sM, LDM, sSR[buf], d0, agg, slots, tid);
+    segment_sums<LD>(sM, LDM, sSR[buf], d0, agg, slots, tid);
     __syncthreads();
     d0 = d1;
     d1 = d2;
@@ -334,9 +342,9 @@ __global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
 }
 
 // ===================================================================== reverse
-template <int PREC>
+template <int PREC, int LD>
 struct BwdLoads {
-  typedef Rows<typename Tr<PREC>::T> RT;
+  typedef Rows<typename Tr<PREC>::T, LD> RT;
   uint4 e[RT::CPT], ps[RT::CPT], pr[RT::CPT];
 };
 
@@ -349,15 +357,18 @@ struct BwdLoads {
 // tile's own gradient rows, which are issued before the next tile's prefetch
 // (vector-memory loads retire in issue order): the forward weights sit in
 // registers and, in bf16, the transposed ones in LDS.
-template <int PREC, bool WREG>
-__global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
+template <int PREC, bool WREG, int LD>
+__global__ void __launch_bounds__(LD * 4) __attribute__((amdgpu_waves_per_eu(LD == 128 ? 2 : 3, LD == 128 ? 2 : 3)))
 k_edge_bwd(EdgeTiles tl, const typename Tr<PREC>::T* __restrict__ e, const float* __restrict__ ebar_in,
            int have_ebar, float* __restrict__ ebar_out, const typename Tr<PREC>::T* __restrict__ Pn,
            const float* __restrict__ aggbar, MlpW w, float eps, typename Tr<PREC>::T* __restrict__ zbar,
            float* __restrict__ R, float* __restrict__ slots, Partials part) {
   typedef Tr<PREC> P;
   typedef typename P::T T;
-  typedef Rows<T> RT;
+  typedef Rows<T, LD> RT;
+  constexpr int D = LD;
+  [[maybe_unused]] constexpr int NW = Width<LD>::NW, NT = Width<LD>::NT;
+  constexpr int NCB = D / 16;
   constexpr bool TX = PREC == MGN_BF16;  // feature-major a1 copy, LDS weights
   constexpr int LDT = D + P::PAD;
   constexpr int LDM = D + 4;
@@ -370,28 +381,28 @@ k_edge_bwd(EdgeTiles tl, const typename Tr<PREC>::T* __restrict__ e, const float
   __shared__ __align__(16) bf16 sA1T[TX ? D * LDTT : 8];
   __shared__ __align__(16) T sW2t[TX ? D * LDT : 8];
   __shared__ __align__(16) T sW1t[TX ? D * LDT : 8];
-  __shared__ LnScratch ln;
+  __shared__ LnScratch<NW> ln;
   __shared__ int2 sSR[2][TM];
 
   const int tid = threadIdx.x, w8 = tid >> 6, lane = tid & 63, i = lane & 15, q = lane >> 4;
   const int n = w8 * 16 + i;
   const float b1 = w.b1[n], b2 = w.b2[n], gam = w.gamma[n];
-  WSlice<PREC, WREG> w1, w2;
+  WSlice<PREC, WREG, LD> w1, w2;
   w1.init((const T*)w.W1, 3 * D, w8 * 16, 0, i, q);
   w2.init((const T*)w.W2, D, w8 * 16, 0, i, q);
-  WSlice<PREC, false> g2t, g1t;
-  WSliceL<PREC> l2t, l1t;
+  WSlice<PREC, false, LD> g2t, g1t;
+  WSliceL<PREC, LD> l2t, l1t;
   g2t.init((const T*)w.W2t, D, w8 * 16, 0, i, q);
   g1t.init((const T*)w.W1t, D, w8 * 16, 0, i, q);
   l2t.init(sW2t, w8 * 16, i, q);
   l1t.init(sW1t, w8 * 16, i, q);
   if constexpr (TX) {
-    stage_weights<PREC>(sW2t, (const T*)w.W2t, tid);
-    stage_weights<PREC>(sW1t, (const T*)w.W1t, tid);
+    stage_weights<PREC, LD>(sW2t, (const T*)w.W2t, tid);
+    stage_weights<PREC, LD>(sW1t, (const T*)w.W1t, tid);
   }
-  f32x4 dW2[8];
+  f32x4 dW2[NCB];
 #pragma unroll
-  for (int cb = 0; cb < 8; ++cb) dW2[cb] = zero4();
+  for (int cb = 0; cb < NCB; ++cb) dW2[cb] = zero4();
   float db1 = 0.f, db2 = 0.f, dg = 0.f, dbt = 0.f;
 
   const int64_t G = gridDim.x, NTL = tl.n_tiles;
@@ -408,7 +419,7 @@ k_edge_bwd(EdgeTiles tl, const typename Tr<PREC>::T* __restrict__ e, const float
   // Prefetch of one tile's edge latents and node products: 32-bit element
   // offsets from uniform bases; rows past the tile's end are clamped to its
   // last row and zeroed afterwards.
-  BwdLoads<PREC> L;
+  BwdLoads<PREC, LD> L;
   auto issue = [&](int4 d, const int2* sr) {
     const int ne_ = d.w - d.z;
     const uint4 z = {0u, 0u, 0u, 0u};
@@ -519,9 +530,9 @@ k_edge_bwd(EdgeTiles tl, const typename Tr<PREC>::T* __restrict__ e, const float
         sG[(rb * 16 + q * 4 + r) * LDT + n] = P::cvt(g[rb][r]);
       }
     if constexpr (TX)
-      gtx_t<8>(dW2, g, sA1T, LDTT, i, q);
+      gtx_t<NCB>(dW2, g, sA1T, LDTT, i, q);
     else
-      gtx<PREC, 8>(dW2, g, sA1, LDT, 0, i, q);
+      gtx<PREC, NCB>(dW2, g, sA1, LDT, 0, i, q);
     __syncthreads();
     // ---- back through W2 and the ReLU
 #pragma unroll
@@ -559,27 +570,29 @@ k_edge_bwd(EdgeTiles tl, const typename Tr<PREC>::T* __restrict__ e, const float
       *reinterpret_cast<uint4*>(zbar + (size_t)(eb + row) * D + col) =
           *reinterpret_cast<const uint4*>(sZ + row * LDT + col);
     }
-    segment_sums(sZ, LDT, sSR[buf], d0, R, slots, tid);
+    segment_sums<LD>(sZ, LDT, sSR[buf], d0, R, slots, tid);
     __syncthreads();
     d0 = d1;
     d1 = d2;
     d2 = d3;
     buf ^= 1;
   }
+  // partial layout: the edge-MLP parameters after W1 (b1, W2, b2, gamma,
+  // beta) at offset D * D
   float* base = part.buf + (size_t)blockIdx.x * part.stride;
 #pragma unroll
-  for (int cb = 0; cb < 8; ++cb)
+  for (int cb = 0; cb < NCB; ++cb)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) base[16512 + (size_t)(w8 * 16 + q * 4 + r) * D + cb * 16 + i] = dW2[cb][r];
+    for (int r = 0; r < 4; ++r) base[D * D + D + (size_t)(w8 * 16 + q * 4 + r) * D + cb * 16 + i] = dW2[cb][r];
   db1 = sum_q(db1);
   db2 = sum_q(db2);
   dg = sum_q(dg);
   dbt = sum_q(dbt);
   if (q == 0) {
-    base[16384 + n] = db1;
-    base[32896 + n] = db2;
-    base[33024 + n] = dg;
-    base[33152 + n] = dbt;
+    base[D * D + n] = db1;
+    base[2 * D * D + D + n] = db2;
+    base[2 * D * D + 2 * D + n] = dg;
+    base[2 * D * D + 3 * D + n] = dbt;
   }
 }
 
@@ -590,20 +603,24 @@ k_edge_bwd(EdgeTiles tl, const typename Tr<PREC>::T* __restrict__ e, const float
 // are taken 32 at a time in order; both chunks are staged feature-major in
 // LDS so each MFMA operand fragment is one 16-byte (bf16) read, and the next
 // chunk is in flight in registers while the current one is multiplied.
-template <int PREC>
-__global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
+template <int PREC, int LD>
+__global__ void __launch_bounds__(LD * 4) __attribute__((amdgpu_waves_per_eu(LD == 128 ? 2 : 3, LD == 128 ? 2 : 3)))
 k_wgrad(int64_t M, const typename Tr<PREC>::T* __restrict__ Gm, const typename Tr<PREC>::T* __restrict__ Xm,
         Partials part) {
   typedef Tr<PREC> P;
   typedef typename P::T T;
-  typedef Rows<T> RT;
+  typedef Rows<T, LD> RT;
+  constexpr int D = LD;
+  [[maybe_unused]] constexpr int NW = Width<LD>::NW, NT = Width<LD>::NT;
+  constexpr int NCB = D / 16;
+
   constexpr int LDF = TM + 8;  // feature-major row stride (elements)
   __shared__ __align__(16) T sGT[D * LDF];
   __shared__ __align__(16) T sXT[D * LDF];
   const int tid = threadIdx.x, w8 = tid >> 6, lane = tid & 63, i = lane & 15, q = lane >> 4;
-  f32x4 acc[8];
+  f32x4 acc[NCB];
 #pragma unroll
-  for (int cb = 0; cb < 8; ++cb) acc[cb] = zero4();
+  for (int cb = 0; cb < NCB; ++cb) acc[cb] = zero4();
   const int64_t nch = (M + TM - 1) / TM, G = gridDim.x;
   uint4 lg[RT::CPT], lx[RT::CPT];
   auto issue = [&](int64_t c) {
@@ -641,13 +658,13 @@ k_wgrad(int64_t M, const typename Tr<PREC>::T* __restrict__ Gm, const typename T
     for (int k0 = 0; k0 < TM; k0 += P::KS) {
       const typename P::Frag a = P::ldb(sGT, LDF, w8 * 16, k0, i, q);
 #pragma unroll
-      for (int cb = 0; cb < 8; ++cb) acc[cb] = P::mma(a, P::ldb(sXT, LDF, cb * 16, k0, i, q), acc[cb]);
+      for (int cb = 0; cb < NCB; ++cb) acc[cb] = P::mma(a, P::ldb(sXT, LDF, cb * 16, k0, i, q), acc[cb]);
     }
     __syncthreads();
   }
   float* base = part.buf + (size_t)blockIdx.x * part.stride;
 #pragma unroll
-  for (int cb = 0; cb < 8; ++cb)
+  for (int cb = 0; cb < NCB; ++cb)
 #pragma unroll
     for (int r = 0; r < 4; ++r) base[(size_t)(w8 * 16 + q * 4 + r) * D + cb * 16 + i] = acc[cb][r];
 }
@@ -661,44 +678,53 @@ static constexpr int kEdgeFwdBlocks = 512;
 static constexpr int kEdgeBwdBlocks = 256;
 static constexpr int kWgradBlocks = 512;
 
-hipError_t launch_edge_fwd(int prec, const EdgeTiles& t, const void* e_in, void* e_out, int write_e, const void* Pn,
-                           const MlpW& w, float eps, float* agg, float* slots, void* a1_out, hipStream_t s) {
+hipError_t launch_edge_fwd(int prec, int lat, const EdgeTiles& t, const void* e_in, void* e_out, int write_e,
+                           const void* Pn, const MlpW& w, float eps, float* agg, float* slots, void* a1_out,
+                           hipStream_t s) {
   if (prec == MGN_BF16) return launch_edge_fwd_rows(t, e_in, e_out, write_e, Pn, w, eps, agg, slots, a1_out, s);
   const int g = grid_for(t.n_tiles, kEdgeFwdBlocks);
   if (!g) return hipSuccess;
-  if (prec == MGN_BF16)
-    hipLaunchKernelGGL((k_edge_fwd<MGN_BF16, true>), dim3(g), dim3(NT), 0, s, t, (const bf16*)e_in, (bf16*)e_out,
-                       write_e, (const bf16*)Pn, w, eps, agg, slots);
-  else
-    hipLaunchKernelGGL((k_edge_fwd<MGN_FP32, false>), dim3(g), dim3(NT), 0, s, t, (const float*)e_in,
-                       (float*)e_out, write_e, (const float*)Pn, w, eps, agg, slots);
+#define F(LD)                                                                                                     \
+  hipLaunchKernelGGL((k_edge_fwd<MGN_FP32, false, LD>), dim3(g), dim3(LD * 4), 0, s, t, (const float*)e_in,       \
+                     (float*)e_out, write_e, (const float*)Pn, w, eps, agg, slots)
+  MGN_BY_WIDTH(lat, F);
+#undef F
   return hipGetLastError();
 }
 
-hipError_t launch_edge_bwd(int prec, const EdgeTiles& t, const void* e, const float* ebar_in, int have_ebar,
+hipError_t launch_edge_bwd(int prec, int lat, const EdgeTiles& t, const void* e, const float* ebar_in, int have_ebar,
                            float* ebar_out, const void* Pn, const float* aggbar, const MlpW& w, float eps, void* zbar,
                            float* R, float* slots, const Partials& part, int* nblocks, hipStream_t s) {
   const int g = grid_for(t.n_tiles, std::min(kEdgeBwdBlocks, part.max_blocks));
   *nblocks = g;
   if (!g) return hipSuccess;
-  if (prec == MGN_BF16)
-    hipLaunchKernelGGL((k_edge_bwd<MGN_BF16, true>), dim3(g), dim3(NT), 0, s, t, (const bf16*)e, ebar_in, have_ebar,
-                       ebar_out, (const bf16*)Pn, aggbar, w, eps, (bf16*)zbar, R, slots, part);
-  else
-    hipLaunchKernelGGL((k_edge_bwd<MGN_FP32, false>), dim3(g), dim3(NT), 0, s, t, (const float*)e, ebar_in,
-                       have_ebar, ebar_out, (const float*)Pn, aggbar, w, eps, (float*)zbar, R, slots, part);
+  if (prec == MGN_BF16) {
+    hipLaunchKernelGGL((k_edge_bwd<MGN_BF16, true, 128>), dim3(g), dim3(NT), 0, s, t, (const bf16*)e, ebar_in,
+                       have_ebar, ebar_out, (const bf16*)Pn, aggbar, w, eps, (bf16*)zbar, R, slots, part);
+  } else {
+#define F(LD)                                                                                                      \
+  hipLaunchKernelGGL((k_edge_bwd<MGN_FP32, false, LD>), dim3(g), dim3(LD * 4), 0, s, t, (const float*)e, ebar_in,  \
+                     have_ebar, ebar_out, (const float*)Pn, aggbar, w, eps, (float*)zbar, R, slots, part)
+    MGN_BY_WIDTH(lat, F);
+#undef F
+  }
   return hipGetLastError();
 }
 
-hipError_t launch_wgrad(int prec, int64_t M, const void* Gm, const void* Xm, const Partials& part, int* nblocks,
-                        hipStream_t s) {
+hipError_t launch_wgrad(int prec, int lat, int64_t M, const void* Gm, const void* Xm, const Partials& part,
+                        int* nblocks, hipStream_t s) {
   const int g = grid_for((M + TM - 1) / TM, std::min(kWgradBlocks, part.max_blocks));
   *nblocks = g;
   if (!g) return hipSuccess;
-  if (prec == MGN_BF16)
-    hipLaunchKernelGGL(k_wgrad<MGN_BF16>, dim3(g), dim3(NT), 0, s, M, (const bf16*)Gm, (const bf16*)Xm, part);
-  else
-    hipLaunchKernelGGL(k_wgrad<MGN_FP32>, dim3(g), dim3(NT), 0, s, M, (const float*)Gm, (const float*)Xm, part);
+  if (prec == MGN_BF16) {
+    hipLaunchKernelGGL((k_wgrad<MGN_BF16, 128>), dim3(g), dim3(NT), 0, s, M, (const bf16*)Gm, (const bf16*)Xm, part);
+  } else {
+#define F(LD)                                                                                                     \
+  hipLaunchKernelGGL((k_wgrad<MGN_FP32, LD>), dim3(g), dim3(LD * 4), 0, s, M, (const float*)Gm, (const float*)Xm, \
+                     part)
+    MGN_BY_WIDTH(lat, F);
+#undef F
+  }
   return hipGetLastError();
 }
 

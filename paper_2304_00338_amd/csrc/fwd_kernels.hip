@@ -29,10 +29,11 @@ __global__ void __launch_bounds__(256) k_pack(const float* __restrict__ params, 
 }
 
 // Node products for the next block's edge MLP: P[v] = [W1s h_v, W1r h_v].
-template <int PREC>
+template <int PREC, int LD>
 __device__ __forceinline__ void emit_P(const typename Tr<PREC>::T* sH, int ld, const MlpW& nx, int64_t r0, int nr,
                                        typename Tr<PREC>::T* __restrict__ P_out, int w8, int i, int q) {
   typedef typename Tr<PREC>::T T;
+  constexpr int D = LD;
   const T* W1 = (const T*)nx.W1;
   f32x4 ps[NRB], pr[NRB];
 #pragma unroll
@@ -54,16 +55,18 @@ __device__ __forceinline__ void emit_P(const typename Tr<PREC>::T* sH, int ld, c
 }
 
 // ------------------------------------------------------- node encoder
-template <int PREC, bool EMIT>
-__global__ void __launch_bounds__(NT) k_node_enc(int64_t N, const float* __restrict__ x_in, MlpW w, MlpW nx,
+template <int PREC, int LD, bool EMIT>
+__global__ void __launch_bounds__(LD * 4) k_node_enc(int64_t N, const float* __restrict__ x_in, MlpW w, MlpW nx,
                                                  float eps, float* __restrict__ h_out,
                                                  typename Tr<PREC>::T* __restrict__ P_out) {
   typedef Tr<PREC> P;
   typedef typename P::T T;
+  constexpr int D = LD;
+  [[maybe_unused]] constexpr int NW = Width<LD>::NW, NT = Width<LD>::NT;
   constexpr int LDT = D + P::PAD;
   __shared__ float sX[TM][8];
   __shared__ __align__(16) T sA[TM * LDT];
-  __shared__ LnScratch ln;
+  __shared__ LnScratch<NW> ln;
   const int tid = threadIdx.x, w8 = tid >> 6, lane = tid & 63, i = lane & 15, q = lane >> 4;
   const int n = w8 * 16 + i;
   const float b1 = w.b1[n], b2 = w.b2[n], gam = w.gamma[n], bet = w.beta[n];
@@ -108,22 +111,24 @@ __global__ void __launch_bounds__(NT) k_node_enc(int64_t N, const float* __restr
       }
     if (EMIT) {
       __syncthreads();
-      emit_P<PREC>(sA, LDT, nx, r0, nr, P_out, w8, i, q);
+      emit_P<PREC, LD>(sA, LDT, nx, r0, nr, P_out, w8, i, q);
     }
     __syncthreads();
   }
 }
 
 // ------------------------------------------------------- edge encoder
-template <int PREC>
-__global__ void __launch_bounds__(NT) k_edge_enc(int64_t E, const float* __restrict__ f_in, MlpW w, float eps,
+template <int PREC, int LD>
+__global__ void __launch_bounds__(LD * 4) k_edge_enc(int64_t E, const float* __restrict__ f_in, MlpW w, float eps,
                                                  typename Tr<PREC>::T* __restrict__ e_out) {
   typedef Tr<PREC> P;
   typedef typename P::T T;
+  constexpr int D = LD;
+  [[maybe_unused]] constexpr int NW = Width<LD>::NW, NT = Width<LD>::NT;
   constexpr int LDT = D + P::PAD;
   __shared__ float sX[TM][4];
   __shared__ __align__(16) T sA[TM * LDT];
-  __shared__ LnScratch ln;
+  __shared__ LnScratch<NW> ln;
   const int tid = threadIdx.x, w8 = tid >> 6, lane = tid & 63, i = lane & 15, q = lane >> 4;
   const int n = w8 * 16 + i;
   const float b1 = w.b1[n], b2 = w.b2[n], gam = w.gamma[n], bet = w.beta[n];
@@ -165,7 +170,7 @@ __global__ void __launch_bounds__(NT) k_edge_enc(int64_t E, const float* __restr
       }
     __syncthreads();
     for (int idx = tid; idx < nr * (D / 8); idx += NT) {
-      const int row = idx >> 4, c = (idx & 15) * 8;
+      const int row = idx / (D / 8), c = (idx % (D / 8)) * 8;
       T* dst = e_out + (size_t)(r0 + row) * D + c;
 #pragma unroll
       for (int j = 0; j < 8; ++j) dst[j] = sA[row * LDT + c + j];
@@ -175,8 +180,10 @@ __global__ void __launch_bounds__(NT) k_edge_enc(int64_t E, const float* __restr
 }
 
 // Long in-segments: dst[v] = sum of the chunk slots in chunk order.
-__global__ void __launch_bounds__(128) k_slot_fixup(const int32_t* __restrict__ longn, const float* __restrict__ slots,
-                                                    float* __restrict__ dst) {
+template <int LD>
+__global__ void __launch_bounds__(LD) k_slot_fixup(const int32_t* __restrict__ longn, const float* __restrict__ slots,
+                                                   float* __restrict__ dst) {
+  constexpr int D = LD;
   const int4 L = reinterpret_cast<const int4*>(longn)[blockIdx.x];
   const int c = threadIdx.x;
   float s = 0.f;
@@ -187,17 +194,19 @@ __global__ void __launch_bounds__(128) k_slot_fixup(const int32_t* __restrict__ 
 // ------------------------------------------------- fused node phase
 // h_out = h + LN(W2 relu(W1 [h, agg] + b1) + b2); optionally the next
 // block's node products P.
-template <int PREC, bool EMIT>
-__global__ void __launch_bounds__(NT) k_node_fwd(int64_t N, const float* __restrict__ h_in, const float* __restrict__ agg,
+template <int PREC, int LD, bool EMIT>
+__global__ void __launch_bounds__(LD * 4) k_node_fwd(int64_t N, const float* __restrict__ h_in, const float* __restrict__ agg,
                                                  MlpW w, MlpW nx, float eps, float* __restrict__ h_out,
                                                  typename Tr<PREC>::T* __restrict__ P_out) {
   typedef Tr<PREC> P;
   typedef typename P::T T;
+  constexpr int D = LD;
+  [[maybe_unused]] constexpr int NW = Width<LD>::NW, NT = Width<LD>::NT;
   constexpr int LDT = D + P::PAD;
   constexpr int LDX = 2 * D + P::PAD;
   __shared__ __align__(16) T sX[TM * LDX];  // [h, agg]; later the new h
   __shared__ __align__(16) T sA[TM * LDT];
-  __shared__ LnScratch ln;
+  __shared__ LnScratch<NW> ln;
   const int tid = threadIdx.x, w8 = tid >> 6, lane = tid & 63, i = lane & 15, q = lane >> 4;
   const int n = w8 * 16 + i;
   const float b1 = w.b1[n], b2 = w.b2[n], gam = w.gamma[n], bet = w.beta[n];
@@ -205,8 +214,8 @@ __global__ void __launch_bounds__(NT) k_node_fwd(int64_t N, const float* __restr
   for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
     const int64_t r0 = t * TM;
     const int nr = (int)min((int64_t)TM, N - r0);
-    stage_rows(sX, LDX, h_in + (size_t)r0 * D, nr, tid);
-    stage_rows(sX + D, LDX, agg + (size_t)r0 * D, nr, tid);
+    stage_rows<D>(sX, LDX, h_in + (size_t)r0 * D, nr, tid);
+    stage_rows<D>(sX + D, LDX, agg + (size_t)r0 * D, nr, tid);
     __syncthreads();
     f32x4 acc[NRB];
 #pragma unroll
@@ -236,7 +245,7 @@ __global__ void __launch_bounds__(NT) k_node_fwd(int64_t N, const float* __restr
       }
     if (EMIT) {
       __syncthreads();
-      emit_P<PREC>(sX, LDX, nx, r0, nr, P_out, w8, i, q);
+      emit_P<PREC, LD>(sX, LDX, nx, r0, nr, P_out, w8, i, q);
     }
     __syncthreads();
   }
@@ -244,10 +253,12 @@ __global__ void __launch_bounds__(NT) k_node_fwd(int64_t N, const float* __restr
 
 // ------------------------------------------------------------ decoder
 // out = W2 relu(W1 h + b1) + b2 (no LayerNorm); 4 outputs per node.
-template <int PREC>
-__global__ void __launch_bounds__(NT) k_decoder(int64_t N, const float* __restrict__ h, MlpW w, float* __restrict__ out) {
+template <int PREC, int LD>
+__global__ void __launch_bounds__(LD * 4) k_decoder(int64_t N, const float* __restrict__ h, MlpW w, float* __restrict__ out) {
   typedef Tr<PREC> P;
   typedef typename P::T T;
+  constexpr int D = LD;
+  [[maybe_unused]] constexpr int NW = Width<LD>::NW, NT = Width<LD>::NT;
   constexpr int LDT = D + P::PAD;
   constexpr int LDM = D + 4;
   __shared__ __align__(16) T sX[TM * LDT];
@@ -259,7 +270,7 @@ __global__ void __launch_bounds__(NT) k_decoder(int64_t N, const float* __restri
   for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
     const int64_t r0 = t * TM;
     const int nr = (int)min((int64_t)TM, N - r0);
-    stage_rows(sX, LDT, h + (size_t)r0 * D, nr, tid);
+    stage_rows<D>(sX, LDT, h + (size_t)r0 * D, nr, tid);
     __syncthreads();
     f32x4 acc[NRB];
 #pragma unroll
@@ -305,73 +316,91 @@ hipError_t launch_pack(int prec, const float* params, void* pack, const PackList
   return hipGetLastError();
 }
 
-hipError_t launch_node_enc(int prec, int64_t N, const float* x, const MlpW& w, const MlpW* nx, float eps,
+hipError_t launch_node_enc(int prec, int lat, int64_t N, const float* x, const MlpW& w, const MlpW* nx, float eps,
                            float* h_out, void* P_out, hipStream_t s) {
   const int g = grid_for((N + TM - 1) / TM, kFwdBlocks);
   if (!g) return hipSuccess;
   const MlpW nn = nx ? *nx : w;
   if (prec == MGN_BF16) {
     if (nx)
-      hipLaunchKernelGGL((k_node_enc<MGN_BF16, true>), dim3(g), dim3(NT), 0, s, N, x, w, nn, eps, h_out, (bf16*)P_out);
+      hipLaunchKernelGGL((k_node_enc<MGN_BF16, 128, true>), dim3(g), dim3(NT), 0, s, N, x, w, nn, eps, h_out,
+                         (bf16*)P_out);
     else
-      hipLaunchKernelGGL((k_node_enc<MGN_BF16, false>), dim3(g), dim3(NT), 0, s, N, x, w, nn, eps, h_out, (bf16*)P_out);
+      hipLaunchKernelGGL((k_node_enc<MGN_BF16, 128, false>), dim3(g), dim3(NT), 0, s, N, x, w, nn, eps, h_out,
+                         (bf16*)P_out);
   } else {
-    if (nx)
-      hipLaunchKernelGGL((k_node_enc<MGN_FP32, true>), dim3(g), dim3(NT), 0, s, N, x, w, nn, eps, h_out, (float*)P_out);
-    else
-      hipLaunchKernelGGL((k_node_enc<MGN_FP32, false>), dim3(g), dim3(NT), 0, s, N, x, w, nn, eps, h_out, (float*)P_out);
+#define F(LD)                                                                                                        \
+  if (nx)                                                                                                            \
+    hipLaunchKernelGGL((k_node_enc<MGN_FP32, LD, true>), dim3(g), dim3(LD * 4), 0, s, N, x, w, nn, eps, h_out,       \
+                       (float*)P_out);                                                                               \
+  else                                                                                                               \
+    hipLaunchKernelGGL((k_node_enc<MGN_FP32, LD, false>), dim3(g), dim3(LD * 4), 0, s, N, x, w, nn, eps, h_out,      \
+                       (float*)P_out)
+    MGN_BY_WIDTH(lat, F);
+#undef F
   }
   return hipGetLastError();
 }
 
-hipError_t launch_edge_enc(int prec, int64_t E, const float* f, const MlpW& w, float eps, void* e_out,
+hipError_t launch_edge_enc(int prec, int lat, int64_t E, const float* f, const MlpW& w, float eps, void* e_out,
                            hipStream_t s) {
   const int g = grid_for((E + TM - 1) / TM, kFwdBlocks);
   if (!g) return hipSuccess;
-  if (prec == MGN_BF16)
-    hipLaunchKernelGGL(k_edge_enc<MGN_BF16>, dim3(g), dim3(NT), 0, s, E, f, w, eps, (bf16*)e_out);
-  else
-    hipLaunchKernelGGL(k_edge_enc<MGN_FP32>, dim3(g), dim3(NT), 0, s, E, f, w, eps, (float*)e_out);
+  if (prec == MGN_BF16) {
+    hipLaunchKernelGGL((k_edge_enc<MGN_BF16, 128>), dim3(g), dim3(NT), 0, s, E, f, w, eps, (bf16*)e_out);
+  } else {
+#define F(LD) hipLaunchKernelGGL((k_edge_enc<MGN_FP32, LD>), dim3(g), dim3(LD * 4), 0, s, E, f, w, eps, (float*)e_out)
+    MGN_BY_WIDTH(lat, F);
+#undef F
+  }
   return hipGetLastError();
 }
 
-hipError_t launch_slot_fixup(const int32_t* long_nodes, int64_t n_long, const float* slots, float* dst,
+hipError_t launch_slot_fixup(int lat, const int32_t* long_nodes, int64_t n_long, const float* slots, float* dst,
                              hipStream_t s) {
   if (n_long <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_slot_fixup, dim3((unsigned)n_long), dim3(128), 0, s, long_nodes, slots, dst);
+#define F(LD) hipLaunchKernelGGL(k_slot_fixup<LD>, dim3((unsigned)n_long), dim3(LD), 0, s, long_nodes, slots, dst)
+  MGN_BY_WIDTH(lat, F);
+#undef F
   return hipGetLastError();
 }
 
-hipError_t launch_node_fwd(int prec, int64_t N, const float* h_in, const float* agg, const MlpW& w,
+hipError_t launch_node_fwd(int prec, int lat, int64_t N, const float* h_in, const float* agg, const MlpW& w,
                            const MlpW* nx, float eps, float* h_out, void* P_out, hipStream_t s) {
   const int g = grid_for((N + TM - 1) / TM, kFwdBlocks);
   if (!g) return hipSuccess;
   const MlpW nn = nx ? *nx : w;
   if (prec == MGN_BF16) {
     if (nx)
-      hipLaunchKernelGGL((k_node_fwd<MGN_BF16, true>), dim3(g), dim3(NT), 0, s, N, h_in, agg, w, nn, eps, h_out,
+      hipLaunchKernelGGL((k_node_fwd<MGN_BF16, 128, true>), dim3(g), dim3(NT), 0, s, N, h_in, agg, w, nn, eps, h_out,
                          (bf16*)P_out);
     else
-      hipLaunchKernelGGL((k_node_fwd<MGN_BF16, false>), dim3(g), dim3(NT), 0, s, N, h_in, agg, w, nn, eps, h_out,
+      hipLaunchKernelGGL((k_node_fwd<MGN_BF16, 128, false>), dim3(g), dim3(NT), 0, s, N, h_in, agg, w, nn, eps, h_out,
                          (bf16*)P_out);
   } else {
-    if (nx)
-      hipLaunchKernelGGL((k_node_fwd<MGN_FP32, true>), dim3(g), dim3(NT), 0, s, N, h_in, agg, w, nn, eps, h_out,
-                         (float*)P_out);
-    else
-      hipLaunchKernelGGL((k_node_fwd<MGN_FP32, false>), dim3(g), dim3(NT), 0, s, N, h_in, agg, w, nn, eps, h_out,
-                         (float*)P_out);
+#define F(LD)                                                                                                        \
+  if (nx)                                                                                                            \
+    hipLaunchKernelGGL((k_node_fwd<MGN_FP32, LD, true>), dim3(g), dim3(LD * 4), 0, s, N, h_in, agg, w, nn, eps,      \
+                       h_out, (float*)P_out);                                                                        \
+  else                                                                                                               \
+    hipLaunchKernelGGL((k_node_fwd<MGN_FP32, LD, false>), dim3(g), dim3(LD * 4), 0, s, N, h_in, agg, w, nn, eps,     \
+                       h_out, (float*)P_out)
+    MGN_BY_WIDTH(lat, F);
+#undef F
   }
   return hipGetLastError();
 }
 
-hipError_t launch_decoder(int prec, int64_t N, const float* h, const MlpW& w, float* out, hipStream_t s) {
+hipError_t launch_decoder(int prec, int lat, int64_t N, const float* h, const MlpW& w, float* out, hipStream_t s) {
   const int g = grid_for((N + TM - 1) / TM, kFwdBlocks);
   if (!g) return hipSuccess;
-  if (prec == MGN_BF16)
-    hipLaunchKernelGGL(k_decoder<MGN_BF16>, dim3(g), dim3(NT), 0, s, N, h, w, out);
-  else
-    hipLaunchKernelGGL(k_decoder<MGN_FP32>, dim3(g), dim3(NT), 0, s, N, h, w, out);
+  if (prec == MGN_BF16) {
+    hipLaunchKernelGGL((k_decoder<MGN_BF16, 128>), dim3(g), dim3(NT), 0, s, N, h, w, out);
+  } else {
+#define F(LD) hipLaunchKernelGGL((k_decoder<MGN_FP32, LD>), dim3(g), dim3(LD * 4), 0, s, N, h, w, out)
+    MGN_BY_WIDTH(lat, F);
+#undef F
+  }
   return hipGetLastError();
 }
 

@@ -74,11 +74,13 @@ int grid_for(int64_t n_tiles, int max_blocks);
 
 hipError_t launch_pack(int prec, const float* params, void* pack, const PackList& L, hipStream_t s);
 
-hipError_t launch_node_enc(int prec, int64_t N, const float* node_in, const MlpW& w, const MlpW* next_edge,
+// Feature-split kernels: lat is the kernel width (128, or 160 for the
+// latent 150 padded with zero columns; fp32 only).
+hipError_t launch_node_enc(int prec, int lat, int64_t N, const float* node_in, const MlpW& w, const MlpW* next_edge,
                            float eps, float* h_out, void* P_out, hipStream_t s);
-hipError_t launch_edge_enc(int prec, int64_t E, const float* efeat, const MlpW& w, float eps, void* e_out,
+hipError_t launch_edge_enc(int prec, int lat, int64_t E, const float* efeat, const MlpW& w, float eps, void* e_out,
                            hipStream_t s);
-hipError_t launch_edge_fwd(int prec, const EdgeTiles& t, const void* e_in, void* e_out, int write_e,
+hipError_t launch_edge_fwd(int prec, int lat, const EdgeTiles& t, const void* e_in, void* e_out, int write_e,
                            const void* P, const MlpW& w, float eps, float* agg, float* slots, void* a1_out,
                            hipStream_t s);
 // bf16 edge forward with one wave per tile (uses MlpW::W1p / W2p); a1_out
@@ -114,31 +116,31 @@ hipError_t launch_edge_enc_rows(int64_t E, const float* efeat, const MlpW& w, fl
 // partials of every encoder parameter (encoder parameter order).
 hipError_t launch_edge_enc_bwd_rows(int64_t E, const float* efeat, const void* ebar, const MlpW& w, float eps,
                                     const Partials& part, int* nblocks, hipStream_t s);
-hipError_t launch_slot_fixup(const int32_t* long_nodes, int64_t n_long, const float* slots, float* dst,
+hipError_t launch_slot_fixup(int lat, const int32_t* long_nodes, int64_t n_long, const float* slots, float* dst,
                              hipStream_t s);
-hipError_t launch_node_fwd(int prec, int64_t N, const float* h_in, const float* agg, const MlpW& w,
+hipError_t launch_node_fwd(int prec, int lat, int64_t N, const float* h_in, const float* agg, const MlpW& w,
                            const MlpW* next_edge, float eps, float* h_out, void* P_out, hipStream_t s);
-hipError_t launch_decoder(int prec, int64_t N, const float* h, const MlpW& w, float* out, hipStream_t s);
+hipError_t launch_decoder(int prec, int lat, int64_t N, const float* h, const MlpW& w, float* out, hipStream_t s);
 
-hipError_t launch_decoder_bwd(int prec, int64_t N, const float* h, const float* gout, const MlpW& w,
+hipError_t launch_decoder_bwd(int prec, int lat, int64_t N, const float* h, const float* gout, const MlpW& w,
                               float* hbar, const Partials& part, int* nblocks, hipStream_t s);
-hipError_t launch_node_bwd(int prec, int64_t N, const float* h, const float* agg, const float* hbar_in,
+hipError_t launch_node_bwd(int prec, int lat, int64_t N, const float* h, const float* agg, const float* hbar_in,
                            const MlpW& w, float eps, float* hbar_part, float* aggbar, const Partials& part,
                            int* nblocks, hipStream_t s);
-hipError_t launch_edge_bwd(int prec, const EdgeTiles& t, const void* e, const float* ebar_in, int have_ebar,
+hipError_t launch_edge_bwd(int prec, int lat, const EdgeTiles& t, const void* e, const float* ebar_in, int have_ebar,
                            float* ebar_out, const void* P, const float* aggbar, const MlpW& w, float eps,
                            void* zbar, float* R, float* slots, const Partials& part, int* nblocks,
                            hipStream_t s);
-// dW[o][i] = sum_rows G[row][o] X[row][i] for [M][128] operand-precision
-// streams, written as per-block [128][128] partials.
-hipError_t launch_wgrad(int prec, int64_t M, const void* G, const void* X, const Partials& part, int* nblocks,
+// dW[o][i] = sum_rows G[row][o] X[row][i] for [M][lat] operand-precision
+// streams, written as per-block [lat][lat] partials.
+hipError_t launch_wgrad(int prec, int lat, int64_t M, const void* G, const void* X, const Partials& part, int* nblocks,
                         hipStream_t s);
-hipError_t launch_node_srcsum(int prec, int64_t N, const int32_t* rowptr, const int32_t* rev, const void* zbar,
+hipError_t launch_node_srcsum(int prec, int lat, int64_t N, const int32_t* rowptr, const int32_t* rev, const void* zbar,
                               const float* R, const float* h, const float* hbar_part, const MlpW& w,
                               float* hbar_out, const Partials& part, int* nblocks, hipStream_t s);
-hipError_t launch_edge_enc_bwd(int prec, int64_t E, const float* efeat, const float* ebar, const MlpW& w,
+hipError_t launch_edge_enc_bwd(int prec, int lat, int64_t E, const float* efeat, const float* ebar, const MlpW& w,
                                float eps, const Partials& part, int* nblocks, hipStream_t s);
-hipError_t launch_node_enc_bwd(int prec, int64_t N, const float* node_in, const float* hbar, const MlpW& w,
+hipError_t launch_node_enc_bwd(int prec, int lat, int64_t N, const float* node_in, const float* hbar, const MlpW& w,
                                float eps, float* gin, const Partials& part, int* nblocks, hipStream_t s);
 
 // grad[dst + r*dst_ld + c] += sum_b part[b*stride + src + r*cols + c]
@@ -155,6 +157,19 @@ struct LinComb {
 };
 hipError_t launch_lincomb(int64_t N, const LinComb& lc, float* out, int32_t out_ld, int32_t out_off,
                           hipStream_t s);
+// Block moves between parameter layouts: for every block,
+// b[b_off + r*b_ld + c] = a[a_off + r*a_ld + c] (or += with accumulate),
+// r < rows, c < cols.
+struct CopyBlock {
+  int64_t a_off, b_off;
+  int32_t rows, cols, a_ld, b_ld;
+};
+constexpr int kCopyMax = 64;
+struct CopyList {
+  CopyBlock b[kCopyMax];
+  int32_t n;
+};
+hipError_t launch_copy_blocks(const CopyList& L, const float* a, float* b, int accumulate, hipStream_t s);
 // p[0..n) = v
 hipError_t launch_fill(float* p, int64_t n, float v, hipStream_t s);
 // Training step: partial rows of the loss sum; noisy gather dst[r] =

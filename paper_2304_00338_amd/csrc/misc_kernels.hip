@@ -56,6 +56,22 @@ __global__ void __launch_bounds__(256) k_scatter_rows4(int64_t n, const float* _
   dst[v * 4 + (t & 3)] = src[t];
 }
 
+// Rectangular block moves between two parameter layouts (the real latent-150
+// layout and the kernels' zero-padded latent-160 one): block k moves
+// a[a_off + r * a_ld + c] to b[b_off + r * b_ld + c], added to b when
+// accumulate is set.  Blocks of one list never overlap in b.
+__global__ void __launch_bounds__(256) k_copy_blocks(CopyList L, const float* __restrict__ a, float* __restrict__ b,
+                                                     int accumulate) {
+  const CopyBlock cb = L.b[blockIdx.y];
+  const int64_t n = (int64_t)cb.rows * cb.cols;
+  for (int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x; idx < n; idx += (int64_t)gridDim.x * 256) {
+    const int64_t r = idx / cb.cols, c = idx % cb.cols;
+    const float v = a[cb.a_off + r * cb.a_ld + c];
+    float* d = b + cb.b_off + r * cb.b_ld + c;
+    *d = accumulate ? *d + v : v;
+  }
+}
+
 }  // namespace dev
 
 using namespace dev;
@@ -74,6 +90,12 @@ hipError_t launch_scatter_rows4(int64_t n, const float* src, const int32_t* idx,
   if (n_dst <= 0) return hipErrorInvalidValue;
   hipLaunchKernelGGL(k_scatter_rows4, dim3((unsigned)((n * 4 + 255) / 256)), dim3(256), 0, s, n, src, idx, mask,
                      n_dst, dst);
+  return hipGetLastError();
+}
+
+hipError_t launch_copy_blocks(const CopyList& L, const float* a, float* b, int accumulate, hipStream_t s) {
+  if (L.n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_copy_blocks, dim3(64, L.n), dim3(256), 0, s, L, a, b, accumulate);
   return hipGetLastError();
 }
 

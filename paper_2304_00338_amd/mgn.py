@@ -297,9 +297,10 @@ class Context:
     """mgn_ctx plus a workspace tensor of the size the library asks for."""
 
     def __init__(self, mp_steps, max_nodes, max_edges, precision="fp32", max_stages=1,
-                 save=False, ln_eps=1e-5, device="cuda", allocate=True):
-        self.cfg = config(mp_steps, precision, ln_eps)
+                 save=False, ln_eps=1e-5, device="cuda", allocate=True, latent=128):
+        self.cfg = config(mp_steps, precision, ln_eps, latent)
         self.mp_steps = int(mp_steps)
+        self.latent = int(latent)
         ws = C.c_size_t()
         h = C.c_void_p()
         _check(lib().mgn_ctx_create(C.byref(self.cfg), int(max_nodes), int(max_edges),

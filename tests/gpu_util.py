@@ -27,10 +27,10 @@ def rel_l2(a, b):
     return float(np.linalg.norm(a - b) / (nb if nb > 0 else 1.0))
 
 
-def segments(m):
+def segments(m, latent=128):
     """(name, start, stop) of every MLP in the flat parameter buffer."""
     out, off = [], 0
-    for name, fields in O.param_layout(m):
+    for name, fields in O.param_layout(m, latent):
         n = sum(int(np.prod(s)) for _, s in fields)
         out.append((name, off, off + n))
         off += n
@@ -83,7 +83,7 @@ def bf16_grad_tols(pb, trials=2, scale=2.0):
 
 class Problem:
     def __init__(self, shape=None, m=2, seed=0, randomize=True, cells=None, pos=None, node_in=None,
-                 smooth=False):
+                 smooth=False, latent=128):
         from paper_2304_00338_amd import mgn
         if shape is not None:
             M = synth.mesh(shape, seed)
@@ -95,10 +95,11 @@ class Problem:
         self.cells, self.pos, self.node_in = cells, pos, node_in.astype(np.float32)
         self.m = m
         self.seed = seed
+        self.latent = latent
         self.g = mgn.build_graph(cells, pos)
         self.go = O.build_graph(cells, pos)
-        self.params = (synth.smooth_params(m, seed) if smooth
-                       else synth.xavier_params(m, seed, randomize_norm=randomize))
+        self.params = (synth.smooth_params(m, seed, latent) if smooth
+                       else synth.xavier_params(m, seed, latent, randomize_norm=randomize))
         self.w = synth.loss_weights(self.g.n_nodes, seed)
 
     def device(self):

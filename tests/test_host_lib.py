@@ -181,11 +181,17 @@ def test_ctx_planning_and_errors():
     with pytest.raises(mgn.MgnError) as e:
         mgn.Context(15, 10, 10, "fp32", max_stages=5, allocate=False)
     assert e.value.code == mgn.ERR_ARG
-    cfg = mgn.config(3)
-    cfg.latent = 150
     ws, h = ctypes.c_size_t(), ctypes.c_void_p()
-    rc = mgn.lib().mgn_ctx_create(ctypes.byref(cfg), 10, 10, 1, 0, ctypes.byref(ws), ctypes.byref(h))
-    assert rc == mgn.ERR_SHAPE
+    for lat, prec in ((140, "fp32"), (256, "fp32"), (150, "bf16")):
+        cfg = mgn.config(3, prec, latent=lat)  # latent 150 runs in fp32 only
+        rc = mgn.lib().mgn_ctx_create(ctypes.byref(cfg), 10, 10, 1, 0, ctypes.byref(ws), ctypes.byref(h))
+        assert rc == mgn.ERR_SHAPE, (lat, prec)
+    # latent 150 (the 3D model, kernels padded to 160): parameter count in the
+    # oracle's layout, a larger workspace than latent 128
+    assert mgn.param_count(3, 150) == O.n_params(3, 150)
+    c150 = mgn.Context(3, 1000, 20000, "fp32", save=True, max_stages=2, latent=150, allocate=False)
+    c128 = mgn.Context(3, 1000, 20000, "fp32", save=True, max_stages=2, allocate=False)
+    assert c150.ws_bytes > c128.ws_bytes
     assert mgn.scheme_stages("rk4") == 4 and mgn.scheme_stages("heun3") == 3
     assert mgn.lib().mgn_scheme_stages(9) == mgn.ERR_ARG
     # backward without a saved call

@@ -25,10 +25,10 @@ import synth
 GOLD = os.path.join(os.path.dirname(__file__), "golden", "paper_facts.json")
 
 
-def small(shape=(5, 4), m=2, seed=0, randomize=True):
+def small(shape=(5, 4), m=2, seed=0, randomize=True, latent=128):
     M = synth.mesh(shape, seed)
     g = O.build_graph(M["cells"], M["pos"])
-    P = synth.xavier_params(m, seed, randomize_norm=randomize)
+    P = synth.xavier_params(m, seed, latent=latent, randomize_norm=randomize)
     return M, g, P
 
 
@@ -110,6 +110,25 @@ def test_dense_brute_force_forward_and_autograd(shape, m):
     Pt = torch.tensor(P.astype(np.float64), requires_grad=True)
     xt = torch.tensor(M["node_in"].astype(np.float64), requires_grad=True)
     ref = dense_mgn(g, Pt, xt, torch.tensor(g.efeat.astype(np.float64)), m)
+    assert np.allclose(out, ref.detach().numpy(), rtol=1e-11, atol=1e-11)
+    (ref * torch.tensor(w.astype(np.float64))).sum().backward()
+    assert np.allclose(gp, Pt.grad.numpy(), rtol=1e-9, atol=1e-9)
+    assert np.allclose(gin, xt.grad.numpy(), rtol=1e-9, atol=1e-9)
+
+
+def test_dense_brute_force_latent150():
+    """The 3D model's width (App. C: latent 150, 3 MP steps): the oracle at
+    latent 150 against the dense torch MGN of that width, outputs and
+    autograd gradients."""
+    m, D = 3, 150
+    M, g, P = small((3, 3, 2), m, seed=9, latent=D)
+    assert P.size == O.n_params(m, D)
+    w = synth.loss_weights(g.n_nodes, 9)
+    out, tape = O.mgn_forward(g, P, M["node_in"], g.efeat, m, latent=D, keep=True)
+    gp, gin = O.mgn_backward(tape, w)
+    Pt = torch.tensor(P.astype(np.float64), requires_grad=True)
+    xt = torch.tensor(M["node_in"].astype(np.float64), requires_grad=True)
+    ref = dense_mgn(g, Pt, xt, torch.tensor(g.efeat.astype(np.float64)), m, D=D)
     assert np.allclose(out, ref.detach().numpy(), rtol=1e-11, atol=1e-11)
     (ref * torch.tensor(w.astype(np.float64))).sum().backward()
     assert np.allclose(gp, Pt.grad.numpy(), rtol=1e-9, atol=1e-9)
