@@ -78,7 +78,9 @@ extern "C" {
 typedef struct mgn_config {
   int32_t node_in;    /* node input features; must be 8 (4 one-hot + 4 state) */
   int32_t edge_in;    /* edge input features; must be 4 */
-  int32_t latent;     /* latent width; must be 128 */
+  int32_t latent;     /* latent width D: 128 (App. C, 2D model) or 150 (App. C,
+                         3D model; MGN_FP32 only, computed 160 wide with zero
+                         padding, LayerNorm over the 150 real features) */
   int32_t out;        /* decoder outputs; must be 4 */
   int32_t mp_steps;   /* m >= 0 message-passing steps (unshared weights) */
   int32_t mlp_layers; /* Linear layers per MLP; must be 2 */
@@ -86,17 +88,19 @@ typedef struct mgn_config {
   int32_t precision;  /* MGN_FP32 or MGN_BF16 */
 } mgn_config;
 
-/* Flat float32 parameter buffer, in this order (weights [out][in] row-major):
- *   enc_node: W1[128][8]  b1[128] W2[128][128] b2[128] gamma[128] beta[128]
- *   enc_edge: W1[128][4]  b1 W2[128][128] b2 gamma beta
+/* Flat float32 parameter buffer, in this order (weights [out][in] row-major,
+ * D = latent):
+ *   enc_node: W1[D][8]  b1[D] W2[D][D] b2[D] gamma[D] beta[D]
+ *   enc_edge: W1[D][4]  b1 W2[D][D] b2 gamma beta
  *   for each block i < m:
- *     edge:   W1[128][384] (input order: edge latent, sender latent,
- *             receiver latent) b1 W2[128][128] b2 gamma beta
- *     node:   W1[128][256] (input order: node latent, aggregate) b1
- *             W2[128][128] b2 gamma beta
- *   dec:      W1[128][128] b1[128] W2[4][128] b2[4]          (no LayerNorm)
- * 17,920 + 17,408 + m * (66,048 + 49,664) + 17,028 floats
- * (1,788,036 at m = 15). */
+ *     edge:   W1[D][3D] (input order: edge latent, sender latent,
+ *             receiver latent) b1 W2[D][D] b2 gamma beta
+ *     node:   W1[D][2D] (input order: node latent, aggregate) b1
+ *             W2[D][D] b2 gamma beta
+ *   dec:      W1[D][D] b1[D] W2[4][D] b2[4]          (no LayerNorm)
+ * At D = 128: 17,920 + 17,408 + m * (66,048 + 49,664) + 17,028 floats
+ * (1,788,036 at m = 15); at D = 150: 547,354 floats at m = 3.  Gradients
+ * are returned in the same layout. */
 int64_t mgn_param_count(const mgn_config* cfg);
 
 /* ---- host graphs (App. B edges, Sec. 2.2 patches) --------------------- */
