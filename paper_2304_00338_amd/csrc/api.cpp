@@ -320,7 +320,10 @@ void plan(Ctx& c) {
   so = al256(so + (size_t)la * N * 2 * D * tsz);
   // bf16 with save: first-layer activations of every edge MLP, read by the
   // backward instead of recomputing the first layer
-  const bool keep_a1 = c.save && c.cfg.precision == MGN_BF16;
+  // bf16 at width 128 runs on the row-layout kernels; every other case on
+  // the feature-split ones
+  const bool rows = c.cfg.precision == MGN_BF16 && c.LD == kRowsD;
+  const bool keep_a1 = c.save && rows;
   L.a1_off = so;
   so = al256(so + (keep_a1 ? (size_t)la * E * D * 2 : 0));
   L.act_stride = so;
@@ -343,8 +346,8 @@ void plan(Ctx& c) {
       L.gpad = o;  // gradients in the padded layout, moved to the caller's layout at the end
       o = al256(o + (size_t)c.M.total * 4);
     }
-    L.ebar = o;  // edge-gradient stream, in the edge-latent element type
-    o = al256(o + (size_t)E * D * c.se);
+    L.ebar = o;  // edge-gradient stream: the edge-latent element type (row layout), else fp32
+    o = al256(o + (size_t)E * D * (rows ? c.se : 4));
     L.zbar = o;
     o = al256(o + (size_t)E * D * c.se);
     L.dz = o;
@@ -399,6 +402,8 @@ struct Run {
   float eps;
   bool keep_a1 = false;  // this call saves (or the backward reads) the edge MLPs' a1
   int D = c.LD;          // kernel latent width
+  // bf16 at width 128 runs on the row-layout kernels
+  bool rows() const { return prec == MGN_BF16 && D == kRowsD; }
 
   // Bracket a launch with profiling events when enabled.
   hipError_t mark_begin(int kind) {
@@ -431,7 +436,7 @@ struct Run {
     return (float*)(set(k) + c.L.agg_off) + (c.save ? (size_t)l * N * D : 0);
   }
   void* a1_l(int k, int l) const {
-    if (!(keep_a1 && c.save && prec == MGN_BF16)) return nullptr;
+    if (!(keep_a1 && c.save && rows())) return nullptr;
     return set(k) + c.L.a1_off + (size_t)l * E * D * 2;
   }
   void* P_l(int k, int l) const {
@@ -494,7 +499,7 @@ struct Run {
     LAUNCH(K_NODE_ENC, launch_node_enc(prec, D, N, node_in, W(M.enc_node, M.p_enc_node), m > 0 ? &e0 : nullptr, eps, h_l(k, 0),
                             P_l(k, 0), s));
     if (m > 0) {
-      if (prec == MGN_BF16)
+      if (rows())
         LAUNCH(K_EDGE_ENC, launch_edge_enc_rows(E, efeat, W(M.enc_edge, M.p_enc_edge), eps, e_l(k, 0), s));
       else
         LAUNCH(K_EDGE_ENC, launch_edge_enc(prec, D, E, efeat, W(M.enc_edge, M.p_enc_edge), eps, e_l(k, 0), s));
@@ -510,7 +515,7 @@ struct Run {
       if (g.n_long > 0) LAUNCH(K_FIXUP, launch_slot_fixup(D, g.long_nodes, g.n_long, slots(), agg_l(k, l), s));
       MlpW nx;
       if (!last) nx = W(M.edge[l + 1], M.p_edge[l + 1]);
-      if (prec == MGN_BF16) {
+      if (rows()) {
         LAUNCH(K_NODE_FWD, launch_node_fwd_rows(N, h_l(k, l), agg_l(k, l), W(M.node[l], M.p_node[l]), eps, h_l(k, l + 1), s));
         if (!last) LAUNCH(K_EMIT, launch_emit_rows(N, h_l(k, l + 1), nx, P_l(k, l + 1), s));
       } else {
@@ -535,7 +540,7 @@ struct Run {
     float* hb_part = (float*)(ws + c.L.hb_b);
     float* aggbar = (float*)(ws + c.L.aggbar);
     float* R = (float*)(ws + c.L.R);
-    void* ebar = ws + c.L.ebar;  // bf16: the edge-latent element type
+    void* ebar = ws + c.L.ebar;  // row layout: the edge-latent element type; else fp32
     void* zbar = ws + c.L.zbar;
     int nb = 0, rc;
     LAUNCH(K_DECODER_BWD, launch_decoder_bwd(prec, D, N, h_l(k, m), gout, W(M.dec, M.p_dec), hb_cur, pt, &nb, s));
@@ -543,7 +548,7 @@ struct Run {
     for (int l = m - 1; l >= 0; --l) {
       const Off& oe = M.edge[l];
       const Off& on = M.node[l];
-      if (prec == MGN_BF16) {
+      if (rows()) {
         char* ns = ws + c.L.nstr;
         void *na1 = ns, *ndz2 = ns + (size_t)N * D * 2, *ndz1 = ns + (size_t)2 * N * D * 2;
         LAUNCH(K_NODE_BWD, launch_node_bwd_rows(N, h_l(k, l), agg_l(k, l), hb_cur, W(on, M.p_node[l]), eps, hb_part, aggbar,
@@ -559,7 +564,7 @@ struct Run {
       if (E == 0) {
         // no edges: the edge MLP gets no gradient and every R is zero
         LAUNCH(K_EDGE_BWD, launch_fill(R, N * D, 0.f, s));
-      } else if (prec == MGN_BF16) {
+      } else if (rows()) {
         void* dz = ws + c.L.dz;
         LAUNCH(K_EDGE_BWD, launch_edge_bwd_rows(tl, a1_l(k, l), ebar, l < m - 1 ? 1 : 0, ebar, aggbar, W(oe, M.p_edge[l]),
                                     eps, zbar, dz, R, slots(), pt, &nb, s));
@@ -582,7 +587,7 @@ struct Run {
       if ((rc = reduce(nb, (int64_t)D * D, D, D, grad, oe.W1 + 2 * D, 3 * D)) != MGN_OK) return rc;
     }
     if (m > 0) {
-      if (prec == MGN_BF16)
+      if (rows())
         LAUNCH(K_EDGE_ENC_BWD, launch_edge_enc_bwd_rows(E, efeat, ebar, W(M.enc_edge, M.p_enc_edge), eps, pt, &nb, s));
       else
         LAUNCH(K_EDGE_ENC_BWD, launch_edge_enc_bwd(prec, D, E, efeat, (float*)ebar, W(M.enc_edge, M.p_enc_edge), eps, pt, &nb, s));
@@ -600,8 +605,6 @@ int check_cfg(const mgn_config* cfg) {
       cfg->mlp_layers != 2)
     return fail(MGN_ERR_SHAPE,
                 "unsupported config (node_in 8, edge_in 4, latent 128 or 150, out 4, mlp_layers 2 are supported)");
-  if (cfg->latent == 150 && cfg->precision != MGN_FP32)
-    return fail(MGN_ERR_SHAPE, "latent 150 runs in fp32 only");
   if (cfg->mp_steps < 0 || cfg->mp_steps > 4096) return fail(MGN_ERR_ARG, "mp_steps out of range");
   if (cfg->precision != MGN_FP32 && cfg->precision != MGN_BF16) return fail(MGN_ERR_ARG, "unknown precision");
   if (!(cfg->ln_eps > 0.f)) return fail(MGN_ERR_ARG, "ln_eps must be > 0");

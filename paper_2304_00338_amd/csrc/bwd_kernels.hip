@@ -530,7 +530,9 @@ hipError_t launch_decoder_bwd(int prec, int lat, int64_t N, const float* h, cons
   *nblocks = g;
   if (!g) return hipSuccess;
   if (prec == MGN_BF16) {
-    hipLaunchKernelGGL((k_decoder_bwd<MGN_BF16, 128>), dim3(g), dim3(NT), 0, s, N, h, gout, w, hbar, part);
+#define F(LD) hipLaunchKernelGGL((k_decoder_bwd<MGN_BF16, LD>), dim3(g), dim3(LD * 4), 0, s, N, h, gout, w, hbar, part)
+    MGN_BY_WIDTH(lat, F);
+#undef F
   } else {
 #define F(LD) hipLaunchKernelGGL((k_decoder_bwd<MGN_FP32, LD>), dim3(g), dim3(LD * 4), 0, s, N, h, gout, w, hbar, part)
     MGN_BY_WIDTH(lat, F);
@@ -546,8 +548,11 @@ hipError_t launch_node_bwd(int prec, int lat, int64_t N, const float* h, const f
   *nblocks = g;
   if (!g) return hipSuccess;
   if (prec == MGN_BF16) {
-    hipLaunchKernelGGL((k_node_bwd<MGN_BF16, 128>), dim3(g), dim3(NT), 0, s, N, h, agg, hbar_in, w, eps, hbar_part,
-                       aggbar, part);
+#define F(LD)                                                                                                         \
+  hipLaunchKernelGGL((k_node_bwd<MGN_BF16, LD>), dim3(g), dim3(LD * 4), 0, s, N, h, agg, hbar_in, w, eps, hbar_part, \
+                     aggbar, part)
+    MGN_BY_WIDTH(lat, F);
+#undef F
   } else {
 #define F(LD)                                                                                                         \
   hipLaunchKernelGGL((k_node_bwd<MGN_FP32, LD>), dim3(g), dim3(LD * 4), 0, s, N, h, agg, hbar_in, w, eps, hbar_part, \
@@ -565,8 +570,11 @@ hipError_t launch_node_srcsum(int prec, int lat, int64_t N, const int32_t* rowpt
   *nblocks = g;
   if (!g) return hipSuccess;
   if (prec == MGN_BF16) {
-    hipLaunchKernelGGL((k_node_srcsum<MGN_BF16, 128>), dim3(g), dim3(NT), 0, s, N, rowptr, rev, (const bf16*)zbar, R,
-                       h, hbar_part, w, hbar_out, part);
+#define F(LD)                                                                                                      \
+  hipLaunchKernelGGL((k_node_srcsum<MGN_BF16, LD>), dim3(g), dim3(LD * 4), 0, s, N, rowptr, rev, (const bf16*)zbar, \
+                     R, h, hbar_part, w, hbar_out, part)
+    MGN_BY_WIDTH(lat, F);
+#undef F
   } else {
 #define F(LD)                                                                                                       \
   hipLaunchKernelGGL((k_node_srcsum<MGN_FP32, LD>), dim3(g), dim3(LD * 4), 0, s, N, rowptr, rev, (const float*)zbar, \
@@ -583,8 +591,11 @@ hipError_t launch_edge_enc_bwd(int prec, int lat, int64_t E, const float* efeat,
   *nblocks = g;
   if (!g) return hipSuccess;
   if (prec == MGN_BF16) {
-    hipLaunchKernelGGL((k_enc_bwd<MGN_BF16, 128, 4>), dim3(g), dim3(NT), 0, s, E, efeat, ebar, w, eps,
-                       (float*)nullptr, part);
+#define F(LD)                                                                                                      \
+  hipLaunchKernelGGL((k_enc_bwd<MGN_BF16, LD, 4>), dim3(g), dim3(LD * 4), 0, s, E, efeat, ebar, w, eps,            \
+                     (float*)nullptr, part)
+    MGN_BY_WIDTH(lat, F);
+#undef F
   } else {
 #define F(LD)                                                                                                      \
   hipLaunchKernelGGL((k_enc_bwd<MGN_FP32, LD, 4>), dim3(g), dim3(LD * 4), 0, s, E, efeat, ebar, w, eps,            \
@@ -601,7 +612,10 @@ hipError_t launch_node_enc_bwd(int prec, int lat, int64_t N, const float* node_i
   *nblocks = g;
   if (!g) return hipSuccess;
   if (prec == MGN_BF16) {
-    hipLaunchKernelGGL((k_enc_bwd<MGN_BF16, 128, 8>), dim3(g), dim3(NT), 0, s, N, node_in, hbar, w, eps, gin, part);
+#define F(LD) \
+  hipLaunchKernelGGL((k_enc_bwd<MGN_BF16, LD, 8>), dim3(g), dim3(LD * 4), 0, s, N, node_in, hbar, w, eps, gin, part)
+    MGN_BY_WIDTH(lat, F);
+#undef F
   } else {
 #define F(LD) \
   hipLaunchKernelGGL((k_enc_bwd<MGN_FP32, LD, 8>), dim3(g), dim3(LD * 4), 0, s, N, node_in, hbar, w, eps, gin, part)

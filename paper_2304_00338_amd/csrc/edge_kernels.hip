@@ -369,7 +369,9 @@ k_edge_bwd(EdgeTiles tl, const typename Tr<PREC>::T* __restrict__ e, const float
   constexpr int D = LD;
   [[maybe_unused]] constexpr int NW = Width<LD>::NW, NT = Width<LD>::NT;
   constexpr int NCB = D / 16;
-  constexpr bool TX = PREC == MGN_BF16;  // feature-major a1 copy, LDS weights
+  // feature-major a1 copy and LDS copies of the transposed weights (bf16 at
+  // width 128; at 160 the two weight copies would not fit in LDS)
+  constexpr bool TX = PREC == MGN_BF16 && LD == 128;
   constexpr int LDT = D + P::PAD;
   constexpr int LDM = D + 4;
   constexpr int LDTT = TM + 8;
@@ -681,14 +683,21 @@ static constexpr int kWgradBlocks = 512;
 hipError_t launch_edge_fwd(int prec, int lat, const EdgeTiles& t, const void* e_in, void* e_out, int write_e,
                            const void* Pn, const MlpW& w, float eps, float* agg, float* slots, void* a1_out,
                            hipStream_t s) {
-  if (prec == MGN_BF16) return launch_edge_fwd_rows(t, e_in, e_out, write_e, Pn, w, eps, agg, slots, a1_out, s);
+  // bf16 at width 128: the row-layout kernel
+  if (prec == MGN_BF16 && lat == 128)
+    return launch_edge_fwd_rows(t, e_in, e_out, write_e, Pn, w, eps, agg, slots, a1_out, s);
   const int g = grid_for(t.n_tiles, kEdgeFwdBlocks);
   if (!g) return hipSuccess;
+  if (prec == MGN_BF16) {
+    hipLaunchKernelGGL((k_edge_fwd<MGN_BF16, true, 160>), dim3(g), dim3(640), 0, s, t, (const bf16*)e_in,
+                       (bf16*)e_out, write_e, (const bf16*)Pn, w, eps, agg, slots);
+  } else {
 #define F(LD)                                                                                                     \
   hipLaunchKernelGGL((k_edge_fwd<MGN_FP32, false, LD>), dim3(g), dim3(LD * 4), 0, s, t, (const float*)e_in,       \
                      (float*)e_out, write_e, (const float*)Pn, w, eps, agg, slots)
-  MGN_BY_WIDTH(lat, F);
+    MGN_BY_WIDTH(lat, F);
 #undef F
+  }
   return hipGetLastError();
 }
 
@@ -699,8 +708,11 @@ hipError_t launch_edge_bwd(int prec, int lat, const EdgeTiles& t, const void* e,
   *nblocks = g;
   if (!g) return hipSuccess;
   if (prec == MGN_BF16) {
-    hipLaunchKernelGGL((k_edge_bwd<MGN_BF16, true, 128>), dim3(g), dim3(NT), 0, s, t, (const bf16*)e, ebar_in,
-                       have_ebar, ebar_out, (const bf16*)Pn, aggbar, w, eps, (bf16*)zbar, R, slots, part);
+#define F(LD)                                                                                                    \
+  hipLaunchKernelGGL((k_edge_bwd<MGN_BF16, true, LD>), dim3(g), dim3(LD * 4), 0, s, t, (const bf16*)e, ebar_in, \
+                     have_ebar, ebar_out, (const bf16*)Pn, aggbar, w, eps, (bf16*)zbar, R, slots, part)
+    MGN_BY_WIDTH(lat, F);
+#undef F
   } else {
 #define F(LD)                                                                                                      \
   hipLaunchKernelGGL((k_edge_bwd<MGN_FP32, false, LD>), dim3(g), dim3(LD * 4), 0, s, t, (const float*)e, ebar_in,  \
@@ -717,7 +729,11 @@ hipError_t launch_wgrad(int prec, int lat, int64_t M, const void* Gm, const void
   *nblocks = g;
   if (!g) return hipSuccess;
   if (prec == MGN_BF16) {
-    hipLaunchKernelGGL((k_wgrad<MGN_BF16, 128>), dim3(g), dim3(NT), 0, s, M, (const bf16*)Gm, (const bf16*)Xm, part);
+#define F(LD)                                                                                                    \
+  hipLaunchKernelGGL((k_wgrad<MGN_BF16, LD>), dim3(g), dim3(LD * 4), 0, s, M, (const bf16*)Gm, (const bf16*)Xm, \
+                     part)
+    MGN_BY_WIDTH(lat, F);
+#undef F
   } else {
 #define F(LD)                                                                                                     \
   hipLaunchKernelGGL((k_wgrad<MGN_FP32, LD>), dim3(g), dim3(LD * 4), 0, s, M, (const float*)Gm, (const float*)Xm, \

@@ -322,12 +322,15 @@ hipError_t launch_node_enc(int prec, int lat, int64_t N, const float* x, const M
   if (!g) return hipSuccess;
   const MlpW nn = nx ? *nx : w;
   if (prec == MGN_BF16) {
-    if (nx)
-      hipLaunchKernelGGL((k_node_enc<MGN_BF16, 128, true>), dim3(g), dim3(NT), 0, s, N, x, w, nn, eps, h_out,
-                         (bf16*)P_out);
-    else
-      hipLaunchKernelGGL((k_node_enc<MGN_BF16, 128, false>), dim3(g), dim3(NT), 0, s, N, x, w, nn, eps, h_out,
-                         (bf16*)P_out);
+#define F(LD)                                                                                                        \
+  if (nx)                                                                                                            \
+    hipLaunchKernelGGL((k_node_enc<MGN_BF16, LD, true>), dim3(g), dim3(LD * 4), 0, s, N, x, w, nn, eps, h_out,       \
+                       (bf16*)P_out);                                                                                \
+  else                                                                                                               \
+    hipLaunchKernelGGL((k_node_enc<MGN_BF16, LD, false>), dim3(g), dim3(LD * 4), 0, s, N, x, w, nn, eps, h_out,      \
+                       (bf16*)P_out)
+    MGN_BY_WIDTH(lat, F);
+#undef F
   } else {
 #define F(LD)                                                                                                        \
   if (nx)                                                                                                            \
@@ -347,7 +350,9 @@ hipError_t launch_edge_enc(int prec, int lat, int64_t E, const float* f, const M
   const int g = grid_for((E + TM - 1) / TM, kFwdBlocks);
   if (!g) return hipSuccess;
   if (prec == MGN_BF16) {
-    hipLaunchKernelGGL((k_edge_enc<MGN_BF16, 128>), dim3(g), dim3(NT), 0, s, E, f, w, eps, (bf16*)e_out);
+#define F(LD) hipLaunchKernelGGL((k_edge_enc<MGN_BF16, LD>), dim3(g), dim3(LD * 4), 0, s, E, f, w, eps, (bf16*)e_out)
+    MGN_BY_WIDTH(lat, F);
+#undef F
   } else {
 #define F(LD) hipLaunchKernelGGL((k_edge_enc<MGN_FP32, LD>), dim3(g), dim3(LD * 4), 0, s, E, f, w, eps, (float*)e_out)
     MGN_BY_WIDTH(lat, F);
@@ -371,12 +376,15 @@ hipError_t launch_node_fwd(int prec, int lat, int64_t N, const float* h_in, cons
   if (!g) return hipSuccess;
   const MlpW nn = nx ? *nx : w;
   if (prec == MGN_BF16) {
-    if (nx)
-      hipLaunchKernelGGL((k_node_fwd<MGN_BF16, 128, true>), dim3(g), dim3(NT), 0, s, N, h_in, agg, w, nn, eps, h_out,
-                         (bf16*)P_out);
-    else
-      hipLaunchKernelGGL((k_node_fwd<MGN_BF16, 128, false>), dim3(g), dim3(NT), 0, s, N, h_in, agg, w, nn, eps, h_out,
-                         (bf16*)P_out);
+#define F(LD)                                                                                                        \
+  if (nx)                                                                                                            \
+    hipLaunchKernelGGL((k_node_fwd<MGN_BF16, LD, true>), dim3(g), dim3(LD * 4), 0, s, N, h_in, agg, w, nn, eps,      \
+                       h_out, (bf16*)P_out);                                                                         \
+  else                                                                                                               \
+    hipLaunchKernelGGL((k_node_fwd<MGN_BF16, LD, false>), dim3(g), dim3(LD * 4), 0, s, N, h_in, agg, w, nn, eps,     \
+                       h_out, (bf16*)P_out)
+    MGN_BY_WIDTH(lat, F);
+#undef F
   } else {
 #define F(LD)                                                                                                        \
   if (nx)                                                                                                            \
@@ -395,7 +403,9 @@ hipError_t launch_decoder(int prec, int lat, int64_t N, const float* h, const Ml
   const int g = grid_for((N + TM - 1) / TM, kFwdBlocks);
   if (!g) return hipSuccess;
   if (prec == MGN_BF16) {
-    hipLaunchKernelGGL((k_decoder<MGN_BF16, 128>), dim3(g), dim3(NT), 0, s, N, h, w, out);
+#define F(LD) hipLaunchKernelGGL((k_decoder<MGN_BF16, LD>), dim3(g), dim3(LD * 4), 0, s, N, h, w, out)
+    MGN_BY_WIDTH(lat, F);
+#undef F
   } else {
 #define F(LD) hipLaunchKernelGGL((k_decoder<MGN_FP32, LD>), dim3(g), dim3(LD * 4), 0, s, N, h, w, out)
     MGN_BY_WIDTH(lat, F);

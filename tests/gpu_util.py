@@ -67,15 +67,16 @@ def kink_resolved(tape, w, gp, gi, tau=KINK_TAU, max_kinks=48):
 def bf16_grad_tols(pb, trials=2, scale=2.0):
     """Per-segment tolerances {name: tol, 'gin': tol} for bf16 gradients at
     an ordinary point (see BF16_GRAD_TOL).  Oracle-only computation."""
-    _, tape = O.mgn_forward(pb.go, pb.params, pb.node_in, pb.go.efeat, pb.m, keep=True)
+    lat = getattr(pb, "latent", 128)
+    _, tape = O.mgn_forward(pb.go, pb.params, pb.node_in, pb.go.efeat, pb.m, latent=lat, keep=True)
     g0, gi0 = O.mgn_backward(tape, pb.w)
     worst = {}
     for t in range(trials):
         xi = np.random.default_rng(1000 + t).choice([-1.0, 1.0], size=pb.params.shape)
         _, t1 = O.mgn_forward(pb.go, pb.params * (1 + 2.0 ** -8 * xi), pb.node_in, pb.go.efeat, pb.m,
-                              keep=True)
+                              latent=lat, keep=True)
         g1, gi1 = O.mgn_backward(t1, pb.w)
-        for name, a, b in segments(pb.m):
+        for name, a, b in segments(pb.m, lat):
             worst[name] = max(worst.get(name, 0.0), rel_l2(g1[a:b], g0[a:b]))
         worst["gin"] = max(worst.get("gin", 0.0), rel_l2(gi1, gi0))
     return {k: max(BF16_GRAD_TOL, scale * v) for k, v in worst.items()}

@@ -182,8 +182,8 @@ def test_ctx_planning_and_errors():
         mgn.Context(15, 10, 10, "fp32", max_stages=5, allocate=False)
     assert e.value.code == mgn.ERR_ARG
     ws, h = ctypes.c_size_t(), ctypes.c_void_p()
-    for lat, prec in ((140, "fp32"), (256, "fp32"), (150, "bf16")):
-        cfg = mgn.config(3, prec, latent=lat)  # latent 150 runs in fp32 only
+    for lat, prec in ((140, "fp32"), (256, "bf16"), (160, "fp32")):
+        cfg = mgn.config(3, prec, latent=lat)  # latents 128 and 150 only
         rc = mgn.lib().mgn_ctx_create(ctypes.byref(cfg), 10, 10, 1, 0, ctypes.byref(ws), ctypes.byref(h))
         assert rc == mgn.ERR_SHAPE, (lat, prec)
     # latent 150 (the 3D model, kernels padded to 160): parameter count in the
