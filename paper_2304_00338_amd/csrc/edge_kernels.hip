@@ -20,8 +20,19 @@
 namespace mgn {
 namespace dev {
 
+// A zero the compiler cannot see through: weight-fragment reads offset by a
+// fresh one per tile are not loop-invariant, so they are not hoisted out of
+// the tile loop into registers (which spills at width 160, where a 10-wave
+// block leaves a wave 168 registers).
+__device__ __forceinline__ int tile_opaque_zero() {
+  int z = 0;
+  asm volatile("" : "+v"(z));
+  return z;
+}
+
 // B fragments of one 16-column weight slice with K = LD (the kernel width):
-// B[k][n] = W[n0 + n][kofs + k].
+// B[k][n] = W[n0 + n][kofs + k].  refresh() starts a tile (no-op for
+// register-resident fragments).
 template <int PREC, bool WREG, int LD>
 struct WSlice;
 
@@ -35,6 +46,7 @@ struct WSlice<PREC, true, LD> {
     for (int kk = 0; kk < NK; ++kk) f[kk] = P::ldb(W, ldw, n0, kofs + kk * P::KS, i, q);
   }
   __device__ __forceinline__ typename P::Frag get(int kk) const { return f[kk]; }
+  __device__ __forceinline__ void refresh() {}
 };
 
 template <int PREC, int LD>
@@ -42,7 +54,7 @@ struct WSlice<PREC, false, LD> {
   typedef Tr<PREC> P;
   static constexpr int NK = LD / P::KS;
   const typename P::T* W;
-  int ldw, n0, kofs, i, q;
+  int ldw, n0, kofs, i, q, z = 0;
   __device__ __forceinline__ void init(const typename P::T* W_, int ldw_, int n0_, int kofs_, int i_, int q_) {
     W = W_;
     ldw = ldw_;
@@ -51,7 +63,10 @@ struct WSlice<PREC, false, LD> {
     i = i_;
     q = q_;
   }
-  __device__ __forceinline__ typename P::Frag get(int kk) const { return P::ldb(W, ldw, n0, kofs + kk * P::KS, i, q); }
+  __device__ __forceinline__ typename P::Frag get(int kk) const {
+    return P::ldb(W, ldw, n0, kofs + z + kk * P::KS, i, q);
+  }
+  __device__ __forceinline__ void refresh() { z = tile_opaque_zero(); }
 };
 
 // B fragments read from an LDS copy of a [LD][LD] matrix with padded rows
@@ -62,14 +77,15 @@ struct WSliceL {
   static constexpr int NK = LD / P::KS;
   static constexpr int LDW = LD + P::PAD;
   const typename P::T* W;
-  int n0, i, q;
+  int n0, i, q, z = 0;
   __device__ __forceinline__ void init(const typename P::T* W_, int n0_, int i_, int q_) {
     W = W_;
     n0 = n0_;
     i = i_;
     q = q_;
   }
-  __device__ __forceinline__ typename P::Frag get(int kk) const { return P::ldb(W, LDW, n0, kk * P::KS, i, q); }
+  __device__ __forceinline__ typename P::Frag get(int kk) const { return P::ldb(W, LDW, n0, z + kk * P::KS, i, q); }
+  __device__ __forceinline__ void refresh() { z = tile_opaque_zero(); }
 };
 
 // Copy the first LD rows of a row-major [.][LD] global matrix into LDS with
@@ -278,6 +294,10 @@ k_edge_fwd(EdgeTiles tl, const typename Tr<PREC>::T* __restrict__ e_in,
   issue(d0, sSR[0]);
   int buf = 0;
   for (; t < NTL; t += G) {
+    if constexpr (LD == 160) {
+      w1.refresh();
+      w2.refresh();
+    }
     // ---- commit the prefetched streams of tile t to LDS
 #pragma unroll
     for (int k = 0; k < RT::CPT; ++k) {
@@ -369,9 +389,11 @@ k_edge_bwd(EdgeTiles tl, const typename Tr<PREC>::T* __restrict__ e, const float
   constexpr int D = LD;
   [[maybe_unused]] constexpr int NW = Width<LD>::NW, NT = Width<LD>::NT;
   constexpr int NCB = D / 16;
-  // feature-major a1 copy and LDS copies of the transposed weights (bf16 at
-  // width 128; at 160 the two weight copies would not fit in LDS)
-  constexpr bool TX = PREC == MGN_BF16 && LD == 128;
+  // bf16: feature-major a1 copy (dW2 operands) and an LDS copy of W2^T; the
+  // LDS copy of W1e^T too at width 128 (at 160 both copies would not fit in
+  // LDS, and W1e^T is read from L2)
+  constexpr bool TX = PREC == MGN_BF16;
+  constexpr bool TX1 = TX && LD == 128;
   constexpr int LDT = D + P::PAD;
   constexpr int LDM = D + 4;
   constexpr int LDTT = TM + 8;
@@ -382,7 +404,7 @@ k_edge_bwd(EdgeTiles tl, const typename Tr<PREC>::T* __restrict__ e, const float
   __shared__ __align__(16) T sZ[TM * LDT];
   __shared__ __align__(16) bf16 sA1T[TX ? D * LDTT : 8];
   __shared__ __align__(16) T sW2t[TX ? D * LDT : 8];
-  __shared__ __align__(16) T sW1t[TX ? D * LDT : 8];
+  __shared__ __align__(16) T sW1t[TX1 ? D * LDT : 8];
   __shared__ LnScratch<NW> ln;
   __shared__ int2 sSR[2][TM];
 
@@ -398,10 +420,8 @@ k_edge_bwd(EdgeTiles tl, const typename Tr<PREC>::T* __restrict__ e, const float
   g1t.init((const T*)w.W1t, D, w8 * 16, 0, i, q);
   l2t.init(sW2t, w8 * 16, i, q);
   l1t.init(sW1t, w8 * 16, i, q);
-  if constexpr (TX) {
-    stage_weights<PREC, LD>(sW2t, (const T*)w.W2t, tid);
-    stage_weights<PREC, LD>(sW1t, (const T*)w.W1t, tid);
-  }
+  if constexpr (TX) stage_weights<PREC, LD>(sW2t, (const T*)w.W2t, tid);
+  if constexpr (TX1) stage_weights<PREC, LD>(sW1t, (const T*)w.W1t, tid);
   f32x4 dW2[NCB];
 #pragma unroll
   for (int cb = 0; cb < NCB; ++cb) dW2[cb] = zero4();
@@ -446,6 +466,13 @@ k_edge_bwd(EdgeTiles tl, const typename Tr<PREC>::T* __restrict__ e, const float
   if (t < NTL) issue(d0, sSR[0]);
   int buf = 0;
   for (; t < NTL; t += G) {
+    if constexpr (LD == 160) {
+      w1.refresh();
+      w2.refresh();
+      g1t.refresh();
+      g2t.refresh();
+      l2t.refresh();
+    }
     // ---- commit tile t
 #pragma unroll
     for (int k = 0; k < RT::CPT; ++k) {
@@ -555,7 +582,7 @@ k_edge_bwd(EdgeTiles tl, const typename Tr<PREC>::T* __restrict__ e, const float
     // ---- back through W1e: ebar_out = ebar_in + W1e^T zbar
 #pragma unroll
     for (int rb = 0; rb < NRB; ++rb) acc[rb] = eb_in[rb];
-    if constexpr (TX)
+    if constexpr (TX1)
       gemm_w<PREC>(acc, sZ, LDT, l1t, i, q);
     else
       gemm_w<PREC>(acc, sZ, LDT, g1t, i, q);
@@ -709,7 +736,7 @@ hipError_t launch_edge_bwd(int prec, int lat, const EdgeTiles& t, const void* e,
   if (!g) return hipSuccess;
   if (prec == MGN_BF16) {
 #define F(LD)                                                                                                    \
-  hipLaunchKernelGGL((k_edge_bwd<MGN_BF16, true, LD>), dim3(g), dim3(LD * 4), 0, s, t, (const bf16*)e, ebar_in, \
+  hipLaunchKernelGGL((k_edge_bwd<MGN_BF16, LD == 128, LD>), dim3(g), dim3(LD * 4), 0, s, t, (const bf16*)e, ebar_in, \
                      have_ebar, ebar_out, (const bf16*)Pn, aggbar, w, eps, (bf16*)zbar, R, slots, part)
     MGN_BY_WIDTH(lat, F);
 #undef F

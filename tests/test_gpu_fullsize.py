@@ -14,6 +14,9 @@
 * C4 patch-decomposed: the same rollout computed slab patch by slab patch
   (16 z-slabs, 15-hop ghost zones, ghost rows refreshed from their owners
   every step) equals the whole-mesh rollout bitwise.
+* The paper's 3D training shape (latent 150, 3 MP steps, Heun 2, 6-hop ghost
+  zones of the 12 x 12 x 15 split of the 146^3 mesh): one training step on a
+  full-size sampled patch against the oracle's step on the same patch.
 * C5: RK4 / midpoint / Euler on the C2 mesh, fp32 and bf16: the integrator
   call equals the explicit composition of its stage MGN calls, forward and
   backward (stage chaining of Sec. 2.3 at full size; the stage arithmetic
@@ -218,3 +221,78 @@ def test_c5_stage_composition(c2, scheme, prec):
     e2 = rel_l2(gy.cpu().numpy(), gy_m.cpu().numpy())
     print(f"C5 {scheme} {prec}: params {e1:.2e}, y {e2:.2e}", flush=True)
     assert e1 < tol and e2 < tol
+
+
+def _paper_3d_patches(M, g, k, n):
+    """The first n of the subdomains the bench samples from the paper's 3D
+    split (12 x 12 x 15 equal parts, App. C), each with a k-hop ghost zone:
+    the library's patches of the whole mesh, and the oracle's patches built
+    from the grid box around each subdomain (its k-hop zone lies within
+    L-infinity distance k of the subdomain, and every edge among those nodes
+    belongs to a cell within distance k + 1), with global node ids."""
+    from fullsize_util import box_submesh
+    part = mgn.partition(M["pos"], (12, 12, 15))
+    ids = np.random.default_rng(0).choice(int(part.max()) + 1, 32, replace=False)[:n]
+    gi = synth.grid_index(BIG)
+    hp, opatches = [], []
+    for p in ids:
+        hp.append(mgn.extract_patch(g, part, int(p), k))
+        sub = gi[part == p]
+        lo, hi = sub.min(0), sub.max(0)
+        c, r = (lo + hi) // 2, int((hi - lo).max() // 2 + 1) + k + 1
+        gids, cells = box_submesh(BIG, c, r)
+        go = O.build_graph(cells, M["pos"][gids])
+        pt = O.extract_patch(go, part[gids], int(p), k)
+        pt.node_l2g = gids[pt.node_l2g]
+        opatches.append(pt)
+        mp = hp[-1].patch_maps()
+        assert np.array_equal(mp["node_l2g"], pt.node_l2g) and hp[-1].n_edges == pt.n_edges
+    return hp, opatches
+
+
+P3D_M, P3D_K, P3D_SEED = 3, 6, 41
+
+
+@pytest.fixture(scope="module")
+def paper_3d(big):
+    """One of the bench's sampled patches of the paper's 3D split (8,467
+    nodes, 109,796 edges) and the oracle's training step on it (about a
+    minute of host time)."""
+    M, g, _ = big
+    hp, opatches = _paper_3d_patches(M, g, P3D_K, 1)
+    print(f"paper 3D patch: {hp[0].n_nodes} nodes, {hp[0].n_edges} edges; oracle step ...", flush=True)
+    P = synth.smooth_params(P3D_M, P3D_SEED, 150)
+    tgt = synth.next_states(M["states"], P3D_SEED)
+    nz = synth.standard_noise(g.n_nodes, P3D_SEED)
+    z = np.zeros(P.size)
+    _, _, _, rloss, rgrad = O.train_step(opatches, P, "heun2", M["onehot"], M["states"], tgt, nz, P3D_M, z, z, 1,
+                                         latent=150)
+    print("oracle step done", flush=True)
+    return hp, P, tgt, nz, rloss, rgrad
+
+
+@pytest.mark.parametrize("prec", ["fp32", "bf16"])
+def test_paper_3d_train_step(big, paper_3d, prec):
+    """The paper's 3D training configuration (App. C: latent 150, 3 MP steps;
+    Heun 2; 6-hop ghost zones of the 12 x 12 x 15 split of the 146^3 mesh) at
+    full patch size, in the launch configuration the bench times: one training
+    step on one of the bench's sampled patches against the oracle's step on
+    the same patch at a smooth point (loss, gradient, Adam update)."""
+    M, g, _ = big
+    hp, P, tgt, nz, rloss, rgrad = paper_3d
+    patches = [mgn.DevicePatch(p) for p in hp]
+    ctx = mgn.Context(P3D_M, max(p.n_nodes for p in hp), max(p.n_edges for p in hp), prec, max_stages=2, save=True,
+                      latent=150)
+    params = d(P)
+    grad, mm, vv = torch.zeros_like(params), torch.zeros_like(params), torch.zeros_like(params)
+    loss = mgn.mgn_train_step(ctx, patches, params, "heun2", d(M["onehot"]), d(M["states"]), d(tgt), d(nz), grad,
+                              mm, vv, mgn.Adam(), 1)
+    z = np.zeros(P.size)
+    tol = FP32_TOL if prec == "fp32" else BF16_TOL
+    assert abs(loss.item() - rloss) < tol * abs(rloss), (loss.item(), rloss)
+    gg = grad.cpu().numpy()
+    assert rel_l2(gg, rgrad) < tol, rel_l2(gg, rgrad)
+    rp, _, _ = O.adam_update(P.astype(np.float64), gg.astype(np.float64), z, z, 1, 1e-3)
+    pg = params.cpu().numpy().astype(np.float64)
+    bound = np.spacing(np.abs(rp).astype(np.float32)).astype(np.float64) + 1e-5 * np.abs(rp - P).max()
+    assert np.all(np.abs(pg - rp) <= bound)
