@@ -331,7 +331,9 @@ def paper_3d_train(S, args, n_patches=32, k=6, m=3, reps=3):
     batch of 32 patches), ghost depth k = 2m so that Heun's two stages are
     exact on each patch, latent 150, m = 3 MP steps; one training step =
     input noise, one H2 step fwd+bwd per patch, masked MSE, gradients summed
-    over the patches, Adam.  Timed in fp32 and in bf16."""
+    over the patches, Adam.  The 32 patches run as one disjoint-union graph
+    (one launch per kernel); the same step over the list of patches (one
+    launch per kernel and patch) is timed beside it."""
     import torch
     import synth
     from paper_2304_00338_amd import mgn
@@ -339,39 +341,47 @@ def paper_3d_train(S, args, n_patches=32, k=6, m=3, reps=3):
     part = mgn.partition(M["pos"], (12, 12, 15))
     ids = np.random.default_rng(0).choice(int(part.max()) + 1, n_patches, replace=False)
     hp = [mgn.extract_patch(g, part, int(p), k) for p in ids]
-    patches = [mgn.DevicePatch(p) for p in hp]
+    un = mgn.patch_union(hp)
+    batches = {"union": [mgn.DevicePatch(un)], "list": [mgn.DevicePatch(p) for p in hp]}
     dev = lambda a: torch.from_numpy(np.ascontiguousarray(a, np.float32)).cuda()
     st, y = dev(M["onehot"]), dev(M["states"])
     tgt, nz = dev(synth.next_states(M["states"], 1)), dev(synth.standard_noise(M["states"].shape[0], 1))
-    pe = sum(p.n_edges for p in hp)
-    res = {"workload": (f"{n_patches} of the 12x12x15 subdomains of the {args.grid}^3 mesh per step, "
-                        f"{k}-hop ghost zones, latent 150, {m} MP steps, Heun 2 fwd+bwd, noise, masked MSE, Adam"),
-           "patch_nodes": sum(p.n_nodes for p in hp), "patch_edges": pe,
-           "interior_nodes": int(sum(p.patch_maps()["n_interior"] for p in hp))}
-    for prec in ("fp32", "bf16"):
-        params = dev(synth.xavier_params(m, 1, 150))
-        ctx = mgn.Context(m, max(p.n_nodes for p in patches), max(p.n_edges for p in patches), prec,
-                          max_stages=2, save=True, latent=150)
-        grad, mm, vv = torch.zeros_like(params), torch.zeros_like(params), torch.zeros_like(params)
-        adam = mgn.Adam()
-        loss = mgn.mgn_train_step(ctx, patches, params, "heun2", st, y, tgt, nz, grad, mm, vv, adam, 1)
-        torch.cuda.synchronize()
-        mgn.mgn_profile_enable(ctx, True)
-        mgn.mgn_profile_collect(ctx)
-        t0 = time.perf_counter()
-        for it in range(2, 2 + reps):
-            loss = mgn.mgn_train_step(ctx, patches, params, "heun2", st, y, tgt, nz, grad, mm, vv, adam, it)
-        torch.cuda.synchronize()
-        dt = (time.perf_counter() - t0) / reps
-        prof = mgn.mgn_profile_collect(ctx)
-        mgn.mgn_profile_enable(ctx, False)
-        res[prec] = {"ms_per_step": round(dt * 1e3, 3), "steps_per_s": round(1.0 / dt, 3),
-                     "mp_edges_per_s_fwdbwd": round(pe * m * 2 / dt, 1),
-                     "kernel_ms_per_step": {kk: round(v[0] / reps, 3)
-                                            for kk, v in sorted(prof.items(), key=lambda x: -x[1][0])},
-                     "loss_finite": bool(np.isfinite(loss.item()))}
-        del ctx
-    del patches
+    pe = un.n_edges
+    res = {"workload": (f"{n_patches} of the 12x12x15 subdomains of the {args.grid}^3 mesh per step as one "
+                        f"disjoint-union graph, {k}-hop ghost zones, latent 150, {m} MP steps, Heun 2 fwd+bwd, "
+                        f"noise, masked MSE, Adam"),
+           "patch_nodes": un.n_nodes, "patch_edges": pe, "interior_nodes": int(un.patch_maps()["n_interior"])}
+    for prec in args.paper3d_precs.split(","):
+        r = {}
+        for mode in ("union", "list"):
+            patches = batches[mode]
+            params = dev(synth.xavier_params(m, 1, 150))
+            ctx = mgn.Context(m, max(p.n_nodes for p in patches), max(p.n_edges for p in patches), prec,
+                              max_stages=2, save=True, latent=150)
+            grad, mm, vv = torch.zeros_like(params), torch.zeros_like(params), torch.zeros_like(params)
+            adam = mgn.Adam()
+            loss = mgn.mgn_train_step(ctx, patches, params, "heun2", st, y, tgt, nz, grad, mm, vv, adam, 1)
+            torch.cuda.synchronize()
+            mgn.mgn_profile_enable(ctx, True)
+            mgn.mgn_profile_collect(ctx)
+            t0 = time.perf_counter()
+            for it in range(2, 2 + reps):
+                loss = mgn.mgn_train_step(ctx, patches, params, "heun2", st, y, tgt, nz, grad, mm, vv, adam, it)
+            torch.cuda.synchronize()
+            dt = (time.perf_counter() - t0) / reps
+            prof = mgn.mgn_profile_collect(ctx)
+            mgn.mgn_profile_enable(ctx, False)
+            if mode == "union":
+                r.update({"ms_per_step": round(dt * 1e3, 3), "steps_per_s": round(1.0 / dt, 3),
+                          "mp_edges_per_s_fwdbwd": round(pe * m * 2 / dt, 1),
+                          "kernel_ms_per_step": {kk: round(v[0] / reps, 3)
+                                                 for kk, v in sorted(prof.items(), key=lambda x: -x[1][0])},
+                          "loss_finite": bool(np.isfinite(loss.item()))})
+            else:
+                r["ms_per_step_patch_list"] = round(dt * 1e3, 3)
+            del ctx
+        res[prec] = r
+    del batches
     return res
 
 
@@ -445,6 +455,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-c4", action="store_true", help="skip the whole-mesh rollout measurement")
     ap.add_argument("--no-paper3d", action="store_true", help="skip the latent-150 3D training-step measurement")
+    ap.add_argument("--paper3d-precs", default="fp32,bf16", help="precisions of the 3D training-step measurement")
     ap.add_argument("--paper3d-only", action="store_true",
                     help="only the latent-150 3D training-step measurement (one JSON object)")
     ap.add_argument("--copy-calibrate", action="store_true",

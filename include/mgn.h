@@ -162,6 +162,21 @@ int mgn_partition(const float* pos, int64_t n, int32_t dim,
 int mgn_extract_patch(const mgn_graph* g, const int32_t* part, int32_t p,
                       int32_t k, mgn_graph** patch);
 
+/* Disjoint union of n patches (of one graph): one patch-like graph whose
+ * parts are the given patches in order, with their nodes and edges renumbered
+ * consecutively (part j's local ids offset by the node / edge counts of parts
+ * 0..j-1) and no edge between parts.  One MGN call on the union computes, for
+ * every node, bitwise what the call on its own patch computes (rows interact
+ * only through their own in-segment sums), so a batch of patches (Sec. 2.2,
+ * condition 3: gradients summed over patches) runs as one launch per kernel;
+ * only the summation order of the weight gradients differs.  Maps: node_l2g
+ * and hop concatenated (a global node that is in several patches appears once
+ * per patch), edge_l2g concatenated, n_interior summed.  The union is owned
+ * by the caller (mgn_graph_destroy) and does not refer to the parts.
+ * Errors: ARG (null), STATE (a part is not a patch), SHAPE (2^31 nodes or
+ * edges). */
+int mgn_patch_union(const mgn_graph* const* patches, int32_t n, mgn_graph** out);
+
 /* Patch maps (host buffers; any pointer may be NULL): node_l2g[Np] global id
  * of each local node, hop[Np] ghost distance (0 = subdomain node),
  * interior[Np] 1 for subdomain nodes, edge_l2g[Ep] global edge id,

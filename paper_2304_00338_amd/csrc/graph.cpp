@@ -341,6 +341,60 @@ int mgn_extract_patch(const mgn_graph* h, const int32_t* part, int32_t p,
   return MGN_OK;
 }
 
+int mgn_patch_union(const mgn_graph* const* patches, int32_t n, mgn_graph** out) {
+  if (!out || n < 0 || (n > 0 && !patches)) return fail(MGN_ERR_ARG, "mgn_patch_union: bad arguments");
+  int64_t N = 0, E = 0;
+  for (int32_t j = 0; j < n; ++j) {
+    if (!patches[j]) return fail(MGN_ERR_ARG, "mgn_patch_union: patch %d is null", j);
+    if (!patches[j]->g.is_patch) return fail(MGN_ERR_STATE, "mgn_patch_union: graph %d is not a patch", j);
+    N += patches[j]->g.n_nodes;
+    E += patches[j]->g.n_edges;
+  }
+  if (N >= (int64_t)INT32_MAX || E >= (int64_t)INT32_MAX)
+    return fail(MGN_ERR_SHAPE, "mgn_patch_union: %lld nodes / %lld edges do not fit int32", (long long)N,
+                (long long)E);
+  mgn_graph* res = nullptr;
+  try {
+    res = new mgn_graph();
+    Graph& q = res->g;
+    q.is_patch = true;
+    q.n_nodes = N;
+    q.n_edges = E;
+    q.rowptr.reserve(N + 1);
+    q.rowptr.push_back(0);
+    q.senders.reserve(E);
+    q.receivers.reserve(E);
+    q.rev.reserve(E);
+    q.efeat.reserve((size_t)E * 4);
+    q.node_l2g.reserve(N);
+    q.hop.reserve(N);
+    q.edge_l2g.reserve(E);
+    int32_t nb = 0, eb = 0;  // node and edge offsets of the current part
+    for (int32_t j = 0; j < n; ++j) {
+      const Graph& g = patches[j]->g;
+      for (int64_t v = 0; v < g.n_nodes; ++v) q.rowptr.push_back(eb + g.rowptr[v + 1]);
+      for (int64_t e = 0; e < g.n_edges; ++e) {
+        q.senders.push_back(nb + g.senders[e]);
+        q.receivers.push_back(nb + g.receivers[e]);
+        q.rev.push_back(eb + g.rev[e]);
+      }
+      q.efeat.insert(q.efeat.end(), g.efeat.begin(), g.efeat.end());
+      q.node_l2g.insert(q.node_l2g.end(), g.node_l2g.begin(), g.node_l2g.end());
+      q.hop.insert(q.hop.end(), g.hop.begin(), g.hop.end());
+      q.edge_l2g.insert(q.edge_l2g.end(), g.edge_l2g.begin(), g.edge_l2g.end());
+      q.n_interior += g.n_interior;
+      nb += (int32_t)g.n_nodes;
+      eb += (int32_t)g.n_edges;
+    }
+    build_schedule(q);
+  } catch (const std::bad_alloc&) {
+    delete res;
+    return fail(MGN_ERR_NOMEM, "mgn_patch_union: out of host memory");
+  }
+  *out = res;
+  return MGN_OK;
+}
+
 int mgn_patch_copy_maps(const mgn_graph* h, int32_t* node_l2g, int32_t* hop,
                         uint8_t* interior, int64_t* edge_l2g,
                         int64_t* n_interior) {

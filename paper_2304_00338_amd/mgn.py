@@ -61,7 +61,7 @@ _lib = None
 EXPORTS = [
     "mgn_param_count", "mgn_build_graph", "mgn_graph_info", "mgn_graph_copy",
     "mgn_graph_schedule", "mgn_tile_edges", "mgn_tile_nodes", "mgn_graph_destroy",
-    "mgn_partition", "mgn_extract_patch", "mgn_patch_copy_maps", "mgn_ctx_create",
+    "mgn_partition", "mgn_extract_patch", "mgn_patch_union", "mgn_patch_copy_maps", "mgn_ctx_create",
     "mgn_ctx_destroy", "mgn_forward", "mgn_backward", "mgn_integrate_step",
     "mgn_pec_step", "mgn_patch_step", "mgn_adam_lr", "mgn_adam_step", "mgn_train_step", "mgn_scheme_stages", "mgn_version", "mgn_last_error", "mgn_profile_enable",
     "mgn_profile_collect",
@@ -88,6 +88,7 @@ def lib():
         "mgn_graph_destroy": (None, [vp]),
         "mgn_partition": (C.c_int, [vp, i64, i32, vp, vp]),
         "mgn_extract_patch": (C.c_int, [vp, vp, i32, i32, P(vp)]),
+        "mgn_patch_union": (C.c_int, [vp, i32, P(vp)]),
         "mgn_patch_copy_maps": (C.c_int, [vp, vp, vp, vp, vp, P(i64)]),
         "mgn_ctx_create": (C.c_int, [P(Config), i64, i64, i32, i32, P(C.c_size_t), P(vp)]),
         "mgn_ctx_destroy": (None, [vp]),
@@ -224,6 +225,14 @@ def extract_patch(g: Graph, part, p, k):
         raise MgnError(ERR_ARG, "part must have one id per node")
     out = C.c_void_p()
     _check(lib().mgn_extract_patch(g._h, pp, int(p), int(k), C.byref(out)))
+    return Graph(out.value, is_patch=True)
+
+
+def patch_union(patches):
+    """Disjoint union of patches as one patch-like graph (see include/mgn.h)."""
+    arr = (C.c_void_p * max(1, len(patches)))(*[p._h.value for p in patches])
+    out = C.c_void_p()
+    _check(lib().mgn_patch_union(arr, len(patches), C.byref(out)))
     return Graph(out.value, is_patch=True)
 
 

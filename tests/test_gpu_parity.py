@@ -282,6 +282,29 @@ def test_patch_rollout_equals_whole_mesh(prec, scheme, k):
             assert rel_l2(yp.cpu().numpy() - M["states"], ref - M["states"]) < tol
 
 
+@pytest.mark.parametrize("prec", ["fp32", "bf16"])
+def test_patch_union_step_bitwise(prec):
+    """A Heun patch step on the disjoint union of the three slab patches
+    equals the step over the patch list bitwise (one launch per kernel
+    instead of one per patch), for three steps."""
+    import synth
+    m, k, shape = 2, 4, (9, 8, 10)
+    M = synth.mesh(shape, 15)
+    g = mgn.build_graph(M["cells"], M["pos"])
+    part = synth.slab_part(shape, 3)
+    hp = [mgn.extract_patch(g, part, p, k) for p in range(3)]
+    u = mgn.patch_union(hp)
+    plist, pu = [mgn.DevicePatch(p) for p in hp], [mgn.DevicePatch(u)]
+    ctx = mgn.Context(m, u.n_nodes, u.n_edges, prec, max_stages=2)
+    d = lambda a: torch.from_numpy(np.ascontiguousarray(a, np.float32)).cuda()
+    st, params = d(M["onehot"]), d(synth.xavier_params(m, 15))
+    ya = yb = d(M["states"])
+    for t in range(3):
+        ya = mgn.mgn_patch_step(ctx, plist, params, "heun2", st, ya)
+        yb = mgn.mgn_patch_step(ctx, pu, params, "heun2", st, yb)
+        assert torch.equal(ya, yb), t
+
+
 def test_patch_rollout_thin_ghost_zone_differs():
     """Negative control: Heun's two stages need k >= 2m; with k = m the
     patch step differs from the whole-mesh step near the slab planes."""
@@ -323,8 +346,9 @@ def _assert_update(p_gpu, p_ref, p0):
     assert np.all(np.abs(p_gpu - p_ref) <= bound), np.abs(p_gpu - p_ref).max()
 
 
+@pytest.mark.parametrize("batched", [False, True])
 @pytest.mark.parametrize("prec", ["fp32", "bf16"])
-def test_train_step_matches_oracle(prec):
+def test_train_step_matches_oracle(prec, batched):
     """One patch-training step (noisy input, Heun step per patch, masked MSE,
     gradients summed over the patches, Adam) against the oracle at a smooth
     point: loss and gradient to the output tolerance, and the update equal
@@ -335,7 +359,9 @@ def test_train_step_matches_oracle(prec):
     g = mgn.build_graph(M["cells"], M["pos"])
     go = O.build_graph(M["cells"], M["pos"])
     part = synth.slab_part(shape, 2)
-    patches = [mgn.DevicePatch(mgn.extract_patch(g, part, p, 2 * m)) for p in range(2)]
+    hp = [mgn.extract_patch(g, part, p, 2 * m) for p in range(2)]
+    # batched: the two patches as one disjoint-union graph (one launch per kernel)
+    patches = [mgn.DevicePatch(mgn.patch_union(hp))] if batched else [mgn.DevicePatch(p) for p in hp]
     opatches = [O.extract_patch(go, part, p, 2 * m) for p in range(2)]
     P = synth.smooth_params(m, 32)
     tgt = synth.next_states(M["states"], 32)

@@ -216,3 +216,39 @@ def test_c3_patch_closed_form():
     dist = np.maximum(0, np.maximum(73 - z, z - 82))
     assert np.array_equal(mp["hop"], dist)
     check_schedule(pt)
+
+
+def test_patch_union_is_block_diagonal():
+    """mgn_patch_union: the parts' arrays concatenated with node / edge
+    offsets (senders, receivers, rev shifted, rowptr continued), features and
+    maps concatenated, no edge between parts, a valid tile schedule; errors
+    for non-patches and null parts."""
+    shape = (9, 8, 10)
+    M = synth.mesh(shape, 3)
+    g = mgn.build_graph(M["cells"], M["pos"])
+    part = synth.slab_part(shape, 3)
+    ps = [mgn.extract_patch(g, part, p, 2) for p in range(3)]
+    u = mgn.patch_union(ps)
+    a, mu = u.arrays(), u.patch_maps()
+    nb = eb = 0
+    for p in ps:
+        b, mp = p.arrays(), p.patch_maps()
+        n, e = p.n_nodes, p.n_edges
+        assert np.array_equal(a["rowptr"][nb:nb + n + 1], b["rowptr"] + eb)
+        for k in ("senders", "receivers"):
+            assert np.array_equal(a[k][eb:eb + e], b[k] + nb)
+        assert np.array_equal(a["rev"][eb:eb + e], b["rev"] + eb)
+        assert np.array_equal(a["efeat"][eb:eb + e], b["efeat"])
+        for k in ("node_l2g", "hop", "interior"):
+            assert np.array_equal(mu[k][nb:nb + n], mp[k])
+        assert np.array_equal(mu["edge_l2g"][eb:eb + e], mp["edge_l2g"])
+        nb, eb = nb + n, eb + e
+    assert (u.n_nodes, u.n_edges) == (nb, eb)
+    assert mu["n_interior"] == g.n_nodes  # the slabs partition the mesh
+    check_schedule(u)
+    assert mgn.patch_union([]).n_nodes == 0
+    with pytest.raises(mgn.MgnError) as e:
+        mgn.patch_union([ps[0], g])
+    assert e.value.code == mgn.ERR_STATE
+    rc = mgn.lib().mgn_patch_union(None, 2, ctypes.byref(ctypes.c_void_p()))
+    assert rc == mgn.ERR_ARG
