@@ -195,3 +195,75 @@ def test_train_step_latent150(prec):
     pg = params.cpu().numpy().astype(np.float64)
     bound = np.spacing(np.abs(rp).astype(np.float32)).astype(np.float64) + 1e-5 * np.abs(rp - P).max()
     assert np.all(np.abs(pg - rp) <= bound)
+
+
+def _oracle_check(pb, prec, res):
+    out, tape = O.mgn_forward(pb.go, pb.params, pb.node_in, pb.go.efeat, pb.m, latent=LAT, keep=True)
+    if prec == "fp32":
+        gp, gi, _ = kink_resolved(tape, pb.w, res[1], res[2])
+        check(res, (out, gp, gi), pb.m, FP32_TOL, FP32_TOL)
+    else:
+        check(res, (out, *O.mgn_backward(tape, pb.w)), pb.m, BF16_TOL, bf16_grad_tols(pb))
+
+
+@pytest.mark.parametrize("prec", PRECS)
+def test_long_segment_hub_latent150(prec):
+    """A centre node with 300 in-edges at width 160: its in-segment spans
+    several chunk tiles whose slot sums are added in chunk order."""
+    k = 300
+    ang = np.linspace(0, 2 * np.pi, k, endpoint=False)
+    rim = np.stack([np.cos(ang), np.sin(ang)], 1)
+    pos = np.concatenate([[[0.0, 0.0]], rim, 2 * rim]).astype(np.float32)
+    cells = np.array([[0, 1 + j, 1 + (j + 1) % k] for j in range(k)] +
+                     [[1 + j, 1 + k + j, 1 + (j + 1) % k] for j in range(k)])
+    rng = np.random.default_rng(31)
+    node_in = np.concatenate([np.eye(4)[rng.integers(0, 4, pos.shape[0])],
+                              rng.standard_normal((pos.shape[0], 4))], 1).astype(np.float32)
+    pb = Problem(None, 2, seed=31, cells=cells, pos=pos, node_in=node_in, latent=LAT).device()
+    assert pb.dg.n_long == 1
+    _oracle_check(pb, prec, run_fwd_bwd(pb, prec))
+
+
+def test_isolated_nodes_and_duplicates_latent150():
+    rng = np.random.default_rng(32)
+    n = 150
+    cells = rng.integers(0, n - 20, size=(200, 3))
+    cells = np.concatenate([cells, cells[:30]])
+    pos = rng.standard_normal((n, 3)).astype(np.float32)
+    node_in = np.concatenate([np.eye(4)[rng.integers(0, 4, n)], rng.standard_normal((n, 4))], 1)
+    pb = Problem(None, 2, seed=32, cells=cells, pos=pos, node_in=node_in, latent=LAT).device()
+    _oracle_check(pb, "fp32", run_fwd_bwd(pb, "fp32"))
+
+
+@pytest.mark.parametrize("prec", PRECS)
+def test_edgeless_graph_latent150(prec):
+    """No edges: every aggregate is zero and the edge MLPs (in the caller's
+    latent-150 layout) get exactly zero gradient."""
+    rng = np.random.default_rng(33)
+    n = 45
+    pos = rng.standard_normal((n, 3)).astype(np.float32)
+    node_in = np.concatenate([np.eye(4)[rng.integers(0, 4, n)], rng.standard_normal((n, 4))], 1)
+    pb = Problem(None, 2, seed=33, cells=np.zeros((0, 3), np.int64), pos=pos, node_in=node_in, latent=LAT)
+    assert pb.g.n_edges == 0
+    pb.device()
+    res = run_fwd_bwd(pb, prec)
+    for name, a, b in segments(pb.m, LAT):
+        if ".edge" in name or name == "enc_edge":
+            assert np.all(res[1][a:b] == 0.0), name
+    _oracle_check(pb, prec, res)
+
+
+def test_empty_graph_latent150():
+    pb = Problem((6, 6), 1, seed=34, latent=LAT)
+    part = np.zeros(pb.g.n_nodes, np.int32)
+    part[:3] = 2
+    pt = mgn.extract_patch(pb.g, part, 1, 1)
+    dpt = mgn.DeviceGraph(pt)
+    ctx = mgn.Context(1, 10, 10, "fp32", save=True, latent=LAT)
+    params = torch.from_numpy(pb.params).cuda()
+    out = mgn.mgn_forward(ctx, dpt, params, torch.zeros((0, 8), dtype=torch.float32, device="cuda"), dpt.efeat,
+                          save=True)
+    assert out.shape == (0, 4)
+    gp = torch.zeros_like(params)
+    mgn.mgn_backward(ctx, torch.zeros((0, 4), device="cuda"), gp)
+    assert float(gp.abs().sum()) == 0.0
