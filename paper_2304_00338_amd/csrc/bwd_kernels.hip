@@ -548,11 +548,10 @@ hipError_t launch_node_bwd(int prec, int lat, int64_t N, const float* h, const f
   *nblocks = g;
   if (!g) return hipSuccess;
   if (prec == MGN_BF16) {
-#define F(LD)                                                                                                         \
-  hipLaunchKernelGGL((k_node_bwd<MGN_BF16, LD>), dim3(g), dim3(LD * 4), 0, s, N, h, agg, hbar_in, w, eps, hbar_part, \
-                     aggbar, part)
-    MGN_BY_WIDTH(lat, F);
-#undef F
+    // bf16 at width 128 runs on the row-layout kernel
+    if (lat != 160) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((k_node_bwd<MGN_BF16, 160>), dim3(g), dim3(640), 0, s, N, h, agg, hbar_in, w, eps, hbar_part,
+                       aggbar, part);
   } else {
 #define F(LD)                                                                                                         \
   hipLaunchKernelGGL((k_node_bwd<MGN_FP32, LD>), dim3(g), dim3(LD * 4), 0, s, N, h, agg, hbar_in, w, eps, hbar_part, \
@@ -591,11 +590,10 @@ hipError_t launch_edge_enc_bwd(int prec, int lat, int64_t E, const float* efeat,
   *nblocks = g;
   if (!g) return hipSuccess;
   if (prec == MGN_BF16) {
-#define F(LD)                                                                                                      \
-  hipLaunchKernelGGL((k_enc_bwd<MGN_BF16, LD, 4>), dim3(g), dim3(LD * 4), 0, s, E, efeat, ebar, w, eps,            \
-                     (float*)nullptr, part)
-    MGN_BY_WIDTH(lat, F);
-#undef F
+    // bf16 at width 128 runs on the row-layout kernel
+    if (lat != 160) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((k_enc_bwd<MGN_BF16, 160, 4>), dim3(g), dim3(640), 0, s, E, efeat, ebar, w, eps,
+                       (float*)nullptr, part);
   } else {
 #define F(LD)                                                                                                      \
   hipLaunchKernelGGL((k_enc_bwd<MGN_FP32, LD, 4>), dim3(g), dim3(LD * 4), 0, s, E, efeat, ebar, w, eps,            \

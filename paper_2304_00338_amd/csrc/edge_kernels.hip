@@ -1,15 +1,17 @@
 // Fused edge-phase kernels of one MGN message-passing step on gfx950, forward
 // and reverse (Sec. 2.1: every edge is updated from its incident nodes, then
-// every node from the sum of its incident edge messages).
+// every node from the sum of its incident edge messages), in the
+// feature-split layout: fp32 at the latent widths 128 and 160, bf16 at 160
+// (bf16 at 128 runs on the row-layout kernels).
 //
 // Both kernels are persistent: block b handles the receiver-aligned tiles
 // b, b+G, b+2G, ...  While a tile is computed, the block already has the
 // next tile's streams in flight in registers (edge latents, gathered node
 // products, and in reverse mode the incoming edge gradient and the gathered
 // aggregate gradient); the tile after that has its sender/receiver ids in
-// flight, and the one after that its descriptor.  Weights stay in registers
-// as MFMA B fragments for the whole loop (bf16); fp32 reads them from the
-// cache per use.
+// flight, and the one after that its descriptor.  The bf16 forward keeps its
+// weights in registers as MFMA B fragments for the whole loop; otherwise
+// they are read from the cache per use (the bf16 reverse stages W2^T in LDS).
 //
 // The first edge-MLP layer is evaluated as W1e e + P_s[s] + P_r[r] with the
 // node products P = [W1s h, W1r h] computed per node (same linear map as
@@ -389,11 +391,10 @@ k_edge_bwd(EdgeTiles tl, const typename Tr<PREC>::T* __restrict__ e, const float
   constexpr int D = LD;
   [[maybe_unused]] constexpr int NW = Width<LD>::NW, NT = Width<LD>::NT;
   constexpr int NCB = D / 16;
-  // bf16: feature-major a1 copy (dW2 operands) and an LDS copy of W2^T; the
-  // LDS copy of W1e^T too at width 128 (at 160 both copies would not fit in
-  // LDS, and W1e^T is read from L2)
+  // bf16 (width 160; width 128 runs on the row-layout kernel): feature-major
+  // a1 copy (dW2 operands) and an LDS copy of W2^T; W1e^T is read from L2
+  // (an LDS copy of it as well would not fit)
   constexpr bool TX = PREC == MGN_BF16;
-  constexpr bool TX1 = TX && LD == 128;
   constexpr int LDT = D + P::PAD;
   constexpr int LDM = D + 4;
   constexpr int LDTT = TM + 8;
@@ -404,7 +405,6 @@ k_edge_bwd(EdgeTiles tl, const typename Tr<PREC>::T* __restrict__ e, const float
   __shared__ __align__(16) T sZ[TM * LDT];
   __shared__ __align__(16) bf16 sA1T[TX ? D * LDTT : 8];
   __shared__ __align__(16) T sW2t[TX ? D * LDT : 8];
-  __shared__ __align__(16) T sW1t[TX1 ? D * LDT : 8];
   __shared__ LnScratch<NW> ln;
   __shared__ int2 sSR[2][TM];
 
@@ -415,13 +415,11 @@ k_edge_bwd(EdgeTiles tl, const typename Tr<PREC>::T* __restrict__ e, const float
   w1.init((const T*)w.W1, 3 * D, w8 * 16, 0, i, q);
   w2.init((const T*)w.W2, D, w8 * 16, 0, i, q);
   WSlice<PREC, false, LD> g2t, g1t;
-  WSliceL<PREC, LD> l2t, l1t;
+  WSliceL<PREC, LD> l2t;
   g2t.init((const T*)w.W2t, D, w8 * 16, 0, i, q);
   g1t.init((const T*)w.W1t, D, w8 * 16, 0, i, q);
   l2t.init(sW2t, w8 * 16, i, q);
-  l1t.init(sW1t, w8 * 16, i, q);
   if constexpr (TX) stage_weights<PREC, LD>(sW2t, (const T*)w.W2t, tid);
-  if constexpr (TX1) stage_weights<PREC, LD>(sW1t, (const T*)w.W1t, tid);
   f32x4 dW2[NCB];
 #pragma unroll
   for (int cb = 0; cb < NCB; ++cb) dW2[cb] = zero4();
@@ -582,10 +580,7 @@ k_edge_bwd(EdgeTiles tl, const typename Tr<PREC>::T* __restrict__ e, const float
     // ---- back through W1e: ebar_out = ebar_in + W1e^T zbar
 #pragma unroll
     for (int rb = 0; rb < NRB; ++rb) acc[rb] = eb_in[rb];
-    if constexpr (TX1)
-      gemm_w<PREC>(acc, sZ, LDT, l1t, i, q);
-    else
-      gemm_w<PREC>(acc, sZ, LDT, g1t, i, q);
+    gemm_w<PREC>(acc, sZ, LDT, g1t, i, q);
     float* ebo = ebar_out + (size_t)eb * D;
 #pragma unroll
     for (int rb = 0; rb < NRB; ++rb)
@@ -735,11 +730,10 @@ hipError_t launch_edge_bwd(int prec, int lat, const EdgeTiles& t, const void* e,
   *nblocks = g;
   if (!g) return hipSuccess;
   if (prec == MGN_BF16) {
-#define F(LD)                                                                                                    \
-  hipLaunchKernelGGL((k_edge_bwd<MGN_BF16, LD == 128, LD>), dim3(g), dim3(LD * 4), 0, s, t, (const bf16*)e, ebar_in, \
-                     have_ebar, ebar_out, (const bf16*)Pn, aggbar, w, eps, (bf16*)zbar, R, slots, part)
-    MGN_BY_WIDTH(lat, F);
-#undef F
+    // bf16 at width 128 runs on the row-layout kernel
+    if (lat != 160) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((k_edge_bwd<MGN_BF16, false, 160>), dim3(g), dim3(640), 0, s, t, (const bf16*)e, ebar_in,
+                       have_ebar, ebar_out, (const bf16*)Pn, aggbar, w, eps, (bf16*)zbar, R, slots, part);
   } else {
 #define F(LD)                                                                                                      \
   hipLaunchKernelGGL((k_edge_bwd<MGN_FP32, false, LD>), dim3(g), dim3(LD * 4), 0, s, t, (const float*)e, ebar_in,  \
@@ -756,11 +750,10 @@ hipError_t launch_wgrad(int prec, int lat, int64_t M, const void* Gm, const void
   *nblocks = g;
   if (!g) return hipSuccess;
   if (prec == MGN_BF16) {
-#define F(LD)                                                                                                    \
-  hipLaunchKernelGGL((k_wgrad<MGN_BF16, LD>), dim3(g), dim3(LD * 4), 0, s, M, (const bf16*)Gm, (const bf16*)Xm, \
-                     part)
-    MGN_BY_WIDTH(lat, F);
-#undef F
+    // bf16 at width 128 runs on the row-layout kernel
+    if (lat != 160) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((k_wgrad<MGN_BF16, 160>), dim3(g), dim3(640), 0, s, M, (const bf16*)Gm, (const bf16*)Xm,
+                       part);
   } else {
 #define F(LD)                                                                                                     \
   hipLaunchKernelGGL((k_wgrad<MGN_FP32, LD>), dim3(g), dim3(LD * 4), 0, s, M, (const float*)Gm, (const float*)Xm, \

@@ -350,9 +350,9 @@ hipError_t launch_edge_enc(int prec, int lat, int64_t E, const float* f, const M
   const int g = grid_for((E + TM - 1) / TM, kFwdBlocks);
   if (!g) return hipSuccess;
   if (prec == MGN_BF16) {
-#define F(LD) hipLaunchKernelGGL((k_edge_enc<MGN_BF16, LD>), dim3(g), dim3(LD * 4), 0, s, E, f, w, eps, (bf16*)e_out)
-    MGN_BY_WIDTH(lat, F);
-#undef F
+    // bf16 at width 128 runs on the row-layout kernel
+    if (lat != 160) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((k_edge_enc<MGN_BF16, 160>), dim3(g), dim3(640), 0, s, E, f, w, eps, (bf16*)e_out);
   } else {
 #define F(LD) hipLaunchKernelGGL((k_edge_enc<MGN_FP32, LD>), dim3(g), dim3(LD * 4), 0, s, E, f, w, eps, (float*)e_out)
     MGN_BY_WIDTH(lat, F);
@@ -376,15 +376,14 @@ hipError_t launch_node_fwd(int prec, int lat, int64_t N, const float* h_in, cons
   if (!g) return hipSuccess;
   const MlpW nn = nx ? *nx : w;
   if (prec == MGN_BF16) {
-#define F(LD)                                                                                                        \
-  if (nx)                                                                                                            \
-    hipLaunchKernelGGL((k_node_fwd<MGN_BF16, LD, true>), dim3(g), dim3(LD * 4), 0, s, N, h_in, agg, w, nn, eps,      \
-                       h_out, (bf16*)P_out);                                                                         \
-  else                                                                                                               \
-    hipLaunchKernelGGL((k_node_fwd<MGN_BF16, LD, false>), dim3(g), dim3(LD * 4), 0, s, N, h_in, agg, w, nn, eps,     \
-                       h_out, (bf16*)P_out)
-    MGN_BY_WIDTH(lat, F);
-#undef F
+    // bf16 at width 128 runs on the row-layout kernel
+    if (lat != 160) return hipErrorInvalidValue;
+    if (nx)
+      hipLaunchKernelGGL((k_node_fwd<MGN_BF16, 160, true>), dim3(g), dim3(640), 0, s, N, h_in, agg, w, nn, eps, h_out,
+                         (bf16*)P_out);
+    else
+      hipLaunchKernelGGL((k_node_fwd<MGN_BF16, 160, false>), dim3(g), dim3(640), 0, s, N, h_in, agg, w, nn, eps, h_out,
+                         (bf16*)P_out);
   } else {
 #define F(LD)                                                                                                        \
   if (nx)                                                                                                            \

@@ -75,7 +75,10 @@ int grid_for(int64_t n_tiles, int max_blocks);
 hipError_t launch_pack(int prec, const float* params, void* pack, const PackList& L, hipStream_t s);
 
 // Feature-split kernels: lat is the kernel width (128, or 160 for the
-// latent 150 padded with zero columns; fp32 only).
+// latent 150 padded with zero columns).  bf16 at width 128 runs on the
+// row-layout kernels for the edge encoder, edge phase, node phase and their
+// reverse (those launchers return hipErrorInvalidValue for it); the node
+// encoder, decoder, sender sums and node-encoder reverse serve both widths.
 hipError_t launch_node_enc(int prec, int lat, int64_t N, const float* node_in, const MlpW& w, const MlpW* next_edge,
                            float eps, float* h_out, void* P_out, hipStream_t s);
 hipError_t launch_edge_enc(int prec, int lat, int64_t E, const float* efeat, const MlpW& w, float eps, void* e_out,
