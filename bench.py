@@ -43,6 +43,29 @@ def log(*a):
 MFMA_FLOP_PER_EDGE = {"edge_fwd": 2 * 128 * 128 * 2 + 24 * 16384 // 16,
                       "edge_bwd": 3 * 2 * 128 * 128}
 MFMA_PEAK_BF16_TFLOPS = 2500.0
+MFMA_PEAK_FP32_TFLOPS = 157.3
+
+
+def edge_bwd_split_roofline(prec, D, N, E, m, avg_ms):
+    """Position of the feature-split edge backward (latent width D, one
+    launch per MP block) against both roofs: algorithmic bytes per launch
+    (per edge: e, the incoming edge gradient except in the last block, the
+    outgoing one and z-bar, sender / receiver ids; per node: P, the gathered
+    aggregate gradient and R) and executed MFMA flop (per edge: 5 products
+    of D x D -- the recomputed W1e e and W2 a1, W2^T dz2, W1e^T zbar and the
+    dW2 accumulation), each divided by the average launch time."""
+    t = 2 if prec == "bf16" else 4
+    per_edge = [D * t + (D * 4 if l < m - 1 else 0) + D * 4 + D * t + 8 for l in range(m)]
+    nbytes = float(np.mean(per_edge)) * E + N * (2 * D * t + D * 4 + D * 4)
+    flop = 10.0 * D * D * E
+    peak = MFMA_PEAK_BF16_TFLOPS if prec == "bf16" else MFMA_PEAK_FP32_TFLOPS
+    gbs = nbytes / (avg_ms * 1e-3) / 1e9
+    tfs = flop / (avg_ms * 1e-3) / 1e12
+    return {"kernel": "edge_bwd", "avg_launch_ms": round(avg_ms, 4),
+            "hbm": {"algorithmic_bytes_per_launch": int(nbytes), "achieved_gbs": round(gbs, 1),
+                    "frac": round(gbs / HBM_PEAK_GBS, 4)},
+            "mfma": {"flop_per_launch": int(flop), "achieved_tflops": round(tfs, 1), "peak_tflops": peak,
+                     "frac": round(tfs / peak, 4)}}
 
 
 def kernel_bytes(kind, N, E, n_tiles, prec, have_ebar=True, write_e=True, keep_a1=True):
@@ -372,6 +395,9 @@ def paper_3d_train(S, args, n_patches=32, k=6, m=3, reps=3):
             prof = mgn.mgn_profile_collect(ctx)
             mgn.mgn_profile_enable(ctx, False)
             if mode == "union":
+                eb = prof.get("edge_bwd")
+                if eb:
+                    r["edge_bwd_roofs"] = edge_bwd_split_roofline(prec, 160, un.n_nodes, pe, m, eb[0] / eb[1])
                 r.update({"ms_per_step": round(dt * 1e3, 3), "steps_per_s": round(1.0 / dt, 3),
                           "mp_edges_per_s_fwdbwd": round(pe * m * 2 / dt, 1),
                           "kernel_ms_per_step": {kk: round(v[0] / reps, 3)
