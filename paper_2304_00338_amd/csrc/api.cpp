@@ -35,6 +35,7 @@ struct Off {
 struct PackOff {
   int64_t W1 = -1, W1t = -1, W2 = -1, W2t = -1, W1p = -1, W2p = -1;
   int64_t W1sp = -1, W1rp = -1;  // edge MLPs: row-permuted sender / receiver column blocks of W1
+  int64_t W2tp = -1, W1tp = -1;  // width 160, edge MLPs: row-permuted W2^T and W1e^T
 };
 
 struct Model {
@@ -88,21 +89,22 @@ void add_pack(Model& M, int64_t src, int rows, int cols, int64_t& W, int64_t& Wt
   M.ents.push_back(e);
 }
 
-// Row-permuted copy (perm_row) of `cols` columns of a [128][ld] matrix
-// starting at float offset src (row-layout kernels, width 128 only).
-void add_perm(Model& M, int64_t src, int ld, int64_t& W, int cols = kRowsD) {
+// Row-permuted copy (perm_row) of `cols` columns of a [rows][ld] matrix
+// starting at float offset src (perm 1), or the row-permuted transpose of
+// its first `rows` columns, `cols` source rows (perm 2).
+void add_perm(Model& M, int64_t src, int ld, int64_t& W, int cols = kRowsD, int rows = kRowsD, int perm = 1) {
   auto al = [](int64_t x) { return (x + 63) & ~int64_t(63); };
   M.pack_elems = al(M.pack_elems);
   W = M.pack_elems;
-  M.pack_elems += (int64_t)kRowsD * cols;
+  M.pack_elems += (int64_t)rows * cols;
   PackEnt e;
   e.src = src;
   e.dst = W;
   e.dstt = -1;
-  e.rows = kRowsD;
+  e.rows = rows;
   e.cols = cols;
   e.ld = ld;
-  e.perm = 1;
+  e.perm = perm;
   M.ents.push_back(e);
 }
 
@@ -138,6 +140,12 @@ Model make_model(int m, int lat) {
       add_perm(M, M.edge[i].W1 + 2 * D, 3 * D, M.p_edge[i].W1rp);
       add_perm(M, M.node[i].W1, 2 * D, M.p_node[i].W1p, 2 * D);
       add_perm(M, M.node[i].W2, D, M.p_node[i].W2p);
+    } else {
+      // width 160 (bf16 row-per-wave edge backward): W2 and the transposes
+      // of W2 and of W1's edge-latent block, rows in perm_row order
+      add_perm(M, M.edge[i].W2, D, M.p_edge[i].W2p, D, D, 1);
+      add_perm(M, M.edge[i].W2, D, M.p_edge[i].W2tp, D, D, 2);
+      add_perm(M, M.edge[i].W1, 3 * D, M.p_edge[i].W1tp, D, D, 2);
     }
     add_pack(M, M.node[i].W1, D, 2 * D, M.p_node[i].W1, M.p_node[i].W1t);
     add_pack(M, M.node[i].W2, D, D, M.p_node[i].W2, M.p_node[i].W2t);
@@ -321,9 +329,11 @@ void plan(Ctx& c) {
   // bf16 with save: first-layer activations of every edge MLP, read by the
   // backward instead of recomputing the first layer
   // bf16 at width 128 runs on the row-layout kernels; every other case on
-  // the feature-split ones
-  const bool rows = c.cfg.precision == MGN_BF16 && c.LD == kRowsD;
-  const bool keep_a1 = c.save && rows;
+  // the feature-split ones, except the bf16 edge backward at width 160 (one
+  // wave per row block, like the row layout)
+  const bool bf = c.cfg.precision == MGN_BF16;
+  const bool rows = bf && c.LD == kRowsD;
+  const bool keep_a1 = c.save && bf;
   L.a1_off = so;
   so = al256(so + (keep_a1 ? (size_t)la * E * D * 2 : 0));
   L.act_stride = so;
@@ -346,15 +356,15 @@ void plan(Ctx& c) {
       L.gpad = o;  // gradients in the padded layout, moved to the caller's layout at the end
       o = al256(o + (size_t)c.M.total * 4);
     }
-    L.ebar = o;  // edge-gradient stream: the edge-latent element type (row layout), else fp32
-    o = al256(o + (size_t)E * D * (rows ? c.se : 4));
+    L.ebar = o;  // edge-gradient stream, in the edge-latent element type
+    o = al256(o + (size_t)E * D * c.se);
     L.zbar = o;
     o = al256(o + (size_t)E * D * c.se);
     L.dz = o;
     o = al256(o + (keep_a1 ? (size_t)E * D * 2 : 0));
     // bf16 node backward: the a1, dz2, dz1 streams of one node MLP
     L.nstr = o;
-    o = al256(o + (keep_a1 ? (size_t)3 * N * D * 2 : 0));
+    o = al256(o + (keep_a1 && rows ? (size_t)3 * N * D * 2 : 0));
     L.hb_a = o;
     o = al256(o + (size_t)N * D * 4);
     L.hb_b = o;
@@ -436,7 +446,7 @@ struct Run {
     return (float*)(set(k) + c.L.agg_off) + (c.save ? (size_t)l * N * D : 0);
   }
   void* a1_l(int k, int l) const {
-    if (!(keep_a1 && c.save && rows())) return nullptr;
+    if (!(keep_a1 && c.save && prec == MGN_BF16)) return nullptr;
     return set(k) + c.L.a1_off + (size_t)l * E * D * 2;
   }
   void* P_l(int k, int l) const {
@@ -450,6 +460,8 @@ struct Run {
     w.W2p = p.W2p >= 0 ? P(p.W2p) : nullptr;
     w.W1sp = p.W1sp >= 0 ? P(p.W1sp) : nullptr;
     w.W1rp = p.W1rp >= 0 ? P(p.W1rp) : nullptr;
+    w.W2tp = p.W2tp >= 0 ? P(p.W2tp) : nullptr;
+    w.W1tp = p.W1tp >= 0 ? P(p.W1tp) : nullptr;
     w.W1 = p.W1 >= 0 ? P(p.W1) : nullptr;
     w.W1t = p.W1t >= 0 ? P(p.W1t) : nullptr;
     w.W2 = p.W2 >= 0 ? P(p.W2) : nullptr;
@@ -540,7 +552,7 @@ struct Run {
     float* hb_part = (float*)(ws + c.L.hb_b);
     float* aggbar = (float*)(ws + c.L.aggbar);
     float* R = (float*)(ws + c.L.R);
-    void* ebar = ws + c.L.ebar;  // row layout: the edge-latent element type; else fp32
+    void* ebar = ws + c.L.ebar;  // the edge-latent element type
     void* zbar = ws + c.L.zbar;
     int nb = 0, rc;
     LAUNCH(K_DECODER_BWD, launch_decoder_bwd(prec, D, N, h_l(k, m), gout, W(M.dec, M.p_dec), hb_cur, pt, &nb, s));
@@ -573,6 +585,18 @@ struct Run {
         LAUNCH(K_WGRAD, launch_wgrad2(E, zbar, e_l(k, l), dz, a1_l(k, l), pt, &nb, s));
         if ((rc = reduce(nb, 16512, 1, D * D + D, grad, oe.W2, 0)) != MGN_OK) return rc;
         if ((rc = reduce(nb, 0, D, D, grad, oe.W1, 3 * D)) != MGN_OK) return rc;
+      } else if (prec == MGN_BF16) {
+        // width 160: one wave per row block from the saved a1; weight
+        // gradients dW1e = sum zbar^T e and dW2 = sum dz2^T a1 in one pass
+        // over the saved streams
+        void* dz = ws + c.L.dz;
+        LAUNCH(K_EDGE_BWD, launch_edge_bwd_w160(tl, a1_l(k, l), ebar, l < m - 1 ? 1 : 0, ebar, aggbar, W(oe, M.p_edge[l]),
+                                    eps, zbar, dz, R, slots(), pt, &nb, s));
+        if ((rc = reduce(nb, 0, 1, D, grad, oe.b1, 0)) != MGN_OK) return rc;
+        if ((rc = reduce(nb, D, 1, 3 * D, grad, oe.b2, 0)) != MGN_OK) return rc;
+        LAUNCH(K_WGRAD, launch_wgrad2_w160(E, zbar, e_l(k, l), dz, a1_l(k, l), pt, &nb, s));
+        if ((rc = reduce(nb, 0, D, D, grad, oe.W1, 3 * D)) != MGN_OK) return rc;
+        if ((rc = reduce(nb, (int64_t)D * D, D, D, grad, oe.W2, D)) != MGN_OK) return rc;
       } else {
         LAUNCH(K_EDGE_BWD, launch_edge_bwd(prec, D, tl, e_l(k, l), (float*)ebar, l < m - 1 ? 1 : 0, (float*)ebar, P_l(k, l), aggbar,
                                 W(oe, M.p_edge[l]), eps, zbar, R, slots(), pt, &nb, s));
@@ -590,7 +614,7 @@ struct Run {
       if (rows())
         LAUNCH(K_EDGE_ENC_BWD, launch_edge_enc_bwd_rows(E, efeat, ebar, W(M.enc_edge, M.p_enc_edge), eps, pt, &nb, s));
       else
-        LAUNCH(K_EDGE_ENC_BWD, launch_edge_enc_bwd(prec, D, E, efeat, (float*)ebar, W(M.enc_edge, M.p_enc_edge), eps, pt, &nb, s));
+        LAUNCH(K_EDGE_ENC_BWD, launch_edge_enc_bwd(prec, D, E, efeat, ebar, W(M.enc_edge, M.p_enc_edge), eps, pt, &nb, s));
       if ((rc = reduce(nb, 0, 1, (int)M.enc_edge.size, grad, M.enc_edge.W1, 0)) != MGN_OK) return rc;
     }
     LAUNCH(K_NODE_ENC_BWD, launch_node_enc_bwd(prec, D, N, node_in, hb_cur, W(M.enc_node, M.p_enc_node), eps, gin, pt, &nb, s));

@@ -233,7 +233,8 @@ __global__ void __launch_bounds__(LD * 4) __attribute__((amdgpu_waves_per_eu(LD 
 k_edge_fwd(EdgeTiles tl, const typename Tr<PREC>::T* __restrict__ e_in,
                                                  typename Tr<PREC>::T* __restrict__ e_out, int write_e,
                                                  const typename Tr<PREC>::T* __restrict__ Pn, MlpW w, float eps,
-                                                 float* __restrict__ agg, float* __restrict__ slots) {
+                                                 float* __restrict__ agg, float* __restrict__ slots,
+                                                 typename Tr<PREC>::T* __restrict__ a1_out) {
   typedef Tr<PREC> P;
   typedef typename P::T T;
   typedef Rows<T, LD> RT;
@@ -331,6 +332,12 @@ k_edge_fwd(EdgeTiles tl, const typename Tr<PREC>::T* __restrict__ e_in,
 #pragma unroll
       for (int r = 0; r < 4; ++r) sA1[(rb * 16 + q * 4 + r) * LDT + n] = P::cvt(fmaxf(acc[rb][r], 0.f));
     __syncthreads();
+    if (a1_out != nullptr)  // saved first-layer activations, read by the reverse
+      for (int idx = tid; idx < ne_ * RT::CPR; idx += NT) {
+        const int row = idx / RT::CPR, col = (idx % RT::CPR) * RT::EPC;
+        *reinterpret_cast<uint4*>(a1_out + (size_t)(eb + row) * D + col) =
+            *reinterpret_cast<const uint4*>(sA1 + row * LDT + col);
+      }
 #pragma unroll
     for (int rb = 0; rb < NRB; ++rb) acc[rb] = f32x4{b2, b2, b2, b2};
     gemm_w<PREC>(acc, sA1, LDT, w2, i, q);
@@ -712,11 +719,11 @@ hipError_t launch_edge_fwd(int prec, int lat, const EdgeTiles& t, const void* e_
   if (!g) return hipSuccess;
   if (prec == MGN_BF16) {
     hipLaunchKernelGGL((k_edge_fwd<MGN_BF16, true, 160>), dim3(g), dim3(640), 0, s, t, (const bf16*)e_in,
-                       (bf16*)e_out, write_e, (const bf16*)Pn, w, eps, agg, slots);
+                       (bf16*)e_out, write_e, (const bf16*)Pn, w, eps, agg, slots, (bf16*)a1_out);
   } else {
 #define F(LD)                                                                                                     \
   hipLaunchKernelGGL((k_edge_fwd<MGN_FP32, false, LD>), dim3(g), dim3(LD * 4), 0, s, t, (const float*)e_in,       \
-                     (float*)e_out, write_e, (const float*)Pn, w, eps, agg, slots)
+                     (float*)e_out, write_e, (const float*)Pn, w, eps, agg, slots, (float*)nullptr)
     MGN_BY_WIDTH(lat, F);
 #undef F
   }

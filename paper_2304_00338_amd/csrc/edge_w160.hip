@@ -1,0 +1,522 @@
+// Edge phase of one MGN message-passing step, reverse, bf16 operands, at the
+// latent width 150 computed 160 wide (App. C: the 3D model; padded features
+// are exactly zero), with one wave per 16-row half of a receiver-aligned
+// tile (Sec. 2.1: every edge latent is updated from itself and its two end
+// nodes, every node from the sum of its in-edge messages; this is the
+// reverse of that update).
+//
+// Lane layout as in the 128-wide row kernels: lane l (i = l & 15, q = l >> 4)
+// holds row i of a 16-row half and the five 8-feature runs [32s + 8q, 32s +
+// 8q + 8), s < 5.  The products run transposed (C[feature][row] = W x^T):
+// the A operand is a 16-row block of a weight matrix whose rows are in
+// perm_row order, so the C fragment of output block ob hands lane q the
+// features fo(ob, q) + r, which are again its runs.  Unlike the 128-wide
+// kernels the products with transposed weights read separately packed
+// transposed copies (W2^T in LDS, W1e^T from the cache) instead of
+// transposing LDS reads, and the LDS rows are padded to 168 elements (336
+// bytes: the 16 rows of an A fragment start in distinct 4-bank groups).
+//
+// Per half: z2 = b2 + W2 a1 from the saved first-layer activations,
+// LayerNorm statistics over the 150 real features, mbar = ebar_in +
+// aggbar[receiver], dgamma / dbeta / db2 column sums (DPP butterflies),
+// dz2 (written for the weight-gradient pass), zbar = (W2^T dz2) where
+// a1 > 0 (written), per-receiver sums of zbar in ascending row order (from a
+// per-wave bf16 stage; also db1), ebar_out = ebar_in + W1e^T zbar.  The only
+// block barriers stage the weights before the loop and combine the column
+// sums after it.
+#include "rows_common.hpp"
+#include "launch.hpp"
+
+namespace mgn {
+namespace dev {
+
+namespace w160 {
+constexpr int L = 160;   // kernel width
+constexpr int LR = 150;  // real latent width
+constexpr int LW = 168;  // LDS row stride of the staged weights and stage (elements)
+constexpr int NS = 5;    // runs per lane
+constexpr int NOB = 10;  // 16-feature output blocks
+
+struct __attribute__((aligned(16))) Lds {
+  __attribute__((aligned(16))) bf16 W2[L * LW];
+  __attribute__((aligned(16))) bf16 W2t[L * LW];
+  __attribute__((aligned(16))) float b2[L];
+  __attribute__((aligned(16))) float g[L];
+  __attribute__((aligned(16))) bf16 stage[NW][16 * LW];
+};
+
+// Copy a row-major [160][160] bf16 matrix into LDS rows of stride LW.
+__device__ __forceinline__ void stage_w(bf16* dst, const bf16* __restrict__ src, int tid) {
+  constexpr int CPR = L / 8;
+  for (int idx = tid; idx < L * CPR; idx += NT) {
+    const int row = idx / CPR, c = idx % CPR;
+    *reinterpret_cast<uint4*>(dst + row * LW + c * 8) = *reinterpret_cast<const uint4*>(src + row * L + c * 8);
+  }
+}
+
+// C-layout fragment of output block ob from the lane's five bf16 runs.
+__device__ __forceinline__ f32x4 run_block5(const uint4 (&runs)[NS], int ob) {
+  const bf16x8 v = __builtin_bit_cast(bf16x8, runs[ob >> 1]);
+  const int h = 4 * (ob & 1);
+  return f32x4{(float)v[h], (float)v[h + 1], (float)v[h + 2], (float)v[h + 3]};
+}
+
+// Mask of the real features among fo(ob, q) + r, r < 4 (bit r).
+__device__ __forceinline__ int live_bits(int ob, int q) {
+  const int f = fo(ob, q);
+  return f + 4 <= LR ? 15 : (f >= LR ? 0 : (1 << (LR - f)) - 1);
+}
+
+// Column sums over the 16 rows of a half of the 8 values v[k] = c[8 + k / 4]
+// [k % 4] (output blocks 8, 9): three halving butterfly steps (partners
+// 15 - i, i ^ 7, i ^ 3) and a final add with lane i ^ 1, after which lanes i
+// and i ^ 1 both hold the sum of the value tail_feature names.  Every lane
+// adds in a fixed order.
+__device__ __forceinline__ float colsum16_tail(const f32x4 (&c)[NOB], int i) {
+  float v[8];
+#pragma unroll
+  for (int k = 0; k < 8; ++k) v[k] = c[8 + (k >> 2)][k & 3];
+  bfly_step<4, 0x140>(v, (i >> 3) & 1);  // row_mirror: lane 15 - i
+  bfly_step<2, 0x141>(v, (i >> 2) & 1);  // row_half_mirror: lane i ^ 7
+  bfly_step<1, 0x1B>(v, (i >> 1) & 1);   // quad_perm [3,2,1,0]: lane i ^ 3
+  return v[0] + dpp_mov<0xB1>(v[0]);     // quad_perm [1,0,3,2]: lane i ^ 1
+}
+// Value index k (feature fo(8 + k / 4, q) + k % 4) whose column sum lane i
+// holds after colsum16_tail: bit 2 of k is bit 3 of i, bit 1 is bit 2, bit 0
+// is bit 1 (the halving steps keep the upper half in the lanes with the bit
+// set).
+__device__ __forceinline__ int tail_feature(int i, int q) {
+  const int k = (((i >> 3) & 1) << 2) | (((i >> 2) & 1) << 1) | ((i >> 1) & 1);
+  return fo(8 + (k >> 2), q) + (k & 3);
+}
+}  // namespace w160
+
+__global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
+k_edge_bwd_w160(EdgeTiles tl, const bf16* __restrict__ a1_in, const bf16* ebar_in, int have_ebar, bf16* ebar_out,
+                const float* __restrict__ aggbar, const bf16* __restrict__ W2p, const bf16* __restrict__ W2tp,
+                const bf16* __restrict__ W1tp, const float* __restrict__ b2, const float* __restrict__ gamma,
+                float eps, bf16* __restrict__ zbar, bf16* __restrict__ dz_out, float* __restrict__ R,
+                float* __restrict__ slots, Partials part) {
+  using namespace w160;
+  __shared__ __align__(16) Lds S;
+  const int tid = threadIdx.x, lane = tid & 63, i = lane & 15, q = lane >> 4;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+  stage_w(S.W2, W2p, tid);
+  stage_w(S.W2t, W2tp, tid);
+  if (tid < L) {
+    S.b2[tid] = b2[tid];
+    S.g[tid] = gamma[tid];
+  }
+  __syncthreads();
+
+  const UnitRange ur = unit_range(tl.n_tiles, wv);
+  int64_t t = ur.t;
+  const int64_t stride = ur.stride, tend = ur.end;
+  const int4* tiles = reinterpret_cast<const int4*>(tl.tiles);
+  auto desc = [&](int64_t tt) -> int4 {
+    const bool ok = tt < tend;
+    const int4 v = tiles[ok ? tt : tend - 1];
+    int4 r;  // per-component selects (an aggregate select goes through scratch)
+    r.x = ok ? v.x : 0;
+    r.y = ok ? v.y : 0;
+    r.z = ok ? v.z : 0;
+    r.w = ok ? v.w : 0;
+    return r;
+  };
+  // the a1 runs of a half are prefetched one half ahead; the incoming edge
+  // gradient of a half is loaded when the half starts (first used after the
+  // z2 product)
+  struct HalfLoads {
+    uint4 a[NS];
+  };
+  const int lastE = (int)max(tl.n_edges - 1, (int64_t)0);
+  auto nrows = [](int4 d) { return d.w - d.z; };
+  auto erow = [&](int4 d, int rb) { return min(max(d.z + min(rb * 16 + i, nrows(d) - 1), 0), lastE); };
+  auto load_half = [&](int4 d, int rb, HalfLoads& H, int& recv) {
+    const size_t row = (size_t)erow(d, rb);
+    recv = tl.receivers[row];
+    const bf16* ap = a1_in + row * L + 8 * q;
+#pragma unroll
+    for (int k = 0; k < NS; ++k) H.a[k] = *reinterpret_cast<const uint4*>(ap + 32 * k);
+  };
+  auto load_eb = [&](int4 d, int rb, uint4 (&eb)[NS]) {
+    const bf16* ep = ebar_in + (size_t)erow(d, rb) * L + 8 * q;
+#pragma unroll
+    for (int k = 0; k < NS; ++k) {
+      const uint4 v = *reinterpret_cast<const uint4*>(ep + 32 * k);
+      eb[k].x = have_ebar ? v.x : 0u;
+      eb[k].y = have_ebar ? v.y : 0u;
+      eb[k].z = have_ebar ? v.z : 0u;
+      eb[k].w = have_ebar ? v.w : 0u;
+    }
+  };
+
+  // column-sum accumulators: main part (lane i: features fo(i/2, q) + 2 (i%2)
+  // + {0, 1}) and tail (lane i: feature tail_feature(i, q))
+  float2 dga = {0.f, 0.f}, dbe = {0.f, 0.f}, db2 = {0.f, 0.f};
+  float tga = 0.f, tbe = 0.f, tb2 = 0.f;
+  // db1 from the receiver sums: lane: features 2 lane, 2 lane + 1 and, for
+  // lanes < 16, 128 + 2 lane, 128 + 2 lane + 1
+  float2 db1 = {0.f, 0.f}, db1t = {0.f, 0.f};
+  bf16* stage = S.stage[wv];
+  const int lv[2] = {w160::live_bits(8, q), w160::live_bits(9, q)};
+
+  auto half = [&](const HalfLoads& H, int recv, int4 d0, int rb, int segraw, bool chunk, int nv, int& j,
+                  float2& carry, float2& carryt) {
+    const int n = nrows(d0);
+    const int row = rb * 16 + i;
+    const bool ok = row < n;
+    // staged weights at an opaque offset: reads of them are not loop-invariant,
+    // so they are not hoisted into registers
+    const int oz = opaque_zero();
+    const bf16* W2s = S.W2 + oz;
+    const bf16* W2ts = S.W2t + oz;
+    // ---- z2 = b2 + W2 a1 and its LayerNorm statistics (150 real features)
+    f32x4 acc[NOB];
+#pragma unroll
+    for (int ob = 0; ob < NOB; ++ob) acc[ob] = *reinterpret_cast<const f32x4*>(S.b2 + fo(ob, q));
+#pragma unroll
+    for (int s = 0; s < NS; ++s)
+#pragma unroll
+      for (int ob = 0; ob < NOB; ++ob) {
+        const bf16x8 a = *reinterpret_cast<const bf16x8*>(W2s + (ob * 16 + i) * LW + 32 * s + 8 * q);
+        acc[ob] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, as_frag(H.a[s]), acc[ob], 0, 0, 0);
+      }
+    float sm = 0.f;
+#pragma unroll
+    for (int ob = 0; ob < NOB; ++ob)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) sm += acc[ob][r];
+    const float mean = sum_rowlanes(sm) * (1.0f / LR);
+    float sq = 0.f;
+#pragma unroll
+    for (int ob = 0; ob < NOB; ++ob) {
+      acc[ob] -= mean;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const bool live = ob < 8 || ((lv[ob - 8] >> r) & 1);
+        sq += live ? acc[ob][r] * acc[ob][r] : 0.f;
+      }
+    }
+    const float rstd = __builtin_amdgcn_rsqf(sum_rowlanes(sq) * (1.0f / LR) + eps);
+    // ---- mbar = ebar_in + aggbar[receiver] (zero on rows past the tile)
+    f32x4 mb[NOB];
+    {
+      uint4 eb[NS];
+      load_eb(d0, rb, eb);
+      const float* gp = aggbar + (size_t)recv * L;
+#pragma unroll
+      for (int ob = 0; ob < NOB; ++ob) {
+        const f32x4 ag = *reinterpret_cast<const f32x4*>(gp + fo(ob, q));
+        mb[ob] = ok ? ag + run_block5(eb, ob) : f32x4{0.f, 0.f, 0.f, 0.f};
+        acc[ob] *= rstd;  // xhat
+      }
+    }
+    // ---- dgamma += sum_rows mbar xhat, dbeta += sum_rows mbar
+    {
+      const float2 d = colsum16(reinterpret_cast<const f32x4(&)[8]>(mb), i);
+      dbe.x += d.x;
+      dbe.y += d.y;
+      tbe += w160::colsum16_tail(mb, i);
+      f32x4 p[NOB];
+#pragma unroll
+      for (int ob = 0; ob < NOB; ++ob) p[ob] = mb[ob] * acc[ob];
+      const float2 c = colsum16(reinterpret_cast<const f32x4(&)[8]>(p), i);
+      dga.x += c.x;
+      dga.y += c.y;
+      tga += w160::colsum16_tail(p, i);
+    }
+    // ---- LayerNorm backward: dz2 = rstd (dxh - mean(dxh) - xhat mean(dxh xhat)),
+    // dxh = mbar gamma (zero on padded features), dz2 = 0 on padded features
+    float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+    for (int ob = 0; ob < NOB; ++ob) {
+      mb[ob] *= *reinterpret_cast<const f32x4*>(S.g + fo(ob, q));  // dxh
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        s1 += mb[ob][r];
+        s2 += mb[ob][r] * acc[ob][r];
+      }
+    }
+    const float m1 = sum_rowlanes(s1) * (1.0f / LR), m2 = sum_rowlanes(s2) * (1.0f / LR);
+#pragma unroll
+    for (int ob = 0; ob < NOB; ++ob)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const bool live = ob < 8 || ((lv[ob - 8] >> r) & 1);
+        acc[ob][r] = live ? rstd * (mb[ob][r] - m1 - acc[ob][r] * m2) : 0.f;
+      }
+    bf16x8 dzf[NS];
+#pragma unroll
+    for (int s = 0; s < NS; ++s) dzf[s] = pack_run(acc[2 * s], acc[2 * s + 1]);
+    if (ok) {
+      bf16* dp = dz_out + ((size_t)d0.z + row) * L + 8 * q;
+#pragma unroll
+      for (int s = 0; s < NS; ++s) *reinterpret_cast<uint4*>(dp + 32 * s) = __builtin_bit_cast(uint4, dzf[s]);
+    }
+    // ---- db2 += sum_rows dz2 (as stored)
+    {
+      f32x4 v[NOB];
+#pragma unroll
+      for (int s = 0; s < NS; ++s)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          v[2 * s][r] = (float)dzf[s][r];
+          v[2 * s + 1][r] = (float)dzf[s][4 + r];
+        }
+      const float2 c = colsum16(reinterpret_cast<const f32x4(&)[8]>(v), i);
+      db2.x += c.x;
+      db2.y += c.y;
+      tb2 += w160::colsum16_tail(v, i);
+    }
+    // ---- da1 = W2^T dz2, zbar = da1 where a1 > 0
+#pragma unroll
+    for (int ob = 0; ob < NOB; ++ob) acc[ob] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s = 0; s < NS; ++s)
+#pragma unroll
+      for (int ob = 0; ob < NOB; ++ob) {
+        const bf16x8 a = *reinterpret_cast<const bf16x8*>(W2ts + (ob * 16 + i) * LW + 32 * s + 8 * q);
+        acc[ob] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, dzf[s], acc[ob], 0, 0, 0);
+      }
+    bf16x8 zf[NS];
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      const bf16x8 a = as_frag(H.a[s]);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        zf[s][r] = (float)a[r] > 0.f ? (bf16)acc[2 * s][r] : (bf16)0.f;
+        zf[s][4 + r] = (float)a[4 + r] > 0.f ? (bf16)acc[2 * s + 1][r] : (bf16)0.f;
+      }
+    }
+    if (ok) {
+      bf16* zp = zbar + ((size_t)d0.z + row) * L + 8 * q;
+#pragma unroll
+      for (int s = 0; s < NS; ++s) *reinterpret_cast<uint4*>(zp + 32 * s) = __builtin_bit_cast(uint4, zf[s]);
+    }
+    // W1e^T fragments come from the cache at the lane's rows ob * 16 + i:
+    // K step s of all ten output blocks at a time, the next step's loads in
+    // flight while a step multiplies (the first ones before the sums below)
+    const bf16* W1t = W1tp + oz + i * L + 8 * q;
+    auto w1t_step = [&](int s, bf16x8 (&f)[NOB]) {
+#pragma unroll
+      for (int ob = 0; ob < NOB; ++ob) f[ob] = *reinterpret_cast<const bf16x8*>(W1t + ob * 16 * L + 32 * s);
+    };
+    bf16x8 fw[2][NOB];
+    w1t_step(0, fw[0]);
+    // ---- per-receiver sums of zbar (as stored) in ascending row order, and db1
+    wave_lds_sync();
+#pragma unroll
+    for (int s = 0; s < NS; ++s) *reinterpret_cast<uint4*>(stage + i * LW + 32 * s + 8 * q) = __builtin_bit_cast(uint4, zf[s]);
+    wave_lds_sync();
+    {
+      const int lo_row = rb * 16, hi_row = lo_row + 16;
+      const bool tl16 = lane < 16;
+      while (j < nv) {
+        const int a = chunk ? 0 : __builtin_amdgcn_readlane(segraw, j) - d0.z;
+        const int b = chunk ? n : __builtin_amdgcn_readlane(segraw, j + 1) - d0.z;
+        const int u0 = max(a, lo_row), u1 = min(b, hi_row);
+        for (int u = u0; u < u1; ++u) {
+          const bf16* sr = stage + (u - lo_row) * LW;
+          typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+          const bf16x2 v = *reinterpret_cast<const bf16x2*>(sr + 2 * lane);
+          carry.x += (float)v[0];
+          carry.y += (float)v[1];
+          if (tl16) {
+            const bf16x2 w = *reinterpret_cast<const bf16x2*>(sr + 128 + 2 * lane);
+            carryt.x += (float)w[0];
+            carryt.y += (float)w[1];
+          }
+        }
+        if (b > hi_row) break;
+        float* dst = !chunk ? R + (size_t)(d0.x + j) * L : slots + (size_t)(-1 - d0.y) * L;
+        *reinterpret_cast<float2*>(dst + 2 * lane) = carry;
+        if (tl16) *reinterpret_cast<float2*>(dst + 128 + 2 * lane) = carryt;
+        db1.x += carry.x;
+        db1.y += carry.y;
+        db1t.x += carryt.x;
+        db1t.y += carryt.y;
+        carry = float2{0.f, 0.f};
+        carryt = float2{0.f, 0.f};
+        ++j;
+      }
+    }
+    // ---- ebar_out = ebar_in + W1e^T zbar (the incoming rows again, from the cache)
+    {
+      uint4 eb[NS];
+      load_eb(d0, rb, eb);
+#pragma unroll
+      for (int ob = 0; ob < NOB; ++ob) acc[ob] = run_block5(eb, ob);
+    }
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      if (s + 1 < NS) w1t_step(s + 1, fw[(s + 1) & 1]);
+#pragma unroll
+      for (int ob = 0; ob < NOB; ++ob)
+        acc[ob] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fw[s & 1][ob], zf[s], acc[ob], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    if (ok) {
+      bf16* op = ebar_out + ((size_t)d0.z + row) * L + 8 * q;
+#pragma unroll
+      for (int s = 0; s < NS; ++s)
+        *reinterpret_cast<uint4*>(op + 32 * s) = __builtin_bit_cast(uint4, pack_run(acc[2 * s], acc[2 * s + 1]));
+    }
+    wave_lds_sync();
+  };
+
+  if (t < tend) {
+    int4 d0 = desc(t);
+    HalfLoads A, B;
+    int rA, rB;
+    load_half(d0, 0, A, rA);
+    for (; t < tend; t += stride) {
+      const bool chunk = d0.y < 0;
+      const int nv = chunk ? 1 : d0.y - d0.x;
+      const int segraw = tl.rowptr[min(d0.x + lane, max(d0.x, d0.y))];
+      const int4 d1 = desc(t + stride);
+      load_half(d0, 1, B, rB);
+      float2 carry = {0.f, 0.f}, carryt = {0.f, 0.f};
+      int j = 0;  // next node whose sum is open
+      half(A, rA, d0, 0, segraw, chunk, nv, j, carry, carryt);
+      load_half(d1, 0, A, rA);
+      half(B, rB, d0, 1, segraw, chunk, nv, j, carry, carryt);
+      d0 = d1;
+    }
+  }
+  // ---- block partials [db1 | db2 | dgamma | dbeta], the 8 waves' sums in wave order
+  __syncthreads();
+  float* red = reinterpret_cast<float*>(S.W2);  // [4][NW][L]
+  {
+    const int fm = fo(i >> 1, q) + 2 * (i & 1), ft = w160::tail_feature(i, q);
+    float* r0 = red + (0 * NW + wv) * L;
+    float* r1 = red + (1 * NW + wv) * L;
+    float* r2 = red + (2 * NW + wv) * L;
+    float* r3 = red + (3 * NW + wv) * L;
+    *reinterpret_cast<float2*>(r0 + 2 * lane) = db1;
+    if (lane < 16) *reinterpret_cast<float2*>(r0 + 128 + 2 * lane) = db1t;
+    *reinterpret_cast<float2*>(r1 + fm) = db2;
+    *reinterpret_cast<float2*>(r2 + fm) = dga;
+    *reinterpret_cast<float2*>(r3 + fm) = dbe;
+    if ((i & 1) == 0) {  // lanes i and i ^ 1 hold the same tail sums
+      r1[ft] = tb2;
+      r2[ft] = tga;
+      r3[ft] = tbe;
+    }
+  }
+  __syncthreads();
+  float* base = part.buf + (size_t)blockIdx.x * part.stride;
+  for (int idx = tid; idx < 4 * L; idx += NT) {
+    const int k = idx / L, f = idx % L;
+    float v = 0.f;
+#pragma unroll
+    for (int u = 0; u < NW; ++u) v += red[(k * NW + u) * L + f];
+    base[idx] = v;
+  }
+}
+
+// Weight gradients of the edge MLP at width 160 from the saved bf16 streams,
+// one pass: dW1e = sum_rows zbar^T e (partials at 0) and dW2 = sum_rows
+// dz2^T a1 (at 160 * 160).  Each 32-row chunk of the four streams is staged
+// row-major in LDS (rows 176 elements apart: 88 dwords, so the 4-row x
+// 4-piece transposing reads below hit distinct banks) while the next chunk
+// is in flight in registers; wave w (10 waves) owns output rows [16w, 16w +
+// 16) of both matrices and reads its MFMA operands with K = the chunk's rows
+// through ds_read_b64_tr_b16.
+namespace w160 {
+constexpr int WG_LD = 176;
+constexpr int WG_NT = 640;
+}  // namespace w160
+
+__global__ void __launch_bounds__(w160::WG_NT) k_wgrad2_w160(int64_t M, const bf16* __restrict__ zb,
+                                                           const bf16* __restrict__ e, const bf16* __restrict__ dz,
+                                                           const bf16* __restrict__ a1, Partials part) {
+  using namespace w160;
+  __shared__ __align__(16) bf16 Sg[2][4][TM * WG_LD];
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, i = lane & 15, q = lane >> 4;
+  const int jp = i >> 2, c4 = i & 3;
+  f32x4 acc1[NOB], acc2[NOB];
+#pragma unroll
+  for (int cb = 0; cb < NOB; ++cb) acc1[cb] = acc2[cb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int64_t nch = (M + TM - 1) / TM, G = gridDim.x;
+  const int srow = tid / (L / 8), scol = (tid % (L / 8)) * 8;
+  const bf16* src[4] = {zb, e, dz, a1};
+  uint4 Ld[4];
+  auto issue = [&](int64_t ch) {
+    const int64_t r = ch * TM + srow;
+    const int64_t rc = r < M ? r : M - 1;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const uint4 v = *reinterpret_cast<const uint4*>(src[k] + rc * L + scol);
+      Ld[k].x = r < M ? v.x : 0u;
+      Ld[k].y = r < M ? v.y : 0u;
+      Ld[k].z = r < M ? v.z : 0u;
+      Ld[k].w = r < M ? v.w : 0u;
+    }
+  };
+  // operand of 16 columns col0.. with K = the chunk's rows q*8 + j
+  auto frag = [&](const bf16* X, int col0) -> bf16x8 {
+    const bf16* p = X + (q * 8 + jp) * WG_LD + col0 + 4 * c4;
+    return cat8(lds_tr(p), lds_tr(p + 4 * WG_LD));
+  };
+  int64_t c = blockIdx.x;
+  int buf = 0;
+  if (c < nch) issue(c);
+  for (; c < nch; c += G) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) *reinterpret_cast<uint4*>(&Sg[buf][k][srow * WG_LD + scol]) = Ld[k];
+    __syncthreads();
+    if (c + G < nch) issue(c + G);
+    const bf16x8 az = frag(Sg[buf][0], 16 * w);
+    const bf16x8 ad = frag(Sg[buf][2], 16 * w);
+#pragma unroll
+    for (int cb = 0; cb < NOB; ++cb) {
+      acc1[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(az, frag(Sg[buf][1], 16 * cb), acc1[cb], 0, 0, 0);
+      acc2[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ad, frag(Sg[buf][3], 16 * cb), acc2[cb], 0, 0, 0);
+    }
+    buf ^= 1;
+  }
+  float* base = part.buf + (size_t)blockIdx.x * part.stride;
+#pragma unroll
+  for (int cb = 0; cb < NOB; ++cb)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int o = w * 16 + q * 4 + r;
+      base[(size_t)o * L + cb * 16 + i] = acc1[cb][r];
+      base[L * L + (size_t)o * L + cb * 16 + i] = acc2[cb][r];
+    }
+}
+
+}  // namespace dev
+
+using namespace dev;
+
+hipError_t launch_edge_bwd_w160(const EdgeTiles& t, const void* a1, const void* ebar_in, int have_ebar,
+                                void* ebar_out, const float* aggbar, const MlpW& w, float eps, void* zbar, void* dz,
+                                float* R, float* slots, const Partials& part, int* nblocks, hipStream_t s) {
+  *nblocks = 0;
+  if (t.n_tiles <= 0) return hipSuccess;
+  if (!w.W2p || !w.W2tp || !w.W1tp || part.stride < 4 * 160) return hipErrorInvalidValue;
+  const int64_t need = (t.n_tiles + NW - 1) / NW;
+  int g = (int)std::min<int64_t>(need, std::min(256, part.max_blocks));
+  if (g >= 8) g &= ~7;
+  *nblocks = g;
+  hipLaunchKernelGGL(k_edge_bwd_w160, dim3(g), dim3(NT), 0, s, t, (const bf16*)a1, (const bf16*)ebar_in, have_ebar,
+                     (bf16*)ebar_out, aggbar, (const bf16*)w.W2p, (const bf16*)w.W2tp, (const bf16*)w.W1tp, w.b2,
+                     w.gamma, eps, (bf16*)zbar, (bf16*)dz, R, slots, part);
+  return hipGetLastError();
+}
+
+hipError_t launch_wgrad2_w160(int64_t M, const void* zbar, const void* e, const void* dz, const void* a1,
+                              const Partials& part, int* nblocks, hipStream_t s) {
+  *nblocks = 0;
+  if (M <= 0) return hipSuccess;
+  if (part.stride < 2 * 160 * 160) return hipErrorInvalidValue;
+  const int g = grid_for((M + TM - 1) / TM, std::min(512, part.max_blocks));
+  *nblocks = g;
+  hipLaunchKernelGGL(k_wgrad2_w160, dim3(g), dim3(w160::WG_NT), 0, s, M, (const bf16*)zbar, (const bf16*)e,
+                     (const bf16*)dz, (const bf16*)a1, part);
+  return hipGetLastError();
+}
+
+}  // namespace mgn

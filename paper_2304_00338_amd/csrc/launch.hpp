@@ -15,6 +15,8 @@ struct MlpW {
   const void* W2p;   // row-permuted copy of W2
   const void* W1sp;  // edge MLPs: row-permuted sender column block of W1
   const void* W1rp;  // edge MLPs: row-permuted receiver column block of W1
+  const void* W2tp;  // width 160, edge MLPs: row-permuted W2^T
+  const void* W1tp;  // width 160, edge MLPs: row-permuted transpose of W1's edge-latent block
   const void* W1;
   const void* W1t;
   const void* W2;
@@ -33,7 +35,8 @@ struct PackEnt {
   int64_t dstt;  // element offset of the transposed copy (-1: none)
   int32_t rows, cols;
   int32_t ld;    // source row stride (floats)
-  int32_t perm;  // 1: copy row perm_row(p) of the source into row p
+  int32_t perm;  // 1: copy row perm_row(p) of the source into row p;
+                 // 2: copy column perm_row(p) of the source into row p
 };
 
 // Output-row order of the weights used by the row-per-wave edge kernels:
@@ -96,6 +99,17 @@ hipError_t launch_edge_fwd_rows(const EdgeTiles& t, const void* e_in, void* e_ou
 hipError_t launch_edge_bwd_rows(const EdgeTiles& t, const void* a1, const void* ebar_in, int have_ebar,
                                 void* ebar_out, const float* aggbar, const MlpW& w, float eps, void* zbar, void* dz,
                                 float* R, float* slots, const Partials& part, int* nblocks, hipStream_t s);
+// bf16 edge backward at width 160 (latent 150) with one wave per 16-row half
+// of a tile, from the saved a1 (uses MlpW::W2p, W2tp, W1tp, b2, gamma); bf16
+// edge-gradient stream (in place allowed); writes zbar, dz2, R / slots and
+// per-block partials [db1 | db2 | dgamma | dbeta] (4 x 160 floats).
+hipError_t launch_edge_bwd_w160(const EdgeTiles& t, const void* a1, const void* ebar_in, int have_ebar,
+                                void* ebar_out, const float* aggbar, const MlpW& w, float eps, void* zbar, void* dz,
+                                float* R, float* slots, const Partials& part, int* nblocks, hipStream_t s);
+// Width 160 (bf16): dW1e = sum zbar^T e at 0 and dW2 = sum dz2^T a1 at
+// 160 * 160 as per-block partials.
+hipError_t launch_wgrad2_w160(int64_t M, const void* zbar, const void* e, const void* dz, const void* a1,
+                              const Partials& part, int* nblocks, hipStream_t s);
 // bf16 dW1e = sum zbar^T e, dW2 = sum dz2^T a1, db2 = sum dz2 as per-block partials.
 hipError_t launch_wgrad2(int64_t M, const void* zbar, const void* e, const void* dz, const void* a1,
                          const Partials& part, int* nblocks, hipStream_t s);
@@ -141,7 +155,8 @@ hipError_t launch_wgrad(int prec, int lat, int64_t M, const void* G, const void*
 hipError_t launch_node_srcsum(int prec, int lat, int64_t N, const int32_t* rowptr, const int32_t* rev, const void* zbar,
                               const float* R, const float* h, const float* hbar_part, const MlpW& w,
                               float* hbar_out, const Partials& part, int* nblocks, hipStream_t s);
-hipError_t launch_edge_enc_bwd(int prec, int lat, int64_t E, const float* efeat, const float* ebar, const MlpW& w,
+// ebar: fp32, or bf16 (the edge-gradient stream of bf16 at width 160)
+hipError_t launch_edge_enc_bwd(int prec, int lat, int64_t E, const float* efeat, const void* ebar, const MlpW& w,
                                float eps, const Partials& part, int* nblocks, hipStream_t s);
 hipError_t launch_node_enc_bwd(int prec, int lat, int64_t N, const float* node_in, const float* hbar, const MlpW& w,
                                float eps, float* gin, const Partials& part, int* nblocks, hipStream_t s);
