@@ -141,8 +141,9 @@ Model make_model(int m, int lat) {
       add_perm(M, M.node[i].W1, 2 * D, M.p_node[i].W1p, 2 * D);
       add_perm(M, M.node[i].W2, D, M.p_node[i].W2p);
     } else {
-      // width 160 (bf16 row-per-wave edge backward): W2 and the transposes
-      // of W2 and of W1's edge-latent block, rows in perm_row order
+      // width 160 (bf16 row-per-wave edge kernels): W1's edge-latent block,
+      // W2 and the transposes of W2 and of that block, rows in perm_row order
+      add_perm(M, M.edge[i].W1, 3 * D, M.p_edge[i].W1p, D, D, 1);
       add_perm(M, M.edge[i].W2, D, M.p_edge[i].W2p, D, D, 1);
       add_perm(M, M.edge[i].W2, D, M.p_edge[i].W2tp, D, D, 2);
       add_perm(M, M.edge[i].W1, 3 * D, M.p_edge[i].W1tp, D, D, 2);

@@ -1,17 +1,16 @@
 // Fused edge-phase kernels of one MGN message-passing step on gfx950, forward
 // and reverse (Sec. 2.1: every edge is updated from its incident nodes, then
 // every node from the sum of its incident edge messages), in the
-// feature-split layout: fp32 at the latent widths 128 and 160, bf16 at 160
-// (bf16 at 128 runs on the row-layout kernels).
+// feature-split layout, fp32 at the latent widths 128 and 160 (bf16 runs on
+// the row-per-wave kernels).
 //
 // Both kernels are persistent: block b handles the receiver-aligned tiles
 // b, b+G, b+2G, ...  While a tile is computed, the block already has the
 // next tile's streams in flight in registers (edge latents, gathered node
 // products, and in reverse mode the incoming edge gradient and the gathered
 // aggregate gradient); the tile after that has its sender/receiver ids in
-// flight, and the one after that its descriptor.  The bf16 forward keeps its
-// weights in registers as MFMA B fragments for the whole loop; otherwise
-// they are read from the cache per use (the bf16 reverse stages W2^T in LDS).
+// flight, and the one after that its descriptor.  Weight fragments are read
+// from the cache per use.
 //
 // The first edge-MLP layer is evaluated as W1e e + P_s[s] + P_r[r] with the
 // node products P = [W1s h, W1r h] computed per node (same linear map as
@@ -32,27 +31,11 @@ __device__ __forceinline__ int tile_opaque_zero() {
   return z;
 }
 
-// B fragments of one 16-column weight slice with K = LD (the kernel width):
-// B[k][n] = W[n0 + n][kofs + k].  refresh() starts a tile (no-op for
-// register-resident fragments).
-template <int PREC, bool WREG, int LD>
-struct WSlice;
-
+// B fragments of one 16-column weight slice with K = LD (the kernel width),
+// B[k][n] = W[n0 + n][kofs + k], read from the cache per use; refresh()
+// starts a tile.
 template <int PREC, int LD>
-struct WSlice<PREC, true, LD> {
-  typedef Tr<PREC> P;
-  static constexpr int NK = LD / P::KS;
-  typename P::Frag f[NK];
-  __device__ __forceinline__ void init(const typename P::T* W, int ldw, int n0, int kofs, int i, int q) {
-#pragma unroll
-    for (int kk = 0; kk < NK; ++kk) f[kk] = P::ldb(W, ldw, n0, kofs + kk * P::KS, i, q);
-  }
-  __device__ __forceinline__ typename P::Frag get(int kk) const { return f[kk]; }
-  __device__ __forceinline__ void refresh() {}
-};
-
-template <int PREC, int LD>
-struct WSlice<PREC, false, LD> {
+struct WSlice {
   typedef Tr<PREC> P;
   static constexpr int NK = LD / P::KS;
   const typename P::T* W;
@@ -71,39 +54,6 @@ struct WSlice<PREC, false, LD> {
   __device__ __forceinline__ void refresh() { z = tile_opaque_zero(); }
 };
 
-// B fragments read from an LDS copy of a [LD][LD] matrix with padded rows
-// (row stride LDW elements), B[k][n] = W[n0 + n][k].
-template <int PREC, int LD>
-struct WSliceL {
-  typedef Tr<PREC> P;
-  static constexpr int NK = LD / P::KS;
-  static constexpr int LDW = LD + P::PAD;
-  const typename P::T* W;
-  int n0, i, q, z = 0;
-  __device__ __forceinline__ void init(const typename P::T* W_, int n0_, int i_, int q_) {
-    W = W_;
-    n0 = n0_;
-    i = i_;
-    q = q_;
-  }
-  __device__ __forceinline__ typename P::Frag get(int kk) const { return P::ldb(W, LDW, n0, z + kk * P::KS, i, q); }
-  __device__ __forceinline__ void refresh() { z = tile_opaque_zero(); }
-};
-
-// Copy the first LD rows of a row-major [.][LD] global matrix into LDS with
-// padded rows (stride LD + PAD elements).
-template <int PREC, int LD>
-__device__ __forceinline__ void stage_weights(typename Tr<PREC>::T* lds, const typename Tr<PREC>::T* __restrict__ W,
-                                              int tid) {
-  typedef typename Tr<PREC>::T T;
-  constexpr int D = LD, NT = Width<LD>::NT;
-  constexpr int EPC = 16 / sizeof(T), LDW = D + Tr<PREC>::PAD;
-  for (int idx = tid; idx < D * D / EPC; idx += NT) {
-    const int row = (idx * EPC) / D, col = (idx * EPC) % D;
-    *reinterpret_cast<uint4*>(lds + row * LDW + col) = *reinterpret_cast<const uint4*>(W + (size_t)row * D + col);
-  }
-}
-
 template <int PREC, class WSL>
 __device__ __forceinline__ void gemm_w(f32x4 (&acc)[NRB], const typename Tr<PREC>::T* A, int lda, const WSL& w,
                                        int i, int q) {
@@ -113,35 +63,6 @@ __device__ __forceinline__ void gemm_w(f32x4 (&acc)[NRB], const typename Tr<PREC
     const typename P::Frag b = w.get(kk);
 #pragma unroll
     for (int rb = 0; rb < NRB; ++rb) acc[rb] = P::mma(P::lda(A, lda, rb * 16, kk * P::KS, i, q), b, acc[rb]);
-  }
-}
-
-// dW slice += G^T X with G in C layout (the wave's 16 output columns) and X
-// a feature-major ("transposed") bf16 tile XT[feature][row] of TM rows: the
-// MFMA's K runs over the tile's rows in the order the C layout holds them.
-template <int NCB>
-__device__ __forceinline__ void gtx_t(f32x4 (&acc)[NCB], const f32x4 (&g)[NRB], const bf16* XT, int ldtt, int i,
-                                      int q) {
-  static_assert(NRB == 2, "one K step of 32 rows");
-  bf16x8 a;
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    a[j] = (bf16)g[0][j];
-    a[4 + j] = (bf16)g[1][j];
-  }
-#pragma unroll 4
-  for (int cb = 0; cb < NCB; ++cb) {
-    const bf16* x = XT + (cb * 16 + i) * ldtt + q * 4;
-    typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-    const bf16x4 lo = *reinterpret_cast<const bf16x4*>(x);
-    const bf16x4 hi = *reinterpret_cast<const bf16x4*>(x + 16);
-    bf16x8 b;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      b[j] = lo[j];
-      b[4 + j] = hi[j];
-    }
-    acc[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc[cb], 0, 0, 0);
   }
 }
 
@@ -228,13 +149,12 @@ struct FwdLoads {
   uint4 e[RT::CPT], ps[RT::CPT], pr[RT::CPT];
 };
 
-template <int PREC, bool WREG, int LD>
+template <int PREC, int LD>
 __global__ void __launch_bounds__(LD * 4) __attribute__((amdgpu_waves_per_eu(LD == 128 ? 2 : 3, LD == 128 ? 2 : 3)))
 k_edge_fwd(EdgeTiles tl, const typename Tr<PREC>::T* __restrict__ e_in,
                                                  typename Tr<PREC>::T* __restrict__ e_out, int write_e,
                                                  const typename Tr<PREC>::T* __restrict__ Pn, MlpW w, float eps,
-                                                 float* __restrict__ agg, float* __restrict__ slots,
-                                                 typename Tr<PREC>::T* __restrict__ a1_out) {
+                                                 float* __restrict__ agg, float* __restrict__ slots) {
   typedef Tr<PREC> P;
   typedef typename P::T T;
   typedef Rows<T, LD> RT;
@@ -256,7 +176,7 @@ k_edge_fwd(EdgeTiles tl, const typename Tr<PREC>::T* __restrict__ e_in,
   const int tid = threadIdx.x, w8 = tid >> 6, lane = tid & 63, i = lane & 15, q = lane >> 4;
   const int n = w8 * 16 + i;
   const float b1 = w.b1[n], b2 = w.b2[n], gam = w.gamma[n], bet = w.beta[n];
-  WSlice<PREC, WREG, LD> w1, w2;
+  WSlice<PREC, LD> w1, w2;
   w1.init((const T*)w.W1, 3 * D, w8 * 16, 0, i, q);
   w2.init((const T*)w.W2, D, w8 * 16, 0, i, q);
 
@@ -332,12 +252,6 @@ k_edge_fwd(EdgeTiles tl, const typename Tr<PREC>::T* __restrict__ e_in,
 #pragma unroll
       for (int r = 0; r < 4; ++r) sA1[(rb * 16 + q * 4 + r) * LDT + n] = P::cvt(fmaxf(acc[rb][r], 0.f));
     __syncthreads();
-    if (a1_out != nullptr)  // saved first-layer activations, read by the reverse
-      for (int idx = tid; idx < ne_ * RT::CPR; idx += NT) {
-        const int row = idx / RT::CPR, col = (idx % RT::CPR) * RT::EPC;
-        *reinterpret_cast<uint4*>(a1_out + (size_t)(eb + row) * D + col) =
-            *reinterpret_cast<const uint4*>(sA1 + row * LDT + col);
-      }
 #pragma unroll
     for (int rb = 0; rb < NRB; ++rb) acc[rb] = f32x4{b2, b2, b2, b2};
     gemm_w<PREC>(acc, sA1, LDT, w2, i, q);
@@ -386,7 +300,7 @@ struct BwdLoads {
 // tile's own gradient rows, which are issued before the next tile's prefetch
 // (vector-memory loads retire in issue order): the forward weights sit in
 // registers and, in bf16, the transposed ones in LDS.
-template <int PREC, bool WREG, int LD>
+template <int PREC, int LD>
 __global__ void __launch_bounds__(LD * 4) __attribute__((amdgpu_waves_per_eu(LD == 128 ? 2 : 3, LD == 128 ? 2 : 3)))
 k_edge_bwd(EdgeTiles tl, const typename Tr<PREC>::T* __restrict__ e, const float* __restrict__ ebar_in,
            int have_ebar, float* __restrict__ ebar_out, const typename Tr<PREC>::T* __restrict__ Pn,
@@ -398,35 +312,25 @@ k_edge_bwd(EdgeTiles tl, const typename Tr<PREC>::T* __restrict__ e, const float
   constexpr int D = LD;
   [[maybe_unused]] constexpr int NW = Width<LD>::NW, NT = Width<LD>::NT;
   constexpr int NCB = D / 16;
-  // bf16 (width 160; width 128 runs on the row-layout kernel): feature-major
-  // a1 copy (dW2 operands) and an LDS copy of W2^T; W1e^T is read from L2
-  // (an LDS copy of it as well would not fit)
-  constexpr bool TX = PREC == MGN_BF16;
   constexpr int LDT = D + P::PAD;
   constexpr int LDM = D + 4;
-  constexpr int LDTT = TM + 8;
   __shared__ __align__(16) T sE[TM * LDT];
   __shared__ __align__(16) float sP[TM * LDM];
   __shared__ __align__(16) T sA1[TM * LDT];
   __shared__ __align__(16) T sG[TM * LDT];
   __shared__ __align__(16) T sZ[TM * LDT];
-  __shared__ __align__(16) bf16 sA1T[TX ? D * LDTT : 8];
-  __shared__ __align__(16) T sW2t[TX ? D * LDT : 8];
   __shared__ LnScratch<NW> ln;
   __shared__ int2 sSR[2][TM];
 
   const int tid = threadIdx.x, w8 = tid >> 6, lane = tid & 63, i = lane & 15, q = lane >> 4;
   const int n = w8 * 16 + i;
   const float b1 = w.b1[n], b2 = w.b2[n], gam = w.gamma[n];
-  WSlice<PREC, WREG, LD> w1, w2;
+  WSlice<PREC, LD> w1, w2;
   w1.init((const T*)w.W1, 3 * D, w8 * 16, 0, i, q);
   w2.init((const T*)w.W2, D, w8 * 16, 0, i, q);
-  WSlice<PREC, false, LD> g2t, g1t;
-  WSliceL<PREC, LD> l2t;
+  WSlice<PREC, LD> g2t, g1t;
   g2t.init((const T*)w.W2t, D, w8 * 16, 0, i, q);
   g1t.init((const T*)w.W1t, D, w8 * 16, 0, i, q);
-  l2t.init(sW2t, w8 * 16, i, q);
-  if constexpr (TX) stage_weights<PREC, LD>(sW2t, (const T*)w.W2t, tid);
   f32x4 dW2[NCB];
 #pragma unroll
   for (int cb = 0; cb < NCB; ++cb) dW2[cb] = zero4();
@@ -476,7 +380,6 @@ k_edge_bwd(EdgeTiles tl, const typename Tr<PREC>::T* __restrict__ e, const float
       w2.refresh();
       g1t.refresh();
       g2t.refresh();
-      l2t.refresh();
     }
     // ---- commit tile t
 #pragma unroll
@@ -523,18 +426,12 @@ k_edge_bwd(EdgeTiles tl, const typename Tr<PREC>::T* __restrict__ e, const float
     gemm_w<PREC>(acc, sE, LDT, w1, i, q);
     uint32_t mask = 0;
 #pragma unroll
-    for (int rb = 0; rb < NRB; ++rb) {
-      typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-      bf16x4 packed;
+    for (int rb = 0; rb < NRB; ++rb)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         if (acc[rb][r] > 0.f) mask |= 1u << (rb * 4 + r);
-        const T a1 = P::cvt(fmaxf(acc[rb][r], 0.f));
-        sA1[(rb * 16 + q * 4 + r) * LDT + n] = a1;
-        if (TX) packed[r] = (bf16)a1;
+        sA1[(rb * 16 + q * 4 + r) * LDT + n] = P::cvt(fmaxf(acc[rb][r], 0.f));
       }
-      if (TX) *reinterpret_cast<bf16x4*>(sA1T + n * LDTT + rb * 16 + q * 4) = packed;
-    }
     __syncthreads();
 #pragma unroll
     for (int rb = 0; rb < NRB; ++rb) acc[rb] = f32x4{b2, b2, b2, b2};
@@ -563,18 +460,12 @@ k_edge_bwd(EdgeTiles tl, const typename Tr<PREC>::T* __restrict__ e, const float
         db2 += g[rb][r];
         sG[(rb * 16 + q * 4 + r) * LDT + n] = P::cvt(g[rb][r]);
       }
-    if constexpr (TX)
-      gtx_t<NCB>(dW2, g, sA1T, LDTT, i, q);
-    else
-      gtx<PREC, NCB>(dW2, g, sA1, LDT, 0, i, q);
+    gtx<PREC, NCB>(dW2, g, sA1, LDT, 0, i, q);
     __syncthreads();
     // ---- back through W2 and the ReLU
 #pragma unroll
     for (int rb = 0; rb < NRB; ++rb) acc[rb] = zero4();
-    if constexpr (TX)
-      gemm_w<PREC>(acc, sG, LDT, l2t, i, q);
-    else
-      gemm_w<PREC>(acc, sG, LDT, g2t, i, q);
+    gemm_w<PREC>(acc, sG, LDT, g2t, i, q);
 #pragma unroll
     for (int rb = 0; rb < NRB; ++rb)
 #pragma unroll
@@ -712,21 +603,17 @@ static constexpr int kWgradBlocks = 512;
 hipError_t launch_edge_fwd(int prec, int lat, const EdgeTiles& t, const void* e_in, void* e_out, int write_e,
                            const void* Pn, const MlpW& w, float eps, float* agg, float* slots, void* a1_out,
                            hipStream_t s) {
-  // bf16 at width 128: the row-layout kernel
+  // bf16: the row-per-wave kernels
   if (prec == MGN_BF16 && lat == 128)
     return launch_edge_fwd_rows(t, e_in, e_out, write_e, Pn, w, eps, agg, slots, a1_out, s);
+  if (prec == MGN_BF16) return launch_edge_fwd_w160(t, e_in, e_out, write_e, Pn, w, eps, agg, slots, a1_out, s);
   const int g = grid_for(t.n_tiles, kEdgeFwdBlocks);
   if (!g) return hipSuccess;
-  if (prec == MGN_BF16) {
-    hipLaunchKernelGGL((k_edge_fwd<MGN_BF16, true, 160>), dim3(g), dim3(640), 0, s, t, (const bf16*)e_in,
-                       (bf16*)e_out, write_e, (const bf16*)Pn, w, eps, agg, slots, (bf16*)a1_out);
-  } else {
 #define F(LD)                                                                                                     \
-  hipLaunchKernelGGL((k_edge_fwd<MGN_FP32, false, LD>), dim3(g), dim3(LD * 4), 0, s, t, (const float*)e_in,       \
-                     (float*)e_out, write_e, (const float*)Pn, w, eps, agg, slots, (float*)nullptr)
-    MGN_BY_WIDTH(lat, F);
+  hipLaunchKernelGGL((k_edge_fwd<MGN_FP32, LD>), dim3(g), dim3(LD * 4), 0, s, t, (const float*)e_in,              \
+                     (float*)e_out, write_e, (const float*)Pn, w, eps, agg, slots)
+  MGN_BY_WIDTH(lat, F);
 #undef F
-  }
   return hipGetLastError();
 }
 
@@ -736,18 +623,14 @@ hipError_t launch_edge_bwd(int prec, int lat, const EdgeTiles& t, const void* e,
   const int g = grid_for(t.n_tiles, std::min(kEdgeBwdBlocks, part.max_blocks));
   *nblocks = g;
   if (!g) return hipSuccess;
-  if (prec == MGN_BF16) {
-    // bf16 at width 128 runs on the row-layout kernel
-    if (lat != 160) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((k_edge_bwd<MGN_BF16, false, 160>), dim3(g), dim3(640), 0, s, t, (const bf16*)e, ebar_in,
-                       have_ebar, ebar_out, (const bf16*)Pn, aggbar, w, eps, (bf16*)zbar, R, slots, part);
-  } else {
+  // bf16 runs on the row-per-wave kernels (k_edge_bwd_rows at width 128,
+  // k_edge_bwd_w160 at 160)
+  if (prec == MGN_BF16) return hipErrorInvalidValue;
 #define F(LD)                                                                                                      \
-  hipLaunchKernelGGL((k_edge_bwd<MGN_FP32, false, LD>), dim3(g), dim3(LD * 4), 0, s, t, (const float*)e, ebar_in,  \
+  hipLaunchKernelGGL((k_edge_bwd<MGN_FP32, LD>), dim3(g), dim3(LD * 4), 0, s, t, (const float*)e, ebar_in,         \
                      have_ebar, ebar_out, (const float*)Pn, aggbar, w, eps, (float*)zbar, R, slots, part)
-    MGN_BY_WIDTH(lat, F);
+  MGN_BY_WIDTH(lat, F);
 #undef F
-  }
   return hipGetLastError();
 }
 
@@ -756,18 +639,13 @@ hipError_t launch_wgrad(int prec, int lat, int64_t M, const void* Gm, const void
   const int g = grid_for((M + TM - 1) / TM, std::min(kWgradBlocks, part.max_blocks));
   *nblocks = g;
   if (!g) return hipSuccess;
-  if (prec == MGN_BF16) {
-    // bf16 at width 128 runs on the row-layout kernel
-    if (lat != 160) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((k_wgrad<MGN_BF16, 160>), dim3(g), dim3(640), 0, s, M, (const bf16*)Gm, (const bf16*)Xm,
-                       part);
-  } else {
+  // bf16 runs on k_wgrad2 (width 128) and k_wgrad2_w160
+  if (prec == MGN_BF16) return hipErrorInvalidValue;
 #define F(LD)                                                                                                     \
   hipLaunchKernelGGL((k_wgrad<MGN_FP32, LD>), dim3(g), dim3(LD * 4), 0, s, M, (const float*)Gm, (const float*)Xm, \
                      part)
-    MGN_BY_WIDTH(lat, F);
+  MGN_BY_WIDTH(lat, F);
 #undef F
-  }
   return hipGetLastError();
 }
 

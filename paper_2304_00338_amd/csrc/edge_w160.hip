@@ -415,6 +415,208 @@ k_edge_bwd_w160(EdgeTiles tl, const bf16* __restrict__ a1_in, const bf16* ebar_i
   }
 }
 
+// Forward edge phase at width 160 (bf16), one wave per 16-row half of a
+// tile: z1 = b1 + P_s[s] + P_r[r] + W1e e, a1 = relu(z1) (written when the
+// caller saves it), z2 = b2 + W2 a1, message m = gamma xhat + beta over the
+// 150 real features (padded ones are exactly 0), e_out = e + m, and the
+// receiver sums of m in ascending row order from 0.0 (in three slices of
+// features, runs {0, 1}, {2, 3}, {4}, staged per wave in fp32).  Row-permuted
+// W1e and W2 are staged in LDS with padded rows.
+namespace w160 {
+constexpr int FS = 68;  // stage row stride (floats) of a 64-feature slice
+struct __attribute__((aligned(16))) FwdLds {
+  __attribute__((aligned(16))) bf16 W1[L * LW];
+  __attribute__((aligned(16))) bf16 W2[L * LW];
+  __attribute__((aligned(16))) float b1[L];
+  __attribute__((aligned(16))) float b2[L];
+  __attribute__((aligned(16))) float g[L];
+  __attribute__((aligned(16))) float bt[L];
+  __attribute__((aligned(16))) float stage[NW][16 * FS];
+};
+}  // namespace w160
+
+__global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
+k_edge_fwd_w160(EdgeTiles tl, const bf16* __restrict__ e_in, bf16* __restrict__ e_out, int write_e,
+                const bf16* __restrict__ Pn, const bf16* __restrict__ W1p, const bf16* __restrict__ W2p,
+                const float* __restrict__ b1, const float* __restrict__ b2, const float* __restrict__ gamma,
+                const float* __restrict__ beta, float eps, float* __restrict__ agg, float* __restrict__ slots,
+                bf16* __restrict__ a1_out) {
+  using namespace w160;
+  __shared__ __align__(16) FwdLds S;
+  const int tid = threadIdx.x, lane = tid & 63, i = lane & 15, q = lane >> 4;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+  stage_w(S.W1, W1p, tid);
+  stage_w(S.W2, W2p, tid);
+  if (tid < L) {
+    S.b1[tid] = b1[tid];
+    S.b2[tid] = b2[tid];
+    S.g[tid] = gamma[tid];
+    S.bt[tid] = beta[tid];
+  }
+  __syncthreads();
+
+  const UnitRange ur = unit_range(tl.n_tiles, wv);
+  int64_t t = ur.t;
+  const int64_t stride = ur.stride, tend = ur.end;
+  const int4* tiles = reinterpret_cast<const int4*>(tl.tiles);
+  auto desc = [&](int64_t tt) -> int4 {
+    const bool ok = tt < tend;
+    const int4 v = tiles[ok ? tt : tend - 1];
+    int4 r;  // per-component selects (an aggregate select goes through scratch)
+    r.x = ok ? v.x : 0;
+    r.y = ok ? v.y : 0;
+    r.z = ok ? v.z : 0;
+    r.w = ok ? v.w : 0;
+    return r;
+  };
+  const int lastE = (int)max(tl.n_edges - 1, (int64_t)0);
+  auto nrows = [](int4 d) { return d.w - d.z; };
+  auto erow = [&](int4 d, int rb) { return min(max(d.z + min(rb * 16 + i, nrows(d) - 1), 0), lastE); };
+  // the streams of one half for this lane's row (prefetched one half ahead):
+  // the five runs of the edge latent and of the two gathered node products
+  struct HalfF {
+    uint4 e[NS], ps[NS], pr[NS];
+  };
+  auto issue_half = [&](int4 d, int rb, HalfF& H) {
+    const size_t row = (size_t)erow(d, rb);
+    const int snd = tl.senders[row], rcv = tl.receivers[row];
+    const bf16* ep = e_in + row * L + 8 * q;
+    const bf16* sp = Pn + (size_t)snd * (2 * L) + 8 * q;
+    const bf16* rp = Pn + (size_t)rcv * (2 * L) + L + 8 * q;
+#pragma unroll
+    for (int k = 0; k < NS; ++k) {
+      H.e[k] = *reinterpret_cast<const uint4*>(ep + 32 * k);
+      H.ps[k] = *reinterpret_cast<const uint4*>(sp + 32 * k);
+      H.pr[k] = *reinterpret_cast<const uint4*>(rp + 32 * k);
+    }
+  };
+  float* stage = S.stage[wv];
+  const int lv[2] = {w160::live_bits(8, q), w160::live_bits(9, q)};
+
+  auto half = [&](const HalfF& H, int4 d0, int rb, int segraw, bool chunk, int nv, int (&js)[3], float (&carry)[3]) {
+    const int n = nrows(d0);
+    const int row = rb * 16 + i;
+    const bool ok = row < n;
+    const int oz = opaque_zero();
+    const bf16* W1s = S.W1 + oz;
+    const bf16* W2s = S.W2 + oz;
+    // ---- z1 = (b1 + P_s) + P_r + W1e e
+    f32x4 acc[NOB];
+#pragma unroll
+    for (int ob = 0; ob < NOB; ++ob)
+      acc[ob] = (*reinterpret_cast<const f32x4*>(S.b1 + fo(ob, q)) + run_block5(H.ps, ob)) + run_block5(H.pr, ob);
+#pragma unroll
+    for (int s = 0; s < NS; ++s)
+#pragma unroll
+      for (int ob = 0; ob < NOB; ++ob) {
+        const bf16x8 a = *reinterpret_cast<const bf16x8*>(W1s + (ob * 16 + i) * LW + 32 * s + 8 * q);
+        acc[ob] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, as_frag(H.e[s]), acc[ob], 0, 0, 0);
+      }
+    // ---- a1 = relu(z1), the B operand of the second layer
+    bf16x8 a1[NS];
+#pragma unroll
+    for (int s = 0; s < NS; ++s)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        a1[s][r] = (bf16)relu(acc[2 * s][r]);
+        a1[s][4 + r] = (bf16)relu(acc[2 * s + 1][r]);
+      }
+    if (a1_out != nullptr && ok) {
+      bf16* ap = a1_out + ((size_t)d0.z + row) * L + 8 * q;
+#pragma unroll
+      for (int s = 0; s < NS; ++s) *reinterpret_cast<uint4*>(ap + 32 * s) = __builtin_bit_cast(uint4, a1[s]);
+    }
+    // ---- z2 = b2 + W2 a1
+#pragma unroll
+    for (int ob = 0; ob < NOB; ++ob) acc[ob] = *reinterpret_cast<const f32x4*>(S.b2 + fo(ob, q));
+#pragma unroll
+    for (int s = 0; s < NS; ++s)
+#pragma unroll
+      for (int ob = 0; ob < NOB; ++ob) {
+        const bf16x8 a = *reinterpret_cast<const bf16x8*>(W2s + (ob * 16 + i) * LW + 32 * s + 8 * q);
+        acc[ob] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, a1[s], acc[ob], 0, 0, 0);
+      }
+    // ---- LayerNorm over the 150 real features; message m = gamma xhat + beta
+    float sm = 0.f;
+#pragma unroll
+    for (int ob = 0; ob < NOB; ++ob)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) sm += acc[ob][r];
+    const float mean = sum_rowlanes(sm) * (1.0f / LR);
+    float sq = 0.f;
+#pragma unroll
+    for (int ob = 0; ob < NOB; ++ob) {
+      acc[ob] -= mean;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const bool live = ob < 8 || ((lv[ob - 8] >> r) & 1);
+        sq += live ? acc[ob][r] * acc[ob][r] : 0.f;
+      }
+    }
+    const float rstd = __builtin_amdgcn_rsqf(sum_rowlanes(sq) * (1.0f / LR) + eps);
+#pragma unroll
+    for (int ob = 0; ob < NOB; ++ob) {
+      const f32x4 ga = *reinterpret_cast<const f32x4*>(S.g + fo(ob, q));
+      const f32x4 be = *reinterpret_cast<const f32x4*>(S.bt + fo(ob, q));
+      acc[ob] = ga * (acc[ob] * rstd) + be;  // message m (exactly 0 on padded features)
+    }
+    // ---- e_out = e + m
+    if (write_e && ok) {
+      bf16* op = e_out + ((size_t)d0.z + row) * L + 8 * q;
+#pragma unroll
+      for (int s = 0; s < NS; ++s) {
+        const f32x4 lo = run_block5(H.e, 2 * s) + acc[2 * s], hi = run_block5(H.e, 2 * s + 1) + acc[2 * s + 1];
+        *reinterpret_cast<uint4*>(op + 32 * s) = __builtin_bit_cast(uint4, pack_run(lo, hi));
+      }
+    }
+    // ---- receiver sums of m, slice by slice (rows past the tile's end are
+    // never inside a segment)
+    const int lo_row = rb * 16, hi_row = lo_row + 16;
+#pragma unroll
+    for (int k = 0; k < 3; ++k) {
+      const int width = k < 2 ? 64 : 32;
+      wave_lds_sync();
+#pragma unroll
+      for (int ob = 4 * k; ob < (k < 2 ? 4 * k + 4 : NOB); ++ob)
+        *reinterpret_cast<f32x4*>(stage + i * FS + fo(ob, q) - 64 * k) = acc[ob];
+      wave_lds_sync();
+      int& j = js[k];
+      while (j < nv) {
+        const int a = chunk ? 0 : __builtin_amdgcn_readlane(segraw, j) - d0.z;
+        const int b = chunk ? n : __builtin_amdgcn_readlane(segraw, j + 1) - d0.z;
+        const int u0 = max(a, lo_row), u1 = min(b, hi_row);
+        if (lane < width)
+          for (int u = u0; u < u1; ++u) carry[k] += stage[(u - lo_row) * FS + lane];
+        if (b > hi_row) break;
+        float* dst = !chunk ? agg + (size_t)(d0.x + j) * L : slots + (size_t)(-1 - d0.y) * L;
+        if (lane < width) dst[64 * k + lane] = carry[k];
+        carry[k] = 0.f;
+        ++j;
+      }
+    }
+    wave_lds_sync();
+  };
+
+  if (t < tend) {
+    int4 d0 = desc(t);
+    HalfF A, B;
+    issue_half(d0, 0, A);
+    for (; t < tend; t += stride) {
+      const bool chunk = d0.y < 0;
+      const int nv = chunk ? 1 : d0.y - d0.x;
+      const int segraw = tl.rowptr[min(d0.x + lane, max(d0.x, d0.y))];
+      const int4 d1 = desc(t + stride);
+      issue_half(d0, 1, B);
+      int js[3] = {0, 0, 0};  // next node whose sum is open, per slice
+      float carry[3] = {0.f, 0.f, 0.f};
+      half(A, d0, 0, segraw, chunk, nv, js, carry);
+      issue_half(d1, 0, A);
+      half(B, d0, 1, segraw, chunk, nv, js, carry);
+      d0 = d1;
+    }
+  }
+}
+
 // Weight gradients of the edge MLP at width 160 from the saved bf16 streams,
 // one pass: dW1e = sum_rows zbar^T e (partials at 0) and dW2 = sum_rows
 // dz2^T a1 (at 160 * 160).  Each 32-row chunk of the four streams is staged
@@ -516,6 +718,19 @@ hipError_t launch_wgrad2_w160(int64_t M, const void* zbar, const void* e, const 
   *nblocks = g;
   hipLaunchKernelGGL(k_wgrad2_w160, dim3(g), dim3(w160::WG_NT), 0, s, M, (const bf16*)zbar, (const bf16*)e,
                      (const bf16*)dz, (const bf16*)a1, part);
+  return hipGetLastError();
+}
+
+hipError_t launch_edge_fwd_w160(const EdgeTiles& t, const void* e_in, void* e_out, int write_e, const void* Pn,
+                                const MlpW& w, float eps, float* agg, float* slots, void* a1_out, hipStream_t s) {
+  if (t.n_tiles <= 0) return hipSuccess;
+  if (!w.W1p || !w.W2p) return hipErrorInvalidValue;
+  const int64_t need = (t.n_tiles + NW - 1) / NW;
+  int g = (int)std::min<int64_t>(need, 512);
+  if (g >= 8) g &= ~7;
+  hipLaunchKernelGGL(k_edge_fwd_w160, dim3(g), dim3(NT), 0, s, t, (const bf16*)e_in, (bf16*)e_out, write_e,
+                     (const bf16*)Pn, (const bf16*)w.W1p, (const bf16*)w.W2p, w.b1, w.b2, w.gamma, w.beta, eps, agg,
+                     slots, (bf16*)a1_out);
   return hipGetLastError();
 }
 

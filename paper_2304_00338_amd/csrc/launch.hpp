@@ -80,8 +80,10 @@ hipError_t launch_pack(int prec, const float* params, void* pack, const PackList
 // Feature-split kernels: lat is the kernel width (128, or 160 for the
 // latent 150 padded with zero columns).  bf16 at width 128 runs on the
 // row-layout kernels for the edge encoder, edge phase, node phase and their
-// reverse (those launchers return hipErrorInvalidValue for it); the node
-// encoder, decoder, sender sums and node-encoder reverse serve both widths.
+// reverse, and the bf16 edge reverse at 160 on k_edge_bwd_w160 /
+// k_wgrad2_w160 (those launchers return hipErrorInvalidValue for them); the
+// node encoder, decoder, sender sums and node-encoder reverse serve both
+// widths.
 hipError_t launch_node_enc(int prec, int lat, int64_t N, const float* node_in, const MlpW& w, const MlpW* next_edge,
                            float eps, float* h_out, void* P_out, hipStream_t s);
 hipError_t launch_edge_enc(int prec, int lat, int64_t E, const float* efeat, const MlpW& w, float eps, void* e_out,
@@ -99,6 +101,11 @@ hipError_t launch_edge_fwd_rows(const EdgeTiles& t, const void* e_in, void* e_ou
 hipError_t launch_edge_bwd_rows(const EdgeTiles& t, const void* a1, const void* ebar_in, int have_ebar,
                                 void* ebar_out, const float* aggbar, const MlpW& w, float eps, void* zbar, void* dz,
                                 float* R, float* slots, const Partials& part, int* nblocks, hipStream_t s);
+// bf16 edge forward at width 160 (latent 150) with one wave per 16-row half of
+// a tile (uses MlpW::W1p, W2p and the fp32 vectors); a1_out (nullable)
+// receives the first-layer activations.
+hipError_t launch_edge_fwd_w160(const EdgeTiles& t, const void* e_in, void* e_out, int write_e, const void* Pn,
+                                const MlpW& w, float eps, float* agg, float* slots, void* a1_out, hipStream_t s);
 // bf16 edge backward at width 160 (latent 150) with one wave per 16-row half
 // of a tile, from the saved a1 (uses MlpW::W2p, W2tp, W1tp, b2, gamma); bf16
 // edge-gradient stream (in place allowed); writes zbar, dz2, R / slots and
