@@ -35,7 +35,6 @@ struct Off {
 struct PackOff {
   int64_t W1 = -1, W1t = -1, W2 = -1, W2t = -1, W1p = -1, W2p = -1;
   int64_t W1sp = -1, W1rp = -1;  // edge MLPs: row-permuted sender / receiver column blocks of W1
-  int64_t W2tp = -1, W1tp = -1;  // width 160, edge MLPs: row-permuted W2^T and W1e^T
 };
 
 struct Model {
@@ -90,9 +89,8 @@ void add_pack(Model& M, int64_t src, int rows, int cols, int64_t& W, int64_t& Wt
 }
 
 // Row-permuted copy (perm_row) of `cols` columns of a [rows][ld] matrix
-// starting at float offset src (perm 1), or the row-permuted transpose of
-// its first `rows` columns, `cols` source rows (perm 2).
-void add_perm(Model& M, int64_t src, int ld, int64_t& W, int cols = kRowsD, int rows = kRowsD, int perm = 1) {
+// starting at float offset src.
+void add_perm(Model& M, int64_t src, int ld, int64_t& W, int cols = kRowsD, int rows = kRowsD) {
   auto al = [](int64_t x) { return (x + 63) & ~int64_t(63); };
   M.pack_elems = al(M.pack_elems);
   W = M.pack_elems;
@@ -104,7 +102,7 @@ void add_perm(Model& M, int64_t src, int ld, int64_t& W, int cols = kRowsD, int 
   e.rows = rows;
   e.cols = cols;
   e.ld = ld;
-  e.perm = perm;
+  e.perm = 1;
   M.ents.push_back(e);
 }
 
@@ -141,12 +139,10 @@ Model make_model(int m, int lat) {
       add_perm(M, M.node[i].W1, 2 * D, M.p_node[i].W1p, 2 * D);
       add_perm(M, M.node[i].W2, D, M.p_node[i].W2p);
     } else {
-      // width 160 (bf16 row-per-wave edge kernels): W1's edge-latent block,
-      // W2 and the transposes of W2 and of that block, rows in perm_row order
-      add_perm(M, M.edge[i].W1, 3 * D, M.p_edge[i].W1p, D, D, 1);
-      add_perm(M, M.edge[i].W2, D, M.p_edge[i].W2p, D, D, 1);
-      add_perm(M, M.edge[i].W2, D, M.p_edge[i].W2tp, D, D, 2);
-      add_perm(M, M.edge[i].W1, 3 * D, M.p_edge[i].W1tp, D, D, 2);
+      // width 160 (bf16 row-per-wave edge kernels): W1's edge-latent block
+      // and W2, rows in perm_row order
+      add_perm(M, M.edge[i].W1, 3 * D, M.p_edge[i].W1p, D, D);
+      add_perm(M, M.edge[i].W2, D, M.p_edge[i].W2p, D, D);
     }
     add_pack(M, M.node[i].W1, D, 2 * D, M.p_node[i].W1, M.p_node[i].W1t);
     add_pack(M, M.node[i].W2, D, D, M.p_node[i].W2, M.p_node[i].W2t);
@@ -461,8 +457,6 @@ struct Run {
     w.W2p = p.W2p >= 0 ? P(p.W2p) : nullptr;
     w.W1sp = p.W1sp >= 0 ? P(p.W1sp) : nullptr;
     w.W1rp = p.W1rp >= 0 ? P(p.W1rp) : nullptr;
-    w.W2tp = p.W2tp >= 0 ? P(p.W2tp) : nullptr;
-    w.W1tp = p.W1tp >= 0 ? P(p.W1tp) : nullptr;
     w.W1 = p.W1 >= 0 ? P(p.W1) : nullptr;
     w.W1t = p.W1t >= 0 ? P(p.W1t) : nullptr;
     w.W2 = p.W2 >= 0 ? P(p.W2) : nullptr;

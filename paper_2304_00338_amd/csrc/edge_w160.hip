@@ -10,11 +10,13 @@
 // 8q + 8), s < 5.  The products run transposed (C[feature][row] = W x^T):
 // the A operand is a 16-row block of a weight matrix whose rows are in
 // perm_row order, so the C fragment of output block ob hands lane q the
-// features fo(ob, q) + r, which are again its runs.  Unlike the 128-wide
-// kernels the products with transposed weights read separately packed
-// transposed copies (W2^T in LDS, W1e^T from the cache) instead of
-// transposing LDS reads, and the LDS rows are padded to 168 elements (336
-// bytes: the 16 rows of an A fragment start in distinct 4-bank groups).
+// features fo(ob, q) + r, which are again its runs.  The forward stages its
+// weights in LDS rows padded to 168 elements (336 bytes: the 16 rows of an A
+// fragment start in distinct 4-bank groups).  The backward stages W2 and W1e
+// unpadded with the 16-byte chunks of row R rotated by R / 4 (mod 20), so
+// that both the row reads of A fragments and the transposing reads
+// (ds_read_b64_tr_b16) for the products with W2^T and W1e^T hit distinct
+// banks.
 //
 // Per half: z2 = b2 + W2 a1 from the saved first-layer activations,
 // LayerNorm statistics over the 150 real features, mbar = ebar_in +
@@ -38,11 +40,59 @@ constexpr int NS = 5;    // runs per lane
 constexpr int NOB = 10;  // 16-feature output blocks
 
 struct __attribute__((aligned(16))) Lds {
-  __attribute__((aligned(16))) bf16 W2[L * LW];
-  __attribute__((aligned(16))) bf16 W2t[L * LW];
+  __attribute__((aligned(16))) bf16 W1[L * L];  // row-permuted W1e, rotated chunks
+  __attribute__((aligned(16))) bf16 W2[L * L];  // row-permuted W2, rotated chunks
   __attribute__((aligned(16))) float b2[L];
   __attribute__((aligned(16))) float g[L];
-  __attribute__((aligned(16))) bf16 stage[NW][16 * LW];
+  __attribute__((aligned(16))) bf16 stage[NW][16 * L];
+};
+
+constexpr int CPR = L / 8;  // 16-byte chunks per row
+// Element offset of chunk C of row R in the rotated layout.
+__device__ __forceinline__ int rot(int R, int C) {
+  int p = C + (R >> 2);
+  p = p >= CPR ? p - CPR : p;
+  p = p >= CPR ? p - CPR : p;
+  return R * L + p * 8;
+}
+// Copy a row-major [160][160] bf16 matrix into LDS in the rotated layout.
+__device__ __forceinline__ void stage_rot(bf16* dst, const bf16* __restrict__ src, int tid) {
+  for (int idx = tid; idx < L * CPR; idx += NT) {
+    const int row = idx / CPR, c = idx % CPR;
+    *reinterpret_cast<uint4*>(dst + rot(row, c)) = *reinterpret_cast<const uint4*>(src + row * L + c * 8);
+  }
+}
+// Per-lane parts of the fragment addresses, so that every read is one of
+// five per-lane offsets plus an immediate.
+// A fragment of output block ob at K step s of W x: row 16 ob + i, chunk
+// 4 s + q, rotated to (4 ((s + ob) mod 5) + q + i / 4) mod 20.
+// A fragment of output block ob at K step s of W^T x from the same copy:
+// A[m][k] = W[o][k'] with k' = perm_row(16 ob + m) (the lane's output runs)
+// and o = 32 s + 8 q + 4 t + j' running over the B operand's run s; row o of
+// W sits at packed row R = 32 s + 16 t + 4 q + j', and lane 4 j' + c
+// supplies the 4 columns 32 (ob / 2) + 8 c + 4 (ob % 2) .. + 3 of it (one
+// 8-byte piece of chunk 4 (ob / 2) + c), rotated by R / 4 = 8 s + 4 t + q to
+// (4 ((ob / 2 + 2 s + t) mod 5) + c + q) mod 20.
+struct RotOff {
+  int a[5], t[5];
+  __device__ __forceinline__ RotOff(int i, int q) {
+    const int b = q + (i >> 2), bt = (i & 3) + q;
+#pragma unroll
+    for (int k = 0; k < 5; ++k) {
+      const int pa = (4 * k + b) % CPR, pt = (4 * k + bt) % CPR;
+      a[k] = i * L + pa * 8;
+      t[k] = (4 * q + (i >> 2)) * L + pt * 8;
+    }
+  }
+  __device__ __forceinline__ bf16x8 a_frag(const bf16* W, int ob, int s) const {
+    return *reinterpret_cast<const bf16x8*>(W + ob * 16 * L + a[(s + ob) % 5]);
+  }
+  __device__ __forceinline__ bf16x8 t_frag(const bf16* W, int ob, int s) const {
+    const int k = ((ob >> 1) + 2 * s) % 5, h = 4 * (ob & 1);
+    const bf16* p0 = W + 32 * s * L + t[k] + h;
+    const bf16* p1 = W + (32 * s + 16) * L + t[(k + 1) % 5] + h;
+    return cat8(lds_tr(p0), lds_tr(p1));
+  }
 };
 
 // Copy a row-major [160][160] bf16 matrix into LDS rows of stride LW.
@@ -93,16 +143,16 @@ __device__ __forceinline__ int tail_feature(int i, int q) {
 
 __global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
 k_edge_bwd_w160(EdgeTiles tl, const bf16* __restrict__ a1_in, const bf16* ebar_in, int have_ebar, bf16* ebar_out,
-                const float* __restrict__ aggbar, const bf16* __restrict__ W2p, const bf16* __restrict__ W2tp,
-                const bf16* __restrict__ W1tp, const float* __restrict__ b2, const float* __restrict__ gamma,
+                const float* __restrict__ aggbar, const bf16* __restrict__ W1p, const bf16* __restrict__ W2p,
+                const float* __restrict__ b2, const float* __restrict__ gamma,
                 float eps, bf16* __restrict__ zbar, bf16* __restrict__ dz_out, float* __restrict__ R,
                 float* __restrict__ slots, Partials part) {
   using namespace w160;
   __shared__ __align__(16) Lds S;
   const int tid = threadIdx.x, lane = tid & 63, i = lane & 15, q = lane >> 4;
   const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
-  stage_w(S.W2, W2p, tid);
-  stage_w(S.W2t, W2tp, tid);
+  stage_rot(S.W1, W1p, tid);
+  stage_rot(S.W2, W2p, tid);
   if (tid < L) {
     S.b2[tid] = b2[tid];
     S.g[tid] = gamma[tid];
@@ -160,6 +210,7 @@ k_edge_bwd_w160(EdgeTiles tl, const bf16* __restrict__ a1_in, const bf16* ebar_i
   float2 db1 = {0.f, 0.f}, db1t = {0.f, 0.f};
   bf16* stage = S.stage[wv];
   const int lv[2] = {w160::live_bits(8, q), w160::live_bits(9, q)};
+  const RotOff RO(i, q);
 
   auto half = [&](const HalfLoads& H, int recv, int4 d0, int rb, int segraw, bool chunk, int nv, int& j,
                   float2& carry, float2& carryt) {
@@ -169,8 +220,8 @@ k_edge_bwd_w160(EdgeTiles tl, const bf16* __restrict__ a1_in, const bf16* ebar_i
     // staged weights at an opaque offset: reads of them are not loop-invariant,
     // so they are not hoisted into registers
     const int oz = opaque_zero();
+    const bf16* W1s = S.W1 + oz;
     const bf16* W2s = S.W2 + oz;
-    const bf16* W2ts = S.W2t + oz;
     // ---- z2 = b2 + W2 a1 and its LayerNorm statistics (150 real features)
     f32x4 acc[NOB];
 #pragma unroll
@@ -179,8 +230,7 @@ k_edge_bwd_w160(EdgeTiles tl, const bf16* __restrict__ a1_in, const bf16* ebar_i
     for (int s = 0; s < NS; ++s)
 #pragma unroll
       for (int ob = 0; ob < NOB; ++ob) {
-        const bf16x8 a = *reinterpret_cast<const bf16x8*>(W2s + (ob * 16 + i) * LW + 32 * s + 8 * q);
-        acc[ob] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, as_frag(H.a[s]), acc[ob], 0, 0, 0);
+        acc[ob] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(RO.a_frag(W2s, ob, s), as_frag(H.a[s]), acc[ob], 0, 0, 0);
       }
     float sm = 0.f;
 #pragma unroll
@@ -276,8 +326,7 @@ k_edge_bwd_w160(EdgeTiles tl, const bf16* __restrict__ a1_in, const bf16* ebar_i
     for (int s = 0; s < NS; ++s)
 #pragma unroll
       for (int ob = 0; ob < NOB; ++ob) {
-        const bf16x8 a = *reinterpret_cast<const bf16x8*>(W2ts + (ob * 16 + i) * LW + 32 * s + 8 * q);
-        acc[ob] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, dzf[s], acc[ob], 0, 0, 0);
+        acc[ob] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(RO.t_frag(W2s, ob, s), dzf[s], acc[ob], 0, 0, 0);
       }
     bf16x8 zf[NS];
 #pragma unroll
@@ -294,20 +343,10 @@ k_edge_bwd_w160(EdgeTiles tl, const bf16* __restrict__ a1_in, const bf16* ebar_i
 #pragma unroll
       for (int s = 0; s < NS; ++s) *reinterpret_cast<uint4*>(zp + 32 * s) = __builtin_bit_cast(uint4, zf[s]);
     }
-    // W1e^T fragments come from the cache at the lane's rows ob * 16 + i:
-    // K step s of all ten output blocks at a time, the next step's loads in
-    // flight while a step multiplies (the first ones before the sums below)
-    const bf16* W1t = W1tp + oz + i * L + 8 * q;
-    auto w1t_step = [&](int s, bf16x8 (&f)[NOB]) {
-#pragma unroll
-      for (int ob = 0; ob < NOB; ++ob) f[ob] = *reinterpret_cast<const bf16x8*>(W1t + ob * 16 * L + 32 * s);
-    };
-    bf16x8 fw[2][NOB];
-    w1t_step(0, fw[0]);
     // ---- per-receiver sums of zbar (as stored) in ascending row order, and db1
     wave_lds_sync();
 #pragma unroll
-    for (int s = 0; s < NS; ++s) *reinterpret_cast<uint4*>(stage + i * LW + 32 * s + 8 * q) = __builtin_bit_cast(uint4, zf[s]);
+    for (int s = 0; s < NS; ++s) *reinterpret_cast<uint4*>(stage + i * L + 32 * s + 8 * q) = __builtin_bit_cast(uint4, zf[s]);
     wave_lds_sync();
     {
       const int lo_row = rb * 16, hi_row = lo_row + 16;
@@ -317,7 +356,7 @@ k_edge_bwd_w160(EdgeTiles tl, const bf16* __restrict__ a1_in, const bf16* ebar_i
         const int b = chunk ? n : __builtin_amdgcn_readlane(segraw, j + 1) - d0.z;
         const int u0 = max(a, lo_row), u1 = min(b, hi_row);
         for (int u = u0; u < u1; ++u) {
-          const bf16* sr = stage + (u - lo_row) * LW;
+          const bf16* sr = stage + (u - lo_row) * L;
           typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
           const bf16x2 v = *reinterpret_cast<const bf16x2*>(sr + 2 * lane);
           carry.x += (float)v[0];
@@ -349,13 +388,10 @@ k_edge_bwd_w160(EdgeTiles tl, const bf16* __restrict__ a1_in, const bf16* ebar_i
       for (int ob = 0; ob < NOB; ++ob) acc[ob] = run_block5(eb, ob);
     }
 #pragma unroll
-    for (int s = 0; s < NS; ++s) {
-      if (s + 1 < NS) w1t_step(s + 1, fw[(s + 1) & 1]);
+    for (int s = 0; s < NS; ++s)
 #pragma unroll
       for (int ob = 0; ob < NOB; ++ob)
-        acc[ob] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fw[s & 1][ob], zf[s], acc[ob], 0, 0, 0);
-      __builtin_amdgcn_sched_barrier(0);
-    }
+        acc[ob] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(RO.t_frag(W1s, ob, s), zf[s], acc[ob], 0, 0, 0);
     if (ok) {
       bf16* op = ebar_out + ((size_t)d0.z + row) * L + 8 * q;
 #pragma unroll
@@ -698,13 +734,13 @@ hipError_t launch_edge_bwd_w160(const EdgeTiles& t, const void* a1, const void* 
                                 float* R, float* slots, const Partials& part, int* nblocks, hipStream_t s) {
   *nblocks = 0;
   if (t.n_tiles <= 0) return hipSuccess;
-  if (!w.W2p || !w.W2tp || !w.W1tp || part.stride < 4 * 160) return hipErrorInvalidValue;
+  if (!w.W1p || !w.W2p || part.stride < 4 * 160) return hipErrorInvalidValue;
   const int64_t need = (t.n_tiles + NW - 1) / NW;
   int g = (int)std::min<int64_t>(need, std::min(256, part.max_blocks));
   if (g >= 8) g &= ~7;
   *nblocks = g;
   hipLaunchKernelGGL(k_edge_bwd_w160, dim3(g), dim3(NT), 0, s, t, (const bf16*)a1, (const bf16*)ebar_in, have_ebar,
-                     (bf16*)ebar_out, aggbar, (const bf16*)w.W2p, (const bf16*)w.W2tp, (const bf16*)w.W1tp, w.b2,
+                     (bf16*)ebar_out, aggbar, (const bf16*)w.W1p, (const bf16*)w.W2p, w.b2,
                      w.gamma, eps, (bf16*)zbar, (bf16*)dz, R, slots, part);
   return hipGetLastError();
 }

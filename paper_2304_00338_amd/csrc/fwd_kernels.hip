@@ -21,10 +21,8 @@ __global__ void __launch_bounds__(256) k_pack(const float* __restrict__ params, 
   const int64_t n = (int64_t)pe.rows * pe.cols;
   for (int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x; idx < n; idx += (int64_t)gridDim.x * 256) {
     const int64_t r = idx / pe.cols, c = idx % pe.cols;
-    // perm 1: row perm_row(r) of the source; perm 2: column perm_row(r) of
-    // the source (rows of its transpose, permuted)
-    const int64_t sr = pe.perm == 1 ? perm_row((int)r) : r;
-    const T v = pe.perm == 2 ? (T)params[pe.src + c * pe.ld + perm_row((int)r)] : (T)params[pe.src + sr * pe.ld + c];
+    const int64_t sr = pe.perm ? perm_row((int)r) : r;
+    const T v = (T)params[pe.src + sr * pe.ld + c];
     pack[pe.dst + idx] = v;
     if (pe.dstt >= 0) pack[pe.dstt + c * pe.rows + r] = v;
   }

@@ -15,8 +15,6 @@ struct MlpW {
   const void* W2p;   // row-permuted copy of W2
   const void* W1sp;  // edge MLPs: row-permuted sender column block of W1
   const void* W1rp;  // edge MLPs: row-permuted receiver column block of W1
-  const void* W2tp;  // width 160, edge MLPs: row-permuted W2^T
-  const void* W1tp;  // width 160, edge MLPs: row-permuted transpose of W1's edge-latent block
   const void* W1;
   const void* W1t;
   const void* W2;
@@ -35,8 +33,7 @@ struct PackEnt {
   int64_t dstt;  // element offset of the transposed copy (-1: none)
   int32_t rows, cols;
   int32_t ld;    // source row stride (floats)
-  int32_t perm;  // 1: copy row perm_row(p) of the source into row p;
-                 // 2: copy column perm_row(p) of the source into row p
+  int32_t perm;  // 1: copy row perm_row(p) of the source into row p
 };
 
 // Output-row order of the weights used by the row-per-wave edge kernels:
@@ -107,7 +104,7 @@ hipError_t launch_edge_bwd_rows(const EdgeTiles& t, const void* a1, const void* 
 hipError_t launch_edge_fwd_w160(const EdgeTiles& t, const void* e_in, void* e_out, int write_e, const void* Pn,
                                 const MlpW& w, float eps, float* agg, float* slots, void* a1_out, hipStream_t s);
 // bf16 edge backward at width 160 (latent 150) with one wave per 16-row half
-// of a tile, from the saved a1 (uses MlpW::W2p, W2tp, W1tp, b2, gamma); bf16
+// of a tile, from the saved a1 (uses MlpW::W1p, W2p, b2, gamma); bf16
 // edge-gradient stream (in place allowed); writes zbar, dz2, R / slots and
 // per-block partials [db1 | db2 | dgamma | dbeta] (4 x 160 floats).
 hipError_t launch_edge_bwd_w160(const EdgeTiles& t, const void* a1, const void* ebar_in, int have_ebar,
