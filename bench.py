@@ -47,18 +47,29 @@ MFMA_PEAK_FP32_TFLOPS = 157.3
 
 
 def edge_bwd_split_roofline(prec, D, N, E, m, avg_ms):
-    """Position of the feature-split edge backward (latent width D, one
-    launch per MP block) against both roofs: algorithmic bytes per launch
-    (per edge: e, the incoming edge gradient except in the last block, the
-    outgoing one and z-bar, sender / receiver ids; per node: P, the gathered
-    aggregate gradient and R) and executed MFMA flop (per edge: 5 products
-    of D x D -- the recomputed W1e e and W2 a1, W2^T dz2, W1e^T zbar and the
-    dW2 accumulation), each divided by the average launch time."""
-    t = 2 if prec == "bf16" else 4
-    per_edge = [D * t + (D * 4 if l < m - 1 else 0) + D * 4 + D * t + 8 for l in range(m)]
-    nbytes = float(np.mean(per_edge)) * E + N * (2 * D * t + D * 4 + D * 4)
-    flop = 10.0 * D * D * E
-    peak = MFMA_PEAK_BF16_TFLOPS if prec == "bf16" else MFMA_PEAK_FP32_TFLOPS
+    """Position of the edge backward at latent width D (one launch per MP
+    block) against both roofs: algorithmic bytes and executed MFMA flop per
+    launch, each divided by the average launch time.
+    fp32 (feature-split kernel): per edge e, the incoming edge gradient (not
+    in the last block), the outgoing one and z-bar (fp32), sender / receiver
+    ids; per node P, the gathered aggregate gradient and R; 5 products of
+    D x D per edge (the recomputed W1e e and W2 a1, W2^T dz2, W1e^T zbar and
+    the dW2 accumulation).
+    bf16 (row-per-wave kernel): per edge the saved a1, the incoming edge
+    gradient (not in the last block), the outgoing one, zbar and dz2 (bf16),
+    the receiver id; per node the gathered aggregate gradient and R (fp32);
+    3 products of D x D per edge (W2 a1, W2^T dz2, W1e^T zbar)."""
+    if prec == "bf16":
+        per_edge = [D * 2 + (D * 2 if l < m - 1 else 0) + 3 * D * 2 + 4 for l in range(m)]
+        per_node = 2 * D * 4
+        flop = 6.0 * D * D * E
+        peak = MFMA_PEAK_BF16_TFLOPS
+    else:
+        per_edge = [D * 4 + (D * 4 if l < m - 1 else 0) + D * 4 + D * 4 + 8 for l in range(m)]
+        per_node = 2 * D * 4 + D * 4 + D * 4
+        flop = 10.0 * D * D * E
+        peak = MFMA_PEAK_FP32_TFLOPS
+    nbytes = float(np.mean(per_edge)) * E + N * per_node
     gbs = nbytes / (avg_ms * 1e-3) / 1e9
     tfs = flop / (avg_ms * 1e-3) / 1e12
     return {"kernel": "edge_bwd", "avg_launch_ms": round(avg_ms, 4),
