@@ -363,11 +363,10 @@ __global__ void __launch_bounds__(LD * 4) k_node_srcsum(int64_t N, const int32_t
 }
 
 // ------------------------------------------------------- encoders
-// ybar: dL/d(encoder output), fp32 or (the bf16 edge-gradient stream at
-// width 160) bf16.
-template <int PREC, int LD, int KIN, typename YT = float>
+// ybar: dL/d(encoder output), fp32.
+template <int PREC, int LD, int KIN>
 __global__ void __launch_bounds__(LD * 4) k_enc_bwd(int64_t M, const float* __restrict__ x_in,
-                                                const YT* __restrict__ ybar, MlpW w, float eps,
+                                                const float* __restrict__ ybar, MlpW w, float eps,
                                                 float* __restrict__ gin, Partials part) {
   typedef Tr<PREC> P;
   typedef typename P::T T;
@@ -428,7 +427,7 @@ __global__ void __launch_bounds__(LD * 4) k_enc_bwd(int64_t M, const float* __re
       for (int r = 0; r < 4; ++r) {
         const int row = rb * 16 + q * 4 + r;
         xh[rb][r] = (acc[rb][r] - mean[rb][r]) * rstd[rb][r];
-        yb[rb][r] = row < nr ? tof(ybar[(size_t)(r0 + row) * D + n]) : 0.f;
+        yb[rb][r] = row < nr ? ybar[(size_t)(r0 + row) * D + n] : 0.f;
         dg += yb[rb][r] * xh[rb][r];
         dbt += yb[rb][r];
       }
@@ -588,21 +587,20 @@ hipError_t launch_node_srcsum(int prec, int lat, int64_t N, const int32_t* rowpt
 
 hipError_t launch_edge_enc_bwd(int prec, int lat, int64_t E, const float* efeat, const void* ebar, const MlpW& w,
                                float eps, const Partials& part, int* nblocks, hipStream_t s) {
+  if (prec == MGN_BF16) {
+    // bf16 runs on the row-layout kernels (launch_edge_enc_bwd_rows at width 128)
+    *nblocks = 0;
+    if (lat != 160) return hipErrorInvalidValue;
+    return launch_edge_enc_bwd_w160(E, efeat, ebar, w, eps, part, nblocks, s);
+  }
   const int g = bwd_grid((E + TM - 1) / TM, part);
   *nblocks = g;
   if (!g) return hipSuccess;
-  if (prec == MGN_BF16) {
-    // bf16 at width 128 runs on the row-layout kernel
-    if (lat != 160) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((k_enc_bwd<MGN_BF16, 160, 4, bf16>), dim3(g), dim3(640), 0, s, E, efeat, (const bf16*)ebar, w,
-                       eps, (float*)nullptr, part);
-  } else {
 #define F(LD)                                                                                                      \
   hipLaunchKernelGGL((k_enc_bwd<MGN_FP32, LD, 4>), dim3(g), dim3(LD * 4), 0, s, E, efeat, (const float*)ebar, w,   \
                      eps, (float*)nullptr, part)
-    MGN_BY_WIDTH(lat, F);
+  MGN_BY_WIDTH(lat, F);
 #undef F
-  }
   return hipGetLastError();
 }
 

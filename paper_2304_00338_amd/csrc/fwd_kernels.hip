@@ -347,17 +347,16 @@ hipError_t launch_node_enc(int prec, int lat, int64_t N, const float* x, const M
 
 hipError_t launch_edge_enc(int prec, int lat, int64_t E, const float* f, const MlpW& w, float eps, void* e_out,
                            hipStream_t s) {
+  if (prec == MGN_BF16) {
+    // bf16 runs on the row-layout kernels (launch_edge_enc_rows at width 128)
+    if (lat != 160) return hipErrorInvalidValue;
+    return launch_edge_enc_w160(E, f, w, eps, e_out, s);
+  }
   const int g = grid_for((E + TM - 1) / TM, kFwdBlocks);
   if (!g) return hipSuccess;
-  if (prec == MGN_BF16) {
-    // bf16 at width 128 runs on the row-layout kernel
-    if (lat != 160) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((k_edge_enc<MGN_BF16, 160>), dim3(g), dim3(640), 0, s, E, f, w, eps, (bf16*)e_out);
-  } else {
 #define F(LD) hipLaunchKernelGGL((k_edge_enc<MGN_FP32, LD>), dim3(g), dim3(LD * 4), 0, s, E, f, w, eps, (float*)e_out)
-    MGN_BY_WIDTH(lat, F);
+  MGN_BY_WIDTH(lat, F);
 #undef F
-  }
   return hipGetLastError();
 }
 
