@@ -22,9 +22,9 @@ constexpr int kPartBlocks = 512;  // persistent blocks of the backward kernels
 // Largest per-block partial at kernel width LD: the node MLP's parameters,
 // W1 [LD][2 LD], b1, W2 [LD][LD], b2, gamma, beta.
 inline int64_t part_stride(int LD) { return 3LL * LD * LD + 4LL * LD; }
-// bf16 node-MLP partial layout (width 128) = its parameter order: W1
-// [128][256], b1, W2, b2 (49408 floats), then gamma, beta
-constexpr int kNodeGammaPart = 49408;
+// Offset of dgamma in the node MLP's parameters (and per-block partials):
+// W1 [D][2D], b1, W2 [D][D], b2 precede it.
+constexpr int64_t node_gamma_part(int D) { return (int64_t)3 * D * D + 2 * D; }
 // the row-layout (bf16) kernels' fixed latent width
 constexpr int kRowsD = 128;
 
@@ -35,6 +35,7 @@ struct Off {
 struct PackOff {
   int64_t W1 = -1, W1t = -1, W2 = -1, W2t = -1, W1p = -1, W2p = -1;
   int64_t W1sp = -1, W1rp = -1;  // edge MLPs: row-permuted sender / receiver column blocks of W1
+  int64_t W1ap = -1;             // node MLPs at width 160: row-permuted agg column block of W1
 };
 
 struct Model {
@@ -143,6 +144,10 @@ Model make_model(int m, int lat) {
       // and W2, rows in perm_row order
       add_perm(M, M.edge[i].W1, 3 * D, M.p_edge[i].W1p, D, D);
       add_perm(M, M.edge[i].W2, D, M.p_edge[i].W2p, D, D);
+      // node MLP: W1's h and agg column blocks and W2
+      add_perm(M, M.node[i].W1, 2 * D, M.p_node[i].W1p, D, D);
+      add_perm(M, M.node[i].W1 + D, 2 * D, M.p_node[i].W1ap, D, D);
+      add_perm(M, M.node[i].W2, D, M.p_node[i].W2p, D, D);
     }
     add_pack(M, M.node[i].W1, D, 2 * D, M.p_node[i].W1, M.p_node[i].W1t);
     add_pack(M, M.node[i].W2, D, D, M.p_node[i].W2, M.p_node[i].W2t);
@@ -361,7 +366,7 @@ void plan(Ctx& c) {
     o = al256(o + (keep_a1 ? (size_t)E * D * 2 : 0));
     // bf16 node backward: the a1, dz2, dz1 streams of one node MLP
     L.nstr = o;
-    o = al256(o + (keep_a1 && rows ? (size_t)3 * N * D * 2 : 0));
+    o = al256(o + (keep_a1 ? (size_t)3 * N * D * 2 : 0));
     L.hb_a = o;
     o = al256(o + (size_t)N * D * 4);
     L.hb_b = o;
@@ -457,6 +462,7 @@ struct Run {
     w.W2p = p.W2p >= 0 ? P(p.W2p) : nullptr;
     w.W1sp = p.W1sp >= 0 ? P(p.W1sp) : nullptr;
     w.W1rp = p.W1rp >= 0 ? P(p.W1rp) : nullptr;
+    w.W1ap = p.W1ap >= 0 ? P(p.W1ap) : nullptr;
     w.W1 = p.W1 >= 0 ? P(p.W1) : nullptr;
     w.W1t = p.W1t >= 0 ? P(p.W1t) : nullptr;
     w.W2 = p.W2 >= 0 ? P(p.W2) : nullptr;
@@ -555,14 +561,24 @@ struct Run {
     for (int l = m - 1; l >= 0; --l) {
       const Off& oe = M.edge[l];
       const Off& on = M.node[l];
-      if (rows()) {
+      if (prec == MGN_BF16) {
+        // one wave per 16-node unit, then the weight gradients from its
+        // a1 / dz2 / dz1 streams
         char* ns = ws + c.L.nstr;
         void *na1 = ns, *ndz2 = ns + (size_t)N * D * 2, *ndz1 = ns + (size_t)2 * N * D * 2;
-        LAUNCH(K_NODE_BWD, launch_node_bwd_rows(N, h_l(k, l), agg_l(k, l), hb_cur, W(on, M.p_node[l]), eps, hb_part, aggbar,
-                                     na1, ndz2, ndz1, pt, &nb, s));
-        if ((rc = reduce(nb, kNodeGammaPart, 1, 2 * D, grad, on.g, 0)) != MGN_OK) return rc;
-        LAUNCH(K_WGRAD_NODE, launch_wgrad_node(N, h_l(k, l), agg_l(k, l), ndz1, ndz2, na1, pt, &nb, s));
-        if ((rc = reduce(nb, 0, 1, kNodeGammaPart, grad, on.W1, 0)) != MGN_OK) return rc;
+        const int64_t gpart = node_gamma_part(D);
+        if (rows())
+          LAUNCH(K_NODE_BWD, launch_node_bwd_rows(N, h_l(k, l), agg_l(k, l), hb_cur, W(on, M.p_node[l]), eps, hb_part,
+                                                  aggbar, na1, ndz2, ndz1, pt, &nb, s));
+        else
+          LAUNCH(K_NODE_BWD, launch_node_bwd_w160(N, h_l(k, l), agg_l(k, l), hb_cur, W(on, M.p_node[l]), eps, hb_part,
+                                                  aggbar, na1, ndz2, ndz1, pt, &nb, s));
+        if ((rc = reduce(nb, gpart, 1, 2 * D, grad, on.g, 0)) != MGN_OK) return rc;
+        if (rows())
+          LAUNCH(K_WGRAD_NODE, launch_wgrad_node(N, h_l(k, l), agg_l(k, l), ndz1, ndz2, na1, pt, &nb, s));
+        else
+          LAUNCH(K_WGRAD_NODE, launch_wgrad_node_w160(N, h_l(k, l), agg_l(k, l), ndz1, ndz2, na1, pt, &nb, s));
+        if ((rc = reduce(nb, 0, 1, (int)gpart, grad, on.W1, 0)) != MGN_OK) return rc;
       } else {
         LAUNCH(K_NODE_BWD, launch_node_bwd(prec, D, N, h_l(k, l), agg_l(k, l), hb_cur, W(on, M.p_node[l]), eps, hb_part, aggbar,
                                 pt, &nb, s));

@@ -553,7 +553,6 @@ k_edge_fwd_w160(EdgeTiles tl, const bf16* __restrict__ e_in, bf16* __restrict__ 
 // 16) of both matrices and reads its MFMA operands with K = the chunk's rows
 // through ds_read_b64_tr_b16.
 namespace w160 {
-constexpr int WG_LD = 176;
 constexpr int WG_NT = 640;
 }  // namespace w160
 

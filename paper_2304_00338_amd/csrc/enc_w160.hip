@@ -26,7 +26,7 @@ namespace dev {
 
 namespace w160 {
 constexpr int KE = 4;      // edge input features
-constexpr int ESL = 176;   // LDS row stride of the staged [rows][160] bf16 tiles
+constexpr int ESL = WG_LD;  // LDS row stride of the staged [rows][160] bf16 tiles
 constexpr int SUB = 64;    // rows staged per sub-round (4 units)
 constexpr int PCOL = 160;  // a1 tile columns 160..175: the input pieces
 
@@ -49,11 +49,6 @@ __device__ __forceinline__ void stage_enc(EncLds& S, const MlpW& w, int tid) {
     S.bt[tid] = w.beta[tid];
   }
 }
-
-// Lane-independent part of fo(ob, q) (fo(ob, q) = 8 q + fo0(ob)): LDS
-// reads at a per-lane base plus this constant fold the constant into the
-// instruction's offset.
-__device__ __forceinline__ constexpr int fo0(int ob) { return 32 * (ob >> 1) + 4 * (ob & 1); }
 
 // z1 = b1 + W1 f for the lane's 40 features (fo(ob, q) + r).
 __device__ __forceinline__ void enc_z1(const EncLds& S, float4 f, int q, f32x4 (&z)[NOB]) {

@@ -15,6 +15,7 @@ struct MlpW {
   const void* W2p;   // row-permuted copy of W2
   const void* W1sp;  // edge MLPs: row-permuted sender column block of W1
   const void* W1rp;  // edge MLPs: row-permuted receiver column block of W1
+  const void* W1ap;  // node MLPs at width 160: row-permuted agg column block of W1 (W1p: the h block)
   const void* W1;
   const void* W1t;
   const void* W2;
@@ -131,6 +132,14 @@ hipError_t launch_node_bwd_rows(int64_t N, const float* h, const float* agg, con
 // bf16 node-MLP weight gradients dW1, db1, dW2, db2 from those streams.
 hipError_t launch_wgrad_node(int64_t N, const float* h, const float* agg, const void* dz1, const void* dz2,
                              const void* a1, const Partials& part, int* nblocks, hipStream_t s);
+// bf16 node phase reverse at width 160 (latent 150): the node backward
+// writes the a1 / dz2 / dz1 streams and the dgamma / dbeta partials, the
+// weight-gradient pass (two launches on one grid) the other partials.
+hipError_t launch_node_bwd_w160(int64_t N, const float* h, const float* agg, const float* hbar_in, const MlpW& w,
+                                float eps, float* hbar_part, float* aggbar, void* a1, void* dz2, void* dz1,
+                                const Partials& part, int* nblocks, hipStream_t s);
+hipError_t launch_wgrad_node_w160(int64_t N, const float* h, const float* agg, const void* dz1, const void* dz2,
+                                  const void* a1, const Partials& part, int* nblocks, hipStream_t s);
 // bf16 edge encoder in the row layout (uses MlpW::W2p and the fp32 W1f).
 hipError_t launch_edge_enc_rows(int64_t E, const float* efeat, const MlpW& w, float eps, void* e_out, hipStream_t s);
 // bf16 edge-encoder backward from the bf16 edge-gradient stream: per-block

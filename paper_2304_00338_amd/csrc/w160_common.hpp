@@ -25,6 +25,15 @@ constexpr int NS = 5;    // runs per lane
 constexpr int NOB = 10;  // 16-feature output blocks
 
 constexpr int CPR = L / 8;  // 16-byte chunks per row
+// LDS row stride (elements) of staged [rows][160] bf16 tiles read by
+// transposing reads (ds_read_b64_tr_b16 at 8 rows x 4 columns per 16 lanes):
+// 352-byte rows keep those reads free of bank conflicts.
+constexpr int WG_LD = 176;
+
+// Lane-independent part of fo(ob, q) (fo(ob, q) = 8 q + fo0(ob)): LDS
+// reads at a per-lane base plus this constant fold the constant into the
+// instruction's offset.
+__device__ __forceinline__ constexpr int fo0(int ob) { return 32 * (ob >> 1) + 4 * (ob & 1); }
 // Element offset of chunk C of row R in the rotated layout.
 __device__ __forceinline__ int rot(int R, int C) {
   int p = C + (R >> 2);
