@@ -144,6 +144,8 @@ Model make_model(int m, int lat) {
       // and W2, rows in perm_row order
       add_perm(M, M.edge[i].W1, 3 * D, M.p_edge[i].W1p, D, D);
       add_perm(M, M.edge[i].W2, D, M.p_edge[i].W2p, D, D);
+      add_perm(M, M.edge[i].W1 + D, 3 * D, M.p_edge[i].W1sp, D, D);
+      add_perm(M, M.edge[i].W1 + 2 * D, 3 * D, M.p_edge[i].W1rp, D, D);
       // node MLP: W1's h and agg column blocks and W2
       add_perm(M, M.node[i].W1, 2 * D, M.p_node[i].W1p, D, D);
       add_perm(M, M.node[i].W1 + D, 2 * D, M.p_node[i].W1ap, D, D);
@@ -531,6 +533,9 @@ struct Run {
       if (rows()) {
         LAUNCH(K_NODE_FWD, launch_node_fwd_rows(N, h_l(k, l), agg_l(k, l), W(M.node[l], M.p_node[l]), eps, h_l(k, l + 1), s));
         if (!last) LAUNCH(K_EMIT, launch_emit_rows(N, h_l(k, l + 1), nx, P_l(k, l + 1), s));
+      } else if (prec == MGN_BF16) {
+        LAUNCH(K_NODE_FWD, launch_node_fwd_w160(N, h_l(k, l), agg_l(k, l), W(M.node[l], M.p_node[l]), eps, h_l(k, l + 1), s));
+        if (!last) LAUNCH(K_EMIT, launch_emit_w160(N, h_l(k, l + 1), nx, P_l(k, l + 1), s));
       } else {
         LAUNCH(K_NODE_FWD, launch_node_fwd(prec, D, N, h_l(k, l), agg_l(k, l), W(M.node[l], M.p_node[l]), last ? nullptr : &nx,
                                 eps, h_l(k, l + 1), last ? nullptr : P_l(k, l + 1), s));

@@ -374,16 +374,8 @@ hipError_t launch_node_fwd(int prec, int lat, int64_t N, const float* h_in, cons
   const int g = grid_for((N + TM - 1) / TM, kFwdBlocks);
   if (!g) return hipSuccess;
   const MlpW nn = nx ? *nx : w;
-  if (prec == MGN_BF16) {
-    // bf16 at width 128 runs on the row-layout kernel
-    if (lat != 160) return hipErrorInvalidValue;
-    if (nx)
-      hipLaunchKernelGGL((k_node_fwd<MGN_BF16, 160, true>), dim3(g), dim3(640), 0, s, N, h_in, agg, w, nn, eps, h_out,
-                         (bf16*)P_out);
-    else
-      hipLaunchKernelGGL((k_node_fwd<MGN_BF16, 160, false>), dim3(g), dim3(640), 0, s, N, h_in, agg, w, nn, eps, h_out,
-                         (bf16*)P_out);
-  } else {
+  // bf16 runs on the row-layout kernels (launch_node_fwd_rows / _w160)
+  if (prec == MGN_BF16) return hipErrorInvalidValue;
 #define F(LD)                                                                                                        \
   if (nx)                                                                                                            \
     hipLaunchKernelGGL((k_node_fwd<MGN_FP32, LD, true>), dim3(g), dim3(LD * 4), 0, s, N, h_in, agg, w, nn, eps,      \
@@ -391,9 +383,8 @@ hipError_t launch_node_fwd(int prec, int lat, int64_t N, const float* h_in, cons
   else                                                                                                               \
     hipLaunchKernelGGL((k_node_fwd<MGN_FP32, LD, false>), dim3(g), dim3(LD * 4), 0, s, N, h_in, agg, w, nn, eps,     \
                        h_out, (float*)P_out)
-    MGN_BY_WIDTH(lat, F);
+  MGN_BY_WIDTH(lat, F);
 #undef F
-  }
   return hipGetLastError();
 }
 

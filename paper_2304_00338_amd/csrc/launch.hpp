@@ -140,6 +140,11 @@ hipError_t launch_node_bwd_w160(int64_t N, const float* h, const float* agg, con
                                 const Partials& part, int* nblocks, hipStream_t s);
 hipError_t launch_wgrad_node_w160(int64_t N, const float* h, const float* agg, const void* dz1, const void* dz2,
                                   const void* a1, const Partials& part, int* nblocks, hipStream_t s);
+// bf16 node phase forward at width 160: h_out (may alias h_in), and the
+// next edge layer's node products P (uses its MlpW::W1sp / W1rp).
+hipError_t launch_node_fwd_w160(int64_t N, const float* h_in, const float* agg, const MlpW& w, float eps,
+                                float* h_out, hipStream_t s);
+hipError_t launch_emit_w160(int64_t N, const float* h, const MlpW& next_edge, void* P, hipStream_t s);
 // bf16 edge encoder in the row layout (uses MlpW::W2p and the fp32 W1f).
 hipError_t launch_edge_enc_rows(int64_t E, const float* efeat, const MlpW& w, float eps, void* e_out, hipStream_t s);
 // bf16 edge-encoder backward from the bf16 edge-gradient stream: per-block

@@ -1,8 +1,9 @@
-// Node phase of one MGN message-passing step, reverse, bf16 operands, at the
+// Node phase of one MGN message-passing step, bf16 operands, at the
 // latent width 150 computed 160 wide (App. C: the 3D model; padded features
 // are exactly zero), in the lane layout of w160_common.hpp (Sec. 2.1: every
 // node latent is updated by the node MLP from itself and the sum of its
-// incoming messages, with a residual connection; this is the reverse).
+// incoming messages, with a residual connection; the first layer of the next
+// edge MLP is split into per-node products).
 //
 //   k_node_bwd_w160    one wave per 16-node unit: recomputes the MLP from h
 //                      and agg, writes a1 = relu(z1), dz2 = dL/dz2 and
@@ -12,6 +13,9 @@
 //                      of dgamma, dbeta
 //   k_wgrad_node_w160  dW1 = sum dz1^T [h; agg], db1 (pass 0) and
 //                      dW2 = sum dz2^T a1, db2 (pass 1) from those streams
+//   k_node_fwd_w160    the forward: h_out = h + LN(W2 relu(W1 [h; agg] + b1)
+//                      + b2) over the 150 real features
+//   k_emit_w160        P = [W1s h; W1r h] of the next edge layer
 //
 // W1 = [W1h W1a] (the columns acting on h and on agg), each block and W2
 // staged row-permuted in the rotated layout (153.6 KB of LDS).
@@ -418,6 +422,119 @@ __global__ void __launch_bounds__(w160::WN_NT) k_wgrad_node_w160(int64_t N, cons
   }
 }
 
+
+// ===================================================================== forward
+// h_out = h_in + LN(MLP([h_in, agg])); h_out may alias h_in (each row is
+// read before it is written, by the same lane).
+__global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
+k_node_fwd_w160(int64_t N, const float* h_in, const float* __restrict__ agg, MlpW w, float eps, float* h_out) {
+  using namespace w160;
+  __shared__ __align__(16) NodeLds S;
+  const int tid = threadIdx.x, lane = tid & 63, i = lane & 15, q = lane >> 4;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+  stage_node(S, w, tid, true);
+  const int lv[2] = {live_bits(8, q), live_bits(9, q)};
+  __syncthreads();
+  const int64_t nu = (N + 15) >> 4;
+  const UnitRange ur = unit_range(nu, wv);
+  if (ur.t >= ur.end) return;
+  auto rowp = [&](int64_t u) -> int64_t { return min(u * 16 + i, N - 1) * L + 8 * q; };
+  auto pack5 = [&](const f32x4 (&v)[NOB], bf16x8* x) {
+#pragma unroll
+    for (int s = 0; s < NS; ++s) x[s] = pack_run(v[2 * s], v[2 * s + 1]);
+  };
+  // hr: the unit's h rows in fp32 (the residual); the next unit's h is in
+  // flight from the first product on, its agg from the LayerNorm on
+  f32x4 hr[NOB], an[NOB];
+  load_row10(h_in + rowp(ur.t), hr);
+  load_row10(agg + rowp(ur.t), an);
+  for (int64_t u = ur.t; u < ur.end; u += ur.stride) {
+    const int64_t p = rowp(u);
+    const int oz = opaque_zero();
+    bf16x8 x[2 * NS];
+    pack5(hr, x);
+    pack5(an, x + NS);
+    f32x4 acc[NOB];
+    node_z1(S, S.W1h + oz, S.W1a + oz, RotOff(i + oz, q), x, q, acc);
+    f32x4 hn[NOB];
+    load_row10(h_in + rowp(u + ur.stride), hn);
+    bf16x8 a1[NS];
+#pragma unroll
+    for (int s = 0; s < NS; ++s)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        a1[s][r] = (bf16)relu(acc[2 * s][r]);
+        a1[s][4 + r] = (bf16)relu(acc[2 * s + 1][r]);
+      }
+    node_z2(S, S.W2 + oz, RotOff(i + oz, q), a1, q, acc);
+    ln_xhat150(acc, lv, eps);
+    load_row10(agg + rowp(u + ur.stride), an);
+    const float* gq = S.g + 8 * q;
+    const float* bq = S.bt + 8 * q;
+#pragma unroll
+    for (int ob = 0; ob < NOB; ++ob)
+      acc[ob] = hr[ob] + (*reinterpret_cast<const f32x4*>(gq + fo0(ob)) * acc[ob] +
+                          *reinterpret_cast<const f32x4*>(bq + fo0(ob)));
+    if (u * 16 + i < N) store_row10(h_out + p, acc);
+#pragma unroll
+    for (int ob = 0; ob < NOB; ++ob) hr[ob] = hn[ob];
+  }
+}
+
+// P[v] = [W1s h[v]; W1r h[v]] in bf16 for the next edge layer (W1s, W1r:
+// its row-permuted sender / receiver column blocks, rotated in LDS).
+namespace w160 {
+struct __attribute__((aligned(16))) EmitLds {
+  __attribute__((aligned(16))) bf16 Ws[L * L];
+  __attribute__((aligned(16))) bf16 Wr[L * L];
+};
+}  // namespace w160
+
+__global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
+k_emit_w160(int64_t N, const float* __restrict__ h, MlpW nx, bf16* __restrict__ P) {
+  using namespace w160;
+  __shared__ __align__(16) EmitLds S;
+  const int tid = threadIdx.x, lane = tid & 63, i = lane & 15, q = lane >> 4;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+  stage_rot(S.Ws, (const bf16*)nx.W1sp, tid);
+  stage_rot(S.Wr, (const bf16*)nx.W1rp, tid);
+  __syncthreads();
+  const int64_t nu = (N + 15) >> 4;
+  const UnitRange ur = unit_range(nu, wv);
+  if (ur.t >= ur.end) return;
+  auto rowp = [&](int64_t u) -> int64_t { return min(u * 16 + i, N - 1) * L + 8 * q; };
+  f32x4 hv[NOB];
+  load_row10(h + rowp(ur.t), hv);
+  for (int64_t u = ur.t; u < ur.end; u += ur.stride) {
+    const int oz = opaque_zero();
+    const RotOff RO(i + oz, q);
+    bf16x8 x[NS];
+#pragma unroll
+    for (int s = 0; s < NS; ++s) x[s] = pack_run(hv[2 * s], hv[2 * s + 1]);
+    load_row10(h + rowp(u + ur.stride), hv);
+    const bool ok = u * 16 + i < N;
+    bf16* out = P + min(u * 16 + i, N - 1) * (2 * L) + 8 * q;
+#pragma unroll
+    for (int part = 0; part < 2; ++part) {
+      const bf16* W = (part == 0 ? S.Ws : S.Wr) + oz;
+      f32x4 acc[NOB];
+#pragma unroll
+      for (int ob = 0; ob < NOB; ++ob) acc[ob] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < NS; ++s) {
+#pragma unroll
+        for (int ob = 0; ob < NOB; ++ob)
+          acc[ob] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(RO.a_frag(W, ob, s), x[s], acc[ob], 0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      bf16x8 o[NS];
+#pragma unroll
+      for (int s = 0; s < NS; ++s) o[s] = pack_run(acc[2 * s], acc[2 * s + 1]);
+      if (ok) store_runs5(out + part * L, o);
+    }
+  }
+}
+
 }  // namespace dev
 
 using namespace dev;
@@ -450,6 +567,27 @@ hipError_t launch_wgrad_node_w160(int64_t N, const float* h, const float* agg, c
                      (const bf16*)nullptr, part);
   hipLaunchKernelGGL(k_wgrad_node_w160<1>, dim3(g), dim3(w160::WN_NT), 0, s, N, h, agg, (const bf16*)dz2,
                      (const bf16*)a1, part);
+  return hipGetLastError();
+}
+
+hipError_t launch_node_fwd_w160(int64_t N, const float* h_in, const float* agg, const MlpW& w, float eps,
+                                float* h_out, hipStream_t s) {
+  if (N <= 0) return hipSuccess;
+  if (!w.W1p || !w.W1ap || !w.W2p) return hipErrorInvalidValue;
+  const int64_t need = (((N + 15) >> 4) + NW - 1) / NW;
+  int g = (int)std::min<int64_t>(need, kNodeBlocks160);
+  if (g >= 8) g &= ~7;
+  hipLaunchKernelGGL(k_node_fwd_w160, dim3(g), dim3(NT), 0, s, N, h_in, agg, w, eps, h_out);
+  return hipGetLastError();
+}
+
+hipError_t launch_emit_w160(int64_t N, const float* h, const MlpW& next_edge, void* P, hipStream_t s) {
+  if (N <= 0) return hipSuccess;
+  if (!next_edge.W1sp || !next_edge.W1rp) return hipErrorInvalidValue;
+  const int64_t need = (((N + 15) >> 4) + NW - 1) / NW;
+  int g = (int)std::min<int64_t>(need, kNodeBlocks160);
+  if (g >= 8) g &= ~7;
+  hipLaunchKernelGGL(k_emit_w160, dim3(g), dim3(NT), 0, s, N, h, next_edge, (bf16*)P);
   return hipGetLastError();
 }
 
