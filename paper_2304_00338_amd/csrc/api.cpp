@@ -125,6 +125,7 @@ Model make_model(int m, int lat) {
   M.total = o;
   const bool rows = lat == kRowsD;  // row-permuted copies for the row-layout kernels
   add_pack(M, M.enc_node.W2, D, D, M.p_enc_node.W2, M.p_enc_node.W2t);
+  if (!rows) add_perm(M, M.enc_node.W2, D, M.p_enc_node.W2p, D, D);  // width-160 node encoder backward
   add_pack(M, M.enc_edge.W2, D, D, M.p_enc_edge.W2, M.p_enc_edge.W2t);
   add_perm(M, M.enc_edge.W2, D, M.p_enc_edge.W2p, D, D);  // row-layout edge encoders
   M.p_edge.resize(m);

@@ -606,14 +606,12 @@ hipError_t launch_edge_enc_bwd(int prec, int lat, int64_t E, const float* efeat,
 
 hipError_t launch_node_enc_bwd(int prec, int lat, int64_t N, const float* node_in, const float* hbar, const MlpW& w,
                                float eps, float* gin, const Partials& part, int* nblocks, hipStream_t s) {
+  if (prec == MGN_BF16 && lat == 160) return launch_node_enc_bwd_w160(N, node_in, hbar, w, eps, gin, part, nblocks, s);
   const int g = bwd_grid((N + TM - 1) / TM, part);
   *nblocks = g;
   if (!g) return hipSuccess;
   if (prec == MGN_BF16) {
-#define F(LD) \
-  hipLaunchKernelGGL((k_enc_bwd<MGN_BF16, LD, 8>), dim3(g), dim3(LD * 4), 0, s, N, node_in, hbar, w, eps, gin, part)
-    MGN_BY_WIDTH(lat, F);
-#undef F
+    hipLaunchKernelGGL((k_enc_bwd<MGN_BF16, 128, 8>), dim3(g), dim3(128 * 4), 0, s, N, node_in, hbar, w, eps, gin, part);
   } else {
 #define F(LD) \
   hipLaunchKernelGGL((k_enc_bwd<MGN_FP32, LD, 8>), dim3(g), dim3(LD * 4), 0, s, N, node_in, hbar, w, eps, gin, part)

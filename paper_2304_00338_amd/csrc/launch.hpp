@@ -157,6 +157,8 @@ hipError_t launch_edge_enc_bwd_rows(int64_t E, const float* efeat, const void* e
 hipError_t launch_edge_enc_w160(int64_t E, const float* efeat, const MlpW& w, float eps, void* e_out, hipStream_t s);
 hipError_t launch_edge_enc_bwd_w160(int64_t E, const float* efeat, const void* ebar, const MlpW& w, float eps,
                                     const Partials& part, int* nblocks, hipStream_t s);
+hipError_t launch_node_enc_bwd_w160(int64_t N, const float* node_in, const float* hbar, const MlpW& w, float eps,
+                                    float* gin, const Partials& part, int* nblocks, hipStream_t s);
 hipError_t launch_slot_fixup(int lat, const int32_t* long_nodes, int64_t n_long, const float* slots, float* dst,
                              hipStream_t s);
 hipError_t launch_node_fwd(int prec, int lat, int64_t N, const float* h_in, const float* agg, const MlpW& w,
