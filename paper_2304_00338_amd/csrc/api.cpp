@@ -622,8 +622,14 @@ struct Run {
         if ((rc = reduce(nb, 0, D, D, grad, oe.W1, 3 * D)) != MGN_OK) return rc;
       }
       if (g.n_long > 0) LAUNCH(K_FIXUP, launch_slot_fixup(D, g.long_nodes, g.n_long, slots(), R, s));
-      LAUNCH(K_SRCSUM, launch_node_srcsum(prec, D, N, g.rowptr, g.rev, zbar, R, h_l(k, l), hb_part, W(oe, M.p_edge[l]), hb_cur,
-                                 pt, &nb, s));
+      if (prec == MGN_BF16 && !rows())
+        // width 160: one wave per 16-node unit, S through the node-stream
+        // scratch (its streams are consumed by now) into the weight gradients
+        LAUNCH(K_SRCSUM, launch_srcsum_w160(N, g.rowptr, g.rev, zbar, R, h_l(k, l), hb_part, W(oe, M.p_edge[l]), hb_cur,
+                                            ws + c.L.nstr, pt, &nb, s));
+      else
+        LAUNCH(K_SRCSUM, launch_node_srcsum(prec, D, N, g.rowptr, g.rev, zbar, R, h_l(k, l), hb_part, W(oe, M.p_edge[l]),
+                                            hb_cur, pt, &nb, s));
       if ((rc = reduce(nb, 0, D, D, grad, oe.W1 + D, 3 * D)) != MGN_OK) return rc;
       if ((rc = reduce(nb, (int64_t)D * D, D, D, grad, oe.W1 + 2 * D, 3 * D)) != MGN_OK) return rc;
     }

@@ -145,6 +145,12 @@ hipError_t launch_wgrad_node_w160(int64_t N, const float* h, const float* agg, c
 hipError_t launch_node_fwd_w160(int64_t N, const float* h_in, const float* agg, const MlpW& w, float eps,
                                 float* h_out, hipStream_t s);
 hipError_t launch_emit_w160(int64_t N, const float* h, const MlpW& next_edge, void* P, hipStream_t s);
+// bf16 per-sender sums at width 160: hbar_out = hbar_part + W1s^T S + W1r^T
+// R and per-block partials of dW1s (at 0) and dW1r (at 160^2); S_buf: N x
+// 160 bf16 scratch for S.
+hipError_t launch_srcsum_w160(int64_t N, const int32_t* rowptr, const int32_t* rev, const void* zbar, const float* R,
+                              const float* h, const float* hbar_part, const MlpW& w, float* hbar_out, void* S_buf,
+                              const Partials& part, int* nblocks, hipStream_t s);
 // bf16 edge encoder in the row layout (uses MlpW::W2p and the fp32 W1f).
 hipError_t launch_edge_enc_rows(int64_t E, const float* efeat, const MlpW& w, float eps, void* e_out, hipStream_t s);
 // bf16 edge-encoder backward from the bf16 edge-gradient stream: per-block

@@ -16,6 +16,11 @@
 //   k_node_fwd_w160    the forward: h_out = h + LN(W2 relu(W1 [h; agg] + b1)
 //                      + b2) over the 150 real features
 //   k_emit_w160        P = [W1s h; W1r h] of the next edge layer
+//   k_srcsum_w160      per-sender sums S of the edge MLP's zbar (over the
+//                      reversed in-edges, in edge order) and hbar_out =
+//                      hbar_part + W1s^T S + W1r^T R; writes S for pass 2
+//                      of k_wgrad_node_w160 (dW1s = sum S h^T, dW1r =
+//                      sum R h^T)
 //
 // W1 = [W1h W1a] (the columns acting on h and on agg), each block and W2
 // staged row-permuted in the rotated layout (153.6 KB of LDS).
@@ -334,14 +339,18 @@ namespace w160 {
 constexpr int WN_NT = 640;
 }  // namespace w160
 
+// Pass 2 (the edge MLP's sender / receiver blocks): dW1s = sum S h^T at 0 and
+// dW1r = sum R h^T at L^2 (S: bf16 stream in dz, R: fp32 in agg, rounded to
+// bf16 as operands), wave w owning output rows [16w, 16w + 16) of both.
 template <int PASS>
 __global__ void __launch_bounds__(w160::WN_NT) k_wgrad_node_w160(int64_t N, const float* __restrict__ h,
                                                                 const float* __restrict__ agg,
                                                                 const bf16* __restrict__ dz,
                                                                 const bf16* __restrict__ a1, Partials part) {
   using namespace w160;
-  constexpr int NSTR = PASS == 0 ? 3 : 2;  // staged streams: dz1, h, agg / dz2, a1
-  constexpr int NCB = PASS == 0 ? 2 * NOB : NOB;
+  // staged streams: dz1, h, agg / dz2, a1 / S, R, h
+  constexpr int NSTR = PASS == 1 ? 2 : 3;
+  constexpr int NCB = PASS == 1 ? NOB : 2 * NOB;
   __shared__ __align__(16) bf16 Sg[2][NSTR][TM * WG_LD];
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, i = lane & 15, q = lane >> 4;
   const int jp = i >> 2, c4 = i & 3;
@@ -383,8 +392,18 @@ __global__ void __launch_bounds__(w160::WN_NT) k_wgrad_node_w160(int64_t N, cons
       const float* gp = agg + rc * L + scol;
       Ld[1] = cvt8(*reinterpret_cast<const float4*>(hp), *reinterpret_cast<const float4*>(hp + 4));
       Ld[2] = cvt8(*reinterpret_cast<const float4*>(gp), *reinterpret_cast<const float4*>(gp + 4));
-    } else {
+    } else if constexpr (PASS == 1) {
       Ld[1] = *reinterpret_cast<const uint4*>(a1 + rc * L + scol);
+    } else {
+      // R rows past N are zeroed like S; h rows are then multiplied by zero
+      const float* gp = agg + rc * L + scol;
+      const float* hp = h + rc * L + scol;
+      const uint4 v = cvt8(*reinterpret_cast<const float4*>(gp), *reinterpret_cast<const float4*>(gp + 4));
+      Ld[1].x = ok ? v.x : 0u;
+      Ld[1].y = ok ? v.y : 0u;
+      Ld[1].z = ok ? v.z : 0u;
+      Ld[1].w = ok ? v.w : 0u;
+      Ld[2] = cvt8(*reinterpret_cast<const float4*>(hp), *reinterpret_cast<const float4*>(hp + 4));
     }
   };
   // operand of 16 columns col0.. with K = the chunk's rows q*8 + j
@@ -400,25 +419,49 @@ __global__ void __launch_bounds__(w160::WN_NT) k_wgrad_node_w160(int64_t N, cons
     for (int k = 0; k < NSTR; ++k) *reinterpret_cast<uint4*>(&Sg[buf][k][srow * WG_LD + scol]) = Ld[k];
     __syncthreads();
     if (c + G < nch) issue(c + G);
-    const bf16x8 az = frag(Sg[buf][0], 16 * w);
+    if constexpr (PASS == 2) {
+      const bf16x8 as = frag(Sg[buf][0], 16 * w), ar = frag(Sg[buf][1], 16 * w);
 #pragma unroll
-    for (int cb = 0; cb < NCB; ++cb)
-      acc[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(az, frag(Sg[buf][1 + cb / NOB], 16 * (cb % NOB)), acc[cb], 0,
-                                                        0, 0);
-    ab = __builtin_amdgcn_mfma_f32_16x16x32_bf16(az, ones, ab, 0, 0, 0);
+      for (int cb = 0; cb < NOB; ++cb) {
+        const bf16x8 bh = frag(Sg[buf][2], 16 * cb);
+        acc[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as, bh, acc[cb], 0, 0, 0);
+        acc[NOB + cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ar, bh, acc[NOB + cb], 0, 0, 0);
+      }
+    } else {
+      const bf16x8 az = frag(Sg[buf][0], 16 * w);
+#pragma unroll
+      for (int cb = 0; cb < NCB; ++cb)
+        acc[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(az, frag(Sg[buf][1 + cb / NOB], 16 * (cb % NOB)), acc[cb],
+                                                          0, 0, 0);
+      ab = __builtin_amdgcn_mfma_f32_16x16x32_bf16(az, ones, ab, 0, 0, 0);
+    }
     buf ^= 1;
   }
-  // dW1: columns cb * 16 (cb < 10: the h block, else the agg block at 160 +);
-  // dW2: columns cb * 16
-  constexpr int ld = PASS == 0 ? 2 * L : L;
-  float* base = part.buf + (size_t)blockIdx.x * part.stride + (PASS == 0 ? 0 : 2 * L * L + L);
-  float* bias = part.buf + (size_t)blockIdx.x * part.stride + (PASS == 0 ? 2 * L * L : 3 * L * L + L);
+  float* blk = part.buf + (size_t)blockIdx.x * part.stride;
+  if constexpr (PASS == 2) {
+    // dW1s [160][160] at 0, dW1r at L^2
 #pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const int o = w * 16 + q * 4 + r;
+    for (int r = 0; r < 4; ++r) {
+      const int o = w * 16 + q * 4 + r;
 #pragma unroll
-    for (int cb = 0; cb < NCB; ++cb) base[(size_t)o * ld + cb * 16 + i] = acc[cb][r];
-    if (i == 0) bias[o] = ab[r];
+      for (int cb = 0; cb < NOB; ++cb) {
+        blk[(size_t)o * L + cb * 16 + i] = acc[cb][r];
+        blk[L * L + (size_t)o * L + cb * 16 + i] = acc[NOB + cb][r];
+      }
+    }
+  } else {
+    // dW1: columns cb * 16 (cb < 10: the h block, else the agg block at 160 +);
+    // dW2: columns cb * 16
+    constexpr int ld = PASS == 0 ? 2 * L : L;
+    float* base = blk + (PASS == 0 ? 0 : 2 * L * L + L);
+    float* bias = blk + (PASS == 0 ? 2 * L * L : 3 * L * L + L);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int o = w * 16 + q * 4 + r;
+#pragma unroll
+      for (int cb = 0; cb < NCB; ++cb) base[(size_t)o * ld + cb * 16 + i] = acc[cb][r];
+      if (i == 0) bias[o] = ab[r];
+    }
   }
 }
 
@@ -535,6 +578,77 @@ k_emit_w160(int64_t N, const float* __restrict__ h, MlpW nx, bf16* __restrict__ 
   }
 }
 
+
+// Per-sender sums of the edge MLP's zbar and the node gradient they feed:
+// S[v] = sum of zbar over the reversed in-edges of v (the out-edges of v in
+// a graph whose every edge has its reverse), in edge order from 0.0 in fp32;
+// hbar_out = hbar_part + W1s^T S + W1r^T R (S and R rounded to bf16 as
+// operands).  S is written in bf16 for the weight-gradient pass.
+__global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
+k_srcsum_w160(int64_t N, const int32_t* __restrict__ rowptr, const int32_t* __restrict__ rev,
+              const bf16* __restrict__ zbar, const float* __restrict__ R, const float* __restrict__ hbar_part,
+              MlpW w, float* __restrict__ hbar_out, bf16* __restrict__ S_out) {
+  using namespace w160;
+  __shared__ __align__(16) EmitLds S;
+  const int tid = threadIdx.x, lane = tid & 63, i = lane & 15, q = lane >> 4;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+  stage_rot(S.Ws, (const bf16*)w.W1sp, tid);
+  stage_rot(S.Wr, (const bf16*)w.W1rp, tid);
+  __syncthreads();
+  const int64_t nu = (N + 15) >> 4;
+  const UnitRange ur = unit_range(nu, wv);
+  constexpr int UE = 4;  // in-edges gathered per step
+  for (int64_t u = ur.t; u < ur.end; u += ur.stride) {
+    const int64_t v = u * 16 + i;
+    const bool ok = v < N;
+    const int64_t vc = ok ? v : N - 1;
+    const int e0 = rowptr[vc], deg = ok ? rowptr[vc + 1] - e0 : 0;
+    int md = deg;  // the unit's largest in-degree (the 4 lane groups hold the same nodes)
+#pragma unroll
+    for (int off = 1; off < 16; off <<= 1) md = max(md, __shfl_xor(md, off, 16));
+    f32x4 sacc[NOB];
+#pragma unroll
+    for (int ob = 0; ob < NOB; ++ob) sacc[ob] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int k0 = 0; k0 < md; k0 += UE) {
+      uint4 zr[UE][NS];
+#pragma unroll
+      for (int k = 0; k < UE; ++k) {
+        // past the node's in-degree: the node's first reversed edge (or edge
+        // 0 for a node without in-edges), not added
+        const int kk = k0 + k < deg ? k0 + k : 0;
+        const int e = deg > 0 ? rev[e0 + kk] : 0;
+        const bf16* zp = zbar + (size_t)e * L + 8 * q;
+#pragma unroll
+        for (int s = 0; s < NS; ++s) zr[k][s] = *reinterpret_cast<const uint4*>(zp + 32 * s);
+      }
+#pragma unroll
+      for (int k = 0; k < UE; ++k)
+        if (k0 + k < deg) {
+#pragma unroll
+          for (int ob = 0; ob < NOB; ++ob) sacc[ob] += run_block5(zr[k], ob);
+        }
+    }
+    const int64_t p = vc * L + 8 * q;
+    bf16x8 sr[NS], rr[NS];
+#pragma unroll
+    for (int s = 0; s < NS; ++s) sr[s] = pack_run(sacc[2 * s], sacc[2 * s + 1]);
+    if (ok) store_runs5(S_out + p, sr);
+    {
+      f32x4 rv[NOB];
+      load_row10(R + p, rv);
+#pragma unroll
+      for (int s = 0; s < NS; ++s) rr[s] = pack_run(rv[2 * s], rv[2 * s + 1]);
+    }
+    f32x4 hb[NOB];
+    load_row10(hbar_part + p, hb);
+    const int oz = opaque_zero();
+    const RotOff RO(i + oz, q);
+    prod_t(S.Ws + oz, RO, sr, hb);
+    prod_t(S.Wr + oz, RO, rr, hb);
+    if (ok) store_row10(hbar_out + p, hb);
+  }
+}
+
 }  // namespace dev
 
 using namespace dev;
@@ -588,6 +702,24 @@ hipError_t launch_emit_w160(int64_t N, const float* h, const MlpW& next_edge, vo
   int g = (int)std::min<int64_t>(need, kNodeBlocks160);
   if (g >= 8) g &= ~7;
   hipLaunchKernelGGL(k_emit_w160, dim3(g), dim3(NT), 0, s, N, h, next_edge, (bf16*)P);
+  return hipGetLastError();
+}
+
+hipError_t launch_srcsum_w160(int64_t N, const int32_t* rowptr, const int32_t* rev, const void* zbar, const float* R,
+                              const float* h, const float* hbar_part, const MlpW& w, float* hbar_out, void* S_buf,
+                              const Partials& part, int* nblocks, hipStream_t s) {
+  *nblocks = 0;
+  if (N <= 0) return hipSuccess;
+  if (!w.W1sp || !w.W1rp || part.stride < 2 * 160 * 160) return hipErrorInvalidValue;
+  const int64_t need = (((N + 15) >> 4) + NW - 1) / NW;
+  int g = (int)std::min<int64_t>(need, kNodeBlocks160);
+  if (g >= 8) g &= ~7;
+  hipLaunchKernelGGL(k_srcsum_w160, dim3(g), dim3(NT), 0, s, N, rowptr, rev, (const bf16*)zbar, R, hbar_part, w,
+                     hbar_out, (bf16*)S_buf);
+  const int gw = grid_for((N + TM - 1) / TM, std::min(512, part.max_blocks));
+  *nblocks = gw;
+  hipLaunchKernelGGL(k_wgrad_node_w160<2>, dim3(gw), dim3(w160::WN_NT), 0, s, N, h, R, (const bf16*)S_buf,
+                     (const bf16*)nullptr, part);
   return hipGetLastError();
 }
 
