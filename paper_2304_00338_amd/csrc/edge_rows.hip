@@ -570,7 +570,7 @@ __global__ void __launch_bounds__(NT) k_wgrad2(int64_t M, const bf16* __restrict
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
       if (r < M)
-        L[k] = *reinterpret_cast<const uint4*>(src[k] + r * D + scol);
+        L[k] = ld_stream(src[k] + r * D + scol);
       else
         L[k] = uint4{0u, 0u, 0u, 0u};
     }

@@ -575,7 +575,7 @@ __global__ void __launch_bounds__(w160::WG_NT) k_wgrad2_w160(int64_t M, const bf
     const int64_t rc = r < M ? r : M - 1;
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
-      const uint4 v = *reinterpret_cast<const uint4*>(src[k] + rc * L + scol);
+      const uint4 v = ld_stream(src[k] + rc * L + scol);
       Ld[k].x = r < M ? v.x : 0u;
       Ld[k].y = r < M ? v.y : 0u;
       Ld[k].z = r < M ? v.z : 0u;

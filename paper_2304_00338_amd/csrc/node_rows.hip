@@ -427,9 +427,9 @@ __global__ void __launch_bounds__(NT) k_wgrad_node(int64_t N, const float* __res
     const int64_t r = ch * TM + srow;
     const bool ok = r < N;
     const int64_t rr = ok ? r : N - 1;
-    const uint4 v1 = *reinterpret_cast<const uint4*>(dz1 + rr * D + scol);
-    const uint4 v2 = *reinterpret_cast<const uint4*>(dz2 + rr * D + scol);
-    L.a = *reinterpret_cast<const uint4*>(a1 + rr * D + scol);
+    const uint4 v1 = ld_stream(dz1 + rr * D + scol);
+    const uint4 v2 = ld_stream(dz2 + rr * D + scol);
+    L.a = ld_stream(a1 + rr * D + scol);
     L.h0 = *reinterpret_cast<const float4*>(h + rr * D + scol);
     L.h1 = *reinterpret_cast<const float4*>(h + rr * D + scol + 4);
     L.g0 = *reinterpret_cast<const float4*>(agg + rr * D + scol);

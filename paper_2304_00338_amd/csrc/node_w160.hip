@@ -382,7 +382,7 @@ __global__ void __launch_bounds__(w160::WN_NT) k_wgrad_node_w160(int64_t N, cons
     const int64_t r = ch * TM + srow;
     const bool ok = r < N;
     const int64_t rc = ok ? r : N - 1;
-    const uint4 v = *reinterpret_cast<const uint4*>(dz + rc * L + scol);
+    const uint4 v = ld_stream(dz + rc * L + scol);
     Ld[0].x = ok ? v.x : 0u;
     Ld[0].y = ok ? v.y : 0u;
     Ld[0].z = ok ? v.z : 0u;
@@ -393,7 +393,7 @@ __global__ void __launch_bounds__(w160::WN_NT) k_wgrad_node_w160(int64_t N, cons
       Ld[1] = cvt8(*reinterpret_cast<const float4*>(hp), *reinterpret_cast<const float4*>(hp + 4));
       Ld[2] = cvt8(*reinterpret_cast<const float4*>(gp), *reinterpret_cast<const float4*>(gp + 4));
     } else if constexpr (PASS == 1) {
-      Ld[1] = *reinterpret_cast<const uint4*>(a1 + rc * L + scol);
+      Ld[1] = ld_stream(a1 + rc * L + scol);
     } else {
       // R rows past N are zeroed like S; h rows are then multiplied by zero
       const float* gp = agg + rc * L + scol;

@@ -98,6 +98,14 @@ __device__ __forceinline__ float sum_rowlanes(float s) {
 // Transposing LDS read (gfx950 ds_read_b64_tr_b16): within each group of 16
 // lanes, result lane l, element j' is element l & 3 of the 8 bytes addressed
 // by lane 4j' + (l >> 2).
+// A 16-byte global load with the nontemporal hint, for streams read once
+// (the weight-gradient passes read their four streams with it: they are not
+// re-read, so they need not displace cached lines).
+__device__ __forceinline__ uint4 ld_stream(const void* p) {
+  typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+  return __builtin_bit_cast(uint4, __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p)));
+}
+
 __device__ __forceinline__ bf16x4 lds_tr(const bf16* p) {
   typedef __attribute__((address_space(3))) bf16x4 lds_v4;
   typedef __attribute__((address_space(3))) bf16 lds_b;
