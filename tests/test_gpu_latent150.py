@@ -267,3 +267,50 @@ def test_empty_graph_latent150():
     gp = torch.zeros_like(params)
     mgn.mgn_backward(ctx, torch.zeros((0, 4), device="cuda"), gp)
     assert float(gp.abs().sum()) == 0.0
+
+
+@pytest.mark.parametrize("prec", PRECS)
+def test_patch_union_multi_unit_latent150(prec):
+    """Past one unit per wave: on the disjoint union of four slab patches
+    (about 49k nodes, so the node and encoder kernels walk several 16-row
+    units or rounds per wave, and the edge kernels several tiles), the
+    forward output and the input gradient equal those of each patch computed
+    alone (under 1,000 units each, at most one per wave) bitwise, and the
+    parameter gradient equals the sum of the patches' gradients up to the
+    order of the fp32 block sums."""
+    import synth
+    m, shape = 2, (36, 36, 32)
+    M = synth.mesh(shape, 43)
+    g = mgn.build_graph(M["cells"], M["pos"])
+    part = synth.slab_part(shape, 4)
+    hp = [mgn.extract_patch(g, part, p, m) for p in range(4)]
+    u = mgn.patch_union(hp)
+    l2g = [p.patch_maps()["node_l2g"] for p in hp]
+    assert np.array_equal(u.patch_maps()["node_l2g"], np.concatenate(l2g))
+    assert u.n_nodes > 16 * 2048 and max(p.n_nodes for p in hp) < 16 * 1000
+    node_in = M["node_in"]
+    params = torch.from_numpy(synth.smooth_params(m, 43, LAT)).cuda()
+    gout = np.random.default_rng(43).standard_normal((u.n_nodes, 4)).astype(np.float32)
+    d = lambda a: torch.from_numpy(np.ascontiguousarray(a, np.float32)).cuda()
+
+    def fwd_bwd(graph, rows, go):
+        dg = mgn.DeviceGraph(graph)
+        ctx = mgn.Context(m, graph.n_nodes, graph.n_edges, prec, save=True, latent=LAT)
+        out = mgn.mgn_forward(ctx, dg, params, d(node_in[rows]), dg.efeat, save=True)
+        gp = torch.zeros_like(params)
+        gi = torch.zeros((graph.n_nodes, 8), dtype=torch.float32, device="cuda")
+        mgn.mgn_backward(ctx, d(go), gp, gi)
+        torch.cuda.synchronize()
+        return out.cpu().numpy(), gp.cpu().numpy(), gi.cpu().numpy()
+
+    ou, gpu_, giu = fwd_bwd(u, np.concatenate(l2g), gout)
+    gsum = np.zeros_like(gpu_, dtype=np.float64)
+    off = 0
+    for p, ids in zip(hp, l2g):
+        n = p.n_nodes
+        op, gp, gi = fwd_bwd(p, ids, gout[off:off + n])
+        assert np.array_equal(ou[off:off + n], op)
+        assert np.array_equal(giu[off:off + n], gi)
+        gsum += gp
+        off += n
+    assert rel_l2(gpu_, gsum) < 1e-5, rel_l2(gpu_, gsum)
