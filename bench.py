@@ -324,6 +324,43 @@ def c4_rollout(S, args, steps=10):
     return res
 
 
+def c3_relabelled(S, args, reps=3, seed=7):
+    """The benchmark's fwd+bwd step on the same patch of the same mesh with
+    the mesh's nodes relabelled by a seeded random permutation, so the
+    patch's node order (and its gathers) lose the grid's locality: the
+    worst case for the sender gathers and node-product reads."""
+    import torch
+    import synth
+    from paper_2304_00338_amd import mgn
+    M, n = S["mesh"], args.grid
+    nn = M["pos"].shape[0]
+    perm = np.random.default_rng(seed).permutation(nn).astype(np.int64)  # old id -> new id
+    inv = np.argsort(perm)                                               # new id -> old id
+    g2 = mgn.build_graph(perm[M["cells"]], M["pos"][inv])
+    part = synth.slab_part((n, n, n), args.slabs)[inv]
+    pt = mgn.extract_patch(g2, part, args.slab, args.ghost)
+    mp = pt.patch_maps()
+    old = inv[mp["node_l2g"]]
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a, np.float32)).cuda()
+    R = dict(S)
+    R.update({"dg": mgn.DeviceGraph(pt), "st": dev(M["onehot"][old]), "y": dev(M["states"][old]),
+              "gout": dev(synth.loss_weights(pt.n_nodes, 0) * mp["interior"][:, None])})
+    R["ynext"] = torch.empty_like(R["y"])
+    step(R, mgn)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        step(R, mgn)
+    torch.cuda.synchronize()
+    dt = (time.perf_counter() - t0) / reps
+    res = {"workload": f"the benchmark patch with the mesh's nodes relabelled by a seeded random permutation "
+                       f"(seed {seed})", "n_nodes": pt.n_nodes, "n_edges": pt.n_edges,
+           "ms_per_step": round(dt * 1e3, 3),
+           "mp_edges_per_s_fwdbwd": round(pt.n_edges * args.mp_steps / dt, 1)}
+    del R, g2, pt
+    return res
+
+
 def step(S, mgn, fwd_only=False):
     S["gp"].zero_()
     mgn.mgn_integrate_step(S["ctx"], S["dg"], S["params"], "euler", S["st"], S["y"], S["dg"].efeat,
@@ -496,6 +533,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-c4", action="store_true", help="skip the whole-mesh rollout measurement")
     ap.add_argument("--no-paper3d", action="store_true", help="skip the latent-150 3D training-step measurement")
+    ap.add_argument("--no-relabelled", action="store_true",
+                    help="skip the benchmark step on the randomly relabelled mesh")
     ap.add_argument("--paper3d-precs", default="fp32,bf16", help="precisions of the 3D training-step measurement")
     ap.add_argument("--paper3d-only", action="store_true",
                     help="only the latent-150 3D training-step measurement (one JSON object)")
@@ -615,6 +654,8 @@ def main():
                        "peak_tflops": MFMA_PEAK_BF16_TFLOPS,
                        "frac": round(fl / (avg_ms * 1e-3) / 1e12 / MFMA_PEAK_BF16_TFLOPS, 4)}
     out["train_step"] = train_steps(S, args)
+    if not args.no_relabelled:
+        out["c3_relabelled"] = c3_relabelled(S, args)
     if not args.no_paper3d:
         out["paper_3d_train"] = paper_3d_train(S, args)
     if not args.no_c4:
