@@ -548,18 +548,13 @@ hipError_t launch_node_bwd(int prec, int lat, int64_t N, const float* h, const f
   const int g = bwd_grid((N + TM - 1) / TM, part);
   *nblocks = g;
   if (!g) return hipSuccess;
-  if (prec == MGN_BF16) {
-    // bf16 at width 128 runs on the row-layout kernel
-    if (lat != 160) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((k_node_bwd<MGN_BF16, 160>), dim3(g), dim3(640), 0, s, N, h, agg, hbar_in, w, eps, hbar_part,
-                       aggbar, part);
-  } else {
+  // bf16 runs on the row-layout kernels (launch_node_bwd_rows / _w160)
+  if (prec == MGN_BF16) return hipErrorInvalidValue;
 #define F(LD)                                                                                                         \
   hipLaunchKernelGGL((k_node_bwd<MGN_FP32, LD>), dim3(g), dim3(LD * 4), 0, s, N, h, agg, hbar_in, w, eps, hbar_part, \
                      aggbar, part)
-    MGN_BY_WIDTH(lat, F);
+  MGN_BY_WIDTH(lat, F);
 #undef F
-  }
   return hipGetLastError();
 }
 
@@ -570,11 +565,10 @@ hipError_t launch_node_srcsum(int prec, int lat, int64_t N, const int32_t* rowpt
   *nblocks = g;
   if (!g) return hipSuccess;
   if (prec == MGN_BF16) {
-#define F(LD)                                                                                                      \
-  hipLaunchKernelGGL((k_node_srcsum<MGN_BF16, LD>), dim3(g), dim3(LD * 4), 0, s, N, rowptr, rev, (const bf16*)zbar, \
-                     R, h, hbar_part, w, hbar_out, part)
-    MGN_BY_WIDTH(lat, F);
-#undef F
+    // width 160 runs on launch_srcsum_w160
+    if (lat != 128) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((k_node_srcsum<MGN_BF16, 128>), dim3(g), dim3(128 * 4), 0, s, N, rowptr, rev,
+                       (const bf16*)zbar, R, h, hbar_part, w, hbar_out, part);
   } else {
 #define F(LD)                                                                                                       \
   hipLaunchKernelGGL((k_node_srcsum<MGN_FP32, LD>), dim3(g), dim3(LD * 4), 0, s, N, rowptr, rev, (const float*)zbar, \
