@@ -113,6 +113,14 @@ k_edge_bwd_w160(EdgeTiles tl, const bf16* __restrict__ a1_in, const bf16* ebar_i
     const int oz = opaque_zero();
     const bf16* W1s = S.W1 + oz;
     const bf16* W2s = S.W2 + oz;
+    // the receiver's aggregate gradient (a gather, mostly from the cache) is
+    // in flight during the z2 product: it is first needed after it
+    f32x4 ag0[NOB];
+    {
+      const float* gp = aggbar + (size_t)recv * L;
+#pragma unroll
+      for (int ob = 0; ob < NOB; ++ob) ag0[ob] = *reinterpret_cast<const f32x4*>(gp + fo(ob, q));
+    }
     // ---- z2 = b2 + W2 a1 and its LayerNorm statistics (150 real features)
     f32x4 acc[NOB];
 #pragma unroll
@@ -145,10 +153,9 @@ k_edge_bwd_w160(EdgeTiles tl, const bf16* __restrict__ a1_in, const bf16* ebar_i
     {
       uint4 eb[NS];
       load_eb(d0, rb, eb);
-      const float* gp = aggbar + (size_t)recv * L;
 #pragma unroll
       for (int ob = 0; ob < NOB; ++ob) {
-        const f32x4 ag = *reinterpret_cast<const f32x4*>(gp + fo(ob, q));
+        const f32x4 ag = ag0[ob];
         mb[ob] = ok ? ag + run_block5(eb, ob) : f32x4{0.f, 0.f, 0.f, 0.f};
         acc[ob] *= rstd;  // xhat
       }
