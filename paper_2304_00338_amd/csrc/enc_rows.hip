@@ -45,15 +45,21 @@ __device__ __forceinline__ void stage_enc(EncLds& S, const MlpW& w, int tid) {
   }
 }
 
+// Lane-independent part of fo(ob, q) = 8 q + fo_c(ob): LDS reads at a
+// per-lane base plus this constant fold the constant into the instruction's
+// offset (one base register instead of one address per feature).
+__device__ __forceinline__ constexpr int fo_c(int ob) { return 32 * (ob >> 1) + 4 * (ob & 1); }
+
 // z1 = b1 + W1 f for the lane's 32 features (fo(ob, q) + r).
 __device__ __forceinline__ void enc_z1(const EncLds& S, float4 f, int q, f32x4 (&z)[8]) {
+  const float4* W1q = S.W1 + 8 * q;
+  const float* b1q = S.b1 + 8 * q;
 #pragma unroll
   for (int ob = 0; ob < 8; ++ob)
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int F = fo(ob, q) + r;
-      const float4 wr = S.W1[F];
-      float v = S.b1[F];
+      const float4 wr = W1q[fo_c(ob) + r];
+      float v = b1q[fo_c(ob) + r];
       v = __builtin_fmaf(wr.x, f.x, v);
       v = __builtin_fmaf(wr.y, f.y, v);
       v = __builtin_fmaf(wr.z, f.z, v);
@@ -73,7 +79,7 @@ __device__ __forceinline__ void enc_z2(const EncLds& S, const AOff<D>& A2, const
       a1[s][4 + r] = (bf16)relu(z1[2 * s + 1][r]);
     }
 #pragma unroll
-  for (int ob = 0; ob < 8; ++ob) acc[ob] = *reinterpret_cast<const f32x4*>(S.b2 + fo(ob, q));
+  for (int ob = 0; ob < 8; ++ob) acc[ob] = *reinterpret_cast<const f32x4*>(S.b2 + 8 * q + fo_c(ob));
 #pragma unroll
   for (int s = 0; s < 4; ++s)
 #pragma unroll
@@ -106,7 +112,8 @@ k_edge_enc_rows(int64_t E, const float* __restrict__ f_in, MlpW w, float eps, bf
     ln_normalize(z, eps);
 #pragma unroll
     for (int ob = 0; ob < 8; ++ob)
-      z[ob] = *reinterpret_cast<const f32x4*>(L.g + fo(ob, q)) * z[ob] + *reinterpret_cast<const f32x4*>(L.bt + fo(ob, q));
+      z[ob] = *reinterpret_cast<const f32x4*>(L.g + 8 * q + fo_c(ob)) * z[ob] +
+              *reinterpret_cast<const f32x4*>(L.bt + 8 * q + fo_c(ob));
     if (u * 16 + i < E) {
       bf16* op = e_out + (u * 16 + i) * D + 8 * q;
 #pragma unroll
@@ -211,7 +218,7 @@ k_edge_enc_bwd_rows(int64_t E, const float* __restrict__ f_in, const bf16* __res
         float s1 = 0.f, s2 = 0.f;
 #pragma unroll
         for (int ob = 0; ob < 8; ++ob) {
-          yb[ob] *= *reinterpret_cast<const f32x4*>(L.g + fo(ob, q));
+          yb[ob] *= *reinterpret_cast<const f32x4*>(L.g + 8 * q + fo_c(ob));
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
             s1 += yb[ob][r];
