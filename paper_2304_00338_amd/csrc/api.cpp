@@ -19,6 +19,9 @@ namespace mgn {
 namespace {
 
 constexpr int kPartBlocks = 512;  // persistent blocks of the backward kernels
+// Partial regions: the backward kernels of one MP block write their
+// per-block partials to distinct regions, reduced together after the block.
+constexpr int kPartRegions = 5;
 // Largest per-block partial at kernel width LD: the node MLP's parameters,
 // W1 [LD][2 LD], b1, W2 [LD][LD], b2, gamma, beta.
 inline int64_t part_stride(int LD) { return 3LL * LD * LD + 4LL * LD; }
@@ -379,7 +382,7 @@ void plan(Ctx& c) {
     L.R = o;
     o = al256(o + (size_t)N * D * 4);
     L.part = o;
-    o = al256(o + (size_t)kPartBlocks * part_stride(D) * 4);
+    o = al256(o + (size_t)kPartRegions * kPartBlocks * part_stride(D) * 4);
     L.kbar = o;
     o = al256(o + (size_t)N * 4 * 4);
     L.ystage = o;
@@ -495,6 +498,11 @@ struct Run {
     p.max_blocks = kPartBlocks;
     return p;
   }
+  Partials partr(int r) const {
+    Partials p = part();
+    p.buf += (size_t)r * kPartBlocks * p.stride;
+    return p;
+  }
 
   int pack_weights() {
     const Model& M = c.M;
@@ -550,11 +558,35 @@ struct Run {
     LAUNCH(K_REDUCE, launch_reduce(part(), nb, src, rows, cols, grad, dst, ld, s));
     return MGN_OK;
   }
+  // Queued reductions of partial region r (launched together by flush).
+  ReduceBatch rq{};
+  int flush(float* grad) {
+    if (rq.n > 0) LAUNCH(K_REDUCE, launch_reduce_batch(part(), (int64_t)kPartBlocks * part_stride(D), rq, grad, s));
+    rq.n = 0;
+    return MGN_OK;
+  }
+  int job(int nb, int r, int64_t src, int rows, int cols, float* grad, int64_t dst, int64_t ld) {
+    if (nb <= 0 || rows <= 0 || cols <= 0) return MGN_OK;
+    int rc;
+    if (rq.n == kMaxReduceJobs && (rc = flush(grad)) != MGN_OK) return rc;
+    ReduceJob& j = rq.j[rq.n++];
+    j.src = src;
+    j.dst = dst;
+    j.ld = ld;
+    j.blk0 = 0;
+    j.rows = rows;
+    j.cols = cols;
+    j.nblocks = nb;
+    j.region = r;
+    return MGN_OK;
+  }
 
   int backward(int k, const float* node_in, const float* efeat, const float* gout, float* grad, float* gin) {
     const Model& M = c.M;
     const EdgeTiles tl = tiles();
     const Partials pt = part();
+    const Partials P0 = partr(0), P1 = partr(1), P2 = partr(2), P3 = partr(3), P4 = partr(4);
+    rq.n = 0;
     float* hb_cur = (float*)(ws + c.L.hb_a);
     float* hb_part = (float*)(ws + c.L.hb_b);
     float* aggbar = (float*)(ws + c.L.aggbar);
@@ -575,20 +607,20 @@ struct Run {
         const int64_t gpart = node_gamma_part(D);
         if (rows())
           LAUNCH(K_NODE_BWD, launch_node_bwd_rows(N, h_l(k, l), agg_l(k, l), hb_cur, W(on, M.p_node[l]), eps, hb_part,
-                                                  aggbar, na1, ndz2, ndz1, pt, &nb, s));
+                                                  aggbar, na1, ndz2, ndz1, P0, &nb, s));
         else
           LAUNCH(K_NODE_BWD, launch_node_bwd_w160(N, h_l(k, l), agg_l(k, l), hb_cur, W(on, M.p_node[l]), eps, hb_part,
-                                                  aggbar, na1, ndz2, ndz1, pt, &nb, s));
-        if ((rc = reduce(nb, gpart, 1, 2 * D, grad, on.g, 0)) != MGN_OK) return rc;
+                                                  aggbar, na1, ndz2, ndz1, P0, &nb, s));
+        if ((rc = job(nb, 0, gpart, 1, 2 * D, grad, on.g, 0)) != MGN_OK) return rc;
         if (rows())
-          LAUNCH(K_WGRAD_NODE, launch_wgrad_node(N, h_l(k, l), agg_l(k, l), ndz1, ndz2, na1, pt, &nb, s));
+          LAUNCH(K_WGRAD_NODE, launch_wgrad_node(N, h_l(k, l), agg_l(k, l), ndz1, ndz2, na1, P1, &nb, s));
         else
-          LAUNCH(K_WGRAD_NODE, launch_wgrad_node_w160(N, h_l(k, l), agg_l(k, l), ndz1, ndz2, na1, pt, &nb, s));
-        if ((rc = reduce(nb, 0, 1, (int)gpart, grad, on.W1, 0)) != MGN_OK) return rc;
+          LAUNCH(K_WGRAD_NODE, launch_wgrad_node_w160(N, h_l(k, l), agg_l(k, l), ndz1, ndz2, na1, P1, &nb, s));
+        if ((rc = job(nb, 1, 0, 1, (int)gpart, grad, on.W1, 0)) != MGN_OK) return rc;
       } else {
         LAUNCH(K_NODE_BWD, launch_node_bwd(prec, D, N, h_l(k, l), agg_l(k, l), hb_cur, W(on, M.p_node[l]), eps, hb_part, aggbar,
-                                pt, &nb, s));
-        if ((rc = reduce(nb, 0, 1, (int)on.size, grad, on.W1, 0)) != MGN_OK) return rc;
+                                P0, &nb, s));
+        if ((rc = job(nb, 0, 0, 1, (int)on.size, grad, on.W1, 0)) != MGN_OK) return rc;
       }
       if (E == 0) {
         // no edges: the edge MLP gets no gradient and every R is zero
@@ -596,42 +628,44 @@ struct Run {
       } else if (rows()) {
         void* dz = ws + c.L.dz;
         LAUNCH(K_EDGE_BWD, launch_edge_bwd_rows(tl, a1_l(k, l), ebar, l < m - 1 ? 1 : 0, ebar, aggbar, W(oe, M.p_edge[l]),
-                                    eps, zbar, dz, R, slots(), pt, &nb, s));
-        if ((rc = reduce(nb, 16384, 1, D, grad, oe.b1, 0)) != MGN_OK) return rc;
-        if ((rc = reduce(nb, 33024, 1, 2 * D, grad, oe.g, 0)) != MGN_OK) return rc;
-        LAUNCH(K_WGRAD, launch_wgrad2(E, zbar, e_l(k, l), dz, a1_l(k, l), pt, &nb, s));
-        if ((rc = reduce(nb, 16512, 1, D * D + D, grad, oe.W2, 0)) != MGN_OK) return rc;
-        if ((rc = reduce(nb, 0, D, D, grad, oe.W1, 3 * D)) != MGN_OK) return rc;
+                                    eps, zbar, dz, R, slots(), P2, &nb, s));
+        if ((rc = job(nb, 2, 16384, 1, D, grad, oe.b1, 0)) != MGN_OK) return rc;
+        if ((rc = job(nb, 2, 33024, 1, 2 * D, grad, oe.g, 0)) != MGN_OK) return rc;
+        LAUNCH(K_WGRAD, launch_wgrad2(E, zbar, e_l(k, l), dz, a1_l(k, l), P3, &nb, s));
+        if ((rc = job(nb, 3, 16512, 1, D * D + D, grad, oe.W2, 0)) != MGN_OK) return rc;
+        if ((rc = job(nb, 3, 0, D, D, grad, oe.W1, 3 * D)) != MGN_OK) return rc;
       } else if (prec == MGN_BF16) {
         // width 160: one wave per row block from the saved a1; weight
         // gradients dW1e = sum zbar^T e and dW2 = sum dz2^T a1 in one pass
         // over the saved streams
         void* dz = ws + c.L.dz;
         LAUNCH(K_EDGE_BWD, launch_edge_bwd_w160(tl, a1_l(k, l), ebar, l < m - 1 ? 1 : 0, ebar, aggbar, W(oe, M.p_edge[l]),
-                                    eps, zbar, dz, R, slots(), pt, &nb, s));
-        if ((rc = reduce(nb, 0, 1, D, grad, oe.b1, 0)) != MGN_OK) return rc;
-        if ((rc = reduce(nb, D, 1, 3 * D, grad, oe.b2, 0)) != MGN_OK) return rc;
-        LAUNCH(K_WGRAD, launch_wgrad2_w160(E, zbar, e_l(k, l), dz, a1_l(k, l), pt, &nb, s));
-        if ((rc = reduce(nb, 0, D, D, grad, oe.W1, 3 * D)) != MGN_OK) return rc;
-        if ((rc = reduce(nb, (int64_t)D * D, D, D, grad, oe.W2, D)) != MGN_OK) return rc;
+                                    eps, zbar, dz, R, slots(), P2, &nb, s));
+        if ((rc = job(nb, 2, 0, 1, D, grad, oe.b1, 0)) != MGN_OK) return rc;
+        if ((rc = job(nb, 2, D, 1, 3 * D, grad, oe.b2, 0)) != MGN_OK) return rc;
+        LAUNCH(K_WGRAD, launch_wgrad2_w160(E, zbar, e_l(k, l), dz, a1_l(k, l), P3, &nb, s));
+        if ((rc = job(nb, 3, 0, D, D, grad, oe.W1, 3 * D)) != MGN_OK) return rc;
+        if ((rc = job(nb, 3, (int64_t)D * D, D, D, grad, oe.W2, D)) != MGN_OK) return rc;
       } else {
         LAUNCH(K_EDGE_BWD, launch_edge_bwd(prec, D, tl, e_l(k, l), (float*)ebar, l < m - 1 ? 1 : 0, (float*)ebar, P_l(k, l), aggbar,
-                                W(oe, M.p_edge[l]), eps, zbar, R, slots(), pt, &nb, s));
-        if ((rc = reduce(nb, (int64_t)D * D, 1, (int)(oe.size - 3 * D * D), grad, oe.b1, 0)) != MGN_OK) return rc;
-        LAUNCH(K_WGRAD, launch_wgrad(prec, D, E, zbar, e_l(k, l), pt, &nb, s));
-        if ((rc = reduce(nb, 0, D, D, grad, oe.W1, 3 * D)) != MGN_OK) return rc;
+                                W(oe, M.p_edge[l]), eps, zbar, R, slots(), P2, &nb, s));
+        if ((rc = job(nb, 2, (int64_t)D * D, 1, (int)(oe.size - 3 * D * D), grad, oe.b1, 0)) != MGN_OK) return rc;
+        LAUNCH(K_WGRAD, launch_wgrad(prec, D, E, zbar, e_l(k, l), P3, &nb, s));
+        if ((rc = job(nb, 3, 0, D, D, grad, oe.W1, 3 * D)) != MGN_OK) return rc;
       }
       if (g.n_long > 0) LAUNCH(K_FIXUP, launch_slot_fixup(D, g.long_nodes, g.n_long, slots(), R, s));
       if (prec == MGN_BF16 && !rows())
         // width 160: one wave per 16-node unit, S through the node-stream
         // scratch (its streams are consumed by now) into the weight gradients
         LAUNCH(K_SRCSUM, launch_srcsum_w160(N, g.rowptr, g.rev, zbar, R, h_l(k, l), hb_part, W(oe, M.p_edge[l]), hb_cur,
-                                            ws + c.L.nstr, pt, &nb, s));
+                                            ws + c.L.nstr, P4, &nb, s));
       else
         LAUNCH(K_SRCSUM, launch_node_srcsum(prec, D, N, g.rowptr, g.rev, zbar, R, h_l(k, l), hb_part, W(oe, M.p_edge[l]),
-                                            hb_cur, pt, &nb, s));
-      if ((rc = reduce(nb, 0, D, D, grad, oe.W1 + D, 3 * D)) != MGN_OK) return rc;
-      if ((rc = reduce(nb, (int64_t)D * D, D, D, grad, oe.W1 + 2 * D, 3 * D)) != MGN_OK) return rc;
+                                            hb_cur, P4, &nb, s));
+      if ((rc = job(nb, 4, 0, D, D, grad, oe.W1 + D, 3 * D)) != MGN_OK) return rc;
+      if ((rc = job(nb, 4, (int64_t)D * D, D, D, grad, oe.W1 + 2 * D, 3 * D)) != MGN_OK) return rc;
+      // the block's partial regions are reused by the next block
+      if ((rc = flush(grad)) != MGN_OK) return rc;
     }
     if (m > 0) {
       if (rows())

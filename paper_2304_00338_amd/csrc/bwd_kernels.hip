@@ -514,6 +514,41 @@ __global__ void __launch_bounds__(256) k_reduce(Partials part, int nblocks, int6
   }
 }
 
+// The jobs of a batch one after the other over the launch's blocks; each
+// entry is summed exactly as in k_reduce.
+__global__ void __launch_bounds__(256) k_reduce_batch(Partials part, int64_t region_floats, ReduceBatch b,
+                                                      float* __restrict__ grad) {
+  __shared__ float red[kRedGroups][kRedCols];
+  int k = 0;
+  while (k + 1 < b.n && (int64_t)blockIdx.x >= b.j[k + 1].blk0) ++k;
+  const ReduceJob& J = b.j[k];
+  const int64_t total = (int64_t)J.rows * J.cols;
+  const int c = threadIdx.x % kRedCols, gr = threadIdx.x / kRedCols;
+  const int64_t idx = ((int64_t)blockIdx.x - J.blk0) * kRedCols + c;
+  float s = 0.f;
+  if (idx < total) {
+    const float* p = part.buf + J.region * region_floats + J.src + idx;
+    int bl = gr;
+    for (; bl + 7 * kRedGroups < J.nblocks; bl += 8 * kRedGroups) {
+      float v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = p[(size_t)(bl + u * kRedGroups) * part.stride];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) s += v[u];
+    }
+    for (; bl < J.nblocks; bl += kRedGroups) s += p[(size_t)bl * part.stride];
+  }
+  red[gr][c] = s;
+  __syncthreads();
+  if (gr == 0 && idx < total) {
+    float t = 0.f;
+#pragma unroll
+    for (int g = 0; g < kRedGroups; ++g) t += red[g][c];
+    const int64_t r = idx / J.cols, cc = idx % J.cols;
+    grad[J.dst + r * J.ld + cc] += t;
+  }
+}
+
 }  // namespace dev
 
 // ============================================================ launchers
@@ -621,6 +656,19 @@ hipError_t launch_reduce(const Partials& part, int nblocks, int64_t src, int32_t
   const int64_t total = (int64_t)rows * cols;
   const int64_t g = (total + kRedCols - 1) / kRedCols;
   hipLaunchKernelGGL(k_reduce, dim3((unsigned)g), dim3(256), 0, s, part, nblocks, src, rows, cols, grad, dst, dst_ld);
+  return hipGetLastError();
+}
+
+hipError_t launch_reduce_batch(const Partials& part, int64_t region_floats, ReduceBatch b, float* grad,
+                               hipStream_t s) {
+  if (b.n <= 0) return hipSuccess;
+  if (b.n > kMaxReduceJobs) return hipErrorInvalidValue;
+  int64_t blocks = 0;
+  for (int k = 0; k < b.n; ++k) {
+    b.j[k].blk0 = blocks;
+    blocks += ((int64_t)b.j[k].rows * b.j[k].cols + kRedCols - 1) / kRedCols;
+  }
+  hipLaunchKernelGGL(k_reduce_batch, dim3((unsigned)blocks), dim3(256), 0, s, part, region_floats, b, grad);
   return hipGetLastError();
 }
 

@@ -196,6 +196,21 @@ hipError_t launch_node_enc_bwd(int prec, int lat, int64_t N, const float* node_i
 // grad[dst + r*dst_ld + c] += sum_b part[b*stride + src + r*cols + c]
 hipError_t launch_reduce(const Partials& part, int nblocks, int64_t src, int32_t rows, int32_t cols,
                          float* grad, int64_t dst, int64_t dst_ld, hipStream_t s);
+// Several reductions of per-block partials in one launch (same per-entry sum
+// order as launch_reduce, so the same results): job k sums rows x cols
+// entries at src of region `region` (regions lie region_floats apart from
+// part.buf) over its nblocks partial rows into grad[dst + r ld + c].
+struct ReduceJob {
+  int64_t src, dst, ld, blk0;  // blk0: first launch block of the job (set by the launcher)
+  int32_t rows, cols, nblocks, region;
+};
+constexpr int kMaxReduceJobs = 8;
+struct ReduceBatch {
+  ReduceJob j[kMaxReduceJobs];
+  int32_t n;
+};
+hipError_t launch_reduce_batch(const Partials& part, int64_t region_floats, ReduceBatch b, float* grad,
+                               hipStream_t s);
 
 // out[v][c] = c0 * x0[v][c] + sum_j cj * xj[v][ldx_j*v + off_j + c], c < 4
 struct LinComb {
