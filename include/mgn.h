@@ -238,6 +238,30 @@ int mgn_forward(mgn_ctx* ctx, const mgn_dgraph* g, const float* params,
                 const float* node_in, const float* efeat, float* out,
                 int32_t save, void* workspace, size_t ws_bytes, void* stream);
 
+/* For callers that cannot allocate device memory at call time (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * mgn_forward with save = 0 whose device scratch is a static device array of
+ * MGN_NOALLOC_SCRATCH_BYTES bytes instead of a caller workspace.  The array
+ * is held once per GPU, from the library's first use on that GPU until the
+ * process ends; its address is looked up on the first call made with that
+ * GPU current (the GPU that runs `stream` must be the current device).  The
+ * call allocates nothing: the caller passes inputs and outputs as for
+ * mgn_forward (params, node_in, efeat, out on the device; the result is
+ * bitwise that of mgn_forward with save = 0).  Every scratch element is
+ * written before it is read, so no clearing is needed between calls.  All
+ * calls on one GPU share its array: two calls that overlap in time on one
+ * GPU (different streams, or different host threads) race and give
+ * undefined results; calls on one stream are ordered and safe.  The call
+ * does not touch the context's saved state other than clearing it (as any
+ * mgn_forward does) and records no profiling events.
+ * Errors: WORKSPACE when the context plans more workspace than the array
+ * holds (mgn_ctx_create's *ws_bytes > MGN_NOALLOC_SCRATCH_BYTES, checked
+ * before any device work), then those of mgn_forward. */
+#define MGN_NOALLOC_SCRATCH_BYTES (128ull << 20)
+int mgn_forward_noalloc(mgn_ctx* ctx, const mgn_dgraph* g, const float* params,
+                        const float* node_in, const float* efeat, float* out,
+                        void* stream);
+
 /* Reverse mode of the last saved mgn_forward or mgn_integrate_step on ctx.
  * grad_out: [N][4] gradient of the loss with respect to out (or to y_next).
  * grad_params: flat float32 [mgn_param_count]; the gradient is ADDED to it, so

@@ -989,6 +989,27 @@ int mgn_forward(mgn_ctx* ctx, const mgn_dgraph* g, const float* params, const fl
   return MGN_OK;
 }
 
+}  // extern "C"
+
+namespace mgn {
+
+size_t ctx_workspace_bytes(const mgn_ctx* ctx) { return ctx->c.L.total; }
+
+int forward_in_scratch(mgn_ctx* ctx, const mgn_dgraph* g, const float* params, const float* node_in,
+                       const float* efeat, float* out, void* scratch, size_t scratch_bytes, void* stream) {
+  // no event creation inside this call: profiling is suspended for it
+  Prof& p = ctx->c.prof;
+  const bool on = p.on;
+  p.on = false;
+  const int rc = mgn_forward(ctx, g, params, node_in, efeat, out, 0, scratch, scratch_bytes, stream);
+  p.on = on;
+  return rc;
+}
+
+}  // namespace mgn
+
+extern "C" {
+
 int mgn_integrate_step(mgn_ctx* ctx, const mgn_dgraph* g, const float* params, int32_t scheme,
                        const float* static_feat, const float* y, const float* efeat, float* y_next, int32_t save,
                        void* ws, size_t ws_bytes, void* stream) {

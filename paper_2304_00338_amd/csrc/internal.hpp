@@ -42,6 +42,14 @@ struct Graph {
 // Greedy receiver-aligned tiling (see mgn_graph_schedule in mgn.h).
 void build_schedule(Graph& g);
 
+// Workspace bytes planned by a context (mgn_ctx_create's *ws_bytes).
+size_t ctx_workspace_bytes(const mgn_ctx* ctx);
+
+// mgn_forward without saved activations into the given scratch (the body of
+// mgn_forward_noalloc): per-kernel profiling events are not recorded.
+int forward_in_scratch(mgn_ctx* ctx, const mgn_dgraph* g, const float* params, const float* node_in,
+                       const float* efeat, float* out, void* scratch, size_t scratch_bytes, void* stream);
+
 // Upper bound on the number of chunk slots a graph with E edges can need.
 inline int64_t max_slots(int64_t n_edges) {
   return 2 * (n_edges / kTileEdges) + 2;

@@ -62,7 +62,7 @@ EXPORTS = [
     "mgn_param_count", "mgn_build_graph", "mgn_graph_info", "mgn_graph_copy",
     "mgn_graph_schedule", "mgn_tile_edges", "mgn_tile_nodes", "mgn_graph_destroy",
     "mgn_partition", "mgn_extract_patch", "mgn_patch_union", "mgn_patch_copy_maps", "mgn_ctx_create",
-    "mgn_ctx_destroy", "mgn_forward", "mgn_backward", "mgn_integrate_step",
+    "mgn_ctx_destroy", "mgn_forward", "mgn_forward_noalloc", "mgn_backward", "mgn_integrate_step",
     "mgn_pec_step", "mgn_patch_step", "mgn_adam_lr", "mgn_adam_step", "mgn_train_step", "mgn_scheme_stages", "mgn_version", "mgn_last_error", "mgn_profile_enable",
     "mgn_profile_collect",
 ]
@@ -93,6 +93,7 @@ def lib():
         "mgn_ctx_create": (C.c_int, [P(Config), i64, i64, i32, i32, P(C.c_size_t), P(vp)]),
         "mgn_ctx_destroy": (None, [vp]),
         "mgn_forward": (C.c_int, [vp, P(DGraph), vp, vp, vp, vp, i32, vp, C.c_size_t, vp]),
+        "mgn_forward_noalloc": (C.c_int, [vp, P(DGraph), vp, vp, vp, vp, vp]),
         "mgn_backward": (C.c_int, [vp, vp, vp, vp, vp]),
         "mgn_integrate_step": (C.c_int, [vp, P(DGraph), vp, i32, vp, vp, vp, vp, i32, vp, C.c_size_t, vp]),
         "mgn_pec_step": (C.c_int, [vp, P(DGraph), vp, vp, vp, vp, vp, vp, i32, vp, C.c_size_t, vp]),
@@ -338,6 +339,22 @@ def mgn_forward(ctx: Context, g: DeviceGraph, params, node_in, efeat, out=None, 
                              _dptr(efeat, torch.float32, (E, 4), "efeat"),
                              _dptr(out, torch.float32, (N, 4), "out"), 1 if save else 0,
                              _dptr(ctx.ws, name="workspace"), ctx.ws_bytes, _stream(stream)))
+    return out
+
+
+NOALLOC_SCRATCH_BYTES = 128 << 20  # MGN_NOALLOC_SCRATCH_BYTES of include/mgn.h
+
+
+def mgn_forward_noalloc(ctx: Context, g: DeviceGraph, params, node_in, efeat, out, stream=None):
+    """mgn_forward (no saved activations) on the library's static device
+    scratch instead of ctx's workspace: the context may be created with
+    allocate=False; `out` must be given (nothing is allocated)."""
+    torch = _torch()
+    N, E = g.n_nodes, g.n_edges
+    _check(lib().mgn_forward_noalloc(ctx._h, C.byref(g.struct), _dptr(params, torch.float32, name="params"),
+                                     _dptr(node_in, torch.float32, (N, 8), "node_in"),
+                                     _dptr(efeat, torch.float32, (E, 4), "efeat"),
+                                     _dptr(out, torch.float32, (N, 4), "out"), _stream(stream)))
     return out
 
 
