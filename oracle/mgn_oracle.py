@@ -301,11 +301,22 @@ def zero_grads(P):
 # --------------------------------------------------------------------------
 # MLP and LayerNorm (textbook definitions)
 # --------------------------------------------------------------------------
+def _rows_times(x, W):
+    """x W^T computed one row at a time (a vector-matrix product per row), so
+    every row's result depends only on that row and never on how many rows
+    are multiplied together: a matrix-matrix BLAS call may block the
+    products differently for different row counts.  With this, the
+    subdomain rows of a patch get bitwise the whole mesh's values (Sec. 2.2,
+    condition 1, with ascending local ids and in-segment sums in ascending
+    order)."""
+    return (x[:, None, :] @ W.T)[:, 0, :]
+
+
 def mlp(x, p):
     """Two Linear layers with a ReLU between: W2 relu(W1 x + b1) + b2."""
-    z1 = x @ p["W1"].T + p["b1"]
+    z1 = _rows_times(x, p["W1"]) + p["b1"]
     a1 = np.maximum(z1, 0.0)
-    return a1 @ p["W2"].T + p["b2"], (x, z1, a1)
+    return _rows_times(a1, p["W2"]) + p["b2"], (x, z1, a1)
 
 
 def layer_norm(z, gamma, beta, eps=LN_EPS):

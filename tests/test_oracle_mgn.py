@@ -240,6 +240,20 @@ def _patch_inputs(M, pt):
     return M["node_in"][pt.node_l2g]
 
 
+def test_mlp_row_results_independent_of_row_count():
+    """The oracle's MLP gives a row bitwise the same result whatever rows are
+    multiplied with it, which the bitwise condition-1 pin below relies on
+    (a matrix-matrix BLAS product need not)."""
+    rng = np.random.default_rng(3)
+    p = {"W1": rng.standard_normal((128, 384)), "b1": rng.standard_normal(128),
+         "W2": rng.standard_normal((128, 128)), "b2": rng.standard_normal(128)}
+    x = rng.standard_normal((5000, 384))
+    full, _ = O.mlp(x, p)
+    for lo, hi in ((0, 1), (7, 29), (1000, 1333), (4990, 5000)):
+        part, _ = O.mlp(x[lo:hi].copy(), p)
+        assert np.array_equal(part, full[lo:hi])
+
+
 @pytest.mark.parametrize("shape,splits,m,k", [((9, 8), (3, 2), 2, 2),
                                               ((5, 5, 6), (1, 1, 3), 2, 3)])
 def test_condition1_interior_outputs_bitwise(shape, splits, m, k):
