@@ -25,7 +25,7 @@ HOST_SOURCES = ["graph.cpp", "api.cpp"]
 COMMON = ["-O3", "-fPIC", "-std=c++17", "-Wall", "-Wno-unused-function",
           "-I", os.path.join(ROOT, "include")]
 DEVICE = ["-x", "hip", f"--offload-arch={ARCH}", "-Xclang", "-target-feature",
-          "-Xclang", "-packed-fp32-ops", "-munsafe-fp-atomics"]
+          "-Xclang", "-packed-fp32-ops"]
 
 
 def _cmds():

@@ -368,8 +368,8 @@ void plan(Ctx& c) {
     o = al256(o + (size_t)E * D * c.se);
     L.zbar = o;
     o = al256(o + (size_t)E * D * c.se);
-    L.dz = o;
-    o = al256(o + (keep_a1 ? (size_t)E * D * 2 : 0));
+    L.dz = o;  // dz2 of the width-160 edge backward (the 128-wide one keeps it on chip)
+    o = al256(o + (keep_a1 && !rows ? (size_t)E * D * 2 : 0));
     // bf16 node backward: the a1, dz2, dz1 streams of one node MLP
     L.nstr = o;
     o = al256(o + (keep_a1 ? (size_t)3 * N * D * 2 : 0));
@@ -626,14 +626,13 @@ struct Run {
         // no edges: the edge MLP gets no gradient and every R is zero
         LAUNCH(K_EDGE_BWD, launch_fill(R, N * D, 0.f, s));
       } else if (rows()) {
-        void* dz = ws + c.L.dz;
-        LAUNCH(K_EDGE_BWD, launch_edge_bwd_rows(tl, a1_l(k, l), ebar, l < m - 1 ? 1 : 0, ebar, aggbar, W(oe, M.p_edge[l]),
-                                    eps, zbar, dz, R, slots(), P2, &nb, s));
+        // one pass: the edge MLP's reverse and its weight gradients
+        LAUNCH(K_EDGE_BWD, launch_edge_bwd_fused(tl, a1_l(k, l), e_l(k, l), ebar, l < m - 1 ? 1 : 0, ebar, aggbar,
+                                                 W(oe, M.p_edge[l]), eps, zbar, R, slots(), P2, &nb, s));
+        if ((rc = job(nb, 2, 0, D, D, grad, oe.W1, 3 * D)) != MGN_OK) return rc;
         if ((rc = job(nb, 2, 16384, 1, D, grad, oe.b1, 0)) != MGN_OK) return rc;
+        if ((rc = job(nb, 2, 16512, 1, D * D + D, grad, oe.W2, 0)) != MGN_OK) return rc;
         if ((rc = job(nb, 2, 33024, 1, 2 * D, grad, oe.g, 0)) != MGN_OK) return rc;
-        LAUNCH(K_WGRAD, launch_wgrad2(E, zbar, e_l(k, l), dz, a1_l(k, l), P3, &nb, s));
-        if ((rc = job(nb, 3, 16512, 1, D * D + D, grad, oe.W2, 0)) != MGN_OK) return rc;
-        if ((rc = job(nb, 3, 0, D, D, grad, oe.W1, 3 * D)) != MGN_OK) return rc;
       } else if (prec == MGN_BF16) {
         // width 160: one wave per row block from the saved a1; weight
         // gradients dW1e = sum zbar^T e and dW2 = sum dz2^T a1 in one pass

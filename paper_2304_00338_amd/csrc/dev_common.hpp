@@ -204,11 +204,16 @@ __device__ __forceinline__ void sum16x(f32x4 (&v)[NRB]) {
     for (int r = 0; r < 4; ++r) v[rb][r] += dpp_f<0x121>(v[rb][r]);
 }
 
-// Sum over the four q groups (lanes i, i+16, i+32, i+48).
+// Sum over the four q groups (lanes i, i+16, i+32, i+48): the pair sums of
+// lanes l, l ^ 16 and then l, l ^ 32 with gfx950's row swaps
+// (v_permlane16_swap / v_permlane32_swap of a value with itself hand every
+// lane both members of its pair, lower row first), on the VALU instead of
+// an LDS permute.  Each pair sum adds the same two values as s + s[l ^ k].
 __device__ __forceinline__ float sum_q(float s) {
-  s += __shfl_xor(s, 16, 64);
-  s += __shfl_xor(s, 32, 64);
-  return s;
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(s), __float_as_uint(s), false, false);
+  s = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(s), __float_as_uint(s), false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
 }
 
 // LDS scratch of the row LayerNorm helpers for NWV waves.  red/red2/red2x

@@ -623,7 +623,7 @@ hipError_t launch_edge_bwd(int prec, int lat, const EdgeTiles& t, const void* e,
   const int g = grid_for(t.n_tiles, std::min(kEdgeBwdBlocks, part.max_blocks));
   *nblocks = g;
   if (!g) return hipSuccess;
-  // bf16 runs on the row-per-wave kernels (k_edge_bwd_rows at width 128,
+  // bf16 runs on the row-per-wave kernels (k_edge_bwd_fused at width 128,
   // k_edge_bwd_w160 at 160)
   if (prec == MGN_BF16) return hipErrorInvalidValue;
 #define F(LD)                                                                                                      \

@@ -62,17 +62,6 @@ __device__ __forceinline__ void seg_pass(const float* stage, int lane, int segra
   }
 }
 
-// Sum over the first nr staged rows of features 2*lane, 2*lane+1.
-__device__ __forceinline__ float2 col_pass(const float* stage, int lane, int nr) {
-  float2 c = {0.f, 0.f};
-  for (int u = 0; u < nr; ++u) {
-    const float2 v = *reinterpret_cast<const float2*>(stage + u * RW_LDM + 2 * lane);
-    c.x += v.x;
-    c.y += v.y;
-  }
-  return c;
-}
-
 __global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
 k_edge_fwd_rows(EdgeTiles tl, const bf16* __restrict__ e_in, bf16* __restrict__ e_out, int write_e,
                 const bf16* __restrict__ Pn, MlpW w, float eps, float* __restrict__ agg,
@@ -269,21 +258,56 @@ k_edge_fwd_rows(EdgeTiles tl, const bf16* __restrict__ e_in, bf16* __restrict__ 
   }
 }
 
-// ===================================================================== reverse
-// Given ebar_in = dL/de_out (absent for the last block), aggbar, and the
-// saved first-layer activations a1 of the edge MLP: mbar = ebar_in +
-// aggbar[receiver]; back through the LayerNorm and the MLP to zbar = dL/dz1
-// (written out, with dz2 = dL/dz2 for the weight-gradient kernel), the
-// per-receiver sums R of zbar, ebar_out = ebar_in + W1e^T zbar, and
-// per-block partials of db1, dgamma, dbeta.  The edge-gradient stream is
-// bf16 like the edge latents it belongs to: ebar_out is formed in fp32 and
-// rounded once.
-__global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
-k_edge_bwd_rows(EdgeTiles tl, const bf16* __restrict__ a1_in, const bf16* ebar_in, int have_ebar,
-                bf16* ebar_out, const float* __restrict__ aggbar, MlpW w, float eps,
-                bf16* __restrict__ zbar, bf16* __restrict__ dz_out, float* __restrict__ R,
-                float* __restrict__ slots, Partials part) {
-  __shared__ __align__(16) RowsLds S;
+// ============================================================ fused reverse
+// The edge phase's reverse with its weight gradients in the same pass: per
+// 16-row half of a tile, from the saved a1, the block's input edge latents
+// e and the incoming gradients (ebar_in, aggbar at the receiver), it writes
+// zbar = dL/dz1 (for the sender sums), the receiver sums R of zbar and
+// ebar_out = ebar_in + W1e^T zbar, and accumulates dW2 = sum dz2^T a1,
+// dW1e = sum zbar^T e, db2 = sum dz2, db1 = sum zbar, dgamma, dbeta.
+//
+// Work split: eight waves per block, two per SIMD, in two roles.  Row waves
+// 0..3 run the reverse of one 16-row half per round (the layout and
+// products of the forward kernel's layout) and stage its rows of dz2, zbar and a1 in
+// LDS (row-major, zeros past the tile's end); gradient waves 4..7 load the
+// matching rows of e into the staging and, while the row waves compute the
+// next round, add the staged 64 rows into the weight gradients: wave 4 + k
+// owns the rows [64 (k % 2), + 64) of dW2 (k < 2: A = dz2^T, B = a1) or of
+// dW1e (A = zbar^T, B = e), with the row index as the MFMA's K dimension
+// (transposing LDS reads) and the column sums db2 / db1 through a ones
+// operand.  So each SIMD runs one row wave and one gradient wave, the
+// accumulators never share a wave with the row work, and two block
+// barriers per round order the staging: after the first the staging is
+// free (the gradient waves have read the previous round, the row waves
+// their own receiver sums), after the second it is full.  dgamma and dbeta
+// are DPP column sums of each half, accumulated per lane of the row waves.
+// Every sum runs in a fixed order, so results are reproducible.
+constexpr int FB_RW = 4;             // row waves per block (= gradient waves)
+constexpr int FB_NT = 128 * FB_RW;   // threads per block
+constexpr int FB_ROWS = 16 * FB_RW;  // rows staged per round
+constexpr int FB_LD = D + 16;        // staged row stride (elements)
+
+struct __attribute__((aligned(16))) FusedLds {
+  __attribute__((aligned(16))) bf16 W1[D * D];
+  __attribute__((aligned(16))) bf16 W2[D * D];
+  __attribute__((aligned(16))) float b2[D];
+  __attribute__((aligned(16))) float g[D];
+  // staged streams of a round: 0 dz2, 1 zbar, 2 a1, 3 e
+  __attribute__((aligned(16))) bf16 st[4][FB_ROWS * FB_LD];
+};
+
+// operand of 16 columns col0.. with K = the 32 staged rows r0 .. r0 + 31
+// (lane (i, q) gets rows r0 + 8q .. + 8 of column col0 + i)
+__device__ __forceinline__ bf16x8 staged_frag(const bf16* X, int r0, int col0, int i, int q) {
+  const bf16* p = X + (r0 + q * 8 + (i >> 2)) * FB_LD + col0 + 4 * (i & 3);
+  return cat8(lds_tr(p), lds_tr(p + 4 * FB_LD));
+}
+
+__global__ void __launch_bounds__(FB_NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
+k_edge_bwd_fused(EdgeTiles tl, const bf16* __restrict__ a1_in, const bf16* __restrict__ e_in, const bf16* ebar_in,
+                 int have_ebar, bf16* ebar_out, const float* __restrict__ aggbar, MlpW w, float eps,
+                 bf16* __restrict__ zbar, float* __restrict__ R, float* __restrict__ slots, Partials part) {
+  __shared__ __align__(16) FusedLds S;
   const int tid = threadIdx.x, lane = tid & 63, i = lane & 15, q = lane >> 4;
   const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
   {
@@ -296,14 +320,32 @@ k_edge_bwd_rows(EdgeTiles tl, const bf16* __restrict__ a1_in, const bf16* ebar_i
   }
   __syncthreads();
 
-  const UnitRange ur = unit_range(tl.n_tiles, wv);
-  int64_t t = ur.t;
-  const int64_t stride = ur.stride, tend = ur.end;
+  // The block's tiles: XCD-contiguous ranges (see unit_range); row wave k
+  // (and gradient wave 4 + k for the e rows) takes tile tb + k of every
+  // round pair; all waves run the same number of rounds (a row wave past
+  // the range runs empty tiles).
+  const int G = gridDim.x;
+  int64_t tb, stride, tend;
+  if ((G & 7) == 0) {
+    const int x = blockIdx.x & 7, per = G >> 3;
+    const int64_t chunk = (tl.n_tiles + 7) >> 3;
+    const int64_t lo = x * chunk;
+    tend = min(tl.n_tiles, lo + chunk);
+    tb = lo + (int64_t)(blockIdx.x >> 3) * FB_RW;
+    stride = (int64_t)per * FB_RW;
+  } else {
+    tb = (int64_t)blockIdx.x * FB_RW;
+    stride = (int64_t)G * FB_RW;
+    tend = tl.n_tiles;
+  }
+  const bool row_wave = wv < FB_RW;
+  const int k = row_wave ? wv : wv - FB_RW;  // the tile slot this wave follows
 
   const int4* tiles = reinterpret_cast<const int4*>(tl.tiles);
+  const int64_t tlast = max(tend - 1, (int64_t)0);
   auto desc = [&](int64_t tt) -> int4 {
     const bool ok = tt < tend;
-    const int4 v = tiles[ok ? tt : tend - 1];
+    const int4 v = tiles[ok ? tt : tlast];
     int4 r;
     r.x = ok ? v.x : 0;
     r.y = ok ? v.y : 0;
@@ -311,18 +353,105 @@ k_edge_bwd_rows(EdgeTiles tl, const bf16* __restrict__ a1_in, const bf16* ebar_i
     r.w = ok ? v.w : 0;
     return r;
   };
-  // The streamed inputs of one 16-row half of a tile for this lane's row:
-  // the four runs of a1 and of the incoming edge gradient.  The next half's streams are in flight while a half is computed;
-  // the receiver's aggregate gradient (shared by the ~14 consecutive rows of
-  // a receiver, so mostly a cache hit) is loaded when the half starts.
+  // Every global load is unconditional from a clamped index (see the
+  // forward kernel); rows past a tile's end (and the rows of an empty tile)
+  // read row 0 or the tile's last row, and are never stored or summed.
+  const int lastE = (int)max(tl.n_edges - 1, (int64_t)0);
+  auto erow = [&](int4 d, int rb) { return min(max(d.z + min(rb * 16 + i, tile_rows(d) - 1), 0), lastE); };
+  const int srow = 16 * k + i;  // this lane's staged row
+  auto stage_runs = [&](bf16* X, const uint4 (&v)[4], bool live) {
+    bf16* p = X + srow * FB_LD + 8 * q;
+#pragma unroll
+    for (int s = 0; s < 4; ++s) *reinterpret_cast<uint4*>(p + 32 * s) = live ? v[s] : uint4{0u, 0u, 0u, 0u};
+  };
+  float* base = part.buf + (size_t)blockIdx.x * part.stride;
+
+  if (!row_wave) {
+    // ================================ gradient waves
+    const int mat = k >> 1, oh = k & 1;
+    const bf16* Ast = S.st[mat];      // dz2 or zbar
+    const bf16* Bst = S.st[2 + mat];  // a1 or e
+    f32x4 acc_w[4][8], acc_b[4];
+#pragma unroll
+    for (int ob = 0; ob < 4; ++ob) {
+      acc_b[ob] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int nb = 0; nb < 8; ++nb) acc_w[ob][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+    bf16x8 ones;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) ones[j] = (bf16)1.f;
+    auto products = [&]() {
+#pragma unroll
+      for (int kc = 0; kc < 2; ++kc) {
+        bf16x8 af[4];
+#pragma unroll
+        for (int ob = 0; ob < 4; ++ob) {
+          af[ob] = staged_frag(Ast, 32 * kc, 64 * oh + 16 * ob, i, q);
+          acc_b[ob] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[ob], ones, acc_b[ob], 0, 0, 0);
+        }
+#pragma unroll
+        for (int nb = 0; nb < 8; ++nb) {
+          const bf16x8 bfr = staged_frag(Bst, 32 * kc, 16 * nb, i, q);
+#pragma unroll
+          for (int ob = 0; ob < 4; ++ob)
+            acc_w[ob][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[ob], bfr, acc_w[ob][nb], 0, 0, 0);
+        }
+      }
+    };
+    auto load_e = [&](int4 d, int rb, uint4 (&v)[4]) {
+      const bf16* xp = e_in + (size_t)erow(d, rb) * D + 8 * q;
+#pragma unroll
+      for (int s = 0; s < 4; ++s) v[s] = *reinterpret_cast<const uint4*>(xp + 32 * s);
+    };
+    if (tb < tend) {
+      int4 d0 = desc(tb + k), d1 = desc(tb + k + stride);
+      uint4 ev[4];
+      load_e(d0, 0, ev);
+      bool first = true;
+      for (; tb < tend; tb += stride) {
+#pragma unroll
+        for (int rb = 0; rb < 2; ++rb) {
+          if (!first) products();  // the previous round's rows
+          first = false;
+          __syncthreads();  // staging free
+          stage_runs(S.st[3], ev, rb * 16 + i < tile_rows(d0));
+          if (rb == 0)
+            load_e(d0, 1, ev);
+          else
+            load_e(d1, 0, ev);
+          __syncthreads();  // staging full
+        }
+        d0 = d1;
+        d1 = desc(tb + k + 2 * stride);
+      }
+      products();  // the last round's rows
+    }
+    // weight gradients straight from the owning wave; db1 / db2 from the
+    // ones column
+    const int wofs = mat == 0 ? 16512 : 0, bofs = mat == 0 ? 32896 : 16384;
+#pragma unroll
+    for (int ob = 0; ob < 4; ++ob) {
+#pragma unroll
+      for (int nb = 0; nb < 8; ++nb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int o = 64 * oh + 16 * ob + 4 * q + r;
+          base[wofs + (size_t)o * D + 16 * nb + i] = acc_w[ob][nb][r];
+        }
+      if (i == 0)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) base[bofs + 64 * oh + 16 * ob + 4 * q + r] = acc_b[ob][r];
+    }
+    __syncthreads();
+    __syncthreads();
+    return;
+  }
+
+  // ==================================== row waves
   struct HalfLoads {
     uint4 a[4], eb[4];
   };
-  // All global loads are unconditional from clamped indices (see the
-  // forward kernel); without an incoming edge gradient the loaded values are
-  // replaced by zeros.
-  const int lastE = (int)max(tl.n_edges - 1, (int64_t)0);
-  auto erow = [&](int4 d, int rb) { return min(max(d.z + min(rb * 16 + i, tile_rows(d) - 1), 0), lastE); };
   auto load_recv = [&](int4 d, int (&rv)[2]) {
 #pragma unroll
     for (int rb = 0; rb < 2; ++rb) rv[rb] = tl.receivers[erow(d, rb)];
@@ -331,15 +460,15 @@ k_edge_bwd_rows(EdgeTiles tl, const bf16* __restrict__ a1_in, const bf16* ebar_i
     const size_t row = (size_t)erow(d, rb);
     const bf16* ap = a1_in + row * D + 8 * q;
 #pragma unroll
-    for (int k = 0; k < 4; ++k) H.a[k] = *reinterpret_cast<const uint4*>(ap + 32 * k);
+    for (int s = 0; s < 4; ++s) H.a[s] = *reinterpret_cast<const uint4*>(ap + 32 * s);
     const bf16* ep = ebar_in + row * D + 8 * q;
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const uint4 v = *reinterpret_cast<const uint4*>(ep + 32 * k);
-      H.eb[k].x = have_ebar ? v.x : 0u;
-      H.eb[k].y = have_ebar ? v.y : 0u;
-      H.eb[k].z = have_ebar ? v.z : 0u;
-      H.eb[k].w = have_ebar ? v.w : 0u;
+    for (int s = 0; s < 4; ++s) {
+      const uint4 v = *reinterpret_cast<const uint4*>(ep + 32 * s);
+      H.eb[s].x = have_ebar ? v.x : 0u;
+      H.eb[s].y = have_ebar ? v.y : 0u;
+      H.eb[s].z = have_ebar ? v.z : 0u;
+      H.eb[s].w = have_ebar ? v.w : 0u;
     }
   };
   auto load_ag = [&](int recv, f32x4 (&ag)[8]) {
@@ -347,29 +476,26 @@ k_edge_bwd_rows(EdgeTiles tl, const bf16* __restrict__ a1_in, const bf16* ebar_i
 #pragma unroll
     for (int ob = 0; ob < 8; ++ob) ag[ob] = *reinterpret_cast<const f32x4*>(gp + fo(ob, q));
   };
+  float2 dga = {0.f, 0.f}, dbe = {0.f, 0.f};
 
-  float2 db1 = {0.f, 0.f}, dga = {0.f, 0.f}, dbe = {0.f, 0.f};
-  float* stage = S.stage[wv];
-  float* srow = stage + i * RW_LDM;
-
-  // One half (rows rb*16 .. +16) of tile d0 with its streams in H.
-  auto half = [&](HalfLoads& H, f32x4 (&ag)[8], int4 d0, int rb, int segraw, bool chunk, int nv, int& j,
-                  float2& carry) {
+  // One round: the reverse of half rb of tile d0 (streams in H), its rows
+  // staged, then the receiver sums of its zbar rows.
+  auto round = [&](HalfLoads& H, f32x4 (&ag)[8], int next_recv, int4 d0, int rb, int segraw, bool chunk, int nv,
+                   int& j, float2& carry) {
     const int n = tile_rows(d0);
     const int row = rb * 16 + i;
-    const int nh = max(0, min(16, n - rb * 16));  // valid rows of this half
+    const bool live = row < n;
     // ---- z2 = b2 + W2 a1 and its LayerNorm statistics
     f32x4 acc[8];
 #pragma unroll
     for (int ob = 0; ob < 8; ++ob) acc[ob] = *reinterpret_cast<const f32x4*>(S.b2 + fo(ob, q));
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
+    for (int s = 0; s < 4; ++s)
 #pragma unroll
       for (int ob = 0; ob < 8; ++ob) {
         const bf16x8 a = *reinterpret_cast<const bf16x8*>(wchunk(S.W2, ob * 16 + i, 4 * s + q));
         acc[ob] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, as_frag(H.a[s]), acc[ob], 0, 0, 0);
       }
-    }
     float sm = 0.f;
 #pragma unroll
     for (int ob = 0; ob < 8; ++ob)
@@ -386,26 +512,22 @@ k_edge_bwd_rows(EdgeTiles tl, const bf16* __restrict__ a1_in, const bf16* ebar_i
     const float rstd = __builtin_amdgcn_rsqf(sum_rowlanes(sq) * (1.0f / D) + eps);
 #pragma unroll
     for (int ob = 0; ob < 8; ++ob) {
-      acc[ob] *= rstd;          // xhat
+      acc[ob] *= rstd;                // xhat
       ag[ob] += run_block(H.eb, ob);  // mbar = ebar_in + aggbar[receiver]
     }
-    // ---- dgamma += sum_rows mbar * xhat, dbeta += sum_rows mbar
-#pragma unroll
-    for (int ob = 0; ob < 8; ++ob) *reinterpret_cast<f32x4*>(srow + fo(ob, q)) = ag[ob] * acc[ob];
-    wave_lds_sync();
+    // ---- dgamma += sum_rows mbar * xhat, dbeta += sum_rows mbar (live rows)
     {
-      const float2 c = col_pass(stage, lane, nh);
+      f32x4 p[8];
+#pragma unroll
+      for (int ob = 0; ob < 8; ++ob) p[ob] = live ? ag[ob] * acc[ob] : f32x4{0.f, 0.f, 0.f, 0.f};
+      const float2 c = colsum16(p, i);
       dga.x += c.x;
       dga.y += c.y;
-    }
-    wave_lds_sync();
 #pragma unroll
-    for (int ob = 0; ob < 8; ++ob) *reinterpret_cast<f32x4*>(srow + fo(ob, q)) = ag[ob];
-    wave_lds_sync();
-    {
-      const float2 c = col_pass(stage, lane, nh);
-      dbe.x += c.x;
-      dbe.y += c.y;
+      for (int ob = 0; ob < 8; ++ob) p[ob] = live ? ag[ob] : f32x4{0.f, 0.f, 0.f, 0.f};
+      const float2 d = colsum16(p, i);
+      dbe.x += d.x;
+      dbe.y += d.y;
     }
     // ---- LayerNorm backward: dz2 = rstd (dxh - mean(dxh) - xhat mean(dxh xhat)), dxh = mbar gamma
     float s1 = 0.f, s2 = 0.f;
@@ -427,20 +549,16 @@ k_edge_bwd_rows(EdgeTiles tl, const bf16* __restrict__ a1_in, const bf16* ebar_i
         dzf[s][r] = (bf16)(rstd * (ag[2 * s][r] - m1 - acc[2 * s][r] * m2));
         dzf[s][4 + r] = (bf16)(rstd * (ag[2 * s + 1][r] - m1 - acc[2 * s + 1][r] * m2));
       }
-    if (row < n) {
-      bf16* dp = dz_out + ((size_t)d0.z + row) * D + 8 * q;
-#pragma unroll
-      for (int s = 0; s < 4; ++s) *reinterpret_cast<uint4*>(dp + 32 * s) = __builtin_bit_cast(uint4, dzf[s]);
-    }
+    // the next half's receiver gradients, in flight for the rest of the round
+    load_ag(next_recv, ag);
     // ---- da1 = W2^T dz2, zbar = da1 where a1 > 0
 #pragma unroll
     for (int ob = 0; ob < 8; ++ob) acc[ob] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
+    for (int s = 0; s < 4; ++s)
 #pragma unroll
       for (int ob = 0; ob < 8; ++ob)
         acc[ob] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wt_frag(S.W2, ob, s, i, q), dzf[s], acc[ob], 0, 0, 0);
-    }
     bf16x8 zf[4];
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
@@ -451,165 +569,108 @@ k_edge_bwd_rows(EdgeTiles tl, const bf16* __restrict__ a1_in, const bf16* ebar_i
         zf[s][4 + r] = (float)a[4 + r] > 0.f ? (bf16)acc[2 * s + 1][r] : (bf16)0.f;
       }
     }
-    if (row < n) {
+    if (live) {
       bf16* zp = zbar + ((size_t)d0.z + row) * D + 8 * q;
 #pragma unroll
       for (int s = 0; s < 4; ++s) *reinterpret_cast<uint4*>(zp + 32 * s) = __builtin_bit_cast(uint4, zf[s]);
     }
-    // ---- per-receiver sums of zbar (as stored) and db1
-    wave_lds_sync();
-#pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      f32x4 lo, hi;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        lo[r] = (float)zf[s][r];
-        hi[r] = (float)zf[s][4 + r];
-      }
-      *reinterpret_cast<f32x4*>(srow + 32 * s + 8 * q) = lo;
-      *reinterpret_cast<f32x4*>(srow + 32 * s + 8 * q + 4) = hi;
-    }
-    wave_lds_sync();
-    seg_pass(stage, lane, segraw, d0.z, chunk, n, nv, rb * 16, j, carry, [&](int jj, float2 v) {
-      float* dst = !chunk ? R + (size_t)(d0.x + jj) * D : slots + (size_t)(-1 - d0.y) * D;
-      *reinterpret_cast<float2*>(dst + 2 * lane) = v;
-      db1.x += v.x;
-      db1.y += v.y;
-    });
     // ---- ebar_out = ebar_in + W1e^T zbar
 #pragma unroll
     for (int ob = 0; ob < 8; ++ob) acc[ob] = run_block(H.eb, ob);
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
+    for (int s = 0; s < 4; ++s)
 #pragma unroll
       for (int ob = 0; ob < 8; ++ob)
         acc[ob] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wt_frag(S.W1, ob, s, i, q), zf[s], acc[ob], 0, 0, 0);
-    }
-    if (row < n) {
+    if (live) {
       bf16* op = ebar_out + ((size_t)d0.z + row) * D + 8 * q;
 #pragma unroll
       for (int s = 0; s < 4; ++s)
         *reinterpret_cast<uint4*>(op + 32 * s) = __builtin_bit_cast(uint4, pack_run(acc[2 * s], acc[2 * s + 1]));
     }
-    wave_lds_sync();
+    // ---- stage the round's rows of dz2, zbar, a1 (zeros past the tile)
+    __syncthreads();  // staging free
+    {
+      uint4 v[4];
+#pragma unroll
+      for (int s = 0; s < 4; ++s) v[s] = __builtin_bit_cast(uint4, dzf[s]);
+      stage_runs(S.st[0], v, live);
+#pragma unroll
+      for (int s = 0; s < 4; ++s) v[s] = __builtin_bit_cast(uint4, zf[s]);
+      stage_runs(S.st[1], v, live);
+      stage_runs(S.st[2], H.a, live);
+    }
+    __syncthreads();  // staging full
+    // ---- per-receiver sums of zbar (as stored) over this wave's staged
+    // rows, each in ascending row order from 0.0 (carried into the next
+    // half while its segment is open)
+    {
+      // the 16 rows' values of this lane's two features, read at once
+      const bf16* zs = S.st[1] + 16 * k * FB_LD;
+      uint32_t zr[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) zr[r] = *reinterpret_cast<const uint32_t*>(zs + r * FB_LD + 2 * lane);
+      const int lo_row = rb * 16, hi_row = lo_row + 16;
+      while (j < nv) {
+        const int a = chunk ? 0 : __builtin_amdgcn_readlane(segraw, j) - d0.z;
+        const int b = chunk ? n : __builtin_amdgcn_readlane(segraw, j + 1) - d0.z;
+        const int u0 = max(a, lo_row), u1 = min(b, hi_row);
+        for (int u = u0; u < u1; ++u) {
+          const uint32_t v = zr[u - lo_row];
+          carry.x += __uint_as_float(v << 16);
+          carry.y += __uint_as_float(v & 0xffff0000u);
+        }
+        if (b > hi_row) break;
+        float* dst = !chunk ? R + (size_t)(d0.x + j) * D : slots + (size_t)(-1 - d0.y) * D;
+        *reinterpret_cast<float2*>(dst + 2 * lane) = carry;
+        carry = float2{0.f, 0.f};
+        ++j;
+      }
+    }
   };
 
-  if (t < tend) {
-    int4 d0 = desc(t), d1 = desc(t + stride);
+  if (tb < tend) {
+    int4 d0 = desc(tb + k), d1 = desc(tb + k + stride);
     int rc0[2], rn[2];
     load_recv(d0, rc0);
+    load_recv(d1, rn);
     HalfLoads A, B;
     load_half(d0, 0, A);
-    for (; t < tend; t += stride) {
+    f32x4 ag[8];
+    load_ag(rc0[0], ag);
+    for (; tb < tend; tb += stride) {
       // issue order = use order, so each wait covers only older requests
       const bool chunk = d0.y < 0;
       const int nv = chunk ? 1 : d0.y - d0.x;
       const int segraw = tl.rowptr[min(d0.x + lane, max(d0.x, d0.y))];
-      const int4 d2 = desc(t + 2 * stride);
-      load_recv(d1, rn);
-      f32x4 ag[8];
-      load_ag(rc0[0], ag);
+      const int4 d2 = desc(tb + k + 2 * stride);
       load_half(d0, 1, B);
       float2 carry = {0.f, 0.f};
       int j = 0;
-      half(A, ag, d0, 0, segraw, chunk, nv, j, carry);
-      load_ag(rc0[1], ag);
+      round(A, ag, rc0[1], d0, 0, segraw, chunk, nv, j, carry);
       load_half(d1, 0, A);
-      half(B, ag, d0, 1, segraw, chunk, nv, j, carry);
-      d0 = d1;
-      d1 = d2;
+      round(B, ag, rn[0], d0, 1, segraw, chunk, nv, j, carry);
       rc0[0] = rn[0];
       rc0[1] = rn[1];
+      load_recv(d2, rn);
+      d0 = d1;
+      d1 = d2;
     }
   }
-  // ---- block partials: the 8 waves' column sums in wave order
+  // ---- dgamma, dbeta: the row waves' sums in wave order
+  __syncthreads();  // the gradient waves have read the last round
+  float* red = reinterpret_cast<float*>(&S.st[0][0]);  // [2][FB_RW][D]
+  const int f = fo(i >> 1, q) + 2 * (i & 1);
+  *reinterpret_cast<float2*>(red + k * D + f) = dga;
+  *reinterpret_cast<float2*>(red + (FB_RW + k) * D + f) = dbe;
   __syncthreads();
-  float* red = &S.stage[0][0];  // [3][NW][D]
-  *reinterpret_cast<float2*>(red + (0 * NW + wv) * D + 2 * lane) = db1;
-  *reinterpret_cast<float2*>(red + (1 * NW + wv) * D + 2 * lane) = dga;
-  *reinterpret_cast<float2*>(red + (2 * NW + wv) * D + 2 * lane) = dbe;
-  __syncthreads();
-  if (tid < 3 * D) {
-    const int k = tid >> 7, f = tid & (D - 1);
+  if (tid < 2 * D) {
+    const int c2 = tid >> 7, c = tid & (D - 1);
     float v = 0.f;
 #pragma unroll
-    for (int u = 0; u < NW; ++u) v += red[(k * NW + u) * D + f];
-    float* base = part.buf + (size_t)blockIdx.x * part.stride;
-    const int off = k == 0 ? 16384 : (k == 1 ? 33024 : 33152);
-    base[off + f] = v;
+    for (int u = 0; u < FB_RW; ++u) v += red[(c2 * FB_RW + u) * D + c];
+    base[33024 + c2 * D + c] = v;
   }
-}
-
-// Weight gradients of the edge MLP from the saved streams, one pass:
-// dW1e = sum_rows zbar^T e, dW2 = sum_rows dz2^T a1, db2 = sum_rows dz2.
-// Each 32-row chunk of the four bf16 streams is staged row-major in LDS
-// (rows 144 elements apart, so the transposing reads below are free of bank
-// conflicts) while the next chunk is in flight in registers; wave w owns
-// output rows [16w, 16w + 16) of both matrices and reads its MFMA operands
-// with K = the chunk's rows through ds_read_b64_tr_b16.
-constexpr int WG_LD = D + 16;
-
-__global__ void __launch_bounds__(NT) k_wgrad2(int64_t M, const bf16* __restrict__ zb, const bf16* __restrict__ e,
-                                               const bf16* __restrict__ dz, const bf16* __restrict__ a1,
-                                               Partials part) {
-  __shared__ __align__(16) bf16 Sg[2][4][TM * WG_LD];
-  const int tid = threadIdx.x, w8 = tid >> 6, lane = tid & 63, i = lane & 15, q = lane >> 4;
-  const int jp = i >> 2, c4 = i & 3;
-  f32x4 acc1[8], acc2[8], accb = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-  for (int cb = 0; cb < 8; ++cb) acc1[cb] = acc2[cb] = f32x4{0.f, 0.f, 0.f, 0.f};
-  bf16x8 ones;
-#pragma unroll
-  for (int j = 0; j < 8; ++j) ones[j] = (bf16)1.f;
-  const int64_t nch = (M + TM - 1) / TM, G = gridDim.x;
-  const int srow = tid >> 4, scol = (tid & 15) * 8;
-  const bf16* src[4] = {zb, e, dz, a1};
-  uint4 L[4];
-  auto issue = [&](int64_t ch) {
-    const int64_t r = ch * TM + srow;
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      if (r < M)
-        L[k] = ld_stream(src[k] + r * D + scol);
-      else
-        L[k] = uint4{0u, 0u, 0u, 0u};
-    }
-  };
-  // operand of 16 columns col0.. with K = the chunk's rows q*8 + j
-  auto frag = [&](const bf16* X, int col0) -> bf16x8 {
-    const bf16* p = X + (q * 8 + jp) * WG_LD + col0 + 4 * c4;
-    return cat8(lds_tr(p), lds_tr(p + 4 * WG_LD));
-  };
-  int64_t c = blockIdx.x;
-  int buf = 0;
-  if (c < nch) issue(c);
-  for (; c < nch; c += G) {
-#pragma unroll
-    for (int k = 0; k < 4; ++k) *reinterpret_cast<uint4*>(&Sg[buf][k][srow * WG_LD + scol]) = L[k];
-    __syncthreads();
-    if (c + G < nch) issue(c + G);
-    const bf16x8 az = frag(Sg[buf][0], 16 * w8);
-    const bf16x8 ad = frag(Sg[buf][2], 16 * w8);
-#pragma unroll
-    for (int cb = 0; cb < 8; ++cb) {
-      acc1[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(az, frag(Sg[buf][1], 16 * cb), acc1[cb], 0, 0, 0);
-      acc2[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ad, frag(Sg[buf][3], 16 * cb), acc2[cb], 0, 0, 0);
-    }
-    accb = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ad, ones, accb, 0, 0, 0);
-    buf ^= 1;
-  }
-  float* base = part.buf + (size_t)blockIdx.x * part.stride;
-#pragma unroll
-  for (int cb = 0; cb < 8; ++cb)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int o = w8 * 16 + q * 4 + r;
-      base[(size_t)o * D + cb * 16 + i] = acc1[cb][r];
-      base[16512 + (size_t)o * D + cb * 16 + i] = acc2[cb][r];
-    }
-  if (i == 0)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) base[32896 + w8 * 16 + q * 4 + r] = accb[r];
 }
 
 }  // namespace dev
@@ -634,30 +695,25 @@ hipError_t launch_edge_fwd_rows(const EdgeTiles& t, const void* e_in, void* e_ou
   return hipGetLastError();
 }
 
-hipError_t launch_edge_bwd_rows(const EdgeTiles& t, const void* a1, const void* ebar_in, int have_ebar,
-                                void* ebar_out, const float* aggbar, const MlpW& w, float eps, void* zbar, void* dz,
-                                float* R, float* slots, const Partials& part, int* nblocks, hipStream_t s) {
+
+
+static constexpr int kFusedBlocks = 256;
+
+hipError_t launch_edge_bwd_fused(const EdgeTiles& t, const void* a1, const void* e, const void* ebar_in,
+                                 int have_ebar, void* ebar_out, const float* aggbar, const MlpW& w, float eps,
+                                 void* zbar, float* R, float* slots, const Partials& part, int* nblocks,
+                                 hipStream_t s) {
   *nblocks = 0;
   if (t.n_tiles <= 0) return hipSuccess;
-  if (t.n_edges <= 0) return hipErrorInvalidValue;
-  const int g = rows_grid(t.n_tiles, std::min(kRowsBlocks, part.max_blocks));
+  if (t.n_edges <= 0 || part.stride < 33280) return hipErrorInvalidValue;
+  const int64_t need = (t.n_tiles + FB_RW - 1) / FB_RW;
+  int g = (int)std::min<int64_t>(need, std::min(kFusedBlocks, part.max_blocks));
+  if (g >= 8) g &= ~7;
   *nblocks = g;
-  hipLaunchKernelGGL(k_edge_bwd_rows, dim3(g), dim3(NT), 0, s, t, (const bf16*)a1, (const bf16*)ebar_in, have_ebar, (bf16*)ebar_out,
-                     aggbar, w, eps, (bf16*)zbar, (bf16*)dz, R, slots, part);
+  hipLaunchKernelGGL(k_edge_bwd_fused, dim3(g), dim3(FB_NT), 0, s, t, (const bf16*)a1, (const bf16*)e,
+                     (const bf16*)ebar_in, have_ebar, (bf16*)ebar_out, aggbar, w, eps, (bf16*)zbar, R, slots, part);
   return hipGetLastError();
 }
 
-static constexpr int kWgrad2Blocks = 512;
-
-hipError_t launch_wgrad2(int64_t M, const void* zbar, const void* e, const void* dz, const void* a1,
-                         const Partials& part, int* nblocks, hipStream_t s) {
-  *nblocks = 0;
-  if (M <= 0) return hipSuccess;
-  const int g = (int)std::min<int64_t>((M + TM - 1) / TM, std::min(kWgrad2Blocks, part.max_blocks));
-  *nblocks = g;
-  hipLaunchKernelGGL(k_wgrad2, dim3(g), dim3(NT), 0, s, M, (const bf16*)zbar, (const bf16*)e, (const bf16*)dz,
-                     (const bf16*)a1, part);
-  return hipGetLastError();
-}
 
 }  // namespace mgn

@@ -93,12 +93,15 @@ hipError_t launch_edge_fwd(int prec, int lat, const EdgeTiles& t, const void* e_
 // (nullable) receives the first-layer activations of every edge.
 hipError_t launch_edge_fwd_rows(const EdgeTiles& t, const void* e_in, void* e_out, int write_e, const void* P,
                                 const MlpW& w, float eps, float* agg, float* slots, void* a1_out, hipStream_t s);
-// bf16 edge backward from the saved a1 (one wave per tile; bf16 edge-gradient
-// stream ebar, in place allowed); writes zbar, dz2, R / slots, ebar_out and
-// per-block partials of db1, dgamma, dbeta.
-hipError_t launch_edge_bwd_rows(const EdgeTiles& t, const void* a1, const void* ebar_in, int have_ebar,
-                                void* ebar_out, const float* aggbar, const MlpW& w, float eps, void* zbar, void* dz,
-                                float* R, float* slots, const Partials& part, int* nblocks, hipStream_t s);
+// bf16 edge backward with its weight gradients in one pass (four waves per
+// block in lockstep rounds): from the saved a1, the block's input edge
+// latents e and ebar_in (in place allowed), writes zbar, R / slots,
+// ebar_out and per-block partials dW1e (0), db1 (16384), dW2 (16512), db2
+// (32896), dgamma (33024), dbeta (33152).
+hipError_t launch_edge_bwd_fused(const EdgeTiles& t, const void* a1, const void* e, const void* ebar_in,
+                                 int have_ebar, void* ebar_out, const float* aggbar, const MlpW& w, float eps,
+                                 void* zbar, float* R, float* slots, const Partials& part, int* nblocks,
+                                 hipStream_t s);
 // bf16 edge forward at width 160 (latent 150) with one wave per 16-row half of
 // a tile (uses MlpW::W1p, W2p and the fp32 vectors); a1_out (nullable)
 // receives the first-layer activations.
@@ -115,9 +118,6 @@ hipError_t launch_edge_bwd_w160(const EdgeTiles& t, const void* a1, const void* 
 // 160 * 160 as per-block partials.
 hipError_t launch_wgrad2_w160(int64_t M, const void* zbar, const void* e, const void* dz, const void* a1,
                               const Partials& part, int* nblocks, hipStream_t s);
-// bf16 dW1e = sum zbar^T e, dW2 = sum dz2^T a1, db2 = sum dz2 as per-block partials.
-hipError_t launch_wgrad2(int64_t M, const void* zbar, const void* e, const void* dz, const void* a1,
-                         const Partials& part, int* nblocks, hipStream_t s);
 // bf16 node phase with one wave per 16-node block (uses MlpW::W1p / W2p of
 // the node MLP): h_out = h_in + LN(MLP([h_in, agg])), h_out may alias h_in.
 hipError_t launch_node_fwd_rows(int64_t N, const float* h_in, const float* agg, const MlpW& w, float eps,

@@ -84,16 +84,8 @@ __device__ __forceinline__ f32x4 run_block(const uint4 (&runs)[4], int ob) {
 // sign bit set, so they compare below +0.0 as signed integers).
 __device__ __forceinline__ float relu(float x) { return __int_as_float(max(__float_as_int(x), 0)); }
 
-template <int CTRL>
-__device__ __forceinline__ float xlane(float v) {
-  return __shfl_xor(v, CTRL, 64);
-}
 // Sum over the four lanes that hold the same row (q = 0..3).
-__device__ __forceinline__ float sum_rowlanes(float s) {
-  s += xlane<16>(s);
-  s += xlane<32>(s);
-  return s;
-}
+__device__ __forceinline__ float sum_rowlanes(float s) { return sum_q(s); }
 
 // Transposing LDS read (gfx950 ds_read_b64_tr_b16): within each group of 16
 // lanes, result lane l, element j' is element l & 3 of the 8 bytes addressed

@@ -64,22 +64,42 @@ def kink_resolved(tape, w, gp, gi, tau=KINK_TAU, max_kinks=48):
     return gS, giS, S
 
 
-def bf16_grad_tols(pb, trials=2, scale=2.0):
-    """Per-segment tolerances {name: tol, 'gin': tol} for bf16 gradients at
-    an ordinary point (see BF16_GRAD_TOL).  Oracle-only computation."""
+def grad_tols(pb, rel, floor, trials=2, scale=2.0):
+    """Per-segment tolerances {name: tol, 'gin': tol} for gradients at an
+    ordinary point: scale times the largest change of the oracle's own
+    gradient under random relative +-rel perturbations of all weights,
+    never below floor.  Oracle-only computation."""
     lat = getattr(pb, "latent", 128)
     _, tape = O.mgn_forward(pb.go, pb.params, pb.node_in, pb.go.efeat, pb.m, latent=lat, keep=True)
     g0, gi0 = O.mgn_backward(tape, pb.w)
+    del tape
     worst = {}
     for t in range(trials):
         xi = np.random.default_rng(1000 + t).choice([-1.0, 1.0], size=pb.params.shape)
-        _, t1 = O.mgn_forward(pb.go, pb.params * (1 + 2.0 ** -8 * xi), pb.node_in, pb.go.efeat, pb.m,
+        _, t1 = O.mgn_forward(pb.go, pb.params * (1 + rel * xi), pb.node_in, pb.go.efeat, pb.m,
                               latent=lat, keep=True)
         g1, gi1 = O.mgn_backward(t1, pb.w)
+        del t1
         for name, a, b in segments(pb.m, lat):
             worst[name] = max(worst.get(name, 0.0), rel_l2(g1[a:b], g0[a:b]))
         worst["gin"] = max(worst.get("gin", 0.0), rel_l2(gi1, gi0))
-    return {k: max(BF16_GRAD_TOL, scale * v) for k, v in worst.items()}
+    return {k: max(floor, scale * v) for k, v in worst.items()}
+
+
+def bf16_grad_tols(pb, trials=2, scale=2.0, floor=BF16_GRAD_TOL):
+    """Tolerances for bf16 gradients at an ordinary point (see
+    BF16_GRAD_TOL): the bf16 path rounds weights and activation operands to
+    8 significant bits, so the perturbation is relative 2^-8."""
+    return grad_tols(pb, 2.0 ** -8, floor, trials, scale)
+
+
+def fp32_grad_tols(pb, trials=2, scale=2.0):
+    """Tolerances for fp32 gradients at an ordinary point of a mesh too large
+    to resolve its ReLU kinks one by one (kink_resolved): the fp32 forward's
+    accumulated rounding in a K = 384 product is about sqrt(K) 2^-24 ~ 2^-20
+    relative, so the valid subgradients spread like the oracle's gradient
+    under relative 2^-20 weight perturbations; never below FP32_TOL."""
+    return grad_tols(pb, 2.0 ** -20, FP32_TOL, trials, scale)
 
 
 class Problem:
