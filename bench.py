@@ -34,14 +34,20 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-# Executed bf16 MFMA work per edge of the bf16 edge kernels (16x16x32 MFMAs
-# at 16,384 flop each over a 16-row block, counted as issued, select
-# operands included): the edge forward runs the K = 128 products of W1e e
-# and W2 a1, 16 + 8 selection MFMAs for P_s + P_r and e + m per 16 rows; the
-# backward the three 128 x 128 products W2 a1 (recomputed z2), W2^T dz2 and
-# W1e^T zbar.
-MFMA_FLOP_PER_EDGE = {"edge_fwd": 2 * 128 * 128 * 2 + 24 * 16384 // 16,
-                      "edge_bwd": 3 * 2 * 128 * 128}
+# Executed MFMA work per edge (flop, counted per edge row; 16x16x32 bf16
+# MFMAs at 16,384 flop over a 16-row block, select operands included).
+# bf16 edge forward: W1e e and W2 a1 (K = 128) plus 16 + 8 selection MFMAs
+# per 16 rows for P_s + P_r and e + m.  bf16 fused edge backward: the row
+# waves' three 128 x 128 products (W2 a1 recomputed, W2^T dz2, W1e^T zbar),
+# the gradient waves' dW2 = dz2^T a1 and dW1e = zbar^T e, and their ones
+# columns (8 MFMAs per 64-row round and gradient wave, 4 waves).
+# fp32 (feature-split kernels): the edge backward's five 128 x 128 products
+# per edge (W1e e and W2 a1 recomputed, W2^T dz2, W1e^T zbar, dW2), the
+# forward's two (W1e e, W2 a1), the separate dW1e pass one.
+MFMA_FLOP_PER_EDGE = {"bf16": {"edge_fwd": 2 * 128 * 128 * 2 + 24 * 16384 // 16,
+                               "edge_bwd": 5 * 2 * 128 * 128 + 4 * 8 * 16384 // 64},
+                      "fp32": {"edge_fwd": 2 * 2 * 128 * 128, "edge_bwd": 5 * 2 * 128 * 128,
+                               "wgrad": 2 * 128 * 128}}
 MFMA_PEAK_BF16_TFLOPS = 2500.0
 MFMA_PEAK_FP32_TFLOPS = 157.3
 
@@ -79,28 +85,34 @@ def edge_bwd_split_roofline(prec, D, N, E, m, avg_ms):
                      "frac": round(tfs / peak, 4)}}
 
 
-def kernel_bytes(kind, N, E, n_tiles, prec, have_ebar=True, write_e=True, keep_a1=True):
-    """Algorithmic HBM bytes of one launch of the kernels this build runs:
-    every input read once and every output written once.  In bf16 the edge
-    latents, their gradient stream, node products P ([N][2D]) and the a1 /
-    zbar / dz streams are 2 bytes per element; node latents, aggregates and
-    node gradients are fp32 throughout."""
+def kernel_bytes(kind, N, E, n_tiles, prec, have_ebar=True, write_e=True, keep_a1=True, method=False):
+    """HBM bytes of one launch of the kernels this build runs: every input
+    read once and every output written once.  In bf16 the edge latents,
+    their gradient stream, node products P ([N][2D]) and the a1 / zbar
+    streams are 2 bytes per element; node latents, aggregates and node
+    gradients are fp32 throughout.  method=True counts only the method's
+    bytes (the MP step's own streams: edge latents in and out, the edge
+    gradient in and out, the sender-side intermediate zbar, indices and
+    node-level rows), leaving out the design's extra streams: the bf16
+    path's saved first-layer activations a1 (written by the forward, read
+    by the backward instead of a recompute)."""
     se = 2 if prec == "bf16" else 4
     row, frow = D * se, D * 4
     erow = row if prec == "bf16" else frow  # edge-gradient stream
     tiles = n_tiles * 16 + 4 * (N + 1)
     bf = prec == "bf16"
+    a1 = row if (keep_a1 and bf and not method) else 0
     if kind == "edge_fwd":
-        return (E * (row + 8 + (row if write_e else 0) + (row if keep_a1 and bf else 0))
+        return (E * (row + 8 + (row if write_e else 0) + a1)
                 + N * (2 * row + frow) + tiles)
     if kind == "edge_bwd":
-        if bf:  # from the saved a1: reads a1, ebar_in, aggbar; writes ebar_out, zbar, dz2, R
-            return (E * (row + (erow if have_ebar else 0) + 4 + erow + 2 * row)
+        if bf:  # fused: reads a1, e, ebar_in, aggbar; writes ebar_out, zbar, R
+            return (E * (a1 + row + (erow if have_ebar else 0) + 4 + erow + row)
                     + N * (frow + frow) + tiles)
         return (E * (row + (frow if have_ebar else 0) + frow + row + 8)
                 + N * (2 * row + frow + frow) + tiles)
-    if kind == "wgrad":
-        return E * row * (4 if bf else 2)
+    if kind == "wgrad":  # fp32 dW1e pass (bf16 computes it inside the fused backward)
+        return E * row * 2
     if kind == "node_srcsum":
         return E * (row + 4) + N * (4 + 4 * frow)
     if kind == "node_fwd":
@@ -122,13 +134,14 @@ def kernel_bytes(kind, N, E, n_tiles, prec, have_ebar=True, write_e=True, keep_a
     return None
 
 
-def step_bytes(kind, N, E, n_tiles, prec, m):
-    """Algorithmic bytes of every launch of `kind` in one fwd+bwd step (one
-    saving MGN call and its backward), or None."""
+def step_bytes(kind, N, E, n_tiles, prec, m, method=False):
+    """Bytes of every launch of `kind` in one fwd+bwd step (one saving MGN
+    call and its backward), or None."""
     if kind == "edge_fwd":
-        return sum(kernel_bytes(kind, N, E, n_tiles, prec, write_e=(l < m - 1)) for l in range(m))
+        return sum(kernel_bytes(kind, N, E, n_tiles, prec, write_e=(l < m - 1), method=method) for l in range(m))
     if kind == "edge_bwd":
-        return sum(kernel_bytes(kind, N, E, n_tiles, prec, have_ebar=(l < m - 1)) for l in range(m))
+        return sum(kernel_bytes(kind, N, E, n_tiles, prec, have_ebar=(l < m - 1), method=method)
+                   for l in range(m))
     if kind == "emit_p":
         return (m - 1) * kernel_bytes(kind, N, E, n_tiles, prec)
     if kind in ("wgrad", "node_srcsum", "node_fwd", "node_bwd", "wgrad_node"):
@@ -142,7 +155,7 @@ def step_bytes(kind, N, E, n_tiles, prec, m):
 KERNEL_SOURCES = {"edge_bwd": ("edge_rows.hip", "rows_common.hpp", "dev_common.hpp")}
 # The kernel symbol a profiled kernel kind runs as on the benchmark patch
 # (bf16): the fp32 kernel of the same kind must not be taken for it.
-KERNEL_SYMBOL = {"edge_bwd": "k_edge_bwd_rows", "edge_fwd": "k_edge_fwd_rows"}
+KERNEL_SYMBOL = {"edge_bwd": "k_edge_bwd_fused", "edge_fwd": "k_edge_fwd_rows"}
 
 
 def source_digest(kernel="edge_bwd"):
@@ -361,6 +374,144 @@ def c3_relabelled(S, args, reps=3, seed=7):
     return res
 
 
+def launch_bytes(kind, N, E, n_tiles, prec, m, method=False):
+    """Mean bytes per launch of `kind` over one fwd+bwd step, or None."""
+    if kind == "edge_bwd":
+        per = [kernel_bytes(kind, N, E, n_tiles, prec, have_ebar=(l < m - 1), method=method) for l in range(m)]
+    elif kind == "edge_fwd":
+        per = [kernel_bytes(kind, N, E, n_tiles, prec, write_e=(l < m - 1), method=method) for l in range(m)]
+    else:
+        per = [kernel_bytes(kind, N, E, n_tiles, prec, method=method)]
+    return float(np.mean(per)) if per[0] is not None else None
+
+
+def c3_other_slab(S, args, slab, reps=3):
+    """The benchmark's fwd+bwd step on another slab patch of the same mesh
+    (slab 7: 9 grid layers instead of 10), on the benchmark's context."""
+    import torch
+    import synth
+    from paper_2304_00338_amd import mgn
+    M, g, n = S["mesh"], S["g"], args.grid
+    part = synth.slab_part((n, n, n), args.slabs)
+    pt = mgn.extract_patch(g, part, slab, args.ghost)
+    mp = pt.patch_maps()
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a, np.float32)).cuda()
+    R = dict(S)
+    R.update({"dg": mgn.DeviceGraph(pt), "st": dev(M["onehot"][mp["node_l2g"]]),
+              "y": dev(M["states"][mp["node_l2g"]]),
+              "gout": dev(synth.loss_weights(pt.n_nodes, 0) * mp["interior"][:, None])})
+    R["ynext"] = torch.empty_like(R["y"])
+    step(R, mgn)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        step(R, mgn)
+    torch.cuda.synchronize()
+    dt = (time.perf_counter() - t0) / reps
+    res = {"workload": f"patch {slab} of {args.slabs} z-slabs, {args.ghost}-hop ghost zone, {args.mp_steps} MP "
+                       f"steps, {args.precision}, one Euler step fwd+bwd", "n_nodes": pt.n_nodes,
+           "n_interior": int(mp["n_interior"]), "n_edges": pt.n_edges, "ms_per_step": round(dt * 1e3, 3),
+           "mp_edges_per_s_fwdbwd": round(pt.n_edges * args.mp_steps / dt, 1)}
+    del R
+    return res
+
+
+def mesh_run(mgn, M, g, m, prec, scheme="euler", reps=5, warmup=2, profile=False):
+    """fwd+bwd integration steps of `scheme` on a whole mesh: the MGN calls
+    of every stage with saved activations, then the reverse through all of
+    them (loss on every node).  Returns the mean step time (ms) and, with
+    profile, the per-kernel event times of the timed steps."""
+    import torch
+    import synth
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a, np.float32)).cuda()
+    dg = mgn.DeviceGraph(g)
+    st, y = dev(M["onehot"]), dev(M["states"])
+    params = dev(synth.xavier_params(m, 0))
+    gout = dev(synth.loss_weights(g.n_nodes, 0))
+    stages = mgn.scheme_stages(scheme)
+    ctx = mgn.Context(m, g.n_nodes, g.n_edges, prec, max_stages=stages, save=True)
+    gp, ynext = torch.zeros_like(params), torch.empty_like(y)
+
+    def one():
+        gp.zero_()
+        mgn.mgn_integrate_step(ctx, dg, params, scheme, st, y, dg.efeat, ynext, save=True)
+        mgn.mgn_backward(ctx, gout, gp)
+    for _ in range(warmup):
+        one()
+    torch.cuda.synchronize()
+    if profile:
+        mgn.mgn_profile_enable(ctx, True)
+        mgn.mgn_profile_collect(ctx)
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        one()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / reps
+    prof = None
+    if profile:
+        prof = mgn.mgn_profile_collect(ctx)
+        mgn.mgn_profile_enable(ctx, False)
+    del ctx
+    return ms, prof
+
+
+def mfma_roofline(prof, prec, E, reps):
+    """The dominant kernel of a profiled fwd+bwd run placed against the MFMA
+    roof of its precision: executed MFMA flop per launch (per-edge count of
+    MFMA_FLOP_PER_EDGE times E) / its average launch time."""
+    dom = max(prof, key=lambda k: prof[k][0])
+    tot, cnt = prof[dom]
+    avg = tot / cnt
+    fpe = MFMA_FLOP_PER_EDGE[prec].get(dom)
+    peak = MFMA_PEAK_FP32_TFLOPS if prec == "fp32" else MFMA_PEAK_BF16_TFLOPS
+    r = {"bound": "mfma", "kernel": dom, "avg_launch_ms": round(avg, 4), "launches_per_step": cnt // reps,
+         "peak": peak, "unit": "TFLOP/s"}
+    if fpe is not None:
+        ach = fpe * E / (avg * 1e-3) / 1e12
+        r.update({"flop_per_launch": int(fpe * E), "achieved": round(ach, 1), "frac": round(ach / peak, 4)})
+    return r
+
+
+def config_lines(args):
+    """The other configurations at their full sizes: C1 (2D 32 x 32, 2 MP
+    steps, fp32), C2 (3D 32^3, 15 MP steps, fp32 and bf16, with the dominant
+    kernel against its MFMA roof) and C5 (the C2 mesh, Euler / midpoint
+    (RK2) / RK4 steps fwd+bwd through all stages, fp32 and bf16)."""
+    import synth
+    from paper_2304_00338_amd import mgn
+    out = {}
+    M1 = synth.mesh((32, 32), 0)
+    g1 = mgn.build_graph(M1["cells"], M1["pos"])
+    ms, prof = mesh_run(mgn, M1, g1, 2, "fp32", reps=20, warmup=3)
+    out["c1"] = {"workload": "2D 32x32 jittered triangulated mesh, 2 MP steps, fp32, one Euler step fwd+bwd",
+                 "n_nodes": g1.n_nodes, "n_edges": g1.n_edges, "ms_per_step": round(ms, 3),
+                 "mp_edges_per_s_fwdbwd": round(g1.n_edges * 2 / (ms * 1e-3), 1),
+                 "mgn_calls_per_s_fwdbwd": round(1e3 / ms, 2)}
+    M2 = synth.mesh((32, 32, 32), 0)
+    g2 = mgn.build_graph(M2["cells"], M2["pos"])
+    m = args.mp_steps
+    c2 = {"workload": f"3D 32^3 jittered Kuhn-tetrahedral mesh, {m} MP steps, one Euler step fwd+bwd",
+          "n_nodes": g2.n_nodes, "n_edges": g2.n_edges}
+    for prec in ("fp32", "bf16"):
+        ms, prof = mesh_run(mgn, M2, g2, m, prec, reps=5, warmup=2, profile=True)
+        c2[prec] = {"ms_per_step": round(ms, 3), "mp_edges_per_s_fwdbwd": round(g2.n_edges * m / (ms * 1e-3), 1),
+                    "mgn_calls_per_s_fwdbwd": round(1e3 / ms, 3),
+                    "roofline": mfma_roofline(prof, prec, g2.n_edges, 5),
+                    "kernel_ms_per_step": {k: round(v[0] / 5, 3)
+                                           for k, v in sorted(prof.items(), key=lambda x: -x[1][0])}}
+    out["c2"] = c2
+    c5 = {"workload": f"C2 mesh, one integration step fwd+bwd through every stage, {m} MP steps"}
+    for prec in ("fp32", "bf16"):
+        r = {}
+        for sc in ("euler", "midpoint", "rk4"):
+            ms, _ = mesh_run(mgn, M2, g2, m, prec, scheme=sc, reps=3, warmup=1)
+            st = mgn.scheme_stages(sc)
+            r[sc] = {"stages": st, "ms_per_step": round(ms, 3), "mgn_calls_per_s_fwdbwd": round(st * 1e3 / ms, 2)}
+        c5[prec] = r
+    out["c5"] = c5
+    return out
+
+
 def step(S, mgn, fwd_only=False):
     S["gp"].zero_()
     mgn.mgn_integrate_step(S["ctx"], S["dg"], S["params"], "euler", S["st"], S["y"], S["dg"].efeat,
@@ -487,35 +638,61 @@ def integrator_steps(S, args, reps=3):
     return out
 
 
-def cpu_baseline(args, min_seconds=10.0, max_calls=50):
-    """The fp64 oracle, as it stands, on a bounded sample: MGN calls (15 MP
-    steps) forward and backward on a jittered Kuhn mesh of the same kind
-    (13^3 grid), repeated until at least min_seconds of CPU work."""
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(args, c3_edges=None):
+    """The fp64 oracle, as it stands, on a bounded sample of the C2 mesh (the
+    3D 32^3 jittered Kuhn mesh, 434,558 edges): one MGN call fwd+bwd with
+    1 MP step and one with 2; their difference is one MP step fwd+bwd, so
+    value = E / (t2 - t1) MP-step edges/s.  Run with the host's BLAS threads
+    (all usable cores) and again limited to one thread; the 15-step C2 call
+    and the C3 patch call (11,674,318 edges) are extrapolated from these
+    (encoder and decoder cost t1 - (t2 - t1), plus 15 MP steps scaled by
+    the edge count), labelled as such."""
     import oracle as O
     import synth
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    except Exception:
-        threads = len(os.sched_getaffinity(0))
-    shape = (args.cpu_grid,) * 3
-    M = synth.mesh(shape, 0)
+    from threadpoolctl import threadpool_info, threadpool_limits
+    M = synth.mesh((32, 32, 32), 0)
     g = O.build_graph(M["cells"], M["pos"])
-    P = synth.xavier_params(args.mp_steps, 0)
     w = synth.loss_weights(g.n_nodes, 0)
-    calls = 0
-    t0 = time.time()
-    while calls < max_calls and (calls == 0 or time.time() - t0 < min_seconds):
-        _, tape = O.mgn_forward(g, P, M["node_in"], g.efeat, args.mp_steps, keep=True)
+    E, m_full = g.n_edges, args.mp_steps
+
+    def call(m):
+        P = synth.xavier_params(m, 0)
+        t0 = time.time()
+        _, tape = O.mgn_forward(g, P, M["node_in"], g.efeat, m, keep=True)
         O.mgn_backward(tape, w)
         del tape
-        calls += 1
-    dt = time.time() - t0
-    return {"value": g.n_edges * args.mp_steps * calls / dt, "unit": "edges/s", "cores": int(threads),
-            "kind": "oracle",
-            "sample": f"{calls} fp64 MGN calls fwd+bwd, {args.mp_steps} MP steps, on a jittered "
-                      f"{shape[0]}^3 Kuhn mesh ({g.n_nodes} nodes, {g.n_edges} edges): {dt:.1f}s",
-            "seconds": dt}
+        return time.time() - t0
+
+    def measure():
+        t1, t2 = call(1), call(2)
+        per = max(t2 - t1, 1e-9)
+        fixed = max(t1 - per, 0.0)
+        return {"t_1step_s": round(t1, 3), "t_2step_s": round(t2, 3), "mp_step_fwdbwd_s": round(per, 3),
+                "edges_per_s": E / per,
+                "c2_call_fwdbwd_s_extrapolated": round(fixed + m_full * per, 2),
+                "c3_call_fwdbwd_s_extrapolated": (round(fixed + m_full * per * c3_edges / E, 1)
+                                                  if c3_edges else None)}
+    blas = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    full = measure()
+    with threadpool_limits(limits=1):
+        one = measure()
+    return {"value": round(full["edges_per_s"], 1), "unit": "edges/s", "cores": int(blas), "kind": "oracle",
+            "sample": (f"fp64 oracle on the C2 mesh ({g.n_nodes} nodes, {E} edges): one MGN call fwd+bwd with 1 MP "
+                       f"step ({full['t_1step_s']} s) and with 2 ({full['t_2step_s']} s); value = E / their "
+                       f"difference, {blas} BLAS threads"),
+            "cpu_model": cpu_model(), "usable_cores": len(os.sched_getaffinity(0)),
+            "all_threads": full,
+            "one_thread": dict(one, value=round(one["edges_per_s"], 1), cores=1)}
 
 
 def main():
@@ -529,10 +706,11 @@ def main():
     ap.add_argument("--slab", type=int, default=8)
     ap.add_argument("--ghost", type=int, default=15)
     ap.add_argument("--mp-steps", type=int, default=15)
-    ap.add_argument("--cpu-grid", type=int, default=13)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-c4", action="store_true", help="skip the whole-mesh rollout measurement")
     ap.add_argument("--no-paper3d", action="store_true", help="skip the latent-150 3D training-step measurement")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the C1 / C2 / C5 and slab-7 lines")
     ap.add_argument("--no-relabelled", action="store_true",
                     help="skip the benchmark step on the randomly relabelled mesh")
     ap.add_argument("--paper3d-precs", default="fp32,bf16", help="precisions of the 3D training-step measurement")
@@ -608,22 +786,19 @@ def main():
     tot, cnt = prof[dom]
     avg_ms = tot / cnt
     n_tiles = S["dg"].n_tiles
-    if dom == "edge_bwd":
-        per = [kernel_bytes(dom, N, E, n_tiles, args.precision, have_ebar=(l < m - 1)) for l in range(m)]
-    elif dom == "edge_fwd":
-        per = [kernel_bytes(dom, N, E, n_tiles, args.precision, write_e=(l < m - 1)) for l in range(m)]
-    else:
-        per = [kernel_bytes(dom, N, E, n_tiles, args.precision)]
-    bytes_per_launch = float(np.mean(per)) if per[0] is not None else None
+    bytes_method = launch_bytes(dom, N, E, n_tiles, args.precision, m, method=True)
+    bytes_io = launch_bytes(dom, N, E, n_tiles, args.precision, m)
     roof = None
-    if bytes_per_launch is not None:
-        ach = bytes_per_launch / (avg_ms * 1e-3) / 1e9
+    if bytes_method is not None:
+        ach = bytes_method / (avg_ms * 1e-3) / 1e9
         traffic = measured_traffic(dom) if args.precision == "bf16" else None
         roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(ach / HBM_PEAK_GBS, 4),
                 "traffic": None if traffic is None else int(traffic), "kernel": dom,
                 "avg_launch_ms": round(avg_ms, 4), "launches_per_step": cnt // args.steps,
-                "algorithmic_bytes_per_launch": int(bytes_per_launch)}
+                "algorithmic_bytes_per_launch": int(bytes_method),
+                "kernel_io_bytes_per_launch": int(bytes_io),
+                "kernel_io_gbs": round(bytes_io / (avg_ms * 1e-3) / 1e9, 1)}
 
     value = E * m / (ms * 1e-3)
     out = {
@@ -647,8 +822,8 @@ def main():
                            for k in sorted(kern_ms, key=lambda x: -kern_ms[x])
                            if (sb := step_bytes(k, N, E, n_tiles, args.precision, m)) is not None},
     }
-    if dom in MFMA_FLOP_PER_EDGE and args.precision == "bf16":
-        fl = MFMA_FLOP_PER_EDGE[dom] * E
+    if dom in MFMA_FLOP_PER_EDGE[args.precision] and args.precision == "bf16":
+        fl = MFMA_FLOP_PER_EDGE[args.precision][dom] * E
         out["mfma"] = {"kernel": dom, "executed_flop_per_launch": fl,
                        "achieved_tflops": round(fl / (avg_ms * 1e-3) / 1e12, 1),
                        "peak_tflops": MFMA_PEAK_BF16_TFLOPS,
@@ -656,13 +831,22 @@ def main():
     out["train_step"] = train_steps(S, args)
     if not args.no_relabelled:
         out["c3_relabelled"] = c3_relabelled(S, args)
+    if not args.no_configs:
+        out["c3_slab7"] = c3_other_slab(S, args, 7)
+    # the benchmark's context (111 GiB) is released before the other runs
+    S["ctx"] = None
+    del ctx
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    if not args.no_configs:
+        out.update(config_lines(args))
     if not args.no_paper3d:
         out["paper_3d_train"] = paper_3d_train(S, args)
     if not args.no_c4:
         out["integrator_fwd_ms_per_step"] = integrator_steps(S, args)
         out["c4_rollout"] = c4_rollout(S, args)
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(args)
+        out["cpu_baseline"] = cpu_baseline(args, c3_edges=E)
     print(json.dumps(out), flush=True)
 
 
