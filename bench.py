@@ -41,13 +41,14 @@ def log(*a):
 # waves' three 128 x 128 products (W2 a1 recomputed, W2^T dz2, W1e^T zbar),
 # the gradient waves' dW2 = dz2^T a1 and dW1e = zbar^T e, and their ones
 # columns (8 MFMAs per 64-row round and gradient wave, 4 waves).
-# fp32 (feature-split kernels): the edge backward's five 128 x 128 products
-# per edge (W1e e and W2 a1 recomputed, W2^T dz2, W1e^T zbar, dW2), the
-# forward's two (W1e e, W2 a1), the separate dW1e pass one.
+# fp32 row-layout kernels (v_mfma_f32_16x16x4_f32, 2,048 flop each): the
+# forward's two 128 x 128 products (W1e e, W2 a1); the fused backward's four
+# (W1e e and W2 a1 recomputed, W2^T dz2, W1e^T zbar), dW2 and dW1e, and the
+# ones columns of db2 / db1 (64 MFMAs per 64-row round and wave, 4 waves).
 MFMA_FLOP_PER_EDGE = {"bf16": {"edge_fwd": 2 * 128 * 128 * 2 + 24 * 16384 // 16,
                                "edge_bwd": 5 * 2 * 128 * 128 + 4 * 8 * 16384 // 64},
-                      "fp32": {"edge_fwd": 2 * 2 * 128 * 128, "edge_bwd": 5 * 2 * 128 * 128,
-                               "wgrad": 2 * 128 * 128}}
+                      "fp32": {"edge_fwd": 2 * 2 * 128 * 128,
+                               "edge_bwd": 6 * 2 * 128 * 128 + 4 * 64 * 2048 // 64}}
 MFMA_PEAK_BF16_TFLOPS = 2500.0
 MFMA_PEAK_FP32_TFLOPS = 157.3
 
@@ -246,6 +247,44 @@ def summarize_profile(d, kernel):
                 tf = mops[k] * 512 / 1e12
                 rate = tf / (avg_ms[k] * 1e-3)
                 print(f"| {k} | {tf:.3f} | {rate:.0f} | {100 * rate / MFMA_PEAK_BF16_TFLOPS:.1f} |")
+    # wave-state counters (passes of at most four counters each): per-launch
+    # averages, as fractions of the waves' lifetime (SQ_WAVE_CYCLES)
+    sq = {}
+    for sub in ("prof_sq1", "prof_sq2", "prof_sq3", "prof_mfma"):
+        con = db(sub)
+        if con is None:
+            continue
+        for n, c, v in con.execute("select kernel_name, counter_name, value from counters_collection"):
+            sq.setdefault(short(n), {}).setdefault(c, []).append(v)
+    sq = {k: {c: sum(v) / len(v) for c, v in cs.items()} for k, cs in sq.items()}
+    if any("SQ_WAVE_CYCLES" in cs for cs in sq.values()):
+        avg_ms = {short(n): avg / 1e3 for n, c, tot, avg, pct in rows}
+        print("\nWave-state counters per launch (fractions of SQ_WAVE_CYCLES, the summed lifetime of the "
+              "kernel's waves): issuing any instruction / VALU / VMEM / LDS, waiting on a dependency "
+              "(SQ_WAIT_INST_ANY) and waiting at all (SQ_WAIT_ANY); LDS bank-conflict cycles per LDS instruction; "
+              "MFMA pipe busy as a fraction of the kernel's SIMD-cycles (SQ_VALU_MFMA_BUSY_CYCLES / (avg time x "
+              "2.4 GHz x 1024 SIMDs)).\n")
+        print("| kernel | waves | issue any | VALU | VMEM | LDS | wait dep | wait any | LDS conflict / inst "
+              "| MFMA busy |")
+        print("|---|---|---|---|---|---|---|---|---|---|")
+        for n, *_ in rows[:12]:
+            k = short(n)
+            cs = sq.get(k, {})
+            wc = cs.get("SQ_WAVE_CYCLES")
+            if not wc:
+                continue
+            fr = lambda c: f"{cs[c] / wc:.3f}" if c in cs else ""
+            conf = (f"{cs['SQ_LDS_BANK_CONFLICT'] / cs['SQ_INSTS_LDS']:.2f}"
+                    if cs.get("SQ_INSTS_LDS") and "SQ_LDS_BANK_CONFLICT" in cs else "")
+            mb = (f"{cs['SQ_VALU_MFMA_BUSY_CYCLES'] / (avg_ms[k] * 1e-3 * 2.4e9 * 1024):.3f}"
+                  if "SQ_VALU_MFMA_BUSY_CYCLES" in cs and avg_ms.get(k) else "")
+            print(f"| {k} | {cs.get('SQ_WAVES', 0):,.0f} | {fr('SQ_ACTIVE_INST_ANY')} | {fr('SQ_ACTIVE_INST_VALU')} | "
+                  f"{fr('SQ_ACTIVE_INST_VMEM')} | {fr('SQ_ACTIVE_INST_LDS')} | {fr('SQ_WAIT_INST_ANY')} | "
+                  f"{fr('SQ_WAIT_ANY')} | {conf} | {mb} |")
+        with open(os.path.join(d, "counters_per_launch.json"), "w") as fh:
+            json.dump({"trace_avg_ms": {short(n): avg / 1e3 for n, c, tot, avg, pct in rows},
+                       "fetch_kib": fetch, "write_kib": write, "fetch_scale": sf, "write_scale": sw,
+                       "sq": sq}, fh, indent=1)
     sym = KERNEL_SYMBOL.get(kernel, "k_" + kernel)
     k = next((short(n) for n, *_ in rows if short(n) == sym), None)
     if k is not None and k in fetch and k in write:
@@ -253,8 +292,9 @@ def summarize_profile(d, kernel):
                "fetch_kib_per_launch": fetch[k], "write_kib_per_launch": write[k],
                "fetch_scale": sf, "write_scale": sw,
                "bytes_per_launch": (fetch[k] * sf + write[k] * sw) * 1024}
-        with open(traffic_file(kernel), "w") as fh:
-            json.dump(out, fh, indent=1)
+        for f in (traffic_file(kernel), os.path.join(d, os.path.basename(traffic_file(kernel)))):
+            with open(f, "w") as fh:
+                json.dump(out, fh, indent=1)
         print(f"\n{k}: {out['bytes_per_launch'] / 1e9:.2f} GB of HBM traffic per launch "
               f"(written to {os.path.relpath(traffic_file(kernel), ROOT)})")
 
@@ -711,6 +751,8 @@ def main():
     ap.add_argument("--no-paper3d", action="store_true", help="skip the latent-150 3D training-step measurement")
     ap.add_argument("--no-configs", action="store_true",
                     help="skip the C1 / C2 / C5 and slab-7 lines")
+    ap.add_argument("--configs-only", action="store_true",
+                    help="only the C1 / C2 / C5 lines (one JSON object)")
     ap.add_argument("--no-relabelled", action="store_true",
                     help="skip the benchmark step on the randomly relabelled mesh")
     ap.add_argument("--paper3d-precs", default="fp32,bf16", help="precisions of the 3D training-step measurement")
@@ -747,6 +789,10 @@ def main():
             b.copy_(a)
         torch.cuda.synchronize()
         print(json.dumps({"copy_bytes_read": 4 * n, "copy_bytes_written": 4 * n, "launches": 3}))
+        return
+
+    if args.configs_only:
+        print(json.dumps(config_lines(args)), flush=True)
         return
 
     if args.paper3d_only:

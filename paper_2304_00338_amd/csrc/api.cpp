@@ -37,6 +37,7 @@ struct Off {
 
 struct PackOff {
   int64_t W1 = -1, W1t = -1, W2 = -1, W2t = -1, W1p = -1, W2p = -1;
+  int64_t F1 = -1, F2 = -1, F1t = -1, F2t = -1;  // fp32 edge MLPs: fragment-major W1e, W2 and transposes
   int64_t W1sp = -1, W1rp = -1;  // edge MLPs: row-permuted sender / receiver column blocks of W1
   int64_t W1ap = -1;             // node MLPs at width 160: row-permuted agg column block of W1
 };
@@ -110,9 +111,29 @@ void add_perm(Model& M, int64_t src, int ld, int64_t& W, int cols = kRowsD, int 
   M.ents.push_back(e);
 }
 
+// Fragment-major fp32 copy (mode 2) or copy of the transpose (mode 3) of
+// the square [n][n] block at float offset src (row stride ld).
+void add_frag(Model& M, int64_t src, int ld, int n, int mode, int64_t& W) {
+  auto al = [](int64_t x) { return (x + 63) & ~int64_t(63); };
+  M.pack_elems = al(M.pack_elems);
+  W = M.pack_elems;
+  M.pack_elems += (int64_t)n * n;
+  PackEnt e;
+  e.src = src;
+  e.dst = W;
+  e.dstt = -1;
+  e.rows = n;
+  e.cols = n;
+  e.ld = ld;
+  e.perm = mode;
+  M.ents.push_back(e);
+}
+
 // Parameter layout and packed operand copies of an MGN with m MP steps and
-// latent width lat (both MLP layers of every block are lat wide).
-Model make_model(int m, int lat) {
+// latent width lat (both MLP layers of every block are lat wide); fp32
+// models also carry the fragment-major edge-MLP copies of the fp32
+// row-layout edge kernels.
+Model make_model(int m, int lat, bool fp32 = false) {
   const int D = lat;
   Model M;
   M.m = m;
@@ -157,6 +178,12 @@ Model make_model(int m, int lat) {
     }
     add_pack(M, M.node[i].W1, D, 2 * D, M.p_node[i].W1, M.p_node[i].W1t);
     add_pack(M, M.node[i].W2, D, D, M.p_node[i].W2, M.p_node[i].W2t);
+    if (fp32) {
+      add_frag(M, M.edge[i].W1, 3 * D, D, 2, M.p_edge[i].F1);
+      add_frag(M, M.edge[i].W2, D, D, 2, M.p_edge[i].F2);
+      add_frag(M, M.edge[i].W1, 3 * D, D, 3, M.p_edge[i].F1t);
+      add_frag(M, M.edge[i].W2, D, D, 3, M.p_edge[i].F2t);
+    }
   }
   add_pack(M, M.dec.W1, D, D, M.p_dec.W1, M.p_dec.W1t);
   return M;
@@ -473,6 +500,10 @@ struct Run {
     w.W1t = p.W1t >= 0 ? P(p.W1t) : nullptr;
     w.W2 = p.W2 >= 0 ? P(p.W2) : nullptr;
     w.W2t = p.W2t >= 0 ? P(p.W2t) : nullptr;
+    w.F1 = p.F1 >= 0 ? (const float*)P(p.F1) : nullptr;
+    w.F2 = p.F2 >= 0 ? (const float*)P(p.F2) : nullptr;
+    w.F1t = p.F1t >= 0 ? (const float*)P(p.F1t) : nullptr;
+    w.F2t = p.F2t >= 0 ? (const float*)P(p.F2t) : nullptr;
     w.W1f = params + o.W1;
     w.W2f = params + o.W2;
     w.b1 = params + o.b1;
@@ -531,7 +562,10 @@ struct Run {
     for (int l = 0; l < m; ++l) {
       const bool last = l == m - 1;
       void* e_out = c.save ? (last ? nullptr : e_l(k, l + 1)) : e_l(k, 0);
-      if (E > 0)
+      if (E > 0 && prec == MGN_FP32)
+        LAUNCH(K_EDGE_FWD, launch_edge_fwd_r32(D, tl, e_l(k, l), e_out, last ? 0 : 1, P_l(k, l),
+                                               W(M.edge[l], M.p_edge[l]), eps, agg_l(k, l), slots(), s));
+      else if (E > 0)
         LAUNCH(K_EDGE_FWD, launch_edge_fwd(prec, D, tl, e_l(k, l), e_out, last ? 0 : 1, P_l(k, l), W(M.edge[l], M.p_edge[l]),
                                 eps, agg_l(k, l), slots(), a1_l(k, l), s));
       else
@@ -645,6 +679,16 @@ struct Run {
         LAUNCH(K_WGRAD, launch_wgrad2_w160(E, zbar, e_l(k, l), dz, a1_l(k, l), P3, &nb, s));
         if ((rc = job(nb, 3, 0, D, D, grad, oe.W1, 3 * D)) != MGN_OK) return rc;
         if ((rc = job(nb, 3, (int64_t)D * D, D, D, grad, oe.W2, D)) != MGN_OK) return rc;
+      } else if (D == kRowsD) {
+        // fp32, width 128: one wave per row block, the reverse and the edge
+        // MLP's weight gradients in one pass
+        LAUNCH(K_EDGE_BWD, launch_edge_bwd_r32(D, tl, e_l(k, l), (float*)ebar, l < m - 1 ? 1 : 0, (float*)ebar,
+                                               P_l(k, l), aggbar, W(oe, M.p_edge[l]), eps, zbar, R, slots(), P2, &nb,
+                                               s));
+        if ((rc = job(nb, 2, 0, D, D, grad, oe.W1, 3 * D)) != MGN_OK) return rc;
+        if ((rc = job(nb, 2, 16384, 1, D, grad, oe.b1, 0)) != MGN_OK) return rc;
+        if ((rc = job(nb, 2, 16512, 1, D * D + D, grad, oe.W2, 0)) != MGN_OK) return rc;
+        if ((rc = job(nb, 2, 33024, 1, 2 * D, grad, oe.g, 0)) != MGN_OK) return rc;
       } else {
         LAUNCH(K_EDGE_BWD, launch_edge_bwd(prec, D, tl, e_l(k, l), (float*)ebar, l < m - 1 ? 1 : 0, (float*)ebar, P_l(k, l), aggbar,
                                 W(oe, M.p_edge[l]), eps, zbar, R, slots(), P2, &nb, s));
@@ -903,7 +947,7 @@ int mgn_ctx_create(const mgn_config* cfg, int64_t max_nodes, int64_t max_edges, 
   c.DR = cfg->latent;
   c.LD = cfg->latent == 150 ? 160 : cfg->latent;
   try {
-    c.M = make_model(cfg->mp_steps, c.LD);
+    c.M = make_model(cfg->mp_steps, c.LD, cfg->precision == MGN_FP32);
     c.Mr = c.LD == c.DR ? c.M : make_model(cfg->mp_steps, c.DR);
     if (c.LD != c.DR) c.pad = pad_blocks(c.Mr, c.M);
   } catch (const std::bad_alloc&) {

@@ -33,7 +33,6 @@ struct __attribute__((aligned(16))) RowsLds {
   __attribute__((aligned(16))) float stage[NW][16 * RW_LDM];
 };
 
-__device__ __forceinline__ int tile_rows(int4 d) { return d.w - d.z; }
 
 // In-segment node sums over one staged 16-row half [lo_row, lo_row + 16) of
 // a tile (rows past the tile's end are never inside a segment).  For a tile

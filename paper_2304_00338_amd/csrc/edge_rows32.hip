@@ -1,0 +1,620 @@
+// Edge phase of one MGN message-passing step in fp32 (Sec. 2.1: every edge
+// latent is updated by the edge MLP from itself and its two end nodes, then
+// each node sums the new messages of its in-edges), with one wave per
+// receiver-aligned tile, at kernel width LD = 128 or 160 (latent 150 padded
+// with zero columns).
+//
+// Lane layout.  Lane l (i = l & 15, g = l >> 4) holds row i of a 16-row
+// block and the KL = LD / 4 features [KL g, KL g + KL) of it: the four lanes
+// of a row hold one contiguous row, and every lane's slice is contiguous in
+// memory (16-byte loads and stores).  The products run transposed on
+// v_mfma_f32_16x16x4_f32, C[feature][row] = W x^T: K step s takes the
+// features KL g + s from lane group g (the lane's own value s is the B
+// operand), and the A operand comes from a fragment-major copy of W whose
+// output rows are ordered so that the C fragment of output block ob gives
+// lane group g the features KL g + 4 ob + r (r < 4), i.e. its own values
+// 4 ob + r: a product's output is the next product's B operand without
+// leaving registers.  The weights are read from global memory (L2) one
+// 16-byte piece per lane per four K steps; in fp32 the MFMA time per row is
+// about 30 times the weight traffic.
+#include "launch.hpp"
+#include "rows_common.hpp"
+
+namespace mgn {
+namespace dev {
+
+template <int LD>
+struct R32 {
+  static constexpr int KL = LD / 4;        // features per lane
+  static constexpr int KC = KL / 4;        // 16-byte pieces per lane
+  static constexpr int NOB = LD / 16;      // 16-feature output blocks
+  static constexpr int DR = Width<LD>::DR; // real latent width
+  static constexpr int SLD = LD + 4;       // LDS row stride of a staged fp32 half-tile
+};
+
+// A fragment of output block ob, K steps 4c .. 4c + 3, of a fragment-major
+// fp32 matrix (lane l holds its four A values, one per K step).
+template <int LD>
+__device__ __forceinline__ f32x4 afrag32(const float* __restrict__ Wf, int ob, int c, int lane) {
+  return *reinterpret_cast<const f32x4*>(Wf + ((size_t)(ob * R32<LD>::KC + c) * 64 + lane) * 4);
+}
+
+// acc[ob] += W x for the lane's KL values x (B operands, K step s = x[s]).
+template <int LD>
+__device__ __forceinline__ void gemm32(f32x4 (&acc)[R32<LD>::NOB], const float (&x)[R32<LD>::KL],
+                                       const float* __restrict__ Wf, int lane) {
+  typedef R32<LD> Z;
+#pragma unroll
+  for (int c = 0; c < Z::KC; ++c) {
+    f32x4 a[Z::NOB];
+#pragma unroll
+    for (int ob = 0; ob < Z::NOB; ++ob) a[ob] = afrag32<LD>(Wf, ob, c, lane);
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+      for (int ob = 0; ob < Z::NOB; ++ob)
+        acc[ob] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[ob][t], x[4 * c + t], acc[ob], 0, 0, 0);
+  }
+}
+
+// The lane's KL contiguous floats of a row starting at p.
+template <int LD>
+__device__ __forceinline__ void load_row32(float (&x)[R32<LD>::KL], const float* __restrict__ p) {
+#pragma unroll
+  for (int c = 0; c < R32<LD>::KC; ++c) {
+    const f32x4 v = *reinterpret_cast<const f32x4*>(p + 4 * c);
+#pragma unroll
+    for (int t = 0; t < 4; ++t) x[4 * c + t] = v[t];
+  }
+}
+template <int LD>
+__device__ __forceinline__ void store_row32(float* __restrict__ p, const f32x4 (&v)[R32<LD>::NOB]) {
+#pragma unroll
+  for (int ob = 0; ob < R32<LD>::NOB; ++ob) *reinterpret_cast<f32x4*>(p + 4 * ob) = v[ob];
+}
+
+// Four waves per block, one per SIMD: a wave has 512 registers (the fp32
+// rows of a half and its prefetch need more than the 256 of two waves per
+// SIMD), and its eight independent accumulator chains keep the MFMA pipe
+// busy on their own.
+constexpr int R32_NW = 4;
+constexpr int R32_NT = 64 * R32_NW;
+
+template <int LD>
+struct __attribute__((aligned(16))) Fwd32Lds {
+  __attribute__((aligned(16))) float stage[R32_NW][16 * R32<LD>::SLD];
+};
+
+// In-segment node sums over one staged 16-row half [lo_row, lo_row + 16) of
+// a tile (as in the bf16 forward): node j's rows are [rp(j) - base,
+// rp(j + 1) - base), rp(j) held by lane j of segraw; a chunk tile is the
+// single segment [0, n).  Each lane sums the LD / 2 feature pairs p = lane,
+// lane + 64 (p < LD / 2) of every row in ascending row order from 0.0;
+// close(j, pair index, sum) stores a finished node sum.
+template <int LD, class F>
+__device__ __forceinline__ void seg_pass32(const float* stage, int lane, int segraw, int base, bool chunk, int n,
+                                           int nv, int lo_row, int& j, float2 (&carry)[2], F&& close) {
+  constexpr int NP = LD / 2, SLD = R32<LD>::SLD;
+  const int hi_row = lo_row + 16;
+  while (j < nv) {
+    const int a = chunk ? 0 : __builtin_amdgcn_readlane(segraw, j) - base;
+    const int b = chunk ? n : __builtin_amdgcn_readlane(segraw, j + 1) - base;
+    const int u0 = max(a, lo_row), u1 = min(b, hi_row);
+    for (int u = u0; u < u1; ++u) {
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int p = lane + 64 * h;
+        if (h == 0 || p < NP) {
+          const float2 v = *reinterpret_cast<const float2*>(stage + (u - lo_row) * SLD + 2 * p);
+          carry[h].x += v.x;
+          carry[h].y += v.y;
+        }
+      }
+    }
+    if (b > hi_row) break;
+    close(j, carry);
+    carry[0] = carry[1] = float2{0.f, 0.f};
+    ++j;
+  }
+}
+
+// Forward: e' = e + m (when write_e), agg = receiver sums of m, with
+// m = LN(W2 relu(b1 + P_s + P_r + W1e e) + b2) (the node products P = [W1s
+// h, W1r h] of the block come from the node kernels).  The next half's rows
+// are in flight while a half is computed; all global loads are
+// unconditional from clamped indices (rows past a tile's end read a valid
+// row that is never stored or summed).
+template <int LD>
+__global__ void __launch_bounds__(R32_NT) __attribute__((amdgpu_waves_per_eu(1, 1)))
+k_edge_fwd_r32(EdgeTiles tl, const float* __restrict__ e_in, float* __restrict__ e_out, int write_e,
+               const float* __restrict__ Pn, MlpW w, float eps, float* __restrict__ agg, float* __restrict__ slots) {
+  typedef R32<LD> Z;
+  __shared__ __align__(16) Fwd32Lds<LD> S;
+  const int tid = threadIdx.x, lane = tid & 63, i = lane & 15, g = lane >> 4;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const UnitRange ur = unit_range<R32_NW>(tl.n_tiles, wv);
+  int64_t t = ur.t;
+  const int64_t stride = ur.stride, tend = ur.end;
+  if (t >= tend) return;
+  const int f0 = Z::KL * g;  // first feature of the lane
+
+  const int4* tiles = reinterpret_cast<const int4*>(tl.tiles);
+  auto desc = [&](int64_t tt) -> int4 {
+    const bool ok = tt < tend;
+    const int4 v = tiles[ok ? tt : tend - 1];
+    int4 r;
+    r.x = ok ? v.x : 0;
+    r.y = ok ? v.y : 0;
+    r.z = ok ? v.z : 0;
+    r.w = ok ? v.w : 0;
+    return r;
+  };
+  const int lastE = (int)max(tl.n_edges - 1, (int64_t)0);
+  auto erow = [&](int4 d, int rb) { return min(max(d.z + min(rb * 16 + i, tile_rows(d) - 1), 0), lastE); };
+  struct Half {
+    float e[Z::KL];
+    f32x4 p[Z::NOB];  // b1 + P_s + P_r in the C layout
+  };
+  auto load_half = [&](int4 d, int rb, Half& H) {
+    const int row = erow(d, rb);
+    const int snd = tl.senders[row], rcv = tl.receivers[row];
+    load_row32<LD>(H.e, e_in + (size_t)row * LD + f0);
+    const float* ps = Pn + (size_t)snd * (2 * LD) + f0;
+    const float* pr = Pn + (size_t)rcv * (2 * LD) + LD + f0;
+#pragma unroll
+    for (int ob = 0; ob < Z::NOB; ++ob) {
+      const f32x4 b1 = *reinterpret_cast<const f32x4*>(w.b1 + f0 + 4 * ob);
+      const f32x4 a = *reinterpret_cast<const f32x4*>(ps + 4 * ob);
+      const f32x4 b = *reinterpret_cast<const f32x4*>(pr + 4 * ob);
+      H.p[ob] = (b1 + a) + b;
+    }
+  };
+  float* stage = S.stage[wv];
+
+  auto half = [&](Half& H, int4 d0, int rb, int segraw, bool chunk, int nv, int& j, float2 (&carry)[2]) {
+    const int n = tile_rows(d0);
+    const int row = rb * 16 + i;
+    // ---- z1 = b1 + P_s + P_r + W1e e, a1 = relu(z1)
+    f32x4 acc[Z::NOB];
+#pragma unroll
+    for (int ob = 0; ob < Z::NOB; ++ob) acc[ob] = H.p[ob];
+    // the weight addresses are opaque per half: otherwise the loop-invariant
+    // fragment loads are hoisted out of the tile loop into registers
+    const int oz = opaque_zero();
+    gemm32<LD>(acc, H.e, w.F1 + oz, lane);
+    float a1[Z::KL];
+#pragma unroll
+    for (int ob = 0; ob < Z::NOB; ++ob)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) a1[4 * ob + r] = relu(acc[ob][r]);
+    // ---- z2 = b2 + W2 a1
+#pragma unroll
+    for (int ob = 0; ob < Z::NOB; ++ob) acc[ob] = *reinterpret_cast<const f32x4*>(w.b2 + f0 + 4 * ob);
+    gemm32<LD>(acc, a1, w.F2 + oz, lane);
+    // ---- LayerNorm over the row's DR real features (padded ones are 0)
+    float sm = 0.f;
+#pragma unroll
+    for (int ob = 0; ob < Z::NOB; ++ob)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) sm += acc[ob][r];
+    const float mean = sum_q(sm) * (1.0f / Z::DR);
+    float sq = 0.f;
+#pragma unroll
+    for (int ob = 0; ob < Z::NOB; ++ob)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float dlt = acc[ob][r] - mean;
+        acc[ob][r] = dlt;
+        if (Z::DR == LD || f0 + 4 * ob + r < Z::DR) sq += dlt * dlt;
+      }
+    const float rstd = __builtin_amdgcn_rsqf(sum_q(sq) * (1.0f / Z::DR) + eps);
+#pragma unroll
+    for (int ob = 0; ob < Z::NOB; ++ob) {
+      const f32x4 ga = *reinterpret_cast<const f32x4*>(w.gamma + f0 + 4 * ob);
+      const f32x4 be = *reinterpret_cast<const f32x4*>(w.beta + f0 + 4 * ob);
+      acc[ob] = ga * (acc[ob] * rstd) + be;  // message m
+    }
+    store_row32<LD>(stage + i * Z::SLD + f0, acc);
+    // ---- e_out = e + m
+    if (write_e && row < n) {
+      f32x4 o[Z::NOB];
+#pragma unroll
+      for (int ob = 0; ob < Z::NOB; ++ob)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) o[ob][r] = H.e[4 * ob + r] + acc[ob][r];
+      store_row32<LD>(e_out + ((size_t)d0.z + row) * LD + f0, o);
+    }
+    wave_lds_sync();
+    seg_pass32<LD>(stage, lane, segraw, d0.z, chunk, n, nv, rb * 16, j, carry, [&](int jj, float2 (&v)[2]) {
+      float* dst = !chunk ? agg + (size_t)(d0.x + jj) * LD : slots + (size_t)(-1 - d0.y) * LD;
+      *reinterpret_cast<float2*>(dst + 2 * lane) = v[0];
+      if (LD / 2 > 64 && lane + 64 < LD / 2) *reinterpret_cast<float2*>(dst + 2 * (lane + 64)) = v[1];
+    });
+    wave_lds_sync();
+  };
+
+  int4 d0 = desc(t), d1 = desc(t + stride);
+  Half A, B;
+  load_half(d0, 0, A);
+  for (; t < tend; t += stride) {
+    const bool chunk = d0.y < 0;
+    const int nv = chunk ? 1 : d0.y - d0.x;
+    const int segraw = tl.rowptr[min(d0.x + lane, max(d0.x, d0.y))];
+    const int4 d2 = desc(t + 2 * stride);
+    load_half(d0, 1, B);
+    float2 carry[2] = {{0.f, 0.f}, {0.f, 0.f}};
+    int j = 0;
+    half(A, d0, 0, segraw, chunk, nv, j, carry);
+    load_half(d1, 0, A);
+    half(B, d0, 1, segraw, chunk, nv, j, carry);
+    d0 = d1;
+    d1 = d2;
+  }
+}
+
+
+// ================================================================= reverse
+// fp32 edge reverse with its weight gradients in one pass (width 128): per
+// 16-row half of a tile, from the block's input edge latents e, the node
+// products P (the first layer is recomputed: z1 = b1 + P_s + P_r + W1e e)
+// and the incoming gradients (ebar_in, aggbar at the receiver), it writes
+// zbar = dL/dz1 (for the sender sums), the receiver sums R of zbar and
+// ebar_out = ebar_in + W1e^T zbar, and accumulates dW2 = sum dz2^T a1,
+// dW1e = sum zbar^T e, db2, db1 (ones columns), dgamma, dbeta (DPP column
+// sums).  Four waves per block, one per SIMD (512 registers: the weight
+// gradient accumulators, a quarter of dW2 and dW1e per wave, live in
+// AGPRs), in lockstep rounds: each wave computes one half and stages its
+// rows of dz2, a1, e and zbar in LDS, then after a block barrier adds the
+// round's 64 rows into its 32 output rows of dW2 and dW1e with the row
+// index as the K dimension.  In fp32 the MFMA work (four 128 x 128 products
+// per row plus the weight gradients) dominates each round, so one wave per
+// SIMD keeps the MFMA pipe busy with its own independent chains.
+constexpr int B32_LD = 128;
+constexpr int B32_SLD = B32_LD + 16;  // staged row stride: lane groups 0, 1 hit distinct banks
+constexpr int B32_ROWS = 16 * R32_NW;
+
+struct __attribute__((aligned(16))) Bwd32Lds {
+  // staged streams of a round: 0 dz2, 1 a1, 2 e, 3 zbar
+  __attribute__((aligned(16))) float st[4][B32_ROWS * B32_SLD];
+};
+
+// in-segment sums of the staged zbar rows (as in seg_pass32, stride B32_SLD)
+template <class F>
+__device__ __forceinline__ void seg_pass_b32(const float* stage, int lane, int segraw, int base, bool chunk, int n,
+                                             int nv, int lo_row, int& j, float2& carry, F&& close) {
+  const int hi_row = lo_row + 16;
+  while (j < nv) {
+    const int a = chunk ? 0 : __builtin_amdgcn_readlane(segraw, j) - base;
+    const int b = chunk ? n : __builtin_amdgcn_readlane(segraw, j + 1) - base;
+    const int u0 = max(a, lo_row), u1 = min(b, hi_row);
+    for (int u = u0; u < u1; ++u) {
+      const float2 v = *reinterpret_cast<const float2*>(stage + (u - lo_row) * B32_SLD + 2 * lane);
+      carry.x += v.x;
+      carry.y += v.y;
+    }
+    if (b > hi_row) break;
+    close(j, carry);
+    carry = float2{0.f, 0.f};
+    ++j;
+  }
+}
+
+__global__ void __launch_bounds__(R32_NT) __attribute__((amdgpu_waves_per_eu(1, 1)))
+k_edge_bwd_r32(EdgeTiles tl, const float* __restrict__ e_in, const float* ebar_in, int have_ebar, float* ebar_out,
+               const float* __restrict__ Pn, const float* __restrict__ aggbar, MlpW w, float eps,
+               float* __restrict__ zbar, float* __restrict__ R, float* __restrict__ slots, Partials part) {
+  constexpr int LD = B32_LD;
+  typedef R32<LD> Z;
+  __shared__ __align__(16) Bwd32Lds S;
+  const int tid = threadIdx.x, lane = tid & 63, i = lane & 15, g = lane >> 4;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int f0 = Z::KL * g;
+
+  // The block's tiles: XCD-contiguous ranges, wave wv takes tile tb + wv of
+  // every round pair; all four waves run the same number of rounds.
+  const int G = gridDim.x;
+  int64_t tb, stride, tend;
+  if ((G & 7) == 0) {
+    const int x = blockIdx.x & 7, per = G >> 3;
+    const int64_t chunk = (tl.n_tiles + 7) >> 3;
+    const int64_t lo = x * chunk;
+    tend = min(tl.n_tiles, lo + chunk);
+    tb = lo + (int64_t)(blockIdx.x >> 3) * R32_NW;
+    stride = (int64_t)per * R32_NW;
+  } else {
+    tb = (int64_t)blockIdx.x * R32_NW;
+    stride = (int64_t)G * R32_NW;
+    tend = tl.n_tiles;
+  }
+  const int4* tiles = reinterpret_cast<const int4*>(tl.tiles);
+  const int64_t tlast = max(tend - 1, (int64_t)0);
+  auto desc = [&](int64_t tt) -> int4 {
+    const bool ok = tt < tend;
+    const int4 v = tiles[ok ? tt : tlast];
+    int4 r;
+    r.x = ok ? v.x : 0;
+    r.y = ok ? v.y : 0;
+    r.z = ok ? v.z : 0;
+    r.w = ok ? v.w : 0;
+    return r;
+  };
+  const int lastE = (int)max(tl.n_edges - 1, (int64_t)0);
+  auto erow = [&](int4 d, int rb) { return min(max(d.z + min(rb * 16 + i, tile_rows(d) - 1), 0), lastE); };
+  struct Half {
+    float e[Z::KL];
+  };
+  auto load_half = [&](int4 d, int rb, Half& H) {
+    load_row32<LD>(H.e, e_in + (size_t)erow(d, rb) * LD + f0);
+  };
+
+  // this wave's share of the weight gradients: output rows [32 wv, 32 wv + 32)
+  f32x4 aw2[2][8], aw1[2][8], ab2[2], ab1[2];
+#pragma unroll
+  for (int ob = 0; ob < 2; ++ob) {
+    ab2[ob] = ab1[ob] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int nb = 0; nb < 8; ++nb) aw2[ob][nb] = aw1[ob][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  // dgamma, dbeta: per half, the column sums over its 16 rows by the DPP
+  // butterfly (lane i ends with 2 of lane group g's 32 column sums),
+  // accumulated per lane
+  float2 dga = {0.f, 0.f}, dbe = {0.f, 0.f};
+  const int srow = 16 * wv + i;
+  auto stage_row = [&](float* X, const float (&v)[Z::KL], bool live) {
+    float* p = X + srow * B32_SLD + f0;
+#pragma unroll
+    for (int c = 0; c < Z::KC; ++c)
+      *reinterpret_cast<f32x4*>(p + 4 * c) =
+          live ? f32x4{v[4 * c], v[4 * c + 1], v[4 * c + 2], v[4 * c + 3]} : f32x4{0.f, 0.f, 0.f, 0.f};
+  };
+
+  auto round = [&](Half& H, int4 d0, int rb, int segraw, bool chunk, int nv, int& j, float2& carry) {
+    const int n = tile_rows(d0);
+    const int row = rb * 16 + i;
+    const bool live = row < n;
+    const size_t grow = (size_t)erow(d0, rb);
+    const int snd = tl.senders[grow], rcv = tl.receivers[grow];
+    const int oz = opaque_zero();
+    // the incoming edge gradient of the half (needed after the forward
+    // recompute: in flight during its two products)
+    float eb[Z::KL];
+    load_row32<LD>(eb, ebar_in + grow * LD + f0);
+    if (!have_ebar)
+#pragma unroll
+      for (int s = 0; s < Z::KL; ++s) eb[s] = 0.f;
+    // ---- z1 = W1e e + (b1 + P_s + P_r), a1 = relu(z1); e is staged right
+    // after its product (the staging is free: every wave has finished the
+    // previous round's products)
+    f32x4 acc[Z::NOB];
+#pragma unroll
+    for (int ob = 0; ob < Z::NOB; ++ob) acc[ob] = f32x4{0.f, 0.f, 0.f, 0.f};
+    __syncthreads();
+    gemm32<LD>(acc, H.e, w.F1 + oz, lane);
+    stage_row(S.st[2], H.e, live);
+    float a1[Z::KL];
+    uint32_t mask = 0;
+    {
+      const float* ps = Pn + (size_t)snd * (2 * LD) + f0;
+      const float* pr = Pn + (size_t)rcv * (2 * LD) + LD + f0;
+#pragma unroll
+      for (int ob = 0; ob < Z::NOB; ++ob) {
+        const f32x4 b1 = *reinterpret_cast<const f32x4*>(w.b1 + f0 + 4 * ob);
+        const f32x4 pa = *reinterpret_cast<const f32x4*>(ps + 4 * ob);
+        const f32x4 pb = *reinterpret_cast<const f32x4*>(pr + 4 * ob);
+        const f32x4 z = acc[ob] + ((b1 + pa) + pb);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          a1[4 * ob + r] = relu(z[r]);
+          if (z[r] > 0.f) mask |= 1u << (4 * ob + r);
+        }
+      }
+    }
+    // ---- z2 = b2 + W2 a1 and its LayerNorm statistics
+#pragma unroll
+    for (int ob = 0; ob < Z::NOB; ++ob) acc[ob] = *reinterpret_cast<const f32x4*>(w.b2 + f0 + 4 * ob);
+    gemm32<LD>(acc, a1, w.F2 + oz, lane);
+    float sm = 0.f;
+#pragma unroll
+    for (int ob = 0; ob < Z::NOB; ++ob)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) sm += acc[ob][r];
+    const float mean = sum_q(sm) * (1.0f / LD);
+    float sq = 0.f;
+#pragma unroll
+    for (int ob = 0; ob < Z::NOB; ++ob) {
+      acc[ob] -= mean;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) sq += acc[ob][r] * acc[ob][r];
+    }
+    const float rstd = __builtin_amdgcn_rsqf(sum_q(sq) * (1.0f / LD) + eps);
+    // ---- mbar = ebar_in + aggbar[receiver]; dgamma, dbeta; LayerNorm reverse
+    float dz[Z::KL];
+    {
+      const float* gp = aggbar + (size_t)rcv * LD + f0;
+      float s1 = 0.f, s2 = 0.f;
+      f32x4 pg[Z::NOB], pb[Z::NOB];
+#pragma unroll
+      for (int ob = 0; ob < Z::NOB; ++ob) {
+        const f32x4 ag = *reinterpret_cast<const f32x4*>(gp + 4 * ob);
+        const f32x4 ga = *reinterpret_cast<const f32x4*>(w.gamma + f0 + 4 * ob);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int s = 4 * ob + r;
+          const float xh = acc[ob][r] * rstd;
+          acc[ob][r] = xh;
+          const float mb = eb[s] + ag[r];
+          pg[ob][r] = live ? mb * xh : 0.f;
+          pb[ob][r] = live ? mb : 0.f;
+          const float dxh = mb * ga[r];
+          dz[s] = dxh;
+          s1 += dxh;
+          s2 += dxh * xh;
+        }
+      }
+      const float2 cg = colsum16(pg, i), cb = colsum16(pb, i);
+      dga.x += cg.x;
+      dga.y += cg.y;
+      dbe.x += cb.x;
+      dbe.y += cb.y;
+      const float m1 = sum_q(s1) * (1.0f / LD), m2 = sum_q(s2) * (1.0f / LD);
+#pragma unroll
+      for (int ob = 0; ob < Z::NOB; ++ob)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) dz[4 * ob + r] = rstd * (dz[4 * ob + r] - m1 - acc[ob][r] * m2);
+    }
+    // ---- stage dz2, a1
+    stage_row(S.st[0], dz, live);
+    stage_row(S.st[1], a1, live);
+    // ---- da1 = W2^T dz2, zbar = da1 where z1 > 0
+#pragma unroll
+    for (int ob = 0; ob < Z::NOB; ++ob) acc[ob] = f32x4{0.f, 0.f, 0.f, 0.f};
+    gemm32<LD>(acc, dz, w.F2t + oz, lane);
+    float zb[Z::KL];
+#pragma unroll
+    for (int ob = 0; ob < Z::NOB; ++ob)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) zb[4 * ob + r] = (mask >> (4 * ob + r)) & 1u ? acc[ob][r] : 0.f;
+    stage_row(S.st[3], zb, live);
+    if (live) {
+      float* zp = zbar + ((size_t)d0.z + row) * LD + f0;
+#pragma unroll
+      for (int c = 0; c < Z::KC; ++c)
+        *reinterpret_cast<f32x4*>(zp + 4 * c) = f32x4{zb[4 * c], zb[4 * c + 1], zb[4 * c + 2], zb[4 * c + 3]};
+    }
+    // ---- ebar_out = ebar_in + W1e^T zbar
+#pragma unroll
+    for (int ob = 0; ob < Z::NOB; ++ob)
+      acc[ob] = f32x4{eb[4 * ob], eb[4 * ob + 1], eb[4 * ob + 2], eb[4 * ob + 3]};
+    gemm32<LD>(acc, zb, w.F1t + oz, lane);
+    if (live) store_row32<LD>(ebar_out + ((size_t)d0.z + row) * LD + f0, acc);
+    __syncthreads();  // the round's rows are staged
+    // ---- receiver sums of zbar over this wave's staged rows
+    seg_pass_b32(S.st[3] + 16 * wv * B32_SLD, lane, segraw, d0.z, chunk, n, nv, rb * 16, j, carry,
+                 [&](int jj, float2 v) {
+                   float* dst = !chunk ? R + (size_t)(d0.x + jj) * LD : slots + (size_t)(-1 - d0.y) * LD;
+                   *reinterpret_cast<float2*>(dst + 2 * lane) = v;
+                 });
+    // ---- the round's 64 rows into this wave's output rows of dW2 and dW1e:
+    // A = dz2^T / zbar^T (rows 32 wv + 16 ob + m), B = a1 / e, K = 4 rows
+#pragma unroll 2
+    for (int kk = 0; kk < B32_ROWS / 4; ++kk) {
+      const int r0 = (4 * kk + g) * B32_SLD;
+      float A2[2], A1[2];
+#pragma unroll
+      for (int ob = 0; ob < 2; ++ob) {
+        A2[ob] = S.st[0][r0 + 32 * wv + 16 * ob + i];
+        A1[ob] = S.st[3][r0 + 32 * wv + 16 * ob + i];
+        ab2[ob] = __builtin_amdgcn_mfma_f32_16x16x4f32(A2[ob], 1.0f, ab2[ob], 0, 0, 0);
+        ab1[ob] = __builtin_amdgcn_mfma_f32_16x16x4f32(A1[ob], 1.0f, ab1[ob], 0, 0, 0);
+      }
+#pragma unroll
+      for (int nb = 0; nb < 8; ++nb) {
+        const float B2 = S.st[1][r0 + 16 * nb + i];
+        const float B1 = S.st[2][r0 + 16 * nb + i];
+#pragma unroll
+        for (int ob = 0; ob < 2; ++ob) {
+          aw2[ob][nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(A2[ob], B2, aw2[ob][nb], 0, 0, 0);
+          aw1[ob][nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(A1[ob], B1, aw1[ob][nb], 0, 0, 0);
+        }
+      }
+    }
+  };
+
+  if (tb < tend) {
+    int4 d0 = desc(tb + wv), d1 = desc(tb + wv + stride);
+    Half A, B;
+    load_half(d0, 0, A);
+    for (; tb < tend; tb += stride) {
+      const bool chunk = d0.y < 0;
+      const int nv = chunk ? 1 : d0.y - d0.x;
+      const int segraw = tl.rowptr[min(d0.x + lane, max(d0.x, d0.y))];
+      const int4 d2 = desc(tb + wv + 2 * stride);
+      load_half(d0, 1, B);
+      float2 carry = {0.f, 0.f};
+      int j = 0;
+      round(A, d0, 0, segraw, chunk, nv, j, carry);
+      load_half(d1, 0, A);
+      round(B, d0, 1, segraw, chunk, nv, j, carry);
+      d0 = d1;
+      d1 = d2;
+    }
+  }
+  // ---- block partials: weight gradients and db from the owning wave;
+  // dgamma, dbeta summed over the 16 rows of each lane group, then over the
+  // waves in wave order
+  float* base = part.buf + (size_t)blockIdx.x * part.stride;
+#pragma unroll
+  for (int ob = 0; ob < 2; ++ob) {
+#pragma unroll
+    for (int nb = 0; nb < 8; ++nb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int o = 32 * wv + 16 * ob + 4 * g + r;
+        base[16512 + (size_t)o * LD + 16 * nb + i] = aw2[ob][nb][r];
+        base[(size_t)o * LD + 16 * nb + i] = aw1[ob][nb][r];
+      }
+    if (i == 0)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        base[32896 + 32 * wv + 16 * ob + 4 * g + r] = ab2[ob][r];
+        base[16384 + 32 * wv + 16 * ob + 4 * g + r] = ab1[ob][r];
+      }
+  }
+  __syncthreads();
+  float* red = &S.st[0][0];  // [2][R32_NW][LD]
+  {
+    // lane i of group g holds the sums of values 2i, 2i + 1 = features
+    // f0 + 4 (i / 2) + 2 (i % 2) + {0, 1}
+    const int f = f0 + 4 * (i >> 1) + 2 * (i & 1);
+    *reinterpret_cast<float2*>(red + (0 * R32_NW + wv) * LD + f) = dga;
+    *reinterpret_cast<float2*>(red + (1 * R32_NW + wv) * LD + f) = dbe;
+  }
+  __syncthreads();
+  {
+    const int k2 = tid >> 7, c = tid & (LD - 1);  // 256 threads: dgamma (k2 = 0), dbeta (1)
+    float v = 0.f;
+#pragma unroll
+    for (int u = 0; u < R32_NW; ++u) v += red[(k2 * R32_NW + u) * LD + c];
+    base[33024 + k2 * LD + c] = v;
+  }
+}
+
+}  // namespace dev
+
+using namespace dev;
+
+static constexpr int kRows32Blocks = 256;
+
+hipError_t launch_edge_fwd_r32(int lat, const EdgeTiles& t, const void* e_in, void* e_out, int write_e,
+                               const void* Pn, const MlpW& w, float eps, float* agg, float* slots, hipStream_t s) {
+  if (t.n_tiles <= 0) return hipSuccess;
+  if (t.n_edges <= 0 || !w.F1 || !w.F2) return hipErrorInvalidValue;
+  const int64_t need = (t.n_tiles + R32_NW - 1) / R32_NW;
+  int g = (int)std::min<int64_t>(need, kRows32Blocks);
+  if (g >= 8) g &= ~7;
+#define F(LD)                                                                                                      \
+  hipLaunchKernelGGL(k_edge_fwd_r32<LD>, dim3(g), dim3(R32_NT), 0, s, t, (const float*)e_in, (float*)e_out, write_e, \
+                     (const float*)Pn, w, eps, agg, slots)
+  MGN_BY_WIDTH(lat, F);
+#undef F
+  return hipGetLastError();
+}
+
+hipError_t launch_edge_bwd_r32(int lat, const EdgeTiles& t, const void* e, const float* ebar_in, int have_ebar,
+                               float* ebar_out, const void* Pn, const float* aggbar, const MlpW& w, float eps,
+                               void* zbar, float* R, float* slots, const Partials& part, int* nblocks,
+                               hipStream_t s) {
+  *nblocks = 0;
+  if (t.n_tiles <= 0) return hipSuccess;
+  if (lat != B32_LD || t.n_edges <= 0 || part.stride < 33280 || !w.F1 || !w.F2 || !w.F1t || !w.F2t)
+    return hipErrorInvalidValue;
+  const int64_t need = (t.n_tiles + R32_NW - 1) / R32_NW;
+  int g = (int)std::min<int64_t>(need, std::min(kRows32Blocks, part.max_blocks));
+  if (g >= 8) g &= ~7;
+  *nblocks = g;
+  hipLaunchKernelGGL(k_edge_bwd_r32, dim3(g), dim3(R32_NT), 0, s, t, (const float*)e, ebar_in, have_ebar, ebar_out,
+                     (const float*)Pn, aggbar, w, eps, (float*)zbar, R, slots, part);
+  return hipGetLastError();
+}
+
+}  // namespace mgn

@@ -19,6 +19,24 @@ template <typename T>
 __global__ void __launch_bounds__(256) k_pack(const float* __restrict__ params, T* __restrict__ pack, PackList L) {
   const PackEnt pe = L.e[blockIdx.y];
   const int64_t n = (int64_t)pe.rows * pe.cols;
+  if (pe.perm >= 2) {
+    // fp32 fragment-major copy for the fp32 row-layout kernels (square
+    // rows x rows matrix M = W, or W^T when perm == 3): element idx =
+    // ((ob * KC + c) * 64 + l) * 4 + t holds M[o][k] with o = KL (m / 4) +
+    // 4 ob + m % 4 (output row of A-fragment row m = l % 16 of block ob) and
+    // k = KL (l / 16) + 4 c + t (K step 4c + t of lane group l / 16),
+    // KL = rows / 4 features per lane, KC = KL / 4.
+    const int KL = pe.rows / 4, KC = KL / 4;
+    for (int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x; idx < n; idx += (int64_t)gridDim.x * 256) {
+      const int t = (int)(idx & 3), l = (int)((idx >> 2) & 63);
+      const int rest = (int)(idx >> 8), c = rest % KC, ob = rest / KC;
+      const int m = l & 15, g = l >> 4;
+      const int64_t o = KL * (m >> 2) + 4 * ob + (m & 3), k = KL * g + 4 * c + t;
+      const int64_t src = pe.perm == 2 ? pe.src + o * pe.ld + k : pe.src + k * pe.ld + o;
+      pack[pe.dst + idx] = (T)params[src];
+    }
+    return;
+  }
   for (int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x; idx < n; idx += (int64_t)gridDim.x * 256) {
     const int64_t r = idx / pe.cols, c = idx % pe.cols;
     const int64_t sr = pe.perm ? perm_row((int)r) : r;

@@ -20,6 +20,10 @@ struct MlpW {
   const void* W1t;
   const void* W2;
   const void* W2t;
+  const float* F1;   // fp32 row-layout kernels: fragment-major copies of the edge
+  const float* F2;   // MLP's W1e (first layer, edge-latent block) and W2, and of
+  const float* F1t;  // their transposes
+  const float* F2t;
   const float* W1f;  // float32 first-layer weights (encoders: K = 4 / 8 on VALU)
   const float* W2f;  // float32 second-layer weights (decoder: 4 outputs on VALU)
   const float* b1;
@@ -34,7 +38,8 @@ struct PackEnt {
   int64_t dstt;  // element offset of the transposed copy (-1: none)
   int32_t rows, cols;
   int32_t ld;    // source row stride (floats)
-  int32_t perm;  // 1: copy row perm_row(p) of the source into row p
+  int32_t perm;  // 1: copy row perm_row(p) of the source into row p; 2 / 3: the
+                 // fp32 fragment-major copy of the square matrix / of its transpose
 };
 
 // Output-row order of the weights used by the row-per-wave edge kernels:
@@ -93,6 +98,20 @@ hipError_t launch_edge_fwd(int prec, int lat, const EdgeTiles& t, const void* e_
 // (nullable) receives the first-layer activations of every edge.
 hipError_t launch_edge_fwd_rows(const EdgeTiles& t, const void* e_in, void* e_out, int write_e, const void* P,
                                 const MlpW& w, float eps, float* agg, float* slots, void* a1_out, hipStream_t s);
+// fp32 edge forward with one wave per 16-row half of a tile at width lat
+// (128 or 160; uses MlpW::F1 / F2, the fragment-major W1e and W2, and the
+// fp32 vectors): e_out = e_in + m (write_e), agg / slots = receiver sums of m.
+hipError_t launch_edge_fwd_r32(int lat, const EdgeTiles& t, const void* e_in, void* e_out, int write_e,
+                               const void* Pn, const MlpW& w, float eps, float* agg, float* slots, hipStream_t s);
+// fp32 edge backward at width 128 with its weight gradients in one pass (one
+// wave per row block, four waves per block in lockstep rounds; recomputes
+// the first layer from e and P; uses MlpW::F1, F2, F1t, F2t): writes zbar,
+// R / slots, ebar_out (in place allowed) and per-block partials dW1e (0),
+// db1 (16384), dW2 (16512), db2 (32896), dgamma (33024), dbeta (33152).
+hipError_t launch_edge_bwd_r32(int lat, const EdgeTiles& t, const void* e, const float* ebar_in, int have_ebar,
+                               float* ebar_out, const void* Pn, const float* aggbar, const MlpW& w, float eps,
+                               void* zbar, float* R, float* slots, const Partials& part, int* nblocks,
+                               hipStream_t s);
 // bf16 edge backward with its weight gradients in one pass (four waves per
 // block in lockstep rounds): from the saved a1, the block's input edge
 // latents e and ebar_in (in place allowed), writes zbar, R / slots,

@@ -59,6 +59,9 @@ __device__ __forceinline__ bf16x8 select_frag(int h, int i, int q) {
   return a;
 }
 
+// Rows of a receiver-aligned tile {node_begin, node_end | -1 - slot, edge_begin, edge_end}.
+__device__ __forceinline__ int tile_rows(int4 d) { return d.w - d.z; }
+
 __device__ __forceinline__ bf16x8 as_frag(const uint4& u) { return __builtin_bit_cast(bf16x8, u); }
 
 // B operand of run s from the two C-layout fragments of blocks 2s, 2s + 1.
@@ -226,6 +229,7 @@ __device__ __forceinline__ const T& fresh(const T& lds) {
 struct UnitRange {
   int64_t t, stride, end;
 };
+template <int NWB = NW>  // waves per block
 __device__ __forceinline__ UnitRange unit_range(int64_t n_units, int wv) {
   const int G = gridDim.x;
   UnitRange u;
@@ -234,11 +238,11 @@ __device__ __forceinline__ UnitRange unit_range(int64_t n_units, int wv) {
     const int64_t chunk = (n_units + 7) >> 3;
     const int64_t lo = x * chunk;
     u.end = min(n_units, lo + chunk);
-    u.t = lo + (int64_t)(blockIdx.x >> 3) * NW + wv;
-    u.stride = (int64_t)per * NW;
+    u.t = lo + (int64_t)(blockIdx.x >> 3) * NWB + wv;
+    u.stride = (int64_t)per * NWB;
   } else {
-    u.t = (int64_t)blockIdx.x * NW + wv;
-    u.stride = (int64_t)G * NW;
+    u.t = (int64_t)blockIdx.x * NWB + wv;
+    u.stride = (int64_t)G * NWB;
     u.end = n_units;
   }
   return u;
