@@ -14,7 +14,9 @@ import os
 import numpy as np
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libmgn.so")
+# MGN_LIB selects another build of the same library (the host-sanitizer
+# build of build_sanitized.py); by default the in-tree libmgn.so
+LIB_PATH = os.environ.get("MGN_LIB") or os.path.join(HERE, "libmgn.so")
 
 OK, ERR_ARG, ERR_RANGE, ERR_SHAPE, ERR_WORKSPACE, ERR_STATE, ERR_DEVICE, ERR_NOMEM = 0, -1, -2, -3, -4, -5, -6, -7
 FP32, BF16 = 0, 1
