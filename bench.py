@@ -57,11 +57,11 @@ def edge_bwd_split_roofline(prec, D, N, E, m, avg_ms):
     """Position of the edge backward at latent width D (one launch per MP
     block) against both roofs: algorithmic bytes and executed MFMA flop per
     launch, each divided by the average launch time.
-    fp32 (feature-split kernel): per edge e, the incoming edge gradient (not
-    in the last block), the outgoing one and z-bar (fp32), sender / receiver
-    ids; per node P, the gathered aggregate gradient and R; 5 products of
-    D x D per edge (the recomputed W1e e and W2 a1, W2^T dz2, W1e^T zbar and
-    the dW2 accumulation).
+    fp32 (row-layout kernel at width 160): per edge e, the incoming edge
+    gradient (not in the last block), the outgoing one and z-bar (fp32),
+    sender / receiver ids; per node P, the gathered aggregate gradient and
+    R; 5 products of D x D per edge (the recomputed W1e e and W2 a1, W2^T
+    dz2, W1e^T zbar and the dW2 accumulation; dW1e is a separate pass).
     bf16 (row-per-wave kernel): per edge the saved a1, the incoming edge
     gradient (not in the last block), the outgoing one, zbar and dz2 (bf16),
     the receiver id; per node the gathered aggregate gradient and R (fp32);

@@ -690,8 +690,11 @@ struct Run {
         if ((rc = job(nb, 2, 16512, 1, D * D + D, grad, oe.W2, 0)) != MGN_OK) return rc;
         if ((rc = job(nb, 2, 33024, 1, 2 * D, grad, oe.g, 0)) != MGN_OK) return rc;
       } else {
-        LAUNCH(K_EDGE_BWD, launch_edge_bwd(prec, D, tl, e_l(k, l), (float*)ebar, l < m - 1 ? 1 : 0, (float*)ebar, P_l(k, l), aggbar,
-                                W(oe, M.p_edge[l]), eps, zbar, R, slots(), P2, &nb, s));
+        // fp32, width 160: one wave per row block (dW2 and the vectors in the
+        // pass), then dW1e = sum zbar^T e over the two streams
+        LAUNCH(K_EDGE_BWD, launch_edge_bwd_r32(D, tl, e_l(k, l), (float*)ebar, l < m - 1 ? 1 : 0, (float*)ebar,
+                                               P_l(k, l), aggbar, W(oe, M.p_edge[l]), eps, zbar, R, slots(), P2, &nb,
+                                               s));
         if ((rc = job(nb, 2, (int64_t)D * D, 1, (int)(oe.size - 3 * D * D), grad, oe.b1, 0)) != MGN_OK) return rc;
         LAUNCH(K_WGRAD, launch_wgrad(prec, D, E, zbar, e_l(k, l), P3, &nb, s));
         if ((rc = job(nb, 3, 0, D, D, grad, oe.W1, 3 * D)) != MGN_OK) return rc;

@@ -19,6 +19,7 @@
 // about 30 times the weight traffic.
 #include "launch.hpp"
 #include "rows_common.hpp"
+#include "w160_common.hpp"
 
 namespace mgn {
 namespace dev {
@@ -93,8 +94,9 @@ struct __attribute__((aligned(16))) Fwd32Lds {
 // close(j, pair index, sum) stores a finished node sum.
 template <int LD, class F>
 __device__ __forceinline__ void seg_pass32(const float* stage, int lane, int segraw, int base, bool chunk, int n,
-                                           int nv, int lo_row, int& j, float2 (&carry)[2], F&& close) {
-  constexpr int NP = LD / 2, SLD = R32<LD>::SLD;
+                                           int nv, int lo_row, int& j, float2 (&carry)[2], F&& close,
+                                           int SLD = R32<LD>::SLD) {
+  constexpr int NP = LD / 2;
   const int hi_row = lo_row + 16;
   while (j < nv) {
     const int a = chunk ? 0 : __builtin_amdgcn_readlane(segraw, j) - base;
@@ -579,6 +581,321 @@ k_edge_bwd_r32(EdgeTiles tl, const float* __restrict__ e_in, const float* ebar_i
   }
 }
 
+
+// ======================================================= reverse, width 160
+// The reverse at width 160 (latent 150 padded with zero columns): as the
+// width-128 pass, but only dW2 (with db2, db1, dgamma, dbeta) accumulates
+// in the kernel; dW1e = sum zbar^T e is left to the weight-gradient pass
+// over the zbar and e streams (at this width both quarters of the two
+// 160 x 160 products would need 224 accumulator registers per wave, and
+// four staged fp32 streams 180 KB of LDS).  Buffers: X (dz2) and Y (a1) of
+// the round's 64 rows, Zs (each wave's own zbar rows, for its receiver
+// sums).  Each wave owns 25 of the 100 16 x 16 tiles of dW2 (25 wv .. + 25,
+// row-major) and the ones columns of output blocks wv, wv + 4, wv + 8.  The
+// LayerNorm runs over the 150 real features (padded features of dz2 are
+// zeroed); db1 is a DPP column sum of zbar per half.
+constexpr int C32_LD = 160;
+constexpr int C32_SLD = C32_LD + 16;  // staged row stride: lane groups 0, 1 hit distinct banks
+constexpr int C32_TILES = 25;         // dW2 tiles per wave
+
+struct __attribute__((aligned(16))) Bwd32wLds {
+  __attribute__((aligned(16))) float st[3][B32_ROWS * C32_SLD];  // X, Y, Zs
+};
+
+// column sums over a half's 16 rows of 40 C-layout values (blocks 0..7 by
+// colsum16, blocks 8, 9 by the tail butterfly), accumulated
+__device__ __forceinline__ void colsum40(const f32x4 (&v)[10], int i, float2& acc8, float& tail) {
+  f32x4 p8[8];
+#pragma unroll
+  for (int ob = 0; ob < 8; ++ob) p8[ob] = v[ob];
+  const float2 c = colsum16(p8, i);
+  acc8.x += c.x;
+  acc8.y += c.y;
+  tail += w160::colsum16_tail(v, i);
+}
+
+__global__ void __launch_bounds__(R32_NT) __attribute__((amdgpu_waves_per_eu(1, 1)))
+k_edge_bwd_r32w(EdgeTiles tl, const float* __restrict__ e_in, const float* ebar_in, int have_ebar, float* ebar_out,
+                const float* __restrict__ Pn, const float* __restrict__ aggbar, MlpW w, float eps,
+                float* __restrict__ zbar, float* __restrict__ R, float* __restrict__ slots, Partials part) {
+  constexpr int LD = C32_LD;
+  typedef R32<LD> Z;
+  __shared__ __align__(16) Bwd32wLds S;
+  float* X = S.st[0];
+  float* Y = S.st[1];
+  float* Zs = S.st[2];
+  const int tid = threadIdx.x, lane = tid & 63, i = lane & 15, g = lane >> 4;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int f0 = Z::KL * g;
+
+  const int G = gridDim.x;
+  int64_t tb, stride, tend;
+  if ((G & 7) == 0) {
+    const int x = blockIdx.x & 7, per = G >> 3;
+    const int64_t chunk = (tl.n_tiles + 7) >> 3;
+    const int64_t lo = x * chunk;
+    tend = min(tl.n_tiles, lo + chunk);
+    tb = lo + (int64_t)(blockIdx.x >> 3) * R32_NW;
+    stride = (int64_t)per * R32_NW;
+  } else {
+    tb = (int64_t)blockIdx.x * R32_NW;
+    stride = (int64_t)G * R32_NW;
+    tend = tl.n_tiles;
+  }
+  const int4* tiles = reinterpret_cast<const int4*>(tl.tiles);
+  const int64_t tlast = max(tend - 1, (int64_t)0);
+  auto desc = [&](int64_t tt) -> int4 {
+    const bool ok = tt < tend;
+    const int4 v = tiles[ok ? tt : tlast];
+    int4 r;
+    r.x = ok ? v.x : 0;
+    r.y = ok ? v.y : 0;
+    r.z = ok ? v.z : 0;
+    r.w = ok ? v.w : 0;
+    return r;
+  };
+  const int lastE = (int)max(tl.n_edges - 1, (int64_t)0);
+  auto erow = [&](int4 d, int rb) { return min(max(d.z + min(rb * 16 + i, tile_rows(d) - 1), 0), lastE); };
+  struct Half {
+    float e[Z::KL];
+  };
+  auto load_half = [&](int4 d, int rb, Half& H) { load_row32<LD>(H.e, e_in + (size_t)erow(d, rb) * LD + f0); };
+
+  f32x4 aw2[C32_TILES], ab2[3];
+#pragma unroll
+  for (int t = 0; t < C32_TILES; ++t) aw2[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int t = 0; t < 3; ++t) ab2[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+  // column sums: dgamma, dbeta, db1 (blocks 0..7 pairwise, blocks 8, 9 tail)
+  float2 dga = {0.f, 0.f}, dbe = {0.f, 0.f}, db1 = {0.f, 0.f};
+  float tga = 0.f, tbe = 0.f, tb1 = 0.f;
+  const int srow = 16 * wv + i;
+  auto stage_row = [&](float* B, const float (&v)[Z::KL], bool live) {
+    float* p = B + srow * C32_SLD + f0;
+#pragma unroll
+    for (int c = 0; c < Z::KC; ++c)
+      *reinterpret_cast<f32x4*>(p + 4 * c) =
+          live ? f32x4{v[4 * c], v[4 * c + 1], v[4 * c + 2], v[4 * c + 3]} : f32x4{0.f, 0.f, 0.f, 0.f};
+  };
+
+  auto round = [&](Half& H, int4 d0, int rb, int segraw, bool chunk, int nv, int& j, float2 (&carry)[2]) {
+    const int n = tile_rows(d0);
+    const int row = rb * 16 + i;
+    const bool live = row < n;
+    const size_t grow = (size_t)erow(d0, rb);
+    const int snd = tl.senders[grow], rcv = tl.receivers[grow];
+    const int oz = opaque_zero();
+    // ---- z1 = W1e e + (b1 + P_s + P_r), a1 = relu(z1)
+    f32x4 acc[Z::NOB];
+#pragma unroll
+    for (int ob = 0; ob < Z::NOB; ++ob) acc[ob] = f32x4{0.f, 0.f, 0.f, 0.f};
+    gemm32<LD>(acc, H.e, w.F1 + oz, lane);
+    float a1[Z::KL];
+    uint64_t mask = 0;
+    {
+      const float* ps = Pn + (size_t)snd * (2 * LD) + f0;
+      const float* pr = Pn + (size_t)rcv * (2 * LD) + LD + f0;
+#pragma unroll
+      for (int ob = 0; ob < Z::NOB; ++ob) {
+        const f32x4 b1 = *reinterpret_cast<const f32x4*>(w.b1 + f0 + 4 * ob);
+        const f32x4 pa = *reinterpret_cast<const f32x4*>(ps + 4 * ob);
+        const f32x4 pb = *reinterpret_cast<const f32x4*>(pr + 4 * ob);
+        const f32x4 z = acc[ob] + ((b1 + pa) + pb);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          a1[4 * ob + r] = relu(z[r]);
+          if (z[r] > 0.f) mask |= 1ull << (4 * ob + r);
+        }
+      }
+    }
+    __syncthreads();  // the previous round's products are done
+    stage_row(Y, a1, live);
+    // ---- z2 = b2 + W2 a1; LayerNorm statistics over the 150 real features
+#pragma unroll
+    for (int ob = 0; ob < Z::NOB; ++ob) acc[ob] = *reinterpret_cast<const f32x4*>(w.b2 + f0 + 4 * ob);
+    gemm32<LD>(acc, a1, w.F2 + oz, lane);
+    // the incoming gradients of the half
+    float eb[Z::KL];
+    load_row32<LD>(eb, ebar_in + grow * LD + f0);
+    if (!have_ebar)
+#pragma unroll
+      for (int s = 0; s < Z::KL; ++s) eb[s] = 0.f;
+    f32x4 t[Z::NOB];  // mbar, then dxh, then dz2
+    {
+      const float* gp = aggbar + (size_t)rcv * LD + f0;
+#pragma unroll
+      for (int ob = 0; ob < Z::NOB; ++ob) {
+        const f32x4 ag = *reinterpret_cast<const f32x4*>(gp + 4 * ob);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) t[ob][r] = eb[4 * ob + r] + ag[r];
+      }
+    }
+    float sm = 0.f;
+#pragma unroll
+    for (int ob = 0; ob < Z::NOB; ++ob)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) sm += acc[ob][r];
+    const float mean = sum_q(sm) * (1.0f / Z::DR);
+    float sq = 0.f;
+#pragma unroll
+    for (int ob = 0; ob < Z::NOB; ++ob)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        acc[ob][r] -= mean;
+        if (f0 + 4 * ob + r < Z::DR) sq += acc[ob][r] * acc[ob][r];
+      }
+    const float rstd = __builtin_amdgcn_rsqf(sum_q(sq) * (1.0f / Z::DR) + eps);
+#pragma unroll
+    for (int ob = 0; ob < Z::NOB; ++ob) acc[ob] *= rstd;  // xhat
+    // ---- dbeta, dgamma (live rows); LayerNorm reverse (padded features:
+    // dxh = 0 from gamma = 0, dz2 zeroed)
+    {
+      f32x4 p[Z::NOB];
+#pragma unroll
+      for (int ob = 0; ob < Z::NOB; ++ob) p[ob] = live ? t[ob] : f32x4{0.f, 0.f, 0.f, 0.f};
+      colsum40(p, i, dbe, tbe);
+#pragma unroll
+      for (int ob = 0; ob < Z::NOB; ++ob) p[ob] = live ? t[ob] * acc[ob] : f32x4{0.f, 0.f, 0.f, 0.f};
+      colsum40(p, i, dga, tga);
+    }
+    float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+    for (int ob = 0; ob < Z::NOB; ++ob) {
+      t[ob] *= *reinterpret_cast<const f32x4*>(w.gamma + f0 + 4 * ob);  // dxh
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        s1 += t[ob][r];
+        s2 += t[ob][r] * acc[ob][r];
+      }
+    }
+    const float m1 = sum_q(s1) * (1.0f / Z::DR), m2 = sum_q(s2) * (1.0f / Z::DR);
+    float dz[Z::KL];
+#pragma unroll
+    for (int ob = 0; ob < Z::NOB; ++ob)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        dz[4 * ob + r] = f0 + 4 * ob + r < Z::DR ? rstd * (t[ob][r] - m1 - acc[ob][r] * m2) : 0.f;
+    stage_row(X, dz, live);
+    // ---- da1 = W2^T dz2, zbar = da1 where z1 > 0 (db1: its column sums)
+#pragma unroll
+    for (int ob = 0; ob < Z::NOB; ++ob) acc[ob] = f32x4{0.f, 0.f, 0.f, 0.f};
+    gemm32<LD>(acc, dz, w.F2t + oz, lane);
+    float zb[Z::KL];
+    {
+      f32x4 pz[Z::NOB];
+#pragma unroll
+      for (int ob = 0; ob < Z::NOB; ++ob)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float z = (mask >> (4 * ob + r)) & 1ull ? acc[ob][r] : 0.f;
+          zb[4 * ob + r] = z;
+          pz[ob][r] = live ? z : 0.f;
+        }
+      colsum40(pz, i, db1, tb1);
+    }
+    stage_row(Zs, zb, live);
+    if (live) {
+      float* zp = zbar + ((size_t)d0.z + row) * LD + f0;
+#pragma unroll
+      for (int c = 0; c < Z::KC; ++c)
+        *reinterpret_cast<f32x4*>(zp + 4 * c) = f32x4{zb[4 * c], zb[4 * c + 1], zb[4 * c + 2], zb[4 * c + 3]};
+    }
+    // ---- ebar_out = ebar_in + W1e^T zbar
+#pragma unroll
+    for (int ob = 0; ob < Z::NOB; ++ob)
+      acc[ob] = f32x4{eb[4 * ob], eb[4 * ob + 1], eb[4 * ob + 2], eb[4 * ob + 3]};
+    gemm32<LD>(acc, zb, w.F1t + oz, lane);
+    if (live) store_row32<LD>(ebar_out + ((size_t)d0.z + row) * LD + f0, acc);
+    __syncthreads();  // X = dz2, Y = a1, Zs = zbar staged
+    // ---- receiver sums of this wave's zbar rows
+    seg_pass32<LD>(Zs + 16 * wv * C32_SLD, lane, segraw, d0.z, chunk, n, nv, rb * 16, j, carry,
+                   [&](int jj, float2 (&v)[2]) {
+                     float* dst = !chunk ? R + (size_t)(d0.x + jj) * LD : slots + (size_t)(-1 - d0.y) * LD;
+                     *reinterpret_cast<float2*>(dst + 2 * lane) = v[0];
+                     if (lane + 64 < LD / 2) *reinterpret_cast<float2*>(dst + 2 * (lane + 64)) = v[1];
+                   },
+                   C32_SLD);
+    // ---- the round's 64 rows into this wave's tiles of dW2 = dz2^T a1
+#pragma unroll 2
+    for (int kk = 0; kk < B32_ROWS / 4; ++kk) {
+      const int r0 = (4 * kk + g) * C32_SLD;
+#pragma unroll
+      for (int t3 = 0; t3 < 3; ++t3) {
+        const int ob = wv + 4 * t3;
+        if (ob < Z::NOB) ab2[t3] = __builtin_amdgcn_mfma_f32_16x16x4f32(X[r0 + 16 * ob + i], 1.0f, ab2[t3], 0, 0, 0);
+      }
+#pragma unroll
+      for (int tt = 0; tt < C32_TILES; ++tt) {
+        const int T = C32_TILES * wv + tt, ob = T / Z::NOB, nb = T % Z::NOB;
+        aw2[tt] = __builtin_amdgcn_mfma_f32_16x16x4f32(X[r0 + 16 * ob + i], Y[r0 + 16 * nb + i], aw2[tt], 0, 0, 0);
+      }
+    }
+  };
+
+  if (tb < tend) {
+    int4 d0 = desc(tb + wv), d1 = desc(tb + wv + stride);
+    Half A, B;
+    load_half(d0, 0, A);
+    for (; tb < tend; tb += stride) {
+      const bool chunk = d0.y < 0;
+      const int nv = chunk ? 1 : d0.y - d0.x;
+      const int segraw = tl.rowptr[min(d0.x + lane, max(d0.x, d0.y))];
+      const int4 d2 = desc(tb + wv + 2 * stride);
+      load_half(d0, 1, B);
+      float2 carry[2] = {{0.f, 0.f}, {0.f, 0.f}};
+      int j = 0;
+      round(A, d0, 0, segraw, chunk, nv, j, carry);
+      load_half(d1, 0, A);
+      round(B, d0, 1, segraw, chunk, nv, j, carry);
+      d0 = d1;
+      d1 = d2;
+    }
+  }
+  // ---- block partials in the layout of the edge MLP's parameters after W1
+  // (offset LD^2): db1, dW2, db2, dgamma, dbeta
+  float* base = part.buf + (size_t)blockIdx.x * part.stride;
+  constexpr int ob1 = LD * LD, oW2 = LD * LD + LD, ob2 = 2 * LD * LD + LD, og = 2 * LD * LD + 2 * LD;
+#pragma unroll
+  for (int t = 0; t < C32_TILES; ++t) {
+    const int T = C32_TILES * wv + t, ob = T / Z::NOB, nb = T % Z::NOB;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) base[oW2 + (size_t)(16 * ob + 4 * g + r) * LD + 16 * nb + i] = aw2[t][r];
+  }
+  if (i == 0)
+#pragma unroll
+    for (int t = 0; t < 3; ++t) {
+      const int ob = wv + 4 * t;
+      if (ob < Z::NOB)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) base[ob2 + 16 * ob + 4 * g + r] = ab2[t][r];
+    }
+  __syncthreads();
+  float* red = S.st[0];  // [3][R32_NW][LD]: dgamma, dbeta, db1
+  {
+    // colsum16: lane i holds features f0 + 4 (i / 2) + 2 (i % 2) + {0, 1};
+    // colsum16_tail: lanes i, i ^ 1 hold value k of blocks 8, 9
+    const int f = f0 + 4 * (i >> 1) + 2 * (i & 1);
+    *reinterpret_cast<float2*>(red + (0 * R32_NW + wv) * LD + f) = dga;
+    *reinterpret_cast<float2*>(red + (1 * R32_NW + wv) * LD + f) = dbe;
+    *reinterpret_cast<float2*>(red + (2 * R32_NW + wv) * LD + f) = db1;
+    if ((i & 1) == 0) {
+      const int k = (((i >> 3) & 1) << 2) | (((i >> 2) & 1) << 1) | ((i >> 1) & 1);
+      const int ft = f0 + 4 * (8 + (k >> 2)) + (k & 3);
+      red[(0 * R32_NW + wv) * LD + ft] = tga;
+      red[(1 * R32_NW + wv) * LD + ft] = tbe;
+      red[(2 * R32_NW + wv) * LD + ft] = tb1;
+    }
+  }
+  __syncthreads();
+  for (int idx = tid; idx < 3 * LD; idx += R32_NT) {
+    const int k2 = idx / LD, c = idx % LD;
+    float v = 0.f;
+#pragma unroll
+    for (int u = 0; u < R32_NW; ++u) v += red[(k2 * R32_NW + u) * LD + c];
+    base[k2 == 2 ? ob1 + c : og + k2 * LD + c] = v;
+  }
+}
+
 }  // namespace dev
 
 using namespace dev;
@@ -606,14 +923,19 @@ hipError_t launch_edge_bwd_r32(int lat, const EdgeTiles& t, const void* e, const
                                hipStream_t s) {
   *nblocks = 0;
   if (t.n_tiles <= 0) return hipSuccess;
-  if (lat != B32_LD || t.n_edges <= 0 || part.stride < 33280 || !w.F1 || !w.F2 || !w.F1t || !w.F2t)
+  if ((lat != B32_LD && lat != C32_LD) || t.n_edges <= 0 || part.stride < 2LL * lat * lat + 4 * lat || !w.F1 ||
+      !w.F2 || !w.F1t || !w.F2t)
     return hipErrorInvalidValue;
   const int64_t need = (t.n_tiles + R32_NW - 1) / R32_NW;
   int g = (int)std::min<int64_t>(need, std::min(kRows32Blocks, part.max_blocks));
   if (g >= 8) g &= ~7;
   *nblocks = g;
-  hipLaunchKernelGGL(k_edge_bwd_r32, dim3(g), dim3(R32_NT), 0, s, t, (const float*)e, ebar_in, have_ebar, ebar_out,
-                     (const float*)Pn, aggbar, w, eps, (float*)zbar, R, slots, part);
+  if (lat == C32_LD)
+    hipLaunchKernelGGL(k_edge_bwd_r32w, dim3(g), dim3(R32_NT), 0, s, t, (const float*)e, ebar_in, have_ebar,
+                       ebar_out, (const float*)Pn, aggbar, w, eps, (float*)zbar, R, slots, part);
+  else
+    hipLaunchKernelGGL(k_edge_bwd_r32, dim3(g), dim3(R32_NT), 0, s, t, (const float*)e, ebar_in, have_ebar,
+                       ebar_out, (const float*)Pn, aggbar, w, eps, (float*)zbar, R, slots, part);
   return hipGetLastError();
 }
 
