@@ -15,8 +15,10 @@ BF16_TOL = 2e-2   # relative L2, bf16-MLP outputs; also bf16 gradients at a
 # and every activation operand once per GEMM (relative 2^-9 each); the bound
 # per MLP segment is twice the largest change of the oracle's own gradient
 # under random relative 2^-8 sign perturbations of all weights (see
-# bf16_grad_tols), never below BF16_GRAD_TOL.
-BF16_GRAD_TOL = 0.15
+# bf16_grad_tols).  Measured errors are 0.28-0.54 of that bound on every
+# segment of the small-mesh cases and about 0.3 on the 32^3 mesh; the floor
+# is only the output contract, for segments whose gradient is zero.
+BF16_GRAD_TOL = BF16_TOL
 KINK_TAU = 3e-6   # |ReLU input| below which fp32 and fp64 may take different branches
 
 
