@@ -10,7 +10,9 @@
 //
 // Adds of bf16 inputs into fp32 accumulators (the node products P_s + P_r
 // and the residual e + m) are MFMAs with a 0/1 selection operand: one
-// product per output, so each is a single fp32 rounding, as a VALU add.
+// product per output and one rounding, though not always to nearest (on
+// random operands about 4% of these sums come out one ulp below the
+// round-to-nearest VALU add, as if the aligned addend were truncated).
 //
 // Node sums: the wave stages each 16-row half of the messages in its own
 // LDS area and sums every in-segment in ascending row order from 0.0, so a
@@ -265,22 +267,23 @@ k_edge_fwd_rows(EdgeTiles tl, const bf16* __restrict__ e_in, bf16* __restrict__ 
 // ebar_out = ebar_in + W1e^T zbar, and accumulates dW2 = sum dz2^T a1,
 // dW1e = sum zbar^T e, db2 = sum dz2, db1 = sum zbar, dgamma, dbeta.
 //
-// Work split: eight waves per block, two per SIMD, in two roles.  Row waves
-// 0..3 run the reverse of one 16-row half per round (the layout and
-// products of the forward kernel's layout) and stage its rows of dz2, zbar and a1 in
-// LDS (row-major, zeros past the tile's end); gradient waves 4..7 load the
-// matching rows of e into the staging and, while the row waves compute the
-// next round, add the staged 64 rows into the weight gradients: wave 4 + k
-// owns the rows [64 (k % 2), + 64) of dW2 (k < 2: A = dz2^T, B = a1) or of
-// dW1e (A = zbar^T, B = e), with the row index as the MFMA's K dimension
-// (transposing LDS reads) and the column sums db2 / db1 through a ones
-// operand.  So each SIMD runs one row wave and one gradient wave, the
-// accumulators never share a wave with the row work, and two block
-// barriers per round order the staging: after the first the staging is
-// free (the gradient waves have read the previous round, the row waves
-// their own receiver sums), after the second it is full.  dgamma and dbeta
-// are DPP column sums of each half, accumulated per lane of the row waves.
-// Every sum runs in a fixed order, so results are reproducible.
+// Work split: eight waves per block, two per SIMD, in two roles.  Row
+// waves 0..3 run the reverse of one 16-row half per round (the layout and
+// products of the forward kernel) and stage its rows of dz2, zbar and a1
+// in LDS (row-major; dz2 and zbar are zero past the tile's end); gradient
+// waves 4..7 load the matching rows of e into the staging and, while the
+// row waves compute the next round, form the receiver sums of the staged
+// zbar rows and add the staged 64 rows into the weight gradients: wave
+// 4 + k owns the rows [64 (k % 2), + 64) of dW2 (k < 2: A = dz2^T, B = a1)
+// or of dW1e (A = zbar^T, B = e), with the row index as the MFMA's K
+// dimension (transposing LDS reads) and the column sums db2 / db1 through a
+// ones operand.  So each SIMD runs one row wave and one gradient wave, the
+// accumulators never share a wave with the row work, and the row waves
+// carry only the work that needs their registers.  Two block barriers per
+// round order the staging: after the first it is free (the gradient waves
+// have read the previous round), after the second it is full.  dgamma and
+// dbeta are DPP column sums of each half, accumulated per lane of the row
+// waves.  Every sum runs in a fixed order, so results are reproducible.
 constexpr int FB_RW = 4;             // row waves per block (= gradient waves)
 constexpr int FB_NT = 128 * FB_RW;   // threads per block
 constexpr int FB_ROWS = 16 * FB_RW;  // rows staged per round
@@ -302,10 +305,22 @@ __device__ __forceinline__ bf16x8 staged_frag(const bf16* X, int r0, int col0, i
   return cat8(lds_tr(p), lds_tr(p + 4 * FB_LD));
 }
 
+// A pair of bf16 values w with each half cleared unless the matching half of
+// a (bf16 bits) is a positive number: the ReLU mask a > 0 on the bit
+// patterns as signed 16-bit integers (+0 and negative values have no
+// positive pattern), in three packed integer operations.
+__device__ __forceinline__ uint32_t relu_mask_pair(uint32_t w, uint32_t a) {
+  typedef short s16x2 __attribute__((ext_vector_type(2)));
+  const s16x2 zero = {0, 0}, one = {1, 1};
+  const s16x2 pos = __builtin_elementwise_min(__builtin_elementwise_max(__builtin_bit_cast(s16x2, a), zero), one);
+  return w & __builtin_bit_cast(uint32_t, zero - pos);
+}
+
+template <bool HAVE_EBAR>
 __global__ void __launch_bounds__(FB_NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
 k_edge_bwd_fused(EdgeTiles tl, const bf16* __restrict__ a1_in, const bf16* __restrict__ e_in, const bf16* ebar_in,
-                 int have_ebar, bf16* ebar_out, const float* __restrict__ aggbar, MlpW w, float eps,
-                 bf16* __restrict__ zbar, float* __restrict__ R, float* __restrict__ slots, Partials part) {
+                 bf16* ebar_out, const float* __restrict__ aggbar, MlpW w, float eps, bf16* __restrict__ zbar,
+                 float* __restrict__ R, float* __restrict__ slots, Partials part) {
   __shared__ __align__(16) FusedLds S;
   const int tid = threadIdx.x, lane = tid & 63, i = lane & 15, q = lane >> 4;
   const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -320,9 +335,9 @@ k_edge_bwd_fused(EdgeTiles tl, const bf16* __restrict__ a1_in, const bf16* __res
   __syncthreads();
 
   // The block's tiles: XCD-contiguous ranges (see unit_range); row wave k
-  // (and gradient wave 4 + k for the e rows) takes tile tb + k of every
-  // round pair; all waves run the same number of rounds (a row wave past
-  // the range runs empty tiles).
+  // (and gradient wave 4 + k for the e rows and the receiver sums) takes
+  // tile tb + k of every round pair; all waves run the same number of
+  // rounds (a row wave past the range runs empty tiles).
   const int G = gridDim.x;
   int64_t tb, stride, tend;
   if ((G & 7) == 0) {
@@ -398,6 +413,34 @@ k_edge_bwd_fused(EdgeTiles tl, const bf16* __restrict__ a1_in, const bf16* __res
         }
       }
     };
+    // Per-receiver sums of zbar (as stored) over the staged rows of row
+    // wave k's half rb of tile d, each in ascending row order from 0.0 and
+    // carried into the next half while its segment is open: nodes d.x + j
+    // of a tile of whole segments (rp(j) in lane j of segraw), or the single
+    // segment of a chunk tile, summed into its slot.
+    auto recv_sums = [&](int4 d, int rb, int segraw, bool chunk, int nv, int& j, float2& carry) {
+      const bf16* zs = S.st[1] + 16 * k * FB_LD;
+      uint32_t zr[16];  // the 16 rows' values of this lane's two features, read at once
+#pragma unroll
+      for (int r = 0; r < 16; ++r) zr[r] = *reinterpret_cast<const uint32_t*>(zs + r * FB_LD + 2 * lane);
+      const int n = tile_rows(d);
+      const int lo_row = rb * 16, hi_row = lo_row + 16;
+      while (j < nv) {
+        const int a = chunk ? 0 : __builtin_amdgcn_readlane(segraw, j) - d.z;
+        const int b = chunk ? n : __builtin_amdgcn_readlane(segraw, j + 1) - d.z;
+        const int u0 = max(a, lo_row), u1 = min(b, hi_row);
+        for (int u = u0; u < u1; ++u) {
+          const uint32_t v = zr[u - lo_row];
+          carry.x += __uint_as_float(v << 16);
+          carry.y += __uint_as_float(v & 0xffff0000u);
+        }
+        if (b > hi_row) break;
+        float* dst = !chunk ? R + (size_t)(d.x + j) * D : slots + (size_t)(-1 - d.y) * D;
+        *reinterpret_cast<float2*>(dst + 2 * lane) = carry;
+        carry = float2{0.f, 0.f};
+        ++j;
+      }
+    };
     auto load_e = [&](int4 d, int rb, uint4 (&v)[4]) {
       const bf16* xp = e_in + (size_t)erow(d, rb) * D + 8 * q;
 #pragma unroll
@@ -407,24 +450,29 @@ k_edge_bwd_fused(EdgeTiles tl, const bf16* __restrict__ a1_in, const bf16* __res
       int4 d0 = desc(tb + k), d1 = desc(tb + k + stride);
       uint4 ev[4];
       load_e(d0, 0, ev);
-      bool first = true;
       for (; tb < tend; tb += stride) {
+        const bool chunk = d0.y < 0;
+        const int nv = chunk ? 1 : d0.y - d0.x;
+        // in-segment starts of the tile's nodes (lane j: rowptr of node j)
+        const int segraw = tl.rowptr[min(d0.x + lane, max(d0.x, d0.y))];
+        float2 carry = {0.f, 0.f};
+        int j = 0;  // next node whose sum is open
 #pragma unroll
         for (int rb = 0; rb < 2; ++rb) {
-          if (!first) products();  // the previous round's rows
-          first = false;
           __syncthreads();  // staging free
           stage_runs(S.st[3], ev, rb * 16 + i < tile_rows(d0));
+          __syncthreads();  // staging full
+          recv_sums(d0, rb, segraw, chunk, nv, j, carry);
+          products();
+          // the next round's e rows, in flight while the row waves finish it
           if (rb == 0)
             load_e(d0, 1, ev);
           else
             load_e(d1, 0, ev);
-          __syncthreads();  // staging full
         }
         d0 = d1;
         d1 = desc(tb + k + 2 * stride);
       }
-      products();  // the last round's rows
     }
     // weight gradients straight from the owning wave; db1 / db2 from the
     // ones column
@@ -460,14 +508,10 @@ k_edge_bwd_fused(EdgeTiles tl, const bf16* __restrict__ a1_in, const bf16* __res
     const bf16* ap = a1_in + row * D + 8 * q;
 #pragma unroll
     for (int s = 0; s < 4; ++s) H.a[s] = *reinterpret_cast<const uint4*>(ap + 32 * s);
-    const bf16* ep = ebar_in + row * D + 8 * q;
+    if (HAVE_EBAR) {
+      const bf16* ep = ebar_in + row * D + 8 * q;
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      const uint4 v = *reinterpret_cast<const uint4*>(ep + 32 * s);
-      H.eb[s].x = have_ebar ? v.x : 0u;
-      H.eb[s].y = have_ebar ? v.y : 0u;
-      H.eb[s].z = have_ebar ? v.z : 0u;
-      H.eb[s].w = have_ebar ? v.w : 0u;
+      for (int s = 0; s < 4; ++s) H.eb[s] = *reinterpret_cast<const uint4*>(ep + 32 * s);
     }
   };
   auto load_ag = [&](int recv, f32x4 (&ag)[8]) {
@@ -475,12 +519,11 @@ k_edge_bwd_fused(EdgeTiles tl, const bf16* __restrict__ a1_in, const bf16* __res
 #pragma unroll
     for (int ob = 0; ob < 8; ++ob) ag[ob] = *reinterpret_cast<const f32x4*>(gp + fo(ob, q));
   };
+  const bf16x8 sel0 = select_frag(0, i, q), sel1 = select_frag(1, i, q);
   float2 dga = {0.f, 0.f}, dbe = {0.f, 0.f};
 
-  // One round: the reverse of half rb of tile d0 (streams in H), its rows
-  // staged, then the receiver sums of its zbar rows.
-  auto round = [&](HalfLoads& H, f32x4 (&ag)[8], int next_recv, int4 d0, int rb, int segraw, bool chunk, int nv,
-                   int& j, float2& carry) {
+  // One round: the reverse of half rb of tile d0 (streams in H), its rows staged.
+  auto round = [&](HalfLoads& H, f32x4 (&ag)[8], int next_recv, int4 d0, int rb) {
     const int n = tile_rows(d0);
     const int row = rb * 16 + i;
     const bool live = row < n;
@@ -509,22 +552,25 @@ k_edge_bwd_fused(EdgeTiles tl, const bf16* __restrict__ a1_in, const bf16* __res
       for (int r = 0; r < 4; ++r) sq += acc[ob][r] * acc[ob][r];
     }
     const float rstd = __builtin_amdgcn_rsqf(sum_rowlanes(sq) * (1.0f / D) + eps);
+    // mbar = aggbar[receiver] + ebar_in, zero on rows past the tile's end
 #pragma unroll
     for (int ob = 0; ob < 8; ++ob) {
-      acc[ob] *= rstd;                // xhat
-      ag[ob] += run_block(H.eb, ob);  // mbar = ebar_in + aggbar[receiver]
+      acc[ob] *= rstd;  // xhat
+      if (HAVE_EBAR) ag[ob] += run_block(H.eb, ob);
     }
-    // ---- dgamma += sum_rows mbar * xhat, dbeta += sum_rows mbar (live rows)
+    if (n < rb * 16 + 16) {  // a partial half (uniform)
+#pragma unroll
+      for (int ob = 0; ob < 8; ++ob) ag[ob] = live ? ag[ob] : f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+    // ---- dgamma += sum_rows mbar * xhat, dbeta += sum_rows mbar
     {
       f32x4 p[8];
 #pragma unroll
-      for (int ob = 0; ob < 8; ++ob) p[ob] = live ? ag[ob] * acc[ob] : f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int ob = 0; ob < 8; ++ob) p[ob] = ag[ob] * acc[ob];
       const float2 c = colsum16(p, i);
       dga.x += c.x;
       dga.y += c.y;
-#pragma unroll
-      for (int ob = 0; ob < 8; ++ob) p[ob] = live ? ag[ob] : f32x4{0.f, 0.f, 0.f, 0.f};
-      const float2 d = colsum16(p, i);
+      const float2 d = colsum16(ag, i);
       dbe.x += d.x;
       dbe.y += d.y;
     }
@@ -552,80 +598,58 @@ k_edge_bwd_fused(EdgeTiles tl, const bf16* __restrict__ a1_in, const bf16* __res
     load_ag(next_recv, ag);
     // ---- da1 = W2^T dz2, zbar = da1 where a1 > 0
 #pragma unroll
-    for (int ob = 0; ob < 8; ++ob) acc[ob] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
     for (int s = 0; s < 4; ++s)
 #pragma unroll
       for (int ob = 0; ob < 8; ++ob)
-        acc[ob] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wt_frag(S.W2, ob, s, i, q), dzf[s], acc[ob], 0, 0, 0);
-    bf16x8 zf[4];
+        acc[ob] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wt_frag(S.W2, ob, s, i, q), dzf[s],
+                                                          s == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : acc[ob], 0, 0, 0);
+    uint4 zw[4];
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
-      const bf16x8 a = as_frag(H.a[s]);
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        zf[s][r] = (float)a[r] > 0.f ? (bf16)acc[2 * s][r] : (bf16)0.f;
-        zf[s][4 + r] = (float)a[4 + r] > 0.f ? (bf16)acc[2 * s + 1][r] : (bf16)0.f;
-      }
+      const uint4 z = __builtin_bit_cast(uint4, pack_run(acc[2 * s], acc[2 * s + 1]));
+      zw[s].x = relu_mask_pair(z.x, H.a[s].x);
+      zw[s].y = relu_mask_pair(z.y, H.a[s].y);
+      zw[s].z = relu_mask_pair(z.z, H.a[s].z);
+      zw[s].w = relu_mask_pair(z.w, H.a[s].w);
     }
     if (live) {
       bf16* zp = zbar + ((size_t)d0.z + row) * D + 8 * q;
 #pragma unroll
-      for (int s = 0; s < 4; ++s) *reinterpret_cast<uint4*>(zp + 32 * s) = __builtin_bit_cast(uint4, zf[s]);
+      for (int s = 0; s < 4; ++s) *reinterpret_cast<uint4*>(zp + 32 * s) = zw[s];
     }
-    // ---- ebar_out = ebar_in + W1e^T zbar
+    // ---- ebar_out = ebar_in + W1e^T zbar (ebar_in entered exactly by a
+    // selection MFMA, then the products in the same order)
 #pragma unroll
-    for (int ob = 0; ob < 8; ++ob) acc[ob] = run_block(H.eb, ob);
+    for (int ob = 0; ob < 8; ++ob)
+      acc[ob] = HAVE_EBAR ? __builtin_amdgcn_mfma_f32_16x16x32_bf16((ob & 1) ? sel1 : sel0, as_frag(H.eb[ob >> 1]),
+                                                                    f32x4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0)
+                          : f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int s = 0; s < 4; ++s)
 #pragma unroll
       for (int ob = 0; ob < 8; ++ob)
-        acc[ob] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wt_frag(S.W1, ob, s, i, q), zf[s], acc[ob], 0, 0, 0);
+        acc[ob] =
+            __builtin_amdgcn_mfma_f32_16x16x32_bf16(wt_frag(S.W1, ob, s, i, q), as_frag(zw[s]), acc[ob], 0, 0, 0);
     if (live) {
       bf16* op = ebar_out + ((size_t)d0.z + row) * D + 8 * q;
 #pragma unroll
       for (int s = 0; s < 4; ++s)
         *reinterpret_cast<uint4*>(op + 32 * s) = __builtin_bit_cast(uint4, pack_run(acc[2 * s], acc[2 * s + 1]));
     }
-    // ---- stage the round's rows of dz2, zbar, a1 (zeros past the tile)
+    // ---- stage the round's rows of dz2, zbar, a1.  Past the tile's end
+    // mbar is zero, so dz2 and zbar are zero there too (a row's LayerNorm
+    // statistics are its own) and those rows add nothing to the weight
+    // gradients; their a1 is a copy of a valid row, finite.
     __syncthreads();  // staging free
     {
       uint4 v[4];
 #pragma unroll
       for (int s = 0; s < 4; ++s) v[s] = __builtin_bit_cast(uint4, dzf[s]);
-      stage_runs(S.st[0], v, live);
-#pragma unroll
-      for (int s = 0; s < 4; ++s) v[s] = __builtin_bit_cast(uint4, zf[s]);
-      stage_runs(S.st[1], v, live);
-      stage_runs(S.st[2], H.a, live);
+      stage_runs(S.st[0], v, true);
+      stage_runs(S.st[1], zw, true);
+      stage_runs(S.st[2], H.a, true);
     }
     __syncthreads();  // staging full
-    // ---- per-receiver sums of zbar (as stored) over this wave's staged
-    // rows, each in ascending row order from 0.0 (carried into the next
-    // half while its segment is open)
-    {
-      // the 16 rows' values of this lane's two features, read at once
-      const bf16* zs = S.st[1] + 16 * k * FB_LD;
-      uint32_t zr[16];
-#pragma unroll
-      for (int r = 0; r < 16; ++r) zr[r] = *reinterpret_cast<const uint32_t*>(zs + r * FB_LD + 2 * lane);
-      const int lo_row = rb * 16, hi_row = lo_row + 16;
-      while (j < nv) {
-        const int a = chunk ? 0 : __builtin_amdgcn_readlane(segraw, j) - d0.z;
-        const int b = chunk ? n : __builtin_amdgcn_readlane(segraw, j + 1) - d0.z;
-        const int u0 = max(a, lo_row), u1 = min(b, hi_row);
-        for (int u = u0; u < u1; ++u) {
-          const uint32_t v = zr[u - lo_row];
-          carry.x += __uint_as_float(v << 16);
-          carry.y += __uint_as_float(v & 0xffff0000u);
-        }
-        if (b > hi_row) break;
-        float* dst = !chunk ? R + (size_t)(d0.x + j) * D : slots + (size_t)(-1 - d0.y) * D;
-        *reinterpret_cast<float2*>(dst + 2 * lane) = carry;
-        carry = float2{0.f, 0.f};
-        ++j;
-      }
-    }
   };
 
   if (tb < tend) {
@@ -639,16 +663,11 @@ k_edge_bwd_fused(EdgeTiles tl, const bf16* __restrict__ a1_in, const bf16* __res
     load_ag(rc0[0], ag);
     for (; tb < tend; tb += stride) {
       // issue order = use order, so each wait covers only older requests
-      const bool chunk = d0.y < 0;
-      const int nv = chunk ? 1 : d0.y - d0.x;
-      const int segraw = tl.rowptr[min(d0.x + lane, max(d0.x, d0.y))];
       const int4 d2 = desc(tb + k + 2 * stride);
       load_half(d0, 1, B);
-      float2 carry = {0.f, 0.f};
-      int j = 0;
-      round(A, ag, rc0[1], d0, 0, segraw, chunk, nv, j, carry);
+      round(A, ag, rc0[1], d0, 0);
       load_half(d1, 0, A);
-      round(B, ag, rn[0], d0, 1, segraw, chunk, nv, j, carry);
+      round(B, ag, rn[0], d0, 1);
       rc0[0] = rn[0];
       rc0[1] = rn[1];
       load_recv(d2, rn);
@@ -709,8 +728,12 @@ hipError_t launch_edge_bwd_fused(const EdgeTiles& t, const void* a1, const void*
   int g = (int)std::min<int64_t>(need, std::min(kFusedBlocks, part.max_blocks));
   if (g >= 8) g &= ~7;
   *nblocks = g;
-  hipLaunchKernelGGL(k_edge_bwd_fused, dim3(g), dim3(FB_NT), 0, s, t, (const bf16*)a1, (const bf16*)e,
-                     (const bf16*)ebar_in, have_ebar, (bf16*)ebar_out, aggbar, w, eps, (bf16*)zbar, R, slots, part);
+  if (have_ebar)
+    hipLaunchKernelGGL(k_edge_bwd_fused<true>, dim3(g), dim3(FB_NT), 0, s, t, (const bf16*)a1, (const bf16*)e,
+                       (const bf16*)ebar_in, (bf16*)ebar_out, aggbar, w, eps, (bf16*)zbar, R, slots, part);
+  else
+    hipLaunchKernelGGL(k_edge_bwd_fused<false>, dim3(g), dim3(FB_NT), 0, s, t, (const bf16*)a1, (const bf16*)e,
+                       (const bf16*)ebar_in, (bf16*)ebar_out, aggbar, w, eps, (bf16*)zbar, R, slots, part);
   return hipGetLastError();
 }
 
