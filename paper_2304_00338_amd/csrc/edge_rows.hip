@@ -585,14 +585,16 @@ k_edge_bwd_fused(EdgeTiles tl, const bf16* __restrict__ a1_in, const bf16* __res
         s2 += ag[ob][r] * acc[ob][r];
       }
     }
+    // dz2 = rstd dxh - rstd m1 - xhat (rstd m2), two fused multiply-adds per value
     const float m1 = sum_rowlanes(s1) * (1.0f / D), m2 = sum_rowlanes(s2) * (1.0f / D);
+    const float c0 = -rstd * m1, c1 = -rstd * m2;
     bf16x8 dzf[4];
 #pragma unroll
     for (int s = 0; s < 4; ++s)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        dzf[s][r] = (bf16)(rstd * (ag[2 * s][r] - m1 - acc[2 * s][r] * m2));
-        dzf[s][4 + r] = (bf16)(rstd * (ag[2 * s + 1][r] - m1 - acc[2 * s + 1][r] * m2));
+        dzf[s][r] = (bf16)__builtin_fmaf(acc[2 * s][r], c1, __builtin_fmaf(rstd, ag[2 * s][r], c0));
+        dzf[s][4 + r] = (bf16)__builtin_fmaf(acc[2 * s + 1][r], c1, __builtin_fmaf(rstd, ag[2 * s + 1][r], c0));
       }
     // the next half's receiver gradients, in flight for the rest of the round
     load_ag(next_recv, ag);
