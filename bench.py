@@ -285,13 +285,19 @@ def summarize_profile(d, kernel):
             json.dump({"trace_avg_ms": {short(n): avg / 1e3 for n, c, tot, avg, pct in rows},
                        "fetch_kib": fetch, "write_kib": write, "fetch_scale": sf, "write_scale": sw,
                        "sq": sq}, fh, indent=1)
+    # the kernel's instances (template specialisations), weighted by their
+    # launches, as the bench's per-launch time averages over all of them
     sym = KERNEL_SYMBOL.get(kernel, "k_" + kernel)
-    k = next((short(n) for n, *_ in rows if short(n) == sym), None)
-    if k is not None and k in fetch and k in write:
+    inst = [(short(n), c) for n, c, *_ in rows if short(n) == sym or short(n).startswith(sym + "<")]
+    if inst and all(k in fetch and k in write for k, _ in inst):
+        calls = sum(c for _, c in inst)
+        fk = sum(fetch[k] * c for k, c in inst) / calls
+        wk = sum(write[k] * c for k, c in inst) / calls
+        k = " + ".join(f"{k} ({c} calls)" for k, c in inst)
         out = {"kernel": kernel, "profiled_as": k, "source_digest": source_digest(kernel),
-               "fetch_kib_per_launch": fetch[k], "write_kib_per_launch": write[k],
+               "fetch_kib_per_launch": fk, "write_kib_per_launch": wk,
                "fetch_scale": sf, "write_scale": sw,
-               "bytes_per_launch": (fetch[k] * sf + write[k] * sw) * 1024}
+               "bytes_per_launch": (fk * sf + wk * sw) * 1024}
         for f in (traffic_file(kernel), os.path.join(d, os.path.basename(traffic_file(kernel)))):
             with open(f, "w") as fh:
                 json.dump(out, fh, indent=1)
