@@ -41,21 +41,35 @@ __device__ __forceinline__ f32x4 afrag32(const float* __restrict__ Wf, int ob, i
 }
 
 // acc[ob] += W x for the lane's KL values x (B operands, K step s = x[s]).
+// The output blocks run in two groups of NOB / 2 interleaved accumulator
+// chains; as soon as a group has used its fragments of K chunk c, the
+// group's fragments of chunk c + 1 are requested into the same registers,
+// so each L2 read has the other group's MFMAs to arrive behind (one wave
+// per SIMD leaves no other wave to cover it) and no registers beyond one
+// chunk's fragments are used.  Every accumulator adds its K steps in
+// ascending order.
 template <int LD>
 __device__ __forceinline__ void gemm32(f32x4 (&acc)[R32<LD>::NOB], const float (&x)[R32<LD>::KL],
                                        const float* __restrict__ Wf, int lane) {
   typedef R32<LD> Z;
+  constexpr int H = Z::NOB / 2;
+  static_assert(Z::NOB % 2 == 0, "two groups of output blocks");
+  f32x4 a[Z::NOB];
 #pragma unroll
-  for (int c = 0; c < Z::KC; ++c) {
-    f32x4 a[Z::NOB];
+  for (int ob = 0; ob < Z::NOB; ++ob) a[ob] = afrag32<LD>(Wf, ob, 0, lane);
 #pragma unroll
-    for (int ob = 0; ob < Z::NOB; ++ob) a[ob] = afrag32<LD>(Wf, ob, c, lane);
+  for (int c = 0; c < Z::KC; ++c)
 #pragma unroll
-    for (int t = 0; t < 4; ++t)
+    for (int h = 0; h < 2; ++h) {
 #pragma unroll
-      for (int ob = 0; ob < Z::NOB; ++ob)
-        acc[ob] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[ob][t], x[4 * c + t], acc[ob], 0, 0, 0);
-  }
+      for (int t = 0; t < 4; ++t)
+#pragma unroll
+        for (int o = h * H; o < h * H + H; ++o)
+          acc[o] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[o][t], x[4 * c + t], acc[o], 0, 0, 0);
+      if (c + 1 < Z::KC)
+#pragma unroll
+        for (int o = h * H; o < h * H + H; ++o) a[o] = afrag32<LD>(Wf, o, c + 1, lane);
+    }
 }
 
 // The lane's KL contiguous floats of a row starting at p.
