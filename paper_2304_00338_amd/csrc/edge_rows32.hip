@@ -98,6 +98,9 @@ constexpr int R32_NT = 64 * R32_NW;
 template <int LD>
 struct __attribute__((aligned(16))) Fwd32Lds {
   __attribute__((aligned(16))) float stage[R32_NW][16 * R32<LD>::SLD];
+  // the fragment-major W2 (64 KB at width 128, 100 KB at 160): the second
+  // product reads its A fragments from LDS instead of L2
+  __attribute__((aligned(16))) float w2[LD * LD];
 };
 
 // In-segment node sums over one staged 16-row half [lo_row, lo_row + 16) of
@@ -148,6 +151,9 @@ k_edge_fwd_r32(EdgeTiles tl, const float* __restrict__ e_in, float* __restrict__
   __shared__ __align__(16) Fwd32Lds<LD> S;
   const int tid = threadIdx.x, lane = tid & 63, i = lane & 15, g = lane >> 4;
   const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+  for (int idx = tid; idx < LD * LD / 4; idx += R32_NT)
+    reinterpret_cast<f32x4*>(S.w2)[idx] = reinterpret_cast<const f32x4*>(w.F2)[idx];
+  __syncthreads();
   const UnitRange ur = unit_range<R32_NW>(tl.n_tiles, wv);
   int64_t t = ur.t;
   const int64_t stride = ur.stride, tend = ur.end;
@@ -206,7 +212,7 @@ k_edge_fwd_r32(EdgeTiles tl, const float* __restrict__ e_in, float* __restrict__
     // ---- z2 = b2 + W2 a1
 #pragma unroll
     for (int ob = 0; ob < Z::NOB; ++ob) acc[ob] = *reinterpret_cast<const f32x4*>(w.b2 + f0 + 4 * ob);
-    gemm32<LD>(acc, a1, w.F2 + oz, lane);
+    gemm32<LD>(acc, a1, S.w2 + oz, lane);
     // ---- LayerNorm over the row's DR real features (padded ones are 0)
     float sm = 0.f;
 #pragma unroll
