@@ -282,8 +282,8 @@ k_edge_fwd_rows(EdgeTiles tl, const bf16* __restrict__ e_in, bf16* __restrict__ 
 // carry only the work that needs their registers.  Two block barriers per
 // round order the staging: after the first it is free (the gradient waves
 // have read the previous round), after the second it is full.  dgamma and
-// dbeta are DPP column sums of each half, accumulated per lane of the row
-// waves.  Every sum runs in a fixed order, so results are reproducible.
+// dbeta are column sums of each half on MFMA (its rows, rounded to bf16,
+// through the wave's own LDS rows), accumulated per lane of the row waves.  Every sum runs in a fixed order, so results are reproducible.
 constexpr int FB_RW = 4;             // row waves per block (= gradient waves)
 constexpr int FB_NT = 128 * FB_RW;   // threads per block
 constexpr int FB_ROWS = 16 * FB_RW;  // rows staged per round
@@ -296,7 +296,29 @@ struct __attribute__((aligned(16))) FusedLds {
   __attribute__((aligned(16))) float g[D];
   // staged streams of a round: 0 dz2, 1 zbar, 2 a1, 3 e
   __attribute__((aligned(16))) bf16 st[4][FB_ROWS * FB_LD];
+  // each row wave's own 16 rows of a column-sum operand (mbar xhat, mbar)
+  __attribute__((aligned(16))) bf16 cs[FB_RW][16 * FB_LD];
 };
+
+// Column sums of a row wave's 16 staged rows (bf16, row stride FB_LD) on
+// MFMA: for each 16-feature block ob, the transposing read gives lane
+// (i, q) rows 4q .. 4q + 3 of feature 16 ob + i (the A operand, M = feature,
+// K = row) and a 0/1 operand that is 1 only in column ob routes the block's
+// sums there, so one accumulator collects all eight blocks: lane (i, q)
+// with i < 8 ends with the sums of features 16 i + 4 q + r (r < 4); lanes
+// with i >= 8 hold zeros.
+__device__ __forceinline__ f32x4 colsum_mfma(const bf16* rows, f32x4 acc, int i, int q) {
+  typedef short s16x4 __attribute__((ext_vector_type(4)));
+  const bf16* p = rows + (4 * q + (i >> 2)) * FB_LD + 4 * (i & 3);
+#pragma unroll
+  for (int ob = 0; ob < 8; ++ob) {
+    const bf16x4 a = lds_tr(p + 16 * ob);
+    const uint32_t w = i == ob ? 0x3F803F80u : 0u;  // bf16 pair (1, 1) or (0, 0)
+    const bf16x4 b = __builtin_bit_cast(bf16x4, uint2{w, w});
+    acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, b, acc, 0, 0, 0);
+  }
+  return acc;
+}
 
 // operand of 16 columns col0.. with K = the 32 staged rows r0 .. r0 + 31
 // (lane (i, q) gets rows r0 + 8q .. + 8 of column col0 + i)
@@ -520,7 +542,8 @@ k_edge_bwd_fused(EdgeTiles tl, const bf16* __restrict__ a1_in, const bf16* __res
     for (int ob = 0; ob < 8; ++ob) ag[ob] = *reinterpret_cast<const f32x4*>(gp + fo(ob, q));
   };
   const bf16x8 sel0 = select_frag(0, i, q), sel1 = select_frag(1, i, q);
-  float2 dga = {0.f, 0.f}, dbe = {0.f, 0.f};
+  f32x4 dga = {0.f, 0.f, 0.f, 0.f}, dbe = {0.f, 0.f, 0.f, 0.f};
+  bf16* csw = S.cs[k];  // this wave's column-sum rows
 
   // One round: the reverse of half rb of tile d0 (streams in H), its rows staged.
   auto round = [&](HalfLoads& H, f32x4 (&ag)[8], int next_recv, int4 d0, int rb) {
@@ -562,17 +585,19 @@ k_edge_bwd_fused(EdgeTiles tl, const bf16* __restrict__ a1_in, const bf16* __res
 #pragma unroll
       for (int ob = 0; ob < 8; ++ob) ag[ob] = live ? ag[ob] : f32x4{0.f, 0.f, 0.f, 0.f};
     }
-    // ---- dgamma += sum_rows mbar * xhat, dbeta += sum_rows mbar
+    // ---- dgamma += sum_rows mbar * xhat, dbeta += sum_rows mbar: the
+    // half's rows (bf16) through this wave's own LDS rows into MFMA column
+    // sums (the second write follows the first operand's reads in the
+    // wave's LDS order)
     {
-      f32x4 p[8];
+      bf16* cp = csw + i * FB_LD + 8 * q;
 #pragma unroll
-      for (int ob = 0; ob < 8; ++ob) p[ob] = ag[ob] * acc[ob];
-      const float2 c = colsum16(p, i);
-      dga.x += c.x;
-      dga.y += c.y;
-      const float2 d = colsum16(ag, i);
-      dbe.x += d.x;
-      dbe.y += d.y;
+      for (int s = 0; s < 4; ++s)
+        *reinterpret_cast<bf16x8*>(cp + 32 * s) = pack_run(ag[2 * s] * acc[2 * s], ag[2 * s + 1] * acc[2 * s + 1]);
+      dga = colsum_mfma(csw, dga, i, q);
+#pragma unroll
+      for (int s = 0; s < 4; ++s) *reinterpret_cast<bf16x8*>(cp + 32 * s) = pack_run(ag[2 * s], ag[2 * s + 1]);
+      dbe = colsum_mfma(csw, dbe, i, q);
     }
     // ---- LayerNorm backward: dz2 = rstd (dxh - mean(dxh) - xhat mean(dxh xhat)), dxh = mbar gamma
     float s1 = 0.f, s2 = 0.f;
@@ -680,9 +705,11 @@ k_edge_bwd_fused(EdgeTiles tl, const bf16* __restrict__ a1_in, const bf16* __res
   // ---- dgamma, dbeta: the row waves' sums in wave order
   __syncthreads();  // the gradient waves have read the last round
   float* red = reinterpret_cast<float*>(&S.st[0][0]);  // [2][FB_RW][D]
-  const int f = fo(i >> 1, q) + 2 * (i & 1);
-  *reinterpret_cast<float2*>(red + k * D + f) = dga;
-  *reinterpret_cast<float2*>(red + (FB_RW + k) * D + f) = dbe;
+  if (i < 8) {
+    const int f = 16 * i + 4 * q;
+    *reinterpret_cast<f32x4*>(red + k * D + f) = dga;
+    *reinterpret_cast<f32x4*>(red + (FB_RW + k) * D + f) = dbe;
+  }
   __syncthreads();
   if (tid < 2 * D) {
     const int c2 = tid >> 7, c = tid & (D - 1);
