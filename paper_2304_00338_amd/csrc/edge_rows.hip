@@ -575,11 +575,15 @@ k_edge_bwd_fused(EdgeTiles tl, const bf16* __restrict__ a1_in, const bf16* __res
       for (int r = 0; r < 4; ++r) sq += acc[ob][r] * acc[ob][r];
     }
     const float rstd = __builtin_amdgcn_rsqf(sum_rowlanes(sq) * (1.0f / D) + eps);
-    // mbar = aggbar[receiver] + ebar_in, zero on rows past the tile's end
+    // mbar = aggbar[receiver] + ebar_in (the bf16 ebar entered by a
+    // selection MFMA: one product per output, within an ulp of the VALU
+    // add), zero on rows past the tile's end
 #pragma unroll
     for (int ob = 0; ob < 8; ++ob) {
       acc[ob] *= rstd;  // xhat
-      if (HAVE_EBAR) ag[ob] += run_block(H.eb, ob);
+      if (HAVE_EBAR)
+        ag[ob] = __builtin_amdgcn_mfma_f32_16x16x32_bf16((ob & 1) ? sel1 : sel0, as_frag(H.eb[ob >> 1]), ag[ob], 0,
+                                                         0, 0);
     }
     if (n < rb * 16 + 16) {  // a partial half (uniform)
 #pragma unroll
