@@ -37,7 +37,7 @@ struct Off {
 
 struct PackOff {
   int64_t W1 = -1, W1t = -1, W2 = -1, W2t = -1, W1p = -1, W2p = -1;
-  int64_t F1 = -1, F2 = -1, F1t = -1, F2t = -1;  // fp32 edge MLPs: fragment-major W1e, W2 and transposes
+  int64_t F1 = -1, F2 = -1, F1t = -1, F2t = -1;  // fp32 edge MLPs (encoder: W2): fragment-major W1e, W2, transposes
   int64_t W1sp = -1, W1rp = -1;  // edge MLPs: row-permuted sender / receiver column blocks of W1
   int64_t W1ap = -1;             // node MLPs at width 160: row-permuted agg column block of W1
 };
@@ -152,6 +152,11 @@ Model make_model(int m, int lat, bool fp32 = false) {
   if (!rows) add_perm(M, M.enc_node.W2, D, M.p_enc_node.W2p, D, D);  // width-160 node encoder backward
   add_pack(M, M.enc_edge.W2, D, D, M.p_enc_edge.W2, M.p_enc_edge.W2t);
   add_perm(M, M.enc_edge.W2, D, M.p_enc_edge.W2p, D, D);  // row-layout edge encoders
+  if (fp32) {
+    // fp32 row-layout edge encoder: fragment-major W2 and its transpose
+    add_frag(M, M.enc_edge.W2, D, D, 2, M.p_enc_edge.F2);
+    add_frag(M, M.enc_edge.W2, D, D, 3, M.p_enc_edge.F2t);
+  }
   M.p_edge.resize(m);
   M.p_node.resize(m);
   for (int i = 0; i < m; ++i) {
@@ -557,7 +562,9 @@ struct Run {
       if (rows())
         LAUNCH(K_EDGE_ENC, launch_edge_enc_rows(E, efeat, W(M.enc_edge, M.p_enc_edge), eps, e_l(k, 0), s));
       else
-        LAUNCH(K_EDGE_ENC, launch_edge_enc(prec, D, E, efeat, W(M.enc_edge, M.p_enc_edge), eps, e_l(k, 0), s));
+        LAUNCH(K_EDGE_ENC, prec == MGN_FP32
+                               ? launch_edge_enc_r32(D, E, efeat, W(M.enc_edge, M.p_enc_edge), eps, e_l(k, 0), s)
+                               : launch_edge_enc(prec, D, E, efeat, W(M.enc_edge, M.p_enc_edge), eps, e_l(k, 0), s));
     }
     for (int l = 0; l < m; ++l) {
       const bool last = l == m - 1;
@@ -717,7 +724,10 @@ struct Run {
       if (rows())
         LAUNCH(K_EDGE_ENC_BWD, launch_edge_enc_bwd_rows(E, efeat, ebar, W(M.enc_edge, M.p_enc_edge), eps, pt, &nb, s));
       else
-        LAUNCH(K_EDGE_ENC_BWD, launch_edge_enc_bwd(prec, D, E, efeat, ebar, W(M.enc_edge, M.p_enc_edge), eps, pt, &nb, s));
+        LAUNCH(K_EDGE_ENC_BWD,
+               prec == MGN_FP32
+                   ? launch_edge_enc_bwd_r32(D, E, efeat, ebar, W(M.enc_edge, M.p_enc_edge), eps, pt, &nb, s)
+                   : launch_edge_enc_bwd(prec, D, E, efeat, ebar, W(M.enc_edge, M.p_enc_edge), eps, pt, &nb, s));
       if ((rc = reduce(nb, 0, 1, (int)M.enc_edge.size, grad, M.enc_edge.W1, 0)) != MGN_OK) return rc;
     }
     LAUNCH(K_NODE_ENC_BWD, launch_node_enc_bwd(prec, D, N, node_in, hb_cur, W(M.enc_node, M.p_enc_node), eps, gin, pt, &nb, s));

@@ -916,6 +916,370 @@ k_edge_bwd_r32w(EdgeTiles tl, const float* __restrict__ e_in, const float* ebar_
   }
 }
 
+// ========================================================= edge encoder
+// The edge encoder e = LN(W2 relu(W1 f + b1) + b2) (Sec. 2.1: the edge
+// features are encoded to the latent width by an MLP with LayerNorm) in this
+// row layout, forward and reverse.  The first layer (K = 4) runs on VALU as
+// one fma chain per feature from b1, k = 0..3, identical in both kernels, so
+// the reverse recomputes the forward's values bitwise; the second layer is
+// gemm32 on the fragment-major W2 (in LDS in the forward, from L2 in the
+// reverse, whose LDS holds the staged rows).
+constexpr int EK = 4;  // edge input features
+
+// z[s] = b1[f0 + s] + W1[f0 + s] . x, the lane's KL features (w1 holds each
+// feature's four input weights).
+template <int LD>
+__device__ __forceinline__ void enc_z1_r32(const float4* w1, const float* b1, float4 x, int f0,
+                                           float (&z)[R32<LD>::KL]) {
+#pragma unroll
+  for (int s = 0; s < R32<LD>::KL; ++s) {
+    const float4 wr = w1[f0 + s];
+    float v = b1[f0 + s];
+    v = __builtin_fmaf(wr.x, x.x, v);
+    v = __builtin_fmaf(wr.y, x.y, v);
+    v = __builtin_fmaf(wr.z, x.z, v);
+    v = __builtin_fmaf(wr.w, x.w, v);
+    z[s] = v;
+  }
+}
+
+template <int LD>
+struct __attribute__((aligned(16))) EncVec32 {
+  __attribute__((aligned(16))) float4 w1[LD];  // W1 by output feature
+  __attribute__((aligned(16))) float b1[LD];
+  __attribute__((aligned(16))) float b2[LD];
+  __attribute__((aligned(16))) float g[LD];
+  __attribute__((aligned(16))) float bt[LD];
+};
+template <int LD>
+__device__ __forceinline__ void stage_enc_vec(EncVec32<LD>& V, const MlpW& w, int tid) {
+  for (int f = tid; f < LD; f += R32_NT) {
+    V.w1[f] = float4{w.W1f[f * EK], w.W1f[f * EK + 1], w.W1f[f * EK + 2], w.W1f[f * EK + 3]};
+    V.b1[f] = w.b1[f];
+    V.b2[f] = w.b2[f];
+    V.g[f] = w.gamma[f];
+    V.bt[f] = w.beta[f];
+  }
+}
+
+template <int LD>
+struct __attribute__((aligned(16))) EncFwd32Lds {
+  EncVec32<LD> V;
+  __attribute__((aligned(16))) float w2[LD * LD];  // fragment-major W2
+};
+
+// Forward: one wave per 16-edge unit, no block barrier in the loop; the
+// next unit's inputs are in flight while one is computed.
+template <int LD>
+__global__ void __launch_bounds__(R32_NT) __attribute__((amdgpu_waves_per_eu(1, 1)))
+k_edge_enc_r32(int64_t E, const float* __restrict__ f_in, MlpW w, float eps, float* __restrict__ e_out) {
+  typedef R32<LD> Z;
+  __shared__ __align__(16) EncFwd32Lds<LD> S;
+  const int tid = threadIdx.x, lane = tid & 63, i = lane & 15, g = lane >> 4;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+  for (int idx = tid; idx < LD * LD / 4; idx += R32_NT)
+    reinterpret_cast<f32x4*>(S.w2)[idx] = reinterpret_cast<const f32x4*>(w.F2)[idx];
+  stage_enc_vec<LD>(S.V, w, tid);
+  __syncthreads();
+  const int64_t nu = (E + 15) >> 4;
+  const UnitRange ur = unit_range<R32_NW>(nu, wv);
+  if (ur.t >= ur.end) return;
+  const int f0 = Z::KL * g;
+  // rows clamped into [0, E): rows past E read row E - 1 and store nothing
+  auto load = [&](int64_t u) { return *reinterpret_cast<const float4*>(f_in + min(u * 16 + i, E - 1) * EK); };
+  float4 fa = load(ur.t);
+  for (int64_t u = ur.t; u < ur.end; u += ur.stride) {
+    const float4 fn = load(u + ur.stride);
+    // LDS reads through an opaque reference: otherwise the loop-invariant
+    // weight reads are hoisted out of the loop into (far too many) registers
+    const EncFwd32Lds<LD>& L = fresh(S);
+    float a1[Z::KL];
+    enc_z1_r32<LD>(L.V.w1, L.V.b1, fa, f0, a1);
+#pragma unroll
+    for (int s = 0; s < Z::KL; ++s) a1[s] = relu(a1[s]);
+    f32x4 acc[Z::NOB];
+#pragma unroll
+    for (int ob = 0; ob < Z::NOB; ++ob) acc[ob] = *reinterpret_cast<const f32x4*>(L.V.b2 + f0 + 4 * ob);
+    gemm32<LD>(acc, a1, L.w2, lane);
+    // ---- LayerNorm over the row's DR real features (padded ones are 0)
+    float sm = 0.f;
+#pragma unroll
+    for (int ob = 0; ob < Z::NOB; ++ob)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) sm += acc[ob][r];
+    const float mean = sum_q(sm) * (1.0f / Z::DR);
+    float sq = 0.f;
+#pragma unroll
+    for (int ob = 0; ob < Z::NOB; ++ob)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float dlt = acc[ob][r] - mean;
+        acc[ob][r] = dlt;
+        if (Z::DR == LD || f0 + 4 * ob + r < Z::DR) sq += dlt * dlt;
+      }
+    const float rstd = __builtin_amdgcn_rsqf(sum_q(sq) * (1.0f / Z::DR) + eps);
+#pragma unroll
+    for (int ob = 0; ob < Z::NOB; ++ob)
+      acc[ob] = *reinterpret_cast<const f32x4*>(L.V.g + f0 + 4 * ob) * (acc[ob] * rstd) +
+                *reinterpret_cast<const f32x4*>(L.V.bt + f0 + 4 * ob);
+    if (u * 16 + i < E) store_row32<LD>(e_out + (size_t)(u * 16 + i) * LD + f0, acc);
+    fa = fn;
+  }
+}
+
+// Reverse: every parameter gradient of the encoder from dL/de in one pass.
+// Four waves per block, each the reverse of one 16-edge unit per round (the
+// forward recomputed bitwise, the LayerNorm reverse, da1 = W2^T dz2, the
+// ReLU mask), staging its rows of dz2, a1, dz1 and the inputs [f, 1] in LDS;
+// after the round's second barrier each wave adds the round's 64 rows into
+// its tiles of dW2 = sum dz2^T a1 (NOB^2 / 4 tiles, row-major), its blocks
+// of dW1 | db1 = sum dz1^T [f, 1] and the ones column db2 = sum dz2 (output
+// blocks wv, wv + 4, wv + 8), with K = the rows.  dgamma and dbeta are DPP
+// column sums per unit.  Per-block partials in the encoder's parameter
+// order: W1 [LD][4], b1, W2 [LD][LD], b2, gamma, beta.
+template <int LD>
+struct __attribute__((aligned(16))) EncBwd32Lds {
+  EncVec32<LD> V;
+  __attribute__((aligned(16))) float st[3][B32_ROWS * (LD + 16)];  // dz2, a1, dz1
+  __attribute__((aligned(16))) float fx[B32_ROWS * 8];             // [f0..f3, 1, 0, 0, 0] per row
+};
+
+template <int LD>
+__global__ void __launch_bounds__(R32_NT) __attribute__((amdgpu_waves_per_eu(1, 1)))
+k_edge_enc_bwd_r32(int64_t E, const float* __restrict__ f_in, const float* __restrict__ ebar, MlpW w, float eps,
+                   Partials part) {
+  typedef R32<LD> Z;
+  constexpr int SL = LD + 16;                 // staged row stride (floats)
+  constexpr int TPW = Z::NOB * Z::NOB / 4;    // dW2 tiles per wave
+  __shared__ __align__(16) EncBwd32Lds<LD> S;
+  float* X = S.st[0];
+  float* Y = S.st[1];
+  float* Z1 = S.st[2];
+  const int tid = threadIdx.x, lane = tid & 63, i = lane & 15, g = lane >> 4;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int f0 = Z::KL * g;
+  stage_enc_vec<LD>(S.V, w, tid);
+  __syncthreads();
+
+  // The block's units: XCD-contiguous ranges; wave wv takes unit tb + wv of
+  // every round; all four waves run the same number of rounds.
+  const int64_t nu = (E + 15) >> 4;
+  const int G = gridDim.x;
+  int64_t tb, stride, tend;
+  if ((G & 7) == 0) {
+    const int x = blockIdx.x & 7, per = G >> 3;
+    const int64_t chunk = (nu + 7) >> 3;
+    const int64_t lo = x * chunk;
+    tend = min(nu, lo + chunk);
+    tb = lo + (int64_t)(blockIdx.x >> 3) * R32_NW;
+    stride = (int64_t)per * R32_NW;
+  } else {
+    tb = (int64_t)blockIdx.x * R32_NW;
+    stride = (int64_t)G * R32_NW;
+    tend = nu;
+  }
+  const int64_t lastE = max(E - 1, (int64_t)0);
+  auto grow = [&](int64_t u) { return min(u * 16 + i, lastE); };
+  struct In {
+    float4 x;
+    float yb[Z::KL];
+  };
+  auto load_in = [&](int64_t u, In& I) {
+    I.x = *reinterpret_cast<const float4*>(f_in + grow(u) * EK);
+    load_row32<LD>(I.yb, ebar + (size_t)grow(u) * LD + f0);
+  };
+
+  f32x4 aw2[TPW], ab2[3], aw1[3];
+#pragma unroll
+  for (int t = 0; t < TPW; ++t) aw2[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int t = 0; t < 3; ++t) ab2[t] = aw1[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float2 dga = {0.f, 0.f}, dbe = {0.f, 0.f};
+  float tga = 0.f, tbe = 0.f;  // width 160: blocks 8, 9 (tail butterfly)
+  const int srow = 16 * wv + i;
+  auto stage_row = [&](float* B, const float (&v)[Z::KL], bool live) {
+    float* p = B + srow * SL + f0;
+#pragma unroll
+    for (int c = 0; c < Z::KC; ++c)
+      *reinterpret_cast<f32x4*>(p + 4 * c) =
+          live ? f32x4{v[4 * c], v[4 * c + 1], v[4 * c + 2], v[4 * c + 3]} : f32x4{0.f, 0.f, 0.f, 0.f};
+  };
+  auto colsum = [&](const f32x4 (&v)[Z::NOB], float2& acc8, float& tail) {
+    f32x4 p8[8];
+#pragma unroll
+    for (int ob = 0; ob < 8; ++ob) p8[ob] = v[ob];
+    const float2 c = colsum16(p8, i);
+    acc8.x += c.x;
+    acc8.y += c.y;
+    if constexpr (Z::NOB == 10) tail += w160::colsum16_tail(reinterpret_cast<const f32x4(&)[10]>(v), i);
+  };
+
+  // units past the block's range (the last round's) are empty: their rows
+  // are never staged as live or stored
+  auto round = [&](In& I, int64_t u) {
+    const bool live = u < tend && u * 16 + i < E;
+    const int oz = opaque_zero();
+    const EncVec32<LD>& V = fresh(S.V);
+    // ---- z1, a1 = relu(z1), the mask z1 > 0 (the forward's values)
+    float a1[Z::KL];
+    enc_z1_r32<LD>(V.w1, V.b1, I.x, f0, a1);
+    uint64_t mask = 0;
+#pragma unroll
+    for (int s = 0; s < Z::KL; ++s) {
+      if (a1[s] > 0.f) mask |= 1ull << s;
+      a1[s] = relu(a1[s]);
+    }
+    __syncthreads();  // every wave's products of the previous round are done
+    stage_row(Y, a1, live);
+    if (g == 0) {
+      float* fp = S.fx + srow * 8;
+      *reinterpret_cast<float4*>(fp) = I.x;
+      *reinterpret_cast<float4*>(fp + 4) = float4{1.f, 0.f, 0.f, 0.f};
+    }
+    // ---- z2 = b2 + W2 a1 and its LayerNorm (DR real features)
+    f32x4 acc[Z::NOB];
+#pragma unroll
+    for (int ob = 0; ob < Z::NOB; ++ob) acc[ob] = *reinterpret_cast<const f32x4*>(V.b2 + f0 + 4 * ob);
+    gemm32<LD>(acc, a1, w.F2 + oz, lane);
+    float sm = 0.f;
+#pragma unroll
+    for (int ob = 0; ob < Z::NOB; ++ob)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) sm += acc[ob][r];
+    const float mean = sum_q(sm) * (1.0f / Z::DR);
+    float sq = 0.f;
+#pragma unroll
+    for (int ob = 0; ob < Z::NOB; ++ob)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        acc[ob][r] -= mean;
+        if (Z::DR == LD || f0 + 4 * ob + r < Z::DR) sq += acc[ob][r] * acc[ob][r];
+      }
+    const float rstd = __builtin_amdgcn_rsqf(sum_q(sq) * (1.0f / Z::DR) + eps);
+#pragma unroll
+    for (int ob = 0; ob < Z::NOB; ++ob) acc[ob] *= rstd;  // xhat
+    // ---- dgamma += sum_rows ybar xhat, dbeta += sum_rows ybar (live rows)
+    f32x4 t[Z::NOB];
+#pragma unroll
+    for (int ob = 0; ob < Z::NOB; ++ob)
+      t[ob] = live ? f32x4{I.yb[4 * ob], I.yb[4 * ob + 1], I.yb[4 * ob + 2], I.yb[4 * ob + 3]}
+                   : f32x4{0.f, 0.f, 0.f, 0.f};
+    colsum(t, dbe, tbe);
+    {
+      f32x4 p[Z::NOB];
+#pragma unroll
+      for (int ob = 0; ob < Z::NOB; ++ob) p[ob] = t[ob] * acc[ob];
+      colsum(p, dga, tga);
+    }
+    // ---- dz2 = rstd (dxh - mean(dxh) - xhat mean(dxh xhat)), dxh = ybar gamma
+    // (padded features: gamma = 0, dz2 zeroed)
+    float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+    for (int ob = 0; ob < Z::NOB; ++ob) {
+      t[ob] *= *reinterpret_cast<const f32x4*>(V.g + f0 + 4 * ob);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        s1 += t[ob][r];
+        s2 += t[ob][r] * acc[ob][r];
+      }
+    }
+    const float m1 = sum_q(s1) * (1.0f / Z::DR), m2 = sum_q(s2) * (1.0f / Z::DR);
+    float dz[Z::KL];
+#pragma unroll
+    for (int ob = 0; ob < Z::NOB; ++ob)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        dz[4 * ob + r] = Z::DR == LD || f0 + 4 * ob + r < Z::DR ? rstd * (t[ob][r] - m1 - acc[ob][r] * m2) : 0.f;
+    stage_row(X, dz, live);
+    // ---- da1 = W2^T dz2, dz1 = da1 where z1 > 0
+#pragma unroll
+    for (int ob = 0; ob < Z::NOB; ++ob) acc[ob] = f32x4{0.f, 0.f, 0.f, 0.f};
+    gemm32<LD>(acc, dz, w.F2t + oz, lane);
+    float d1[Z::KL];
+#pragma unroll
+    for (int ob = 0; ob < Z::NOB; ++ob)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) d1[4 * ob + r] = (mask >> (4 * ob + r)) & 1ull ? acc[ob][r] : 0.f;
+    stage_row(Z1, d1, live);
+    __syncthreads();  // the round's rows are staged
+    // ---- the round's 64 rows into this wave's gradient tiles
+#pragma unroll 2
+    for (int kk = 0; kk < B32_ROWS / 4; ++kk) {
+      const int rr = 4 * kk + g, r0 = rr * SL;
+      const float fb = i < 8 ? S.fx[rr * 8 + i] : 0.f;  // [f, 1, 0...] of row rr, column i
+#pragma unroll
+      for (int t3 = 0; t3 < 3; ++t3) {
+        const int ob = wv + 4 * t3;
+        if (ob < Z::NOB) {
+          ab2[t3] = __builtin_amdgcn_mfma_f32_16x16x4f32(X[r0 + 16 * ob + i], 1.0f, ab2[t3], 0, 0, 0);
+          aw1[t3] = __builtin_amdgcn_mfma_f32_16x16x4f32(Z1[r0 + 16 * ob + i], fb, aw1[t3], 0, 0, 0);
+        }
+      }
+#pragma unroll
+      for (int tt = 0; tt < TPW; ++tt) {
+        const int T = TPW * wv + tt, ob = T / Z::NOB, nb = T % Z::NOB;
+        aw2[tt] = __builtin_amdgcn_mfma_f32_16x16x4f32(X[r0 + 16 * ob + i], Y[r0 + 16 * nb + i], aw2[tt], 0, 0, 0);
+      }
+    }
+  };
+
+  if (tb < tend) {
+    In A, B;
+    load_in(tb + wv, A);
+    for (; tb < tend; tb += 2 * stride) {
+      load_in(tb + wv + stride, B);
+      round(A, tb + wv);
+      load_in(tb + wv + 2 * stride, A);
+      if (tb + stride < tend) round(B, tb + wv + stride);
+    }
+  }
+  // ---- block partials in the encoder's parameter order
+  float* base = part.buf + (size_t)blockIdx.x * part.stride;
+  constexpr int oW1 = 0, ob1 = EK * LD, oW2 = (EK + 1) * LD, ob2 = (EK + 1) * LD + LD * LD;
+  constexpr int og = ob2 + LD, obt = og + LD;
+#pragma unroll
+  for (int tt = 0; tt < TPW; ++tt) {
+    const int T = TPW * wv + tt, ob = T / Z::NOB, nb = T % Z::NOB;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) base[oW2 + (size_t)(16 * ob + 4 * g + r) * LD + 16 * nb + i] = aw2[tt][r];
+  }
+#pragma unroll
+  for (int t3 = 0; t3 < 3; ++t3) {
+    const int ob = wv + 4 * t3;
+    if (ob < Z::NOB)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int f = 16 * ob + 4 * g + r;
+        if (i == 0) base[ob2 + f] = ab2[t3][r];
+        if (i < EK) base[oW1 + f * EK + i] = aw1[t3][r];
+        if (i == EK) base[ob1 + f] = aw1[t3][r];
+      }
+  }
+  __syncthreads();
+  float* red = S.st[0];  // [2][R32_NW][LD]: dgamma, dbeta
+  {
+    // colsum16: lane i holds features f0 + 4 (i / 2) + 2 (i % 2) + {0, 1};
+    // colsum16_tail (width 160): lanes i, i ^ 1 hold value k of blocks 8, 9
+    const int f = f0 + 4 * (i >> 1) + 2 * (i & 1);
+    *reinterpret_cast<float2*>(red + (0 * R32_NW + wv) * LD + f) = dga;
+    *reinterpret_cast<float2*>(red + (1 * R32_NW + wv) * LD + f) = dbe;
+    if (Z::NOB == 10 && (i & 1) == 0) {
+      const int k = (((i >> 3) & 1) << 2) | (((i >> 2) & 1) << 1) | ((i >> 1) & 1);
+      const int ft = f0 + 4 * (8 + (k >> 2)) + (k & 3);
+      red[(0 * R32_NW + wv) * LD + ft] = tga;
+      red[(1 * R32_NW + wv) * LD + ft] = tbe;
+    }
+  }
+  __syncthreads();
+  for (int idx = tid; idx < 2 * LD; idx += R32_NT) {
+    const int k2 = idx / LD, c = idx % LD;
+    float v = 0.f;
+#pragma unroll
+    for (int u = 0; u < R32_NW; ++u) v += red[(k2 * R32_NW + u) * LD + c];
+    base[(k2 == 0 ? og : obt) + c] = v;
+  }
+}
+
 }  // namespace dev
 
 using namespace dev;
@@ -956,6 +1320,37 @@ hipError_t launch_edge_bwd_r32(int lat, const EdgeTiles& t, const void* e, const
   else
     hipLaunchKernelGGL(k_edge_bwd_r32, dim3(g), dim3(R32_NT), 0, s, t, (const float*)e, ebar_in, have_ebar,
                        ebar_out, (const float*)Pn, aggbar, w, eps, (float*)zbar, R, slots, part);
+  return hipGetLastError();
+}
+
+hipError_t launch_edge_enc_r32(int lat, int64_t E, const float* f, const MlpW& w, float eps, void* e_out,
+                               hipStream_t s) {
+  if (E <= 0) return hipSuccess;
+  if (!w.F2) return hipErrorInvalidValue;
+  const int64_t need = ((E + 15) / 16 + R32_NW - 1) / R32_NW;
+  int g = (int)std::min<int64_t>(need, kRows32Blocks);
+  if (g >= 8) g &= ~7;
+#define F(LD) \
+  hipLaunchKernelGGL(k_edge_enc_r32<LD>, dim3(g), dim3(R32_NT), 0, s, E, f, w, eps, (float*)e_out)
+  MGN_BY_WIDTH(lat, F);
+#undef F
+  return hipGetLastError();
+}
+
+hipError_t launch_edge_enc_bwd_r32(int lat, int64_t E, const float* f, const void* ebar, const MlpW& w, float eps,
+                                   const Partials& part, int* nblocks, hipStream_t s) {
+  *nblocks = 0;
+  if (E <= 0) return hipSuccess;
+  if (!w.F2 || !w.F2t || part.stride < (int64_t)lat * lat + (EK + 4) * lat) return hipErrorInvalidValue;
+  const int64_t need = ((E + 15) / 16 + R32_NW - 1) / R32_NW;
+  int g = (int)std::min<int64_t>(need, std::min(kRows32Blocks, part.max_blocks));
+  if (g >= 8) g &= ~7;
+  *nblocks = g;
+#define F(LD)                                                                                                 \
+  hipLaunchKernelGGL(k_edge_enc_bwd_r32<LD>, dim3(g), dim3(R32_NT), 0, s, E, f, (const float*)ebar, w, eps, \
+                     part)
+  MGN_BY_WIDTH(lat, F);
+#undef F
   return hipGetLastError();
 }
 

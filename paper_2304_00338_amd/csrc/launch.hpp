@@ -89,6 +89,14 @@ hipError_t launch_pack(int prec, const float* params, void* pack, const PackList
 // widths.
 hipError_t launch_node_enc(int prec, int lat, int64_t N, const float* node_in, const MlpW& w, const MlpW* next_edge,
                            float eps, float* h_out, void* P_out, hipStream_t s);
+// fp32 edge encoder in the row layout (width 128 or 160; needs the
+// fragment-major W2 and, for the reverse, its transpose): e = LN(W2 relu(W1
+// f + b1) + b2), and all encoder parameter gradients from ebar as per-block
+// partials in the encoder's parameter order.
+hipError_t launch_edge_enc_r32(int lat, int64_t E, const float* f, const MlpW& w, float eps, void* e_out,
+                               hipStream_t s);
+hipError_t launch_edge_enc_bwd_r32(int lat, int64_t E, const float* f, const void* ebar, const MlpW& w, float eps,
+                                   const Partials& part, int* nblocks, hipStream_t s);
 hipError_t launch_edge_enc(int prec, int lat, int64_t E, const float* efeat, const MlpW& w, float eps, void* e_out,
                            hipStream_t s);
 hipError_t launch_edge_fwd(int prec, int lat, const EdgeTiles& t, const void* e_in, void* e_out, int write_e,
