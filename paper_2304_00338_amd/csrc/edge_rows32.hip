@@ -97,10 +97,14 @@ constexpr int R32_NT = 64 * R32_NW;
 
 template <int LD>
 struct __attribute__((aligned(16))) Fwd32Lds {
-  __attribute__((aligned(16))) float stage[R32_NW][16 * R32<LD>::SLD];
-  // the fragment-major W2 (64 KB at width 128, 100 KB at 160): the second
-  // product reads its A fragments from LDS instead of L2
+  // At width 128 both products' fragment-major weights fit in LDS (64 KB
+  // each) beside an unpadded message staging (exactly 160 KiB); at 160 only
+  // W2 (100 KB) does, and the staging rows are padded.
+  static constexpr bool W1L = LD == 128;
+  static constexpr int SS = W1L ? LD : R32<LD>::SLD;  // staging row stride
+  __attribute__((aligned(16))) float stage[R32_NW][16 * SS];
   __attribute__((aligned(16))) float w2[LD * LD];
+  __attribute__((aligned(16))) float w1[W1L ? LD * LD : 4];
 };
 
 // In-segment node sums over one staged 16-row half [lo_row, lo_row + 16) of
@@ -151,8 +155,11 @@ k_edge_fwd_r32(EdgeTiles tl, const float* __restrict__ e_in, float* __restrict__
   __shared__ __align__(16) Fwd32Lds<LD> S;
   const int tid = threadIdx.x, lane = tid & 63, i = lane & 15, g = lane >> 4;
   const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
-  for (int idx = tid; idx < LD * LD / 4; idx += R32_NT)
+  typedef Fwd32Lds<LD> L;
+  for (int idx = tid; idx < LD * LD / 4; idx += R32_NT) {
     reinterpret_cast<f32x4*>(S.w2)[idx] = reinterpret_cast<const f32x4*>(w.F2)[idx];
+    if (L::W1L) reinterpret_cast<f32x4*>(S.w1)[idx] = reinterpret_cast<const f32x4*>(w.F1)[idx];
+  }
   __syncthreads();
   const UnitRange ur = unit_range<R32_NW>(tl.n_tiles, wv);
   int64_t t = ur.t;
@@ -203,7 +210,7 @@ k_edge_fwd_r32(EdgeTiles tl, const float* __restrict__ e_in, float* __restrict__
     // the weight addresses are opaque per half: otherwise the loop-invariant
     // fragment loads are hoisted out of the tile loop into registers
     const int oz = opaque_zero();
-    gemm32<LD>(acc, H.e, w.F1 + oz, lane);
+    gemm32<LD>(acc, H.e, (L::W1L ? S.w1 : w.F1) + oz, lane);
     float a1[Z::KL];
 #pragma unroll
     for (int ob = 0; ob < Z::NOB; ++ob)
@@ -236,7 +243,7 @@ k_edge_fwd_r32(EdgeTiles tl, const float* __restrict__ e_in, float* __restrict__
       const f32x4 be = *reinterpret_cast<const f32x4*>(w.beta + f0 + 4 * ob);
       acc[ob] = ga * (acc[ob] * rstd) + be;  // message m
     }
-    store_row32<LD>(stage + i * Z::SLD + f0, acc);
+    store_row32<LD>(stage + i * L::SS + f0, acc);
     // ---- e_out = e + m
     if (write_e && row < n) {
       f32x4 o[Z::NOB];
@@ -251,7 +258,7 @@ k_edge_fwd_r32(EdgeTiles tl, const float* __restrict__ e_in, float* __restrict__
       float* dst = !chunk ? agg + (size_t)(d0.x + jj) * LD : slots + (size_t)(-1 - d0.y) * LD;
       *reinterpret_cast<float2*>(dst + 2 * lane) = v[0];
       if (LD / 2 > 64 && lane + 64 < LD / 2) *reinterpret_cast<float2*>(dst + 2 * (lane + 64)) = v[1];
-    });
+    }, L::SS);
     wave_lds_sync();
   };
 
