@@ -564,7 +564,7 @@ struct Run {
       else
         LAUNCH(K_EDGE_ENC, prec == MGN_FP32
                                ? launch_edge_enc_r32(D, E, efeat, W(M.enc_edge, M.p_enc_edge), eps, e_l(k, 0), s)
-                               : launch_edge_enc(prec, D, E, efeat, W(M.enc_edge, M.p_enc_edge), eps, e_l(k, 0), s));
+                               : launch_edge_enc_w160(E, efeat, W(M.enc_edge, M.p_enc_edge), eps, e_l(k, 0), s));
     }
     for (int l = 0; l < m; ++l) {
       const bool last = l == m - 1;
@@ -727,7 +727,7 @@ struct Run {
         LAUNCH(K_EDGE_ENC_BWD,
                prec == MGN_FP32
                    ? launch_edge_enc_bwd_r32(D, E, efeat, ebar, W(M.enc_edge, M.p_enc_edge), eps, pt, &nb, s)
-                   : launch_edge_enc_bwd(prec, D, E, efeat, ebar, W(M.enc_edge, M.p_enc_edge), eps, pt, &nb, s));
+                   : launch_edge_enc_bwd_w160(E, efeat, ebar, W(M.enc_edge, M.p_enc_edge), eps, pt, &nb, s));
       if ((rc = reduce(nb, 0, 1, (int)M.enc_edge.size, grad, M.enc_edge.W1, 0)) != MGN_OK) return rc;
     }
     LAUNCH(K_NODE_ENC_BWD, launch_node_enc_bwd(prec, D, N, node_in, hb_cur, W(M.enc_node, M.p_enc_node), eps, gin, pt, &nb, s));

@@ -362,8 +362,8 @@ __global__ void __launch_bounds__(LD * 4) k_node_srcsum(int64_t N, const int32_t
   put_w<NCB>(base + D * D, D, dWr, w8, i, q);
 }
 
-// ------------------------------------------------------- encoders
-// ybar: dL/d(encoder output), fp32.
+// ------------------------------------------------------- node encoder
+// ybar: dL/d(encoder output), fp32; KIN inputs per row (the node encoder's 8).
 template <int PREC, int LD, int KIN>
 __global__ void __launch_bounds__(LD * 4) k_enc_bwd(int64_t M, const float* __restrict__ x_in,
                                                 const float* __restrict__ ybar, MlpW w, float eps,
@@ -611,25 +611,6 @@ hipError_t launch_node_srcsum(int prec, int lat, int64_t N, const int32_t* rowpt
     MGN_BY_WIDTH(lat, F);
 #undef F
   }
-  return hipGetLastError();
-}
-
-hipError_t launch_edge_enc_bwd(int prec, int lat, int64_t E, const float* efeat, const void* ebar, const MlpW& w,
-                               float eps, const Partials& part, int* nblocks, hipStream_t s) {
-  if (prec == MGN_BF16) {
-    // bf16 runs on the row-layout kernels (launch_edge_enc_bwd_rows at width 128)
-    *nblocks = 0;
-    if (lat != 160) return hipErrorInvalidValue;
-    return launch_edge_enc_bwd_w160(E, efeat, ebar, w, eps, part, nblocks, s);
-  }
-  const int g = bwd_grid((E + TM - 1) / TM, part);
-  *nblocks = g;
-  if (!g) return hipSuccess;
-#define F(LD)                                                                                                      \
-  hipLaunchKernelGGL((k_enc_bwd<MGN_FP32, LD, 4>), dim3(g), dim3(LD * 4), 0, s, E, efeat, (const float*)ebar, w,   \
-                     eps, (float*)nullptr, part)
-  MGN_BY_WIDTH(lat, F);
-#undef F
   return hipGetLastError();
 }
 

@@ -1,5 +1,5 @@
 // Forward kernels of one MGN call on gfx950 (Sec. 2.1 of the paper): weight
-// packing, node/edge encoders, the fused edge phase (gather -> edge MLP ->
+// packing, the node encoder, the fused edge phase (gather -> edge MLP ->
 // LayerNorm -> residual -> deterministic receiver sum), the fused node phase
 // and the decoder.
 //
@@ -130,68 +130,6 @@ __global__ void __launch_bounds__(LD * 4) k_node_enc(int64_t N, const float* __r
     if (EMIT) {
       __syncthreads();
       emit_P<PREC, LD>(sA, LDT, nx, r0, nr, P_out, w8, i, q);
-    }
-    __syncthreads();
-  }
-}
-
-// ------------------------------------------------------- edge encoder
-template <int PREC, int LD>
-__global__ void __launch_bounds__(LD * 4) k_edge_enc(int64_t E, const float* __restrict__ f_in, MlpW w, float eps,
-                                                 typename Tr<PREC>::T* __restrict__ e_out) {
-  typedef Tr<PREC> P;
-  typedef typename P::T T;
-  constexpr int D = LD;
-  [[maybe_unused]] constexpr int NW = Width<LD>::NW, NT = Width<LD>::NT;
-  constexpr int LDT = D + P::PAD;
-  __shared__ float sX[TM][4];
-  __shared__ __align__(16) T sA[TM * LDT];
-  __shared__ LnScratch<NW> ln;
-  const int tid = threadIdx.x, w8 = tid >> 6, lane = tid & 63, i = lane & 15, q = lane >> 4;
-  const int n = w8 * 16 + i;
-  const float b1 = w.b1[n], b2 = w.b2[n], gam = w.gamma[n], bet = w.beta[n];
-  float w1[4];
-#pragma unroll
-  for (int k = 0; k < 4; ++k) w1[k] = w.W1f[n * 4 + k];
-  const int64_t ntiles = (E + TM - 1) / TM;
-  for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
-    const int64_t r0 = t * TM;
-    const int nr = (int)min((int64_t)TM, E - r0);
-    if (tid < TM * 4) {
-      const int row = tid >> 2, k = tid & 3;
-      sX[row][k] = row < nr ? f_in[(r0 + row) * 4 + k] : 0.f;
-    }
-    __syncthreads();
-#pragma unroll
-    for (int rb = 0; rb < NRB; ++rb)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int row = rb * 16 + q * 4 + r;
-        float z = b1;
-#pragma unroll
-        for (int k = 0; k < 4; ++k) z += w1[k] * sX[row][k];
-        sA[row * LDT + n] = P::cvt(fmaxf(z, 0.f));
-      }
-    __syncthreads();
-    f32x4 acc[NRB];
-#pragma unroll
-    for (int rb = 0; rb < NRB; ++rb) acc[rb] = f32x4{b2, b2, b2, b2};
-    gemm_tile<PREC, D>(acc, sA, LDT, (const T*)w.W2, D, w8 * 16, 0, i, q);
-    f32x4 mean[NRB], rstd[NRB];
-    ln_stats(acc, ln, eps, w8, i, q, mean, rstd);
-#pragma unroll
-    for (int rb = 0; rb < NRB; ++rb)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int row = rb * 16 + q * 4 + r;
-        sA[row * LDT + n] = P::cvt(gam * ((acc[rb][r] - mean[rb][r]) * rstd[rb][r]) + bet);
-      }
-    __syncthreads();
-    for (int idx = tid; idx < nr * (D / 8); idx += NT) {
-      const int row = idx / (D / 8), c = (idx % (D / 8)) * 8;
-      T* dst = e_out + (size_t)(r0 + row) * D + c;
-#pragma unroll
-      for (int j = 0; j < 8; ++j) dst[j] = sA[row * LDT + c + j];
     }
     __syncthreads();
   }
@@ -360,21 +298,6 @@ hipError_t launch_node_enc(int prec, int lat, int64_t N, const float* x, const M
     MGN_BY_WIDTH(lat, F);
 #undef F
   }
-  return hipGetLastError();
-}
-
-hipError_t launch_edge_enc(int prec, int lat, int64_t E, const float* f, const MlpW& w, float eps, void* e_out,
-                           hipStream_t s) {
-  if (prec == MGN_BF16) {
-    // bf16 runs on the row-layout kernels (launch_edge_enc_rows at width 128)
-    if (lat != 160) return hipErrorInvalidValue;
-    return launch_edge_enc_w160(E, f, w, eps, e_out, s);
-  }
-  const int g = grid_for((E + TM - 1) / TM, kFwdBlocks);
-  if (!g) return hipSuccess;
-#define F(LD) hipLaunchKernelGGL((k_edge_enc<MGN_FP32, LD>), dim3(g), dim3(LD * 4), 0, s, E, f, w, eps, (float*)e_out)
-  MGN_BY_WIDTH(lat, F);
-#undef F
   return hipGetLastError();
 }
 

@@ -97,8 +97,6 @@ hipError_t launch_edge_enc_r32(int lat, int64_t E, const float* f, const MlpW& w
                                hipStream_t s);
 hipError_t launch_edge_enc_bwd_r32(int lat, int64_t E, const float* f, const void* ebar, const MlpW& w, float eps,
                                    const Partials& part, int* nblocks, hipStream_t s);
-hipError_t launch_edge_enc(int prec, int lat, int64_t E, const float* efeat, const MlpW& w, float eps, void* e_out,
-                           hipStream_t s);
 hipError_t launch_edge_fwd(int prec, int lat, const EdgeTiles& t, const void* e_in, void* e_out, int write_e,
                            const void* P, const MlpW& w, float eps, float* agg, float* slots, void* a1_out,
                            hipStream_t s);
@@ -214,9 +212,6 @@ hipError_t launch_wgrad(int prec, int lat, int64_t M, const void* G, const void*
 hipError_t launch_node_srcsum(int prec, int lat, int64_t N, const int32_t* rowptr, const int32_t* rev, const void* zbar,
                               const float* R, const float* h, const float* hbar_part, const MlpW& w,
                               float* hbar_out, const Partials& part, int* nblocks, hipStream_t s);
-// ebar: fp32, or bf16 (the edge-gradient stream of bf16 at width 160)
-hipError_t launch_edge_enc_bwd(int prec, int lat, int64_t E, const float* efeat, const void* ebar, const MlpW& w,
-                               float eps, const Partials& part, int* nblocks, hipStream_t s);
 hipError_t launch_node_enc_bwd(int prec, int lat, int64_t N, const float* node_in, const float* hbar, const MlpW& w,
                                float eps, float* gin, const Partials& part, int* nblocks, hipStream_t s);
 
