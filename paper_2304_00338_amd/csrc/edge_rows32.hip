@@ -44,10 +44,11 @@ __device__ __forceinline__ f32x4 afrag32(const float* __restrict__ Wf, int ob, i
 // The output blocks run in two groups of NOB / 2 interleaved accumulator
 // chains; as soon as a group has used its fragments of K chunk c, the
 // group's fragments of chunk c + 1 are requested into the same registers,
-// so each L2 read has the other group's MFMAs to arrive behind (one wave
-// per SIMD leaves no other wave to cover it) and no registers beyond one
-// chunk's fragments are used.  Every accumulator adds its K steps in
-// ascending order.
+// so each L2 read has the other group's MFMAs (4 NOB / 2 of them) to arrive
+// behind (one wave per SIMD leaves no other wave to cover it) and no
+// registers beyond one chunk's fragments are used.  A scheduling barrier
+// after each group's requests holds that order.  Every accumulator adds
+// its K steps in ascending order.
 template <int LD>
 __device__ __forceinline__ void gemm32(f32x4 (&acc)[R32<LD>::NOB], const float (&x)[R32<LD>::KL],
                                        const float* __restrict__ Wf, int lane) {
@@ -69,6 +70,9 @@ __device__ __forceinline__ void gemm32(f32x4 (&acc)[R32<LD>::NOB], const float (
       if (c + 1 < Z::KC)
 #pragma unroll
         for (int o = h * H; o < h * H + H; ++o) a[o] = afrag32<LD>(Wf, o, c + 1, lane);
+      // without it the compiler interleaves the two groups by K step and
+      // waits for each request a few MFMAs after issuing it
+      __builtin_amdgcn_sched_barrier(0);
     }
 }
 
@@ -705,7 +709,11 @@ k_edge_bwd_r32w(EdgeTiles tl, const float* __restrict__ e_in, const float* ebar_
           live ? f32x4{v[4 * c], v[4 * c + 1], v[4 * c + 2], v[4 * c + 3]} : f32x4{0.f, 0.f, 0.f, 0.f};
   };
 
-  auto round = [&](Half& H, int4 d0, int rb, int segraw, bool chunk, int nv, int& j, float2 (&carry)[2]) {
+  // H holds the half's e rows, used by the first product only; after the
+  // last product the next half's rows (tile dn, half rbn) are requested into
+  // the same registers and arrive behind the receiver sums and dW2 products.
+  auto round = [&](Half& H, int4 d0, int rb, int4 dn, int rbn, int segraw, bool chunk, int nv, int& j,
+                   float2 (&carry)[2]) {
     const int n = tile_rows(d0);
     const int row = rb * 16 + i;
     const bool live = row < n;
@@ -833,6 +841,7 @@ k_edge_bwd_r32w(EdgeTiles tl, const float* __restrict__ e_in, const float* ebar_
       acc[ob] = f32x4{eb[4 * ob], eb[4 * ob + 1], eb[4 * ob + 2], eb[4 * ob + 3]};
     gemm32<LD>(acc, zb, w.F1t + oz, lane);
     if (live) store_row32<LD>(ebar_out + ((size_t)d0.z + row) * LD + f0, acc);
+    load_half(dn, rbn, H);
     __syncthreads();  // X = dz2, Y = a1, Zs = zbar staged
     // ---- receiver sums of this wave's zbar rows
     seg_pass32<LD>(Zs + 16 * wv * C32_SLD, lane, segraw, d0.z, chunk, n, nv, rb * 16, j, carry,
@@ -861,19 +870,17 @@ k_edge_bwd_r32w(EdgeTiles tl, const float* __restrict__ e_in, const float* ebar_
 
   if (tb < tend) {
     int4 d0 = desc(tb + wv), d1 = desc(tb + wv + stride);
-    Half A, B;
+    Half A;
     load_half(d0, 0, A);
     for (; tb < tend; tb += stride) {
       const bool chunk = d0.y < 0;
       const int nv = chunk ? 1 : d0.y - d0.x;
       const int segraw = tl.rowptr[min(d0.x + lane, max(d0.x, d0.y))];
       const int4 d2 = desc(tb + wv + 2 * stride);
-      load_half(d0, 1, B);
       float2 carry[2] = {{0.f, 0.f}, {0.f, 0.f}};
       int j = 0;
-      round(A, d0, 0, segraw, chunk, nv, j, carry);
-      load_half(d1, 0, A);
-      round(B, d0, 1, segraw, chunk, nv, j, carry);
+      round(A, d0, 0, d0, 1, segraw, chunk, nv, j, carry);
+      round(A, d0, 1, d1, 0, segraw, chunk, nv, j, carry);
       d0 = d1;
       d1 = d2;
     }
