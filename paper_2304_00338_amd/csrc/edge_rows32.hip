@@ -47,11 +47,12 @@ __device__ __forceinline__ f32x4 afrag32(const float* __restrict__ Wf, int ob, i
 // so each L2 read has the other group's MFMAs (4 NOB / 2 of them) to arrive
 // behind (one wave per SIMD leaves no other wave to cover it) and no
 // registers beyond one chunk's fragments are used.  A scheduling barrier
-// after each group's requests holds that order.  Every accumulator adds
-// its K steps in ascending order.
-template <int LD>
+// after each group's requests holds that order.  mid() runs once, halfway
+// through the K chunks (for loads that the caller needs after the product).
+// Every accumulator adds its K steps in ascending order.
+template <int LD, class F>
 __device__ __forceinline__ void gemm32(f32x4 (&acc)[R32<LD>::NOB], const float (&x)[R32<LD>::KL],
-                                       const float* __restrict__ Wf, int lane) {
+                                       const float* __restrict__ Wf, int lane, F&& mid) {
   typedef R32<LD> Z;
   constexpr int H = Z::NOB / 2;
   static_assert(Z::NOB % 2 == 0, "two groups of output blocks");
@@ -70,10 +71,16 @@ __device__ __forceinline__ void gemm32(f32x4 (&acc)[R32<LD>::NOB], const float (
       if (c + 1 < Z::KC)
 #pragma unroll
         for (int o = h * H; o < h * H + H; ++o) a[o] = afrag32<LD>(Wf, o, c + 1, lane);
+      if (h == 1 && c == Z::KC / 2 - 1) mid();
       // without it the compiler interleaves the two groups by K step and
       // waits for each request a few MFMAs after issuing it
       __builtin_amdgcn_sched_barrier(0);
     }
+}
+template <int LD>
+__device__ __forceinline__ void gemm32(f32x4 (&acc)[R32<LD>::NOB], const float (&x)[R32<LD>::KL],
+                                       const float* __restrict__ Wf, int lane) {
+  gemm32<LD>(acc, x, Wf, lane, [] {});
 }
 
 // The lane's KL contiguous floats of a row starting at p.
@@ -401,7 +408,11 @@ k_edge_bwd_r32(EdgeTiles tl, const float* __restrict__ e_in, const float* ebar_i
           live ? f32x4{v[4 * c], v[4 * c + 1], v[4 * c + 2], v[4 * c + 3]} : f32x4{0.f, 0.f, 0.f, 0.f};
   };
 
-  auto round = [&](Half& H, int4 d0, int rb, int segraw, bool chunk, int nv, int& j, float2& carry) {
+  // H holds the half's e rows (the first product's operand, then staged);
+  // after the last product the next half's rows (tile dn, half rbn) are
+  // requested into the same registers.
+  auto round = [&](Half& H, int4 d0, int rb, int4 dn, int rbn, int segraw, bool chunk, int nv, int& j,
+                   float2& carry) {
     const int n = tile_rows(d0);
     const int row = rb * 16 + i;
     const bool live = row < n;
@@ -422,19 +433,25 @@ k_edge_bwd_r32(EdgeTiles tl, const float* __restrict__ e_in, const float* ebar_i
 #pragma unroll
     for (int ob = 0; ob < Z::NOB; ++ob) acc[ob] = f32x4{0.f, 0.f, 0.f, 0.f};
     __syncthreads();
-    gemm32<LD>(acc, H.e, w.F1 + oz, lane);
-    stage_row(S.st[2], H.e, live);
-    float a1[Z::KL];
-    uint32_t mask = 0;
-    {
+    // the gathered node products are requested halfway through the product
+    f32x4 pa[Z::NOB], pb[Z::NOB];
+    gemm32<LD>(acc, H.e, w.F1 + oz, lane, [&] {
       const float* ps = Pn + (size_t)snd * (2 * LD) + f0;
       const float* pr = Pn + (size_t)rcv * (2 * LD) + LD + f0;
 #pragma unroll
       for (int ob = 0; ob < Z::NOB; ++ob) {
+        pa[ob] = *reinterpret_cast<const f32x4*>(ps + 4 * ob);
+        pb[ob] = *reinterpret_cast<const f32x4*>(pr + 4 * ob);
+      }
+    });
+    stage_row(S.st[2], H.e, live);
+    float a1[Z::KL];
+    uint32_t mask = 0;
+    {
+#pragma unroll
+      for (int ob = 0; ob < Z::NOB; ++ob) {
         const f32x4 b1 = *reinterpret_cast<const f32x4*>(w.b1 + f0 + 4 * ob);
-        const f32x4 pa = *reinterpret_cast<const f32x4*>(ps + 4 * ob);
-        const f32x4 pb = *reinterpret_cast<const f32x4*>(pr + 4 * ob);
-        const f32x4 z = acc[ob] + ((b1 + pa) + pb);
+        const f32x4 z = acc[ob] + ((b1 + pa[ob]) + pb[ob]);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           a1[4 * ob + r] = relu(z[r]);
@@ -445,7 +462,13 @@ k_edge_bwd_r32(EdgeTiles tl, const float* __restrict__ e_in, const float* ebar_i
     // ---- z2 = b2 + W2 a1 and its LayerNorm statistics
 #pragma unroll
     for (int ob = 0; ob < Z::NOB; ++ob) acc[ob] = *reinterpret_cast<const f32x4*>(w.b2 + f0 + 4 * ob);
-    gemm32<LD>(acc, a1, w.F2 + oz, lane);
+    // the receiver's aggregate gradient, requested halfway through the product
+    f32x4 ag[Z::NOB];
+    gemm32<LD>(acc, a1, w.F2 + oz, lane, [&] {
+      const float* gp = aggbar + (size_t)rcv * LD + f0;
+#pragma unroll
+      for (int ob = 0; ob < Z::NOB; ++ob) ag[ob] = *reinterpret_cast<const f32x4*>(gp + 4 * ob);
+    });
     float sm = 0.f;
 #pragma unroll
     for (int ob = 0; ob < Z::NOB; ++ob)
@@ -463,19 +486,17 @@ k_edge_bwd_r32(EdgeTiles tl, const float* __restrict__ e_in, const float* ebar_i
     // ---- mbar = ebar_in + aggbar[receiver]; dgamma, dbeta; LayerNorm reverse
     float dz[Z::KL];
     {
-      const float* gp = aggbar + (size_t)rcv * LD + f0;
       float s1 = 0.f, s2 = 0.f;
       f32x4 pg[Z::NOB], pb[Z::NOB];
 #pragma unroll
       for (int ob = 0; ob < Z::NOB; ++ob) {
-        const f32x4 ag = *reinterpret_cast<const f32x4*>(gp + 4 * ob);
         const f32x4 ga = *reinterpret_cast<const f32x4*>(w.gamma + f0 + 4 * ob);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int s = 4 * ob + r;
           const float xh = acc[ob][r] * rstd;
           acc[ob][r] = xh;
-          const float mb = eb[s] + ag[r];
+          const float mb = eb[s] + ag[ob][r];
           pg[ob][r] = live ? mb * xh : 0.f;
           pb[ob][r] = live ? mb : 0.f;
           const float dxh = mb * ga[r];
@@ -520,6 +541,7 @@ k_edge_bwd_r32(EdgeTiles tl, const float* __restrict__ e_in, const float* ebar_i
       acc[ob] = f32x4{eb[4 * ob], eb[4 * ob + 1], eb[4 * ob + 2], eb[4 * ob + 3]};
     gemm32<LD>(acc, zb, w.F1t + oz, lane);
     if (live) store_row32<LD>(ebar_out + ((size_t)d0.z + row) * LD + f0, acc);
+    load_half(dn, rbn, H);
     __syncthreads();  // the round's rows are staged
     // ---- receiver sums of zbar over this wave's staged rows
     seg_pass_b32(S.st[3] + 16 * wv * B32_SLD, lane, segraw, d0.z, chunk, n, nv, rb * 16, j, carry,
@@ -555,19 +577,17 @@ k_edge_bwd_r32(EdgeTiles tl, const float* __restrict__ e_in, const float* ebar_i
 
   if (tb < tend) {
     int4 d0 = desc(tb + wv), d1 = desc(tb + wv + stride);
-    Half A, B;
+    Half A;
     load_half(d0, 0, A);
     for (; tb < tend; tb += stride) {
       const bool chunk = d0.y < 0;
       const int nv = chunk ? 1 : d0.y - d0.x;
       const int segraw = tl.rowptr[min(d0.x + lane, max(d0.x, d0.y))];
       const int4 d2 = desc(tb + wv + 2 * stride);
-      load_half(d0, 1, B);
       float2 carry = {0.f, 0.f};
       int j = 0;
-      round(A, d0, 0, segraw, chunk, nv, j, carry);
-      load_half(d1, 0, A);
-      round(B, d0, 1, segraw, chunk, nv, j, carry);
+      round(A, d0, 0, d0, 1, segraw, chunk, nv, j, carry);
+      round(A, d0, 1, d1, 0, segraw, chunk, nv, j, carry);
       d0 = d1;
       d1 = d2;
     }
@@ -724,18 +744,24 @@ k_edge_bwd_r32w(EdgeTiles tl, const float* __restrict__ e_in, const float* ebar_
     f32x4 acc[Z::NOB];
 #pragma unroll
     for (int ob = 0; ob < Z::NOB; ++ob) acc[ob] = f32x4{0.f, 0.f, 0.f, 0.f};
-    gemm32<LD>(acc, H.e, w.F1 + oz, lane);
-    float a1[Z::KL];
-    uint64_t mask = 0;
-    {
+    // the gathered node products are requested halfway through the product
+    f32x4 pa[Z::NOB], pb[Z::NOB];
+    gemm32<LD>(acc, H.e, w.F1 + oz, lane, [&] {
       const float* ps = Pn + (size_t)snd * (2 * LD) + f0;
       const float* pr = Pn + (size_t)rcv * (2 * LD) + LD + f0;
 #pragma unroll
       for (int ob = 0; ob < Z::NOB; ++ob) {
+        pa[ob] = *reinterpret_cast<const f32x4*>(ps + 4 * ob);
+        pb[ob] = *reinterpret_cast<const f32x4*>(pr + 4 * ob);
+      }
+    });
+    float a1[Z::KL];
+    uint64_t mask = 0;
+    {
+#pragma unroll
+      for (int ob = 0; ob < Z::NOB; ++ob) {
         const f32x4 b1 = *reinterpret_cast<const f32x4*>(w.b1 + f0 + 4 * ob);
-        const f32x4 pa = *reinterpret_cast<const f32x4*>(ps + 4 * ob);
-        const f32x4 pb = *reinterpret_cast<const f32x4*>(pr + 4 * ob);
-        const f32x4 z = acc[ob] + ((b1 + pa) + pb);
+        const f32x4 z = acc[ob] + ((b1 + pa[ob]) + pb[ob]);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           a1[4 * ob + r] = relu(z[r]);
@@ -748,23 +774,22 @@ k_edge_bwd_r32w(EdgeTiles tl, const float* __restrict__ e_in, const float* ebar_
     // ---- z2 = b2 + W2 a1; LayerNorm statistics over the 150 real features
 #pragma unroll
     for (int ob = 0; ob < Z::NOB; ++ob) acc[ob] = *reinterpret_cast<const f32x4*>(w.b2 + f0 + 4 * ob);
-    gemm32<LD>(acc, a1, w.F2 + oz, lane);
-    // the incoming gradients of the half
     float eb[Z::KL];
+    f32x4 ag[Z::NOB];
+    gemm32<LD>(acc, a1, w.F2 + oz, lane, [&] {
+      const float* gp = aggbar + (size_t)rcv * LD + f0;
+#pragma unroll
+      for (int ob = 0; ob < Z::NOB; ++ob) ag[ob] = *reinterpret_cast<const f32x4*>(gp + 4 * ob);
+    });
     load_row32<LD>(eb, ebar_in + grow * LD + f0);
     if (!have_ebar)
 #pragma unroll
       for (int s = 0; s < Z::KL; ++s) eb[s] = 0.f;
     f32x4 t[Z::NOB];  // mbar, then dxh, then dz2
-    {
-      const float* gp = aggbar + (size_t)rcv * LD + f0;
 #pragma unroll
-      for (int ob = 0; ob < Z::NOB; ++ob) {
-        const f32x4 ag = *reinterpret_cast<const f32x4*>(gp + 4 * ob);
+    for (int ob = 0; ob < Z::NOB; ++ob)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) t[ob][r] = eb[4 * ob + r] + ag[r];
-      }
-    }
+      for (int r = 0; r < 4; ++r) t[ob][r] = eb[4 * ob + r] + ag[ob][r];
     float sm = 0.f;
 #pragma unroll
     for (int ob = 0; ob < Z::NOB; ++ob)
