@@ -573,8 +573,12 @@ struct Run {
         LAUNCH(K_EDGE_FWD, launch_edge_fwd_r32(D, tl, e_l(k, l), e_out, last ? 0 : 1, P_l(k, l),
                                                W(M.edge[l], M.p_edge[l]), eps, agg_l(k, l), slots(), s));
       else if (E > 0)
-        LAUNCH(K_EDGE_FWD, launch_edge_fwd(prec, D, tl, e_l(k, l), e_out, last ? 0 : 1, P_l(k, l), W(M.edge[l], M.p_edge[l]),
-                                eps, agg_l(k, l), slots(), a1_l(k, l), s));
+        LAUNCH(K_EDGE_FWD, rows() ? launch_edge_fwd_rows(tl, e_l(k, l), e_out, last ? 0 : 1, P_l(k, l),
+                                                         W(M.edge[l], M.p_edge[l]), eps, agg_l(k, l), slots(),
+                                                         a1_l(k, l), s)
+                                  : launch_edge_fwd_w160(tl, e_l(k, l), e_out, last ? 0 : 1, P_l(k, l),
+                                                         W(M.edge[l], M.p_edge[l]), eps, agg_l(k, l), slots(),
+                                                         a1_l(k, l), s));
       else
         LAUNCH(K_EDGE_FWD, launch_fill(agg_l(k, l), N * D, 0.f, s));  // no edges: every aggregate is zero
       if (g.n_long > 0) LAUNCH(K_FIXUP, launch_slot_fixup(D, g.long_nodes, g.n_long, slots(), agg_l(k, l), s));
@@ -703,7 +707,7 @@ struct Run {
                                                P_l(k, l), aggbar, W(oe, M.p_edge[l]), eps, zbar, R, slots(), P2, &nb,
                                                s));
         if ((rc = job(nb, 2, (int64_t)D * D, 1, (int)(oe.size - 3 * D * D), grad, oe.b1, 0)) != MGN_OK) return rc;
-        LAUNCH(K_WGRAD, launch_wgrad(prec, D, E, zbar, e_l(k, l), P3, &nb, s));
+        LAUNCH(K_WGRAD, launch_wgrad_r32(D, E, (const float*)zbar, (const float*)e_l(k, l), P3, &nb, s));
         if ((rc = job(nb, 3, 0, D, D, grad, oe.W1, 3 * D)) != MGN_OK) return rc;
       }
       if (g.n_long > 0) LAUNCH(K_FIXUP, launch_slot_fixup(D, g.long_nodes, g.n_long, slots(), R, s));

@@ -641,13 +641,15 @@ k_edge_bwd_r32(EdgeTiles tl, const float* __restrict__ e_in, const float* ebar_i
 // 160 x 160 products would need 224 accumulator registers per wave, and
 // four staged fp32 streams 180 KB of LDS).  Buffers: X (dz2) and Y (a1) of
 // the round's 64 rows, Zs (each wave's own zbar rows, for its receiver
-// sums).  Each wave owns 25 of the 100 16 x 16 tiles of dW2 (25 wv .. + 25,
-// row-major) and the ones columns of output blocks wv, wv + 4, wv + 8.  The
-// LayerNorm runs over the 150 real features (padded features of dz2 are
-// zeroed); db1 is a DPP column sum of zbar per half.
+// sums).  Each wave owns a 5 x 5 block of the 100 16 x 16 tiles of dW2
+// (output blocks 5 (wv / 2) .., input blocks 5 (wv % 2) ..) and the ones
+// columns of three or two of its five output blocks.  The LayerNorm runs
+// over the 150 real features (padded features of dz2 are zeroed); db1 is a
+// DPP column sum of zbar per half.
 constexpr int C32_LD = 160;
 constexpr int C32_SLD = C32_LD + 16;  // staged row stride: lane groups 0, 1 hit distinct banks
-constexpr int C32_TILES = 25;         // dW2 tiles per wave
+constexpr int C32_HB = 5;             // a wave's dW2 tiles: a 5 x 5 block of the 10 x 10
+constexpr int C32_TILES = C32_HB * C32_HB;
 
 struct __attribute__((aligned(16))) Bwd32wLds {
   __attribute__((aligned(16))) float st[3][B32_ROWS * C32_SLD];  // X, Y, Zs
@@ -678,6 +680,10 @@ k_edge_bwd_r32w(EdgeTiles tl, const float* __restrict__ e_in, const float* ebar_
   const int tid = threadIdx.x, lane = tid & 63, i = lane & 15, g = lane >> 4;
   const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int f0 = Z::KL * g;
+  // this wave's block of dW2 tiles and the output blocks of its db2 ones
+  // columns (the two waves of a block row split its five output blocks)
+  const int ob0 = C32_HB * (wv >> 1), nb0 = C32_HB * (wv & 1);
+  const int uones = (wv & 1) ? 3 : 0, nones = (wv & 1) ? 2 : 3;
 
   const int G = gridDim.x;
   int64_t tb, stride, tend;
@@ -876,19 +882,28 @@ k_edge_bwd_r32w(EdgeTiles tl, const float* __restrict__ e_in, const float* ebar_
                      if (lane + 64 < LD / 2) *reinterpret_cast<float2*>(dst + 2 * (lane + 64)) = v[1];
                    },
                    C32_SLD);
-    // ---- the round's 64 rows into this wave's tiles of dW2 = dz2^T a1
+    // ---- the round's 64 rows into this wave's block of dW2 = dz2^T a1
+    // (per 4 rows: 10 LDS reads, 25 products and the db2 ones columns)
+    {
+      const float* pa = X + g * C32_SLD + 16 * ob0 + i;
+      const float* pb = Y + g * C32_SLD + 16 * nb0 + i;
 #pragma unroll 2
-    for (int kk = 0; kk < B32_ROWS / 4; ++kk) {
-      const int r0 = (4 * kk + g) * C32_SLD;
+      for (int kk = 0; kk < B32_ROWS / 4; ++kk) {
+        float A[C32_HB], B[C32_HB];
 #pragma unroll
-      for (int t3 = 0; t3 < 3; ++t3) {
-        const int ob = wv + 4 * t3;
-        if (ob < Z::NOB) ab2[t3] = __builtin_amdgcn_mfma_f32_16x16x4f32(X[r0 + 16 * ob + i], 1.0f, ab2[t3], 0, 0, 0);
-      }
+        for (int u = 0; u < C32_HB; ++u) {
+          A[u] = pa[4 * kk * C32_SLD + 16 * u];
+          B[u] = pb[4 * kk * C32_SLD + 16 * u];
+        }
 #pragma unroll
-      for (int tt = 0; tt < C32_TILES; ++tt) {
-        const int T = C32_TILES * wv + tt, ob = T / Z::NOB, nb = T % Z::NOB;
-        aw2[tt] = __builtin_amdgcn_mfma_f32_16x16x4f32(X[r0 + 16 * ob + i], Y[r0 + 16 * nb + i], aw2[tt], 0, 0, 0);
+        for (int t3 = 0; t3 < 3; ++t3)
+          if (t3 < nones) ab2[t3] = __builtin_amdgcn_mfma_f32_16x16x4f32(A[uones + t3], 1.0f, ab2[t3], 0, 0, 0);
+#pragma unroll
+        for (int u = 0; u < C32_HB; ++u)
+#pragma unroll
+          for (int v = 0; v < C32_HB; ++v)
+            aw2[u * C32_HB + v] =
+                __builtin_amdgcn_mfma_f32_16x16x4f32(A[u], B[v], aw2[u * C32_HB + v], 0, 0, 0);
       }
     }
   };
@@ -915,19 +930,18 @@ k_edge_bwd_r32w(EdgeTiles tl, const float* __restrict__ e_in, const float* ebar_
   float* base = part.buf + (size_t)blockIdx.x * part.stride;
   constexpr int ob1 = LD * LD, oW2 = LD * LD + LD, ob2 = 2 * LD * LD + LD, og = 2 * LD * LD + 2 * LD;
 #pragma unroll
-  for (int t = 0; t < C32_TILES; ++t) {
-    const int T = C32_TILES * wv + t, ob = T / Z::NOB, nb = T % Z::NOB;
+  for (int u = 0; u < C32_HB; ++u)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) base[oW2 + (size_t)(16 * ob + 4 * g + r) * LD + 16 * nb + i] = aw2[t][r];
-  }
+    for (int v = 0; v < C32_HB; ++v)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        base[oW2 + (size_t)(16 * (ob0 + u) + 4 * g + r) * LD + 16 * (nb0 + v) + i] = aw2[u * C32_HB + v][r];
   if (i == 0)
 #pragma unroll
-    for (int t = 0; t < 3; ++t) {
-      const int ob = wv + 4 * t;
-      if (ob < Z::NOB)
+    for (int t = 0; t < 3; ++t)
+      if (t < nones)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) base[ob2 + 16 * ob + 4 * g + r] = ab2[t][r];
-    }
+        for (int r = 0; r < 4; ++r) base[ob2 + 16 * (ob0 + uones + t) + 4 * g + r] = ab2[t][r];
   __syncthreads();
   float* red = S.st[0];  // [3][R32_NW][LD]: dgamma, dbeta, db1
   {
@@ -953,6 +967,82 @@ k_edge_bwd_r32w(EdgeTiles tl, const float* __restrict__ e_in, const float* ebar_
     for (int u = 0; u < R32_NW; ++u) v += red[(k2 * R32_NW + u) * LD + c];
     base[k2 == 2 ? ob1 + c : og + k2 * LD + c] = v;
   }
+}
+
+// ======================================================= weight gradient
+// dW[o][n] = sum over rows of G[row][o] X[row][n] for two row-major fp32
+// [M][LD] streams (the width-160 reverse leaves dW1e = sum zbar^T e to this
+// pass).  Rounds of 64 rows: each wave loads 16 rows of both streams in the
+// row layout, stages them in LDS, and after a block barrier adds the round
+// into its quarter of dW, a block of (NOB / 2)^2 16 x 16 tiles, with the
+// rows as K (accumulators in AGPRs; per 4 rows NOB LDS reads feed
+// (NOB / 2)^2 MFMAs); the next round's rows are requested before the
+// round's MFMAs.  Rows are added in ascending order within a block.
+template <int LD>
+__global__ void __launch_bounds__(R32_NT) __attribute__((amdgpu_waves_per_eu(1, 1)))
+k_wgrad_r32(int64_t M, const float* __restrict__ Gm, const float* __restrict__ Xm, Partials part) {
+  typedef R32<LD> Z;
+  constexpr int SLD = LD + 16;  // lane groups 0, 1 of a staging write hit distinct banks
+  // wave wv owns the HB x HB block of 16 x 16 tiles (ob0 + u, nb0 + v)
+  constexpr int HB = Z::NOB / 2, TPW = HB * HB;
+  __shared__ __align__(16) float st[2][B32_ROWS * SLD];
+  const int tid = threadIdx.x, lane = tid & 63, i = lane & 15, g = lane >> 4;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int f0 = Z::KL * g;
+  const int ob0 = HB * (wv >> 1), nb0 = HB * (wv & 1);
+  const int64_t nr = (M + B32_ROWS - 1) / B32_ROWS;
+  f32x4 aw[TPW];
+#pragma unroll
+  for (int t = 0; t < TPW; ++t) aw[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float xg[Z::KL], xx[Z::KL];
+  auto load = [&](int64_t r) {
+    const int64_t row = min(r * B32_ROWS + 16 * wv + i, M - 1);
+    load_row32<LD>(xg, Gm + (size_t)row * LD + f0);
+    load_row32<LD>(xx, Xm + (size_t)row * LD + f0);
+  };
+  auto stage = [&](float* B, const float (&v)[Z::KL], bool live) {
+    float* q = B + (16 * wv + i) * SLD + f0;
+#pragma unroll
+    for (int c = 0; c < Z::KC; ++c)
+      *reinterpret_cast<f32x4*>(q + 4 * c) =
+          live ? f32x4{v[4 * c], v[4 * c + 1], v[4 * c + 2], v[4 * c + 3]} : f32x4{0.f, 0.f, 0.f, 0.f};
+  };
+  int64_t r = blockIdx.x;
+  if (r < nr) load(r);
+  for (; r < nr; r += gridDim.x) {
+    const bool live = r * B32_ROWS + 16 * wv + i < M;
+    stage(st[0], xg, live);
+    stage(st[1], xx, live);
+    __syncthreads();
+    if (r + gridDim.x < nr) load(r + gridDim.x);
+    __builtin_amdgcn_sched_barrier(0);
+    // A[m][k] = G[row k][16 ob + m], B[k][n] = X[row k][16 nb + n], K = 4 rows
+    const float* pa = st[0] + g * SLD + 16 * ob0 + i;
+    const float* pb = st[1] + g * SLD + 16 * nb0 + i;
+#pragma unroll 2
+    for (int kk = 0; kk < B32_ROWS / 4; ++kk) {
+      float A[HB], B[HB];
+#pragma unroll
+      for (int u = 0; u < HB; ++u) {
+        A[u] = pa[4 * kk * SLD + 16 * u];
+        B[u] = pb[4 * kk * SLD + 16 * u];
+      }
+#pragma unroll
+      for (int u = 0; u < HB; ++u)
+#pragma unroll
+        for (int v = 0; v < HB; ++v)
+          aw[u * HB + v] = __builtin_amdgcn_mfma_f32_16x16x4f32(A[u], B[v], aw[u * HB + v], 0, 0, 0);
+    }
+    __syncthreads();
+  }
+  float* base = part.buf + (size_t)blockIdx.x * part.stride;
+#pragma unroll
+  for (int u = 0; u < HB; ++u)
+#pragma unroll
+    for (int v = 0; v < HB; ++v)
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        base[(size_t)(16 * (ob0 + u) + 4 * g + q) * LD + 16 * (nb0 + v) + i] = aw[u * HB + v][q];
 }
 
 // ========================================================= edge encoder
@@ -1089,7 +1179,9 @@ k_edge_enc_bwd_r32(int64_t E, const float* __restrict__ f_in, const float* __res
                    Partials part) {
   typedef R32<LD> Z;
   constexpr int SL = LD + 16;                 // staged row stride (floats)
-  constexpr int TPW = Z::NOB * Z::NOB / 4;    // dW2 tiles per wave
+  // wave wv owns the HB x HB block of dW2 tiles (ob0 + u, nb0 + v) and the
+  // db2 / dW1 | db1 columns of nones of its block row's HB output blocks
+  constexpr int HB = Z::NOB / 2, TPW = HB * HB;
   __shared__ __align__(16) EncBwd32Lds<LD> S;
   float* X = S.st[0];
   float* Y = S.st[1];
@@ -1097,6 +1189,8 @@ k_edge_enc_bwd_r32(int64_t E, const float* __restrict__ f_in, const float* __res
   const int tid = threadIdx.x, lane = tid & 63, i = lane & 15, g = lane >> 4;
   const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int f0 = Z::KL * g;
+  const int ob0 = HB * (wv >> 1), nb0 = HB * (wv & 1);
+  const int uones = (wv & 1) ? HB - HB / 2 : 0, nones = (wv & 1) ? HB / 2 : HB - HB / 2;
   stage_enc_vec<LD>(S.V, w, tid);
   __syncthreads();
 
@@ -1246,19 +1340,23 @@ k_edge_enc_bwd_r32(int64_t E, const float* __restrict__ f_in, const float* __res
     for (int kk = 0; kk < B32_ROWS / 4; ++kk) {
       const int rr = 4 * kk + g, r0 = rr * SL;
       const float fb = i < 8 ? S.fx[rr * 8 + i] : 0.f;  // [f, 1, 0...] of row rr, column i
+      float A[HB], B[HB];
 #pragma unroll
-      for (int t3 = 0; t3 < 3; ++t3) {
-        const int ob = wv + 4 * t3;
-        if (ob < Z::NOB) {
-          ab2[t3] = __builtin_amdgcn_mfma_f32_16x16x4f32(X[r0 + 16 * ob + i], 1.0f, ab2[t3], 0, 0, 0);
-          aw1[t3] = __builtin_amdgcn_mfma_f32_16x16x4f32(Z1[r0 + 16 * ob + i], fb, aw1[t3], 0, 0, 0);
+      for (int u = 0; u < HB; ++u) {
+        A[u] = X[r0 + 16 * (ob0 + u) + i];
+        B[u] = Y[r0 + 16 * (nb0 + u) + i];
+      }
+#pragma unroll
+      for (int t3 = 0; t3 < 3; ++t3)
+        if (t3 < nones) {
+          ab2[t3] = __builtin_amdgcn_mfma_f32_16x16x4f32(A[uones + t3], 1.0f, ab2[t3], 0, 0, 0);
+          aw1[t3] = __builtin_amdgcn_mfma_f32_16x16x4f32(Z1[r0 + 16 * (ob0 + uones + t3) + i], fb, aw1[t3], 0, 0, 0);
         }
-      }
 #pragma unroll
-      for (int tt = 0; tt < TPW; ++tt) {
-        const int T = TPW * wv + tt, ob = T / Z::NOB, nb = T % Z::NOB;
-        aw2[tt] = __builtin_amdgcn_mfma_f32_16x16x4f32(X[r0 + 16 * ob + i], Y[r0 + 16 * nb + i], aw2[tt], 0, 0, 0);
-      }
+      for (int u = 0; u < HB; ++u)
+#pragma unroll
+        for (int v = 0; v < HB; ++v)
+          aw2[u * HB + v] = __builtin_amdgcn_mfma_f32_16x16x4f32(A[u], B[v], aw2[u * HB + v], 0, 0, 0);
     }
   };
 
@@ -1277,15 +1375,16 @@ k_edge_enc_bwd_r32(int64_t E, const float* __restrict__ f_in, const float* __res
   constexpr int oW1 = 0, ob1 = EK * LD, oW2 = (EK + 1) * LD, ob2 = (EK + 1) * LD + LD * LD;
   constexpr int og = ob2 + LD, obt = og + LD;
 #pragma unroll
-  for (int tt = 0; tt < TPW; ++tt) {
-    const int T = TPW * wv + tt, ob = T / Z::NOB, nb = T % Z::NOB;
+  for (int u = 0; u < HB; ++u)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) base[oW2 + (size_t)(16 * ob + 4 * g + r) * LD + 16 * nb + i] = aw2[tt][r];
-  }
+    for (int v = 0; v < HB; ++v)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        base[oW2 + (size_t)(16 * (ob0 + u) + 4 * g + r) * LD + 16 * (nb0 + v) + i] = aw2[u * HB + v][r];
 #pragma unroll
   for (int t3 = 0; t3 < 3; ++t3) {
-    const int ob = wv + 4 * t3;
-    if (ob < Z::NOB)
+    const int ob = ob0 + uones + t3;
+    if (t3 < nones)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int f = 16 * ob + 4 * g + r;
@@ -1359,6 +1458,21 @@ hipError_t launch_edge_bwd_r32(int lat, const EdgeTiles& t, const void* e, const
   else
     hipLaunchKernelGGL(k_edge_bwd_r32, dim3(g), dim3(R32_NT), 0, s, t, (const float*)e, ebar_in, have_ebar,
                        ebar_out, (const float*)Pn, aggbar, w, eps, (float*)zbar, R, slots, part);
+  return hipGetLastError();
+}
+
+hipError_t launch_wgrad_r32(int lat, int64_t M, const float* G, const float* X, const Partials& part, int* nblocks,
+                            hipStream_t s) {
+  *nblocks = 0;
+  if (M <= 0) return hipSuccess;
+  if ((lat != B32_LD && lat != C32_LD) || part.stride < (int64_t)lat * lat) return hipErrorInvalidValue;
+  const int64_t need = (M + B32_ROWS - 1) / B32_ROWS;
+  const int g = (int)std::min<int64_t>(need, std::min(kRows32Blocks, part.max_blocks));
+  *nblocks = g;
+  if (lat == C32_LD)
+    hipLaunchKernelGGL(k_wgrad_r32<C32_LD>, dim3(g), dim3(R32_NT), 0, s, M, G, X, part);
+  else
+    hipLaunchKernelGGL(k_wgrad_r32<B32_LD>, dim3(g), dim3(R32_NT), 0, s, M, G, X, part);
   return hipGetLastError();
 }
 

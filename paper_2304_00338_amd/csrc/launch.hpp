@@ -97,9 +97,6 @@ hipError_t launch_edge_enc_r32(int lat, int64_t E, const float* f, const MlpW& w
                                hipStream_t s);
 hipError_t launch_edge_enc_bwd_r32(int lat, int64_t E, const float* f, const void* ebar, const MlpW& w, float eps,
                                    const Partials& part, int* nblocks, hipStream_t s);
-hipError_t launch_edge_fwd(int prec, int lat, const EdgeTiles& t, const void* e_in, void* e_out, int write_e,
-                           const void* P, const MlpW& w, float eps, float* agg, float* slots, void* a1_out,
-                           hipStream_t s);
 // bf16 edge forward with one wave per tile (uses MlpW::W1p / W2p); a1_out
 // (nullable) receives the first-layer activations of every edge.
 hipError_t launch_edge_fwd_rows(const EdgeTiles& t, const void* e_in, void* e_out, int write_e, const void* P,
@@ -201,14 +198,11 @@ hipError_t launch_decoder_bwd(int prec, int lat, int64_t N, const float* h, cons
 hipError_t launch_node_bwd(int prec, int lat, int64_t N, const float* h, const float* agg, const float* hbar_in,
                            const MlpW& w, float eps, float* hbar_part, float* aggbar, const Partials& part,
                            int* nblocks, hipStream_t s);
-hipError_t launch_edge_bwd(int prec, int lat, const EdgeTiles& t, const void* e, const float* ebar_in, int have_ebar,
-                           float* ebar_out, const void* P, const float* aggbar, const MlpW& w, float eps,
-                           void* zbar, float* R, float* slots, const Partials& part, int* nblocks,
-                           hipStream_t s);
-// dW[o][i] = sum_rows G[row][o] X[row][i] for [M][lat] operand-precision
-// streams, written as per-block [lat][lat] partials.
-hipError_t launch_wgrad(int prec, int lat, int64_t M, const void* G, const void* X, const Partials& part, int* nblocks,
-                        hipStream_t s);
+// dW[o][i] = sum_rows G[row][o] X[row][i] for fp32 [M][lat] streams (lat
+// 128 or 160), in the fp32 row layout, written as per-block [lat][lat]
+// partials.
+hipError_t launch_wgrad_r32(int lat, int64_t M, const float* G, const float* X, const Partials& part, int* nblocks,
+                            hipStream_t s);
 hipError_t launch_node_srcsum(int prec, int lat, int64_t N, const int32_t* rowptr, const int32_t* rev, const void* zbar,
                               const float* R, const float* h, const float* hbar_part, const MlpW& w,
                               float* hbar_out, const Partials& part, int* nblocks, hipStream_t s);
