@@ -90,10 +90,9 @@ k_edge_fwd_rows(EdgeTiles tl, const bf16* __restrict__ e_in, bf16* __restrict__ 
   if (t >= tend) return;
 
   const bf16x8 sel0 = select_frag(0, i, q), sel1 = select_frag(1, i, q);
-  const int4* tiles = reinterpret_cast<const int4*>(tl.tiles);
   auto desc = [&](int64_t tt) -> int4 {
     const bool ok = tt < tend;
-    const int4 v = tiles[ok ? tt : tend - 1];
+    const int4 v = tile_desc(tl.tiles, ok ? tt : tend - 1);
     int4 r;
     r.x = ok ? v.x : 0;
     r.y = ok ? v.y : 0;
@@ -377,11 +376,10 @@ k_edge_bwd_fused(EdgeTiles tl, const bf16* __restrict__ a1_in, const bf16* __res
   const bool row_wave = wv < FB_RW;
   const int k = row_wave ? wv : wv - FB_RW;  // the tile slot this wave follows
 
-  const int4* tiles = reinterpret_cast<const int4*>(tl.tiles);
   const int64_t tlast = max(tend - 1, (int64_t)0);
   auto desc = [&](int64_t tt) -> int4 {
     const bool ok = tt < tend;
-    const int4 v = tiles[ok ? tt : tlast];
+    const int4 v = tile_desc(tl.tiles, ok ? tt : tlast);
     int4 r;
     r.x = ok ? v.x : 0;
     r.y = ok ? v.y : 0;

@@ -62,6 +62,19 @@ __device__ __forceinline__ bf16x8 select_frag(int h, int i, int q) {
 // Rows of a receiver-aligned tile {node_begin, node_end | -1 - slot, edge_begin, edge_end}.
 __device__ __forceinline__ int tile_rows(int4 d) { return d.w - d.z; }
 
+// Descriptor t of the tile table.  The table is read-only while a kernel
+// runs, and a wave reads one descriptor at a time (t uniform): read through
+// the constant address space it becomes a scalar load, which the compiler
+// waits for with lgkmcnt.  As a vector load it was waited for with vmcnt,
+// and the kernels need its fields early as scalars, so that wait also
+// waited for the next half's streams requested before it.
+typedef int TileWords __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(4))) const TileWords ConstTileWords;
+__device__ __forceinline__ int4 tile_desc(const int32_t* tiles, int64_t t) {
+  const TileWords v = ((const ConstTileWords*)tiles)[t];
+  return make_int4(v.x, v.y, v.z, v.w);
+}
+
 __device__ __forceinline__ bf16x8 as_frag(const uint4& u) { return __builtin_bit_cast(bf16x8, u); }
 
 // B operand of run s from the two C-layout fragments of blocks 2s, 2s + 1.
