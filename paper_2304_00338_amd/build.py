@@ -19,7 +19,7 @@ BUILD = os.path.join(ROOT, "_build")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-HIP_SOURCES = ["fwd_kernels.hip", "edge_rows.hip", "edge_w160.hip", "node_rows.hip", "node_w160.hip", "enc_rows.hip", "enc_w160.hip", "train_kernels.hip", "bwd_kernels.hip", "misc_kernels.hip", "noalloc.hip", "edge_rows32.hip"]
+HIP_SOURCES = ["fwd_kernels.hip", "edge_rows.hip", "edge_w160.hip", "node_rows.hip", "node_w160.hip", "enc_rows.hip", "enc_w160.hip", "train_kernels.hip", "bwd_kernels.hip", "misc_kernels.hip", "noalloc.hip", "edge_rows32.hip", "node_rows32.hip"]
 HOST_SOURCES = ["graph.cpp", "api.cpp"]
 
 COMMON = ["-O3", "-fPIC", "-std=c++17", "-Wall", "-Wno-unused-function",

@@ -40,6 +40,9 @@ struct PackOff {
   int64_t F1 = -1, F2 = -1, F1t = -1, F2t = -1;  // fp32 edge MLPs (encoder: W2): fragment-major W1e, W2, transposes
   int64_t W1sp = -1, W1rp = -1;  // edge MLPs: row-permuted sender / receiver column blocks of W1
   int64_t W1ap = -1;             // node MLPs at width 160: row-permuted agg column block of W1
+  // fp32 row-layout node kernels: node MLPs' W1 agg block (F1: its h block),
+  // edge MLPs' W1 sender and receiver blocks, fragment-major and transposed
+  int64_t F1a = -1, F1at = -1, F1s = -1, F1r = -1, F1st = -1, F1rt = -1;
 };
 
 struct Model {
@@ -188,6 +191,16 @@ Model make_model(int m, int lat, bool fp32 = false) {
       add_frag(M, M.edge[i].W2, D, D, 2, M.p_edge[i].F2);
       add_frag(M, M.edge[i].W1, 3 * D, D, 3, M.p_edge[i].F1t);
       add_frag(M, M.edge[i].W2, D, D, 3, M.p_edge[i].F2t);
+      add_frag(M, M.edge[i].W1 + D, 3 * D, D, 2, M.p_edge[i].F1s);
+      add_frag(M, M.edge[i].W1 + 2 * D, 3 * D, D, 2, M.p_edge[i].F1r);
+      add_frag(M, M.edge[i].W1 + D, 3 * D, D, 3, M.p_edge[i].F1st);
+      add_frag(M, M.edge[i].W1 + 2 * D, 3 * D, D, 3, M.p_edge[i].F1rt);
+      add_frag(M, M.node[i].W1, 2 * D, D, 2, M.p_node[i].F1);
+      add_frag(M, M.node[i].W1 + D, 2 * D, D, 2, M.p_node[i].F1a);
+      add_frag(M, M.node[i].W2, D, D, 2, M.p_node[i].F2);
+      add_frag(M, M.node[i].W1, 2 * D, D, 3, M.p_node[i].F1t);
+      add_frag(M, M.node[i].W1 + D, 2 * D, D, 3, M.p_node[i].F1at);
+      add_frag(M, M.node[i].W2, D, D, 3, M.p_node[i].F2t);
     }
   }
   add_pack(M, M.dec.W1, D, D, M.p_dec.W1, M.p_dec.W1t);
@@ -509,6 +522,12 @@ struct Run {
     w.F2 = p.F2 >= 0 ? (const float*)P(p.F2) : nullptr;
     w.F1t = p.F1t >= 0 ? (const float*)P(p.F1t) : nullptr;
     w.F2t = p.F2t >= 0 ? (const float*)P(p.F2t) : nullptr;
+    w.F1a = p.F1a >= 0 ? (const float*)P(p.F1a) : nullptr;
+    w.F1at = p.F1at >= 0 ? (const float*)P(p.F1at) : nullptr;
+    w.F1s = p.F1s >= 0 ? (const float*)P(p.F1s) : nullptr;
+    w.F1r = p.F1r >= 0 ? (const float*)P(p.F1r) : nullptr;
+    w.F1st = p.F1st >= 0 ? (const float*)P(p.F1st) : nullptr;
+    w.F1rt = p.F1rt >= 0 ? (const float*)P(p.F1rt) : nullptr;
     w.W1f = params + o.W1;
     w.W2f = params + o.W2;
     w.b1 = params + o.b1;
@@ -591,8 +610,9 @@ struct Run {
         LAUNCH(K_NODE_FWD, launch_node_fwd_w160(N, h_l(k, l), agg_l(k, l), W(M.node[l], M.p_node[l]), eps, h_l(k, l + 1), s));
         if (!last) LAUNCH(K_EMIT, launch_emit_w160(N, h_l(k, l + 1), nx, P_l(k, l + 1), s));
       } else {
-        LAUNCH(K_NODE_FWD, launch_node_fwd(prec, D, N, h_l(k, l), agg_l(k, l), W(M.node[l], M.p_node[l]), last ? nullptr : &nx,
-                                eps, h_l(k, l + 1), last ? nullptr : P_l(k, l + 1), s));
+        LAUNCH(K_NODE_FWD, launch_node_fwd_r32(D, N, h_l(k, l), agg_l(k, l), W(M.node[l], M.p_node[l]),
+                                               last ? nullptr : &nx, eps, h_l(k, l + 1),
+                                               last ? nullptr : (float*)P_l(k, l + 1), s));
       }
     }
     LAUNCH(K_DECODER, launch_decoder(prec, D, N, h_l(k, m), W(M.dec, M.p_dec), out, s));

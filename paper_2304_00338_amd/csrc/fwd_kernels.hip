@@ -1,7 +1,6 @@
-// Forward kernels of one MGN call on gfx950 (Sec. 2.1 of the paper): weight
-// packing, the node encoder, the fused edge phase (gather -> edge MLP ->
-// LayerNorm -> residual -> deterministic receiver sum), the fused node phase
-// and the decoder.
+// Forward kernels of one MGN call on gfx950 (Sec. 2.1 of the paper) in the
+// feature-split layout: weight packing, the node encoder, the decoder and
+// the long-segment fixup of the receiver sums.
 //
 // The first edge-MLP layer acts on the concatenation [e, h_s, h_r]; it is
 // evaluated as W1e e + W1s h_s + W1r h_r, where the node products
@@ -147,66 +146,6 @@ __global__ void __launch_bounds__(LD) k_slot_fixup(const int32_t* __restrict__ l
   dst[(size_t)L.x * D + c] = s;
 }
 
-// ------------------------------------------------- fused node phase
-// h_out = h + LN(W2 relu(W1 [h, agg] + b1) + b2); optionally the next
-// block's node products P.
-template <int PREC, int LD, bool EMIT>
-__global__ void __launch_bounds__(LD * 4) k_node_fwd(int64_t N, const float* __restrict__ h_in, const float* __restrict__ agg,
-                                                 MlpW w, MlpW nx, float eps, float* __restrict__ h_out,
-                                                 typename Tr<PREC>::T* __restrict__ P_out) {
-  typedef Tr<PREC> P;
-  typedef typename P::T T;
-  constexpr int D = LD;
-  [[maybe_unused]] constexpr int NW = Width<LD>::NW, NT = Width<LD>::NT;
-  constexpr int LDT = D + P::PAD;
-  constexpr int LDX = 2 * D + P::PAD;
-  __shared__ __align__(16) T sX[TM * LDX];  // [h, agg]; later the new h
-  __shared__ __align__(16) T sA[TM * LDT];
-  __shared__ LnScratch<NW> ln;
-  const int tid = threadIdx.x, w8 = tid >> 6, lane = tid & 63, i = lane & 15, q = lane >> 4;
-  const int n = w8 * 16 + i;
-  const float b1 = w.b1[n], b2 = w.b2[n], gam = w.gamma[n], bet = w.beta[n];
-  const int64_t ntiles = (N + TM - 1) / TM;
-  for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
-    const int64_t r0 = t * TM;
-    const int nr = (int)min((int64_t)TM, N - r0);
-    stage_rows<D>(sX, LDX, h_in + (size_t)r0 * D, nr, tid);
-    stage_rows<D>(sX + D, LDX, agg + (size_t)r0 * D, nr, tid);
-    __syncthreads();
-    f32x4 acc[NRB];
-#pragma unroll
-    for (int rb = 0; rb < NRB; ++rb) acc[rb] = f32x4{b1, b1, b1, b1};
-    gemm_tile<PREC, 2 * D>(acc, sX, LDX, (const T*)w.W1, 2 * D, w8 * 16, 0, i, q);
-#pragma unroll
-    for (int rb = 0; rb < NRB; ++rb)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) sA[(rb * 16 + q * 4 + r) * LDT + n] = P::cvt(fmaxf(acc[rb][r], 0.f));
-    __syncthreads();
-#pragma unroll
-    for (int rb = 0; rb < NRB; ++rb) acc[rb] = f32x4{b2, b2, b2, b2};
-    gemm_tile<PREC, D>(acc, sA, LDT, (const T*)w.W2, D, w8 * 16, 0, i, q);
-    f32x4 mean[NRB], rstd[NRB];
-    ln_stats(acc, ln, eps, w8, i, q, mean, rstd);
-#pragma unroll
-    for (int rb = 0; rb < NRB; ++rb)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int row = rb * 16 + q * 4 + r;
-        float y = gam * ((acc[rb][r] - mean[rb][r]) * rstd[rb][r]) + bet;
-        if (row < nr) {
-          y += h_in[(size_t)(r0 + row) * D + n];
-          h_out[(size_t)(r0 + row) * D + n] = y;
-        }
-        if (EMIT) sX[row * LDX + n] = P::cvt(row < nr ? y : 0.f);
-      }
-    if (EMIT) {
-      __syncthreads();
-      emit_P<PREC, LD>(sX, LDX, nx, r0, nr, P_out, w8, i, q);
-    }
-    __syncthreads();
-  }
-}
-
 // ------------------------------------------------------------ decoder
 // out = W2 relu(W1 h + b1) + b2 (no LayerNorm); 4 outputs per node.
 template <int PREC, int LD>
@@ -305,25 +244,6 @@ hipError_t launch_slot_fixup(int lat, const int32_t* long_nodes, int64_t n_long,
                              hipStream_t s) {
   if (n_long <= 0) return hipSuccess;
 #define F(LD) hipLaunchKernelGGL(k_slot_fixup<LD>, dim3((unsigned)n_long), dim3(LD), 0, s, long_nodes, slots, dst)
-  MGN_BY_WIDTH(lat, F);
-#undef F
-  return hipGetLastError();
-}
-
-hipError_t launch_node_fwd(int prec, int lat, int64_t N, const float* h_in, const float* agg, const MlpW& w,
-                           const MlpW* nx, float eps, float* h_out, void* P_out, hipStream_t s) {
-  const int g = grid_for((N + TM - 1) / TM, kFwdBlocks);
-  if (!g) return hipSuccess;
-  const MlpW nn = nx ? *nx : w;
-  // bf16 runs on the row-layout kernels (launch_node_fwd_rows / _w160)
-  if (prec == MGN_BF16) return hipErrorInvalidValue;
-#define F(LD)                                                                                                        \
-  if (nx)                                                                                                            \
-    hipLaunchKernelGGL((k_node_fwd<MGN_FP32, LD, true>), dim3(g), dim3(LD * 4), 0, s, N, h_in, agg, w, nn, eps,      \
-                       h_out, (float*)P_out);                                                                        \
-  else                                                                                                               \
-    hipLaunchKernelGGL((k_node_fwd<MGN_FP32, LD, false>), dim3(g), dim3(LD * 4), 0, s, N, h_in, agg, w, nn, eps,     \
-                       h_out, (float*)P_out)
   MGN_BY_WIDTH(lat, F);
 #undef F
   return hipGetLastError();

@@ -22,8 +22,14 @@ struct MlpW {
   const void* W2t;
   const float* F1;   // fp32 row-layout kernels: fragment-major copies of the edge
   const float* F2;   // MLP's W1e (first layer, edge-latent block) and W2, and of
-  const float* F1t;  // their transposes
+  const float* F1t;  // their transposes (node MLPs: F1 is W1's h block)
   const float* F2t;
+  const float* F1a;   // fp32 node MLPs: fragment-major agg block of W1 and its transpose
+  const float* F1at;
+  const float* F1s;   // fp32 edge MLPs: fragment-major sender / receiver blocks of W1
+  const float* F1r;   // (the node products P = [W1s h, W1r h]) and their transposes
+  const float* F1st;
+  const float* F1rt;
   const float* W1f;  // float32 first-layer weights (encoders: K = 4 / 8 on VALU)
   const float* W2f;  // float32 second-layer weights (decoder: 4 outputs on VALU)
   const float* b1;
@@ -93,6 +99,12 @@ hipError_t launch_node_enc(int prec, int lat, int64_t N, const float* node_in, c
 // fragment-major W2 and, for the reverse, its transpose): e = LN(W2 relu(W1
 // f + b1) + b2), and all encoder parameter gradients from ebar as per-block
 // partials in the encoder's parameter order.
+// fp32 node phase in the row layout (width 128 or 160; needs the node MLP's
+// fragment-major F1, F1a, F2 and, with nx, the next edge MLP's F1s, F1r):
+// h_out = h + LN(W2 relu(W1 [h, agg] + b1) + b2), and with nx the next
+// block's node products P_out = [W1s h_out, W1r h_out] ([N][2 lat] fp32).
+hipError_t launch_node_fwd_r32(int lat, int64_t N, const float* h_in, const float* agg, const MlpW& w,
+                               const MlpW* nx, float eps, float* h_out, float* P_out, hipStream_t s);
 hipError_t launch_edge_enc_r32(int lat, int64_t E, const float* f, const MlpW& w, float eps, void* e_out,
                                hipStream_t s);
 hipError_t launch_edge_enc_bwd_r32(int lat, int64_t E, const float* f, const void* ebar, const MlpW& w, float eps,
@@ -189,8 +201,6 @@ hipError_t launch_node_enc_bwd_w160(int64_t N, const float* node_in, const float
                                     float* gin, const Partials& part, int* nblocks, hipStream_t s);
 hipError_t launch_slot_fixup(int lat, const int32_t* long_nodes, int64_t n_long, const float* slots, float* dst,
                              hipStream_t s);
-hipError_t launch_node_fwd(int prec, int lat, int64_t N, const float* h_in, const float* agg, const MlpW& w,
-                           const MlpW* next_edge, float eps, float* h_out, void* P_out, hipStream_t s);
 hipError_t launch_decoder(int prec, int lat, int64_t N, const float* h, const MlpW& w, float* out, hipStream_t s);
 
 hipError_t launch_decoder_bwd(int prec, int lat, int64_t N, const float* h, const float* gout, const MlpW& w,

@@ -1,0 +1,148 @@
+// Node phase of one MGN message-passing step in fp32 (Sec. 2.1: every node
+// latent is updated by the node MLP from itself and the sum of its incoming
+// edge messages, with LayerNorm and a residual), in the fp32 row layout of
+// rows32_common.hpp at kernel width LD = 128 or 160 (latent 150 padded with
+// zero columns): one wave per 16-node unit, the four lanes of a node holding
+// its contiguous row, every product on gemm32 from fragment-major weights.
+//
+// The first layer acts on the concatenation [h, agg]; it is evaluated as
+// (b1 + W1h h) + W1a agg with the two column blocks of W1 (the same linear
+// map, in this summation order in the forward and the reverse's recompute).
+#include "rows32_common.hpp"
+
+namespace mgn {
+namespace dev {
+
+// z1 = (b1 + W1h h) + W1a agg for the lane's features (the C layout of
+// gemm32: acc[ob][r] is feature f0 + 4 ob + r).  Shared by the forward and
+// the reverse, so the reverse's recompute equals the forward bitwise.
+template <int LD>
+__device__ __forceinline__ void node_z1_r32(f32x4 (&acc)[R32<LD>::NOB], const float (&h)[R32<LD>::KL],
+                                            const float (&a)[R32<LD>::KL], const MlpW& w, int f0, int lane,
+                                            int oz) {
+#pragma unroll
+  for (int ob = 0; ob < R32<LD>::NOB; ++ob) acc[ob] = *reinterpret_cast<const f32x4*>(w.b1 + f0 + 4 * ob);
+  gemm32<LD>(acc, h, w.F1 + oz, lane);
+  gemm32<LD>(acc, a, w.F1a + oz, lane);
+}
+
+// LayerNorm statistics of a row over its DR real features (padded features
+// hold 0 and are left out of the variance): acc becomes acc - mean.
+template <int LD>
+__device__ __forceinline__ float ln_center_r32(f32x4 (&acc)[R32<LD>::NOB], int f0, float eps) {
+  typedef R32<LD> Z;
+  float sm = 0.f;
+#pragma unroll
+  for (int ob = 0; ob < Z::NOB; ++ob)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) sm += acc[ob][r];
+  const float mean = sum_q(sm) * (1.0f / Z::DR);
+  float sq = 0.f;
+#pragma unroll
+  for (int ob = 0; ob < Z::NOB; ++ob)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float dlt = acc[ob][r] - mean;
+      acc[ob][r] = dlt;
+      if (Z::DR == LD || f0 + 4 * ob + r < Z::DR) sq += dlt * dlt;
+    }
+  return __builtin_amdgcn_rsqf(sum_q(sq) * (1.0f / Z::DR) + eps);
+}
+
+// Forward: h_out = h + LN(W2 relu(z1) + b2); with EMIT, also the next
+// block's node products P_out = [W1s h_out, W1r h_out] ([N][2 LD]) from the
+// next edge MLP nx.  The next unit's agg row is requested after the first
+// layer, its h row after the residual (single buffers: each is dead by
+// then); rows past N read row N - 1 and store nothing.
+template <int LD, bool EMIT>
+__global__ void __launch_bounds__(R32_NT) __attribute__((amdgpu_waves_per_eu(1, 1)))
+k_node_fwd_r32(int64_t N, const float* __restrict__ h_in, const float* __restrict__ agg, MlpW w, MlpW nx, float eps,
+               float* __restrict__ h_out, float* __restrict__ P_out) {
+  typedef R32<LD> Z;
+  const int tid = threadIdx.x, lane = tid & 63, i = lane & 15, g = lane >> 4;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int64_t nu = (N + 15) >> 4;
+  const UnitRange ur = unit_range<R32_NW>(nu, wv);
+  if (ur.t >= ur.end) return;
+  const int f0 = Z::KL * g;
+  auto rowp = [&](int64_t u) { return (size_t)min(u * 16 + i, N - 1) * LD + f0; };
+  float h[Z::KL], a[Z::KL];
+  load_row32<LD>(h, h_in + rowp(ur.t));
+  load_row32<LD>(a, agg + rowp(ur.t));
+  for (int64_t u = ur.t; u < ur.end; u += ur.stride) {
+    const int64_t un = u + ur.stride;
+    const bool live = u * 16 + i < N;
+    // the weight addresses are opaque per unit: otherwise the loop-invariant
+    // fragment loads are hoisted out of the loop into registers
+    const int oz = opaque_zero();
+    f32x4 acc[Z::NOB];
+    node_z1_r32<LD>(acc, h, a, w, f0, lane, oz);
+    load_row32<LD>(a, agg + rowp(un));
+    float a1[Z::KL];
+#pragma unroll
+    for (int ob = 0; ob < Z::NOB; ++ob)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) a1[4 * ob + r] = relu(acc[ob][r]);
+#pragma unroll
+    for (int ob = 0; ob < Z::NOB; ++ob) acc[ob] = *reinterpret_cast<const f32x4*>(w.b2 + f0 + 4 * ob);
+    gemm32<LD>(acc, a1, w.F2 + oz, lane);
+    const float rstd = ln_center_r32<LD>(acc, f0, eps);
+    float y[Z::KL];
+#pragma unroll
+    for (int ob = 0; ob < Z::NOB; ++ob) {
+      const f32x4 ga = *reinterpret_cast<const f32x4*>(w.gamma + f0 + 4 * ob);
+      const f32x4 be = *reinterpret_cast<const f32x4*>(w.beta + f0 + 4 * ob);
+      const f32x4 m = ga * (acc[ob] * rstd) + be;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) y[4 * ob + r] = m[r] + h[4 * ob + r];
+    }
+    if (live) {
+      float* p = h_out + (size_t)(u * 16 + i) * LD + f0;
+#pragma unroll
+      for (int c = 0; c < Z::KC; ++c)
+        *reinterpret_cast<f32x4*>(p + 4 * c) = f32x4{y[4 * c], y[4 * c + 1], y[4 * c + 2], y[4 * c + 3]};
+    }
+    load_row32<LD>(h, h_in + rowp(un));
+    if (EMIT) {
+      f32x4 ps[Z::NOB];
+#pragma unroll
+      for (int ob = 0; ob < Z::NOB; ++ob) acc[ob] = ps[ob] = f32x4{0.f, 0.f, 0.f, 0.f};
+      gemm32<LD>(ps, y, nx.F1s + oz, lane);
+      gemm32<LD>(acc, y, nx.F1r + oz, lane);
+      if (live) {
+        float* p = P_out + (size_t)(u * 16 + i) * (2 * LD) + f0;
+        store_row32<LD>(p, ps);
+        store_row32<LD>(p + LD, acc);
+      }
+    }
+  }
+}
+
+}  // namespace dev
+
+using namespace dev;
+
+static constexpr int kNodeRows32Blocks = 256;
+
+hipError_t launch_node_fwd_r32(int lat, int64_t N, const float* h_in, const float* agg, const MlpW& w,
+                               const MlpW* nx, float eps, float* h_out, float* P_out, hipStream_t s) {
+  if (N <= 0) return hipSuccess;
+  if ((lat != 128 && lat != 160) || !w.F1 || !w.F1a || !w.F2 || (nx && (!nx->F1s || !nx->F1r || !P_out)))
+    return hipErrorInvalidValue;
+  const int64_t need = ((N + 15) / 16 + R32_NW - 1) / R32_NW;
+  int g = (int)std::min<int64_t>(need, kNodeRows32Blocks);
+  if (g >= 8) g &= ~7;
+  const MlpW nn = nx ? *nx : w;
+#define F(L)                                                                                                     \
+  if (nx)                                                                                                        \
+    hipLaunchKernelGGL((k_node_fwd_r32<L, true>), dim3(g), dim3(R32_NT), 0, s, N, h_in, agg, w, nn, eps, h_out, \
+                       P_out);                                                                                   \
+  else                                                                                                           \
+    hipLaunchKernelGGL((k_node_fwd_r32<L, false>), dim3(g), dim3(R32_NT), 0, s, N, h_in, agg, w, nn, eps, h_out, \
+                       P_out)
+  MGN_BY_WIDTH(lat, F);
+#undef F
+  return hipGetLastError();
+}
+
+}  // namespace mgn
