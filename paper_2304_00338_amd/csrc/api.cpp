@@ -415,9 +415,9 @@ void plan(Ctx& c) {
     o = al256(o + (size_t)E * D * c.se);
     L.dz = o;  // dz2 of the width-160 edge backward (the 128-wide one keeps it on chip)
     o = al256(o + (keep_a1 && !rows ? (size_t)E * D * 2 : 0));
-    // bf16 node backward: the a1, dz2, dz1 streams of one node MLP
+    // node backward: the a1, dz2, dz1 streams of one node MLP (bf16 / fp32)
     L.nstr = o;
-    o = al256(o + (keep_a1 ? (size_t)3 * N * D * 2 : 0));
+    o = al256(o + (size_t)3 * N * D * (bf ? 2 : 4));
     L.hb_a = o;
     o = al256(o + (size_t)N * D * 4);
     L.hb_b = o;
@@ -683,9 +683,25 @@ struct Run {
           LAUNCH(K_WGRAD_NODE, launch_wgrad_node_w160(N, h_l(k, l), agg_l(k, l), ndz1, ndz2, na1, P1, &nb, s));
         if ((rc = job(nb, 1, 0, 1, (int)gpart, grad, on.W1, 0)) != MGN_OK) return rc;
       } else {
-        LAUNCH(K_NODE_BWD, launch_node_bwd(prec, D, N, h_l(k, l), agg_l(k, l), hb_cur, W(on, M.p_node[l]), eps, hb_part, aggbar,
-                                P0, &nb, s));
-        if ((rc = job(nb, 0, 0, 1, (int)on.size, grad, on.W1, 0)) != MGN_OK) return rc;
+        // fp32: the row-layout reverse (db1, db2, dgamma, dbeta as its
+        // partials), then the weight gradients from its a1 / dz2 / dz1
+        // streams: dW1 by its h and agg column blocks, and dW2
+        float* ns = (float*)(ws + c.L.nstr);
+        const size_t nd = (size_t)N * D;
+        LAUNCH(K_NODE_BWD, launch_node_bwd_r32(D, N, h_l(k, l), agg_l(k, l), hb_cur, W(on, M.p_node[l]), eps,
+                                               hb_part, aggbar, ns, P0, &nb, s));
+        if ((rc = job(nb, 0, 0, 1, D, grad, on.b1, 0)) != MGN_OK) return rc;
+        if ((rc = job(nb, 0, D, 1, D, grad, on.b2, 0)) != MGN_OK) return rc;
+        if ((rc = job(nb, 0, 2 * D, 1, 2 * D, grad, on.g, 0)) != MGN_OK) return rc;
+        Partials q = P1;
+        LAUNCH(K_WGRAD_NODE, launch_wgrad_r32(D, N, ns + 2 * nd, h_l(k, l), q, &nb, s));
+        if ((rc = job(nb, 1, 0, D, D, grad, on.W1, 2 * D)) != MGN_OK) return rc;
+        q.buf += (size_t)D * D;
+        LAUNCH(K_WGRAD_NODE, launch_wgrad_r32(D, N, ns + 2 * nd, agg_l(k, l), q, &nb, s));
+        if ((rc = job(nb, 1, (int64_t)D * D, D, D, grad, on.W1 + D, 2 * D)) != MGN_OK) return rc;
+        q.buf += (size_t)D * D;
+        LAUNCH(K_WGRAD_NODE, launch_wgrad_r32(D, N, ns + nd, ns, q, &nb, s));
+        if ((rc = job(nb, 1, 2 * (int64_t)D * D, D, D, grad, on.W2, D)) != MGN_OK) return rc;
       }
       if (E == 0) {
         // no edges: the edge MLP gets no gradient and every R is zero

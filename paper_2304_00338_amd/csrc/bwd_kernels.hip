@@ -1,5 +1,6 @@
-// Reverse-mode kernels of one MGN call on gfx950: decoder, node phase, edge
-// phase, sender-side sums and encoders.  Activations inside each MLP are
+// Reverse-mode kernels of one MGN call on gfx950 in the feature-split
+// layout: decoder, sender-side sums, the node encoder and the reduction of
+// the per-block partials.  Activations inside each MLP are
 // recomputed from the saved block inputs (edge latents, node latents,
 // aggregates and node products).  Weight gradients are accumulated per
 // persistent block in registers and written as per-block partials, which
@@ -110,124 +111,6 @@ __global__ void __launch_bounds__(LD * 4) k_decoder_bwd(int64_t N, const float* 
 #pragma unroll
   for (int o = 0; o < 4; ++o) put_col(base + D * D + D + o * D + n, dW2[o], q);
   if (tid < 4) base[D * D + 5 * D + tid] = db2;
-}
-
-// --------------------------------------------------------- node phase
-// Given hbar_in = dL/dh_out for h_out = h + LN(MLP([h, agg])):
-// hbar_part = hbar_in + dL/dh through the MLP, aggbar = dL/dagg.
-template <int PREC, int LD>
-__global__ void __launch_bounds__(LD * 4) k_node_bwd(int64_t N, const float* __restrict__ h, const float* __restrict__ agg,
-                                                 const float* __restrict__ hbar_in, MlpW w, float eps,
-                                                 float* __restrict__ hbar_part, float* __restrict__ aggbar,
-                                                 Partials part) {
-  typedef Tr<PREC> P;
-  typedef typename P::T T;
-  constexpr int D = LD;
-  [[maybe_unused]] constexpr int NW = Width<LD>::NW, NT = Width<LD>::NT;
-  constexpr int NCB = D / 16;
-  constexpr int LDT = D + P::PAD;
-  constexpr int LDX = 2 * D + P::PAD;
-  __shared__ __align__(16) T sX[TM * LDX];
-  __shared__ __align__(16) T sA[TM * LDT];
-  __shared__ __align__(16) T sG[TM * LDT];
-  __shared__ LnScratch<NW> ln;
-  const int tid = threadIdx.x, w8 = tid >> 6, lane = tid & 63, i = lane & 15, q = lane >> 4;
-  const int n = w8 * 16 + i;
-  const float b1 = w.b1[n], b2 = w.b2[n], gam = w.gamma[n];
-  f32x4 dW1[2 * NCB], dW2[NCB];
-#pragma unroll
-  for (int cb = 0; cb < 2 * NCB; ++cb) dW1[cb] = zero4();
-#pragma unroll
-  for (int cb = 0; cb < NCB; ++cb) dW2[cb] = zero4();
-  float db1 = 0.f, db2 = 0.f, dg = 0.f, dbt = 0.f;
-  const int64_t ntiles = (N + TM - 1) / TM;
-  for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
-    const int64_t r0 = t * TM;
-    const int nr = (int)min((int64_t)TM, N - r0);
-    stage_rows<D>(sX, LDX, h + (size_t)r0 * D, nr, tid);
-    stage_rows<D>(sX + D, LDX, agg + (size_t)r0 * D, nr, tid);
-    __syncthreads();
-    f32x4 acc[NRB];
-#pragma unroll
-    for (int rb = 0; rb < NRB; ++rb) acc[rb] = f32x4{b1, b1, b1, b1};
-    gemm_tile<PREC, 2 * D>(acc, sX, LDX, (const T*)w.W1, 2 * D, w8 * 16, 0, i, q);
-    uint32_t mask = 0;
-#pragma unroll
-    for (int rb = 0; rb < NRB; ++rb)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        if (acc[rb][r] > 0.f) mask |= 1u << (rb * 4 + r);
-        sA[(rb * 16 + q * 4 + r) * LDT + n] = P::cvt(fmaxf(acc[rb][r], 0.f));
-      }
-    __syncthreads();
-#pragma unroll
-    for (int rb = 0; rb < NRB; ++rb) acc[rb] = f32x4{b2, b2, b2, b2};
-    gemm_tile<PREC, D>(acc, sA, LDT, (const T*)w.W2, D, w8 * 16, 0, i, q);
-    f32x4 mean[NRB], rstd[NRB], xh[NRB], yb[NRB];
-    ln_stats(acc, ln, eps, w8, i, q, mean, rstd);
-#pragma unroll
-    for (int rb = 0; rb < NRB; ++rb)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int row = rb * 16 + q * 4 + r;
-        xh[rb][r] = (acc[rb][r] - mean[rb][r]) * rstd[rb][r];
-        yb[rb][r] = row < nr ? hbar_in[(size_t)(r0 + row) * D + n] : 0.f;
-        dg += yb[rb][r] * xh[rb][r];
-        dbt += yb[rb][r];
-      }
-    f32x4 g[NRB];
-    ln_bwd(g, yb, xh, rstd, gam, ln, w8, i, q);
-#pragma unroll
-    for (int rb = 0; rb < NRB; ++rb)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        db2 += g[rb][r];
-        sG[(rb * 16 + q * 4 + r) * LDT + n] = P::cvt(g[rb][r]);
-      }
-    gtx<PREC, NCB>(dW2, g, sA, LDT, 0, i, q);
-    __syncthreads();
-#pragma unroll
-    for (int rb = 0; rb < NRB; ++rb) acc[rb] = zero4();
-    gemm_tile<PREC, D>(acc, sG, LDT, (const T*)w.W2t, D, w8 * 16, 0, i, q);
-#pragma unroll
-    for (int rb = 0; rb < NRB; ++rb)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        g[rb][r] = (mask >> (rb * 4 + r)) & 1u ? acc[rb][r] : 0.f;
-        db1 += g[rb][r];
-      }
-    gtx<PREC, 2 * NCB>(dW1, g, sX, LDX, 0, i, q);
-    __syncthreads();
-#pragma unroll
-    for (int rb = 0; rb < NRB; ++rb)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) sG[(rb * 16 + q * 4 + r) * LDT + n] = P::cvt(g[rb][r]);
-    __syncthreads();
-    f32x4 xa[NRB];
-#pragma unroll
-    for (int rb = 0; rb < NRB; ++rb) acc[rb] = xa[rb] = zero4();
-    gemm_tile<PREC, D>(acc, sG, LDT, (const T*)w.W1t, D, w8 * 16, 0, i, q);
-    gemm_tile<PREC, D>(xa, sG, LDT, (const T*)w.W1t, D, D + w8 * 16, 0, i, q);
-#pragma unroll
-    for (int rb = 0; rb < NRB; ++rb)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int row = rb * 16 + q * 4 + r;
-        if (row < nr) {
-          hbar_part[(size_t)(r0 + row) * D + n] = yb[rb][r] + acc[rb][r];
-          aggbar[(size_t)(r0 + row) * D + n] = xa[rb][r];
-        }
-      }
-    __syncthreads();
-  }
-  float* base = part.buf + (size_t)blockIdx.x * part.stride;
-  // node-MLP parameter order: W1 [D][2D], b1, W2 [D][D], b2, gamma, beta
-  put_w<2 * NCB>(base, 2 * D, dW1, w8, i, q);
-  put_col(base + 2 * D * D + n, db1, q);
-  put_w<NCB>(base + 2 * D * D + D, D, dW2, w8, i, q);
-  put_col(base + 3 * D * D + D + n, db2, q);
-  put_col(base + 3 * D * D + 2 * D + n, dg, q);
-  put_col(base + 3 * D * D + 3 * D + n, dbt, q);
 }
 
 // 8 consecutive elements of a row as one (bf16) or two (fp32) 16-byte loads.
@@ -574,22 +457,6 @@ hipError_t launch_decoder_bwd(int prec, int lat, int64_t N, const float* h, cons
     MGN_BY_WIDTH(lat, F);
 #undef F
   }
-  return hipGetLastError();
-}
-
-hipError_t launch_node_bwd(int prec, int lat, int64_t N, const float* h, const float* agg, const float* hbar_in,
-                           const MlpW& w, float eps, float* hbar_part, float* aggbar, const Partials& part,
-                           int* nblocks, hipStream_t s) {
-  const int g = bwd_grid((N + TM - 1) / TM, part);
-  *nblocks = g;
-  if (!g) return hipSuccess;
-  // bf16 runs on the row-layout kernels (launch_node_bwd_rows / _w160)
-  if (prec == MGN_BF16) return hipErrorInvalidValue;
-#define F(LD)                                                                                                         \
-  hipLaunchKernelGGL((k_node_bwd<MGN_FP32, LD>), dim3(g), dim3(LD * 4), 0, s, N, h, agg, hbar_in, w, eps, hbar_part, \
-                     aggbar, part)
-  MGN_BY_WIDTH(lat, F);
-#undef F
   return hipGetLastError();
 }
 

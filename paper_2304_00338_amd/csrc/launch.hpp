@@ -105,6 +105,13 @@ hipError_t launch_node_enc(int prec, int lat, int64_t N, const float* node_in, c
 // block's node products P_out = [W1s h_out, W1r h_out] ([N][2 lat] fp32).
 hipError_t launch_node_fwd_r32(int lat, int64_t N, const float* h_in, const float* agg, const MlpW& w,
                                const MlpW* nx, float eps, float* h_out, float* P_out, hipStream_t s);
+// Its reverse: hbar_part = hbar_in + W1h^T dz1, aggbar = W1a^T dz1, the
+// rows of a1, dz2, dz1 into streams ([3][N][lat] fp32, for the weight
+// gradients by launch_wgrad_r32), and per-block [4][lat] partials of db1,
+// db2, dgamma, dbeta (needs F1t, F1at, F2t too).
+hipError_t launch_node_bwd_r32(int lat, int64_t N, const float* h, const float* agg, const float* hbar_in,
+                               const MlpW& w, float eps, float* hbar_part, float* aggbar, float* streams,
+                               const Partials& part, int* nblocks, hipStream_t s);
 hipError_t launch_edge_enc_r32(int lat, int64_t E, const float* f, const MlpW& w, float eps, void* e_out,
                                hipStream_t s);
 hipError_t launch_edge_enc_bwd_r32(int lat, int64_t E, const float* f, const void* ebar, const MlpW& w, float eps,
@@ -205,9 +212,6 @@ hipError_t launch_decoder(int prec, int lat, int64_t N, const float* h, const Ml
 
 hipError_t launch_decoder_bwd(int prec, int lat, int64_t N, const float* h, const float* gout, const MlpW& w,
                               float* hbar, const Partials& part, int* nblocks, hipStream_t s);
-hipError_t launch_node_bwd(int prec, int lat, int64_t N, const float* h, const float* agg, const float* hbar_in,
-                           const MlpW& w, float eps, float* hbar_part, float* aggbar, const Partials& part,
-                           int* nblocks, hipStream_t s);
 // dW[o][i] = sum_rows G[row][o] X[row][i] for fp32 [M][lat] streams (lat
 // 128 or 160), in the fp32 row layout, written as per-block [lat][lat]
 // partials.

@@ -118,6 +118,150 @@ k_node_fwd_r32(int64_t N, const float* __restrict__ h_in, const float* __restric
   }
 }
 
+// Reverse of the node phase for the rows of hbar_in = dL/dh_out: the
+// forward recomputed (z1 bitwise as in the forward), the LayerNorm reverse
+// (padded features of dz2 zeroed), da1 = W2^T dz2, dz1 = da1 where z1 > 0,
+// hbar_part = hbar_in + W1h^T dz1 and aggbar = W1a^T dz1.  The rows of a1,
+// dz2 and dz1 go to the streams (fp32 [N][LD] each) for the weight-gradient
+// passes (dW1 = sum dz1^T [h, agg], dW2 = sum dz2^T a1); db1, db2, dgamma
+// and dbeta are DPP column sums, written per block as [4][LD] partials (db1,
+// db2, dgamma, dbeta).  Each input row is requested again for the next unit
+// once its last use is issued.
+template <int LD>
+__global__ void __launch_bounds__(R32_NT) __attribute__((amdgpu_waves_per_eu(1, 1)))
+k_node_bwd_r32(int64_t N, const float* __restrict__ h_in, const float* __restrict__ agg,
+               const float* __restrict__ hbar_in, MlpW w, float eps, float* __restrict__ hbar_part,
+               float* __restrict__ aggbar, float* __restrict__ a1s, float* __restrict__ dz2s,
+               float* __restrict__ dz1s, Partials part) {
+  typedef R32<LD> Z;
+  __shared__ __align__(16) float red[4][R32_NW][LD];
+  const int tid = threadIdx.x, lane = tid & 63, i = lane & 15, g = lane >> 4;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int64_t nu = (N + 15) >> 4;
+  const UnitRange ur = unit_range<R32_NW>(nu, wv);
+  const int f0 = Z::KL * g;
+  ColSum32<LD> cs[4];  // db1, db2, dgamma, dbeta
+  if (ur.t < ur.end) {
+    auto rowp = [&](int64_t u) { return (size_t)min(u * 16 + i, N - 1) * LD + f0; };
+    float h[Z::KL], a[Z::KL], yb[Z::KL];
+    load_row32<LD>(h, h_in + rowp(ur.t));
+    load_row32<LD>(a, agg + rowp(ur.t));
+    load_row32<LD>(yb, hbar_in + rowp(ur.t));
+    for (int64_t u = ur.t; u < ur.end; u += ur.stride) {
+      const int64_t un = u + ur.stride;
+      const bool live = u * 16 + i < N;
+      const size_t orow = (size_t)(u * 16 + i) * LD + f0;
+      const int oz = opaque_zero();
+      // ---- the forward: z1, its ReLU mask, a1, z2 and its LayerNorm
+      f32x4 acc[Z::NOB];
+      node_z1_r32<LD>(acc, h, a, w, f0, lane, oz);
+      load_row32<LD>(h, h_in + rowp(un));
+      load_row32<LD>(a, agg + rowp(un));
+      float a1[Z::KL];
+      uint64_t mask = 0;
+#pragma unroll
+      for (int ob = 0; ob < Z::NOB; ++ob)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          a1[4 * ob + r] = relu(acc[ob][r]);
+          if (acc[ob][r] > 0.f) mask |= 1ull << (4 * ob + r);
+        }
+      if (live) {
+        float* p = a1s + orow;
+#pragma unroll
+        for (int c = 0; c < Z::KC; ++c)
+          *reinterpret_cast<f32x4*>(p + 4 * c) = f32x4{a1[4 * c], a1[4 * c + 1], a1[4 * c + 2], a1[4 * c + 3]};
+      }
+#pragma unroll
+      for (int ob = 0; ob < Z::NOB; ++ob) acc[ob] = *reinterpret_cast<const f32x4*>(w.b2 + f0 + 4 * ob);
+      gemm32<LD>(acc, a1, w.F2 + oz, lane);
+      const float rstd = ln_center_r32<LD>(acc, f0, eps);
+#pragma unroll
+      for (int ob = 0; ob < Z::NOB; ++ob) acc[ob] *= rstd;  // xhat
+      // ---- dbeta, dgamma (live rows); the LayerNorm reverse
+      f32x4 t[Z::NOB];
+      {
+        f32x4 p[Z::NOB];
+#pragma unroll
+        for (int ob = 0; ob < Z::NOB; ++ob) {
+          t[ob] = f32x4{yb[4 * ob], yb[4 * ob + 1], yb[4 * ob + 2], yb[4 * ob + 3]};
+          p[ob] = live ? t[ob] : f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+        cs[3].add(p, i);
+#pragma unroll
+        for (int ob = 0; ob < Z::NOB; ++ob) p[ob] = live ? t[ob] * acc[ob] : f32x4{0.f, 0.f, 0.f, 0.f};
+        cs[2].add(p, i);
+      }
+      float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+      for (int ob = 0; ob < Z::NOB; ++ob) {
+        t[ob] *= *reinterpret_cast<const f32x4*>(w.gamma + f0 + 4 * ob);  // dxh
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          s1 += t[ob][r];
+          s2 += t[ob][r] * acc[ob][r];
+        }
+      }
+      const float m1 = sum_q(s1) * (1.0f / Z::DR), m2 = sum_q(s2) * (1.0f / Z::DR);
+      float dz[Z::KL];
+#pragma unroll
+      for (int ob = 0; ob < Z::NOB; ++ob)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          dz[4 * ob + r] = (Z::DR == LD || f0 + 4 * ob + r < Z::DR) ? rstd * (t[ob][r] - m1 - acc[ob][r] * m2) : 0.f;
+      {
+        f32x4 p[Z::NOB];
+#pragma unroll
+        for (int ob = 0; ob < Z::NOB; ++ob)
+          p[ob] = live ? f32x4{dz[4 * ob], dz[4 * ob + 1], dz[4 * ob + 2], dz[4 * ob + 3]} : f32x4{0.f, 0.f, 0.f, 0.f};
+        cs[1].add(p, i);
+        if (live) store_row32<LD>(dz2s + orow, p);
+      }
+      // ---- da1 = W2^T dz2, dz1 = da1 where z1 > 0
+#pragma unroll
+      for (int ob = 0; ob < Z::NOB; ++ob) acc[ob] = f32x4{0.f, 0.f, 0.f, 0.f};
+      gemm32<LD>(acc, dz, w.F2t + oz, lane);
+      float d1[Z::KL];
+      {
+        f32x4 p[Z::NOB];
+#pragma unroll
+        for (int ob = 0; ob < Z::NOB; ++ob)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const float v = (mask >> (4 * ob + r)) & 1ull ? acc[ob][r] : 0.f;
+            d1[4 * ob + r] = v;
+            p[ob][r] = live ? v : 0.f;
+          }
+        cs[0].add(p, i);
+        if (live) store_row32<LD>(dz1s + orow, p);
+      }
+      // ---- hbar_part = hbar_in + W1h^T dz1, aggbar = W1a^T dz1
+#pragma unroll
+      for (int ob = 0; ob < Z::NOB; ++ob)
+        acc[ob] = f32x4{yb[4 * ob], yb[4 * ob + 1], yb[4 * ob + 2], yb[4 * ob + 3]};
+      gemm32<LD>(acc, d1, w.F1t + oz, lane);
+      if (live) store_row32<LD>(hbar_part + orow, acc);
+      load_row32<LD>(yb, hbar_in + rowp(un));
+#pragma unroll
+      for (int ob = 0; ob < Z::NOB; ++ob) acc[ob] = f32x4{0.f, 0.f, 0.f, 0.f};
+      gemm32<LD>(acc, d1, w.F1at + oz, lane);
+      if (live) store_row32<LD>(aggbar + orow, acc);
+    }
+  }
+  // ---- block partials [4][LD]: the waves' column sums added in wave order
+#pragma unroll
+  for (int k = 0; k < 4; ++k) cs[k].put(red[k][wv], f0, i);
+  __syncthreads();
+  float* base = part.buf + (size_t)blockIdx.x * part.stride;
+  for (int idx = tid; idx < 4 * LD; idx += R32_NT) {
+    const int k = idx / LD, c = idx % LD;
+    float v = 0.f;
+#pragma unroll
+    for (int u = 0; u < R32_NW; ++u) v += red[k][u][c];
+    base[idx] = v;
+  }
+}
+
 }  // namespace dev
 
 using namespace dev;
@@ -140,6 +284,29 @@ hipError_t launch_node_fwd_r32(int lat, int64_t N, const float* h_in, const floa
   else                                                                                                           \
     hipLaunchKernelGGL((k_node_fwd_r32<L, false>), dim3(g), dim3(R32_NT), 0, s, N, h_in, agg, w, nn, eps, h_out, \
                        P_out)
+  MGN_BY_WIDTH(lat, F);
+#undef F
+  return hipGetLastError();
+}
+
+hipError_t launch_node_bwd_r32(int lat, int64_t N, const float* h, const float* agg, const float* hbar_in,
+                               const MlpW& w, float eps, float* hbar_part, float* aggbar, float* streams,
+                               const Partials& part, int* nblocks, hipStream_t s) {
+  *nblocks = 0;
+  if (N <= 0) return hipSuccess;
+  if ((lat != 128 && lat != 160) || !w.F1 || !w.F1a || !w.F2 || !w.F1t || !w.F1at || !w.F2t ||
+      part.stride < 4LL * lat)
+    return hipErrorInvalidValue;
+  const int64_t need = ((N + 15) / 16 + R32_NW - 1) / R32_NW;
+  int g = (int)std::min<int64_t>(need, std::min(kNodeRows32Blocks, part.max_blocks));
+  if (g >= 8) g &= ~7;
+  *nblocks = g;
+  float* a1s = streams;
+  float* dz2s = streams + (size_t)N * lat;
+  float* dz1s = streams + (size_t)2 * N * lat;
+#define F(L)                                                                                                    \
+  hipLaunchKernelGGL(k_node_bwd_r32<L>, dim3(g), dim3(R32_NT), 0, s, N, h, agg, hbar_in, w, eps, hbar_part,     \
+                     aggbar, a1s, dz2s, dz1s, part)
   MGN_BY_WIDTH(lat, F);
 #undef F
   return hipGetLastError();

@@ -17,6 +17,7 @@
 #pragma once
 #include "launch.hpp"
 #include "rows_common.hpp"
+#include "w160_common.hpp"
 
 namespace mgn {
 namespace dev {
@@ -102,6 +103,35 @@ __device__ __forceinline__ void store_row32(float* __restrict__ p, const f32x4 (
 // busy on their own.
 constexpr int R32_NW = 4;
 constexpr int R32_NT = 64 * R32_NW;
+
+// Per-lane column sums over 16-row blocks of C-layout values (feature
+// f0 + 4 ob + r), accumulated block after block: DPP butterflies leave lane
+// i of group g with features f0 + 4 (i / 2) + 2 (i % 2) + {0, 1} of blocks
+// 0..7 (v) and, at width 160, one feature of blocks 8, 9 (t, lanes of even
+// i).  put() writes a wave's sums into its row of an LDS array [LD].
+template <int LD>
+struct ColSum32 {
+  float2 v = {0.f, 0.f};
+  float t = 0.f;
+  __device__ __forceinline__ void add(const f32x4 (&p)[R32<LD>::NOB], int i) {
+    f32x4 p8[8];
+#pragma unroll
+    for (int ob = 0; ob < 8; ++ob) p8[ob] = p[ob];
+    const float2 c = colsum16(p8, i);
+    v.x += c.x;
+    v.y += c.y;
+    if constexpr (R32<LD>::NOB == 10) t += w160::colsum16_tail(p, i);
+  }
+  __device__ __forceinline__ void put(float* row, int f0, int i) const {
+    *reinterpret_cast<float2*>(row + f0 + 4 * (i >> 1) + 2 * (i & 1)) = v;
+    if constexpr (R32<LD>::NOB == 10) {
+      if ((i & 1) == 0) {
+        const int k = (((i >> 3) & 1) << 2) | (((i >> 2) & 1) << 1) | ((i >> 1) & 1);
+        row[f0 + 4 * (8 + (k >> 2)) + (k & 3)] = t;
+      }
+    }
+  }
+};
 
 }  // namespace dev
 }  // namespace mgn
