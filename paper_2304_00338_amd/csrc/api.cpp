@@ -752,11 +752,26 @@ struct Run {
         // scratch (its streams are consumed by now) into the weight gradients
         LAUNCH(K_SRCSUM, launch_srcsum_w160(N, g.rowptr, g.rev, zbar, R, h_l(k, l), hb_part, W(oe, M.p_edge[l]), hb_cur,
                                             ws + c.L.nstr, P4, &nb, s));
-      else
+      else if (prec == MGN_FP32) {
+        // fp32: S into the node-stream scratch (its streams are consumed by
+        // now), then dW1s = sum S h^T and dW1r = sum R h^T from the rows
+        float* Sv = (float*)(ws + c.L.nstr);
+        LAUNCH(K_SRCSUM, launch_node_srcsum_r32(D, N, g.rowptr, g.rev, (const float*)zbar, R, hb_part,
+                                                W(oe, M.p_edge[l]), hb_cur, Sv, s));
+        Partials q = P4;
+        LAUNCH(K_SRCSUM, launch_wgrad_r32(D, N, Sv, h_l(k, l), q, &nb, s));
+        if ((rc = job(nb, 4, 0, D, D, grad, oe.W1 + D, 3 * D)) != MGN_OK) return rc;
+        q.buf += (size_t)D * D;
+        LAUNCH(K_SRCSUM, launch_wgrad_r32(D, N, R, h_l(k, l), q, &nb, s));
+        if ((rc = job(nb, 4, (int64_t)D * D, D, D, grad, oe.W1 + 2 * D, 3 * D)) != MGN_OK) return rc;
+      } else {
         LAUNCH(K_SRCSUM, launch_node_srcsum(prec, D, N, g.rowptr, g.rev, zbar, R, h_l(k, l), hb_part, W(oe, M.p_edge[l]),
                                             hb_cur, P4, &nb, s));
-      if ((rc = job(nb, 4, 0, D, D, grad, oe.W1 + D, 3 * D)) != MGN_OK) return rc;
-      if ((rc = job(nb, 4, (int64_t)D * D, D, D, grad, oe.W1 + 2 * D, 3 * D)) != MGN_OK) return rc;
+      }
+      if (prec != MGN_FP32) {
+        if ((rc = job(nb, 4, 0, D, D, grad, oe.W1 + D, 3 * D)) != MGN_OK) return rc;
+        if ((rc = job(nb, 4, (int64_t)D * D, D, D, grad, oe.W1 + 2 * D, 3 * D)) != MGN_OK) return rc;
+      }
       // the block's partial regions are reused by the next block
       if ((rc = flush(grad)) != MGN_OK) return rc;
     }

@@ -463,21 +463,15 @@ hipError_t launch_decoder_bwd(int prec, int lat, int64_t N, const float* h, cons
 hipError_t launch_node_srcsum(int prec, int lat, int64_t N, const int32_t* rowptr, const int32_t* rev,
                               const void* zbar, const float* R, const float* h, const float* hbar_part, const MlpW& w,
                               float* hbar_out, const Partials& part, int* nblocks, hipStream_t s) {
+  // bf16 at width 128 (fp32 runs on launch_node_srcsum_r32, bf16 at width
+  // 160 on launch_srcsum_w160)
+  *nblocks = 0;
+  if (prec != MGN_BF16 || lat != 128) return hipErrorInvalidValue;
   const int g = bwd_grid((N + TM - 1) / TM, part);
   *nblocks = g;
   if (!g) return hipSuccess;
-  if (prec == MGN_BF16) {
-    // width 160 runs on launch_srcsum_w160
-    if (lat != 128) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((k_node_srcsum<MGN_BF16, 128>), dim3(g), dim3(128 * 4), 0, s, N, rowptr, rev,
-                       (const bf16*)zbar, R, h, hbar_part, w, hbar_out, part);
-  } else {
-#define F(LD)                                                                                                       \
-  hipLaunchKernelGGL((k_node_srcsum<MGN_FP32, LD>), dim3(g), dim3(LD * 4), 0, s, N, rowptr, rev, (const float*)zbar, \
-                     R, h, hbar_part, w, hbar_out, part)
-    MGN_BY_WIDTH(lat, F);
-#undef F
-  }
+  hipLaunchKernelGGL((k_node_srcsum<MGN_BF16, 128>), dim3(g), dim3(128 * 4), 0, s, N, rowptr, rev, (const bf16*)zbar,
+                     R, h, hbar_part, w, hbar_out, part);
   return hipGetLastError();
 }
 

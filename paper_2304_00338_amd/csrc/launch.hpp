@@ -112,6 +112,12 @@ hipError_t launch_node_fwd_r32(int lat, int64_t N, const float* h_in, const floa
 hipError_t launch_node_bwd_r32(int lat, int64_t N, const float* h, const float* agg, const float* hbar_in,
                                const MlpW& w, float eps, float* hbar_part, float* aggbar, float* streams,
                                const Partials& part, int* nblocks, hipStream_t s);
+// fp32 sender-side sums in the row layout (needs the edge MLP's F1st, F1rt):
+// S = sum of zbar over each node's out-edges (through rev, in edge order)
+// into S_out ([N][lat]), hbar_out = hbar_part + W1s^T S + W1r^T R.
+hipError_t launch_node_srcsum_r32(int lat, int64_t N, const int32_t* rowptr, const int32_t* rev, const float* zbar,
+                                  const float* R, const float* hbar_part, const MlpW& w, float* hbar_out,
+                                  float* S_out, hipStream_t s);
 hipError_t launch_edge_enc_r32(int lat, int64_t E, const float* f, const MlpW& w, float eps, void* e_out,
                                hipStream_t s);
 hipError_t launch_edge_enc_bwd_r32(int lat, int64_t E, const float* f, const void* ebar, const MlpW& w, float eps,

@@ -262,6 +262,76 @@ k_node_bwd_r32(int64_t N, const float* __restrict__ h_in, const float* __restric
   }
 }
 
+
+// Sender-side sums and the node gradient through the edge MLP's sender and
+// receiver blocks: S_v = sum of zbar over the reverses of v's in-edges (the
+// out-edges of v), added in edge order; hbar_out = hbar_part + W1s^T S +
+// W1r^T R.  The rows of S go to S_out (fp32 [N][LD]) for the weight
+// gradients dW1s = sum S h^T, dW1r = sum R h^T.  Each lane gathers its KL
+// features of four edges' rows at a time; rows of an edge-less or a dead
+// node add nothing.
+template <int LD>
+__global__ void __launch_bounds__(R32_NT) __attribute__((amdgpu_waves_per_eu(1, 1)))
+k_node_srcsum_r32(int64_t N, const int32_t* __restrict__ rowptr, const int32_t* __restrict__ rev,
+                  const float* __restrict__ zbar, const float* __restrict__ R, const float* __restrict__ hbar_part,
+                  MlpW w, float* __restrict__ hbar_out, float* __restrict__ S_out) {
+  typedef R32<LD> Z;
+  constexpr int GE = 4;  // edges gathered at a time
+  const int tid = threadIdx.x, lane = tid & 63, i = lane & 15, g = lane >> 4;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int64_t nu = (N + 15) >> 4;
+  const UnitRange ur = unit_range<R32_NW>(nu, wv);
+  const int f0 = Z::KL * g;
+  for (int64_t u = ur.t; u < ur.end; u += ur.stride) {
+    const bool live = u * 16 + i < N;
+    const int64_t v = min(u * 16 + i, N - 1);
+    const size_t orow = (size_t)v * LD + f0;
+    const int e0 = rowptr[v], e1 = live ? rowptr[v + 1] : e0;
+    float hb[Z::KL], rr[Z::KL];
+    load_row32<LD>(hb, hbar_part + orow);
+    load_row32<LD>(rr, R + orow);
+    int md = e1 - e0;  // the unit's largest in-degree
+#pragma unroll
+    for (int o = 1; o < 16; o <<= 1) md = max(md, __shfl_xor(md, o));
+    float S[Z::KL];
+#pragma unroll
+    for (int c = 0; c < Z::KL; ++c) S[c] = 0.f;
+    for (int k0 = 0; k0 < md; k0 += GE) {
+      f32x4 x[GE][Z::KC];
+#pragma unroll
+      for (int k = 0; k < GE; ++k) {
+        const int e = e0 + k0 + k;
+        if (e < e1) {
+          const float* zp = zbar + (size_t)rev[e] * LD + f0;
+#pragma unroll
+          for (int c = 0; c < Z::KC; ++c) x[k][c] = *reinterpret_cast<const f32x4*>(zp + 4 * c);
+        }
+      }
+#pragma unroll
+      for (int k = 0; k < GE; ++k)
+        if (e0 + k0 + k < e1)
+#pragma unroll
+          for (int c = 0; c < Z::KC; ++c)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) S[4 * c + r] += x[k][c][r];
+    }
+    if (live) {
+      float* p = S_out + orow;
+#pragma unroll
+      for (int c = 0; c < Z::KC; ++c)
+        *reinterpret_cast<f32x4*>(p + 4 * c) = f32x4{S[4 * c], S[4 * c + 1], S[4 * c + 2], S[4 * c + 3]};
+    }
+    const int oz = opaque_zero();
+    f32x4 acc[Z::NOB];
+#pragma unroll
+    for (int ob = 0; ob < Z::NOB; ++ob)
+      acc[ob] = f32x4{hb[4 * ob], hb[4 * ob + 1], hb[4 * ob + 2], hb[4 * ob + 3]};
+    gemm32<LD>(acc, S, w.F1st + oz, lane);
+    gemm32<LD>(acc, rr, w.F1rt + oz, lane);
+    if (live) store_row32<LD>(hbar_out + orow, acc);
+  }
+}
+
 }  // namespace dev
 
 using namespace dev;
@@ -307,6 +377,22 @@ hipError_t launch_node_bwd_r32(int lat, int64_t N, const float* h, const float* 
 #define F(L)                                                                                                    \
   hipLaunchKernelGGL(k_node_bwd_r32<L>, dim3(g), dim3(R32_NT), 0, s, N, h, agg, hbar_in, w, eps, hbar_part,     \
                      aggbar, a1s, dz2s, dz1s, part)
+  MGN_BY_WIDTH(lat, F);
+#undef F
+  return hipGetLastError();
+}
+
+hipError_t launch_node_srcsum_r32(int lat, int64_t N, const int32_t* rowptr, const int32_t* rev, const float* zbar,
+                                  const float* R, const float* hbar_part, const MlpW& w, float* hbar_out,
+                                  float* S_out, hipStream_t s) {
+  if (N <= 0) return hipSuccess;
+  if ((lat != 128 && lat != 160) || !w.F1st || !w.F1rt) return hipErrorInvalidValue;
+  const int64_t need = ((N + 15) / 16 + R32_NW - 1) / R32_NW;
+  int g = (int)std::min<int64_t>(need, kNodeRows32Blocks);
+  if (g >= 8) g &= ~7;
+#define F(L)                                                                                                    \
+  hipLaunchKernelGGL(k_node_srcsum_r32<L>, dim3(g), dim3(R32_NT), 0, s, N, rowptr, rev, zbar, R, hbar_part, w, \
+                     hbar_out, S_out)
   MGN_BY_WIDTH(lat, F);
 #undef F
   return hipGetLastError();
