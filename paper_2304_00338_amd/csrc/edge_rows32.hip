@@ -223,6 +223,9 @@ constexpr int B32_ROWS = 16 * R32_NW;
 struct __attribute__((aligned(16))) Bwd32Lds {
   // staged streams of a round: 0 dz2, 1 a1, 2 e, 3 zbar
   __attribute__((aligned(16))) float st[4][B32_ROWS * B32_SLD];
+  // b1, b2, gamma: read per half from LDS, not L2 (the L2 reads, issued
+  // where they are used, left their latency exposed)
+  __attribute__((aligned(16))) float vec[3][B32_LD];
 };
 
 // in-segment sums of the staged zbar rows (as in seg_pass32, stride B32_SLD)
@@ -256,6 +259,12 @@ k_edge_bwd_r32(EdgeTiles tl, const float* __restrict__ e_in, const float* ebar_i
   const int tid = threadIdx.x, lane = tid & 63, i = lane & 15, g = lane >> 4;
   const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int f0 = Z::KL * g;
+  for (int idx = tid; idx < LD; idx += R32_NT) {
+    S.vec[0][idx] = w.b1[idx];
+    S.vec[1][idx] = w.b2[idx];
+    S.vec[2][idx] = w.gamma[idx];
+  }
+  __syncthreads();
 
   // The block's tiles: XCD-contiguous ranges, wave wv takes tile tb + wv of
   // every round pair; all four waves run the same number of rounds.
@@ -357,7 +366,7 @@ k_edge_bwd_r32(EdgeTiles tl, const float* __restrict__ e_in, const float* ebar_i
     {
 #pragma unroll
       for (int ob = 0; ob < Z::NOB; ++ob) {
-        const f32x4 b1 = *reinterpret_cast<const f32x4*>(w.b1 + f0 + 4 * ob);
+        const f32x4 b1 = *reinterpret_cast<const f32x4*>(S.vec[0] + f0 + 4 * ob);
         const f32x4 z = acc[ob] + ((b1 + pa[ob]) + pb[ob]);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
@@ -368,7 +377,7 @@ k_edge_bwd_r32(EdgeTiles tl, const float* __restrict__ e_in, const float* ebar_i
     }
     // ---- z2 = b2 + W2 a1 and its LayerNorm statistics
 #pragma unroll
-    for (int ob = 0; ob < Z::NOB; ++ob) acc[ob] = *reinterpret_cast<const f32x4*>(w.b2 + f0 + 4 * ob);
+    for (int ob = 0; ob < Z::NOB; ++ob) acc[ob] = *reinterpret_cast<const f32x4*>(S.vec[1] + f0 + 4 * ob);
     // the receiver's aggregate gradient, requested halfway through the product
     f32x4 ag[Z::NOB];
     gemm32<LD>(acc, a1, w.F2 + oz, lane, [&] {
@@ -397,7 +406,7 @@ k_edge_bwd_r32(EdgeTiles tl, const float* __restrict__ e_in, const float* ebar_i
       f32x4 pg[Z::NOB], pb[Z::NOB];
 #pragma unroll
       for (int ob = 0; ob < Z::NOB; ++ob) {
-        const f32x4 ga = *reinterpret_cast<const f32x4*>(w.gamma + f0 + 4 * ob);
+        const f32x4 ga = *reinterpret_cast<const f32x4*>(S.vec[2] + f0 + 4 * ob);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int s = 4 * ob + r;
@@ -560,6 +569,7 @@ constexpr int C32_TILES = C32_HB * C32_HB;
 
 struct __attribute__((aligned(16))) Bwd32wLds {
   __attribute__((aligned(16))) float st[3][B32_ROWS * C32_SLD];  // X, Y, Zs
+  __attribute__((aligned(16))) float vec[3][C32_LD];              // b1, b2, gamma (as at width 128)
 };
 
 // column sums over a half's 16 rows of 40 C-layout values (blocks 0..7 by
@@ -587,6 +597,12 @@ k_edge_bwd_r32w(EdgeTiles tl, const float* __restrict__ e_in, const float* ebar_
   const int tid = threadIdx.x, lane = tid & 63, i = lane & 15, g = lane >> 4;
   const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int f0 = Z::KL * g;
+  for (int idx = tid; idx < LD; idx += R32_NT) {
+    S.vec[0][idx] = w.b1[idx];
+    S.vec[1][idx] = w.b2[idx];
+    S.vec[2][idx] = w.gamma[idx];
+  }
+  __syncthreads();
   // this wave's block of dW2 tiles and the output blocks of its db2 ones
   // columns (the two waves of a block row split its five output blocks)
   const int ob0 = C32_HB * (wv >> 1), nb0 = C32_HB * (wv & 1);
@@ -673,7 +689,7 @@ k_edge_bwd_r32w(EdgeTiles tl, const float* __restrict__ e_in, const float* ebar_
     {
 #pragma unroll
       for (int ob = 0; ob < Z::NOB; ++ob) {
-        const f32x4 b1 = *reinterpret_cast<const f32x4*>(w.b1 + f0 + 4 * ob);
+        const f32x4 b1 = *reinterpret_cast<const f32x4*>(S.vec[0] + f0 + 4 * ob);
         const f32x4 z = acc[ob] + ((b1 + pa[ob]) + pb[ob]);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
@@ -686,7 +702,7 @@ k_edge_bwd_r32w(EdgeTiles tl, const float* __restrict__ e_in, const float* ebar_
     stage_row(Y, a1, live);
     // ---- z2 = b2 + W2 a1; LayerNorm statistics over the 150 real features
 #pragma unroll
-    for (int ob = 0; ob < Z::NOB; ++ob) acc[ob] = *reinterpret_cast<const f32x4*>(w.b2 + f0 + 4 * ob);
+    for (int ob = 0; ob < Z::NOB; ++ob) acc[ob] = *reinterpret_cast<const f32x4*>(S.vec[1] + f0 + 4 * ob);
     float eb[Z::KL];
     f32x4 ag[Z::NOB];
     gemm32<LD>(acc, a1, w.F2 + oz, lane, [&] {
@@ -734,7 +750,7 @@ k_edge_bwd_r32w(EdgeTiles tl, const float* __restrict__ e_in, const float* ebar_
     float s1 = 0.f, s2 = 0.f;
 #pragma unroll
     for (int ob = 0; ob < Z::NOB; ++ob) {
-      t[ob] *= *reinterpret_cast<const f32x4*>(w.gamma + f0 + 4 * ob);  // dxh
+      t[ob] *= *reinterpret_cast<const f32x4*>(S.vec[2] + f0 + 4 * ob);  // dxh
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         s1 += t[ob][r];
