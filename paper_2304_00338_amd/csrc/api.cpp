@@ -156,9 +156,11 @@ Model make_model(int m, int lat, bool fp32 = false) {
   add_pack(M, M.enc_edge.W2, D, D, M.p_enc_edge.W2, M.p_enc_edge.W2t);
   add_perm(M, M.enc_edge.W2, D, M.p_enc_edge.W2p, D, D);  // row-layout edge encoders
   if (fp32) {
-    // fp32 row-layout edge encoder: fragment-major W2 and its transpose
+    // fp32 row-layout encoders: fragment-major W2 and its transpose
     add_frag(M, M.enc_edge.W2, D, D, 2, M.p_enc_edge.F2);
     add_frag(M, M.enc_edge.W2, D, D, 3, M.p_enc_edge.F2t);
+    add_frag(M, M.enc_node.W2, D, D, 2, M.p_enc_node.F2);
+    add_frag(M, M.enc_node.W2, D, D, 3, M.p_enc_node.F2t);
   }
   M.p_edge.resize(m);
   M.p_node.resize(m);
@@ -204,6 +206,11 @@ Model make_model(int m, int lat, bool fp32 = false) {
     }
   }
   add_pack(M, M.dec.W1, D, D, M.p_dec.W1, M.p_dec.W1t);
+  if (fp32) {
+    // fp32 row-layout decoder: fragment-major W1 and its transpose
+    add_frag(M, M.dec.W1, D, D, 2, M.p_dec.F1);
+    add_frag(M, M.dec.W1, D, D, 3, M.p_dec.F1t);
+  }
   return M;
 }
 
@@ -575,8 +582,12 @@ struct Run {
     const EdgeTiles tl = tiles();
     MlpW e0;
     if (m > 0) e0 = W(M.edge[0], M.p_edge[0]);
-    LAUNCH(K_NODE_ENC, launch_node_enc(prec, D, N, node_in, W(M.enc_node, M.p_enc_node), m > 0 ? &e0 : nullptr, eps, h_l(k, 0),
-                            P_l(k, 0), s));
+    if (prec == MGN_FP32)
+      LAUNCH(K_NODE_ENC, launch_node_enc_r32(D, N, node_in, W(M.enc_node, M.p_enc_node), m > 0 ? &e0 : nullptr, eps,
+                                             h_l(k, 0), m > 0 ? (float*)P_l(k, 0) : nullptr, s));
+    else
+      LAUNCH(K_NODE_ENC, launch_node_enc(prec, D, N, node_in, W(M.enc_node, M.p_enc_node), m > 0 ? &e0 : nullptr, eps,
+                                         h_l(k, 0), P_l(k, 0), s));
     if (m > 0) {
       if (rows())
         LAUNCH(K_EDGE_ENC, launch_edge_enc_rows(E, efeat, W(M.enc_edge, M.p_enc_edge), eps, e_l(k, 0), s));
@@ -615,7 +626,8 @@ struct Run {
                                                last ? nullptr : (float*)P_l(k, l + 1), s));
       }
     }
-    LAUNCH(K_DECODER, launch_decoder(prec, D, N, h_l(k, m), W(M.dec, M.p_dec), out, s));
+    LAUNCH(K_DECODER, prec == MGN_FP32 ? launch_decoder_r32(D, N, h_l(k, m), W(M.dec, M.p_dec), out, s)
+                                       : launch_decoder(prec, D, N, h_l(k, m), W(M.dec, M.p_dec), out, s));
     return MGN_OK;
   }
 
@@ -659,8 +671,19 @@ struct Run {
     void* ebar = ws + c.L.ebar;  // the edge-latent element type
     void* zbar = ws + c.L.zbar;
     int nb = 0, rc;
-    LAUNCH(K_DECODER_BWD, launch_decoder_bwd(prec, D, N, h_l(k, m), gout, W(M.dec, M.p_dec), hb_cur, pt, &nb, s));
-    if ((rc = reduce(nb, 0, 1, (int)M.dec.size, grad, M.dec.W1, 0)) != MGN_OK) return rc;
+    if (prec == MGN_FP32) {
+      // fp32: the row-layout reverse (db1, dW2, db2 as its partials), then
+      // dW1 = sum dz1^T h from its dz1 rows (the node-stream scratch); each
+      // reduction runs before the next launch reuses the partial region
+      float* dz1 = (float*)(ws + c.L.nstr);
+      LAUNCH(K_DECODER_BWD, launch_decoder_bwd_r32(D, N, h_l(k, m), gout, W(M.dec, M.p_dec), hb_cur, dz1, pt, &nb, s));
+      if ((rc = reduce(nb, 0, 1, 5 * D + 4, grad, M.dec.b1, 0)) != MGN_OK) return rc;
+      LAUNCH(K_DECODER_BWD, launch_wgrad_r32(D, N, dz1, h_l(k, m), pt, &nb, s));
+      if ((rc = reduce(nb, 0, D, D, grad, M.dec.W1, D)) != MGN_OK) return rc;
+    } else {
+      LAUNCH(K_DECODER_BWD, launch_decoder_bwd(prec, D, N, h_l(k, m), gout, W(M.dec, M.p_dec), hb_cur, pt, &nb, s));
+      if ((rc = reduce(nb, 0, 1, (int)M.dec.size, grad, M.dec.W1, 0)) != MGN_OK) return rc;
+    }
     for (int l = m - 1; l >= 0; --l) {
       const Off& oe = M.edge[l];
       const Off& on = M.node[l];
@@ -785,8 +808,21 @@ struct Run {
                    : launch_edge_enc_bwd_w160(E, efeat, ebar, W(M.enc_edge, M.p_enc_edge), eps, pt, &nb, s));
       if ((rc = reduce(nb, 0, 1, (int)M.enc_edge.size, grad, M.enc_edge.W1, 0)) != MGN_OK) return rc;
     }
-    LAUNCH(K_NODE_ENC_BWD, launch_node_enc_bwd(prec, D, N, node_in, hb_cur, W(M.enc_node, M.p_enc_node), eps, gin, pt, &nb, s));
-    if ((rc = reduce(nb, 0, 1, (int)M.enc_node.size, grad, M.enc_node.W1, 0)) != MGN_OK) return rc;
+    if (prec == MGN_FP32) {
+      // fp32: the row-layout reverse (W1, b1 and the vectors as its
+      // partials), then dW2 = sum dz2^T a1 from its streams
+      float* ns = (float*)(ws + c.L.nstr);
+      const Off& o = M.enc_node;
+      LAUNCH(K_NODE_ENC_BWD, launch_node_enc_bwd_r32(D, N, node_in, hb_cur, W(o, M.p_enc_node), eps, gin, ns, pt, &nb, s));
+      if ((rc = reduce(nb, 0, 1, 9 * D, grad, o.W1, 0)) != MGN_OK) return rc;
+      if ((rc = reduce(nb, 9 * D, 1, 3 * D, grad, o.b2, 0)) != MGN_OK) return rc;
+      LAUNCH(K_NODE_ENC_BWD, launch_wgrad_r32(D, N, ns + (size_t)N * D, ns, pt, &nb, s));
+      if ((rc = reduce(nb, 0, D, D, grad, o.W2, D)) != MGN_OK) return rc;
+    } else {
+      LAUNCH(K_NODE_ENC_BWD, launch_node_enc_bwd(prec, D, N, node_in, hb_cur, W(M.enc_node, M.p_enc_node), eps, gin, pt,
+                                                 &nb, s));
+      if ((rc = reduce(nb, 0, 1, (int)M.enc_node.size, grad, M.enc_node.W1, 0)) != MGN_OK) return rc;
+    }
     return MGN_OK;
   }
 };

@@ -445,18 +445,15 @@ static int bwd_grid(int64_t n_tiles, const Partials& p) {
 
 hipError_t launch_decoder_bwd(int prec, int lat, int64_t N, const float* h, const float* gout, const MlpW& w,
                               float* hbar, const Partials& part, int* nblocks, hipStream_t s) {
+  *nblocks = 0;
+  // bf16 (fp32 runs on launch_decoder_bwd_r32)
+  if (prec != MGN_BF16) return hipErrorInvalidValue;
   const int g = bwd_grid((N + TM - 1) / TM, part);
   *nblocks = g;
   if (!g) return hipSuccess;
-  if (prec == MGN_BF16) {
 #define F(LD) hipLaunchKernelGGL((k_decoder_bwd<MGN_BF16, LD>), dim3(g), dim3(LD * 4), 0, s, N, h, gout, w, hbar, part)
-    MGN_BY_WIDTH(lat, F);
+  MGN_BY_WIDTH(lat, F);
 #undef F
-  } else {
-#define F(LD) hipLaunchKernelGGL((k_decoder_bwd<MGN_FP32, LD>), dim3(g), dim3(LD * 4), 0, s, N, h, gout, w, hbar, part)
-    MGN_BY_WIDTH(lat, F);
-#undef F
-  }
   return hipGetLastError();
 }
 
@@ -478,17 +475,13 @@ hipError_t launch_node_srcsum(int prec, int lat, int64_t N, const int32_t* rowpt
 hipError_t launch_node_enc_bwd(int prec, int lat, int64_t N, const float* node_in, const float* hbar, const MlpW& w,
                                float eps, float* gin, const Partials& part, int* nblocks, hipStream_t s) {
   if (prec == MGN_BF16 && lat == 160) return launch_node_enc_bwd_w160(N, node_in, hbar, w, eps, gin, part, nblocks, s);
+  *nblocks = 0;
+  // bf16 at width 128 (fp32 runs on launch_node_enc_bwd_r32)
+  if (prec != MGN_BF16 || lat != 128) return hipErrorInvalidValue;
   const int g = bwd_grid((N + TM - 1) / TM, part);
   *nblocks = g;
   if (!g) return hipSuccess;
-  if (prec == MGN_BF16) {
-    hipLaunchKernelGGL((k_enc_bwd<MGN_BF16, 128, 8>), dim3(g), dim3(128 * 4), 0, s, N, node_in, hbar, w, eps, gin, part);
-  } else {
-#define F(LD) \
-  hipLaunchKernelGGL((k_enc_bwd<MGN_FP32, LD, 8>), dim3(g), dim3(LD * 4), 0, s, N, node_in, hbar, w, eps, gin, part)
-    MGN_BY_WIDTH(lat, F);
-#undef F
-  }
+  hipLaunchKernelGGL((k_enc_bwd<MGN_BF16, 128, 8>), dim3(g), dim3(128 * 4), 0, s, N, node_in, hbar, w, eps, gin, part);
   return hipGetLastError();
 }
 

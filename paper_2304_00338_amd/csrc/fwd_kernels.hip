@@ -216,7 +216,8 @@ hipError_t launch_node_enc(int prec, int lat, int64_t N, const float* x, const M
   const int g = grid_for((N + TM - 1) / TM, kFwdBlocks);
   if (!g) return hipSuccess;
   const MlpW nn = nx ? *nx : w;
-  if (prec == MGN_BF16) {
+  // bf16 (fp32 runs on launch_node_enc_r32)
+  if (prec != MGN_BF16) return hipErrorInvalidValue;
 #define F(LD)                                                                                                        \
   if (nx)                                                                                                            \
     hipLaunchKernelGGL((k_node_enc<MGN_BF16, LD, true>), dim3(g), dim3(LD * 4), 0, s, N, x, w, nn, eps, h_out,       \
@@ -224,19 +225,8 @@ hipError_t launch_node_enc(int prec, int lat, int64_t N, const float* x, const M
   else                                                                                                               \
     hipLaunchKernelGGL((k_node_enc<MGN_BF16, LD, false>), dim3(g), dim3(LD * 4), 0, s, N, x, w, nn, eps, h_out,      \
                        (bf16*)P_out)
-    MGN_BY_WIDTH(lat, F);
+  MGN_BY_WIDTH(lat, F);
 #undef F
-  } else {
-#define F(LD)                                                                                                        \
-  if (nx)                                                                                                            \
-    hipLaunchKernelGGL((k_node_enc<MGN_FP32, LD, true>), dim3(g), dim3(LD * 4), 0, s, N, x, w, nn, eps, h_out,       \
-                       (float*)P_out);                                                                               \
-  else                                                                                                               \
-    hipLaunchKernelGGL((k_node_enc<MGN_FP32, LD, false>), dim3(g), dim3(LD * 4), 0, s, N, x, w, nn, eps, h_out,      \
-                       (float*)P_out)
-    MGN_BY_WIDTH(lat, F);
-#undef F
-  }
   return hipGetLastError();
 }
 
@@ -252,15 +242,11 @@ hipError_t launch_slot_fixup(int lat, const int32_t* long_nodes, int64_t n_long,
 hipError_t launch_decoder(int prec, int lat, int64_t N, const float* h, const MlpW& w, float* out, hipStream_t s) {
   const int g = grid_for((N + TM - 1) / TM, kFwdBlocks);
   if (!g) return hipSuccess;
-  if (prec == MGN_BF16) {
+  // bf16 (fp32 runs on launch_decoder_r32)
+  if (prec != MGN_BF16) return hipErrorInvalidValue;
 #define F(LD) hipLaunchKernelGGL((k_decoder<MGN_BF16, LD>), dim3(g), dim3(LD * 4), 0, s, N, h, w, out)
-    MGN_BY_WIDTH(lat, F);
+  MGN_BY_WIDTH(lat, F);
 #undef F
-  } else {
-#define F(LD) hipLaunchKernelGGL((k_decoder<MGN_FP32, LD>), dim3(g), dim3(LD * 4), 0, s, N, h, w, out)
-    MGN_BY_WIDTH(lat, F);
-#undef F
-  }
   return hipGetLastError();
 }
 

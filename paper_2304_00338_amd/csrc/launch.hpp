@@ -118,6 +118,24 @@ hipError_t launch_node_bwd_r32(int lat, int64_t N, const float* h, const float* 
 hipError_t launch_node_srcsum_r32(int lat, int64_t N, const int32_t* rowptr, const int32_t* rev, const float* zbar,
                                   const float* R, const float* hbar_part, const MlpW& w, float* hbar_out,
                                   float* S_out, hipStream_t s);
+// fp32 decoder in the row layout (needs the decoder's fragment-major F1 and,
+// for the reverse, F1t): out = W2 relu(W1 h + b1) + b2 ([N][4]); the
+// reverse writes hbar = W1^T dz1, the dz1 rows (for dW1 by launch_wgrad_r32)
+// and per-block partials [lat] db1, [4][lat] dW2, [4] db2.
+hipError_t launch_decoder_r32(int lat, int64_t N, const float* h, const MlpW& w, float* out, hipStream_t s);
+hipError_t launch_decoder_bwd_r32(int lat, int64_t N, const float* h, const float* gout, const MlpW& w, float* hbar,
+                                  float* dz1s, const Partials& part, int* nblocks, hipStream_t s);
+// fp32 node encoder in the row layout (needs the encoder's fragment-major F2
+// and, for the reverse, F2t; with nx the first edge MLP's F1s, F1r): h0 =
+// LN(W2 relu(W1 x + b1) + b2) from the 8 node inputs, with nx also the node
+// products of the first MP block.  The reverse writes gin = dL/dx (when
+// given), the a1 and dz2 rows into streams ([2][N][lat], for dW2 by
+// launch_wgrad_r32) and per-block partials [lat][8] dW1, [lat] db1, db2,
+// dgamma, dbeta.
+hipError_t launch_node_enc_r32(int lat, int64_t N, const float* x, const MlpW& w, const MlpW* nx, float eps,
+                               float* h_out, float* P_out, hipStream_t s);
+hipError_t launch_node_enc_bwd_r32(int lat, int64_t N, const float* x, const float* ybar, const MlpW& w, float eps,
+                                   float* gin, float* streams, const Partials& part, int* nblocks, hipStream_t s);
 hipError_t launch_edge_enc_r32(int lat, int64_t E, const float* f, const MlpW& w, float eps, void* e_out,
                                hipStream_t s);
 hipError_t launch_edge_enc_bwd_r32(int lat, int64_t E, const float* f, const void* ebar, const MlpW& w, float eps,
