@@ -253,7 +253,7 @@ struct Layout {
   size_t node_in = 0, K = 0, slots = 0;
   // backward
   size_t pio = 0, lossp = 0, pcopy = 0;
-  size_t ebar = 0, zbar = 0, dz = 0, nstr = 0, hb_a = 0, hb_b = 0, aggbar = 0, R = 0, part = 0, kbar = 0, ystage = 0, gin = 0;
+  size_t ebar = 0, ebar_st = 0, zbar = 0, dz = 0, nstr = 0, hb_a = 0, hb_b = 0, aggbar = 0, R = 0, part = 0, kbar = 0, ystage = 0, gin = 0;
   size_t total = 0;
 };
 
@@ -418,6 +418,10 @@ void plan(Ctx& c) {
     }
     L.ebar = o;  // edge-gradient stream, in the edge-latent element type
     o = al256(o + (size_t)E * D * c.se);
+    // several stages: the encoder output's gradient summed over the stages
+    // (the stages share one edge-encoder output; see Run::backward)
+    L.ebar_st = o;
+    o = al256(o + (c.max_stages > 1 ? (size_t)E * D * c.se : 0));
     L.zbar = o;
     o = al256(o + (size_t)E * D * c.se);
     L.dz = o;  // dz2 of the width-160 edge backward (the 128-wide one keeps it on chip)
@@ -471,6 +475,10 @@ struct Run {
   int prec;
   float eps;
   bool keep_a1 = false;  // this call saves (or the backward reads) the edge MLPs' a1
+  // stages of the saved integration step: they share the first stage's
+  // edge-encoder output, and the reverse runs the encoder once on the sum of
+  // the stages' gradients of it
+  int n_st = 1;
   int D = c.LD;          // kernel latent width
   // bf16 at width 128 runs on the row-layout kernels
   bool rows() const { return prec == MGN_BF16 && D == kRowsD; }
@@ -498,7 +506,12 @@ struct Run {
   size_t tsz() const { return prec == MGN_BF16 ? 2 : 4; }
   const void* P(int64_t off) const { return pack() + (size_t)off * tsz(); }
   char* set(int k) const { return ws + c.L.act + (size_t)k * c.L.act_stride; }
-  void* e_l(int k, int l) const { return set(k) + c.L.e_off + (c.save ? (size_t)l * E * D * c.se : 0); }
+  // With saving, stage k > 0 reads the first stage's encoder output: the
+  // encoder's inputs (edge features, parameters) are the same in every stage.
+  void* e_l(int k, int l) const {
+    if (!c.save) return set(k) + c.L.e_off;
+    return set(l == 0 ? 0 : k) + c.L.e_off + (size_t)l * E * D * c.se;
+  }
   float* h_l(int k, int l) const {
     return (float*)(set(k) + c.L.h_off) + (c.save ? (size_t)l * N * D : 0);
   }
@@ -588,7 +601,7 @@ struct Run {
     else
       LAUNCH(K_NODE_ENC, launch_node_enc(prec, D, N, node_in, W(M.enc_node, M.p_enc_node), m > 0 ? &e0 : nullptr, eps,
                                          h_l(k, 0), P_l(k, 0), s));
-    if (m > 0) {
+    if (m > 0 && !(c.save && k > 0)) {
       if (rows())
         LAUNCH(K_EDGE_ENC, launch_edge_enc_rows(E, efeat, W(M.enc_edge, M.p_enc_edge), eps, e_l(k, 0), s));
       else
@@ -668,7 +681,9 @@ struct Run {
     float* hb_part = (float*)(ws + c.L.hb_b);
     float* aggbar = (float*)(ws + c.L.aggbar);
     float* R = (float*)(ws + c.L.R);
-    void* ebar = ws + c.L.ebar;  // the edge-latent element type
+    // the edge-latent element type; the last stage of several keeps its
+    // gradient of the shared encoder output in the stage-sum buffer
+    void* ebar = ws + (n_st > 1 && k == n_st - 1 ? c.L.ebar_st : c.L.ebar);
     void* zbar = ws + c.L.zbar;
     int nb = 0, rc;
     if (prec == MGN_FP32) {
@@ -798,7 +813,15 @@ struct Run {
       // the block's partial regions are reused by the next block
       if ((rc = flush(grad)) != MGN_OK) return rc;
     }
-    if (m > 0) {
+    if (m > 0 && n_st > 1) {
+      // dL/de0 summed over the stages, accumulated from the last stage to
+      // the first (each stage's own gradient of the shared encoder output
+      // is in ebar when its block reverses are done)
+      void* est = ws + c.L.ebar_st;
+      if (k > 0 && k < n_st - 1) LAUNCH(K_EDGE_ENC_BWD, launch_add_stream(prec, E * D, ebar, est, s));
+      if (k == 0) LAUNCH(K_EDGE_ENC_BWD, launch_add_stream(prec, E * D, est, ebar, s));
+    }
+    if (m > 0 && (n_st == 1 || k == 0)) {
       if (rows())
         LAUNCH(K_EDGE_ENC_BWD, launch_edge_enc_bwd_rows(E, efeat, ebar, W(M.enc_edge, M.p_enc_edge), eps, pt, &nb, s));
       else
@@ -959,6 +982,7 @@ int backward_steps(Ctx& c, const float* grad_out, float* grad_params, float* gra
   if (c.saved == 1) return r.backward(0, c.node_in, c.efeat, grad_out, grad_params, grad_in);
   Tableau tb;
   tableau(c.scheme, tb);
+  r.n_st = tb.s;
   char* w = c.ws;
   float* node_in = (float*)(w + c.L.node_in);
   float* kbar = (float*)(w + c.L.kbar);

@@ -291,6 +291,9 @@ struct CopyList {
 hipError_t launch_copy_blocks(const CopyList& L, const float* a, float* b, int accumulate, hipStream_t s);
 // p[0..n) = v
 hipError_t launch_fill(float* p, int64_t n, float v, hipStream_t s);
+// b += a over n values of an edge-latent stream in precision prec (n a
+// multiple of 8; bf16 values added in fp32 and rounded to nearest even)
+hipError_t launch_add_stream(int prec, int64_t n, const void* a, void* b, hipStream_t s);
 // Training step: partial rows of the loss sum; noisy gather dst[r] =
 // y[idx[r]] + sd * noise[idx[r]] (noise nullable); masked squared error of
 // pred against target[idx[r]] over mask rows: gradient 2 d inv, loss +=

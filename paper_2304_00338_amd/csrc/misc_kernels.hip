@@ -72,9 +72,47 @@ __global__ void __launch_bounds__(256) k_copy_blocks(CopyList L, const float* __
   }
 }
 
+// b = a + b over n values of an edge-latent stream (fp32, or bf16 added in
+// fp32 and rounded to nearest even), 8 values per thread; n is a multiple of
+// 8 (the latent width is).
+__global__ void __launch_bounds__(256) k_add_stream_f32(int64_t n8, const float4* __restrict__ a,
+                                                        float4* __restrict__ b) {
+  for (int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x; t < n8; t += (int64_t)gridDim.x * 256) {
+    const float4 x0 = a[2 * t], x1 = a[2 * t + 1];
+    float4 y0 = b[2 * t], y1 = b[2 * t + 1];
+    y0.x += x0.x; y0.y += x0.y; y0.z += x0.z; y0.w += x0.w;
+    y1.x += x1.x; y1.y += x1.y; y1.z += x1.z; y1.w += x1.w;
+    b[2 * t] = y0;
+    b[2 * t + 1] = y1;
+  }
+}
+
+__global__ void __launch_bounds__(256) k_add_stream_bf16(int64_t n8, const uint4* __restrict__ a,
+                                                         uint4* __restrict__ b) {
+  for (int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x; t < n8; t += (int64_t)gridDim.x * 256) {
+    const bf16x8 x = __builtin_bit_cast(bf16x8, a[t]);
+    bf16x8 y = __builtin_bit_cast(bf16x8, b[t]);
+#pragma unroll
+    for (int u = 0; u < 8; ++u) y[u] = (bf16)((float)y[u] + (float)x[u]);
+    b[t] = __builtin_bit_cast(uint4, y);
+  }
+}
+
 }  // namespace dev
 
 using namespace dev;
+
+hipError_t launch_add_stream(int prec, int64_t n, const void* a, void* b, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  if (n % 8) return hipErrorInvalidValue;
+  const int64_t n8 = n / 8;
+  const unsigned g = (unsigned)std::min<int64_t>((n8 + 255) / 256, 8192);
+  if (prec == MGN_BF16)
+    hipLaunchKernelGGL(k_add_stream_bf16, dim3(g), dim3(256), 0, s, n8, (const uint4*)a, (uint4*)b);
+  else
+    hipLaunchKernelGGL(k_add_stream_f32, dim3(g), dim3(256), 0, s, n8, (const float4*)a, (float4*)b);
+  return hipGetLastError();
+}
 
 hipError_t launch_gather_rows4(int64_t n, const float* src, const int32_t* idx, int64_t n_src, float* dst,
                                hipStream_t s) {
