@@ -467,27 +467,46 @@ k_edge_bwd_r32(EdgeTiles tl, const float* __restrict__ e_in, const float* ebar_i
                  });
     // ---- the round's 64 rows into this wave's output rows of dW2 and dW1e:
     // A = dz2^T / zbar^T (rows 32 wv + 16 ob + m), B = a1 / e, K = 4 rows
-#pragma unroll 2
-    for (int kk = 0; kk < B32_ROWS / 4; ++kk) {
+    // (the next 4 rows' operands are read before this step's products)
+    struct Ops {
+      float a2[2], a1[2], b2[8], b1[8];
+    };
+    auto rd = [&](int kk, Ops& o) {
       const int r0 = (4 * kk + g) * B32_SLD;
-      float A2[2], A1[2];
 #pragma unroll
       for (int ob = 0; ob < 2; ++ob) {
-        A2[ob] = S.st[0][r0 + 32 * wv + 16 * ob + i];
-        A1[ob] = S.st[3][r0 + 32 * wv + 16 * ob + i];
-        ab2[ob] = __builtin_amdgcn_mfma_f32_16x16x4f32(A2[ob], 1.0f, ab2[ob], 0, 0, 0);
-        ab1[ob] = __builtin_amdgcn_mfma_f32_16x16x4f32(A1[ob], 1.0f, ab1[ob], 0, 0, 0);
+        o.a2[ob] = S.st[0][r0 + 32 * wv + 16 * ob + i];
+        o.a1[ob] = S.st[3][r0 + 32 * wv + 16 * ob + i];
       }
 #pragma unroll
       for (int nb = 0; nb < 8; ++nb) {
-        const float B2 = S.st[1][r0 + 16 * nb + i];
-        const float B1 = S.st[2][r0 + 16 * nb + i];
+        o.b2[nb] = S.st[1][r0 + 16 * nb + i];
+        o.b1[nb] = S.st[2][r0 + 16 * nb + i];
+      }
+    };
+    auto step = [&](const Ops& o) {
+#pragma unroll
+      for (int ob = 0; ob < 2; ++ob) {
+        ab2[ob] = __builtin_amdgcn_mfma_f32_16x16x4f32(o.a2[ob], 1.0f, ab2[ob], 0, 0, 0);
+        ab1[ob] = __builtin_amdgcn_mfma_f32_16x16x4f32(o.a1[ob], 1.0f, ab1[ob], 0, 0, 0);
+      }
+#pragma unroll
+      for (int nb = 0; nb < 8; ++nb)
 #pragma unroll
         for (int ob = 0; ob < 2; ++ob) {
-          aw2[ob][nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(A2[ob], B2, aw2[ob][nb], 0, 0, 0);
-          aw1[ob][nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(A1[ob], B1, aw1[ob][nb], 0, 0, 0);
+          aw2[ob][nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(o.a2[ob], o.b2[nb], aw2[ob][nb], 0, 0, 0);
+          aw1[ob][nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(o.a1[ob], o.b1[nb], aw1[ob][nb], 0, 0, 0);
         }
-      }
+    };
+    Ops o0, o1;
+    rd(0, o0);
+    for (int kk = 0; kk < B32_ROWS / 4; kk += 2) {
+      rd(kk + 1, o1);
+      __builtin_amdgcn_sched_barrier(0);
+      step(o0);
+      if (kk + 2 < B32_ROWS / 4) rd(kk + 2, o0);
+      __builtin_amdgcn_sched_barrier(0);
+      step(o1);
     }
   };
 
@@ -939,22 +958,31 @@ k_wgrad_r32(int64_t M, const float* __restrict__ Gm, const float* __restrict__ X
     __syncthreads();
     if (r + gridDim.x < nr) load(r + gridDim.x);
     __builtin_amdgcn_sched_barrier(0);
-    // A[m][k] = G[row k][16 ob + m], B[k][n] = X[row k][16 nb + n], K = 4 rows
+    // A[m][k] = G[row k][16 ob + m], B[k][n] = X[row k][16 nb + n], K = 4
+    // rows; the next 4 rows' operands are read from LDS before this step's
+    // products (the scheduling barrier keeps them there), so their latency
+    // lies under the MFMAs
     const float* pa = st[0] + g * SLD + 16 * ob0 + i;
     const float* pb = st[1] + g * SLD + 16 * nb0 + i;
-#pragma unroll 2
-    for (int kk = 0; kk < B32_ROWS / 4; ++kk) {
-      float A[HB], B[HB];
+    float A[2][HB], B[2][HB];
+    auto rd = [&](int kk, float (&a)[HB], float (&b)[HB]) {
 #pragma unroll
       for (int u = 0; u < HB; ++u) {
-        A[u] = pa[4 * kk * SLD + 16 * u];
-        B[u] = pb[4 * kk * SLD + 16 * u];
+        a[u] = pa[4 * kk * SLD + 16 * u];
+        b[u] = pb[4 * kk * SLD + 16 * u];
       }
+    };
+    rd(0, A[0], B[0]);
+#pragma unroll
+    for (int kk = 0; kk < B32_ROWS / 4; ++kk) {
+      const int c = kk & 1;
+      if (kk + 1 < B32_ROWS / 4) rd(kk + 1, A[c ^ 1], B[c ^ 1]);
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int u = 0; u < HB; ++u)
 #pragma unroll
         for (int v = 0; v < HB; ++v)
-          aw[u * HB + v] = __builtin_amdgcn_mfma_f32_16x16x4f32(A[u], B[v], aw[u * HB + v], 0, 0, 0);
+          aw[u * HB + v] = __builtin_amdgcn_mfma_f32_16x16x4f32(A[c][u], B[c][v], aw[u * HB + v], 0, 0, 0);
     }
     __syncthreads();
   }
