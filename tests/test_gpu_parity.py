@@ -212,6 +212,10 @@ def test_integrators(scheme, prec):
     assert rel_l2(yn - ps.states, ryn - ps.states) < tol
     assert rel_l2(gp, rgp) < tol
     assert rel_l2(gy, rgy) < tol
+    # every MLP on its own; the stages share one edge-encoder output, whose
+    # gradient is summed over the stages before the encoder's reverse
+    for name, a, b in segments(ps.m):
+        assert rel_l2(gp[a:b], rgp[a:b]) < tol, (scheme, name, rel_l2(gp[a:b], rgp[a:b]))
 
 
 @pytest.mark.parametrize("prec", ["fp32", "bf16"])
