@@ -440,7 +440,7 @@ using namespace dev;
 static constexpr int kBwdBlocks = 512;
 
 static int bwd_grid(int64_t n_tiles, const Partials& p) {
-  return grid_for(n_tiles, std::min(kBwdBlocks, p.max_blocks));
+  return part_grid(n_tiles, std::min(kBwdBlocks, p.max_blocks));
 }
 
 hipError_t launch_decoder_bwd(int prec, int lat, int64_t N, const float* h, const float* gout, const MlpW& w,

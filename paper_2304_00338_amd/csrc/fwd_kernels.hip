@@ -199,6 +199,12 @@ int grid_for(int64_t n_tiles, int max_blocks) {
   return (int)std::min<int64_t>(n_tiles, (int64_t)max_blocks);
 }
 
+int part_grid(int64_t n_tiles, int max_blocks) {
+  if (n_tiles <= 0) return 0;
+  const int64_t cap = std::max<int64_t>(256, n_tiles / 16);
+  return (int)std::min<int64_t>(std::min<int64_t>(n_tiles, (int64_t)max_blocks), cap);
+}
+
 static constexpr int kFwdBlocks = 1024;
 
 hipError_t launch_pack(int prec, const float* params, void* pack, const PackList& L, hipStream_t s) {

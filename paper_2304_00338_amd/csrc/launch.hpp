@@ -83,6 +83,11 @@ struct Partials {
 // Persistent grid size: number of blocks the kernels are launched with for
 // a given number of tiles (also the number of partial rows to reduce).
 int grid_for(int64_t n_tiles, int max_blocks);
+// Blocks of a reverse kernel whose per-block weight-gradient partials are
+// summed afterwards: at most max_blocks, and on small inputs at most one
+// block per 16 tiles (but at least 256, one per CU), so the reduction reads
+// no more partial copies than the work needs.
+int part_grid(int64_t n_tiles, int max_blocks);
 
 hipError_t launch_pack(int prec, const float* params, void* pack, const PackList& L, hipStream_t s);
 

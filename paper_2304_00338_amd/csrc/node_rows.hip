@@ -545,7 +545,7 @@ hipError_t launch_wgrad_node(int64_t N, const float* h, const float* agg, const 
                              const void* a1, const Partials& part, int* nblocks, hipStream_t s) {
   *nblocks = 0;
   if (N <= 0) return hipSuccess;
-  const int g = (int)std::min<int64_t>((N + TM - 1) / TM, std::min(kWgradNodeBlocks, part.max_blocks));
+  const int g = part_grid((N + TM - 1) / TM, std::min(kWgradNodeBlocks, part.max_blocks));
   *nblocks = g;
   hipLaunchKernelGGL(k_wgrad_node, dim3(g), dim3(NT), 0, s, N, h, agg, (const bf16*)dz1, (const bf16*)dz2,
                      (const bf16*)a1, part);
