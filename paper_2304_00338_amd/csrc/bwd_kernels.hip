@@ -174,42 +174,73 @@ __global__ void __launch_bounds__(LD * 4) k_node_srcsum(int64_t N, const int32_t
 #pragma unroll
   for (int cb = 0; cb < NCB; ++cb) dWs[cb] = dWr[cb] = zero4();
   const int64_t ntiles = (N + TM - 1) / TM;
+  // D/8 lanes per node, 8 features per lane; the node's reversed in-edges
+  // are gathered 8 at a time (independent loads) and added in edge order.
+  // The first 8 of the next tile's node go through their three dependent
+  // loads (rowptr, then rev, then zbar) one step at a time around this
+  // tile's staging and products, so each has work to hide behind.
+  const int j = tid / (D / 8), c8 = (tid % (D / 8)) * 8;
+  struct First {
+    int e, e1;
+    int rv[8];
+    typename RowChunk<T>::V x[8];
+  };
+  auto f_rowptr = [&](int64_t t, First& F) {
+    F.e = F.e1 = 0;
+    if (t < ntiles && t * TM + j < N) {
+      const int v = (int)(t * TM + j);
+      F.e = rowptr[v];
+      F.e1 = rowptr[v + 1];
+    }
+  };
+  auto f_rev = [&](First& F) {
+#pragma unroll
+    for (int k = 0; k < 8; ++k) F.rv[k] = F.e + k < F.e1 ? rev[F.e + k] : -1;
+  };
+  auto f_z = [&](First& F) {
+#pragma unroll
+    for (int k = 0; k < 8; ++k)
+      if (F.rv[k] >= 0) F.x[k] = RowChunk<T>::load(zbar + (size_t)F.rv[k] * D + c8);
+  };
+  First F, Fn;
+  f_rowptr(blockIdx.x, F);
+  f_rev(F);
+  f_z(F);
   for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
     const int64_t r0 = t * TM;
     const int nr = (int)min((int64_t)TM, N - r0);
     {
-      // D/8 lanes per node, 8 features per lane; the node's reversed in-edges
-      // are gathered 8 at a time (independent loads) and added in edge order
-      const int j = tid / (D / 8), c8 = (tid % (D / 8)) * 8;
       float acc8[8];
 #pragma unroll
       for (int u = 0; u < 8; ++u) acc8[u] = 0.f;
-      if (j < nr) {
-        const int v = (int)(r0 + j);
-        const int e1 = rowptr[v + 1];
-        for (int e = rowptr[v]; e < e1; e += 8) {
-          int rv[8];
 #pragma unroll
-          for (int k = 0; k < 8; ++k) rv[k] = e + k < e1 ? rev[e + k] : -1;
-          typename RowChunk<T>::V x[8];
+      for (int k = 0; k < 8; ++k)
+        if (F.rv[k] >= 0) RowChunk<T>::add(acc8, F.x[k]);
+      for (int e = F.e + 8; e < F.e1; e += 8) {
+        int rv[8];
 #pragma unroll
-          for (int k = 0; k < 8; ++k)
-            if (rv[k] >= 0) x[k] = RowChunk<T>::load(zbar + (size_t)rv[k] * D + c8);
+        for (int k = 0; k < 8; ++k) rv[k] = e + k < F.e1 ? rev[e + k] : -1;
+        typename RowChunk<T>::V x[8];
 #pragma unroll
-          for (int k = 0; k < 8; ++k)
-            if (rv[k] >= 0) RowChunk<T>::add(acc8, x[k]);
-        }
+        for (int k = 0; k < 8; ++k)
+          if (rv[k] >= 0) x[k] = RowChunk<T>::load(zbar + (size_t)rv[k] * D + c8);
+#pragma unroll
+        for (int k = 0; k < 8; ++k)
+          if (rv[k] >= 0) RowChunk<T>::add(acc8, x[k]);
       }
       T o[8];
 #pragma unroll
       for (int u = 0; u < 8; ++u) o[u] = P::cvt(acc8[u]);
+      // rows past the tile's end get zeros (their rv are all -1)
 #pragma unroll
       for (int u = 0; u < (int)(8 * sizeof(T)) / 16; ++u)
         reinterpret_cast<uint4*>(sSR + j * LDX + c8)[u] = reinterpret_cast<const uint4*>(o)[u];
     }
+    f_rowptr(t + gridDim.x, Fn);
     stage_rows<D>(sSR + D, LDX, R + (size_t)r0 * D, nr, tid);
     stage_rows<D>(sH, LDT, h + (size_t)r0 * D, nr, tid);
     __syncthreads();
+    f_rev(Fn);
     f32x4 acc[NRB];
 #pragma unroll
     for (int rb = 0; rb < NRB; ++rb)
@@ -220,6 +251,7 @@ __global__ void __launch_bounds__(LD * 4) k_node_srcsum(int64_t N, const int32_t
       }
     gemm_tile<PREC, D>(acc, sSR, LDX, (const T*)w.W1t, D, D + w8 * 16, 0, i, q);
     gemm_tile<PREC, D>(acc, sSR + D, LDX, (const T*)w.W1t, D, 2 * D + w8 * 16, 0, i, q);
+    f_z(Fn);
 #pragma unroll
     for (int rb = 0; rb < NRB; ++rb)
 #pragma unroll
@@ -239,6 +271,7 @@ __global__ void __launch_bounds__(LD * 4) k_node_srcsum(int64_t N, const int32_t
       for (int r = 0; r < 4; ++r) g[rb][r] = tof(sSR[(rb * 16 + q * 4 + r) * LDX + D + n]);
     gtx<PREC, NCB>(dWr, g, sH, LDT, 0, i, q);
     __syncthreads();
+    F = Fn;
   }
   float* base = part.buf + (size_t)blockIdx.x * part.stride;
   put_w<NCB>(base, D, dWs, w8, i, q);
