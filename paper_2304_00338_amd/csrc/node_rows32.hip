@@ -282,11 +282,35 @@ k_node_srcsum_r32(int64_t N, const int32_t* __restrict__ rowptr, const int32_t* 
   const int64_t nu = (N + 15) >> 4;
   const UnitRange ur = unit_range<R32_NW>(nu, wv);
   const int f0 = Z::KL * g;
+  // The reversed edge ids of a gather round are requested one round ahead
+  // (with the zbar rows of the current round), and the next unit's segment
+  // bounds and first ids during this unit's products, so each round waits
+  // for one load latency instead of two.
+  struct Seg {
+    int e0, e1;
+    int r[GE];
+  };
+  auto seg = [&](int64_t uu, Seg& q) {
+    q.e0 = q.e1 = 0;
+    if (uu < ur.end && uu * 16 + i < N) {
+      q.e0 = rowptr[uu * 16 + i];
+      q.e1 = rowptr[uu * 16 + i + 1];
+    }
+  };
+  auto ids = [&](const Seg& q, int k0, int (&r)[GE]) {
+#pragma unroll
+    for (int k = 0; k < GE; ++k) r[k] = q.e0 + k0 + k < q.e1 ? rev[q.e0 + k0 + k] : 0;
+  };
+  Seg sg;
+  if (ur.t < ur.end) {
+    seg(ur.t, sg);
+    ids(sg, 0, sg.r);
+  }
   for (int64_t u = ur.t; u < ur.end; u += ur.stride) {
     const bool live = u * 16 + i < N;
     const int64_t v = min(u * 16 + i, N - 1);
     const size_t orow = (size_t)v * LD + f0;
-    const int e0 = rowptr[v], e1 = live ? rowptr[v + 1] : e0;
+    const int e0 = sg.e0, e1 = sg.e1;
     float hb[Z::KL], rr[Z::KL];
     load_row32<LD>(hb, hbar_part + orow);
     load_row32<LD>(rr, R + orow);
@@ -296,13 +320,18 @@ k_node_srcsum_r32(int64_t N, const int32_t* __restrict__ rowptr, const int32_t* 
     float S[Z::KL];
 #pragma unroll
     for (int c = 0; c < Z::KL; ++c) S[c] = 0.f;
+    int rc[GE];
+#pragma unroll
+    for (int k = 0; k < GE; ++k) rc[k] = sg.r[k];
     for (int k0 = 0; k0 < md; k0 += GE) {
+      int rn[GE];
+      ids(sg, k0 + GE, rn);
       f32x4 x[GE][Z::KC];
 #pragma unroll
       for (int k = 0; k < GE; ++k) {
         const int e = e0 + k0 + k;
         if (e < e1) {
-          const float* zp = zbar + (size_t)rev[e] * LD + f0;
+          const float* zp = zbar + (size_t)rc[k] * LD + f0;
 #pragma unroll
           for (int c = 0; c < Z::KC; ++c) x[k][c] = *reinterpret_cast<const f32x4*>(zp + 4 * c);
         }
@@ -314,6 +343,8 @@ k_node_srcsum_r32(int64_t N, const int32_t* __restrict__ rowptr, const int32_t* 
           for (int c = 0; c < Z::KC; ++c)
 #pragma unroll
             for (int r = 0; r < 4; ++r) S[4 * c + r] += x[k][c][r];
+#pragma unroll
+      for (int k = 0; k < GE; ++k) rc[k] = rn[k];
     }
     if (live) {
       float* p = S_out + orow;
@@ -326,7 +357,9 @@ k_node_srcsum_r32(int64_t N, const int32_t* __restrict__ rowptr, const int32_t* 
 #pragma unroll
     for (int ob = 0; ob < Z::NOB; ++ob)
       acc[ob] = f32x4{hb[4 * ob], hb[4 * ob + 1], hb[4 * ob + 2], hb[4 * ob + 3]};
+    seg(u + ur.stride, sg);
     gemm32<LD>(acc, S, w.F1st + oz, lane);
+    ids(sg, 0, sg.r);
     gemm32<LD>(acc, rr, w.F1rt + oz, lane);
     if (live) store_row32<LD>(hbar_out + orow, acc);
   }
