@@ -1,6 +1,7 @@
 // Reverse-mode kernels of one MGN call on gfx950 in the feature-split
-// layout: decoder, sender-side sums, the node encoder and the reduction of
-// the per-block partials.  Activations inside each MLP are
+// layout, bf16 only (fp32 runs on the row-layout kernels): the decoder, and
+// at width 128 the sender-side sums and the node encoder; and the
+// reduction of the per-block partials (both precisions).  Activations inside each MLP are
 // recomputed from the saved block inputs (edge latents, node latents,
 // aggregates and node products).  Weight gradients are accumulated per
 // persistent block in registers and written as per-block partials, which

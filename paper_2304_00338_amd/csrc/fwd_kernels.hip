@@ -1,6 +1,7 @@
 // Forward kernels of one MGN call on gfx950 (Sec. 2.1 of the paper) in the
-// feature-split layout: weight packing, the node encoder, the decoder and
-// the long-segment fixup of the receiver sums.
+// feature-split layout: weight packing (both precisions), the bf16 node
+// encoder and decoder (fp32 runs them on the row layout) and the
+// long-segment fixup of the receiver sums.
 //
 // The first edge-MLP layer acts on the concatenation [e, h_s, h_r]; it is
 // evaluated as W1e e + W1s h_s + W1r h_r, where the node products
