@@ -471,7 +471,7 @@ __global__ void __launch_bounds__(256) k_reduce_batch(Partials part, int64_t reg
 // ============================================================ launchers
 using namespace dev;
 
-static constexpr int kBwdBlocks = 512;
+static constexpr int kBwdBlocks = 256;
 
 static int bwd_grid(int64_t n_tiles, const Partials& p) {
   return part_grid(n_tiles, std::min(kBwdBlocks, p.max_blocks));

@@ -539,7 +539,7 @@ hipError_t launch_node_bwd_rows(int64_t N, const float* h, const float* agg, con
   return hipGetLastError();
 }
 
-static constexpr int kWgradNodeBlocks = 512;
+static constexpr int kWgradNodeBlocks = 256;
 
 hipError_t launch_wgrad_node(int64_t N, const float* h, const float* agg, const void* dz1, const void* dz2,
                              const void* a1, const Partials& part, int* nblocks, hipStream_t s) {
