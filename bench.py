@@ -87,7 +87,7 @@ def edge_bwd_split_roofline(prec, D, N, E, m, avg_ms):
 
 
 def kernel_bytes(kind, N, E, n_tiles, prec, have_ebar=True, write_e=True, keep_a1=True, method=False):
-    """HBM bytes of one launch of the kernels this build runs: every input
+    """HBM bytes of one launch of the library's kernels: every input
     read once and every output written once.  In bf16 the edge latents,
     their gradient stream, node products P ([N][2D]) and the a1 / zbar
     streams are 2 bytes per element; node latents, aggregates and node
@@ -775,8 +775,8 @@ def main():
         summarize_profile(args.summarize_profile, args.profile_kernel)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU: this build has no multi-GPU path "
-              "(the patch-parallel design is described in DESIGN.md); run with --gpus 1",
+        print("bench.py measures one GPU: the library runs on one GPU only "
+              "(patch-parallel sharding across GPUs is not implemented); run with --gpus 1",
               file=sys.stderr)
         sys.exit(2)
 
