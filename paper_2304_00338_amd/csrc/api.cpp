@@ -250,6 +250,7 @@ struct Layout {
   // activation sets
   size_t act = 0, act_stride = 0;
   size_t e_off = 0, h_off = 0, agg_off = 0, P_off = 0, a1_off = 0;  // within a set
+  size_t e0 = 0;  // without saving, several stages: the shared edge-encoder output
   size_t node_in = 0, K = 0, slots = 0;
   // backward
   size_t pio = 0, lossp = 0, pcopy = 0;
@@ -399,6 +400,12 @@ void plan(Ctx& c) {
   L.act_stride = so;
   L.act = o;
   o = al256(o + so * c.ne_sets);
+  if (!c.save && c.max_stages > 1) {
+    // the stages of a non-saving step share one edge-encoder output; the
+    // processor updates its own edge buffer in place, so this one stays
+    L.e0 = o;
+    o = al256(o + (size_t)E * D * c.se);
+  }
   L.node_in = o;
   o = al256(o + (size_t)c.max_stages * N * 8 * 4);
   L.K = o;
@@ -512,6 +519,12 @@ struct Run {
     if (!c.save) return set(k) + c.L.e_off;
     return set(l == 0 ? 0 : k) + c.L.e_off + (size_t)l * E * D * c.se;
   }
+  // The edge-encoder output of a call, read by its first processor block in
+  // every stage: with saving the first stage's (no block overwrites it);
+  // without saving, when several stages are planned, a buffer of its own
+  // (the processor updates its edge buffer in place); else the edge buffer.
+  bool shared_e0() const { return c.save || c.max_stages > 1; }
+  void* e_enc() const { return !c.save && c.max_stages > 1 ? ws + c.L.e0 : e_l(0, 0); }
   float* h_l(int k, int l) const {
     return (float*)(set(k) + c.L.h_off) + (c.save ? (size_t)l * N * D : 0);
   }
@@ -590,7 +603,9 @@ struct Run {
     return MGN_OK;
   }
 
-  int forward(const float* node_in, const float* efeat, float* out, int k) {
+  // k: the activation set (the stage with saving, else 0); stage: the stage
+  // of the call (later stages reuse the edge-encoder output when it is kept)
+  int forward(const float* node_in, const float* efeat, float* out, int k, int stage = 0) {
     const Model& M = c.M;
     const EdgeTiles tl = tiles();
     MlpW e0;
@@ -601,25 +616,26 @@ struct Run {
     else
       LAUNCH(K_NODE_ENC, launch_node_enc(prec, D, N, node_in, W(M.enc_node, M.p_enc_node), m > 0 ? &e0 : nullptr, eps,
                                          h_l(k, 0), P_l(k, 0), s));
-    if (m > 0 && !(c.save && k > 0)) {
+    if (m > 0 && !(stage > 0 && shared_e0())) {
       if (rows())
-        LAUNCH(K_EDGE_ENC, launch_edge_enc_rows(E, efeat, W(M.enc_edge, M.p_enc_edge), eps, e_l(k, 0), s));
+        LAUNCH(K_EDGE_ENC, launch_edge_enc_rows(E, efeat, W(M.enc_edge, M.p_enc_edge), eps, e_enc(), s));
       else
         LAUNCH(K_EDGE_ENC, prec == MGN_FP32
-                               ? launch_edge_enc_r32(D, E, efeat, W(M.enc_edge, M.p_enc_edge), eps, e_l(k, 0), s)
-                               : launch_edge_enc_w160(E, efeat, W(M.enc_edge, M.p_enc_edge), eps, e_l(k, 0), s));
+                               ? launch_edge_enc_r32(D, E, efeat, W(M.enc_edge, M.p_enc_edge), eps, e_enc(), s)
+                               : launch_edge_enc_w160(E, efeat, W(M.enc_edge, M.p_enc_edge), eps, e_enc(), s));
     }
     for (int l = 0; l < m; ++l) {
       const bool last = l == m - 1;
+      const void* e_in = l == 0 ? e_enc() : e_l(k, l);
       void* e_out = c.save ? (last ? nullptr : e_l(k, l + 1)) : e_l(k, 0);
       if (E > 0 && prec == MGN_FP32)
-        LAUNCH(K_EDGE_FWD, launch_edge_fwd_r32(D, tl, e_l(k, l), e_out, last ? 0 : 1, P_l(k, l),
+        LAUNCH(K_EDGE_FWD, launch_edge_fwd_r32(D, tl, e_in, e_out, last ? 0 : 1, P_l(k, l),
                                                W(M.edge[l], M.p_edge[l]), eps, agg_l(k, l), slots(), s));
       else if (E > 0)
-        LAUNCH(K_EDGE_FWD, rows() ? launch_edge_fwd_rows(tl, e_l(k, l), e_out, last ? 0 : 1, P_l(k, l),
+        LAUNCH(K_EDGE_FWD, rows() ? launch_edge_fwd_rows(tl, e_in, e_out, last ? 0 : 1, P_l(k, l),
                                                          W(M.edge[l], M.p_edge[l]), eps, agg_l(k, l), slots(),
                                                          a1_l(k, l), s)
-                                  : launch_edge_fwd_w160(tl, e_l(k, l), e_out, last ? 0 : 1, P_l(k, l),
+                                  : launch_edge_fwd_w160(tl, e_in, e_out, last ? 0 : 1, P_l(k, l),
                                                          W(M.edge[l], M.p_edge[l]), eps, agg_l(k, l), slots(),
                                                          a1_l(k, l), s));
       else
@@ -932,7 +948,7 @@ int integrate_core(Ctx& c, const mgn_dgraph& g, const float* params, const Table
       }
     float* ni = node_in + (size_t)i * N * 8;
     HIP_TRY(launch_stage_input(N, static_feat, lc, ni, s));
-    if ((rc = r.forward(ni, efeat, K + (size_t)i * N * 4, save ? i : 0)) != MGN_OK) return rc;
+    if ((rc = r.forward(ni, efeat, K + (size_t)i * N * 4, save ? i : 0, i)) != MGN_OK) return rc;
   }
   LinComb lc{};
   lc.x[0] = y;
@@ -1390,7 +1406,7 @@ int mgn_pec_step(mgn_ctx* ctx, const mgn_dgraph* g, const float* params, const f
   }
   // predict, evaluate, correct
   HIP_TRY(launch_stage_input(N, static_feat, comb({{y, 1.f}, {K0, 1.5f}, {K1, -0.5f}}), node_in, S(stream)));
-  if ((rc = r.forward(node_in, efeat, Kp, 0)) != MGN_OK) return rc;
+  if ((rc = r.forward(node_in, efeat, Kp, 0, first ? 1 : 0)) != MGN_OK) return rc;
   HIP_TRY(launch_lincomb(N, comb({{y, 1.f}, {Kp, 0.5f}, {K0, 0.5f}}), y_next, 4, 0, S(stream)));
   // history <- (K_p, K_n)
   HIP_TRY(launch_lincomb(N, comb({{K0, 1.f}}), K1, 4, 0, S(stream)));
