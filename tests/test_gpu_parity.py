@@ -193,6 +193,25 @@ def run_integrate(pb, prec, scheme):
     return yn.cpu().numpy(), gp.cpu().numpy(), gy.cpu().numpy()
 
 
+@pytest.mark.parametrize("scheme", ["heun2", "rk4"])
+@pytest.mark.parametrize("prec", ["fp32", "bf16"])
+def test_saving_and_nonsaving_steps_agree(scheme, prec):
+    """Both modes share one edge-encoder output between the stages (the
+    saving step through the first stage's buffer, the non-saving one through
+    a buffer of its own, since it updates its edge buffer in place): the
+    next states agree bitwise, also on a second call with other inputs."""
+    pb = Problem((7, 6, 5), 3, seed=9).device()
+    N, E = pb.g.n_nodes, pb.g.n_edges
+    cs = mgn.Context(pb.m, N, E, prec, max_stages=4, save=True)
+    cn = mgn.Context(pb.m, N, E, prec, max_stages=4)
+    for y in (pb.d_states, pb.d_states * 0.5 + 0.1):
+        y = y.contiguous()
+        ys = mgn.mgn_integrate_step(cs, pb.dg, pb.d_params, scheme, pb.d_onehot, y, pb.dg.efeat, save=True)
+        yn = mgn.mgn_integrate_step(cn, pb.dg, pb.d_params, scheme, pb.d_onehot, y, pb.dg.efeat)
+        torch.cuda.synchronize()
+        assert torch.equal(ys, yn)
+
+
 @pytest.mark.parametrize("scheme", ["euler", "heun2", "midpoint", "heun3", "rk4", "ralston2", "ralston3"])
 @pytest.mark.parametrize("prec", ["fp32", "bf16"])
 def test_integrators(scheme, prec):
