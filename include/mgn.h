@@ -276,7 +276,10 @@ int mgn_backward(mgn_ctx* ctx, const float* grad_out, float* grad_params,
 /* One explicit integration step with MGN as the scaled derivative
  * (Sec. 2.1, Sec. 2.3, App. A): K_i = MGN([static, y + sum_j a_ij K_j]),
  * y_next = y + sum_i b_i K_i.  static [N][4] (one-hot node type),
- * y [N][4], efeat [E][4], y_next [N][4] (device).
+ * y [N][4], efeat [E][4], y_next [N][4] (device).  The edge encoder's inputs
+ * (efeat, parameters) are the same in every stage, so the edges are encoded
+ * once per step and the stages share that output (and, with save, the
+ * backward sums the stages' gradients of it before the encoder's reverse).
  * Errors: ARG (unknown scheme, or more stages than the context plans), plus
  * those of mgn_forward. */
 int mgn_integrate_step(mgn_ctx* ctx, const mgn_dgraph* g, const float* params,
